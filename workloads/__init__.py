@@ -1,0 +1,93 @@
+"""Seeded synthetic inputs shared by the oracle tests, the GPU tests and the benchmark.
+
+This module holds random-number generation and workload shapes only; it does
+none of the scheme's arithmetic.  Every random quantity the scheme draws
+(secret, encryption and key randomness, errors) is produced here and passed
+explicitly to both the oracle and the GPU library, so the two see identical
+inputs.
+
+Seeding convention: ``numpy.random.default_rng(100 * config + role)`` with
+roles 1 data, 2 weights, 3 secret, 4 encryption randomness, 5 keys.
+
+The paper evaluates on Meta-Llama-3-8B weights and WikiText-2/C4 text; none of
+that is used.  Activations are uniform on [-1, 1] and weights are N(0, 0.02^2),
+at the shapes of the paper's projections (Evaluation, Table linear-performance).
+"""
+from dataclasses import dataclass, field
+from typing import Optional, Sequence
+
+import numpy as np
+
+ROLE_DATA, ROLE_WEIGHTS, ROLE_SECRET, ROLE_ENC, ROLE_KEYS = 1, 2, 3, 4, 5
+
+
+def rng(config: int, role: int, extra: int = 0) -> np.random.Generator:
+    return np.random.default_rng(100 * config + role + 1000 * extra)
+
+
+def ternary_secret(g: np.random.Generator, n: int) -> np.ndarray:
+    """Uniform ternary coefficients, P(-1) = P(0) = P(1) = 1/3, as int8."""
+    return g.integers(-1, 2, size=n, dtype=np.int64).astype(np.int8)
+
+
+def gaussian_error(g: np.random.Generator, shape, sigma: float = 3.2, bound: int = 19) -> np.ndarray:
+    """Rounded centred Gaussian with standard deviation sigma, clipped to +-bound, as int32."""
+    e = np.rint(g.normal(0.0, sigma, size=shape))
+    return np.clip(e, -bound, bound).astype(np.int32)
+
+
+def uniform_residues(g: np.random.Generator, moduli: Sequence[int], n: int, lead=()) -> np.ndarray:
+    """Uniform integers in [0, m) for each modulus m: shape lead + (len(moduli), n), uint64."""
+    lead = tuple(lead)
+    out = np.empty(lead + (len(moduli), n), dtype=np.uint64)
+    for k, m in enumerate(moduli):
+        out[..., k, :] = g.integers(0, int(m), size=lead + (n,), dtype=np.uint64)
+    return out
+
+
+def uniform_slots(g: np.random.Generator, shape, lo: float = -1.0, hi: float = 1.0) -> np.ndarray:
+    return g.uniform(lo, hi, size=shape)
+
+
+def gaussian_weights(g: np.random.Generator, shape, std: float = 0.02) -> np.ndarray:
+    return g.normal(0.0, std, size=shape)
+
+
+@dataclass(frozen=True)
+class Config:
+    """Shape of one workload: ring, modulus chain, and projection geometry."""
+    name: str
+    index: int
+    log_n: int
+    q_bits: int
+    n_q: int
+    n_p: int
+    dnum: int
+    scale_log2: int = 40
+    level: Optional[int] = None          # ciphertext level (limbs = level + 1); None = top
+    tokens: int = 0                       # T, tokens per ciphertext
+    d_in: int = 0
+    d_out: int = 0
+    n1: int = 0                           # baby-step count
+    batch: int = 0                        # polynomials per NTT batch / rotations per hoisted batch
+    notes: str = ""
+
+    @property
+    def n(self) -> int:
+        return 1 << self.log_n
+
+    @property
+    def feats(self) -> int:
+        return (self.n // 2) // self.tokens if self.tokens else 0
+
+
+# Toy end-to-end case: N = 2^12, 4 limbs of 36-bit primes, scale 2^30, 16 tokens x 128 features,
+# 128 x 128 weights through the plain diagonal method (127 rotations).
+TOY = Config("toy", 1, 12, 36, 4, 2, 2, scale_log2=30, level=3, tokens=16, d_in=128, d_out=128, n1=128)
+# NTT microbench: N = 2^16, 36 limbs of 50-bit primes, 64 polynomials.
+NTT_BENCH = Config("ntt", 2, 16, 50, 36, 0, 1, batch=64)
+# Hybrid key switching: N = 2^16, 24 + 8 limbs, dnum 3, 32 hoisted rotations by 1..32.
+KEYSWITCH = Config("keyswitch", 3, 16, 50, 24, 8, 3, scale_log2=40, level=23, batch=32)
+# Llama-3-8B-shaped projection: 4096 -> 14336 at level 12, 128 tokens x 256 features per ciphertext.
+PROJECTION = Config("projection", 4, 16, 50, 24, 8, 3, scale_log2=40, level=12, tokens=128,
+                    d_in=4096, d_out=14336, n1=32)
