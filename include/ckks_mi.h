@@ -1,0 +1,219 @@
+/*
+ * ckks_mi.h -- C ABI of libckks_mi.so: RNS-CKKS arithmetic under the packed
+ * ciphertext x plaintext linear projection, on one AMD Instinct MI355X (gfx950).
+ *
+ * The paper (Background, "The CKKS Computation Model") uses the primitives
+ * Encode, Add, PCMult, Mult, Rot_k, KeySwitch and Rescale; its projections
+ * evaluate Ax = sum_k D_k(A) * rho^k(x) over slot vectors (Section "Matrix
+ * Representations and Linear Computation in CKKS", Eq. slot-diagonal-matvec)
+ * with baby-step/giant-step reuse of rotations.  The calls below are those
+ * primitives plus the projection itself.  Internals follow the standard RNS
+ * form of CKKS with hybrid key switching.
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * Memory.  Every pointer named dev_* or held in a ckks_buf is device memory
+ *   owned by the caller.  The library owns only its context tables and a
+ *   grow-only scratch arena inside the context.  Nothing is freed behind the
+ *   caller's back.
+ * Layout.  A polynomial is a [limbs][N] array of uint64 residues, limb-major;
+ *   limb k of a ciphertext or plaintext is reduced modulo q_k and stored in
+ *   the NTT domain: index j holds a(psi_k^(2*brev(j)+1)) mod q_k, where psi_k
+ *   is the context's primitive 2N-th root for q_k (ckks_ctx_primes).  Every
+ *   stored residue is canonical, in [0, q_k).  A ciphertext is [2][limbs][N]
+ *   (c0 then c1); its level is limbs - 1.
+ * Streams.  Calls are asynchronous on the context's HIP stream and validate
+ *   all arguments on the host before the first launch.  Calls that return
+ *   data to the host say so.
+ * Errors.  Every call returns a ckks_status; on failure nothing has been
+ *   launched unless the status is CKKS_EHIP, and ckks_last_error() describes
+ *   the problem (thread-local, valid until the next call on the thread).  No
+ *   C++ exception crosses this boundary.
+ * Threads.  A context may be used by one host thread at a time.
+ */
+#ifndef CKKS_MI_H
+#define CKKS_MI_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct ckks_ctx ckks_ctx;
+
+typedef enum {
+    CKKS_OK = 0,
+    CKKS_EINVAL = -1,      /* bad argument: null pointer, shape, range */
+    CKKS_ELEVEL = -2,      /* operand levels do not match or level too low */
+    CKKS_ESCALE = -3,      /* operand scales differ where they must be equal */
+    CKKS_ENOKEY = -4,      /* no switching key given for a requested rotation */
+    CKKS_EHIP = -5,        /* a HIP runtime call failed */
+    CKKS_ENOMEM = -6,      /* device or host allocation failed */
+    CKKS_EUNSUPPORTED = -7 /* parameters outside what the kernels support */
+} ckks_status;
+
+/* Scheme parameters.  N = 2^log_n with 4 <= log_n <= 16.  The modulus chain
+ * is q_0..q_{n_q-1}; P = p_0 * ... * p_{n_p-1} are the special primes of
+ * hybrid key switching with dnum digits of alpha = ceil(n_q/dnum) limbs
+ * (digit j holds q-limbs [j*alpha, min((j+1)*alpha, n_q))).
+ * Primes: if q (resp. p) is NULL they are generated: the largest primes
+ * below 2^q_bits that are 1 mod 2N, in descending order; q takes the first
+ * n_q of that list and p the next n_p of the list for p_bits (skipping any
+ * prime already in q).  Every prime must be 1 mod 2N and below 2^62; explicit
+ * primes are checked. */
+typedef struct {
+    uint32_t log_n, n_q, n_p, dnum;
+    const uint64_t *q; /* host, n_q entries, or NULL */
+    const uint64_t *p; /* host, n_p entries, or NULL */
+    uint32_t q_bits, p_bits;
+} ckks_params;
+
+/* A plaintext (n_polys = 1) or ciphertext (n_polys = 2): data is
+ * [n_polys][n_limbs][N] uint64 on the device, NTT domain, limb k mod q_k. */
+typedef struct {
+    uint64_t *data;
+    uint32_t n_polys, n_limbs;
+    double scale;
+} ckks_buf;
+
+/* ---- context ------------------------------------------------------------ */
+
+/* Create a context on the current HIP device: generates or checks primes,
+ * finds psi_k (x^((q-1)/2N) for the smallest x >= 2 with psi^N = -1), and
+ * uploads twiddle, Shoup-companion, FFT and basis-conversion tables.
+ * hip_stream: the hipStream_t all calls are enqueued on (NULL = default). */
+ckks_status ckks_ctx_create(const ckks_params *params, void *hip_stream, ckks_ctx **out);
+void ckks_ctx_destroy(ckks_ctx *ctx);
+ckks_status ckks_ctx_set_stream(ckks_ctx *ctx, void *hip_stream);
+/* Host copies of the primes q (n_q), p (n_p) and psi (n_q + n_p, q first);
+ * any pointer may be NULL. */
+ckks_status ckks_ctx_primes(const ckks_ctx *ctx, uint64_t *q, uint64_t *p, uint64_t *psi);
+/* Galois element 5^steps mod 2N of a left slot rotation by steps (any sign). */
+uint32_t ckks_galois_elt(const ckks_ctx *ctx, int32_t steps);
+const char *ckks_last_error(void);
+
+/* ---- number-theoretic transforms --------------------------------------- */
+
+/* In-place negacyclic NTT / inverse NTT of dev[batch][n_limbs][N]; row limb k
+ * uses prime index limb0 + k of the combined list (q_0..q_{n_q-1},
+ * p_0..p_{n_p-1}).  Input and output residues are canonical. */
+ckks_status ckks_ntt(ckks_ctx *ctx, uint64_t *dev, uint32_t batch, uint32_t limb0, uint32_t n_limbs);
+ckks_status ckks_intt(ckks_ctx *ctx, uint64_t *dev, uint32_t batch, uint32_t limb0, uint32_t n_limbs);
+
+/* ---- encoding ------------------------------------------------------------ */
+
+/* Encode N/2 complex slots (dev_re, dev_im: fp64 device arrays; dev_im may
+ * be NULL for real slots) at scale `scale` into pt_out (n_polys = 1, n_limbs
+ * limbs, NTT domain).  The integer coefficients are
+ *   m_i = round(scale * (2/N) * Re sum_j z_j zeta^(-i 5^j)), zeta = e^(i pi/N),
+ * rounding half away from zero, evaluated in fp64 by the radix-2 FFT whose
+ * operation order the library fixes (canonical embedding of CKKS). */
+ckks_status ckks_encode(ckks_ctx *ctx, const double *dev_re, const double *dev_im, double scale,
+                        uint32_t n_limbs, ckks_buf *pt_out);
+/* Decode pt (n_polys = 1) at pt->scale into N/2 slots written to the device
+ * arrays dev_re/dev_im.  Uses the centred lift of limbs 0 and 1 (limb 0
+ * alone if the plaintext has one limb), so |m| must be below q_0*q_1/2. */
+ckks_status ckks_decode(ckks_ctx *ctx, const ckks_buf *pt, double *dev_re, double *dev_im);
+
+/* ---- encryption (test path) ---------------------------------------------- */
+
+/* Secret-key encryption ct = (-a*s + e + m, a) over the limbs of pt.
+ * dev_s: int8 [N] ternary secret (coefficients); dev_a: uint64 [limbs][N]
+ * uniform residues, NTT domain; dev_e: int32 [N] error coefficients. */
+ckks_status ckks_encrypt_sk(ckks_ctx *ctx, const int8_t *dev_s, const ckks_buf *pt, const uint64_t *dev_a,
+                            const int32_t *dev_e, ckks_buf *ct_out);
+/* pt = c0 + c1*s over the ciphertext's limbs; pt_out->scale = ct->scale. */
+ckks_status ckks_decrypt(ckks_ctx *ctx, const int8_t *dev_s, const ckks_buf *ct, ckks_buf *pt_out);
+
+/* Switching keys, [dnum][2][n_q + n_p][N] uint64 (key_j = (b_j, a_j)):
+ *   b_j = -a_j*s + e_j + [P]_{q_i} * t * [i in digit j]  on q-limbs,
+ *   b_j = -a_j*s + e_j                                    on p-limbs,
+ * with t = sigma_g(s) for a Galois key and t = s^2 for the relinearisation
+ * key.  dev_a: [dnum][n_q+n_p][N] NTT domain; dev_e: int32 [dnum][N]. */
+ckks_status ckks_keygen_galois(ckks_ctx *ctx, const int8_t *dev_s, uint32_t galois_elt, const uint64_t *dev_a,
+                               const int32_t *dev_e, uint64_t *dev_key);
+ckks_status ckks_keygen_relin(ckks_ctx *ctx, const int8_t *dev_s, const uint64_t *dev_a, const int32_t *dev_e,
+                              uint64_t *dev_key);
+
+/* ---- homomorphic operations ---------------------------------------------- */
+
+/* Add: equal limbs and bit-identical scales required (CKKS_ELEVEL/ESCALE). */
+ckks_status ckks_add(ckks_ctx *ctx, const ckks_buf *a, const ckks_buf *b, ckks_buf *out);
+/* PCMult: ct * pt slot-wise; pt needs at least ct's limbs; scale multiplies. */
+ckks_status ckks_mul_plain(ckks_ctx *ctx, const ckks_buf *ct, const ckks_buf *pt, ckks_buf *out);
+/* Mult + relinearisation: tensor (a0b0, a0b1+a1b0, a1b1), then key switch of
+ * a1b1 with dev_rlk; scale multiplies. */
+ckks_status ckks_mul_relin(ckks_ctx *ctx, const ckks_buf *a, const ckks_buf *b, const uint64_t *dev_rlk,
+                           ckks_buf *out);
+/* Rescale: c_i' = (c_i - [centred c_l mod q_l]) * q_l^-1 mod q_i, i < l,
+ * i.e. round(c / q_l); out has one limb fewer and scale / q_l. */
+ckks_status ckks_rescale(ckks_ctx *ctx, const ckks_buf *in, ckks_buf *out);
+/* Rot_steps: left rotation of the slot vector, (rho^k x)_i = x_{i+k}.  The
+ * key must be the Galois key for ckks_galois_elt(steps).  out may not alias in. */
+ckks_status ckks_rotate(ckks_ctx *ctx, const ckks_buf *in, int32_t steps, const uint64_t *dev_key, ckks_buf *out);
+/* count rotations of one ciphertext sharing a single ModUp of c1 (hoisting).
+ * Result r equals ckks_rotate(in, steps[r], dev_keys[r]) bit for bit. */
+ckks_status ckks_rotate_hoisted(ckks_ctx *ctx, const ckks_buf *in, const int32_t *steps, uint32_t count,
+                                const uint64_t *const *dev_keys, ckks_buf *outs);
+
+/* ---- key-switching stages (exposed for per-stage checks) ----------------- */
+
+/* ModUp of dev_c ([level+1][N], NTT domain): for each digit j meeting
+ * [0, level], INTT of its limbs, fast basis conversion to the other q-limbs
+ * and P (non-centred, uncorrected), NTT.  dev_digits: [n_digits][level+1+n_p][N]
+ * (q-limbs 0..level then p-limbs); n_digits = digits with a limb <= level. */
+ckks_status ckks_modup(ckks_ctx *ctx, const uint64_t *dev_c, uint32_t level, uint64_t *dev_digits);
+/* ModDown of dev_x ([level+1+n_p][N]): (x - NTT(Conv_{P->Q}(INTT([x]_P)))) * P^-1. */
+ckks_status ckks_moddown(ckks_ctx *ctx, const uint64_t *dev_x, uint32_t level, uint64_t *dev_out);
+/* NTT-domain automorphism sigma_g of rows of N: out[j] = in[j'] with
+ * 2 brev(j') + 1 = (2 brev(j) + 1) g mod 2N.  g odd.  out may not alias in. */
+ckks_status ckks_automorph(ckks_ctx *ctx, const uint64_t *dev_in, uint32_t rows, uint32_t galois_elt,
+                           uint64_t *dev_out);
+
+/* ---- the projection ------------------------------------------------------ */
+
+/* Feature-major packed projection Y = X W (X: tokens x d_in, W: d_in x d_out
+ * row-major fp64 on the device).  Slot f*tokens + t of input ciphertext i
+ * holds X[t, i*D + f], D = N/2/tokens features per ciphertext; output
+ * ciphertext j holds Y[t, j*D + o] at slot o*tokens + t.  With A = W^T and
+ * the cyclic diagonals D_k(A_{j,i})[o] = A_{j,i}[o, (o+k) mod D]:
+ *   out_j = Rescale( sum_{g<n2} Rot_{T n1 g}( sum_{i,b<n1} pt_{j,i,g,b} * Rot_{T b}(x_i) ) )
+ * where pt_{j,i,g,b} encodes at scale q_level the slot vector
+ *   p[f*T + t] = D_{n1 g + b}(A_{j,i})[(f - n1 g) mod D],  n2 = ceil(D/n1).
+ * Weight plaintexts are encoded on the fly from W.  Keys: key_steps[r] ->
+ * dev_keys[r]; steps T*b (0 < b < n1) and T*n1*g (0 < g < n2) must be present.
+ * in: d_in/D ciphertexts, all with the same n_limbs = level + 1 >= 2 and the
+ * same scale; out: d_out/D ciphertexts with n_limbs = level (the rescale
+ * drops q_level) whose scale is set to the input scale (the plaintext scale
+ * q_level cancels exactly in the rescale).  Scratch comes from the context's
+ * arena (grown with hipMalloc on first use). */
+typedef struct {
+    uint32_t tokens, d_in, d_out, n1;
+} ckks_proj_shape;
+ckks_status ckks_linear_project(ckks_ctx *ctx, const ckks_buf *in, const double *dev_W, const ckks_proj_shape *shape,
+                                const int32_t *key_steps, const uint64_t *const *dev_keys, uint32_t n_keys,
+                                ckks_buf *out);
+
+/* ---- measurement helpers ------------------------------------------------- */
+
+/* Per-kernel-class timing with HIP events on the context stream.  While
+ * enabled, every launch of the named classes is bracketed by events; read
+ * back (synchronizes) the summed milliseconds and launch count. */
+ckks_status ckks_profile_enable(ckks_ctx *ctx, int on);
+ckks_status ckks_profile_read(ckks_ctx *ctx, const char *kernel_class, double *total_ms, uint64_t *launches);
+ckks_status ckks_profile_reset(ckks_ctx *ctx);
+/* A plain device copy of `bytes` bytes (multiple of 16) on the context stream,
+ * for calibrating HBM counters and achievable bandwidth. */
+ckks_status ckks_calib_copy(ckks_ctx *ctx, void *dev_dst, const void *dev_src, size_t bytes);
+/* Modular-multiply throughput probe: `iters` dependent-chain multiplications
+ * per lane on `lanes` lanes, mode 0 = integer Shoup (64-bit, built from 32-bit
+ * multiplies), mode 1 = fp64 fused-multiply-add reduction.  Writes one value
+ * per lane to dev_out (uint64 [lanes]) so the work cannot be elided. */
+ckks_status ckks_calib_modmul(ckks_ctx *ctx, uint64_t *dev_out, uint32_t lanes, uint32_t iters, int mode);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* CKKS_MI_H */

@@ -52,6 +52,7 @@ def lib():
         i64, u64, f64 = ctypes.c_int64, ctypes.c_uint64, ctypes.c_double
         L.or_ntt.argtypes = [u64p, i64, i64, u64, u64]
         L.or_intt.argtypes = [u64p, i64, i64, u64, u64]
+        L.or_ntt_rows.argtypes = [u64p, i64, i64, u64p, u64p, ctypes.c_int]
         for name in ("or_mul", "or_add", "or_sub"):
             getattr(L, name).argtypes = [u64p, u64p, u64p, i64, i64, u64p]
         L.or_mul_scalar.argtypes = [u64p, u64p, u64p, i64, i64, u64p]
@@ -59,7 +60,7 @@ def lib():
         L.or_conv.argtypes = [u64p, u64p, i64, u64p, u64p, i64, i64, u64p, u64p]
         L.or_encode_round.argtypes = [f64p, ctypes.c_void_p, i64, f64, i64p]
         L.or_encode_def_round.argtypes = [f64p, ctypes.c_void_p, i64, f64, i64p, f64p]
-        for name in ("or_ntt", "or_intt", "or_mul", "or_add", "or_sub", "or_mul_scalar",
+        for name in ("or_ntt", "or_intt", "or_ntt_rows", "or_mul", "or_add", "or_sub", "or_mul_scalar",
                      "or_reduce_i64", "or_conv", "or_encode_round", "or_encode_def_round"):
             getattr(L, name).restype = None
         _LIB = L
@@ -173,24 +174,15 @@ class Ckks:
         return sum(1 for j in range(self.dnum) if self.digit_limbs(j, level))
 
     # ---------------- transforms ----------------
-    def ntt(self, a: np.ndarray, idx: Sequence[int]) -> np.ndarray:
-        """Forward negacyclic NTT of each row; row r uses prime idx[r]."""
+    def ntt(self, a: np.ndarray, idx: Sequence[int], inverse: bool = False) -> np.ndarray:
+        """Forward (or inverse) negacyclic NTT of each row; row r uses prime idx[r]."""
         a = _u64(a).copy()
-        a2 = a.reshape(len(idx), self.n)
-        for r, k in enumerate(idx):
-            row = np.ascontiguousarray(a2[r])
-            lib().or_ntt(row, 1, self.n, self.primes[k], self.psi[k])
-            a2[r] = row
+        lib().or_ntt_rows(a.reshape(-1), len(idx), self.n, self.mods(idx),
+                          _u64([self.psi[k] for k in idx]), int(inverse))
         return a
 
     def intt(self, a: np.ndarray, idx: Sequence[int]) -> np.ndarray:
-        a = _u64(a).copy()
-        a2 = a.reshape(len(idx), self.n)
-        for r, k in enumerate(idx):
-            row = np.ascontiguousarray(a2[r])
-            lib().or_intt(row, 1, self.n, self.primes[k], self.psi[k])
-            a2[r] = row
-        return a
+        return self.ntt(a, idx, inverse=True)
 
     def ntt_rows_same_prime(self, a: np.ndarray, k: int, inverse: bool = False) -> np.ndarray:
         """Transform every row of a [rows][N] array with prime k (the batched microbench form)."""

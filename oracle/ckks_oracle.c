@@ -67,6 +67,18 @@ static int ilog2(int64_t n)
     return l;
 }
 
+/* tw[k] = root^brev(k) for k < n (powers built by repeated multiplication). */
+static uint64_t *root_powers_brev(uint64_t root, int64_t n, int logn, uint64_t q)
+{
+    uint64_t *pw = (uint64_t *)malloc(sizeof(uint64_t) * (size_t)n);
+    uint64_t *tw = (uint64_t *)malloc(sizeof(uint64_t) * (size_t)n);
+    pw[0] = 1 % q;
+    for (int64_t e = 1; e < n; e++) pw[e] = mulm(pw[e - 1], root, q);
+    for (int64_t k = 0; k < n; k++) tw[k] = pw[brev((uint32_t)k, logn)];
+    free(pw);
+    return tw;
+}
+
 /* ------------------------------------------------------------------------ */
 /* Negacyclic NTT.                                                           */
 /* Output index j holds a(psi^(2*brev(j)+1)) mod q: evaluations at the odd   */
@@ -77,8 +89,7 @@ static int ilog2(int64_t n)
 void or_ntt(uint64_t *a, int64_t rows, int64_t n, uint64_t q, uint64_t psi)
 {
     int logn = ilog2(n);
-    uint64_t *tw = (uint64_t *)malloc(sizeof(uint64_t) * (size_t)n);
-    for (int64_t k = 0; k < n; k++) tw[k] = powm(psi, brev((uint32_t)k, logn), q);
+    uint64_t *tw = root_powers_brev(psi, n, logn, q);
 #pragma omp parallel for schedule(dynamic)
     for (int64_t r = 0; r < rows; r++) {
         uint64_t *x = a + r * n;
@@ -104,8 +115,7 @@ void or_intt(uint64_t *a, int64_t rows, int64_t n, uint64_t q, uint64_t psi)
     int logn = ilog2(n);
     uint64_t psi_inv = invm(psi, q);
     uint64_t n_inv = invm((uint64_t)(n % (int64_t)q), q);
-    uint64_t *tw = (uint64_t *)malloc(sizeof(uint64_t) * (size_t)n);
-    for (int64_t k = 0; k < n; k++) tw[k] = powm(psi_inv, brev((uint32_t)k, logn), q);
+    uint64_t *tw = root_powers_brev(psi_inv, n, logn, q);
 #pragma omp parallel for schedule(dynamic)
     for (int64_t r = 0; r < rows; r++) {
         uint64_t *x = a + r * n;
@@ -122,6 +132,19 @@ void or_intt(uint64_t *a, int64_t rows, int64_t n, uint64_t q, uint64_t psi)
         for (int64_t j = 0; j < n; j++) x[j] = mulm(x[j], n_inv, q);
     }
     free(tw);
+}
+
+/* The same transforms over rows that each carry their own prime and root
+ * (row r: qs[r], psis[r]); rows run in parallel. */
+void or_ntt_rows(uint64_t *a, int64_t rows, int64_t n, const uint64_t *qs, const uint64_t *psis, int inverse)
+{
+#pragma omp parallel for schedule(dynamic)
+    for (int64_t r = 0; r < rows; r++) {
+        if (inverse)
+            or_intt(a + r * n, 1, n, qs[r], psis[r]);
+        else
+            or_ntt(a + r * n, 1, n, qs[r], psis[r]);
+    }
 }
 
 /* ------------------------------------------------------------------------ */

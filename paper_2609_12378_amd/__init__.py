@@ -1,0 +1,350 @@
+"""Python binding of libckks_mi.so (RNS-CKKS on MI355X).
+
+Argument marshalling only: every computation runs in the library's HIP
+kernels.  Device memory comes from torch tensors (``torch.uint64`` residues,
+``torch.float64`` slots and weights, ``torch.int8`` secrets, ``torch.int32``
+errors); calls are enqueued on the context's HIP stream, which defaults to the
+current torch stream at context creation.  The library must be built first
+(``python -m paper_2609_12378_amd.build``); importing this package on a machine
+without the built library raises instead of falling back to anything else.
+"""
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Dict, List, Optional, Sequence
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libckks_mi.so")
+
+__all__ = ["Context", "Buf", "CkksError", "load_library", "LIB_PATH"]
+
+
+class CkksError(RuntimeError):
+    pass
+
+
+class _Params(ctypes.Structure):
+    _fields_ = [("log_n", ctypes.c_uint32), ("n_q", ctypes.c_uint32), ("n_p", ctypes.c_uint32),
+                ("dnum", ctypes.c_uint32), ("q", ctypes.POINTER(ctypes.c_uint64)),
+                ("p", ctypes.POINTER(ctypes.c_uint64)), ("q_bits", ctypes.c_uint32), ("p_bits", ctypes.c_uint32)]
+
+
+class _Buf(ctypes.Structure):
+    _fields_ = [("data", ctypes.c_void_p), ("n_polys", ctypes.c_uint32), ("n_limbs", ctypes.c_uint32),
+                ("scale", ctypes.c_double)]
+
+
+class _ProjShape(ctypes.Structure):
+    _fields_ = [("tokens", ctypes.c_uint32), ("d_in", ctypes.c_uint32), ("d_out", ctypes.c_uint32),
+                ("n1", ctypes.c_uint32)]
+
+
+_LIB = None
+
+# name -> (restype, argtypes)
+_VP, _U32, _I32, _U64, _DBL, _SZ = ctypes.c_void_p, ctypes.c_uint32, ctypes.c_int32, ctypes.c_uint64, \
+    ctypes.c_double, ctypes.c_size_t
+_BP = ctypes.POINTER(_Buf)
+_SIGS = {
+    "ckks_ctx_create": (ctypes.c_int, [ctypes.POINTER(_Params), _VP, ctypes.POINTER(_VP)]),
+    "ckks_ctx_destroy": (None, [_VP]),
+    "ckks_ctx_set_stream": (ctypes.c_int, [_VP, _VP]),
+    "ckks_ctx_primes": (ctypes.c_int, [_VP, _VP, _VP, _VP]),
+    "ckks_galois_elt": (_U32, [_VP, _I32]),
+    "ckks_last_error": (ctypes.c_char_p, []),
+    "ckks_ntt": (ctypes.c_int, [_VP, _VP, _U32, _U32, _U32]),
+    "ckks_intt": (ctypes.c_int, [_VP, _VP, _U32, _U32, _U32]),
+    "ckks_encode": (ctypes.c_int, [_VP, _VP, _VP, _DBL, _U32, _BP]),
+    "ckks_decode": (ctypes.c_int, [_VP, _BP, _VP, _VP]),
+    "ckks_encrypt_sk": (ctypes.c_int, [_VP, _VP, _BP, _VP, _VP, _BP]),
+    "ckks_decrypt": (ctypes.c_int, [_VP, _VP, _BP, _BP]),
+    "ckks_keygen_galois": (ctypes.c_int, [_VP, _VP, _U32, _VP, _VP, _VP]),
+    "ckks_keygen_relin": (ctypes.c_int, [_VP, _VP, _VP, _VP, _VP]),
+    "ckks_add": (ctypes.c_int, [_VP, _BP, _BP, _BP]),
+    "ckks_mul_plain": (ctypes.c_int, [_VP, _BP, _BP, _BP]),
+    "ckks_mul_relin": (ctypes.c_int, [_VP, _BP, _BP, _VP, _BP]),
+    "ckks_rescale": (ctypes.c_int, [_VP, _BP, _BP]),
+    "ckks_rotate": (ctypes.c_int, [_VP, _BP, _I32, _VP, _BP]),
+    "ckks_rotate_hoisted": (ctypes.c_int, [_VP, _BP, _VP, _U32, _VP, _BP]),
+    "ckks_modup": (ctypes.c_int, [_VP, _VP, _U32, _VP]),
+    "ckks_moddown": (ctypes.c_int, [_VP, _VP, _U32, _VP]),
+    "ckks_automorph": (ctypes.c_int, [_VP, _VP, _U32, _U32, _VP]),
+    "ckks_linear_project": (ctypes.c_int, [_VP, _BP, _VP, ctypes.POINTER(_ProjShape), _VP, _VP, _U32, _BP]),
+    "ckks_profile_enable": (ctypes.c_int, [_VP, ctypes.c_int]),
+    "ckks_profile_read": (ctypes.c_int, [_VP, ctypes.c_char_p, ctypes.POINTER(_DBL), ctypes.POINTER(_U64)]),
+    "ckks_profile_reset": (ctypes.c_int, [_VP]),
+    "ckks_calib_copy": (ctypes.c_int, [_VP, _VP, _VP, _SZ]),
+    "ckks_calib_modmul": (ctypes.c_int, [_VP, _VP, _U32, _U32, ctypes.c_int]),
+}
+EXPORTED = tuple(_SIGS)
+
+
+def load_library(path: str = LIB_PATH):
+    """Load libckks_mi.so and declare every exported call; raise if it is missing."""
+    global _LIB
+    if _LIB is None:
+        if not os.path.exists(path):
+            raise CkksError("libckks_mi.so is not built (%s); run python -m paper_2609_12378_amd.build" % path)
+        L = ctypes.CDLL(path)
+        for name, (res, args) in _SIGS.items():
+            fn = getattr(L, name, None)
+            if fn is None:
+                continue
+            fn.restype = res
+            fn.argtypes = args
+        _LIB = L
+    return _LIB
+
+
+def missing_symbols(path: str = LIB_PATH) -> List[str]:
+    """Declared calls that the built library does not export."""
+    L = load_library(path)
+    return [n for n in _SIGS if getattr(L, n, None) is None]
+
+
+def _check(st: int, what: str):
+    if st != 0:
+        msg = load_library().ckks_last_error().decode(errors="replace")
+        raise CkksError("%s failed (status %d): %s" % (what, st, msg))
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise CkksError("expected a device tensor")
+    if not t.is_contiguous():
+        raise CkksError("expected a contiguous tensor")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+@dataclass
+class Buf:
+    """A plaintext ([1][limbs][N]) or ciphertext ([2][limbs][N]) tensor with its scale."""
+    data: torch.Tensor
+    scale: float
+
+    @property
+    def n_polys(self) -> int:
+        return self.data.shape[0]
+
+    @property
+    def n_limbs(self) -> int:
+        return self.data.shape[1]
+
+    @property
+    def level(self) -> int:
+        return self.n_limbs - 1
+
+    def c(self) -> _Buf:
+        d = self.data
+        if d.dtype != torch.uint64 or d.dim() != 3:
+            raise CkksError("buffer must be a 3-d uint64 tensor")
+        return _Buf(_ptr(d), d.shape[0], d.shape[1], float(self.scale))
+
+
+class Context:
+    """A libckks_mi context on the current HIP device and stream."""
+
+    def __init__(self, log_n: int, n_q: int, n_p: int = 0, dnum: int = 1, q_bits: int = 50, p_bits: int = 0,
+                 q: Optional[Sequence[int]] = None, p: Optional[Sequence[int]] = None, stream=None):
+        L = load_library()
+        self.lib = L
+        qa = (ctypes.c_uint64 * n_q)(*q) if q is not None else None
+        pa = (ctypes.c_uint64 * n_p)(*p) if p is not None else None
+        prm = _Params(log_n, n_q, n_p, dnum, qa, pa, q_bits, p_bits or q_bits)
+        if stream is None:
+            stream = torch.cuda.current_stream()
+        self._stream = stream
+        h = ctypes.c_void_p()
+        _check(L.ckks_ctx_create(ctypes.byref(prm), ctypes.c_void_p(stream.cuda_stream), ctypes.byref(h)),
+               "ckks_ctx_create")
+        self.h = h
+        self.log_n, self.n = log_n, 1 << log_n
+        self.n_q, self.n_p, self.dnum = n_q, n_p, dnum
+        self.alpha = -(-n_q // dnum)
+        qo = (ctypes.c_uint64 * max(n_q, 1))()
+        po = (ctypes.c_uint64 * max(n_p, 1))()
+        so = (ctypes.c_uint64 * (n_q + n_p))()
+        _check(L.ckks_ctx_primes(h, qo, po, so), "ckks_ctx_primes")
+        self.q = list(qo)[:n_q]
+        self.p = list(po)[:n_p]
+        self.psi = list(so)
+        self.primes = self.q + self.p
+
+    def __del__(self):
+        h = getattr(self, "h", None)
+        if h is not None and h.value:
+            try:
+                self.lib.ckks_ctx_destroy(h)
+            except Exception:
+                pass
+            self.h = None
+
+    # ---------------- helpers ----------------
+    def galois_elt(self, steps: int) -> int:
+        return int(self.lib.ckks_galois_elt(self.h, steps))
+
+    def n_digits(self, level: int) -> int:
+        return level // self.alpha + 1
+
+    def zeros(self, n_polys: int, n_limbs: int) -> torch.Tensor:
+        return torch.zeros((n_polys, n_limbs, self.n), dtype=torch.uint64, device="cuda")
+
+    # ---------------- transforms ----------------
+    def ntt(self, t: torch.Tensor, limb0: int = 0, inverse: bool = False):
+        """In-place (inverse) NTT of t viewed as [batch][limbs][N]; limbs use primes limb0.."""
+        nl = t.shape[-2]
+        batch = t.numel() // (nl * self.n)
+        fn = self.lib.ckks_intt if inverse else self.lib.ckks_ntt
+        _check(fn(self.h, _ptr(t), batch, limb0, nl), "ckks_intt" if inverse else "ckks_ntt")
+        return t
+
+    def intt(self, t: torch.Tensor, limb0: int = 0):
+        return self.ntt(t, limb0, inverse=True)
+
+    # ---------------- encoding ----------------
+    def encode(self, re: torch.Tensor, im: Optional[torch.Tensor], scale: float, n_limbs: int,
+               out: Optional[torch.Tensor] = None) -> Buf:
+        out = self.zeros(1, n_limbs) if out is None else out
+        b = Buf(out, scale)
+        cb = b.c()
+        _check(self.lib.ckks_encode(self.h, _ptr(re), _ptr(im), float(scale), n_limbs, ctypes.byref(cb)),
+               "ckks_encode")
+        return b
+
+    def decode(self, pt: Buf):
+        re = torch.empty(self.n // 2, dtype=torch.float64, device="cuda")
+        im = torch.empty(self.n // 2, dtype=torch.float64, device="cuda")
+        cb = pt.c()
+        _check(self.lib.ckks_decode(self.h, ctypes.byref(cb), _ptr(re), _ptr(im)), "ckks_decode")
+        return re, im
+
+    # ---------------- encryption ----------------
+    def encrypt(self, s: torch.Tensor, pt: Buf, a: torch.Tensor, e: torch.Tensor) -> Buf:
+        out = Buf(self.zeros(2, pt.n_limbs), pt.scale)
+        cp, co = pt.c(), out.c()
+        _check(self.lib.ckks_encrypt_sk(self.h, _ptr(s), ctypes.byref(cp), _ptr(a), _ptr(e), ctypes.byref(co)),
+               "ckks_encrypt_sk")
+        return out
+
+    def decrypt(self, s: torch.Tensor, ct: Buf) -> Buf:
+        out = Buf(self.zeros(1, ct.n_limbs), ct.scale)
+        ci, co = ct.c(), out.c()
+        _check(self.lib.ckks_decrypt(self.h, _ptr(s), ctypes.byref(ci), ctypes.byref(co)), "ckks_decrypt")
+        return out
+
+    def key_shape(self):
+        return (self.dnum, 2, self.n_q + self.n_p, self.n)
+
+    def keygen_galois(self, s, g: int, a, e, out=None) -> torch.Tensor:
+        out = torch.empty(self.key_shape(), dtype=torch.uint64, device="cuda") if out is None else out
+        _check(self.lib.ckks_keygen_galois(self.h, _ptr(s), g, _ptr(a), _ptr(e), _ptr(out)), "ckks_keygen_galois")
+        return out
+
+    def keygen_relin(self, s, a, e, out=None) -> torch.Tensor:
+        out = torch.empty(self.key_shape(), dtype=torch.uint64, device="cuda") if out is None else out
+        _check(self.lib.ckks_keygen_relin(self.h, _ptr(s), _ptr(a), _ptr(e), _ptr(out)), "ckks_keygen_relin")
+        return out
+
+    # ---------------- ciphertext operations ----------------
+    def _binop(self, name, a: Buf, b: Buf, out_scale: float, out_limbs: int) -> Buf:
+        out = Buf(self.zeros(2, out_limbs), out_scale)
+        ca, cb, co = a.c(), b.c(), out.c()
+        _check(getattr(self.lib, name)(self.h, ctypes.byref(ca), ctypes.byref(cb), ctypes.byref(co)), name)
+        return out
+
+    def add(self, a: Buf, b: Buf) -> Buf:
+        return self._binop("ckks_add", a, b, a.scale, a.n_limbs)
+
+    def mul_plain(self, ct: Buf, pt: Buf) -> Buf:
+        return self._binop("ckks_mul_plain", ct, pt, ct.scale * pt.scale, ct.n_limbs)
+
+    def mul_relin(self, a: Buf, b: Buf, rlk: torch.Tensor) -> Buf:
+        out = Buf(self.zeros(2, a.n_limbs), a.scale * b.scale)
+        ca, cb, co = a.c(), b.c(), out.c()
+        _check(self.lib.ckks_mul_relin(self.h, ctypes.byref(ca), ctypes.byref(cb), _ptr(rlk), ctypes.byref(co)),
+               "ckks_mul_relin")
+        return out
+
+    def rescale(self, ct: Buf) -> Buf:
+        out = Buf(self.zeros(2, ct.n_limbs - 1), ct.scale / self.q[ct.level])
+        ci, co = ct.c(), out.c()
+        _check(self.lib.ckks_rescale(self.h, ctypes.byref(ci), ctypes.byref(co)), "ckks_rescale")
+        return out
+
+    def rotate(self, ct: Buf, steps: int, key: torch.Tensor) -> Buf:
+        out = Buf(self.zeros(2, ct.n_limbs), ct.scale)
+        ci, co = ct.c(), out.c()
+        _check(self.lib.ckks_rotate(self.h, ctypes.byref(ci), steps, _ptr(key), ctypes.byref(co)), "ckks_rotate")
+        return out
+
+    def rotate_hoisted(self, ct: Buf, steps: Sequence[int], keys: Sequence[torch.Tensor],
+                       outs: Optional[Sequence[Buf]] = None) -> List[Buf]:
+        cnt = len(steps)
+        if outs is None:
+            outs = [Buf(self.zeros(2, ct.n_limbs), ct.scale) for _ in range(cnt)]
+        st = (ctypes.c_int32 * cnt)(*steps)
+        kp = (ctypes.c_void_p * cnt)(*[k.data_ptr() for k in keys])
+        ob = (_Buf * cnt)(*[o.c() for o in outs])
+        ci = ct.c()
+        _check(self.lib.ckks_rotate_hoisted(self.h, ctypes.byref(ci), st, cnt, kp, ob), "ckks_rotate_hoisted")
+        return list(outs)
+
+    def modup(self, c: torch.Tensor, level: int) -> torch.Tensor:
+        out = torch.empty((self.n_digits(level), level + 1 + self.n_p, self.n), dtype=torch.uint64, device="cuda")
+        _check(self.lib.ckks_modup(self.h, _ptr(c), level, _ptr(out)), "ckks_modup")
+        return out
+
+    def moddown(self, x: torch.Tensor, level: int) -> torch.Tensor:
+        out = torch.empty((level + 1, self.n), dtype=torch.uint64, device="cuda")
+        _check(self.lib.ckks_moddown(self.h, _ptr(x), level, _ptr(out)), "ckks_moddown")
+        return out
+
+    def automorph(self, x: torch.Tensor, g: int) -> torch.Tensor:
+        out = torch.empty_like(x)
+        rows = x.numel() // self.n
+        _check(self.lib.ckks_automorph(self.h, _ptr(x), rows, g, _ptr(out)), "ckks_automorph")
+        return out
+
+    def linear_project(self, cts: Sequence[Buf], W: torch.Tensor, tokens: int, n1: int,
+                       keys: Dict[int, torch.Tensor], outs: Optional[Sequence[Buf]] = None) -> List[Buf]:
+        d_in, d_out = W.shape
+        D = (self.n // 2) // tokens
+        n_out = d_out // D
+        level = cts[0].level
+        if outs is None:
+            outs = [Buf(self.zeros(2, level), cts[0].scale) for _ in range(n_out)]
+        inb = (_Buf * len(cts))(*[c.c() for c in cts])
+        ob = (_Buf * n_out)(*[o.c() for o in outs])
+        steps = sorted(keys)
+        ks = (ctypes.c_int32 * len(steps))(*steps)
+        kp = (ctypes.c_void_p * len(steps))(*[keys[s].data_ptr() for s in steps])
+        shape = _ProjShape(tokens, d_in, d_out, n1)
+        _check(self.lib.ckks_linear_project(self.h, inb, _ptr(W), ctypes.byref(shape), ks, kp, len(steps), ob),
+               "ckks_linear_project")
+        for o, b in zip(outs, ob):
+            o.scale = b.scale
+        return list(outs)
+
+    # ---------------- measurement ----------------
+    def profile(self, on: bool = True):
+        _check(self.lib.ckks_profile_enable(self.h, int(on)), "ckks_profile_enable")
+
+    def profile_reset(self):
+        _check(self.lib.ckks_profile_reset(self.h), "ckks_profile_reset")
+
+    def profile_read(self, cls: str):
+        ms, cnt = ctypes.c_double(), ctypes.c_uint64()
+        _check(self.lib.ckks_profile_read(self.h, cls.encode(), ctypes.byref(ms), ctypes.byref(cnt)),
+               "ckks_profile_read")
+        return ms.value, cnt.value
+
+    def calib_copy(self, dst: torch.Tensor, src: torch.Tensor):
+        _check(self.lib.ckks_calib_copy(self.h, _ptr(dst), _ptr(src), src.numel() * src.element_size()),
+               "ckks_calib_copy")
+
+    def calib_modmul(self, out: torch.Tensor, iters: int, mode: int):
+        _check(self.lib.ckks_calib_modmul(self.h, _ptr(out), out.numel(), iters, mode), "ckks_calib_modmul")

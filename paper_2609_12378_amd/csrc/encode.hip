@@ -1,0 +1,298 @@
+// CKKS encoding through the canonical embedding (Cheon-Kim-Kim-Song 2017),
+// batched over many slot vectors.
+//
+// The integer coefficients of Encode_Delta(z) are
+//   m_i = round(Delta * (2/N) * Re sum_{j<N/2} z_j zeta^(-i 5^j)),  zeta = e^(i pi/N).
+// With M = N/2 the exponents 5^j mod 2N are exactly the residues 1 mod 4, so
+// writing 5^j = 4s + 1 turns the sum into v_k = zeta^-k * Y_k, where Y is the
+// length-M DFT with omega^(-k s) (omega = e^(2 pi i/M)) of y_s = z_j; then
+// m_k = round(c Re v_k), m_{k+M} = round(c Im v_k), c = Delta * 2/N.
+//
+// Rounding near a half-integer depends on every bit of the fp64 result, so the
+// evaluation order is fixed: a radix-2 decimation-in-time FFT from bit-reversed
+// input, stages len = 2, 4, ..., M, butterfly t = w * a[hi], a[hi] = a[lo] - t,
+// a[lo] = a[lo] + t with w = omega^(-k M/len), complex products formed as
+// (ar*br - ai*bi, ar*bi + ai*br) without fused multiply-add, twiddles taken from
+// host tables (cos, -sin) of the angles 2 pi e / M and pi k / N.  The schedule
+// below (which butterflies run on which thread, in which pass) is free; each
+// butterfly's arithmetic is not.
+//
+// MI355X mapping: pass A runs the first log2(BA) stages on contiguous blocks of
+// BA = min(M, 2048) points in LDS; pass B runs the remaining <= 4 stages with
+// each thread holding one column of M/BA points in registers, and fuses the
+// twist, scaling and rounding.  Slot vectors of the projection are generated
+// inside the gather kernel from W's cyclic diagonals, so they never exist in
+// memory.
+#pragma clang fp contract(off)
+#include "ckks_internal.h"
+#include "ops.h"
+
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kLogBA = 11;  // pass-A block: 2048 complex = 32 KiB of LDS
+
+__device__ __forceinline__ double2 cmul(double2 a, double2 b)
+{
+    const double p1 = a.x * b.x, p2 = a.y * b.y, p3 = a.x * b.y, p4 = a.y * b.x;
+    return make_double2(p1 - p2, p3 + p4);
+}
+
+// slot value j of plaintext p of the batch
+__device__ __forceinline__ double2 slot_value(const SlotSource &s, uint32_t p, uint32_t j, uint32_t M)
+{
+    if (s.W == nullptr) {
+        const double re = s.re[(size_t)p * M + j];
+        const double im = s.im ? s.im[(size_t)p * M + j] : 0.0;
+        return make_double2(re, im);
+    }
+    // feature-major slot j = f*T + t holds D_{n1 g + b}(A_{jb,i})[(f - n1 g) mod D] with
+    // A = W^T, A_{jb,i}[o][c] = W[i D + c][jb D + o], D_k(A)[o] = A[o][(o + k) mod D]
+    const uint32_t D = s.feats;
+    const uint32_t jb = s.j0 + p / s.pairs;
+    const uint32_t pair = s.ib0 + p % s.pairs;
+    const uint32_t i = pair / s.bcount, b = pair % s.bcount;
+    const uint32_t f = j / s.tokens;
+    const uint32_t o = (f + D - s.n1g % D) % D;
+    const uint32_t c = (o + s.n1g + b) % D;
+    return make_double2(s.W[(size_t)(i * D + c) * s.d_out + (size_t)jb * D + o], 0.0);
+}
+
+// gather into bit-reversed FFT order: a[p][pos[j]] = z_j
+__global__ __launch_bounds__(kThreads) void k_gather(double2 *a, SlotSource s, const uint32_t *__restrict__ pos,
+                                                      uint32_t M)
+{
+    const uint32_t j = blockIdx.x * kThreads + threadIdx.x;
+    const uint32_t p = blockIdx.y;
+    if (j >= M) return;
+    a[(size_t)p * M + pos[j]] = slot_value(s, p, j, M);
+}
+
+__device__ __forceinline__ void round_out(int64_t *m, size_t base, uint32_t k, uint32_t M, double2 y, double2 tw,
+                                          double c)
+{
+    const double2 v = cmul(tw, y);
+    m[base + k] = (int64_t)round(c * v.x);
+    m[base + k + M] = (int64_t)round(c * v.y);
+}
+
+// Pass A: stages len = 2 .. 2^logb on contiguous blocks of 2^logb points.
+// mode 0: write complex back; mode 1: final pass, twist/round into m.
+__global__ __launch_bounds__(kThreads) void k_fft_a(double2 *a, const double2 *__restrict__ w, uint32_t logm,
+                                                     uint32_t logb, int mode, const double2 *__restrict__ twist,
+                                                     double c, int64_t *m)
+{
+    extern __shared__ double2 sh[];
+    const uint32_t M = 1u << logm, B = 1u << logb;
+    const uint32_t blocks_per = M >> logb;
+    const uint32_t p = blockIdx.x / blocks_per, blk = blockIdx.x % blocks_per;
+    double2 *src = a + (size_t)p * M + (size_t)blk * B;
+    for (uint32_t x = threadIdx.x; x < B; x += kThreads) sh[x] = src[x];
+    __syncthreads();
+    for (uint32_t ls = 1; ls <= logb; ls++) {
+        const uint32_t half = 1u << (ls - 1);
+        const uint32_t step = M >> ls;  // twiddle exponent multiplier M/len
+        for (uint32_t bf = threadIdx.x; bf < B / 2; bf += kThreads) {
+            const uint32_t k = bf & (half - 1);
+            const uint32_t lo = ((bf >> (ls - 1)) << ls) + k, hi = lo + half;
+            const double2 t = cmul(w[k * step], sh[hi]);
+            const double2 u = sh[lo];
+            sh[lo] = make_double2(u.x + t.x, u.y + t.y);
+            sh[hi] = make_double2(u.x - t.x, u.y - t.y);
+        }
+        __syncthreads();
+    }
+    if (mode == 0) {
+        for (uint32_t x = threadIdx.x; x < B; x += kThreads) src[x] = sh[x];
+    } else {
+        for (uint32_t x = threadIdx.x; x < B; x += kThreads) round_out(m, (size_t)p * 2 * M, x, M, sh[x], twist[x], c);
+    }
+}
+
+// Pass B: stages len = 2^(logb+1) .. M; thread owns column c (points h*B + c, h < 2^HB).
+template <int HB>
+__global__ __launch_bounds__(kThreads) void k_fft_b(double2 *a, const double2 *__restrict__ w, uint32_t logm,
+                                                     uint32_t logb, int mode, const double2 *__restrict__ twist,
+                                                     double c, int64_t *m)
+{
+    const uint32_t M = 1u << logm, B = 1u << logb;
+    const uint32_t cols_blocks = B / kThreads;
+    const uint32_t p = blockIdx.x / cols_blocks;
+    const uint32_t col = (blockIdx.x % cols_blocks) * kThreads + threadIdx.x;
+    double2 *src = a + (size_t)p * M;
+    double2 x[1 << HB];
+#pragma unroll
+    for (int h = 0; h < (1 << HB); h++) x[h] = src[(size_t)h * B + col];
+#pragma unroll
+    for (int s = 1; s <= HB; s++) {
+        const int half = 1 << (s - 1);
+        const uint32_t step = M >> (logb + s);  // M / len
+#pragma unroll
+        for (int h = 0; h < (1 << HB); h++) {
+            if (h & half) continue;
+            const uint32_t k = (uint32_t)(h & (half - 1)) * B + col;  // position inside the len-block
+            const double2 t = cmul(w[k * step], x[h + half]);
+            const double2 u = x[h];
+            x[h] = make_double2(u.x + t.x, u.y + t.y);
+            x[h + half] = make_double2(u.x - t.x, u.y - t.y);
+        }
+    }
+    if (mode == 0) {
+#pragma unroll
+        for (int h = 0; h < (1 << HB); h++) src[(size_t)h * B + col] = x[h];
+    } else {
+#pragma unroll
+        for (int h = 0; h < (1 << HB); h++) {
+            const uint32_t k = (uint32_t)h * B + col;
+            round_out(m, (size_t)p * 2 * M, k, M, x[h], twist[k], c);
+        }
+    }
+}
+
+// m (int64 [batch][N]) -> residues [batch][limbs][N]
+__global__ __launch_bounds__(kThreads) void k_to_rns(uint64_t *out, const int64_t *m, uint32_t limbs, uint32_t log_n,
+                                                      const ModQ *__restrict__ mods)
+{
+    const uint32_t n = 1u << log_n;
+    const uint32_t col = blockIdx.x * kThreads + threadIdx.x;
+    const uint32_t p = blockIdx.y;
+    if (col >= n) return;
+    const int64_t v = m[((size_t)p << log_n) + col];
+    const bool neg = v < 0;
+    const uint64_t mag = neg ? (uint64_t)(-(v + 1)) + 1u : (uint64_t)v;
+    for (uint32_t l = 0; l < limbs; l++) {
+        const ModQ md = mods[l];
+        uint64_t r = csub(mag - mulhi64(mag, md.one_s) * md.q, md.q);
+        if (neg && r) r = md.q - r;
+        out[(((size_t)p * limbs + l) << log_n) + col] = r;
+    }
+}
+
+// Decode, step 1: centred CRT lift of limbs 0 (and 1) of the coefficient form,
+// scaled by 1/Delta, twisted by zeta^-i and conjugated, into bit-reversed FFT
+// order: the inverse-direction FFT of conj((m_i + i m_{i+M}) zeta^i) is the
+// conjugate of the decoding sum.
+__global__ __launch_bounds__(kThreads) void k_decode_in(double2 *a, const uint64_t *coef, uint32_t limbs,
+                                                         uint32_t log_n, const ModQ *__restrict__ mods,
+                                                         const double2 *__restrict__ twist, double inv_scale,
+                                                         uint64_t q0inv, uint64_t q0inv_s)
+{
+    const uint32_t n = 1u << log_n, M = n / 2, logm = log_n - 1;
+    const uint32_t i = blockIdx.x * kThreads + threadIdx.x;
+    if (i >= M) return;
+    const uint64_t q0 = mods[0].q;
+    double v[2];
+    for (int h = 0; h < 2; h++) {
+        const uint32_t idx = i + h * M;
+        const uint64_t x0 = coef[idx];
+        double val;
+        if (limbs == 1) {
+            val = x0 > q0 / 2 ? -(double)(q0 - x0) : (double)x0;
+        } else {
+            const uint64_t q1 = mods[1].q;
+            const uint64_t x1 = coef[n + idx];
+            const uint64_t d = shoup(submod(x1, csub(x0, q1), q1), q0inv, q0inv_s, q1);
+            const unsigned __int128 Q = (unsigned __int128)q0 * q1;
+            const unsigned __int128 x = (unsigned __int128)q0 * d + x0;  // in [0, q0 q1)
+            const bool neg = x > Q / 2;
+            const unsigned __int128 mag = neg ? Q - x : x;
+            const double dv = (double)(uint64_t)(mag >> 64) * 18446744073709551616.0 + (double)(uint64_t)mag;
+            val = neg ? -dv : dv;
+        }
+        v[h] = val * inv_scale;
+    }
+    a[__brev(i) >> (32 - logm)] = cmul(twist[i], make_double2(v[0], -v[1]));
+}
+
+// Decode, step 3: slot j = conj(Y[s(j)]), s(j) the natural index whose bit reversal is pos[j]
+__global__ __launch_bounds__(kThreads) void k_decode_out(const double2 *y, const uint32_t *__restrict__ pos,
+                                                          uint32_t logm, double *re, double *im)
+{
+    const uint32_t M = 1u << logm;
+    const uint32_t j = blockIdx.x * kThreads + threadIdx.x;
+    if (j >= M) return;
+    const double2 v = y[__brev(pos[j]) >> (32 - logm)];
+    re[j] = v.x;
+    im[j] = -v.y;
+}
+
+}  // namespace
+
+size_t enc_work_bytes(const ckks_ctx *ctx, uint32_t batch) { return (size_t)batch * (ctx->n / 2) * sizeof(double2); }
+
+ckks_status fft_passes(ckks_ctx *ctx, double2 *work, uint32_t batch, int mode, double c, int64_t *m)
+{
+    const uint32_t logm = ctx->log_n - 1, M = 1u << logm;
+    const uint32_t logb = logm < (uint32_t)kLogBA ? logm : (uint32_t)kLogBA;
+    const uint32_t B = 1u << logb;
+    const bool single = logb == logm;
+    prof_begin(ctx, K_ENCODE_FFT);
+    hipLaunchKernelGGL(k_fft_a, dim3(batch * (M >> logb)), dim3(kThreads), B * sizeof(double2), ctx->stream, work,
+                       ctx->d_fft_w, logm, logb, single ? mode : 0, ctx->d_fft_twist, c, m);
+    if (!single) {
+        const uint32_t hb = logm - logb;
+        const dim3 grid(batch * (B / kThreads));
+        switch (hb) {
+        case 1: hipLaunchKernelGGL(k_fft_b<1>, grid, dim3(kThreads), 0, ctx->stream, work, ctx->d_fft_w, logm, logb,
+                                   mode, ctx->d_fft_twist, c, m); break;
+        case 2: hipLaunchKernelGGL(k_fft_b<2>, grid, dim3(kThreads), 0, ctx->stream, work, ctx->d_fft_w, logm, logb,
+                                   mode, ctx->d_fft_twist, c, m); break;
+        case 3: hipLaunchKernelGGL(k_fft_b<3>, grid, dim3(kThreads), 0, ctx->stream, work, ctx->d_fft_w, logm, logb,
+                                   mode, ctx->d_fft_twist, c, m); break;
+        case 4: hipLaunchKernelGGL(k_fft_b<4>, grid, dim3(kThreads), 0, ctx->stream, work, ctx->d_fft_w, logm, logb,
+                                   mode, ctx->d_fft_twist, c, m); break;
+        default: prof_end(ctx, K_ENCODE_FFT); return set_error(CKKS_EUNSUPPORTED, "fft: unsupported size");
+        }
+    }
+    prof_end(ctx, K_ENCODE_FFT);
+    HIP_TRY(hipGetLastError());
+    return CKKS_OK;
+}
+
+ckks_status enc_coeffs(ckks_ctx *ctx, const SlotSource &src, uint32_t batch, double scale, double2 *work,
+                       int64_t *m_out)
+{
+    if (!batch) return CKKS_OK;
+    const uint32_t M = ctx->n / 2;
+    hipLaunchKernelGGL(k_gather, dim3((M + kThreads - 1) / kThreads, batch), dim3(kThreads), 0, ctx->stream, work,
+                       src, ctx->d_slot_pos, M);
+    HIP_TRY(hipGetLastError());
+    return fft_passes(ctx, work, batch, 1, scale * (2.0 / (double)ctx->n), m_out);
+}
+
+ckks_status enc_to_rns(ckks_ctx *ctx, const int64_t *m, uint32_t batch, uint32_t limbs, uint64_t *out)
+{
+    if (!batch) return CKKS_OK;
+    hipLaunchKernelGGL(k_to_rns, dim3((ctx->n + kThreads - 1) / kThreads, batch), dim3(kThreads), 0, ctx->stream,
+                       out, m, limbs, ctx->log_n, ctx->d_mod);
+    HIP_TRY(hipGetLastError());
+    return CKKS_OK;
+}
+
+ckks_status dec_slots(ckks_ctx *ctx, const uint64_t *coef, uint32_t limbs, double scale, double2 *work, double *re,
+                      double *im)
+{
+    const uint32_t M = ctx->n / 2;
+    uint64_t q0inv = 0, q0inv_s = 0;
+    if (limbs > 1) {
+        const unsigned __int128 q1 = ctx->primes[1];
+        // q0^-1 mod q1 by Fermat
+        uint64_t b = ctx->primes[0] % ctx->primes[1], e = ctx->primes[1] - 2, r = 1;
+        while (e) {
+            if (e & 1) r = (uint64_t)((unsigned __int128)r * b % q1);
+            b = (uint64_t)((unsigned __int128)b * b % q1);
+            e >>= 1;
+        }
+        q0inv = r;
+        q0inv_s = (uint64_t)(((unsigned __int128)r << 64) / q1);
+    }
+    const dim3 grid((M + kThreads - 1) / kThreads);
+    hipLaunchKernelGGL(k_decode_in, grid, dim3(kThreads), 0, ctx->stream, work, coef, limbs > 1 ? 2u : 1u,
+                       ctx->log_n, ctx->d_mod, ctx->d_fft_twist, 1.0 / scale, q0inv, q0inv_s);
+    HIP_TRY(hipGetLastError());
+    CK_TRY(fft_passes(ctx, work, 1, 0, 0.0, nullptr));
+    hipLaunchKernelGGL(k_decode_out, grid, dim3(kThreads), 0, ctx->stream, work, ctx->d_slot_pos, ctx->log_n - 1, re,
+                       im);
+    HIP_TRY(hipGetLastError());
+    return CKKS_OK;
+}

@@ -1,0 +1,220 @@
+// Hybrid key switching (Han-Ki 2020) in the RNS form of CKKS:
+//
+//   ModUp of digit j:  INTT of the digit's limbs, fast basis conversion to the
+//                      other q-limbs and the special primes P, NTT;
+//   inner product:     (u0, u1) = sum_j sigma_g(d_j) * (b_j, a_j) over Q_l u P,
+//                      with the Galois automorphism folded into the digit loads;
+//   ModDown:           u -> (u - NTT(Conv_{P->Q}(INTT([u]_P)))) * P^-1, fused
+//                      with the final additions of the rotation or relinearisation.
+//
+// The fast basis conversion (Cheon-Han-Kim-Kim-Song 2018) is
+//   Conv(x)_t = sum_i [x_i * Qhat_i^-1]_{q_i} * [Qhat_i]_t  (mod t),
+// non-centred and without overflow correction.  Every constant multiplier is a
+// Shoup product, so a conversion with ns source limbs and nt targets costs
+// ns + ns*nt Shoup multiplications per coefficient.  The inner dimension
+// (ns <= 8 at the benchmark parameters) is far too small and too wide-integer
+// for the matrix cores, so it runs on the vector ALUs.
+#include "ckks_internal.h"
+#include "ops.h"
+
+namespace {
+
+constexpr int kThreads = 256;
+
+__device__ __forceinline__ uint32_t auto_index(uint32_t j, uint32_t g, uint32_t log_n)
+{
+    const uint32_t two_n_mask = (2u << log_n) - 1;
+    const uint32_t k = 2u * (__brev(j) >> (32 - log_n)) + 1u;
+    const uint32_t kg = (uint32_t)(((uint64_t)k * g) & two_n_mask);
+    return __brev((kg - 1u) >> 1) >> (32 - log_n);
+}
+
+struct ConvArgs {
+    int ns, nt;
+    uint8_t src[kMaxPrimes];
+    uint8_t dst[kMaxPrimes];
+};
+
+// in: [polys][ns][N] (stride in_stride rows between polys), coefficient form;
+// out row for target ti: out + (poly*out_stride + (ti < split ? ti : ti + skip)) * N
+template <int NS_MAX>
+__global__ __launch_bounds__(kThreads) void k_conv(const uint64_t *in, uint32_t in_stride, uint64_t *out,
+                                                    uint32_t out_stride, uint32_t split, uint32_t skip, ConvArgs a,
+                                                    const ulonglong2 *__restrict__ qhat_inv,
+                                                    const ulonglong2 *__restrict__ qhat_mod,
+                                                    const ModQ *__restrict__ mods, uint32_t log_n)
+{
+    const uint32_t n = 1u << log_n;
+    const uint32_t col = blockIdx.x * kThreads + threadIdx.x;
+    const uint32_t poly = blockIdx.y;
+    if (col >= n) return;
+    const uint64_t *src = in + ((size_t)poly * in_stride << log_n) + col;
+    uint64_t y[NS_MAX];
+#pragma unroll
+    for (int i = 0; i < NS_MAX; i++) {
+        if (i < a.ns) {
+            const uint64_t q = mods[a.src[i]].q;
+            const ulonglong2 w = qhat_inv[i];
+            y[i] = shoup(src[(size_t)i << log_n], w.x, w.y, q);
+        }
+    }
+    uint64_t *dst = out + ((size_t)poly * out_stride << log_n) + col;
+    for (int t = 0; t < a.nt; t++) {
+        const uint64_t qt = mods[a.dst[t]].q, two = 2 * qt;
+        uint64_t acc = 0;
+#pragma unroll
+        for (int i = 0; i < NS_MAX; i++) {
+            if (i < a.ns) {
+                const ulonglong2 w = qhat_mod[i * a.nt + t];
+                acc = csub(acc + shoup_lazy(y[i], w.x, w.y, qt), two);
+            }
+        }
+        const uint32_t row = t < (int)split ? t : t + skip;
+        dst[(size_t)row << log_n] = csub(acc, qt);
+    }
+}
+
+// u[k][r][n] = sum_{j<nd} d_j[r][sigma(n)] * key[j][k][krow(r)][n], rows r over Q_level u P
+__global__ __launch_bounds__(kThreads) void k_key_ip(const uint64_t *__restrict__ digits,
+                                                      const uint64_t *__restrict__ key, uint64_t *u, uint32_t nd,
+                                                      uint32_t ext, uint32_t level, uint32_t n_q, uint32_t key_rows,
+                                                      uint32_t g, const ModQ *__restrict__ mods, uint32_t log_n)
+{
+    const uint32_t n = 1u << log_n;
+    const uint32_t col = blockIdx.x * kThreads + threadIdx.x;
+    const uint32_t r = blockIdx.y;
+    if (col >= n) return;
+    const uint32_t prime = r <= level ? r : n_q + (r - level - 1);
+    const ModQ m = mods[prime];
+    const uint32_t sc = g == 1 ? col : auto_index(col, g, log_n);
+    acc128 a0{0, 0}, a1{0, 0};
+    for (uint32_t j = 0; j < nd; j++) {
+        const uint64_t d = digits[(((size_t)j * ext + r) << log_n) + sc];
+        const size_t kb = ((size_t)j * 2 * key_rows + prime) << log_n;
+        mac(a0, d, key[kb + col]);
+        mac(a1, d, key[kb + ((size_t)key_rows << log_n) + col]);
+    }
+    u[((size_t)r << log_n) + col] = reduce128(a0, m);
+    u[(((size_t)ext + r) << log_n) + col] = reduce128(a1, m);
+}
+
+// out[k][i][n] = (u[k][i][n] - c[k][i][n]) * P^-1 + add_k[i][sigma_k(n)], i <= level
+__global__ __launch_bounds__(kThreads) void k_moddown_finish(uint64_t *out, const uint64_t *u, const uint64_t *c,
+                                                              const uint64_t *add0, uint32_t add0_g,
+                                                              const uint64_t *add1, uint32_t ext, uint32_t level,
+                                                              const ulonglong2 *__restrict__ pinv,
+                                                              const ModQ *__restrict__ mods, uint32_t log_n)
+{
+    const uint32_t n = 1u << log_n;
+    const uint32_t col = blockIdx.x * kThreads + threadIdx.x;
+    const uint32_t i = blockIdx.y, k = blockIdx.z;
+    if (col >= n) return;
+    const uint32_t L = level + 1;
+    const uint64_t q = mods[i].q;
+    const uint64_t x = u[(((size_t)k * ext + i) << log_n) + col];
+    const uint64_t cv = c[(((size_t)k * L + i) << log_n) + col];
+    const ulonglong2 w = pinv[i];
+    uint64_t r = shoup(submod(x, cv, q), w.x, w.y, q);
+    const uint64_t *add = k == 0 ? add0 : add1;
+    if (add) {
+        const uint32_t sc = (k == 0 && add0_g != 1) ? auto_index(col, add0_g, log_n) : col;
+        r = addmod(r, add[((size_t)i << log_n) + sc], q);
+    }
+    out[(((size_t)k * L + i) << log_n) + col] = r;
+}
+
+ckks_status launch_conv(ckks_ctx *ctx, const ConvDev *cd, const uint64_t *in, uint32_t in_stride, uint64_t *out,
+                        uint32_t out_stride, uint32_t split, uint32_t skip, uint32_t polys)
+{
+    ConvArgs a;
+    a.ns = cd->ns;
+    a.nt = cd->nt;
+    for (int i = 0; i < cd->ns; i++) a.src[i] = cd->src[i];
+    for (int t = 0; t < cd->nt; t++) a.dst[t] = cd->dst[t];
+    const dim3 grid((ctx->n + kThreads - 1) / kThreads, polys), block(kThreads);
+    prof_begin(ctx, K_CONV);
+    if (a.ns <= 4)
+        hipLaunchKernelGGL(k_conv<4>, grid, block, 0, ctx->stream, in, in_stride, out, out_stride, split, skip, a,
+                           cd->d_qhat_inv, cd->d_qhat_mod, ctx->d_mod, ctx->log_n);
+    else if (a.ns <= 8)
+        hipLaunchKernelGGL(k_conv<8>, grid, block, 0, ctx->stream, in, in_stride, out, out_stride, split, skip, a,
+                           cd->d_qhat_inv, cd->d_qhat_mod, ctx->d_mod, ctx->log_n);
+    else if (a.ns <= 16)
+        hipLaunchKernelGGL(k_conv<16>, grid, block, 0, ctx->stream, in, in_stride, out, out_stride, split, skip, a,
+                           cd->d_qhat_inv, cd->d_qhat_mod, ctx->d_mod, ctx->log_n);
+    else
+        hipLaunchKernelGGL(k_conv<kMaxPrimes>, grid, block, 0, ctx->stream, in, in_stride, out, out_stride, split,
+                           skip, a, cd->d_qhat_inv, cd->d_qhat_mod, ctx->d_mod, ctx->log_n);
+    prof_end(ctx, K_CONV);
+    HIP_TRY(hipGetLastError());
+    return CKKS_OK;
+}
+
+}  // namespace
+
+size_t ks_scratch_words(const ckks_ctx *ctx, uint32_t level)
+{
+    const size_t ext = level + 1 + ctx->n_p;
+    const size_t nd = n_digits(ctx, level);
+    // digits + u[2][ext] + conv out [2][level+1] + INTT staging [alpha]
+    return ((nd * ext) + 2 * ext + 2 * (level + 1) + ctx->alpha) << ctx->log_n;
+}
+
+ckks_status ks_modup(ckks_ctx *ctx, const uint64_t *c, uint32_t level, uint64_t *digits)
+{
+    const uint32_t K = ctx->n_p, ext = level + 1 + K, nd = n_digits(ctx, level);
+    const size_t N = ctx->n;
+    for (uint32_t j = 0; j < nd; j++) {
+        const uint32_t lo = digit_lo(ctx, j), hi = digit_hi(ctx, j, level), ns = hi - lo;
+        uint64_t *dj = digits + (size_t)j * ext * N;
+        // the digit's own limbs keep their NTT-domain values
+        HIP_TRY(hipMemcpyAsync(dj + lo * N, c + lo * N, ns * N * sizeof(uint64_t), hipMemcpyDeviceToDevice,
+                               ctx->stream));
+        // coefficient form of the digit's limbs, staged in the alpha rows after the digits
+        uint64_t *coef = digits + (size_t)nd * ext * N;
+        HIP_TRY(hipMemcpyAsync(coef, c + lo * N, ns * N * sizeof(uint64_t), hipMemcpyDeviceToDevice, ctx->stream));
+        CK_TRY(launch_ntt(ctx, coef, ns, limb_range(lo, ns), true));
+        const ConvDev *cd;
+        CK_TRY(ctx_conv(ctx, (int)level, (int)j, &cd));
+        CK_TRY(launch_conv(ctx, cd, coef, 0, dj, 0, lo, ns, 1));
+        // NTT of the converted rows: [0, lo) and [hi, ext)
+        if (lo) CK_TRY(launch_ntt(ctx, dj, lo, limb_range(0, lo), false));
+        LimbMap m{};
+        m.n = ext - hi;
+        for (uint32_t r = hi; r < ext; r++) m.prime[r - hi] = (uint8_t)(r <= level ? r : ctx->n_q + (r - level - 1));
+        CK_TRY(launch_ntt(ctx, dj + (size_t)hi * N, m.n, m, false));
+    }
+    return CKKS_OK;
+}
+
+ckks_status ks_inner_product(ckks_ctx *ctx, const uint64_t *digits, uint32_t nd, const uint64_t *key,
+                             uint32_t level, uint32_t g, uint64_t *u)
+{
+    const uint32_t ext = level + 1 + ctx->n_p;
+    const dim3 grid((ctx->n + kThreads - 1) / kThreads, ext), block(kThreads);
+    prof_begin(ctx, K_KEYIP);
+    hipLaunchKernelGGL(k_key_ip, grid, block, 0, ctx->stream, digits, key, u, nd, ext, level, ctx->n_q,
+                       ctx->n_primes(), g, ctx->d_mod, ctx->log_n);
+    prof_end(ctx, K_KEYIP);
+    HIP_TRY(hipGetLastError());
+    return CKKS_OK;
+}
+
+ckks_status ks_moddown(ckks_ctx *ctx, uint64_t *u, uint32_t polys, uint32_t level, const uint64_t *add0,
+                       uint32_t add0_g, const uint64_t *add1, uint64_t *out, uint64_t *work)
+{
+    const uint32_t K = ctx->n_p, ext = level + 1 + K, L = level + 1;
+    const size_t N = ctx->n;
+    // INTT of the P rows of every polynomial, in place
+    LimbMap pm = limb_range(ctx->n_q, K);
+    CK_TRY(launch_ntt_strided(ctx, u + (size_t)L * N, polys, ext, pm, true));
+    const ConvDev *cd;
+    CK_TRY(ctx_conv(ctx, (int)level, -1, &cd));
+    CK_TRY(launch_conv(ctx, cd, u + (size_t)L * N, ext, work, L, L, 0, polys));
+    CK_TRY(launch_ntt(ctx, work, polys * L, limb_range(0, L), false));
+    const dim3 grid((ctx->n + kThreads - 1) / kThreads, L, polys), block(kThreads);
+    hipLaunchKernelGGL(k_moddown_finish, grid, block, 0, ctx->stream, out, u, work, add0, add0_g, add1, ext, level,
+                       ctx->d_pinv, ctx->d_mod, ctx->log_n);
+    HIP_TRY(hipGetLastError());
+    return CKKS_OK;
+}

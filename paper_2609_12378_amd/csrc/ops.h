@@ -1,0 +1,61 @@
+// Launchers of the element-wise, structural, key-switching, encoding and
+// projection kernels (definitions in ops.hip, keyswitch.hip, encode.hip,
+// project.hip).
+#pragma once
+#include "ckks_internal.h"
+
+enum { EW_ADD = 0, EW_SUB = 1, EW_MUL = 2 };
+
+ckks_status launch_binary(ckks_ctx *ctx, uint64_t *out, const uint64_t *a, const uint64_t *b, uint32_t rows,
+                          const LimbMap &map, int op);
+ckks_status launch_mul_plain(ckks_ctx *ctx, uint64_t *out, const uint64_t *ct, const uint64_t *pt, uint32_t polys,
+                             uint32_t limbs);
+ckks_status launch_tensor(ckks_ctx *ctx, uint64_t *d0, uint64_t *d1, uint64_t *d2, const uint64_t *a,
+                          const uint64_t *b, uint32_t limbs);
+ckks_status launch_expand_i8(ckks_ctx *ctx, uint64_t *out, const int8_t *v, const LimbMap &map);
+ckks_status launch_expand_i32(ckks_ctx *ctx, uint64_t *out, const int32_t *v, const LimbMap &map);
+ckks_status launch_encrypt(ckks_ctx *ctx, uint64_t *c0, uint64_t *c1, const uint64_t *a, const uint64_t *s,
+                           const uint64_t *e, const uint64_t *m, const LimbMap &map);
+ckks_status launch_keygen_digit(ckks_ctx *ctx, uint64_t *b_out, uint64_t *a_out, const uint64_t *a,
+                                const uint64_t *s, const uint64_t *e, const uint64_t *t, uint32_t dig_lo,
+                                uint32_t dig_hi);
+ckks_status launch_rescale_spread(ckks_ctx *ctx, uint64_t *out, const uint64_t *top, uint32_t polys, uint32_t l);
+ckks_status launch_rescale_finish(ckks_ctx *ctx, uint64_t *out, const uint64_t *c, const uint64_t *r,
+                                  uint32_t polys, uint32_t l);
+
+// key switching (keyswitch.hip)
+// digits: [nd][level+1+K][N] from c ([level+1][N]); the buffer must hold alpha more rows
+// after the digits (staging for the INTT of a digit's limbs)
+ckks_status ks_modup(ckks_ctx *ctx, const uint64_t *c, uint32_t level, uint64_t *digits);
+// (u0, u1) = sum_j sigma_g(d_j) (b_j, a_j); g = 1 for no automorphism; u: [2][level+1+K][N]
+ckks_status ks_inner_product(ckks_ctx *ctx, const uint64_t *digits, uint32_t nd, const uint64_t *key,
+                             uint32_t level, uint32_t g, uint64_t *u);
+// out_k = (u_k - Conv(INTT([u_k]_P))) P^-1 (+ add_k), k < polys; u ([polys][level+1+K][N]) is clobbered.
+// add0/add1: [level+1][N] or null, add0 read through the automorphism add0_g (1 = none);
+// out: [polys][level+1][N]; work: [polys][level+1][N]
+ckks_status ks_moddown(ckks_ctx *ctx, uint64_t *u, uint32_t polys, uint32_t level, const uint64_t *add0,
+                       uint32_t add0_g, const uint64_t *add1, uint64_t *out, uint64_t *work);
+// scratch words needed by ks_rotate_core for one rotation batch
+size_t ks_scratch_words(const ckks_ctx *ctx, uint32_t level);
+
+// encoding (encode.hip)
+struct SlotSource {
+    // explicit slots: re/im [batch][N/2] (im may be null)
+    const double *re = nullptr, *im = nullptr;
+    // or the projection's weight plaintexts, generated from W (d_in x d_out, row-major):
+    // plaintext p of the batch is (output block j0 + p / pairs, pair ib0 + p % pairs), where
+    // pair = i * bcount + b names input block i and baby step b of giant step g (n1g = n1 * g)
+    const double *W = nullptr;
+    uint32_t d_out = 0, tokens = 0, feats = 0;
+    uint32_t n1g = 0, bcount = 0;
+    uint32_t j0 = 0, ib0 = 0, pairs = 1;
+};
+// m_out: [batch][N] int64 rounded coefficients; work: [batch][N/2] double2
+ckks_status enc_coeffs(ckks_ctx *ctx, const SlotSource &src, uint32_t batch, double scale, double2 *work,
+                       int64_t *m_out);
+// residues of m ([batch][N]) into out ([batch][limbs][N]), primes 0..limbs-1
+ckks_status enc_to_rns(ckks_ctx *ctx, const int64_t *m, uint32_t batch, uint32_t limbs, uint64_t *out);
+size_t enc_work_bytes(const ckks_ctx *ctx, uint32_t batch);
+// decode: coef = coefficient form of limbs 0..min(limbs,2)-1 ([limbs][N]); writes N/2 slots
+ckks_status dec_slots(ckks_ctx *ctx, const uint64_t *coef, uint32_t limbs, double scale, double2 *work, double *re,
+                      double *im);

@@ -1,0 +1,273 @@
+// Element-wise and structural kernels on NTT-domain polynomials: add, subtract,
+// products, the ciphertext tensor product, the Galois automorphism, the secret
+// expansion used by encryption and key generation, and the rescale steps.
+//
+// These are streaming kernels bound by HBM: each thread handles one residue
+// per row, rows are mapped to primes through a LimbMap, and the row index is
+// recovered from a flat grid with one division per thread.
+#include "ckks_internal.h"
+#include "ops.h"
+
+namespace {
+
+constexpr int kThreads = 256;
+
+__device__ __forceinline__ bool flat(uint32_t log_n, size_t total, size_t &i, uint32_t &row, uint32_t &col)
+{
+    i = (size_t)blockIdx.x * kThreads + threadIdx.x;
+    if (i >= total) return false;
+    row = (uint32_t)(i >> log_n);
+    col = (uint32_t)(i & ((1u << log_n) - 1));
+    return true;
+}
+
+inline dim3 grid_for(size_t total) { return dim3((unsigned)((total + kThreads - 1) / kThreads)); }
+
+__global__ __launch_bounds__(kThreads) void k_binary(uint64_t *out, const uint64_t *a, const uint64_t *b,
+                                                      size_t total, uint32_t log_n, LimbMap map, const ModQ *mods,
+                                                      int op)
+{
+    size_t i;
+    uint32_t row, col;
+    if (!flat(log_n, total, i, row, col)) return;
+    const ModQ m = mods[map.prime[row % map.n]];
+    const uint64_t x = a[i], y = b[i];
+    uint64_t r;
+    if (op == EW_ADD) r = addmod(x, y, m.q);
+    else if (op == EW_SUB) r = submod(x, y, m.q);
+    else r = mulmod(x, y, m);
+    out[i] = r;
+}
+
+// out[p][l][n] = ct[p][l][n] * pt[l][n]
+__global__ __launch_bounds__(kThreads) void k_mul_plain(uint64_t *out, const uint64_t *ct, const uint64_t *pt,
+                                                         size_t total, uint32_t log_n, uint32_t limbs,
+                                                         const ModQ *mods)
+{
+    size_t i;
+    uint32_t row, col;
+    if (!flat(log_n, total, i, row, col)) return;
+    const uint32_t l = row % limbs;
+    out[i] = mulmod(ct[i], pt[((size_t)l << log_n) + col], mods[l]);
+}
+
+// d0 = a0 b0, d1 = a0 b1 + a1 b0, d2 = a1 b1 over `limbs` q-limbs
+__global__ __launch_bounds__(kThreads) void k_tensor(uint64_t *d0, uint64_t *d1, uint64_t *d2, const uint64_t *a,
+                                                      const uint64_t *b, size_t total, uint32_t log_n,
+                                                      const ModQ *mods)
+{
+    size_t i;
+    uint32_t row, col;
+    if (!flat(log_n, total, i, row, col)) return;
+    const ModQ m = mods[row];
+    const uint64_t a0 = a[i], a1 = a[i + total], b0 = b[i], b1 = b[i + total];
+    d0[i] = mulmod(a0, b0, m);
+    acc128 x{0, 0};
+    mac(x, a0, b1);
+    mac(x, a1, b0);
+    d1[i] = reduce128(x, m);
+    d2[i] = mulmod(a1, b1, m);
+}
+
+__device__ __forceinline__ uint32_t auto_index(uint32_t j, uint32_t g, uint32_t log_n)
+{
+    // NTT index j holds a(psi^(2 brev(j) + 1)); sigma_g(a) there is a(psi^((2 brev(j)+1) g))
+    const uint32_t two_n_mask = (2u << log_n) - 1;
+    const uint32_t k = 2u * (__brev(j) >> (32 - log_n)) + 1u;
+    const uint32_t kg = (uint32_t)(((uint64_t)k * g) & two_n_mask);
+    return __brev((kg - 1u) >> 1) >> (32 - log_n);
+}
+
+__global__ __launch_bounds__(kThreads) void k_automorph(uint64_t *out, const uint64_t *in, size_t total,
+                                                         uint32_t log_n, uint32_t g)
+{
+    size_t i;
+    uint32_t row, col;
+    if (!flat(log_n, total, i, row, col)) return;
+    out[i] = in[((size_t)row << log_n) + auto_index(col, g, log_n)];
+}
+
+// small signed integers (int8 or int32 coefficients) into residues [limbs][N]
+template <typename T>
+__global__ __launch_bounds__(kThreads) void k_expand(uint64_t *out, const T *v, size_t total, uint32_t log_n,
+                                                      LimbMap map, const ModQ *mods)
+{
+    size_t i;
+    uint32_t row, col;
+    if (!flat(log_n, total, i, row, col)) return;
+    const uint64_t q = mods[map.prime[row % map.n]].q;
+    const int64_t x = (int64_t)v[col];
+    out[i] = x >= 0 ? (uint64_t)x : q - (uint64_t)(-x);
+}
+
+// c0 = -a*s + e + m ; rows over limbs (map), batch 1
+__global__ __launch_bounds__(kThreads) void k_encrypt(uint64_t *c0, uint64_t *c1, const uint64_t *a,
+                                                       const uint64_t *s, const uint64_t *e, const uint64_t *m,
+                                                       size_t total, uint32_t log_n, LimbMap map, const ModQ *mods)
+{
+    size_t i;
+    uint32_t row, col;
+    if (!flat(log_n, total, i, row, col)) return;
+    const ModQ md = mods[map.prime[row % map.n]];
+    const uint64_t as = mulmod(a[i], s[i], md);
+    uint64_t r = submod(e[i], as, md.q);
+    if (m) r = addmod(r, m[i], md.q);
+    c0[i] = r;
+    if (c1) c1[i] = a[i];
+}
+
+// b = -a*s + e (+ [P] t on the digit's q-limbs); rows = all primes of the context
+__global__ __launch_bounds__(kThreads) void k_keygen(uint64_t *b_out, uint64_t *a_out, const uint64_t *a,
+                                                      const uint64_t *s, const uint64_t *e, const uint64_t *t,
+                                                      const ulonglong2 *pmodq, uint32_t dig_lo, uint32_t dig_hi,
+                                                      size_t total, uint32_t log_n, const ModQ *mods)
+{
+    size_t i;
+    uint32_t row, col;
+    if (!flat(log_n, total, i, row, col)) return;
+    const ModQ md = mods[row];
+    uint64_t r = submod(e[i], mulmod(a[i], s[i], md), md.q);
+    if (row >= dig_lo && row < dig_hi) {
+        const ulonglong2 P = pmodq[row];
+        r = addmod(r, shoup(t[i], P.x, P.y, md.q), md.q);
+    }
+    b_out[i] = r;
+    a_out[i] = a[i];
+}
+
+// Rescale, step 1: top-limb coefficients t (mod q_l) -> centred -> residues mod q_i, i < l.
+// top: [polys][N] coefficients; out: [polys][l][N]
+__global__ __launch_bounds__(kThreads) void k_rescale_spread(uint64_t *out, const uint64_t *top, size_t total,
+                                                              uint32_t log_n, uint32_t l, const ModQ *mods)
+{
+    size_t i;
+    uint32_t row, col;
+    if (!flat(log_n, total, i, row, col)) return;
+    const uint32_t poly = row / l, li = row % l;
+    const uint64_t ql = mods[l].q;
+    const ModQ mi = mods[li];
+    const uint64_t t = top[((size_t)poly << log_n) + col];
+    const bool neg = t > (ql >> 1);
+    const uint64_t mag = neg ? ql - t : t;  // |centred value| < q_l / 2
+    uint64_t r = csub(mag - mulhi64(mag, mi.one_s) * mi.q, mi.q);
+    if (neg && r) r = mi.q - r;
+    out[i] = r;
+}
+
+// Rescale, step 2: out_i = (c_i - r_i) * q_l^-1 mod q_i; c: [polys][l+1][N], r/out: [polys][l][N]
+__global__ __launch_bounds__(kThreads) void k_rescale_finish(uint64_t *out, const uint64_t *c, const uint64_t *r,
+                                                              size_t total, uint32_t log_n, uint32_t l,
+                                                              const ulonglong2 *qlinv_row, const ModQ *mods)
+{
+    size_t i;
+    uint32_t row, col;
+    if (!flat(log_n, total, i, row, col)) return;
+    const uint32_t poly = row / l, li = row % l;
+    const uint64_t q = mods[li].q;
+    const uint64_t ci = c[(((size_t)poly * (l + 1) + li) << log_n) + col];
+    const ulonglong2 w = qlinv_row[li];
+    out[i] = shoup(submod(ci, r[i], q), w.x, w.y, q);
+}
+
+}  // namespace
+
+ckks_status launch_binary(ckks_ctx *ctx, uint64_t *out, const uint64_t *a, const uint64_t *b, uint32_t rows,
+                          const LimbMap &map, int op)
+{
+    const size_t total = (size_t)rows << ctx->log_n;
+    if (!total) return CKKS_OK;
+    prof_begin(ctx, K_ELEM);
+    hipLaunchKernelGGL(k_binary, grid_for(total), dim3(kThreads), 0, ctx->stream, out, a, b, total, ctx->log_n, map,
+                       ctx->d_mod, op);
+    prof_end(ctx, K_ELEM);
+    HIP_TRY(hipGetLastError());
+    return CKKS_OK;
+}
+
+ckks_status launch_mul_plain(ckks_ctx *ctx, uint64_t *out, const uint64_t *ct, const uint64_t *pt, uint32_t polys,
+                             uint32_t limbs)
+{
+    const size_t total = ((size_t)polys * limbs) << ctx->log_n;
+    if (!total) return CKKS_OK;
+    hipLaunchKernelGGL(k_mul_plain, grid_for(total), dim3(kThreads), 0, ctx->stream, out, ct, pt, total, ctx->log_n,
+                       limbs, ctx->d_mod);
+    HIP_TRY(hipGetLastError());
+    return CKKS_OK;
+}
+
+ckks_status launch_tensor(ckks_ctx *ctx, uint64_t *d0, uint64_t *d1, uint64_t *d2, const uint64_t *a,
+                          const uint64_t *b, uint32_t limbs)
+{
+    const size_t total = (size_t)limbs << ctx->log_n;
+    hipLaunchKernelGGL(k_tensor, grid_for(total), dim3(kThreads), 0, ctx->stream, d0, d1, d2, a, b, total,
+                       ctx->log_n, ctx->d_mod);
+    HIP_TRY(hipGetLastError());
+    return CKKS_OK;
+}
+
+ckks_status launch_automorph(ckks_ctx *ctx, const uint64_t *in, uint64_t *out, uint32_t rows, uint32_t g)
+{
+    const size_t total = (size_t)rows << ctx->log_n;
+    if (!total) return CKKS_OK;
+    hipLaunchKernelGGL(k_automorph, grid_for(total), dim3(kThreads), 0, ctx->stream, out, in, total, ctx->log_n, g);
+    HIP_TRY(hipGetLastError());
+    return CKKS_OK;
+}
+
+ckks_status launch_expand_i8(ckks_ctx *ctx, uint64_t *out, const int8_t *v, const LimbMap &map)
+{
+    const size_t total = (size_t)map.n << ctx->log_n;
+    hipLaunchKernelGGL(k_expand<int8_t>, grid_for(total), dim3(kThreads), 0, ctx->stream, out, v, total, ctx->log_n,
+                       map, ctx->d_mod);
+    HIP_TRY(hipGetLastError());
+    return CKKS_OK;
+}
+
+ckks_status launch_expand_i32(ckks_ctx *ctx, uint64_t *out, const int32_t *v, const LimbMap &map)
+{
+    const size_t total = (size_t)map.n << ctx->log_n;
+    hipLaunchKernelGGL(k_expand<int32_t>, grid_for(total), dim3(kThreads), 0, ctx->stream, out, v, total,
+                       ctx->log_n, map, ctx->d_mod);
+    HIP_TRY(hipGetLastError());
+    return CKKS_OK;
+}
+
+ckks_status launch_encrypt(ckks_ctx *ctx, uint64_t *c0, uint64_t *c1, const uint64_t *a, const uint64_t *s,
+                           const uint64_t *e, const uint64_t *m, const LimbMap &map)
+{
+    const size_t total = (size_t)map.n << ctx->log_n;
+    hipLaunchKernelGGL(k_encrypt, grid_for(total), dim3(kThreads), 0, ctx->stream, c0, c1, a, s, e, m, total,
+                       ctx->log_n, map, ctx->d_mod);
+    HIP_TRY(hipGetLastError());
+    return CKKS_OK;
+}
+
+ckks_status launch_keygen_digit(ckks_ctx *ctx, uint64_t *b_out, uint64_t *a_out, const uint64_t *a,
+                                const uint64_t *s, const uint64_t *e, const uint64_t *t, uint32_t dig_lo,
+                                uint32_t dig_hi)
+{
+    const size_t total = (size_t)ctx->n_primes() << ctx->log_n;
+    hipLaunchKernelGGL(k_keygen, grid_for(total), dim3(kThreads), 0, ctx->stream, b_out, a_out, a, s, e, t,
+                       ctx->d_pmodq, dig_lo, dig_hi, total, ctx->log_n, ctx->d_mod);
+    HIP_TRY(hipGetLastError());
+    return CKKS_OK;
+}
+
+ckks_status launch_rescale_spread(ckks_ctx *ctx, uint64_t *out, const uint64_t *top, uint32_t polys, uint32_t l)
+{
+    const size_t total = ((size_t)polys * l) << ctx->log_n;
+    hipLaunchKernelGGL(k_rescale_spread, grid_for(total), dim3(kThreads), 0, ctx->stream, out, top, total,
+                       ctx->log_n, l, ctx->d_mod);
+    HIP_TRY(hipGetLastError());
+    return CKKS_OK;
+}
+
+ckks_status launch_rescale_finish(ckks_ctx *ctx, uint64_t *out, const uint64_t *c, const uint64_t *r,
+                                  uint32_t polys, uint32_t l)
+{
+    const size_t total = ((size_t)polys * l) << ctx->log_n;
+    hipLaunchKernelGGL(k_rescale_finish, grid_for(total), dim3(kThreads), 0, ctx->stream, out, c, r, total,
+                       ctx->log_n, l, ctx->d_qlinv + (size_t)l * ctx->n_q, ctx->d_mod);
+    HIP_TRY(hipGetLastError());
+    return CKKS_OK;
+}

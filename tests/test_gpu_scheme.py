@@ -1,0 +1,202 @@
+"""GPU parity of encoding, encryption, key generation, the homomorphic operations and
+each key-switching stage, bit for bit against the oracle on the same seeded inputs.
+
+Two parameter sets: the toy ring (N = 2^12, 4 + 2 limbs of 36-bit primes, dnum 2)
+and the key-switching / projection chain at full degree (N = 2^16, 24 + 8 limbs of
+50-bit primes, dnum 3) at level 12 (partial second digit) and level 23.
+"""
+import numpy as np
+import pytest
+
+from gpu_common import require_gpu, say, to_dev, to_host
+from oracle import Ckks
+from workloads import (KEYSWITCH, TOY, gaussian_error, rng, ternary_secret, uniform_residues,
+                       uniform_slots)
+
+pytestmark = pytest.mark.gpu
+
+
+class Env:
+    def __init__(self, cfg, seed):
+        require_gpu()
+        from paper_2609_12378_amd import Buf, Context
+        self.Buf = Buf
+        self.cfg = cfg
+        self.ctx = Context(cfg.log_n, cfg.n_q, cfg.n_p, cfg.dnum, q_bits=cfg.q_bits)
+        self.ck = Ckks(cfg.log_n, self.ctx.q, self.ctx.p, cfg.dnum)
+        self.n = self.ctx.n
+        self.s = ternary_secret(rng(cfg.index, 3, extra=seed), self.n)
+        self.s_dev = to_dev(self.s)
+        self.seed = seed
+
+    def slots(self, seed, cplx=True):
+        g = rng(self.cfg.index, 1, extra=self.seed * 100 + seed)
+        re = uniform_slots(g, self.n // 2)
+        im = uniform_slots(g, self.n // 2) if cplx else None
+        return re, im
+
+    def encrypt_both(self, seed, limbs, scale):
+        re, im = self.slots(seed)
+        pt_o = self.ck.encode(re, im, scale, limbs)
+        g = rng(self.cfg.index, 4, extra=self.seed * 100 + seed)
+        a = uniform_residues(g, self.ctx.q[:limbs], self.n)
+        e = gaussian_error(g, self.n)
+        ct_o = self.ck.encrypt(self.s, pt_o, a, e)
+        pt_g = self.ctx.encode(to_dev(re), to_dev(im), scale, limbs)
+        ct_g = self.ctx.encrypt(self.s_dev, pt_g, to_dev(a), to_dev(e))
+        return ct_o, ct_g, (re, im)
+
+    def key_randomness(self, seed):
+        g = rng(self.cfg.index, 5, extra=self.seed * 100 + seed)
+        a = uniform_residues(g, self.ctx.primes, self.n, lead=(self.cfg.dnum,))
+        e = gaussian_error(g, (self.cfg.dnum, self.n))
+        return a, e
+
+    def galois_keys(self, seed, steps):
+        a, e = self.key_randomness(seed)
+        g = self.ck.galois_elt(steps)
+        assert self.ctx.galois_elt(steps) == g
+        return self.ck.keygen_galois(self.s, g, a, e), self.ctx.keygen_galois(self.s_dev, g, to_dev(a), to_dev(e))
+
+
+@pytest.fixture(scope="module")
+def toy():
+    return Env(TOY, 1)
+
+
+@pytest.fixture(scope="module")
+def big():
+    return Env(KEYSWITCH, 2)
+
+
+def eq(dev, host):
+    got = to_host(dev)
+    assert got.shape == host.shape, (got.shape, host.shape)
+    bad = np.argwhere(got != host)
+    assert bad.size == 0, "first mismatches at %s" % bad[:5].tolist()
+
+
+@pytest.mark.parametrize("scale_log2,cplx", [(30, True), (30, False), (35, True)])
+def test_encode_toy(toy, scale_log2, cplx):
+    re, im = toy.slots(10 + scale_log2, cplx)
+    scale = float(2 ** scale_log2)
+    pt = toy.ctx.encode(to_dev(re), to_dev(im) if cplx else None, scale, 4)
+    eq(pt.data[0], toy.ck.encode(re, im, scale, 4))
+
+
+def test_encode_full_degree_at_projection_scale(big):
+    # the projection encodes weights at scale q_12 (about 2^50): many coefficients lie within
+    # the fp64 error of a rounding tie, so this checks that the evaluation order matches
+    g = rng(4, 2, extra=7)
+    re = g.normal(0, 0.02, big.n // 2)
+    scale = float(big.ctx.q[12])
+    pt = big.ctx.encode(to_dev(re), None, scale, 13)
+    eq(pt.data[0], big.ck.encode(re, None, scale, 13))
+
+
+def test_decode(toy, big):
+    for env, limbs, scale in ((toy, 4, 2.0 ** 30), (toy, 1, 2.0 ** 30), (big, 13, 2.0 ** 40)):
+        re, im = env.slots(20)
+        pt = env.ctx.encode(to_dev(re), to_dev(im), scale, limbs)
+        dre, dim = env.ctx.decode(pt)
+        z = to_host(dre) + 1j * to_host(dim)
+        assert np.max(np.abs(z - (re + 1j * im))) <= env.n / (2 * scale) + 1e-9
+
+
+def test_encrypt_decrypt(toy):
+    ct_o, ct_g, (re, im) = toy.encrypt_both(1, 4, 2.0 ** 30)
+    eq(ct_g.data, ct_o)
+    pt_g = toy.ctx.decrypt(toy.s_dev, ct_g)
+    eq(pt_g.data[0], toy.ck.decrypt(toy.s, ct_o))
+
+
+def test_keygen(toy, big):
+    for env in (toy, big):
+        ko, kg = env.galois_keys(3, 5)
+        eq(kg, ko)
+    a, e = toy.key_randomness(4)
+    eq(toy.ctx.keygen_relin(toy.s_dev, to_dev(a), to_dev(e)), toy.ck.keygen_relin(toy.s, a, e))
+
+
+def test_add_mul_plain_rescale(toy):
+    c1o, c1g, _ = toy.encrypt_both(5, 4, 2.0 ** 30)
+    c2o, c2g, _ = toy.encrypt_both(6, 4, 2.0 ** 30)
+    eq(toy.ctx.add(c1g, c2g).data, toy.ck.ct_add(c1o, c2o))
+    re, im = toy.slots(7)
+    pto = toy.ck.encode(re, im, float(toy.ctx.q[3]), 4)
+    ptg = toy.ctx.encode(to_dev(re), to_dev(im), float(toy.ctx.q[3]), 4)
+    prod_g = toy.ctx.mul_plain(c1g, ptg)
+    prod_o = toy.ck.ct_mul_plain(c1o, pto)
+    eq(prod_g.data, prod_o)
+    eq(toy.ctx.rescale(prod_g).data, toy.ck.rescale(prod_o))
+
+
+def test_add_rejects_mismatched_scales(toy):
+    from paper_2609_12378_amd import CkksError
+    _, c1g, _ = toy.encrypt_both(8, 4, 2.0 ** 30)
+    _, c2g, _ = toy.encrypt_both(9, 4, 2.0 ** 31)
+    with pytest.raises(CkksError, match="scale"):
+        toy.ctx.add(c1g, c2g)
+
+
+@pytest.mark.parametrize("level", [3, 2, 0])
+def test_modup_moddown_automorph_toy(toy, level):
+    c = uniform_residues(rng(1, 6, extra=level), toy.ctx.q[:level + 1], toy.n)
+    eq(toy.ctx.modup(to_dev(c), level), toy.ck.modup(c, level))
+    ext = toy.ck.ext_primes(level)
+    x = uniform_residues(rng(1, 7, extra=level), [toy.ck.primes[k] for k in ext], toy.n)
+    eq(toy.ctx.moddown(to_dev(x), level), toy.ck.moddown(x, level))
+    for g in (5, 25, 2 * toy.n - 1):
+        eq(toy.ctx.automorph(to_dev(c), g), toy.ck.automorph(c, g))
+
+
+@pytest.mark.parametrize("level", [12, 23])
+def test_modup_moddown_full_degree(big, level):
+    say("modup/moddown level", level)
+    c = uniform_residues(rng(3, 6, extra=level), big.ctx.q[:level + 1], big.n)
+    eq(big.ctx.modup(to_dev(c), level), big.ck.modup(c, level))
+    ext = big.ck.ext_primes(level)
+    x = uniform_residues(rng(3, 7, extra=level), [big.ck.primes[k] for k in ext], big.n)
+    eq(big.ctx.moddown(to_dev(x), level), big.ck.moddown(x, level))
+
+
+@pytest.mark.parametrize("steps", [1, 7, -2])
+def test_rotate_toy(toy, steps):
+    cto, ctg, _ = toy.encrypt_both(11, 4, 2.0 ** 30)
+    ko, kg = toy.galois_keys(20 + steps, steps)
+    eq(toy.ctx.rotate(ctg, steps, kg).data, toy.ck.rotate(cto, steps, ko))
+
+
+def test_rotate_hoisted_toy_lower_level(toy):
+    cto, ctg, _ = toy.encrypt_both(12, 3, 2.0 ** 30)   # level 2: partial second digit
+    steps = [1, 2, 16, 100]
+    keys = [toy.galois_keys(40 + s, s) for s in steps]
+    outs_g = toy.ctx.rotate_hoisted(ctg, steps, [k[1] for k in keys])
+    outs_o = toy.ck.rotate_hoisted(cto, steps, [k[0] for k in keys])
+    for og, oo in zip(outs_g, outs_o):
+        eq(og.data, oo)
+
+
+def test_rotate_full_degree(big):
+    say("rotate full degree")
+    cto, ctg, _ = big.encrypt_both(13, 13, 2.0 ** 40)
+    ko, kg = big.galois_keys(50, 3)
+    eq(big.ctx.rotate(ctg, 3, kg).data, big.ck.rotate(cto, 3, ko))
+
+
+def test_mul_relin(toy):
+    c1o, c1g, _ = toy.encrypt_both(14, 4, 2.0 ** 30)
+    c2o, c2g, _ = toy.encrypt_both(15, 4, 2.0 ** 30)
+    a, e = toy.key_randomness(60)
+    rlk_o = toy.ck.keygen_relin(toy.s, a, e)
+    rlk_g = toy.ctx.keygen_relin(toy.s_dev, to_dev(a), to_dev(e))
+    eq(toy.ctx.mul_relin(c1g, c2g, rlk_g).data, toy.ck.mul_relin(c1o, c2o, rlk_o))
+
+
+def test_decrypted_rotation_is_slot_shift(toy):
+    cto, ctg, (re, im) = toy.encrypt_both(16, 4, 2.0 ** 30)
+    _, kg = toy.galois_keys(70, 5)
+    out = toy.ctx.rotate(ctg, 5, kg)
+    dre, dim = toy.ctx.decode(toy.ctx.decrypt(toy.s_dev, out))
+    z = to_host(dre) + 1j * to_host(dim)
+    assert np.max(np.abs(z - np.roll(re + 1j * im, -5))) < 1e-2
