@@ -153,7 +153,7 @@ extern "C" ckks_status ckks_linear_project(ckks_ctx *ctx, const ckks_buf *in, co
     // ---- scratch layout
     const size_t N = ctx->n, ctw = 2 * (size_t)L * N;
     const uint32_t maxpairs = n_in * n1;
-    const uint32_t Pb = std::min<uint32_t>(maxpairs, std::max<uint32_t>(1, (uint32_t)((1u << 29) / (kJ * L * N * 8))));
+    const uint32_t Pb = std::min<uint32_t>(maxpairs, std::max<uint32_t>(1, (uint32_t)((size_t(1) << 31) / ((size_t)kJ * L * N * 8))));
     const size_t xrot_w = (size_t)n_in * n1 * ctw;
     const size_t acc_w = (size_t)kJ * ctw, tot_w = (size_t)kJ * ctw, rot_w = ctw;
     const size_t pt_w = (size_t)kJ * Pb * L * N;
