@@ -1,0 +1,327 @@
+#!/usr/bin/env python3
+"""Benchmark of the RNS-CKKS projection path on one MI355X.
+
+One step is one full Llama-3-8B-shaped ciphertext x plaintext projection
+(4096 -> 14336, 128 tokens x 256 features per ciphertext, N = 2^16, level 12,
+24 + 8 limbs of 50-bit primes, dnum 3, BSGS n1 = 32 / n2 = 8): 16 hoisted
+ModUps and 496 baby-step rotations, 229,376 weight plaintexts encoded on the
+fly from W (FFT, rounding, RNS, NTT) and multiply-accumulated, 392 giant-step
+rotations and 56 rescales.  Inputs (W, ciphertexts, keys) are resident in HBM
+before the timed region.  The same JSON line also carries the hoisted
+key-switching rate (32 rotations of a level-23 ciphertext) and the batched NTT
+microbenchmark (64 polynomials x 36 limbs).
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
+Prints exactly one JSON line on stdout; progress goes to stderr.
+"""
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "rotations/s at N=2^16 (keyswitch) and s per 4096x14336 ct-pt projection"
+HBM_PEAK_GBS = 8000.0
+# 256 CUs x 64 lanes x 2.4 GHz of 32-bit integer VALU issue
+INT_LANE_OPS = 256 * 64 * 2.4e9
+# one 64-bit Shoup product on gfx950: 10 32-bit multiplies (v_mad_u64_u32 / v_mul_lo_u32 /
+# v_mul_hi_u32) plus 6 adds/subtracts; a butterfly adds 8 more for the lazy add/sub/correct
+OPS_PER_BUTTERFLY = 24
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def fm_pack(X, T, D, i):
+    return X[:, i * D:(i + 1) * D].T.reshape(-1)
+
+
+class Timer:
+    def __init__(self, torch):
+        self.torch = torch
+
+    def __enter__(self):
+        self.torch.cuda.synchronize()
+        self.a = self.torch.cuda.Event(enable_timing=True)
+        self.b = self.torch.cuda.Event(enable_timing=True)
+        self.a.record()
+        return self
+
+    def __exit__(self, *exc):
+        self.b.record()
+        self.torch.cuda.synchronize()
+        self.ms = self.a.elapsed_time(self.b)
+
+
+def setup_projection(torch, np, cfg):
+    from paper_2609_12378_amd import Context
+    from workloads import (gaussian_error, gaussian_weights, rng, ternary_secret, uniform_residues,
+                           uniform_slots)
+    ctx = Context(cfg.log_n, cfg.n_q, cfg.n_p, cfg.dnum, q_bits=cfg.q_bits)
+    n, T, D, level, n1 = ctx.n, cfg.tokens, cfg.feats, cfg.level, cfg.n1
+    n2 = -(-D // n1)
+    s = torch.from_numpy(ternary_secret(rng(cfg.index, 3), n)).cuda()
+    X = uniform_slots(rng(cfg.index, 1), (T, cfg.d_in))
+    W = gaussian_weights(rng(cfg.index, 2), (cfg.d_in, cfg.d_out))
+    Wd = torch.from_numpy(W).cuda()
+    delta = float(2 ** cfg.scale_log2)
+    ge = rng(cfg.index, 4)
+    cts = []
+    for i in range(cfg.d_in // D):
+        pt = ctx.encode(torch.from_numpy(fm_pack(X, T, D, i)).cuda(), None, delta, level + 1)
+        a = torch.from_numpy(uniform_residues(ge, ctx.q[:level + 1], n)).cuda()
+        e = torch.from_numpy(gaussian_error(ge, n)).cuda()
+        cts.append(ctx.encrypt(s, pt, a, e))
+    steps = [T * b for b in range(1, n1)] + [T * n1 * g for g in range(1, n2)]
+    gk = rng(cfg.index, 5)
+    keys = {}
+    for st in steps:
+        a = torch.from_numpy(uniform_residues(gk, ctx.primes, n, lead=(cfg.dnum,))).cuda()
+        e = torch.from_numpy(gaussian_error(gk, (cfg.dnum, n))).cuda()
+        keys[st] = ctx.keygen_galois(s, ctx.galois_elt(st), a, e)
+    torch.cuda.synchronize()
+    return dict(ctx=ctx, s=s, X=X, W=W, Wd=Wd, cts=cts, keys=keys, T=T, D=D, n1=n1, delta=delta)
+
+
+def check_projection(np, st, outs, blocks=(0, 27, 55)):
+    """Decrypt sampled outputs and compare with X @ W (property check at full size)."""
+    ctx, T, D = st["ctx"], st["T"], st["D"]
+    errs = []
+    for j in blocks:
+        if j >= len(outs):
+            continue
+        re, _ = ctx.decode(ctx.decrypt(st["s"], outs[j]))
+        want = fm_pack(st["X"] @ st["W"][:, j * D:(j + 1) * D], T, D, 0)
+        errs.append(float(np.max(np.abs(re.cpu().numpy() - want))))
+    return max(errs) if errs else None
+
+
+def roofline(prof, ntt_rows_per_launch=None):
+    """Pick the kernel with the most total time; report its achieved rate against HBM and ALU peaks."""
+    name, (ms, cnt, by) = max(prof.items(), key=lambda kv: kv[1][0])
+    avg_ms = ms / cnt
+    gbs = by / (ms * 1e-3) / 1e9
+    out = {"kernel": name, "launches": cnt, "avg_ms": avg_ms, "bytes_per_launch": by / cnt}
+    if name.startswith("ntt_"):
+        # butterflies of one pass: half a residue per stage, log2(256) = 8 stages per pass at N = 2^16
+        residues = by / 16.0
+        bfly_per_s = residues * 4.0 / (ms * 1e-3)
+        alu_frac = bfly_per_s * OPS_PER_BUTTERFLY / INT_LANE_OPS
+        out["alu"] = {"butterflies_per_s": bfly_per_s, "ops_per_butterfly": OPS_PER_BUTTERFLY,
+                      "peak_lane_ops_per_s": INT_LANE_OPS, "frac": alu_frac}
+    out.update({"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": gbs / HBM_PEAK_GBS})
+    return out
+
+
+def load_traffic(kernel):
+    """HBM bytes per launch measured by rocprofv3 counters, if recorded for the current source."""
+    path = os.path.join(ROOT, "profiles", "pmc_traffic.md")
+    if not os.path.exists(path):
+        return None
+    srcs = sorted(os.listdir(os.path.join(ROOT, "paper_2609_12378_amd", "csrc")))
+    h = hashlib.sha256()
+    for f in srcs:
+        with open(os.path.join(ROOT, "paper_2609_12378_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    sha = h.hexdigest()[:16]
+    for line in open(path):
+        m = re.match(r"\|\s*(\S+)\s*\|\s*([0-9a-f]{16})\s*\|\s*([0-9.eE+]+)\s*\|", line)
+        if m and m.group(1) == kernel and m.group(2) == sha:
+            return float(m.group(3))
+    return None
+
+
+def bench_keyswitch(torch, np, steps, warmup):
+    from paper_2609_12378_amd import Context
+    from workloads import KEYSWITCH as cfg, gaussian_error, rng, ternary_secret, uniform_residues, uniform_slots
+    ctx = Context(cfg.log_n, cfg.n_q, cfg.n_p, cfg.dnum, q_bits=cfg.q_bits)
+    n, L = ctx.n, cfg.level + 1
+    s = torch.from_numpy(ternary_secret(rng(cfg.index, 3), n)).cuda()
+    z = uniform_slots(rng(cfg.index, 1), n // 2)
+    pt = ctx.encode(torch.from_numpy(z).cuda(), None, float(2 ** cfg.scale_log2), L)
+    ge = rng(cfg.index, 4)
+    ct = ctx.encrypt(s, pt, torch.from_numpy(uniform_residues(ge, ctx.q[:L], n)).cuda(),
+                     torch.from_numpy(gaussian_error(ge, n)).cuda())
+    rsteps = list(range(1, cfg.batch + 1))
+    gk = rng(cfg.index, 5)
+    keys = []
+    for r in rsteps:
+        a = torch.from_numpy(uniform_residues(gk, ctx.primes, n, lead=(cfg.dnum,))).cuda()
+        e = torch.from_numpy(gaussian_error(gk, (cfg.dnum, n))).cuda()
+        keys.append(ctx.keygen_galois(s, ctx.galois_elt(r), a, e))
+    outs = ctx.rotate_hoisted(ct, rsteps, keys)
+    for _ in range(warmup):
+        ctx.rotate_hoisted(ct, rsteps, keys, outs)
+    ctx.profile(True)
+    ctx.profile_reset()
+    with Timer(torch) as t:
+        for _ in range(steps):
+            ctx.rotate_hoisted(ct, rsteps, keys, outs)
+    prof = ctx.profile_all()
+    ctx.profile(False)
+    re, _ = ctx.decode(ctx.decrypt(s, outs[-1]))
+    err = float(np.max(np.abs(re.cpu().numpy() - np.roll(z, -rsteps[-1]))))
+    ms = t.ms / steps
+    res = {"workload": "32 hoisted rotations by 1..32 of one level-23 ciphertext, N=2^16, L=24+K=8, dnum=3",
+           "ms_per_batch": ms, "rotations_per_s": cfg.batch / (ms * 1e-3), "decrypt_err_last": err,
+           "kernels_ms": {k: v[0] / steps for k, v in prof.items()}}
+    del keys, outs, ct, ctx
+    return res
+
+
+def bench_ntt(torch, steps):
+    from paper_2609_12378_amd import Context
+    from workloads import NTT_BENCH as cfg
+    ctx = Context(cfg.log_n, cfg.n_q, 0, 1, q_bits=cfg.q_bits)
+    g = torch.Generator(device="cuda").manual_seed(202)
+    x = torch.randint(0, 1 << 49, (cfg.batch, cfg.n_q, ctx.n), generator=g, device="cuda",
+                      dtype=torch.int64).view(torch.uint64)
+    ctx.ntt(x)
+    ctx.intt(x)
+    ctx.profile(True)
+    ctx.profile_reset()
+    with Timer(torch) as tf:
+        for _ in range(steps):
+            ctx.ntt(x)
+    with Timer(torch) as ti:
+        for _ in range(steps):
+            ctx.intt(x)
+    prof = ctx.profile_all()
+    ctx.profile(False)
+    algo = 16.0 * cfg.batch * cfg.n_q * ctx.n
+    res = {"workload": "64 polys x 36 limbs x 2^16, 50-bit primes", "fwd_ms": tf.ms / steps, "inv_ms": ti.ms / steps,
+           "algorithmic_bytes_per_direction": algo,
+           "fwd_GBps": algo / (tf.ms / steps * 1e-3) / 1e9, "inv_GBps": algo / (ti.ms / steps * 1e-3) / 1e9,
+           "kernels": {k: {"avg_ms": v[0] / v[1], "GBps": v[2] / (v[0] * 1e-3) / 1e9} for k, v in prof.items()}}
+    del x, ctx
+    return res
+
+
+def cpu_baseline(np, cfg, budget_s=20.0):
+    """The oracle on a bounded sample of the projection, extrapolated to one full projection."""
+    from oracle import Ckks, gen_primes
+    from workloads import gaussian_error, gaussian_weights, rng, ternary_secret, uniform_residues, uniform_slots
+    pr = gen_primes(cfg.q_bits, 2 * cfg.n, cfg.n_q + cfg.n_p)
+    ck = Ckks(cfg.log_n, pr[:cfg.n_q], pr[cfg.n_q:], cfg.dnum)
+    n, T, D, level, n1 = ck.n, cfg.tokens, cfg.feats, cfg.level, cfg.n1
+    s = ternary_secret(rng(cfg.index, 3), n)
+    W = gaussian_weights(rng(cfg.index, 2), (D, D))
+    X = uniform_slots(rng(cfg.index, 1), (T, D))
+    ge = rng(cfg.index, 4)
+    ct = ck.encrypt(s, ck.encode(fm_pack(X, T, D, 0), None, 2.0 ** 40, level + 1),
+                    uniform_residues(ge, ck.q[:level + 1], n), gaussian_error(ge, n))
+    gk = rng(cfg.index, 5)
+    key = ck.keygen_galois(s, ck.galois_elt(T), uniform_residues(gk, ck.primes, n, lead=(cfg.dnum,)),
+                           gaussian_error(gk, (cfg.dnum, n)))
+    qd = float(ck.q[level])
+    t0 = time.time()
+    n_pts, acc = 0, None
+    while time.time() - t0 < budget_s * 0.6 or n_pts < 2:
+        z = Ckks.diag_slot_vector(W, T, D, 0, 0, n1, 0, n_pts % n1)
+        term = ck.ct_mul_plain(ct, ck.encode(z, None, qd, level + 1))
+        acc = term if acc is None else ck.ct_add(acc, term)
+        n_pts += 1
+    t_pt = (time.time() - t0) / n_pts
+    t1 = time.time()
+    ck.rotate(ct, T, key)
+    t_rot = time.time() - t1
+    t2 = time.time()
+    ck.rescale(acc)
+    t_rs = time.time() - t2
+    n_in, n_out = cfg.d_in // D, cfg.d_out // D
+    n2 = -(-D // n1)
+    total = (n_out * n_in * D) * t_pt + (n_in * (n1 - 1) + n_out * (n2 - 1)) * t_rot + n_out * t_rs
+    cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    return {"value": total, "unit": "s/projection (extrapolated)", "cores": cores, "kind": "oracle",
+            "sample": "%d weight plaintexts encoded+multiplied+accumulated (%.3f s each), 1 rotation (%.2f s), "
+                      "1 rescale (%.2f s) at N=2^16 level 12; scaled by 229376 plaintexts, 888 rotations, "
+                      "56 rescales" % (n_pts, t_pt, t_rot, t_rs)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-secondary", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py runs on one GPU: the projection path is single-GPU in this build (--gpus %d requested)"
+              % args.gpus, file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+    from workloads import PROJECTION as cfg
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    log("setup: projection 4096 -> 14336")
+    st = setup_projection(torch, np, cfg)
+    ctx = st["ctx"]
+    outs = None
+    for w in range(args.warmup):
+        outs = ctx.linear_project(st["cts"], st["Wd"], st["T"], st["n1"], st["keys"], outs)
+        torch.cuda.synchronize()
+        log("warmup", w, "done")
+    ctx.profile(True)
+    ctx.profile_reset()
+    with Timer(torch) as t:
+        for _ in range(args.steps):
+            outs = ctx.linear_project(st["cts"], st["Wd"], st["T"], st["n1"], st["keys"], outs)
+    prof = ctx.profile_all()
+    ctx.profile(False)
+    ms = t.ms / args.steps
+    log("projection: %.1f ms/step" % ms)
+    err = check_projection(np, st, outs)
+    log("decrypted outputs 0/27/55: max |err| vs X@W = %.3g" % err)
+    roof = roofline(prof)
+    roof["traffic"] = load_traffic(roof["kernel"])
+    kernels_ms = {k: round(v[0] / args.steps, 3) for k, v in sorted(prof.items(), key=lambda kv: -kv[1][0])}
+    del st, outs, ctx
+    torch.cuda.empty_cache()
+    secondary = {}
+    if not args.no_secondary:
+        log("keyswitch batch")
+        secondary["keyswitch"] = bench_keyswitch(torch, np, max(args.steps, 3), 1)
+        torch.cuda.empty_cache()
+        log("ntt microbench")
+        secondary["ntt"] = bench_ntt(torch, max(args.steps, 5))
+        torch.cuda.empty_cache()
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("cpu baseline (oracle sample)")
+        cpu = cpu_baseline(np, cfg)
+    line = {
+        "metric": METRIC,
+        "value": ms / 1e3,
+        "unit": "s/projection",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u64",
+        "data": "synthetic",
+        "config": {"workload": "Llama-3-8B-shaped ct-pt projection 4096x14336, N=2^16, level 12 (13 limbs), "
+                               "24+8 x 50-bit primes, dnum 3, 128 tokens x 256 features, BSGS n1=32 n2=8",
+                   "rotations_per_s": secondary.get("keyswitch", {}).get("rotations_per_s")},
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "decrypt_max_abs_err": err,
+        "kernels_ms_per_step": kernels_ms,
+        "secondary": secondary,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -198,12 +198,18 @@ ckks_status ckks_linear_project(ckks_ctx *ctx, const ckks_buf *in, const double 
 
 /* ---- measurement helpers ------------------------------------------------- */
 
-/* Per-kernel-class timing with HIP events on the context stream.  While
- * enabled, every launch of the named classes is bracketed by events; read
- * back (synchronizes) the summed milliseconds and launch count. */
+/* Per-kernel timing with HIP events on the context stream.  While enabled,
+ * every kernel launch is bracketed by two events and tagged with its
+ * algorithmic HBM bytes (each input and output word once; cache-resident
+ * tables excluded).  ckks_profile_read synchronizes and returns, for the
+ * kernel named `kernel`, the summed milliseconds, launch count and bytes
+ * (any output pointer may be NULL).  ckks_profile_name(i) enumerates the
+ * kernel names (NULL past the last). */
 ckks_status ckks_profile_enable(ckks_ctx *ctx, int on);
-ckks_status ckks_profile_read(ckks_ctx *ctx, const char *kernel_class, double *total_ms, uint64_t *launches);
+ckks_status ckks_profile_read(ckks_ctx *ctx, const char *kernel, double *total_ms, uint64_t *launches,
+                              double *bytes);
 ckks_status ckks_profile_reset(ckks_ctx *ctx);
+const char *ckks_profile_name(int i);
 /* A plain device copy of `bytes` bytes (multiple of 16) on the context stream,
  * for calibrating HBM counters and achievable bandwidth. */
 ckks_status ckks_calib_copy(ckks_ctx *ctx, void *dev_dst, const void *dev_src, size_t bytes);

@@ -60,8 +60,10 @@ def lib():
         L.or_conv.argtypes = [u64p, u64p, i64, u64p, u64p, i64, i64, u64p, u64p]
         L.or_encode_round.argtypes = [f64p, ctypes.c_void_p, i64, f64, i64p]
         L.or_encode_def_round.argtypes = [f64p, ctypes.c_void_p, i64, f64, i64p, f64p]
+        L.or_encode_unrounded.argtypes = [f64p, ctypes.c_void_p, i64, f64, f64p]
         for name in ("or_ntt", "or_intt", "or_ntt_rows", "or_mul", "or_add", "or_sub", "or_mul_scalar",
-                     "or_reduce_i64", "or_conv", "or_encode_round", "or_encode_def_round"):
+                     "or_reduce_i64", "or_conv", "or_encode_round", "or_encode_def_round",
+                     "or_encode_unrounded"):
             getattr(L, name).restype = None
         _LIB = L
     return _LIB
@@ -255,6 +257,14 @@ class Ckks:
             zi = np.ascontiguousarray(zi, dtype=np.float64)
             lib().or_encode_round(zr, zi.ctypes.data, self.n, float(delta), m)
         return m
+
+    def encode_unrounded(self, zr, zi, delta: float) -> np.ndarray:
+        """The fp64 values whose rounding (half away from zero) gives encode_int."""
+        zr = np.ascontiguousarray(zr, dtype=np.float64)
+        x = np.empty(self.n, dtype=np.float64)
+        lib().or_encode_unrounded(zr, None if zi is None else np.ascontiguousarray(zi, dtype=np.float64).ctypes.data,
+                                  self.n, float(delta), x)
+        return x
 
     def encode_int_def(self, zr, zi, delta):
         """Definitional O(N^2) encode in long double: (rounded ints, distance of each to a tie)."""

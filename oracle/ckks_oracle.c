@@ -17,6 +17,7 @@
  *
  * Build: gcc -O2 -fPIC -shared -fopenmp -ffp-contract=off (see build.py).
  */
+#define _GNU_SOURCE /* sincos */
 #include <math.h>
 #include <stddef.h>
 #include <stdint.h>
@@ -237,6 +238,10 @@ void or_conv(const uint64_t *in, const uint64_t *qin, int64_t ni, uint64_t *out,
 /* with omega^-e = (cos(2*pi*e/M), -sin(2*pi*e/M)), zeta^-k = (cos(pi*k/N),  */
 /* -sin(pi*k/N)), and a complex product computed as                          */
 /*   (ar*br - ai*bi, ar*bi + ai*br) without fused multiply-add.              */
+/* The cosine and sine of an angle are the two outputs of one call to the C  */
+/* library's sincos(): it can differ from separate sin() and cos() calls in  */
+/* the last bit, and compilers merge or split such calls at will, so the     */
+/* call is named explicitly.                                                 */
 /* ------------------------------------------------------------------------ */
 static void cmul(double ar, double ai, double br, double bi, double *cr, double *ci)
 {
@@ -245,7 +250,23 @@ static void cmul(double ar, double ai, double br, double bi, double *cr, double 
     *ci = p3 + p4;
 }
 
+static void encode_fft(const double *zr, const double *zi, int64_t n, double delta, double *x_out);
+
 void or_encode_round(const double *zr, const double *zi, int64_t n, double delta, int64_t *m_out)
+{
+    double *x = (double *)malloc(sizeof(double) * (size_t)n);
+    encode_fft(zr, zi, n, delta, x);
+    for (int64_t i = 0; i < n; i++) m_out[i] = (int64_t)round(x[i]);
+    free(x);
+}
+
+/* The scaled, unrounded values c * Re v_k, c * Im v_k whose rounding gives m. */
+void or_encode_unrounded(const double *zr, const double *zi, int64_t n, double delta, double *x_out)
+{
+    encode_fft(zr, zi, n, delta, x_out);
+}
+
+static void encode_fft(const double *zr, const double *zi, int64_t n, double delta, double *x_out)
 {
     int64_t M = n / 2, two_n = 2 * n;
     int logm = ilog2(M);
@@ -265,7 +286,9 @@ void or_encode_round(const double *zr, const double *zi, int64_t n, double delta
         for (int64_t b = 0; b < M; b += len) {
             for (int64_t k = 0; k < half; k++) {
                 double ang = 2.0 * M_PI * (double)(k * step) / (double)M;
-                double wr = cos(ang), wi = -sin(ang);
+                double sn, cs;
+                sincos(ang, &sn, &cs);
+                double wr = cs, wi = -sn;
                 double tr, ti;
                 cmul(wr, wi, ar[b + k + half], ai[b + k + half], &tr, &ti);
                 double ur = ar[b + k], ui = ai[b + k];
@@ -279,11 +302,13 @@ void or_encode_round(const double *zr, const double *zi, int64_t n, double delta
     double c = delta * (2.0 / (double)n);
     for (int64_t k = 0; k < M; k++) {
         double ang = M_PI * (double)k / (double)n;
-        double tr = cos(ang), ti = -sin(ang);
+        double sn, cs;
+        sincos(ang, &sn, &cs);
+        double tr = cs, ti = -sn;
         double vr, vi;
         cmul(tr, ti, ar[k], ai[k], &vr, &vi);
-        m_out[k] = (int64_t)round(c * vr);
-        m_out[k + M] = (int64_t)round(c * vi);
+        x_out[k] = c * vr;
+        x_out[k + M] = c * vi;
     }
     free(ar);
     free(ai);

@@ -73,7 +73,9 @@ _SIGS = {
     "ckks_automorph": (ctypes.c_int, [_VP, _VP, _U32, _U32, _VP]),
     "ckks_linear_project": (ctypes.c_int, [_VP, _BP, _VP, ctypes.POINTER(_ProjShape), _VP, _VP, _U32, _BP]),
     "ckks_profile_enable": (ctypes.c_int, [_VP, ctypes.c_int]),
-    "ckks_profile_read": (ctypes.c_int, [_VP, ctypes.c_char_p, ctypes.POINTER(_DBL), ctypes.POINTER(_U64)]),
+    "ckks_profile_read": (ctypes.c_int, [_VP, ctypes.c_char_p, ctypes.POINTER(_DBL), ctypes.POINTER(_U64),
+                                         ctypes.POINTER(_DBL)]),
+    "ckks_profile_name": (ctypes.c_char_p, [ctypes.c_int]),
     "ckks_profile_reset": (ctypes.c_int, [_VP]),
     "ckks_calib_copy": (ctypes.c_int, [_VP, _VP, _VP, _SZ]),
     "ckks_calib_modmul": (ctypes.c_int, [_VP, _VP, _U32, _U32, ctypes.c_int]),
@@ -336,11 +338,24 @@ class Context:
     def profile_reset(self):
         _check(self.lib.ckks_profile_reset(self.h), "ckks_profile_reset")
 
-    def profile_read(self, cls: str):
-        ms, cnt = ctypes.c_double(), ctypes.c_uint64()
-        _check(self.lib.ckks_profile_read(self.h, cls.encode(), ctypes.byref(ms), ctypes.byref(cnt)),
-               "ckks_profile_read")
-        return ms.value, cnt.value
+    def profile_read(self, kernel: str):
+        """(total ms, launches, algorithmic bytes) of one kernel since the last reset."""
+        ms, cnt, by = ctypes.c_double(), ctypes.c_uint64(), ctypes.c_double()
+        _check(self.lib.ckks_profile_read(self.h, kernel.encode(), ctypes.byref(ms), ctypes.byref(cnt),
+                                          ctypes.byref(by)), "ckks_profile_read")
+        return ms.value, cnt.value, by.value
+
+    def profile_all(self):
+        """{kernel: (total ms, launches, algorithmic bytes)} for every kernel that ran."""
+        out, i = {}, 0
+        while True:
+            name = self.lib.ckks_profile_name(i)
+            if name is None:
+                return out
+            r = self.profile_read(name.decode())
+            if r[1]:
+                out[name.decode()] = r
+            i += 1
 
     def calib_copy(self, dst: torch.Tensor, src: torch.Tensor):
         _check(self.lib.ckks_calib_copy(self.h, _ptr(dst), _ptr(src), src.numel() * src.element_size()),

@@ -54,8 +54,14 @@ struct ConvDev {
     ulonglong2 *d_qhat_mod = nullptr;  // [ns][nt] (value, Shoup companion) mod dst_t
 };
 
-// Kernel classes timed by the optional per-kernel event profiler.
-enum KClass { K_NTT_FWD = 0, K_NTT_INV, K_ENCODE_FFT, K_ENCODE_NTT, K_MAC, K_KEYIP, K_CONV, K_ELEM, K_NCLASS };
+// Kernels timed by the optional event profiler.  Each launch is bracketed by
+// two events and tagged with its algorithmic bytes: the bytes the kernel must
+// read and write in HBM at minimum (each input and output word once; twiddle
+// and constant tables, which stay cache-resident, are not counted).
+enum KClass {
+    K_NTT_FWD_COL = 0, K_NTT_FWD_ROW, K_NTT_INV_ROW, K_NTT_INV_COL, K_FFT_A, K_FFT_B, K_GATHER, K_TO_RNS,
+    K_MAC, K_KEYIP, K_CONV, K_MODDOWN, K_ELEM, K_NCLASS
+};
 extern const char *const kKClassNames[K_NCLASS];
 
 struct ckks_ctx {
@@ -81,10 +87,15 @@ struct ckks_ctx {
     void *scratch = nullptr;
     size_t scratch_bytes = 0;
 
-    // optional per-kernel-class event profiling
+    // optional per-kernel event profiling
     bool profiling = false;
-    std::vector<std::pair<hipEvent_t, hipEvent_t>> prof_events[K_NCLASS];
+    struct ProfRec {
+        hipEvent_t a, b;
+        double bytes;
+    };
+    std::vector<ProfRec> prof_events[K_NCLASS];
     double prof_ms[K_NCLASS] = {0};
+    double prof_bytes[K_NCLASS] = {0};
     uint64_t prof_count[K_NCLASS] = {0};
 
     uint32_t n_primes() const { return n_q + n_p; }
@@ -93,8 +104,9 @@ struct ckks_ctx {
 // scratch of at least `bytes` bytes (256-byte aligned), growing the arena
 ckks_status ctx_scratch(ckks_ctx *ctx, size_t bytes, void **out);
 
-// profiler brackets: call prof_begin before a launch and prof_end after
-void prof_begin(ckks_ctx *ctx, KClass k);
+// profiler brackets: call prof_begin before a launch and prof_end after;
+// bytes = the launch's algorithmic HBM bytes
+void prof_begin(ckks_ctx *ctx, KClass k, double bytes);
 void prof_end(ckks_ctx *ctx, KClass k);
 
 // basis-conversion tables for ModUp of digit j at `level` (dst = other q-limbs

@@ -29,8 +29,9 @@ ckks_status set_error(ckks_status st, const char *fmt, ...)
 void clear_error() { g_err[0] = 0; }
 extern "C" const char *ckks_last_error(void) { return g_err; }
 
-const char *const kKClassNames[K_NCLASS] = {"ntt_fwd", "ntt_inv", "encode_fft", "encode_ntt",
-                                            "mac",     "key_ip",  "conv",       "elementwise"};
+const char *const kKClassNames[K_NCLASS] = {"ntt_fwd_col", "ntt_fwd_row", "ntt_inv_row", "ntt_inv_col", "fft_a",
+                                            "fft_b",       "gather",      "to_rns",      "mac",         "key_ip",
+                                            "conv",        "moddown",     "elementwise"};
 
 // --------------------------------------------------------------- host math --
 namespace hm {
@@ -156,16 +157,23 @@ static ckks_status build_tables(ckks_ctx *c)
     // fp64 tables of the encode/decode FFT.  The expressions are fixed (the
     // rounding of the encoded integers depends on every bit of them):
     //   omega^-e = (cos(2 pi e / M), -sin(2 pi e / M)),  M = N/2,
-    //   zeta^-k  = (cos(pi k / N),  -sin(pi k / N)).
+    //   zeta^-k  = (cos(pi k / N),  -sin(pi k / N)),
+    // with cosine and sine taken from one call to the C library's sincos(),
+    // named explicitly because it can differ from separate sin()/cos() calls
+    // in the last bit and compilers merge or split such calls at will.
     const uint32_t M = n / 2;
     std::vector<double2> w(M / 2 > 0 ? M / 2 : 1), twist(M);
     for (uint32_t e = 0; e < M / 2; e++) {
         const double ang = 2.0 * M_PI * (double)e / (double)M;
-        w[e] = make_double2(cos(ang), -sin(ang));
+        double sn, cs;
+        sincos(ang, &sn, &cs);
+        w[e] = make_double2(cs, -sn);
     }
     for (uint32_t k = 0; k < M; k++) {
         const double ang = M_PI * (double)k / (double)n;
-        twist[k] = make_double2(cos(ang), -sin(ang));
+        double sn, cs;
+        sincos(ang, &sn, &cs);
+        twist[k] = make_double2(cs, -sn);
     }
     std::vector<uint32_t> pos(M);
     int logm = 0;
@@ -271,7 +279,7 @@ ckks_status ctx_scratch(ckks_ctx *c, size_t bytes, void **out)
     return CKKS_OK;
 }
 
-void prof_begin(ckks_ctx *c, KClass k)
+void prof_begin(ckks_ctx *c, KClass k, double bytes)
 {
     if (!c->profiling) return;
     hipEvent_t a, b;
@@ -281,25 +289,26 @@ void prof_begin(ckks_ctx *c, KClass k)
         return;
     }
     (void)hipEventRecord(a, c->stream);
-    c->prof_events[k].push_back({a, b});
+    c->prof_events[k].push_back({a, b, bytes});
 }
 void prof_end(ckks_ctx *c, KClass k)
 {
     if (!c->profiling || c->prof_events[k].empty()) return;
-    (void)hipEventRecord(c->prof_events[k].back().second, c->stream);
+    (void)hipEventRecord(c->prof_events[k].back().b, c->stream);
 }
 
 static ckks_status prof_collect(ckks_ctx *c)
 {
     for (int k = 0; k < K_NCLASS; k++) {
         for (auto &ev : c->prof_events[k]) {
-            HIP_TRY(hipEventSynchronize(ev.second));
+            HIP_TRY(hipEventSynchronize(ev.b));
             float ms = 0;
-            HIP_TRY(hipEventElapsedTime(&ms, ev.first, ev.second));
+            HIP_TRY(hipEventElapsedTime(&ms, ev.a, ev.b));
             c->prof_ms[k] += ms;
+            c->prof_bytes[k] += ev.bytes;
             c->prof_count[k]++;
-            (void)hipEventDestroy(ev.first);
-            (void)hipEventDestroy(ev.second);
+            (void)hipEventDestroy(ev.a);
+            (void)hipEventDestroy(ev.b);
         }
         c->prof_events[k].clear();
     }
@@ -424,11 +433,12 @@ ckks_status ckks_profile_reset(ckks_ctx *c)
     CK_TRY(prof_collect(c));
     for (int k = 0; k < K_NCLASS; k++) {
         c->prof_ms[k] = 0;
+        c->prof_bytes[k] = 0;
         c->prof_count[k] = 0;
     }
     return CKKS_OK;
 }
-ckks_status ckks_profile_read(ckks_ctx *c, const char *cls, double *total_ms, uint64_t *launches)
+ckks_status ckks_profile_read(ckks_ctx *c, const char *cls, double *total_ms, uint64_t *launches, double *bytes)
 {
     clear_error();
     CK_REQUIRE(c && cls, CKKS_EINVAL, "null argument");
@@ -437,10 +447,12 @@ ckks_status ckks_profile_read(ckks_ctx *c, const char *cls, double *total_ms, ui
         if (strcmp(cls, kKClassNames[k]) == 0) {
             if (total_ms) *total_ms = c->prof_ms[k];
             if (launches) *launches = c->prof_count[k];
+            if (bytes) *bytes = c->prof_bytes[k];
             return CKKS_OK;
         }
     }
-    return set_error(CKKS_EINVAL, "unknown kernel class '%s'", cls);
+    return set_error(CKKS_EINVAL, "unknown kernel '%s'", cls);
 }
+const char *ckks_profile_name(int k) { return (k >= 0 && k < K_NCLASS) ? kKClassNames[k] : nullptr; }
 
 }  // extern "C"

@@ -226,12 +226,15 @@ ckks_status fft_passes(ckks_ctx *ctx, double2 *work, uint32_t batch, int mode, d
     const uint32_t logb = logm < (uint32_t)kLogBA ? logm : (uint32_t)kLogBA;
     const uint32_t B = 1u << logb;
     const bool single = logb == logm;
-    prof_begin(ctx, K_ENCODE_FFT);
+    const double bytes = 32.0 * batch * M;  // read and write every complex point (or its two integers)
+    prof_begin(ctx, K_FFT_A, bytes);
     hipLaunchKernelGGL(k_fft_a, dim3(batch * (M >> logb)), dim3(kThreads), B * sizeof(double2), ctx->stream, work,
                        ctx->d_fft_w, logm, logb, single ? mode : 0, ctx->d_fft_twist, c, m);
+    prof_end(ctx, K_FFT_A);
     if (!single) {
         const uint32_t hb = logm - logb;
         const dim3 grid(batch * (B / kThreads));
+        prof_begin(ctx, K_FFT_B, bytes);
         switch (hb) {
         case 1: hipLaunchKernelGGL(k_fft_b<1>, grid, dim3(kThreads), 0, ctx->stream, work, ctx->d_fft_w, logm, logb,
                                    mode, ctx->d_fft_twist, c, m); break;
@@ -241,10 +244,10 @@ ckks_status fft_passes(ckks_ctx *ctx, double2 *work, uint32_t batch, int mode, d
                                    mode, ctx->d_fft_twist, c, m); break;
         case 4: hipLaunchKernelGGL(k_fft_b<4>, grid, dim3(kThreads), 0, ctx->stream, work, ctx->d_fft_w, logm, logb,
                                    mode, ctx->d_fft_twist, c, m); break;
-        default: prof_end(ctx, K_ENCODE_FFT); return set_error(CKKS_EUNSUPPORTED, "fft: unsupported size");
+        default: prof_end(ctx, K_FFT_B); return set_error(CKKS_EUNSUPPORTED, "fft: unsupported size");
         }
+        prof_end(ctx, K_FFT_B);
     }
-    prof_end(ctx, K_ENCODE_FFT);
     HIP_TRY(hipGetLastError());
     return CKKS_OK;
 }
@@ -254,8 +257,12 @@ ckks_status enc_coeffs(ckks_ctx *ctx, const SlotSource &src, uint32_t batch, dou
 {
     if (!batch) return CKKS_OK;
     const uint32_t M = ctx->n / 2;
+    // write every complex point; read the slots (W-generated: the D distinct weights of each plaintext)
+    const double reads = src.W ? 8.0 * src.feats : (src.im ? 16.0 : 8.0) * M;
+    prof_begin(ctx, K_GATHER, batch * (16.0 * M + reads));
     hipLaunchKernelGGL(k_gather, dim3((M + kThreads - 1) / kThreads, batch), dim3(kThreads), 0, ctx->stream, work,
                        src, ctx->d_slot_pos, M);
+    prof_end(ctx, K_GATHER);
     HIP_TRY(hipGetLastError());
     return fft_passes(ctx, work, batch, 1, scale * (2.0 / (double)ctx->n), m_out);
 }
@@ -263,8 +270,10 @@ ckks_status enc_coeffs(ckks_ctx *ctx, const SlotSource &src, uint32_t batch, dou
 ckks_status enc_to_rns(ckks_ctx *ctx, const int64_t *m, uint32_t batch, uint32_t limbs, uint64_t *out)
 {
     if (!batch) return CKKS_OK;
+    prof_begin(ctx, K_TO_RNS, 8.0 * batch * ctx->n * (1 + limbs));
     hipLaunchKernelGGL(k_to_rns, dim3((ctx->n + kThreads - 1) / kThreads, batch), dim3(kThreads), 0, ctx->stream,
                        out, m, limbs, ctx->log_n, ctx->d_mod);
+    prof_end(ctx, K_TO_RNS);
     HIP_TRY(hipGetLastError());
     return CKKS_OK;
 }

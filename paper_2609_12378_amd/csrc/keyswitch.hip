@@ -132,7 +132,7 @@ ckks_status launch_conv(ckks_ctx *ctx, const ConvDev *cd, const uint64_t *in, ui
     for (int i = 0; i < cd->ns; i++) a.src[i] = cd->src[i];
     for (int t = 0; t < cd->nt; t++) a.dst[t] = cd->dst[t];
     const dim3 grid((ctx->n + kThreads - 1) / kThreads, polys), block(kThreads);
-    prof_begin(ctx, K_CONV);
+    prof_begin(ctx, K_CONV, 8.0 * polys * (a.ns + a.nt) * ctx->n);
     if (a.ns <= 4)
         hipLaunchKernelGGL(k_conv<4>, grid, block, 0, ctx->stream, in, in_stride, out, out_stride, split, skip, a,
                            cd->d_qhat_inv, cd->d_qhat_mod, ctx->d_mod, ctx->log_n);
@@ -192,7 +192,8 @@ ckks_status ks_inner_product(ckks_ctx *ctx, const uint64_t *digits, uint32_t nd,
 {
     const uint32_t ext = level + 1 + ctx->n_p;
     const dim3 grid((ctx->n + kThreads - 1) / kThreads, ext), block(kThreads);
-    prof_begin(ctx, K_KEYIP);
+    // digits (nd rows of ext), key rows (nd x 2 x ext), two outputs of ext rows
+    prof_begin(ctx, K_KEYIP, 8.0 * ctx->n * ext * (3.0 * nd + 2.0));
     hipLaunchKernelGGL(k_key_ip, grid, block, 0, ctx->stream, digits, key, u, nd, ext, level, ctx->n_q,
                        ctx->n_primes(), g, ctx->d_mod, ctx->log_n);
     prof_end(ctx, K_KEYIP);
@@ -213,8 +214,11 @@ ckks_status ks_moddown(ckks_ctx *ctx, uint64_t *u, uint32_t polys, uint32_t leve
     CK_TRY(launch_conv(ctx, cd, u + (size_t)L * N, ext, work, L, L, 0, polys));
     CK_TRY(launch_ntt(ctx, work, polys * L, limb_range(0, L), false));
     const dim3 grid((ctx->n + kThreads - 1) / kThreads, L, polys), block(kThreads);
+    const double adds = (add0 ? 1.0 : 0.0) + (add1 ? 1.0 : 0.0);
+    prof_begin(ctx, K_MODDOWN, 8.0 * ctx->n * L * (3.0 * polys + adds));
     hipLaunchKernelGGL(k_moddown_finish, grid, block, 0, ctx->stream, out, u, work, add0, add0_g, add1, ext, level,
                        ctx->d_pinv, ctx->d_mod, ctx->log_n);
+    prof_end(ctx, K_MODDOWN);
     HIP_TRY(hipGetLastError());
     return CKKS_OK;
 }

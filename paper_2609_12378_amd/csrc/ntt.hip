@@ -312,18 +312,31 @@ ckks_status launch_ntt_strided(ckks_ctx *ctx, uint64_t *data, uint32_t batch, ui
     if (s1 > 0 && s1 < 4) s1 = 4;
     const int s2 = log_n - s1;
     hipError_t e = hipSuccess;
-    prof_begin(ctx, inverse ? K_NTT_INV : K_NTT_FWD);
+    const double bytes = 16.0 * batch * map.n * ctx->n;  // each pass reads and writes every residue
     if (!inverse) {
-        if (s1) e = dispatch_col<false>(s1, ctx, data, batch, bstride, map, ctx->d_tw);
-        if (e == hipSuccess) e = dispatch_row<false, true>(s2, ctx, data, batch, bstride, map, ctx->d_tw);
+        if (s1) {
+            prof_begin(ctx, K_NTT_FWD_COL, bytes);
+            e = dispatch_col<false>(s1, ctx, data, batch, bstride, map, ctx->d_tw);
+            prof_end(ctx, K_NTT_FWD_COL);
+        }
+        if (e == hipSuccess) {
+            prof_begin(ctx, K_NTT_FWD_ROW, bytes);
+            e = dispatch_row<false, true>(s2, ctx, data, batch, bstride, map, ctx->d_tw);
+            prof_end(ctx, K_NTT_FWD_ROW);
+        }
     } else {
+        prof_begin(ctx, K_NTT_INV_ROW, bytes);
         if (s1)
             e = dispatch_row<true, false>(s2, ctx, data, batch, bstride, map, ctx->d_itw);
         else
             e = dispatch_row<true, true>(s2, ctx, data, batch, bstride, map, ctx->d_itw);
-        if (e == hipSuccess && s1) e = dispatch_col<true>(s1, ctx, data, batch, bstride, map, ctx->d_itw);
+        prof_end(ctx, K_NTT_INV_ROW);
+        if (e == hipSuccess && s1) {
+            prof_begin(ctx, K_NTT_INV_COL, bytes);
+            e = dispatch_col<true>(s1, ctx, data, batch, bstride, map, ctx->d_itw);
+            prof_end(ctx, K_NTT_INV_COL);
+        }
     }
-    prof_end(ctx, inverse ? K_NTT_INV : K_NTT_FWD);
     if (e != hipSuccess) return set_error(CKKS_EHIP, "ntt launch failed: %s", hipGetErrorString(e));
     return CKKS_OK;
 }

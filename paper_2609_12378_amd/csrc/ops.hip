@@ -176,7 +176,7 @@ ckks_status launch_binary(ckks_ctx *ctx, uint64_t *out, const uint64_t *a, const
 {
     const size_t total = (size_t)rows << ctx->log_n;
     if (!total) return CKKS_OK;
-    prof_begin(ctx, K_ELEM);
+    prof_begin(ctx, K_ELEM, 24.0 * total);
     hipLaunchKernelGGL(k_binary, grid_for(total), dim3(kThreads), 0, ctx->stream, out, a, b, total, ctx->log_n, map,
                        ctx->d_mod, op);
     prof_end(ctx, K_ELEM);

@@ -83,7 +83,9 @@ ckks_status launch_mac(ckks_ctx *ctx, uint64_t *acc, const uint64_t *pt, const u
                        uint32_t jc, uint32_t ib0, uint32_t bcount, uint32_t n1, uint32_t L, bool accumulate)
 {
     const dim3 grid((ctx->n + kThreads - 1) / kThreads, L), block(kThreads);
-    prof_begin(ctx, K_MAC);
+    // plaintexts (jc x P), rotated inputs (P ciphertexts), accumulators written (and read when accumulating)
+    const double w = 8.0 * L * ctx->n;
+    prof_begin(ctx, K_MAC, w * ((double)jc * P + 2.0 * P + 2.0 * jc * (accumulate ? 2 : 1)));
     if (jc <= 1)
         hipLaunchKernelGGL(k_mac<1>, grid, block, 0, ctx->stream, acc, pt, xrot, P, jc, ib0, bcount, n1, L,
                            ctx->log_n, (int)accumulate, ctx->d_mod);
@@ -205,9 +207,7 @@ extern "C" ckks_status ckks_linear_project(ckks_ctx *ctx, const ckks_buf *in, co
                 const uint32_t batch = jc * P;
                 CK_TRY(enc_coeffs(ctx, src, batch, delta_w, fft, mint));
                 CK_TRY(enc_to_rns(ctx, mint, batch, L, pts));
-                prof_begin(ctx, K_ENCODE_NTT);
                 CK_TRY(launch_ntt(ctx, pts, batch * L, limb_range(0, L), false));
-                prof_end(ctx, K_ENCODE_NTT);
                 CK_TRY(launch_mac(ctx, acc, pts, xrot, P, jc, pb0, bcount, n1, L, pb0 > 0));
             }
             for (uint32_t jj = 0; jj < jc; jj++) {

@@ -94,6 +94,17 @@ def test_encode_full_degree_at_projection_scale(big):
     eq(pt.data[0], big.ck.encode(re, None, scale, 13))
 
 
+def test_encode_many_weight_vectors_full_degree(big):
+    # 24 more weight-like vectors at scale q_12: each has tens of coefficients within one ulp
+    # of a rounding tie, so any difference in twiddles or operation order shows up here
+    g = rng(4, 2, extra=8)
+    scale = float(big.ctx.q[12])
+    for r in range(24):
+        re = np.repeat(g.normal(0, 0.02, 256), 128)
+        pt = big.ctx.encode(to_dev(re), None, scale, 2)
+        eq(pt.data[0], big.ck.encode(re, None, scale, 2))
+
+
 def test_decode(toy, big):
     for env, limbs, scale in ((toy, 4, 2.0 ** 30), (toy, 1, 2.0 ** 30), (big, 13, 2.0 ** 40)):
         re, im = env.slots(20)
