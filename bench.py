@@ -252,6 +252,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-secondary", action="store_true")
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="also run one plain device copy of this many MiB (for hardware-counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py runs on one GPU: the projection path is single-GPU in this build (--gpus %d requested)"
@@ -265,6 +267,13 @@ def main():
     log("setup: projection 4096 -> 14336")
     st = setup_projection(torch, np, cfg)
     ctx = st["ctx"]
+    if args.calib_copy_mib:
+        src = torch.ones(args.calib_copy_mib << 17, dtype=torch.uint64, device="cuda")
+        dst = torch.empty_like(src)
+        ctx.calib_copy(dst, src)
+        torch.cuda.synchronize()
+        log("calibration copy of %d MiB done" % args.calib_copy_mib)
+        del src, dst
     outs = None
     for w in range(args.warmup):
         outs = ctx.linear_project(st["cts"], st["Wd"], st["T"], st["n1"], st["keys"], outs)
