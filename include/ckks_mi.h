@@ -87,6 +87,12 @@ typedef struct {
 ckks_status ckks_ctx_create(const ckks_params *params, void *hip_stream, ckks_ctx **out);
 void ckks_ctx_destroy(ckks_ctx *ctx);
 ckks_status ckks_ctx_set_stream(ckks_ctx *ctx, void *hip_stream);
+/* Arithmetic of the number-theoretic transforms.  mode 0 (default): fp64
+ * butterflies (exact integer-valued doubles with an FMA error term) for every
+ * launch whose primes are all below 2^50, 64-bit integer Shoup butterflies
+ * otherwise; mode 1: integer Shoup butterflies everywhere.  Both produce
+ * identical canonical residues. */
+ckks_status ckks_ctx_set_ntt_arith(ckks_ctx *ctx, int mode);
 /* Host copies of the primes q (n_q), p (n_p) and psi (n_q + n_p, q first);
  * any pointer may be NULL. */
 ckks_status ckks_ctx_primes(const ckks_ctx *ctx, uint64_t *q, uint64_t *p, uint64_t *psi);

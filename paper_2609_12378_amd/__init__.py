@@ -51,6 +51,7 @@ _SIGS = {
     "ckks_ctx_create": (ctypes.c_int, [ctypes.POINTER(_Params), _VP, ctypes.POINTER(_VP)]),
     "ckks_ctx_destroy": (None, [_VP]),
     "ckks_ctx_set_stream": (ctypes.c_int, [_VP, _VP]),
+    "ckks_ctx_set_ntt_arith": (ctypes.c_int, [_VP, ctypes.c_int]),
     "ckks_ctx_primes": (ctypes.c_int, [_VP, _VP, _VP, _VP]),
     "ckks_galois_elt": (_U32, [_VP, _I32]),
     "ckks_last_error": (ctypes.c_char_p, []),
@@ -186,6 +187,10 @@ class Context:
             self.h = None
 
     # ---------------- helpers ----------------
+    def set_ntt_arith(self, mode: int):
+        """0: fp64 butterflies where every prime is below 2^50 (default); 1: integer Shoup everywhere."""
+        _check(self.lib.ckks_ctx_set_ntt_arith(self.h, mode), "ckks_ctx_set_ntt_arith")
+
     def galois_elt(self, steps: int) -> int:
         return int(self.lib.ckks_galois_elt(self.h, steps))
 

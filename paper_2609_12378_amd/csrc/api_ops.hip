@@ -75,8 +75,7 @@ ckks_status ckks_encode(ckks_ctx *ctx, const double *re, const double *im, doubl
     src.re = re;
     src.im = im;
     CK_TRY(enc_coeffs(ctx, src, 1, scale, work, m));
-    CK_TRY(enc_to_rns(ctx, m, 1, n_limbs, pt->data));
-    CK_TRY(launch_ntt(ctx, pt->data, n_limbs, limb_range(0, n_limbs), false));
+    CK_TRY(launch_ntt_from_i64(ctx, m, pt->data, 1, n_limbs));
     pt->scale = scale;
     return CKKS_OK;
 }

@@ -75,6 +75,10 @@ struct ckks_ctx {
     ModQ *d_mod = nullptr;               // [n_primes]
     ulonglong2 *d_tw = nullptr;          // [n_primes][N] (psi^brev(k), Shoup)
     ulonglong2 *d_itw = nullptr;         // [n_primes][N] (psi^-brev(k), Shoup)
+    double *d_twf = nullptr;             // [n_primes][N] psi^brev(k) as doubles (primes < 2^50)
+    double *d_itwf = nullptr;            // [n_primes][N] psi^-brev(k) as doubles
+    bool f64_ok[kMaxPrimes] = {};        // q < 2^50: the fp64 butterflies are exact
+    bool int_only = false;               // force the integer Shoup butterflies
     double2 *d_fft_w = nullptr;          // [N/4]  omega^-e, omega = exp(2 pi i/(N/2))
     double2 *d_fft_twist = nullptr;      // [N/2]  zeta^-k, zeta = exp(i pi / N)
     uint32_t *d_slot_pos = nullptr;      // [N/2]  bit-reversed FFT position of slot j
@@ -131,6 +135,8 @@ ckks_status launch_ntt(ckks_ctx *ctx, uint64_t *data, uint32_t rows, const LimbM
 // NTT of `batch` groups of map.n rows; group b starts at row b * bstride of `data`.
 ckks_status launch_ntt_strided(ckks_ctx *ctx, uint64_t *data, uint32_t batch, uint32_t bstride, const LimbMap &map,
                                bool inverse);
+// forward NTT of signed coefficient rows m[batch][N] into out[batch][limbs][N] (primes 0..limbs-1)
+ckks_status launch_ntt_from_i64(ckks_ctx *ctx, const int64_t *m, uint64_t *out, uint32_t batch, uint32_t limbs);
 // identity map for a contiguous range of prime indices
 LimbMap limb_range(uint32_t first, uint32_t count);
 

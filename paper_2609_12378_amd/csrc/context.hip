@@ -117,6 +117,7 @@ static ckks_status build_tables(ckks_ctx *c)
     c->psi.resize(np);
     c->mods.resize(np);
     std::vector<ulonglong2> tw((size_t)np * n), itw((size_t)np * n);
+    std::vector<double> twf((size_t)np * n), itwf((size_t)np * n);
     for (uint32_t k = 0; k < np; k++) {
         const uint64_t q = c->primes[k];
         uint64_t psi = 0;
@@ -140,7 +141,10 @@ static ckks_status build_tables(ckks_ctx *c)
             const uint32_t e = hm::brev(i, (int)c->log_n);
             tw[(size_t)k * n + i] = shoup_pair(pw[e], q);
             itw[(size_t)k * n + i] = shoup_pair(ipw[e], q);
+            twf[(size_t)k * n + i] = (double)pw[e];
+            itwf[(size_t)k * n + i] = (double)ipw[e];
         }
+        c->f64_ok[k] = q < (1ull << 50);
         ModQ &m = c->mods[k];
         m.q = q;
         m.twoq = 2 * q;
@@ -149,9 +153,14 @@ static ckks_status build_tables(ckks_ctx *c)
         m.one_s = (uint64_t)(((u128)1 << 64) / q);
         m.ninv = hm::inv(n % q, q);
         m.ninvs = hm::shoup(m.ninv, q);
+        m.qd = (double)q;
+        m.qinvd = 1.0 / (double)q;
+        m.ninvd = (double)m.ninv;
     }
     CK_TRY(upload((void **)&c->d_tw, tw.data(), tw.size() * sizeof(ulonglong2)));
     CK_TRY(upload((void **)&c->d_itw, itw.data(), itw.size() * sizeof(ulonglong2)));
+    CK_TRY(upload((void **)&c->d_twf, twf.data(), twf.size() * sizeof(double)));
+    CK_TRY(upload((void **)&c->d_itwf, itwf.data(), itwf.size() * sizeof(double)));
     CK_TRY(upload((void **)&c->d_mod, c->mods.data(), c->mods.size() * sizeof(ModQ)));
 
     // fp64 tables of the encode/decode FFT.  The expressions are fixed (the
@@ -382,7 +391,7 @@ void ckks_ctx_destroy(ckks_ctx *c)
     if (!c) return;
     (void)hipDeviceSynchronize();
     (void)prof_collect(c);
-    void *ptrs[] = {c->d_mod, c->d_tw, c->d_itw, c->d_fft_w, c->d_fft_twist, c->d_slot_pos,
+    void *ptrs[] = {c->d_mod, c->d_tw, c->d_itw, c->d_twf, c->d_itwf, c->d_fft_w, c->d_fft_twist, c->d_slot_pos,
                     c->d_pinv, c->d_pmodq, c->d_qlinv, c->scratch};
     for (void *p : ptrs)
         if (p) (void)hipFree(p);
@@ -398,6 +407,15 @@ ckks_status ckks_ctx_set_stream(ckks_ctx *c, void *stream)
     clear_error();
     CK_REQUIRE(c, CKKS_EINVAL, "null context");
     c->stream = (hipStream_t)stream;
+    return CKKS_OK;
+}
+
+ckks_status ckks_ctx_set_ntt_arith(ckks_ctx *c, int mode)
+{
+    clear_error();
+    CK_REQUIRE(c, CKKS_EINVAL, "null context");
+    CK_REQUIRE(mode == 0 || mode == 1, CKKS_EINVAL, "ntt arithmetic mode %d is not 0 or 1", mode);
+    c->int_only = mode == 1;
     return CKKS_OK;
 }
 

@@ -21,6 +21,8 @@ struct ModQ {
     uint64_t r64, r64s;   // 2^64 mod q and its Shoup companion
     uint64_t one_s;       // floor(2^64 / q): the Shoup companion of 1
     uint64_t ninv, ninvs; // N^-1 mod q and its Shoup companion
+    double qd, qinvd;     // q and fl(1/q) for the fp64 arithmetic (q < 2^50)
+    double ninvd;         // N^-1 mod q as a double
 };
 
 __device__ __forceinline__ uint64_t mulhi64(uint64_t a, uint64_t b)

@@ -17,6 +17,7 @@
 //  3. giant-step rotation of each partial sum at level l, summation, rescale.
 // The plaintext scale is q_l, so the rescale returns the input scale exactly.
 #include <algorithm>
+#include <cstdlib>
 #include <cstring>
 #include <vector>
 
@@ -155,7 +156,11 @@ extern "C" ckks_status ckks_linear_project(ckks_ctx *ctx, const ckks_buf *in, co
     // ---- scratch layout
     const size_t N = ctx->n, ctw = 2 * (size_t)L * N;
     const uint32_t maxpairs = n_in * n1;
-    const uint32_t Pb = std::min<uint32_t>(maxpairs, std::max<uint32_t>(1, (uint32_t)((size_t(1) << 31) / ((size_t)kJ * L * N * 8))));
+    size_t budget = size_t(1) << 31;
+    uint32_t Jt = kJ;
+    if (const char *e = getenv("CKKS_PROJ_BATCH_MIB")) budget = (size_t)atol(e) << 20;
+    if (const char *e = getenv("CKKS_PROJ_J")) Jt = std::max<uint32_t>(1, std::min<uint32_t>(kJ, (uint32_t)atoi(e)));
+    const uint32_t Pb = std::min<uint32_t>(maxpairs, std::max<uint32_t>(1, (uint32_t)(budget / ((size_t)Jt * L * N * 8))));
     const size_t xrot_w = (size_t)n_in * n1 * ctw;
     const size_t acc_w = (size_t)kJ * ctw, tot_w = (size_t)kJ * ctw, rot_w = ctw;
     const size_t pt_w = (size_t)kJ * Pb * L * N;
@@ -187,8 +192,8 @@ extern "C" ckks_status ckks_linear_project(ckks_ctx *ctx, const ckks_buf *in, co
 
     // ---- 2./3. tiles of output blocks
     const double delta_w = (double)ctx->primes[level];
-    for (uint32_t j0 = 0; j0 < n_out; j0 += kJ) {
-        const uint32_t jc = std::min<uint32_t>(kJ, n_out - j0);
+    for (uint32_t j0 = 0; j0 < n_out; j0 += Jt) {
+        const uint32_t jc = std::min<uint32_t>(Jt, n_out - j0);
         for (uint32_t g = 0; g < n2; g++) {
             const uint32_t bcount = std::min<uint32_t>(n1, D - n1 * g);
             const uint32_t pairs = n_in * bcount;
@@ -206,8 +211,7 @@ extern "C" ckks_status ckks_linear_project(ckks_ctx *ctx, const ckks_buf *in, co
                 src.pairs = P;
                 const uint32_t batch = jc * P;
                 CK_TRY(enc_coeffs(ctx, src, batch, delta_w, fft, mint));
-                CK_TRY(enc_to_rns(ctx, mint, batch, L, pts));
-                CK_TRY(launch_ntt(ctx, pts, batch * L, limb_range(0, L), false));
+                CK_TRY(launch_ntt_from_i64(ctx, mint, pts, batch, L));
                 CK_TRY(launch_mac(ctx, acc, pts, xrot, P, jc, pb0, bcount, n1, L, pb0 > 0));
             }
             for (uint32_t jj = 0; jj < jc; jj++) {

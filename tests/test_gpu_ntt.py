@@ -28,9 +28,11 @@ def test_context_primes_match_oracle(ctx16):
     assert ctx16.psi[:4] == ck.psi
 
 
+@pytest.mark.parametrize("arith", [0, 1], ids=["fp64", "int"])
 @pytest.mark.parametrize("batch,limb0,n_limbs", [(1, 0, 36), (3, 5, 7)])
-def test_ntt_n16_parity(ctx16, batch, limb0, n_limbs):
-    say("ntt n=2^16 batch", batch, "limbs", limb0, n_limbs)
+def test_ntt_n16_parity(ctx16, batch, limb0, n_limbs, arith):
+    say("ntt n=2^16 batch", batch, "limbs", limb0, n_limbs, "arith", arith)
+    ctx16.set_ntt_arith(arith)
     ck = Ckks(16, ctx16.q)
     primes = ctx16.q[limb0:limb0 + n_limbs]
     a = uniform_residues(rng(2, 1, extra=batch), primes, 1 << 16, lead=(batch,))
@@ -47,14 +49,17 @@ def test_ntt_n16_parity(ctx16, batch, limb0, n_limbs):
     ctx16.intt(t2, limb0)
     want_inv = np.stack([ck.intt(a[b], idx) for b in range(batch)])
     assert np.array_equal(to_host(t2), want_inv)
+    ctx16.set_ntt_arith(0)
 
 
+@pytest.mark.parametrize("arith", [0, 1], ids=["fp64", "int"])
 @pytest.mark.parametrize("log_n", list(range(4, 16)))
-def test_ntt_all_degrees(log_n):
+def test_ntt_all_degrees(log_n, arith):
     require_gpu()
     from paper_2609_12378_amd import Context
-    say("ntt log_n", log_n)
+    say("ntt log_n", log_n, "arith", arith)
     ctx = Context(log_n, 3, 0, 1, q_bits=50)
+    ctx.set_ntt_arith(arith)
     ck = Ckks(log_n, ctx.q)
     a = uniform_residues(rng(2, 2, extra=log_n), ctx.q, ctx.n, lead=(5,))
     t = to_dev(a)
@@ -79,6 +84,24 @@ def test_ntt_sixty_bit_primes():
     assert np.array_equal(to_host(t), ck.ntt(a, [0, 1, 2]))
     ctx.intt(t)
     assert np.array_equal(to_host(t), a)
+
+
+def test_fp64_extreme_residues():
+    # residues 0, 1, q-1 and (q-1)/2 everywhere: the fp64 butterflies' range reductions at their edges
+    require_gpu()
+    from paper_2609_12378_amd import Context
+    ctx = Context(16, 2, 0, 1, q_bits=50)
+    ck = Ckks(16, ctx.q)
+    for fill in ("zero", "one", "max", "half"):
+        a = np.empty((2, ctx.n), dtype=np.uint64)
+        for r, q in enumerate(ctx.q):
+            a[r] = {"zero": 0, "one": 1, "max": q - 1, "half": (q - 1) // 2}[fill]
+        a[:, 1::3] = np.array(ctx.q, dtype=np.uint64)[:, None] - 1
+        t = to_dev(a)
+        ctx.ntt(t)
+        assert np.array_equal(to_host(t), ck.ntt(a, [0, 1])), fill
+        ctx.intt(t)
+        assert np.array_equal(to_host(t), a), fill
 
 
 def test_empty_batch_is_a_no_op(ctx16):

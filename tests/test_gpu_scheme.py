@@ -94,6 +94,28 @@ def test_encode_full_degree_at_projection_scale(big):
     eq(pt.data[0], big.ck.encode(re, None, scale, 13))
 
 
+def test_encode_integer_arithmetic(big):
+    # the same plaintexts through the integer Shoup butterflies
+    g = rng(4, 2, extra=9)
+    scale = float(big.ctx.q[12])
+    big.ctx.set_ntt_arith(1)
+    try:
+        for r in range(4):
+            re = np.repeat(g.normal(0, 0.02, 256), 128)
+            pt = big.ctx.encode(to_dev(re), None, scale, 13)
+            eq(pt.data[0], big.ck.encode(re, None, scale, 13))
+    finally:
+        big.ctx.set_ntt_arith(0)
+
+
+def test_encode_large_coefficients(toy):
+    # coefficients beyond 2^52 take the exact integer reduction inside the fp64 transform
+    re, im = toy.slots(99)
+    scale = float(2 ** 61)
+    pt = toy.ctx.encode(to_dev(re), to_dev(im), scale, 4)
+    eq(pt.data[0], toy.ck.encode(re, im, scale, 4))
+
+
 def test_encode_many_weight_vectors_full_degree(big):
     # 24 more weight-like vectors at scale q_12: each has tens of coefficients within one ulp
     # of a rounding tie, so any difference in twiddles or operation order shows up here
