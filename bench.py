@@ -28,11 +28,11 @@ if ROOT not in sys.path:
 
 METRIC = "rotations/s at N=2^16 (keyswitch) and s per 4096x14336 ct-pt projection"
 HBM_PEAK_GBS = 8000.0
-# 256 CUs x 64 lanes x 2.4 GHz of 32-bit integer VALU issue
-INT_LANE_OPS = 256 * 64 * 2.4e9
-# one 64-bit Shoup product on gfx950: 10 32-bit multiplies (v_mad_u64_u32 / v_mul_lo_u32 /
-# v_mul_hi_u32) plus 6 adds/subtracts; a butterfly adds 8 more for the lazy add/sub/correct
-OPS_PER_BUTTERFLY = 24
+# 256 CUs x 64 lanes x 2.4 GHz of VALU issue (fp64 FMA and 32-bit integer ops are full rate)
+LANE_OPS = 256 * 64 * 2.4e9
+# fp64 butterfly (primes < 2^50): product, FMA low part, quotient estimate and rint, FMA
+# remainder, add (6) + range reduction of the other input (3) + add/sub (2)
+OPS_PER_BUTTERFLY = 11
 
 
 def log(*a):
@@ -113,9 +113,9 @@ def roofline(prof, ntt_rows_per_launch=None):
         # butterflies of one pass: half a residue per stage, log2(256) = 8 stages per pass at N = 2^16
         residues = by / 16.0
         bfly_per_s = residues * 4.0 / (ms * 1e-3)
-        alu_frac = bfly_per_s * OPS_PER_BUTTERFLY / INT_LANE_OPS
-        out["alu"] = {"butterflies_per_s": bfly_per_s, "ops_per_butterfly": OPS_PER_BUTTERFLY,
-                      "peak_lane_ops_per_s": INT_LANE_OPS, "frac": alu_frac}
+        alu_frac = bfly_per_s * OPS_PER_BUTTERFLY / LANE_OPS
+        out["alu"] = {"arith": "fp64", "butterflies_per_s": bfly_per_s, "ops_per_butterfly": OPS_PER_BUTTERFLY,
+                      "peak_lane_ops_per_s": LANE_OPS, "frac": alu_frac}
     out.update({"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": gbs / HBM_PEAK_GBS})
     return out
 
@@ -252,6 +252,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-secondary", action="store_true")
+    ap.add_argument("--only", choices=["keyswitch", "ntt"], default=None,
+                    help="run only this secondary workload (for profiling); prints its JSON")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also run one plain device copy of this many MiB (for hardware-counter calibration)")
     args = ap.parse_args()
@@ -264,6 +266,12 @@ def main():
     from workloads import PROJECTION as cfg
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
+    if args.only == "keyswitch":
+        print(json.dumps(bench_keyswitch(torch, np, args.steps, args.warmup)), flush=True)
+        return
+    if args.only == "ntt":
+        print(json.dumps(bench_ntt(torch, args.steps)), flush=True)
+        return
     log("setup: projection 4096 -> 14336")
     st = setup_projection(torch, np, cfg)
     ctx = st["ctx"]

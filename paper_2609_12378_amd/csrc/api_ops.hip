@@ -2,6 +2,7 @@
 // Every call validates its arguments on the host before the first launch.
 #include <cmath>
 #include <cstring>
+#include <vector>
 
 #include "ckks_internal.h"
 #include "ops.h"
@@ -22,21 +23,23 @@ size_t words(const ckks_ctx *ctx, size_t rows) { return rows << ctx->log_n; }
 
 }  // namespace
 
-// rotations of one ciphertext sharing a single ModUp (used by the API and the projection).
-// work: ks_scratch_words(level) words
+// rotations of one ciphertext sharing a single ModUp (used by the API and the projection),
+// processed in batches of ks_rot_batch(count).  work: ks_scratch_words(level, ks_rot_batch(count)) words
 ckks_status rotate_core(ckks_ctx *ctx, const uint64_t *c, uint32_t level, const int32_t *steps,
                         const uint64_t *const *keys, uint32_t count, uint64_t *const *outs, uint64_t *work)
 {
+    if (!count) return CKKS_OK;
     const uint32_t L = level + 1, ext = L + ctx->n_p, nd = n_digits(ctx, level);
     const size_t N = ctx->n;
     uint64_t *digits = work;
-    uint64_t *u = digits + ((size_t)nd * ext + ctx->alpha) * N;
-    uint64_t *cw = u + 2 * (size_t)ext * N;
+    uint64_t *rw = digits + ((size_t)nd * ext + ctx->alpha) * N;
     CK_TRY(ks_modup(ctx, c + (size_t)L * N, level, digits));
-    for (uint32_t r = 0; r < count; r++) {
-        const uint32_t g = ckks_galois_elt(ctx, steps[r]);
-        CK_TRY(ks_inner_product(ctx, digits, nd, keys[r], level, g, u));
-        CK_TRY(ks_moddown(ctx, u, 2, level, c, g, nullptr, outs[r], cw));
+    const uint32_t bs = ks_rot_batch(count);
+    std::vector<uint32_t> g(count);
+    for (uint32_t r = 0; r < count; r++) g[r] = ckks_galois_elt(ctx, steps[r]);
+    for (uint32_t r0 = 0; r0 < count; r0 += bs) {
+        const uint32_t cnt = count - r0 < bs ? count - r0 : bs;
+        CK_TRY(ks_rotate_batch(ctx, c, level, digits, cnt, g.data() + r0, keys + r0, outs + r0, rw));
     }
     return CKKS_OK;
 }
@@ -245,7 +248,7 @@ ckks_status ckks_rotate_hoisted(ckks_ctx *ctx, const ckks_buf *in, const int32_t
     }
     const uint32_t level = in->n_limbs - 1;
     void *w;
-    CK_TRY(ctx_scratch(ctx, ks_scratch_words(ctx, level) * 8, &w));
+    CK_TRY(ctx_scratch(ctx, ks_scratch_words(ctx, level, ks_rot_batch(count)) * 8, &w));
     CK_TRY(rotate_core(ctx, in->data, level, steps, keys, count, op.data(), (uint64_t *)w));
     for (uint32_t r = 0; r < count; r++) outs[r].scale = in->scale;
     return CKKS_OK;
@@ -270,7 +273,7 @@ ckks_status ckks_mul_relin(ckks_ctx *ctx, const ckks_buf *a, const ckks_buf *b, 
     const uint32_t ext = L + ctx->n_p, nd = n_digits(ctx, level);
     const size_t N = ctx->n;
     void *w;
-    CK_TRY(ctx_scratch(ctx, (3 * (size_t)L * N + ks_scratch_words(ctx, level)) * 8, &w));
+    CK_TRY(ctx_scratch(ctx, (3 * (size_t)L * N + ks_scratch_words(ctx, level, 1)) * 8, &w));
     uint64_t *d0 = (uint64_t *)w, *d1 = d0 + L * N, *d2 = d1 + L * N;
     uint64_t *digits = d2 + L * N;
     uint64_t *u = digits + ((size_t)nd * ext + ctx->alpha) * N;

@@ -82,6 +82,7 @@ struct ckks_ctx {
     double2 *d_fft_w = nullptr;          // [N/4]  omega^-e, omega = exp(2 pi i/(N/2))
     double2 *d_fft_twist = nullptr;      // [N/2]  zeta^-k, zeta = exp(i pi / N)
     uint32_t *d_slot_pos = nullptr;      // [N/2]  bit-reversed FFT position of slot j
+    uint32_t *d_pos_slot = nullptr;      // [N/2]  slot index held at FFT position x (inverse of d_slot_pos)
     std::map<std::pair<int, int>, ConvDev> conv;  // (level, digit) ; digit -1 = ModDown
     ulonglong2 *d_pinv = nullptr;        // [n_q] (P^-1 mod q_i, Shoup)
     ulonglong2 *d_pmodq = nullptr;       // [n_q] ([P]_{q_i}, Shoup)

@@ -195,6 +195,9 @@ static ckks_status build_tables(ckks_ctx *c)
     CK_TRY(upload((void **)&c->d_fft_w, w.data(), w.size() * sizeof(double2)));
     CK_TRY(upload((void **)&c->d_fft_twist, twist.data(), twist.size() * sizeof(double2)));
     CK_TRY(upload((void **)&c->d_slot_pos, pos.data(), pos.size() * sizeof(uint32_t)));
+    std::vector<uint32_t> inv_pos(M);
+    for (uint32_t j = 0; j < M; j++) inv_pos[pos[j]] = j;
+    CK_TRY(upload((void **)&c->d_pos_slot, inv_pos.data(), inv_pos.size() * sizeof(uint32_t)));
 
     // P mod q_i, P^-1 mod q_i, q_l^-1 mod q_i
     std::vector<ulonglong2> pm(c->n_q), pinv(c->n_q), qlinv((size_t)c->n_q * c->n_q);
@@ -392,6 +395,7 @@ void ckks_ctx_destroy(ckks_ctx *c)
     (void)hipDeviceSynchronize();
     (void)prof_collect(c);
     void *ptrs[] = {c->d_mod, c->d_tw, c->d_itw, c->d_twf, c->d_itwf, c->d_fft_w, c->d_fft_twist, c->d_slot_pos,
+                    c->d_pos_slot,
                     c->d_pinv, c->d_pmodq, c->d_qlinv, c->scratch};
     for (void *p : ptrs)
         if (p) (void)hipFree(p);

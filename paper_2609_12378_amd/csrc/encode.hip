@@ -58,16 +58,6 @@ __device__ __forceinline__ double2 slot_value(const SlotSource &s, uint32_t p, u
     return make_double2(s.W[(size_t)(i * D + c) * s.d_out + (size_t)jb * D + o], 0.0);
 }
 
-// gather into bit-reversed FFT order: a[p][pos[j]] = z_j
-__global__ __launch_bounds__(kThreads) void k_gather(double2 *a, SlotSource s, const uint32_t *__restrict__ pos,
-                                                      uint32_t M)
-{
-    const uint32_t j = blockIdx.x * kThreads + threadIdx.x;
-    const uint32_t p = blockIdx.y;
-    if (j >= M) return;
-    a[(size_t)p * M + pos[j]] = slot_value(s, p, j, M);
-}
-
 __device__ __forceinline__ void round_out(int64_t *m, size_t base, uint32_t k, uint32_t M, double2 y, double2 tw,
                                           double c)
 {
@@ -77,17 +67,25 @@ __device__ __forceinline__ void round_out(int64_t *m, size_t base, uint32_t k, u
 }
 
 // Pass A: stages len = 2 .. 2^logb on contiguous blocks of 2^logb points.
+// Input: from `a` (bit-reversed order), or, when `gather` is set, straight from
+// the slot source through slot_of_pos (FFT position -> slot index).
 // mode 0: write complex back; mode 1: final pass, twist/round into m.
 __global__ __launch_bounds__(kThreads) void k_fft_a(double2 *a, const double2 *__restrict__ w, uint32_t logm,
                                                      uint32_t logb, int mode, const double2 *__restrict__ twist,
-                                                     double c, int64_t *m)
+                                                     double c, int64_t *m, int gather, SlotSource ss,
+                                                     const uint32_t *__restrict__ slot_of_pos)
 {
     extern __shared__ double2 sh[];
     const uint32_t M = 1u << logm, B = 1u << logb;
     const uint32_t blocks_per = M >> logb;
     const uint32_t p = blockIdx.x / blocks_per, blk = blockIdx.x % blocks_per;
     double2 *src = a + (size_t)p * M + (size_t)blk * B;
-    for (uint32_t x = threadIdx.x; x < B; x += kThreads) sh[x] = src[x];
+    if (gather) {
+        for (uint32_t x = threadIdx.x; x < B; x += kThreads)
+            sh[x] = slot_value(ss, p, slot_of_pos[(size_t)blk * B + x], M);
+    } else {
+        for (uint32_t x = threadIdx.x; x < B; x += kThreads) sh[x] = src[x];
+    }
     __syncthreads();
     for (uint32_t ls = 1; ls <= logb; ls++) {
         const uint32_t half = 1u << (ls - 1);
@@ -220,16 +218,23 @@ __global__ __launch_bounds__(kThreads) void k_decode_out(const double2 *y, const
 
 size_t enc_work_bytes(const ckks_ctx *ctx, uint32_t batch) { return (size_t)batch * (ctx->n / 2) * sizeof(double2); }
 
-ckks_status fft_passes(ckks_ctx *ctx, double2 *work, uint32_t batch, int mode, double c, int64_t *m)
+ckks_status fft_passes(ckks_ctx *ctx, double2 *work, uint32_t batch, int mode, double c, int64_t *m,
+                       const SlotSource *gather)
 {
     const uint32_t logm = ctx->log_n - 1, M = 1u << logm;
     const uint32_t logb = logm < (uint32_t)kLogBA ? logm : (uint32_t)kLogBA;
     const uint32_t B = 1u << logb;
     const bool single = logb == logm;
     const double bytes = 32.0 * batch * M;  // read and write every complex point (or its two integers)
-    prof_begin(ctx, K_FFT_A, bytes);
+    // with the gather fused, pass A reads the D distinct weights of each plaintext (or the explicit slots)
+    const double bytes_a = gather ? batch * (16.0 * M + (gather->W ? 8.0 * gather->feats
+                                                                    : (gather->im ? 16.0 : 8.0) * M))
+                                  : bytes;
+    SlotSource none;
+    prof_begin(ctx, K_FFT_A, bytes_a);
     hipLaunchKernelGGL(k_fft_a, dim3(batch * (M >> logb)), dim3(kThreads), B * sizeof(double2), ctx->stream, work,
-                       ctx->d_fft_w, logm, logb, single ? mode : 0, ctx->d_fft_twist, c, m);
+                       ctx->d_fft_w, logm, logb, single ? mode : 0, ctx->d_fft_twist, c, m, gather ? 1 : 0,
+                       gather ? *gather : none, ctx->d_pos_slot);
     prof_end(ctx, K_FFT_A);
     if (!single) {
         const uint32_t hb = logm - logb;
@@ -256,15 +261,7 @@ ckks_status enc_coeffs(ckks_ctx *ctx, const SlotSource &src, uint32_t batch, dou
                        int64_t *m_out)
 {
     if (!batch) return CKKS_OK;
-    const uint32_t M = ctx->n / 2;
-    // write every complex point; read the slots (W-generated: the D distinct weights of each plaintext)
-    const double reads = src.W ? 8.0 * src.feats : (src.im ? 16.0 : 8.0) * M;
-    prof_begin(ctx, K_GATHER, batch * (16.0 * M + reads));
-    hipLaunchKernelGGL(k_gather, dim3((M + kThreads - 1) / kThreads, batch), dim3(kThreads), 0, ctx->stream, work,
-                       src, ctx->d_slot_pos, M);
-    prof_end(ctx, K_GATHER);
-    HIP_TRY(hipGetLastError());
-    return fft_passes(ctx, work, batch, 1, scale * (2.0 / (double)ctx->n), m_out);
+    return fft_passes(ctx, work, batch, 1, scale * (2.0 / (double)ctx->n), m_out, &src);
 }
 
 ckks_status enc_to_rns(ckks_ctx *ctx, const int64_t *m, uint32_t batch, uint32_t limbs, uint64_t *out)
@@ -299,7 +296,7 @@ ckks_status dec_slots(ckks_ctx *ctx, const uint64_t *coef, uint32_t limbs, doubl
     hipLaunchKernelGGL(k_decode_in, grid, dim3(kThreads), 0, ctx->stream, work, coef, limbs > 1 ? 2u : 1u,
                        ctx->log_n, ctx->d_mod, ctx->d_fft_twist, 1.0 / scale, q0inv, q0inv_s);
     HIP_TRY(hipGetLastError());
-    CK_TRY(fft_passes(ctx, work, 1, 0, 0.0, nullptr));
+    CK_TRY(fft_passes(ctx, work, 1, 0, 0.0, nullptr, nullptr));
     hipLaunchKernelGGL(k_decode_out, grid, dim3(kThreads), 0, ctx->stream, work, ctx->d_slot_pos, ctx->log_n - 1, re,
                        im);
     HIP_TRY(hipGetLastError());

@@ -20,6 +20,7 @@
 namespace {
 
 constexpr int kThreads = 256;
+constexpr int kRotBatch = 32;  // rotations per batched launch
 
 __device__ __forceinline__ uint32_t auto_index(uint32_t j, uint32_t g, uint32_t log_n)
 {
@@ -36,7 +37,10 @@ struct ConvArgs {
 };
 
 // in: [polys][ns][N] (stride in_stride rows between polys), coefficient form;
-// out row for target ti: out + (poly*out_stride + (ti < split ? ti : ti + skip)) * N
+// out row for target ti: out + (poly*out_stride + (ti < split ? ti : ti + skip)) * N.
+// The ns + ns*nt Shoup constants and the target moduli are staged in LDS once per
+// block, so the per-target loop reads them at LDS latency instead of waiting on
+// scalar memory loads.
 template <int NS_MAX>
 __global__ __launch_bounds__(kThreads) void k_conv(const uint64_t *in, uint32_t in_stride, uint64_t *out,
                                                     uint32_t out_stride, uint32_t split, uint32_t skip, ConvArgs a,
@@ -44,6 +48,12 @@ __global__ __launch_bounds__(kThreads) void k_conv(const uint64_t *in, uint32_t 
                                                     const ulonglong2 *__restrict__ qhat_mod,
                                                     const ModQ *__restrict__ mods, uint32_t log_n)
 {
+    __shared__ ulonglong2 s_mod[NS_MAX * kMaxPrimes];
+    __shared__ uint64_t s_tq[kMaxPrimes];
+    const int ns = a.ns, nt = a.nt;
+    for (int k = threadIdx.x; k < ns * nt; k += kThreads) s_mod[k] = qhat_mod[k];
+    for (int k = threadIdx.x; k < nt; k += kThreads) s_tq[k] = mods[a.dst[k]].q;
+    __syncthreads();
     const uint32_t n = 1u << log_n;
     const uint32_t col = blockIdx.x * kThreads + threadIdx.x;
     const uint32_t poly = blockIdx.y;
@@ -52,20 +62,20 @@ __global__ __launch_bounds__(kThreads) void k_conv(const uint64_t *in, uint32_t 
     uint64_t y[NS_MAX];
 #pragma unroll
     for (int i = 0; i < NS_MAX; i++) {
-        if (i < a.ns) {
+        if (i < ns) {
             const uint64_t q = mods[a.src[i]].q;
             const ulonglong2 w = qhat_inv[i];
             y[i] = shoup(src[(size_t)i << log_n], w.x, w.y, q);
         }
     }
     uint64_t *dst = out + ((size_t)poly * out_stride << log_n) + col;
-    for (int t = 0; t < a.nt; t++) {
-        const uint64_t qt = mods[a.dst[t]].q, two = 2 * qt;
+    for (int t = 0; t < nt; t++) {
+        const uint64_t qt = s_tq[t], two = 2 * qt;
         uint64_t acc = 0;
 #pragma unroll
         for (int i = 0; i < NS_MAX; i++) {
-            if (i < a.ns) {
-                const ulonglong2 w = qhat_mod[i * a.nt + t];
+            if (i < ns) {
+                const ulonglong2 w = s_mod[i * nt + t];
                 acc = csub(acc + shoup_lazy(y[i], w.x, w.y, qt), two);
             }
         }
@@ -123,6 +133,61 @@ __global__ __launch_bounds__(kThreads) void k_moddown_finish(uint64_t *out, cons
     out[(((size_t)k * L + i) << log_n) + col] = r;
 }
 
+// Batched rotations (hoisting): rotation r of the batch uses Galois element
+// g[r], key key[r] and writes out[r].
+struct RotArgs {
+    uint32_t count;
+    uint32_t g[kRotBatch];
+    const uint64_t *key[kRotBatch];
+    uint64_t *out[kRotBatch];
+};
+
+// u[r][k][row][n] = sum_j d_j[row][sigma_{g_r}(n)] * key_r[j][k][krow][n]
+__global__ __launch_bounds__(kThreads) void k_key_ip_batch(const uint64_t *__restrict__ digits, RotArgs ra,
+                                                            uint64_t *u, uint32_t nd, uint32_t ext, uint32_t level,
+                                                            uint32_t n_q, uint32_t key_rows,
+                                                            const ModQ *__restrict__ mods, uint32_t log_n)
+{
+    const uint32_t n = 1u << log_n;
+    const uint32_t col = blockIdx.x * kThreads + threadIdx.x;
+    const uint32_t row = blockIdx.y, r = blockIdx.z;
+    if (col >= n) return;
+    const uint32_t prime = row <= level ? row : n_q + (row - level - 1);
+    const ModQ m = mods[prime];
+    const uint32_t sc = auto_index(col, ra.g[r], log_n);
+    const uint64_t *key = ra.key[r];
+    acc128 a0{0, 0}, a1{0, 0};
+    for (uint32_t j = 0; j < nd; j++) {
+        const uint64_t d = digits[(((size_t)j * ext + row) << log_n) + sc];
+        const size_t kb = ((size_t)j * 2 * key_rows + prime) << log_n;
+        mac(a0, d, key[kb + col]);
+        mac(a1, d, key[kb + ((size_t)key_rows << log_n) + col]);
+    }
+    uint64_t *ur = u + (((size_t)r * 2 * ext + row) << log_n) + col;
+    ur[0] = reduce128(a0, m);
+    ur[(size_t)ext << log_n] = reduce128(a1, m);
+}
+
+// out_r[k][i][n] = (u[r][k][i][n] - c[r][k][i][n]) * P^-1 (+ c0[i][sigma_{g_r}(n)] for k = 0)
+__global__ __launch_bounds__(kThreads) void k_moddown_finish_batch(RotArgs ra, const uint64_t *u, const uint64_t *c,
+                                                                    const uint64_t *c0, uint32_t ext, uint32_t level,
+                                                                    const ulonglong2 *__restrict__ pinv,
+                                                                    const ModQ *__restrict__ mods, uint32_t log_n)
+{
+    const uint32_t n = 1u << log_n;
+    const uint32_t col = blockIdx.x * kThreads + threadIdx.x;
+    const uint32_t i = blockIdx.y, rk = blockIdx.z, r = rk >> 1, k = rk & 1;
+    if (col >= n) return;
+    const uint32_t L = level + 1;
+    const uint64_t q = mods[i].q;
+    const uint64_t x = u[(((size_t)rk * ext + i) << log_n) + col];
+    const uint64_t cv = c[(((size_t)rk * L + i) << log_n) + col];
+    const ulonglong2 w = pinv[i];
+    uint64_t res = shoup(submod(x, cv, q), w.x, w.y, q);
+    if (k == 0) res = addmod(res, c0[((size_t)i << log_n) + auto_index(col, ra.g[r], log_n)], q);
+    ra.out[r][(((size_t)k * L + i) << log_n) + col] = res;
+}
+
 ckks_status launch_conv(ckks_ctx *ctx, const ConvDev *cd, const uint64_t *in, uint32_t in_stride, uint64_t *out,
                         uint32_t out_stride, uint32_t split, uint32_t skip, uint32_t polys)
 {
@@ -142,9 +207,13 @@ ckks_status launch_conv(ckks_ctx *ctx, const ConvDev *cd, const uint64_t *in, ui
     else if (a.ns <= 16)
         hipLaunchKernelGGL(k_conv<16>, grid, block, 0, ctx->stream, in, in_stride, out, out_stride, split, skip, a,
                            cd->d_qhat_inv, cd->d_qhat_mod, ctx->d_mod, ctx->log_n);
-    else
-        hipLaunchKernelGGL(k_conv<kMaxPrimes>, grid, block, 0, ctx->stream, in, in_stride, out, out_stride, split,
-                           skip, a, cd->d_qhat_inv, cd->d_qhat_mod, ctx->d_mod, ctx->log_n);
+    else if (a.ns <= 32)
+        hipLaunchKernelGGL(k_conv<32>, grid, block, 0, ctx->stream, in, in_stride, out, out_stride, split, skip, a,
+                           cd->d_qhat_inv, cd->d_qhat_mod, ctx->d_mod, ctx->log_n);
+    else {
+        prof_end(ctx, K_CONV);
+        return set_error(CKKS_EUNSUPPORTED, "basis conversion from %d limbs (at most 32)", a.ns);
+    }
     prof_end(ctx, K_CONV);
     HIP_TRY(hipGetLastError());
     return CKKS_OK;
@@ -152,12 +221,55 @@ ckks_status launch_conv(ckks_ctx *ctx, const ConvDev *cd, const uint64_t *in, ui
 
 }  // namespace
 
-size_t ks_scratch_words(const ckks_ctx *ctx, uint32_t level)
+uint32_t ks_rot_batch(uint32_t count) { return count < (uint32_t)kRotBatch ? count : (uint32_t)kRotBatch; }
+
+size_t ks_scratch_words(const ckks_ctx *ctx, uint32_t level, uint32_t batch)
 {
     const size_t ext = level + 1 + ctx->n_p;
     const size_t nd = n_digits(ctx, level);
-    // digits + u[2][ext] + conv out [2][level+1] + INTT staging [alpha]
-    return ((nd * ext) + 2 * ext + 2 * (level + 1) + ctx->alpha) << ctx->log_n;
+    if (batch < 1) batch = 1;
+    // digits + INTT staging [alpha] + per rotation: u[2][ext] and the converted rows [2][level+1]
+    return ((nd * ext) + ctx->alpha + (size_t)batch * (2 * ext + 2 * (level + 1))) << ctx->log_n;
+}
+
+ckks_status ks_rotate_batch(ckks_ctx *ctx, const uint64_t *c, uint32_t level, const uint64_t *digits,
+                            uint32_t count, const uint32_t *g, const uint64_t *const *keys, uint64_t *const *outs,
+                            uint64_t *work)
+{
+    CK_REQUIRE(count >= 1 && count <= (uint32_t)kRotBatch, CKKS_EINVAL, "rotation batch of %u", count);
+    const uint32_t L = level + 1, K = ctx->n_p, ext = L + K, nd = n_digits(ctx, level);
+    const size_t N = ctx->n;
+    RotArgs ra{};
+    ra.count = count;
+    for (uint32_t r = 0; r < count; r++) {
+        ra.g[r] = g[r];
+        ra.key[r] = keys[r];
+        ra.out[r] = outs[r];
+    }
+    uint64_t *u = work;                              // [count][2][ext][N]
+    uint64_t *cw = u + (size_t)count * 2 * ext * N;  // [count][2][L][N]
+    {
+        const dim3 grid((ctx->n + kThreads - 1) / kThreads, ext, count), block(kThreads);
+        prof_begin(ctx, K_KEYIP, 8.0 * ctx->n * ext * (count * (2.0 * nd + 2.0) + nd));
+        hipLaunchKernelGGL(k_key_ip_batch, grid, block, 0, ctx->stream, digits, ra, u, nd, ext, level, ctx->n_q,
+                           ctx->n_primes(), ctx->d_mod, ctx->log_n);
+        prof_end(ctx, K_KEYIP);
+        HIP_TRY(hipGetLastError());
+    }
+    CK_TRY(launch_ntt_strided(ctx, u + (size_t)L * N, 2 * count, ext, limb_range(ctx->n_q, K), true));
+    const ConvDev *cd;
+    CK_TRY(ctx_conv(ctx, (int)level, -1, &cd));
+    CK_TRY(launch_conv(ctx, cd, u + (size_t)L * N, ext, cw, L, L, 0, 2 * count));
+    CK_TRY(launch_ntt(ctx, cw, 2 * count * L, limb_range(0, L), false));
+    {
+        const dim3 grid((ctx->n + kThreads - 1) / kThreads, L, 2 * count), block(kThreads);
+        prof_begin(ctx, K_MODDOWN, 8.0 * ctx->n * L * count * 7.0);
+        hipLaunchKernelGGL(k_moddown_finish_batch, grid, block, 0, ctx->stream, ra, u, cw, c, ext, level,
+                           ctx->d_pinv, ctx->d_mod, ctx->log_n);
+        prof_end(ctx, K_MODDOWN);
+        HIP_TRY(hipGetLastError());
+    }
+    return CKKS_OK;
 }
 
 ckks_status ks_modup(ckks_ctx *ctx, const uint64_t *c, uint32_t level, uint64_t *digits)

@@ -35,8 +35,16 @@ ckks_status ks_inner_product(ckks_ctx *ctx, const uint64_t *digits, uint32_t nd,
 // out: [polys][level+1][N]; work: [polys][level+1][N]
 ckks_status ks_moddown(ckks_ctx *ctx, uint64_t *u, uint32_t polys, uint32_t level, const uint64_t *add0,
                        uint32_t add0_g, const uint64_t *add1, uint64_t *out, uint64_t *work);
-// scratch words needed by ks_rotate_core for one rotation batch
-size_t ks_scratch_words(const ckks_ctx *ctx, uint32_t level);
+// scratch words for rotations at `level` processed `batch` at a time (see rotate_core)
+size_t ks_scratch_words(const ckks_ctx *ctx, uint32_t level, uint32_t batch);
+// rotations per batched launch for `count` requested rotations
+uint32_t ks_rot_batch(uint32_t count);
+// `count` (<= 32) rotations of ciphertext c sharing the ModUp digits: key inner product with the
+// automorphism g[r], ModDown and the sigma_{g_r}(c0) addition, each stage one launch for all r.
+// work: count * (2 ext + 2 (level+1)) N words
+ckks_status ks_rotate_batch(ckks_ctx *ctx, const uint64_t *c, uint32_t level, const uint64_t *digits,
+                            uint32_t count, const uint32_t *g, const uint64_t *const *keys, uint64_t *const *outs,
+                            uint64_t *work);
 
 // encoding (encode.hip)
 struct SlotSource {

@@ -9,15 +9,15 @@
 // Schedule on the GPU:
 //  1. hoisted baby-step rotations: one ModUp per input ciphertext, n1 - 1
 //     key switches each, into xrot[i][b] (b = 0 is a copy of x_i);
-//  2. for a tile of J output blocks and one giant step g, the weight
+//  2. for a tile of J = 8 output blocks and one giant step g, the weight
 //     plaintexts of a sub-batch of (i, b) pairs are encoded on the fly from W
-//     (gather -> fp64 FFT -> round -> RNS -> NTT) and immediately consumed by
-//     the multiply-accumulate kernel, which loads each xrot residue once for
-//     all J output blocks and accumulates exactly in 128 bits;
+//     (slot generation fused into the fp64 FFT -> round -> NTT column pass with
+//     the RNS reduction fused in -> NTT row pass) and consumed by the
+//     multiply-accumulate kernel, which loads each xrot residue once for all J
+//     output blocks and accumulates exactly in 128 bits;
 //  3. giant-step rotation of each partial sum at level l, summation, rescale.
 // The plaintext scale is q_l, so the rescale returns the input scale exactly.
 #include <algorithm>
-#include <cstdlib>
 #include <cstring>
 #include <vector>
 
@@ -156,17 +156,16 @@ extern "C" ckks_status ckks_linear_project(ckks_ctx *ctx, const ckks_buf *in, co
     // ---- scratch layout
     const size_t N = ctx->n, ctw = 2 * (size_t)L * N;
     const uint32_t maxpairs = n_in * n1;
-    size_t budget = size_t(1) << 31;
-    uint32_t Jt = kJ;
-    if (const char *e = getenv("CKKS_PROJ_BATCH_MIB")) budget = (size_t)atol(e) << 20;
-    if (const char *e = getenv("CKKS_PROJ_J")) Jt = std::max<uint32_t>(1, std::min<uint32_t>(kJ, (uint32_t)atoi(e)));
+    // plaintext sub-batch of at most 2 GiB: J output blocks x Pb (i, b) pairs
+    const size_t budget = size_t(1) << 31;
+    const uint32_t Jt = kJ;
     const uint32_t Pb = std::min<uint32_t>(maxpairs, std::max<uint32_t>(1, (uint32_t)(budget / ((size_t)Jt * L * N * 8))));
     const size_t xrot_w = (size_t)n_in * n1 * ctw;
     const size_t acc_w = (size_t)kJ * ctw, tot_w = (size_t)kJ * ctw, rot_w = ctw;
-    const size_t pt_w = (size_t)kJ * Pb * L * N;
-    const size_t m_w = (size_t)kJ * Pb * N;                       // int64 coefficients
-    const size_t fft_w = (size_t)kJ * Pb * (N / 2) * 2;            // double2 per slot
-    const size_t ks_w = ks_scratch_words(ctx, level);
+    const size_t pt_w = (size_t)Jt * Pb * L * N;
+    const size_t m_w = (size_t)Jt * Pb * N;                       // int64 coefficients
+    const size_t fft_w = (size_t)Jt * Pb * (N / 2) * 2;            // double2 per slot
+    const size_t ks_w = ks_scratch_words(ctx, level, ks_rot_batch(n1 > 1 ? n1 - 1 : 1));
     const size_t total = xrot_w + acc_w + tot_w + rot_w + pt_w + m_w + fft_w + ks_w;
     void *w;
     CK_TRY(ctx_scratch(ctx, total * 8, &w));
