@@ -30,9 +30,6 @@ METRIC = "rotations/s at N=2^16 (keyswitch) and s per 4096x14336 ct-pt projectio
 HBM_PEAK_GBS = 8000.0
 # 256 CUs x 64 lanes x 2.4 GHz of VALU issue (fp64 FMA and 32-bit integer ops are full rate)
 LANE_OPS = 256 * 64 * 2.4e9
-# fp64 butterfly (primes < 2^50): product, FMA low part, quotient estimate and rint, FMA
-# remainder, add (6) + range reduction of the other input (3) + add/sub (2)
-OPS_PER_BUTTERFLY = 11
 
 
 def log(*a):
@@ -103,38 +100,66 @@ def check_projection(np, st, outs, blocks=(0, 27, 55)):
     return max(errs) if errs else None
 
 
-def roofline(prof, ntt_rows_per_launch=None):
-    """Pick the kernel with the most total time; report its achieved rate against HBM and ALU peaks."""
-    name, (ms, cnt, by) = max(prof.items(), key=lambda kv: kv[1][0])
-    avg_ms = ms / cnt
-    gbs = by / (ms * 1e-3) / 1e9
-    out = {"kernel": name, "launches": cnt, "avg_ms": avg_ms, "bytes_per_launch": by / cnt}
-    if name.startswith("ntt_"):
-        # butterflies of one pass: half a residue per stage, log2(256) = 8 stages per pass at N = 2^16
-        residues = by / 16.0
-        bfly_per_s = residues * 4.0 / (ms * 1e-3)
-        alu_frac = bfly_per_s * OPS_PER_BUTTERFLY / LANE_OPS
-        out["alu"] = {"arith": "fp64", "butterflies_per_s": bfly_per_s, "ops_per_butterfly": OPS_PER_BUTTERFLY,
-                      "peak_lane_ops_per_s": LANE_OPS, "frac": alu_frac}
-    out.update({"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": gbs / HBM_PEAK_GBS})
+def roofline(prof):
+    """The kernel with the most total time, against the HBM roof and the VALU issue roof.
+
+    HBM: algorithmic bytes per launch / average launch time vs 8 TB/s.  VALU: the kernel's nominal lane
+    instructions (its arithmetic model, reported by the library) per second vs 256 CUs x 64 lanes x 2.4 GHz
+    (fp64 FMA and 32-bit integer instructions issue at full rate).  "bound" names the roof the kernel is
+    nearer to; the top-level achieved/peak/frac are for that roof.
+    """
+    name, (ms, cnt, by, ops) = max(prof.items(), key=lambda kv: kv[1][0])
+    sec = ms * 1e-3
+    gbs = by / sec / 1e9
+    hbm = {"achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": gbs / HBM_PEAK_GBS}
+    out = {"kernel": name, "launches": cnt, "avg_ms": ms / cnt, "bytes_per_launch": by / cnt}
+    alu = None
+    if ops:
+        gops = ops / sec / 1e9
+        alu = {"achieved": gops, "peak": LANE_OPS / 1e9, "unit": "G VALU lane-instr/s", "frac": gops * 1e9 / LANE_OPS,
+               "instr_per_launch": ops / cnt}
+    bound = "alu" if alu and alu["frac"] > hbm["frac"] else "hbm"
+    out["bound"] = bound
+    out.update(alu if bound == "alu" else hbm)
+    out["hbm"] = hbm
+    if alu:
+        out["alu"] = alu
     return out
 
 
-def load_traffic(kernel):
-    """HBM bytes per launch measured by rocprofv3 counters, if recorded for the current source."""
-    path = os.path.join(ROOT, "profiles", "pmc_traffic.md")
-    if not os.path.exists(path):
+# sources whose text determines a kernel's memory traffic; a recorded counter value applies only while
+# their hash is unchanged
+KERNEL_SOURCES = {
+    "ntt_row_mac": ["project.hip", "ntt_core.h", "modarith.h", "ckks_internal.h"],
+    "ntt_fwd_col": ["ntt.hip", "ntt_core.h", "modarith.h", "ckks_internal.h"],
+}
+
+
+def sources_sha(kernel):
+    names = KERNEL_SOURCES.get(kernel)
+    if not names:
         return None
-    srcs = sorted(os.listdir(os.path.join(ROOT, "paper_2609_12378_amd", "csrc")))
     h = hashlib.sha256()
-    for f in srcs:
+    for f in names:
         with open(os.path.join(ROOT, "paper_2609_12378_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
-    sha = h.hexdigest()[:16]
+    return h.hexdigest()[:16]
+
+
+def load_traffic(kernel):
+    """HBM bytes per launch measured with rocprofv3 FETCH_SIZE + WRITE_SIZE (copy-calibrated), if recorded
+    in profiles/pmc_traffic.md for the current text of the kernel's sources; else None."""
+    path = os.path.join(ROOT, "profiles", "pmc_traffic.md")
+    sha = sources_sha(kernel)
+    if sha is None or not os.path.exists(path):
+        return None
     for line in open(path):
-        m = re.match(r"\|\s*(\S+)\s*\|\s*([0-9a-f]{16})\s*\|\s*([0-9.eE+]+)\s*\|", line)
-        if m and m.group(1) == kernel and m.group(2) == sha:
-            return float(m.group(3))
+        cells = [c.strip() for c in line.strip().strip("|").split("|")]
+        if len(cells) >= 6 and cells[0] == kernel and cells[2] == sha:
+            try:
+                return float(cells[5])
+            except ValueError:
+                return None
     return None
 
 
@@ -204,6 +229,40 @@ def bench_ntt(torch, steps):
     return res
 
 
+def bench_tile(torch, np, steps, warmup, calib_mib):
+    """One output tile of the projection: 4096 -> 14 x 256 features, the same launches as the full one.
+
+    A smaller process for hardware-counter passes; per-launch figures of its kernels apply to the full
+    projection, whose launches have the same shapes.
+    """
+    import dataclasses
+    from workloads import PROJECTION
+    cfg = dataclasses.replace(PROJECTION, d_out=14 * PROJECTION.feats)
+    st = setup_projection(torch, np, cfg)
+    ctx = st["ctx"]
+    if calib_mib:
+        src = torch.ones(calib_mib << 17, dtype=torch.uint64, device="cuda")
+        dst = torch.empty_like(src)
+        ctx.calib_copy(dst, src)
+        torch.cuda.synchronize()
+        del src, dst
+    outs = None
+    for _ in range(warmup):
+        outs = ctx.linear_project(st["cts"], st["Wd"], st["T"], st["n1"], st["keys"], outs)
+    ctx.profile(True)
+    ctx.profile_reset()
+    with Timer(torch) as t:
+        for _ in range(steps):
+            outs = ctx.linear_project(st["cts"], st["Wd"], st["T"], st["n1"], st["keys"], outs)
+    prof = ctx.profile_all()
+    ctx.profile(False)
+    err = check_projection(np, st, outs, blocks=(0, 13))
+    return {"workload": "projection 4096x3584 (one tile of 14 output ciphertexts of the 4096x14336 projection)",
+            "ms_per_step": t.ms / steps, "decrypt_max_abs_err": err,
+            "kernels": {k: {"launches": v[1] / steps, "avg_ms": v[0] / v[1], "bytes_per_launch": v[2] / v[1],
+                            "GBps": v[2] / (v[0] * 1e-3) / 1e9} for k, v in prof.items()}}
+
+
 def cpu_baseline(np, cfg, budget_s=20.0):
     """The oracle on a bounded sample of the projection, extrapolated to one full projection."""
     from oracle import Ckks, gen_primes
@@ -252,7 +311,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-secondary", action="store_true")
-    ap.add_argument("--only", choices=["keyswitch", "ntt"], default=None,
+    ap.add_argument("--only", choices=["keyswitch", "ntt", "tile"], default=None,
                     help="run only this secondary workload (for profiling); prints its JSON")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also run one plain device copy of this many MiB (for hardware-counter calibration)")
@@ -271,6 +330,9 @@ def main():
         return
     if args.only == "ntt":
         print(json.dumps(bench_ntt(torch, args.steps)), flush=True)
+        return
+    if args.only == "tile":
+        print(json.dumps(bench_tile(torch, np, args.steps, args.warmup, args.calib_copy_mib)), flush=True)
         return
     log("setup: projection 4096 -> 14336")
     st = setup_projection(torch, np, cfg)

@@ -93,6 +93,11 @@ ckks_status ckks_ctx_set_stream(ckks_ctx *ctx, void *hip_stream);
  * otherwise; mode 1: integer Shoup butterflies everywhere.  Both produce
  * identical canonical residues. */
 ckks_status ckks_ctx_set_ntt_arith(ckks_ctx *ctx, int mode);
+/* Upper bound on the (input ciphertext, baby step) pairs whose weight
+ * plaintexts ckks_linear_project encodes and accumulates per launch (0, the
+ * default: as many as fit a 2 GiB staging buffer).  Smaller values use less
+ * scratch memory and more launches; results are identical for every value. */
+ckks_status ckks_ctx_set_proj_batch(ckks_ctx *ctx, uint32_t max_pairs);
 /* Host copies of the primes q (n_q), p (n_p) and psi (n_q + n_p, q first);
  * any pointer may be NULL. */
 ckks_status ckks_ctx_primes(const ckks_ctx *ctx, uint64_t *q, uint64_t *p, uint64_t *psi);
@@ -207,13 +212,16 @@ ckks_status ckks_linear_project(ckks_ctx *ctx, const ckks_buf *in, const double 
 /* Per-kernel timing with HIP events on the context stream.  While enabled,
  * every kernel launch is bracketed by two events and tagged with its
  * algorithmic HBM bytes (each input and output word once; cache-resident
- * tables excluded).  ckks_profile_read synchronizes and returns, for the
- * kernel named `kernel`, the summed milliseconds, launch count and bytes
- * (any output pointer may be NULL).  ckks_profile_name(i) enumerates the
- * kernel names (NULL past the last). */
+ * tables excluded) and its nominal VALU lane instructions (the kernel's
+ * arithmetic model: 11 per fp64 butterfly, 37 per integer one, plus the
+ * stated extra work; 0 where no model is given).  ckks_profile_read
+ * synchronizes and returns, for the kernel named `kernel`, the summed
+ * milliseconds, launch count, bytes and VALU instructions (any output pointer
+ * may be NULL).  ckks_profile_name(i) enumerates the kernel names (NULL past
+ * the last). */
 ckks_status ckks_profile_enable(ckks_ctx *ctx, int on);
 ckks_status ckks_profile_read(ckks_ctx *ctx, const char *kernel, double *total_ms, uint64_t *launches,
-                              double *bytes);
+                              double *bytes, double *valu_ops);
 ckks_status ckks_profile_reset(ckks_ctx *ctx);
 const char *ckks_profile_name(int i);
 /* A plain device copy of `bytes` bytes (multiple of 16) on the context stream,

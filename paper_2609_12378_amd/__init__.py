@@ -52,6 +52,7 @@ _SIGS = {
     "ckks_ctx_destroy": (None, [_VP]),
     "ckks_ctx_set_stream": (ctypes.c_int, [_VP, _VP]),
     "ckks_ctx_set_ntt_arith": (ctypes.c_int, [_VP, ctypes.c_int]),
+    "ckks_ctx_set_proj_batch": (ctypes.c_int, [_VP, _U32]),
     "ckks_ctx_primes": (ctypes.c_int, [_VP, _VP, _VP, _VP]),
     "ckks_galois_elt": (_U32, [_VP, _I32]),
     "ckks_last_error": (ctypes.c_char_p, []),
@@ -75,7 +76,7 @@ _SIGS = {
     "ckks_linear_project": (ctypes.c_int, [_VP, _BP, _VP, ctypes.POINTER(_ProjShape), _VP, _VP, _U32, _BP]),
     "ckks_profile_enable": (ctypes.c_int, [_VP, ctypes.c_int]),
     "ckks_profile_read": (ctypes.c_int, [_VP, ctypes.c_char_p, ctypes.POINTER(_DBL), ctypes.POINTER(_U64),
-                                         ctypes.POINTER(_DBL)]),
+                                         ctypes.POINTER(_DBL), ctypes.POINTER(_DBL)]),
     "ckks_profile_name": (ctypes.c_char_p, [ctypes.c_int]),
     "ckks_profile_reset": (ctypes.c_int, [_VP]),
     "ckks_calib_copy": (ctypes.c_int, [_VP, _VP, _VP, _SZ]),
@@ -190,6 +191,10 @@ class Context:
     def set_ntt_arith(self, mode: int):
         """0: fp64 butterflies where every prime is below 2^50 (default); 1: integer Shoup everywhere."""
         _check(self.lib.ckks_ctx_set_ntt_arith(self.h, mode), "ckks_ctx_set_ntt_arith")
+
+    def set_proj_batch(self, max_pairs: int):
+        """Cap the (input, baby step) pairs per projection launch (0 = by the 2 GiB staging budget)."""
+        _check(self.lib.ckks_ctx_set_proj_batch(self.h, max_pairs), "ckks_ctx_set_proj_batch")
 
     def galois_elt(self, steps: int) -> int:
         return int(self.lib.ckks_galois_elt(self.h, steps))
@@ -344,14 +349,14 @@ class Context:
         _check(self.lib.ckks_profile_reset(self.h), "ckks_profile_reset")
 
     def profile_read(self, kernel: str):
-        """(total ms, launches, algorithmic bytes) of one kernel since the last reset."""
-        ms, cnt, by = ctypes.c_double(), ctypes.c_uint64(), ctypes.c_double()
+        """(total ms, launches, algorithmic bytes, nominal VALU instructions) of one kernel since the last reset."""
+        ms, cnt, by, ops = ctypes.c_double(), ctypes.c_uint64(), ctypes.c_double(), ctypes.c_double()
         _check(self.lib.ckks_profile_read(self.h, kernel.encode(), ctypes.byref(ms), ctypes.byref(cnt),
-                                          ctypes.byref(by)), "ckks_profile_read")
-        return ms.value, cnt.value, by.value
+                                          ctypes.byref(by), ctypes.byref(ops)), "ckks_profile_read")
+        return ms.value, cnt.value, by.value, ops.value
 
     def profile_all(self):
-        """{kernel: (total ms, launches, algorithmic bytes)} for every kernel that ran."""
+        """{kernel: (total ms, launches, algorithmic bytes, VALU instructions)} for every kernel that ran."""
         out, i = {}, 0
         while True:
             name = self.lib.ckks_profile_name(i)

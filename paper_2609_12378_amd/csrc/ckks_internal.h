@@ -60,7 +60,7 @@ struct ConvDev {
 // and constant tables, which stay cache-resident, are not counted).
 enum KClass {
     K_NTT_FWD_COL = 0, K_NTT_FWD_ROW, K_NTT_INV_ROW, K_NTT_INV_COL, K_FFT_A, K_FFT_B, K_GATHER, K_TO_RNS,
-    K_MAC, K_KEYIP, K_CONV, K_MODDOWN, K_ELEM, K_NCLASS
+    K_MAC, K_KEYIP, K_CONV, K_MODDOWN, K_ELEM, K_ROW_MAC, K_NCLASS
 };
 extern const char *const kKClassNames[K_NCLASS];
 
@@ -79,6 +79,7 @@ struct ckks_ctx {
     double *d_itwf = nullptr;            // [n_primes][N] psi^-brev(k) as doubles
     bool f64_ok[kMaxPrimes] = {};        // q < 2^50: the fp64 butterflies are exact
     bool int_only = false;               // force the integer Shoup butterflies
+    uint32_t proj_max_pairs = 0;         // projection sub-batch limit (0 = by the staging budget)
     double2 *d_fft_w = nullptr;          // [N/4]  omega^-e, omega = exp(2 pi i/(N/2))
     double2 *d_fft_twist = nullptr;      // [N/2]  zeta^-k, zeta = exp(i pi / N)
     uint32_t *d_slot_pos = nullptr;      // [N/2]  bit-reversed FFT position of slot j
@@ -96,11 +97,12 @@ struct ckks_ctx {
     bool profiling = false;
     struct ProfRec {
         hipEvent_t a, b;
-        double bytes;
+        double bytes, ops;
     };
     std::vector<ProfRec> prof_events[K_NCLASS];
     double prof_ms[K_NCLASS] = {0};
     double prof_bytes[K_NCLASS] = {0};
+    double prof_ops[K_NCLASS] = {0};
     uint64_t prof_count[K_NCLASS] = {0};
 
     uint32_t n_primes() const { return n_q + n_p; }
@@ -110,8 +112,9 @@ struct ckks_ctx {
 ckks_status ctx_scratch(ckks_ctx *ctx, size_t bytes, void **out);
 
 // profiler brackets: call prof_begin before a launch and prof_end after;
-// bytes = the launch's algorithmic HBM bytes
-void prof_begin(ckks_ctx *ctx, KClass k, double bytes);
+// bytes = the launch's algorithmic HBM bytes, ops = its nominal VALU lane
+// instructions (the arithmetic model of the kernel; 0 where none is stated)
+void prof_begin(ckks_ctx *ctx, KClass k, double bytes, double ops = 0.0);
 void prof_end(ckks_ctx *ctx, KClass k);
 
 // basis-conversion tables for ModUp of digit j at `level` (dst = other q-limbs
@@ -138,6 +141,16 @@ ckks_status launch_ntt_strided(ckks_ctx *ctx, uint64_t *data, uint32_t batch, ui
                                bool inverse);
 // forward NTT of signed coefficient rows m[batch][N] into out[batch][limbs][N] (primes 0..limbs-1)
 ckks_status launch_ntt_from_i64(ckks_ctx *ctx, const int64_t *m, uint64_t *out, uint32_t batch, uint32_t limbs);
+// split of log_n into the column pass (s1 stages, 0 = single pass) and the row pass (s2 stages)
+void ntt_split(uint32_t log_n, int *s1, int *s2);
+// the transforms over primes 0..limbs-1 use the fp64 butterflies
+bool ntt_uses_f64(const ckks_ctx *ctx, uint32_t limbs);
+// column pass only of launch_ntt_from_i64 (two-pass sizes); the rows stay in the inter-pass form
+ckks_status launch_ntt_col_i64(ckks_ctx *ctx, const int64_t *m, uint64_t *out, uint32_t batch, uint32_t limbs);
+// nominal VALU instructions of one radix-2 butterfly: fp64 (product with FMA
+// error term, quotient estimate and rint, remainder, range reduction of the
+// other input, add and subtract) and 64-bit integer Shoup (from the gfx950 ISA)
+constexpr double kOpsButterflyF64 = 11.0, kOpsButterflyInt = 37.0;
 // identity map for a contiguous range of prime indices
 LimbMap limb_range(uint32_t first, uint32_t count);
 

@@ -31,7 +31,7 @@ extern "C" const char *ckks_last_error(void) { return g_err; }
 
 const char *const kKClassNames[K_NCLASS] = {"ntt_fwd_col", "ntt_fwd_row", "ntt_inv_row", "ntt_inv_col", "fft_a",
                                             "fft_b",       "gather",      "to_rns",      "mac",         "key_ip",
-                                            "conv",        "moddown",     "elementwise"};
+                                            "conv",        "moddown",     "elementwise", "ntt_row_mac"};
 
 // --------------------------------------------------------------- host math --
 namespace hm {
@@ -291,7 +291,7 @@ ckks_status ctx_scratch(ckks_ctx *c, size_t bytes, void **out)
     return CKKS_OK;
 }
 
-void prof_begin(ckks_ctx *c, KClass k, double bytes)
+void prof_begin(ckks_ctx *c, KClass k, double bytes, double ops)
 {
     if (!c->profiling) return;
     hipEvent_t a, b;
@@ -301,7 +301,7 @@ void prof_begin(ckks_ctx *c, KClass k, double bytes)
         return;
     }
     (void)hipEventRecord(a, c->stream);
-    c->prof_events[k].push_back({a, b, bytes});
+    c->prof_events[k].push_back({a, b, bytes, ops});
 }
 void prof_end(ckks_ctx *c, KClass k)
 {
@@ -318,6 +318,7 @@ static ckks_status prof_collect(ckks_ctx *c)
             HIP_TRY(hipEventElapsedTime(&ms, ev.a, ev.b));
             c->prof_ms[k] += ms;
             c->prof_bytes[k] += ev.bytes;
+            c->prof_ops[k] += ev.ops;
             c->prof_count[k]++;
             (void)hipEventDestroy(ev.a);
             (void)hipEventDestroy(ev.b);
@@ -423,6 +424,14 @@ ckks_status ckks_ctx_set_ntt_arith(ckks_ctx *c, int mode)
     return CKKS_OK;
 }
 
+ckks_status ckks_ctx_set_proj_batch(ckks_ctx *c, uint32_t max_pairs)
+{
+    clear_error();
+    CK_REQUIRE(c, CKKS_EINVAL, "null context");
+    c->proj_max_pairs = max_pairs;
+    return CKKS_OK;
+}
+
 ckks_status ckks_ctx_primes(const ckks_ctx *c, uint64_t *q, uint64_t *p, uint64_t *psi)
 {
     clear_error();
@@ -456,11 +465,13 @@ ckks_status ckks_profile_reset(ckks_ctx *c)
     for (int k = 0; k < K_NCLASS; k++) {
         c->prof_ms[k] = 0;
         c->prof_bytes[k] = 0;
+        c->prof_ops[k] = 0;
         c->prof_count[k] = 0;
     }
     return CKKS_OK;
 }
-ckks_status ckks_profile_read(ckks_ctx *c, const char *cls, double *total_ms, uint64_t *launches, double *bytes)
+ckks_status ckks_profile_read(ckks_ctx *c, const char *cls, double *total_ms, uint64_t *launches, double *bytes,
+                              double *valu_ops)
 {
     clear_error();
     CK_REQUIRE(c && cls, CKKS_EINVAL, "null argument");
@@ -470,6 +481,7 @@ ckks_status ckks_profile_read(ckks_ctx *c, const char *cls, double *total_ms, ui
             if (total_ms) *total_ms = c->prof_ms[k];
             if (launches) *launches = c->prof_count[k];
             if (bytes) *bytes = c->prof_bytes[k];
+            if (valu_ops) *valu_ops = c->prof_ops[k];
             return CKKS_OK;
         }
     }

@@ -35,189 +35,12 @@
 #include <type_traits>
 
 #include "ckks_internal.h"
+#include "ntt_core.h"
 #include "ops.h"
 
 namespace {
 
-constexpr int kE = 16;  // residues per thread
-
-template <bool F>
-struct Ar;
-
-template <>
-struct Ar<false> {
-    using E = uint64_t;
-    using W = ulonglong2;
-    uint64_t q, twoq, ninv, ninvs;
-    __device__ explicit Ar(const ModQ &m) : q(m.q), twoq(m.twoq), ninv(m.ninv), ninvs(m.ninvs) {}
-    __device__ E from_u64(uint64_t v) const { return v; }
-    __device__ E from_raw(uint64_t v) const { return v; }
-    __device__ uint64_t to_raw(E x) const { return x; }
-    __device__ uint64_t to_canon(E x) const { return csub(csub(x, twoq), q); }  // from [0, 4q)
-    __device__ E from_i64(int64_t v, const ModQ &m) const
-    {
-        const bool neg = v < 0;
-        const uint64_t mag = neg ? (uint64_t)(-(v + 1)) + 1u : (uint64_t)v;
-        const uint64_t r = csub(mag - mulhi64(mag, m.one_s) * m.q, m.q);
-        return (neg && r) ? m.q - r : r;
-    }
-    // X, Y in [0, 4q) -> [0, 4q)
-    __device__ void ct(E &X, E &Y, W w) const
-    {
-        const uint64_t x = csub(X, twoq);
-        const uint64_t t = shoup_lazy(Y, w.x, w.y, q);
-        X = x + t;
-        Y = x + twoq - t;
-    }
-    // X, Y in [0, 2q) -> [0, 2q)
-    __device__ void gs(E &X, E &Y, W w) const
-    {
-        const uint64_t x = X, y = Y;
-        X = csub(x + y, twoq);
-        Y = shoup_lazy(x + twoq - y, w.x, w.y, q);
-    }
-    __device__ E scale_n(E x) const { return shoup(x, ninv, ninvs, q); }
-};
-
-template <>
-struct Ar<true> {
-    using E = double;
-    using W = double;
-    double q, qinv, ninv;
-    __device__ explicit Ar(const ModQ &m) : q(m.qd), qinv(m.qinvd), ninv(m.ninvd) {}
-    __device__ static E from_u64(uint64_t v)
-    {
-        return (double)(uint32_t)(v >> 32) * 4294967296.0 + (double)(uint32_t)v;
-    }
-    __device__ static E from_raw(uint64_t v) { return __longlong_as_double((long long)v); }
-    __device__ static uint64_t to_raw(E x) { return (uint64_t)__double_as_longlong(x); }
-    // |x| < 2^52 -> |result| <= q/2 + 1
-    __device__ E red(E x) const { return fma(-rint(x * qinv), q, x); }
-    // |a| < 4q, 0 <= w < q -> a w mod q, exact, |result| < 2q
-    __device__ E mul(E a, E w) const
-    {
-        const double h = a * w;
-        const double l = fma(a, w, -h);
-        const double c = rint(h * qinv);
-        return fma(-c, q, h) + l;
-    }
-    __device__ uint64_t to_canon(E x) const
-    {
-        double t = fma(-floor(x * qinv), q, x);
-        t = t < 0.0 ? t + q : t;
-        t = t >= q ? t - q : t;
-        const double hi = floor(t * (1.0 / 4294967296.0));
-        const double lo = fma(-hi, 4294967296.0, t);
-        return ((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo;
-    }
-    // exact for any int64: |v| <= 2^52 converts exactly; larger values are reduced as integers first
-    __device__ E from_i64(int64_t v, const ModQ &m) const
-    {
-        if (v >= -(1ll << 52) && v <= (1ll << 52)) return red((double)v);
-        const bool neg = v < 0;
-        const uint64_t mag = neg ? (uint64_t)(-(v + 1)) + 1u : (uint64_t)v;
-        const uint64_t r = csub(mag - mulhi64(mag, m.one_s) * m.q, m.q);
-        return neg ? -(double)r : (double)r;
-    }
-    // |X|, |Y| < 2q -> |X'|, |Y'| < 2q
-    __device__ void ct(E &X, E &Y, W w) const
-    {
-        const double x = red(X);
-        const double r = mul(Y, w);
-        X = x + r;
-        Y = x - r;
-    }
-    __device__ void gs(E &X, E &Y, W w) const
-    {
-        const double u = X + Y, v = X - Y;
-        X = red(u);
-        Y = mul(v, w);
-    }
-    __device__ E scale_n(E x) const { return mul(x, ninv); }
-};
-
-// Forward, top 4 stages of a sub-transform: x[k] is point u = r + TS*k.
-template <bool F>
-__device__ __forceinline__ void fwd_top(typename Ar<F>::E (&x)[kE], const typename Ar<F>::W *tw, uint32_t B,
-                                        const Ar<F> &ar)
-{
-#pragma unroll
-    for (int lm = 0; lm < 4; lm++) {
-        const int mp = 1 << lm, tk = 8 >> lm;
-#pragma unroll
-        for (int g = 0; g < mp; g++) {
-            const typename Ar<F>::W w = tw[B * mp + g];
-#pragma unroll
-            for (int j = 0; j < tk; j++) ar.ct(x[g * 2 * tk + j], x[g * 2 * tk + j + tk], w);
-        }
-    }
-}
-// Forward, remaining LOGS-4 stages: x[k] is point u = 16 r + k.
-template <int LOGS, bool F>
-__device__ __forceinline__ void fwd_low(typename Ar<F>::E (&x)[kE], const typename Ar<F>::W *tw, uint32_t B,
-                                        uint32_t r, const Ar<F> &ar)
-{
-#pragma unroll
-    for (int l = 0; l < LOGS - 4; l++) {
-        const int mp = 16 << l, t = (1 << LOGS) / (2 * mp), gpt = 8 / t;
-#pragma unroll
-        for (int g = 0; g < gpt; g++) {
-            const typename Ar<F>::W w = tw[B * mp + r * gpt + g];
-#pragma unroll
-            for (int j = 0; j < t; j++) ar.ct(x[g * 2 * t + j], x[g * 2 * t + j + t], w);
-        }
-    }
-}
-template <int LOGS, bool F>
-__device__ __forceinline__ void inv_low(typename Ar<F>::E (&x)[kE], const typename Ar<F>::W *tw, uint32_t B,
-                                        uint32_t r, const Ar<F> &ar)
-{
-#pragma unroll
-    for (int l = LOGS - 5; l >= 0; l--) {
-        const int mp = 16 << l, t = (1 << LOGS) / (2 * mp), gpt = 8 / t;
-#pragma unroll
-        for (int g = 0; g < gpt; g++) {
-            const typename Ar<F>::W w = tw[B * mp + r * gpt + g];
-#pragma unroll
-            for (int j = 0; j < t; j++) ar.gs(x[g * 2 * t + j], x[g * 2 * t + j + t], w);
-        }
-    }
-}
-template <bool F>
-__device__ __forceinline__ void inv_top(typename Ar<F>::E (&x)[kE], const typename Ar<F>::W *tw, uint32_t B,
-                                        const Ar<F> &ar)
-{
-#pragma unroll
-    for (int lm = 3; lm >= 0; lm--) {
-        const int mp = 1 << lm, tk = 8 >> lm;
-#pragma unroll
-        for (int g = 0; g < mp; g++) {
-            const typename Ar<F>::W w = tw[B * mp + g];
-#pragma unroll
-            for (int j = 0; j < tk; j++) ar.gs(x[g * 2 * tk + j], x[g * 2 * tk + j + tk], w);
-        }
-    }
-}
-
-// padded LDS index of point u of sub-transform `sub`
-template <int LOGS>
-__device__ __forceinline__ uint32_t lidx(uint32_t sub, uint32_t u)
-{
-    return sub * ((1u << LOGS) + (1u << LOGS) / 16 + 1) + u + (u >> 4);
-}
-
-// write x[k] at points ua(k), barrier, read x[k] from points ub(k)
-template <int LOGS, bool A_TOP, typename E>
-__device__ __forceinline__ void transpose(E (&x)[kE], E *lds, uint32_t sub, uint32_t r)
-{
-    constexpr uint32_t TS = (1u << LOGS) / 16;
-#pragma unroll
-    for (int k = 0; k < kE; k++) lds[lidx<LOGS>(sub, A_TOP ? r + TS * k : 16 * r + k)] = x[k];
-    __syncthreads();
-#pragma unroll
-    for (int k = 0; k < kE; k++) x[k] = lds[lidx<LOGS>(sub, A_TOP ? 16 * r + k : r + TS * k)];
-    __syncthreads();
-}
+using namespace nttc;
 
 __device__ __forceinline__ size_t row_of_block(uint32_t blk_row, uint32_t batch, uint32_t bstride,
                                                uint32_t *prime_slot)
@@ -226,12 +49,6 @@ __device__ __forceinline__ size_t row_of_block(uint32_t blk_row, uint32_t batch,
     const uint32_t limb = blk_row / batch, b = blk_row % batch;
     *prime_slot = limb;
     return (size_t)b * bstride + limb;
-}
-
-template <bool F>
-__device__ __forceinline__ const typename Ar<F>::W *twp(const void *tw_all, uint32_t prime, uint32_t log_n)
-{
-    return (const typename Ar<F>::W *)tw_all + ((size_t)prime << log_n);
 }
 
 // Column pass over N1 = 2^LOGS points at stride N2 = 2^(log_n - LOGS).
@@ -301,13 +118,37 @@ __global__ __launch_bounds__(256) void ntt_col_from_i64(const int64_t *__restric
     int64_t v[kE];
 #pragma unroll
     for (int k = 0; k < kE; k++) v[k] = src[(size_t)(r + TS * k) * n2];
+    // fp64: coefficients within 2^52 are converted once for all limbs; a thread holding a larger one takes the
+    // exact integer reduction for every limb, re-reading its coefficients
+    double vd[kE];
+    bool big = false;
+    if constexpr (F) {
+#pragma unroll
+        for (int k = 0; k < kE; k++) {
+            big |= v[k] > (1ll << 52) || v[k] < -(1ll << 52);
+            vd[k] = (double)v[k];
+        }
+    }
     for (uint32_t l = 0; l < limbs; l++) {
         const ModQ md = mods[l];
         const Ar<F> ar(md);
         const typename Ar<F>::W *tw = twp<F>(tw_all, l, log_n);
         E x[kE];
+        if constexpr (F) {
+            if (!big) {
 #pragma unroll
-        for (int k = 0; k < kE; k++) x[k] = ar.from_i64(v[k], md);
+                for (int k = 0; k < kE; k++) x[k] = ar.red(vd[k]);
+            } else {
+                // an opaque copy of the pointer: the 16 addresses are formed here, not kept live across the loop
+                auto sg = (const __attribute__((address_space(1))) int64_t *)src;
+                asm volatile("" : "+v"(sg));
+#pragma unroll
+                for (int k = 0; k < kE; k++) x[k] = ar.from_i64(sg[(size_t)(r + TS * k) * n2], md);
+            }
+        } else {
+#pragma unroll
+            for (int k = 0; k < kE; k++) x[k] = ar.from_i64(v[k], md);
+        }
         fwd_top<F>(x, tw, 1, ar);
         if (LOGS > 4) {
             transpose<LOGS, true>(x, lds, col, r);
@@ -369,12 +210,6 @@ __global__ __launch_bounds__(256) void ntt_row(uint64_t *data, LimbMap map, uint
     }
 #pragma unroll
     for (int k = 0; k < kE; k++) base[r + TS * k] = LAST ? ar.to_canon(x[k]) : ar.to_raw(x[k]);
-}
-
-template <int LOGS>
-size_t lds_bytes(uint32_t subs)
-{
-    return (size_t)subs * ((1u << LOGS) + (1u << LOGS) / 16 + 1) * sizeof(uint64_t);
 }
 
 template <bool F>
@@ -488,27 +323,30 @@ hipError_t ntt_passes(ckks_ctx *ctx, uint64_t *data, uint32_t batch, uint32_t bs
 {
     int s1, s2;
     split_log((int)ctx->log_n, &s1, &s2);
-    const double bytes = 16.0 * batch * map.n * ctx->n;  // each pass reads and writes every residue
+    const double res = (double)batch * map.n * ctx->n;
+    const double bytes = 16.0 * res;  // each pass reads and writes every residue
+    // butterflies per residue: half the stages of the pass
+    const double bf = F ? kOpsButterflyF64 : kOpsButterflyInt, ops1 = res * bf * s1 / 2, ops2 = res * bf * s2 / 2;
     hipError_t e = hipSuccess;
     if (!inverse) {
         if (s1) {
-            prof_begin(ctx, K_NTT_FWD_COL, bytes);
+            prof_begin(ctx, K_NTT_FWD_COL, bytes, ops1);
             e = dispatch_col<false, F>(s1, ctx, data, batch, bstride, map);
             prof_end(ctx, K_NTT_FWD_COL);
         }
         if (e == hipSuccess) {
-            prof_begin(ctx, K_NTT_FWD_ROW, bytes);
+            prof_begin(ctx, K_NTT_FWD_ROW, bytes, ops2);
             e = s1 ? dispatch_row<false, false, true, F>(s2, ctx, data, batch, bstride, map)
                    : dispatch_row<false, true, true, F>(s2, ctx, data, batch, bstride, map);
             prof_end(ctx, K_NTT_FWD_ROW);
         }
     } else {
-        prof_begin(ctx, K_NTT_INV_ROW, bytes);
+        prof_begin(ctx, K_NTT_INV_ROW, bytes, ops2);
         e = s1 ? dispatch_row<true, true, false, F>(s2, ctx, data, batch, bstride, map)
                : dispatch_row<true, true, true, F>(s2, ctx, data, batch, bstride, map);
         prof_end(ctx, K_NTT_INV_ROW);
         if (e == hipSuccess && s1) {
-            prof_begin(ctx, K_NTT_INV_COL, bytes);
+            prof_begin(ctx, K_NTT_INV_COL, bytes, ops1);
             e = dispatch_col<true, F>(s1, ctx, data, batch, bstride, map);
             prof_end(ctx, K_NTT_INV_COL);
         }
@@ -545,6 +383,30 @@ ckks_status launch_ntt_strided(ckks_ctx *ctx, uint64_t *data, uint32_t batch, ui
     return CKKS_OK;
 }
 
+void ntt_split(uint32_t log_n, int *s1, int *s2) { split_log((int)log_n, s1, s2); }
+
+bool ntt_uses_f64(const ckks_ctx *ctx, uint32_t limbs) { return use_f64(ctx, limb_range(0, limbs)); }
+
+// First (column) pass only of the forward NTT of m[batch][N] into out[batch][limbs][N]; the rows are left in the
+// inter-pass form of the arithmetic ntt_uses_f64 selects.  Needs a two-pass size (s1 > 0).
+ckks_status launch_ntt_col_i64(ckks_ctx *ctx, const int64_t *m, uint64_t *out, uint32_t batch, uint32_t limbs)
+{
+    if (!batch || !limbs) return CKKS_OK;
+    int s1, s2;
+    split_log((int)ctx->log_n, &s1, &s2);
+    CK_REQUIRE(s1 > 0, CKKS_EINVAL, "ntt: a single-pass size has no column pass");
+    const bool f = use_f64(ctx, limb_range(0, limbs));
+    // butterflies of s1 stages plus the reduction of each coefficient (fp64: one range reduction)
+    const double res = (double)batch * limbs * ctx->n;
+    prof_begin(ctx, K_NTT_FWD_COL, 8.0 * batch * ctx->n * (1 + limbs),
+               res * ((f ? kOpsButterflyF64 : kOpsButterflyInt) * s1 / 2 + (f ? 3.0 : 8.0)));
+    const hipError_t e = f ? dispatch_col_i64<true>(s1, ctx, m, out, batch, limbs)
+                           : dispatch_col_i64<false>(s1, ctx, m, out, batch, limbs);
+    prof_end(ctx, K_NTT_FWD_COL);
+    if (e != hipSuccess) return set_error(CKKS_EHIP, "ntt launch failed: %s", hipGetErrorString(e));
+    return CKKS_OK;
+}
+
 // Forward NTT of signed coefficient rows m[batch][N] into out[batch][limbs][N]
 // over primes 0..limbs-1 (reduction fused into the first pass).
 ckks_status launch_ntt_from_i64(ckks_ctx *ctx, const int64_t *m, uint64_t *out, uint32_t batch, uint32_t limbs)
@@ -560,11 +422,12 @@ ckks_status launch_ntt_from_i64(ckks_ctx *ctx, const int64_t *m, uint64_t *out, 
     const LimbMap map = limb_range(0, limbs);
     const bool f = use_f64(ctx, map);
     hipError_t e;
-    prof_begin(ctx, K_NTT_FWD_COL, 8.0 * batch * ctx->n * (1 + limbs));
+    const double res = (double)batch * limbs * ctx->n, bf = f ? kOpsButterflyF64 : kOpsButterflyInt;
+    prof_begin(ctx, K_NTT_FWD_COL, 8.0 * batch * ctx->n * (1 + limbs), res * (bf * s1 / 2 + (f ? 3.0 : 8.0)));
     e = f ? dispatch_col_i64<true>(s1, ctx, m, out, batch, limbs) : dispatch_col_i64<false>(s1, ctx, m, out, batch, limbs);
     prof_end(ctx, K_NTT_FWD_COL);
     if (e == hipSuccess) {
-        prof_begin(ctx, K_NTT_FWD_ROW, 16.0 * batch * limbs * ctx->n);
+        prof_begin(ctx, K_NTT_FWD_ROW, 16.0 * batch * limbs * ctx->n, res * bf * s2 / 2);
         e = f ? dispatch_row<false, false, true, true>(s2, ctx, out, batch, limbs, map)
               : dispatch_row<false, false, true, false>(s2, ctx, out, batch, limbs, map);
         prof_end(ctx, K_NTT_FWD_ROW);

@@ -12,9 +12,12 @@
 //  2. for a tile of J = 8 output blocks and one giant step g, the weight
 //     plaintexts of a sub-batch of (i, b) pairs are encoded on the fly from W
 //     (slot generation fused into the fp64 FFT -> round -> NTT column pass with
-//     the RNS reduction fused in -> NTT row pass) and consumed by the
-//     multiply-accumulate kernel, which loads each xrot residue once for all J
-//     output blocks and accumulates exactly in 128 bits;
+//     the RNS reduction fused in) and consumed by k_row_mac, which finishes
+//     each plaintext's transform (the row pass) in registers and accumulates
+//     pt * xrot there, so the plaintexts' NTT values never reach HBM.  With the
+//     integer transform arithmetic (primes of 50 bits or more) the row pass
+//     writes the plaintexts and k_mac accumulates them exactly in 128 bits,
+//     loading each xrot residue once for all J output blocks;
 //  3. giant-step rotation of each partial sum at level l, summation, rescale.
 // The plaintext scale is q_l, so the rescale returns the input scale exactly.
 #include <algorithm>
@@ -22,6 +25,7 @@
 #include <vector>
 
 #include "ckks_internal.h"
+#include "ntt_core.h"
 #include "ops.h"
 
 ckks_status rotate_core(ckks_ctx *ctx, const uint64_t *c, uint32_t level, const int32_t *steps,
@@ -78,7 +82,150 @@ __global__ __launch_bounds__(kThreads) void k_mac(uint64_t *acc, const uint64_t 
     }
 }
 
-constexpr uint32_t kJ = 8;  // output blocks per tile
+// output blocks per tile: the blocks of one tile share each xrot read; 14 (a divisor of the 56 outputs of the
+// 4096 x 14336 projection) fills the last wave of the multiply-accumulate launches best among the divisors tried
+constexpr uint32_t kJ = 14;
+
+// Row pass of the forward NTT fused with the multiply-accumulate (fp64
+// arithmetic, primes below 2^50).  Block (jj, tile) owns rows_per_block rows of
+// 2^LOGS residues of limb l for output block jj; for each (i, b) pair p of the
+// sub-batch it loads the column-pass output of plaintext (jj, p), finishes its
+// transform in registers and LDS, and accumulates pt * xrot[pair] for both
+// ciphertext components into registers.  The plaintexts' NTT values never go
+// to HBM; only the column-pass rows are read, once.  The jc blocks of one tile
+// read the same xrot rows at about the same time: with xcd set they are
+// numbered so that all of them land on one XCD (blocks are dealt to the 8 XCDs
+// round robin) and share those reads in its L2.
+//
+// Accumulators hold exact integer-valued doubles: a product of a transform
+// output (|x| < 2q) and a canonical residue is reduced to |r| <= 1.25 q, the
+// running sum is range-reduced to |a| <= q/2 + 1 every 4 pairs, so it stays
+// below 5.5 q < 2^53.
+template <int LOGS>
+__global__ __launch_bounds__(64) void k_row_mac(uint64_t *acc, const uint64_t *__restrict__ colout,
+                                                 const double *__restrict__ xrot, uint32_t P, uint32_t jc,
+                                                 uint32_t ib0, uint32_t bcount, uint32_t n1, uint32_t L,
+                                                 uint32_t log_n, int accumulate, const ModQ *__restrict__ mods,
+                                                 const double *__restrict__ twf, uint32_t rows_per_block,
+                                                 uint32_t blocks_per_limb, int xcd)
+{
+    using nttc::kE;
+    constexpr uint32_t S = 1u << LOGS, TS = S / 16;
+    extern __shared__ uint64_t lds_raw[];
+    double *lds = (double *)lds_raw;
+    const uint32_t bid = blockIdx.x;
+    uint32_t jj, tile;
+    if (xcd) {
+        const uint32_t k = bid >> 3;
+        jj = k % jc;
+        tile = (k / jc) * 8 + (bid & 7);
+    } else {
+        jj = bid % jc;
+        tile = bid / jc;
+    }
+    const uint32_t l = tile / blocks_per_limb, blk = tile % blocks_per_limb;
+    const nttc::Ar<true> ar(mods[l]);
+    const double *tw = twf + ((size_t)l << log_n);
+    const uint32_t rows = 1u << (log_n - LOGS);
+    const uint32_t sub = threadIdx.x / TS, r = threadIdx.x % TS;
+    const uint32_t h = blk * rows_per_block + sub;
+    const uint32_t B = rows + h;
+    const size_t pt_words = (size_t)L << log_n, ct_words = 2 * pt_words;
+    const size_t off = ((size_t)l << log_n) + (size_t)h * S + r;
+    double a0[kE], a1[kE];
+#pragma unroll
+    for (int k = 0; k < kE; k++) a0[k] = a1[k] = 0.0;
+    for (uint32_t p = 0; p < P; p++) {
+        const uint64_t *src = colout + ((size_t)jj * P + p) * pt_words + off;
+        double x[kE];
+#pragma unroll
+        for (int k = 0; k < kE; k++) x[k] = nttc::Ar<true>::from_raw(src[TS * k]);
+        // an opaque copy of the table pointer keeps the compiler from hoisting the twiddle loads (cache hits) out
+        // of the loop into ~60 registers that would halve the occupancy
+        auto twg = (const __attribute__((address_space(1))) double *)tw;
+        asm volatile("" : "+v"(twg));
+        const double *twl = (const double *)twg;
+        nttc::fwd_top<true>(x, twl, B, ar);
+        if (LOGS > 4) {
+            nttc::transpose<LOGS, true>(x, lds, sub, r);
+            nttc::fwd_low<LOGS, true>(x, twl, B, r, ar);
+            nttc::transpose<LOGS, false>(x, lds, sub, r);
+        }
+        const uint32_t pair = ib0 + p;
+        const double *xr = xrot + (size_t)((pair / bcount) * n1 + pair % bcount) * ct_words + off;
+#pragma unroll
+        for (int k = 0; k < kE; k++) {
+            a0[k] += ar.mul(x[k], xr[TS * k]);
+            a1[k] += ar.mul(x[k], xr[pt_words + TS * k]);
+        }
+        if ((p & 3) == 3) {
+#pragma unroll
+            for (int k = 0; k < kE; k++) {
+                a0[k] = ar.red(a0[k]);
+                a1[k] = ar.red(a1[k]);
+            }
+        }
+    }
+    uint64_t *dst = acc + (size_t)jj * ct_words + off;
+    const uint64_t q = mods[l].q;
+#pragma unroll
+    for (int k = 0; k < kE; k++) {
+        uint64_t r0 = ar.to_canon(a0[k]), r1 = ar.to_canon(a1[k]);
+        if (accumulate) {
+            r0 = addmod(r0, dst[TS * k], q);
+            r1 = addmod(r1, dst[pt_words + TS * k], q);
+        }
+        dst[TS * k] = r0;
+        dst[pt_words + TS * k] = r1;
+    }
+}
+
+// canonical residues -> the same values as doubles (exact below 2^53), in place
+__global__ __launch_bounds__(kThreads) void k_to_f64(uint64_t *v, size_t n)
+{
+    const size_t i = (size_t)blockIdx.x * kThreads + threadIdx.x;
+    if (i < n) v[i] = (uint64_t)__double_as_longlong((double)v[i]);
+}
+
+template <int LOGS>
+hipError_t launch_row_mac_t(ckks_ctx *ctx, uint64_t *acc, const uint64_t *colout, const double *xrot, uint32_t P,
+                            uint32_t jc, uint32_t ib0, uint32_t bcount, uint32_t n1, uint32_t L, bool accumulate)
+{
+    const uint32_t rows = 1u << (ctx->log_n - LOGS), TS = (1u << LOGS) / 16;
+    // one wave per block: 64 / TS rows
+    uint32_t rpb = 64 / TS;
+    if (rpb > rows) rpb = rows;
+    const uint32_t bpl = rows / rpb, tiles = L * bpl;
+    const int xcd = tiles % 8 == 0;
+    const dim3 grid(jc * tiles), block(rpb * TS);
+    hipLaunchKernelGGL(k_row_mac<LOGS>, grid, block, nttc::lds_bytes<LOGS>(rpb), ctx->stream, acc, colout, xrot, P,
+                       jc, ib0, bcount, n1, L, ctx->log_n, (int)accumulate, ctx->d_mod, ctx->d_twf, rpb, bpl, xcd);
+    return hipGetLastError();
+}
+
+ckks_status launch_row_mac(ckks_ctx *ctx, uint64_t *acc, const uint64_t *colout, const double *xrot, uint32_t P,
+                           uint32_t jc, uint32_t ib0, uint32_t bcount, uint32_t n1, uint32_t L, bool accumulate)
+{
+    int s1, s2;
+    ntt_split(ctx->log_n, &s1, &s2);
+    // column-pass rows (jc x P), rotated inputs (P ciphertexts), accumulators written (and read when accumulating)
+    const double w = 8.0 * L * ctx->n;
+    // per plaintext residue: the row pass's butterflies, two exact products and additions (14), and the range
+    // reduction of both sums every 4 pairs (1.5)
+    const double res = (double)jc * P * L * ctx->n;
+    prof_begin(ctx, K_ROW_MAC, w * ((double)jc * P + 2.0 * P + 2.0 * jc * (accumulate ? 2 : 1)),
+               res * (kOpsButterflyF64 * s2 / 2 + 15.5));
+    hipError_t e = hipErrorInvalidValue;
+    switch (s2) {
+    case 5: e = launch_row_mac_t<5>(ctx, acc, colout, xrot, P, jc, ib0, bcount, n1, L, accumulate); break;
+    case 6: e = launch_row_mac_t<6>(ctx, acc, colout, xrot, P, jc, ib0, bcount, n1, L, accumulate); break;
+    case 7: e = launch_row_mac_t<7>(ctx, acc, colout, xrot, P, jc, ib0, bcount, n1, L, accumulate); break;
+    case 8: e = launch_row_mac_t<8>(ctx, acc, colout, xrot, P, jc, ib0, bcount, n1, L, accumulate); break;
+    }
+    prof_end(ctx, K_ROW_MAC);
+    if (e != hipSuccess) return set_error(CKKS_EHIP, "row/mac launch failed: %s", hipGetErrorString(e));
+    return CKKS_OK;
+}
 
 ckks_status launch_mac(ckks_ctx *ctx, uint64_t *acc, const uint64_t *pt, const uint64_t *xrot, uint32_t P,
                        uint32_t jc, uint32_t ib0, uint32_t bcount, uint32_t n1, uint32_t L, bool accumulate)
@@ -159,7 +306,9 @@ extern "C" ckks_status ckks_linear_project(ckks_ctx *ctx, const ckks_buf *in, co
     // plaintext sub-batch of at most 2 GiB: J output blocks x Pb (i, b) pairs
     const size_t budget = size_t(1) << 31;
     const uint32_t Jt = kJ;
-    const uint32_t Pb = std::min<uint32_t>(maxpairs, std::max<uint32_t>(1, (uint32_t)(budget / ((size_t)Jt * L * N * 8))));
+    uint32_t Pmax = std::min<uint32_t>(maxpairs, std::max<uint32_t>(1, (uint32_t)(budget / ((size_t)Jt * L * N * 8))));
+    if (ctx->proj_max_pairs) Pmax = std::min(Pmax, ctx->proj_max_pairs);
+    const uint32_t Pb = Pmax;
     const size_t xrot_w = (size_t)n_in * n1 * ctw;
     const size_t acc_w = (size_t)kJ * ctw, tot_w = (size_t)kJ * ctw, rot_w = ctw;
     const size_t pt_w = (size_t)Jt * Pb * L * N;
@@ -188,6 +337,17 @@ extern "C" ckks_status ckks_linear_project(ckks_ctx *ctx, const ckks_buf *in, co
             CK_TRY(rotate_core(ctx, in[i].data, level, bsteps.data(), bkeys.data(), n1 - 1, outs.data(), ksw));
         }
     }
+    // fp64 two-pass transforms: the row pass runs inside the multiply-accumulate, which reads xrot as doubles
+    int s1, s2;
+    ntt_split(ctx->log_n, &s1, &s2);
+    const bool fused = s1 > 0 && ntt_uses_f64(ctx, L);
+    if (fused) {
+        prof_begin(ctx, K_ELEM, 16.0 * xrot_w);
+        hipLaunchKernelGGL(k_to_f64, dim3((unsigned)((xrot_w + kThreads - 1) / kThreads)), dim3(kThreads), 0,
+                           ctx->stream, xrot, xrot_w);
+        prof_end(ctx, K_ELEM);
+        HIP_TRY(hipGetLastError());
+    }
 
     // ---- 2./3. tiles of output blocks
     const double delta_w = (double)ctx->primes[level];
@@ -196,8 +356,10 @@ extern "C" ckks_status ckks_linear_project(ckks_ctx *ctx, const ckks_buf *in, co
         for (uint32_t g = 0; g < n2; g++) {
             const uint32_t bcount = std::min<uint32_t>(n1, D - n1 * g);
             const uint32_t pairs = n_in * bcount;
-            for (uint32_t pb0 = 0; pb0 < pairs; pb0 += Pb) {
-                const uint32_t P = std::min<uint32_t>(Pb, pairs - pb0);
+            // sub-batches of equal size (within one pair): no short tail launch
+            const uint32_t nsub = (pairs + Pb - 1) / Pb;
+            for (uint32_t sb = 0, pb0 = 0; sb < nsub; sb++) {
+                const uint32_t P = pairs / nsub + (sb < pairs % nsub ? 1 : 0);
                 SlotSource src;
                 src.W = W;
                 src.d_out = shape->d_out;
@@ -210,8 +372,14 @@ extern "C" ckks_status ckks_linear_project(ckks_ctx *ctx, const ckks_buf *in, co
                 src.pairs = P;
                 const uint32_t batch = jc * P;
                 CK_TRY(enc_coeffs(ctx, src, batch, delta_w, fft, mint));
-                CK_TRY(launch_ntt_from_i64(ctx, mint, pts, batch, L));
-                CK_TRY(launch_mac(ctx, acc, pts, xrot, P, jc, pb0, bcount, n1, L, pb0 > 0));
+                if (fused) {
+                    CK_TRY(launch_ntt_col_i64(ctx, mint, pts, batch, L));
+                    CK_TRY(launch_row_mac(ctx, acc, pts, (const double *)xrot, P, jc, pb0, bcount, n1, L, pb0 > 0));
+                } else {
+                    CK_TRY(launch_ntt_from_i64(ctx, mint, pts, batch, L));
+                    CK_TRY(launch_mac(ctx, acc, pts, xrot, P, jc, pb0, bcount, n1, L, pb0 > 0));
+                }
+                pb0 += P;
             }
             for (uint32_t jj = 0; jj < jc; jj++) {
                 uint64_t *a = acc + (size_t)jj * ctw, *t = tot + (size_t)jj * ctw;

@@ -3,11 +3,19 @@
 * toy ring, the whole workload (16 tokens x 128 features, 128 x 128 weights, plain
   diagonal method with 127 hoisted rotations): every output ciphertext bit for bit,
   and decrypted within 2^-12 of X @ W;
+* toy ring with the integer transform arithmetic (the unfused path: separate row
+  pass and multiply-accumulate kernels);
+* toy ring with a baby-step/giant-step split (n1 = 16, n2 = 8), two input and 17
+  output ciphertexts (a full tile of output blocks and a ragged one) and at most
+  seven (input, baby step) pairs per launch, so partial sums are carried across
+  launches of unequal sizes;
 * the Llama-shaped projection parameters at full ring degree (N = 2^16, 24 + 8
   limbs of 50-bit primes, dnum 3, level 12, 128 tokens x 256 features, n1 = 32,
   n2 = 8 so 31 baby and 7 giant rotations) on a 256 x 512 slice of the weights
   (one input ciphertext, two output ciphertexts), bit for bit.
 """
+import dataclasses
+
 import numpy as np
 import pytest
 
@@ -23,10 +31,12 @@ def fm_pack(X, T, D, i):
     return X[:, i * D:(i + 1) * D].T.reshape(-1)
 
 
-def run_case(cfg, d_in, d_out, oracle_outputs):
+def run_case(cfg, d_in, d_out, oracle_outputs, arith=0, max_pairs=0):
     require_gpu()
     from paper_2609_12378_amd import Context
     ctx = Context(cfg.log_n, cfg.n_q, cfg.n_p, cfg.dnum, q_bits=cfg.q_bits)
+    ctx.set_ntt_arith(arith)
+    ctx.set_proj_batch(max_pairs)
     ck = Ckks(cfg.log_n, ctx.q, ctx.p, cfg.dnum)
     n, T, D, n1, level = ctx.n, cfg.tokens, cfg.feats, cfg.n1, cfg.level
     n2 = -(-D // n1)
@@ -77,6 +87,19 @@ def run_case(cfg, d_in, d_out, oracle_outputs):
 def test_toy_projection_bit_exact():
     err = run_case(TOY, TOY.d_in, TOY.d_out, [0])
     say("toy max error vs X@W", err)
+    assert err <= 2.0 ** -12
+
+
+def test_toy_projection_integer_arithmetic():
+    err = run_case(TOY, TOY.d_in, TOY.d_out, [0], arith=1)
+    say("toy (integer transforms) max error vs X@W", err)
+    assert err <= 2.0 ** -12
+
+
+def test_toy_projection_bsgs_tiles_and_carried_sums():
+    cfg = dataclasses.replace(TOY, n1=16)
+    err = run_case(cfg, 2 * cfg.feats, 17 * cfg.feats, [0, 13, 14, 16], max_pairs=7)
+    say("toy BSGS max error vs X@W", err)
     assert err <= 2.0 ** -12
 
 
