@@ -160,6 +160,82 @@ __global__ __launch_bounds__(256) void ntt_col_from_i64(const int64_t *__restric
     }
 }
 
+// The same first pass for 256-point columns (N = 2^16) with 8 residues per
+// thread and fp64 butterflies (nttc::fwd8_256): a block of 512 threads holds 16
+// adjacent columns (consecutive lanes take consecutive columns, so every load
+// and store moves 128-byte segments).  The twiddles of limb l+1 (Psi[1..255],
+// shared by all columns) are staged into the idle half of a double-buffered LDS
+// table while limb l is transformed.
+__global__ __launch_bounds__(512) void ntt_col8_from_i64(const int64_t *__restrict__ m, uint64_t *out,
+                                                         uint32_t limbs, const ModQ *mods, const double *twf,
+                                                         uint32_t log_n, uint32_t blocks_per_row)
+{
+    using nttc::kE8;
+    __shared__ double tws[2][256];
+    __shared__ double tr[16][nttc::kTr8];
+    const uint32_t b = blockIdx.x / blocks_per_row, blk = blockIdx.x % blocks_per_row;
+    const uint32_t n2 = 1u << (log_n - 8);
+    const uint32_t col = threadIdx.x & 15, t = threadIdx.x >> 4;
+    const size_t coff = (size_t)blk * 16 + col;
+    const int64_t *src = m + ((size_t)b << log_n) + coff;
+    int64_t v[kE8];
+#pragma unroll
+    for (int k = 0; k < kE8; k++) v[k] = src[(size_t)nttc::u8<0>(t, k) * n2];
+    double vd[kE8];
+    bool big = false;
+#pragma unroll
+    for (int k = 0; k < kE8; k++) {
+        big |= v[k] > (1ll << 52) || v[k] < -(1ll << 52);
+        vd[k] = (double)v[k];
+    }
+    if (threadIdx.x < 255) tws[0][threadIdx.x + 1] = twf[threadIdx.x + 1];
+    __syncthreads();
+    for (uint32_t l = 0; l < limbs; l++) {
+        const ModQ md = mods[l];
+        const Ar<true> ar(md);
+        // next limb's twiddle, written to the other table after the first barrier of this limb (when every
+        // thread has finished reading it for limb l - 1)
+        double wnext = 0.0;
+        if (l + 1 < limbs && threadIdx.x < 255) wnext = twf[((size_t)(l + 1) << log_n) + threadIdx.x + 1];
+        double x[kE8];
+        if (!big) {
+#pragma unroll
+            for (int k = 0; k < kE8; k++) x[k] = ar.red(vd[k]);
+        } else {
+            auto sg = (const __attribute__((address_space(1))) int64_t *)src;
+            asm volatile("" : "+v"(sg));
+#pragma unroll
+            for (int k = 0; k < kE8; k++) x[k] = ar.from_i64(sg[(size_t)nttc::u8<0>(t, k) * n2], md);
+        }
+        const double *tw = tws[l & 1];
+        double *trc = tr[col];
+        nttc::fwd8_stage<0, 0>(x, tw, t, ar);
+        nttc::fwd8_stage<0, 1>(x, tw, t, ar);
+        nttc::fwd8_stage<0, 2>(x, tw, t, ar);
+#pragma unroll
+        for (int k = 0; k < kE8; k++) trc[nttc::pad_ac(nttc::u8<0>(t, k))] = x[k];
+        __syncthreads();
+        if (l + 1 < limbs && threadIdx.x < 255) tws[(l + 1) & 1][threadIdx.x + 1] = wnext;
+#pragma unroll
+        for (int k = 0; k < kE8; k++) x[k] = trc[nttc::pad_ac(nttc::u8<1>(t, k))];
+        __syncthreads();
+        nttc::fwd8_stage<1, 3>(x, tw, t, ar);
+        nttc::fwd8_stage<1, 4>(x, tw, t, ar);
+        nttc::fwd8_stage<1, 5>(x, tw, t, ar);
+#pragma unroll
+        for (int k = 0; k < kE8; k++) trc[nttc::pad_cb(nttc::u8<1>(t, k))] = x[k];
+        __syncthreads();
+#pragma unroll
+        for (int k = 0; k < kE8; k++) x[k] = trc[nttc::pad_cb(nttc::u8<2>(t, k))];
+        __syncthreads();
+        nttc::fwd8_stage<2, 6>(x, tw, t, ar);
+        nttc::fwd8_stage<2, 7>(x, tw, t, ar);
+        uint64_t *dst = out + (((size_t)b * limbs + l) << log_n) + coff;
+#pragma unroll
+        for (int k = 0; k < kE8; k++) dst[(size_t)nttc::u8<2>(t, k) * n2] = Ar<true>::to_raw(x[k]);
+    }
+}
+
 // Row pass over N2 = 2^LOGS contiguous points of row h, twiddle base N1 + h.
 // FIRST: input is canonical residues; LAST: write canonical residues (and, for
 // the inverse, multiply by N^-1).
@@ -400,8 +476,16 @@ ckks_status launch_ntt_col_i64(ckks_ctx *ctx, const int64_t *m, uint64_t *out, u
     const double res = (double)batch * limbs * ctx->n;
     prof_begin(ctx, K_NTT_FWD_COL, 8.0 * batch * ctx->n * (1 + limbs),
                res * ((f ? kOpsButterflyF64 : kOpsButterflyInt) * s1 / 2 + (f ? 3.0 : 8.0)));
-    const hipError_t e = f ? dispatch_col_i64<true>(s1, ctx, m, out, batch, limbs)
-                           : dispatch_col_i64<false>(s1, ctx, m, out, batch, limbs);
+    hipError_t e;
+    if (f && s1 == 8) {
+        const uint32_t bpr = (ctx->n >> 8) / 16;
+        hipLaunchKernelGGL(ntt_col8_from_i64, dim3(batch * bpr), dim3(512), 0, ctx->stream, m, out, limbs,
+                           ctx->d_mod, ctx->d_twf, ctx->log_n, bpr);
+        e = hipGetLastError();
+    } else {
+        e = f ? dispatch_col_i64<true>(s1, ctx, m, out, batch, limbs)
+              : dispatch_col_i64<false>(s1, ctx, m, out, batch, limbs);
+    }
     prof_end(ctx, K_NTT_FWD_COL);
     if (e != hipSuccess) return set_error(CKKS_EHIP, "ntt launch failed: %s", hipGetErrorString(e));
     return CKKS_OK;
@@ -419,19 +503,14 @@ ckks_status launch_ntt_from_i64(ckks_ctx *ctx, const int64_t *m, uint64_t *out, 
         CK_TRY(enc_to_rns(ctx, m, batch, limbs, out));
         return launch_ntt(ctx, out, batch * limbs, limb_range(0, limbs), false);
     }
+    CK_TRY(launch_ntt_col_i64(ctx, m, out, batch, limbs));
     const LimbMap map = limb_range(0, limbs);
     const bool f = use_f64(ctx, map);
-    hipError_t e;
     const double res = (double)batch * limbs * ctx->n, bf = f ? kOpsButterflyF64 : kOpsButterflyInt;
-    prof_begin(ctx, K_NTT_FWD_COL, 8.0 * batch * ctx->n * (1 + limbs), res * (bf * s1 / 2 + (f ? 3.0 : 8.0)));
-    e = f ? dispatch_col_i64<true>(s1, ctx, m, out, batch, limbs) : dispatch_col_i64<false>(s1, ctx, m, out, batch, limbs);
-    prof_end(ctx, K_NTT_FWD_COL);
-    if (e == hipSuccess) {
-        prof_begin(ctx, K_NTT_FWD_ROW, 16.0 * batch * limbs * ctx->n, res * bf * s2 / 2);
-        e = f ? dispatch_row<false, false, true, true>(s2, ctx, out, batch, limbs, map)
-              : dispatch_row<false, false, true, false>(s2, ctx, out, batch, limbs, map);
-        prof_end(ctx, K_NTT_FWD_ROW);
-    }
+    prof_begin(ctx, K_NTT_FWD_ROW, 16.0 * batch * limbs * ctx->n, res * bf * s2 / 2);
+    const hipError_t e = f ? dispatch_row<false, false, true, true>(s2, ctx, out, batch, limbs, map)
+                           : dispatch_row<false, false, true, false>(s2, ctx, out, batch, limbs, map);
+    prof_end(ctx, K_NTT_FWD_ROW);
     if (e != hipSuccess) return set_error(CKKS_EHIP, "ntt launch failed: %s", hipGetErrorString(e));
     return CKKS_OK;
 }

@@ -203,4 +203,100 @@ size_t lds_bytes(uint32_t subs)
     return (size_t)subs * ((1u << LOGS) + (1u << LOGS) / 16 + 1) * sizeof(uint64_t);
 }
 
+// ---- 256-point sub-transforms with 8 residues per thread (fp64 arithmetic) ----
+//
+// 32 threads hold one 256-point sub-transform, 8 points each, in three layouts
+// (t: thread index within the sub-transform, k: register index):
+//   A: u = t + 32 k                              register bits u7 u6 u5: stages 0-2
+//   C: u = (t >> 2) << 5 | k << 2 | (t & 3)      register bits u4 u3 u2: stages 3-5
+//   B: u = (k >> 2) << 7 | t << 2 | (k & 3)      register bits u7 u1 u0: stages 6-7
+// Stage s pairs the points that differ in bit 7 - s, exactly as the 16-residue
+// code above; group g of stage s (the top s bits of u) takes the twiddle
+// tws[2^s + g], where tws is the sub-transform's table Psi[B 2^s + g] staged in
+// LDS.  Half the residues of the 16-per-thread layout halve the registers a
+// thread needs, so twice the waves fit on a SIMD.
+// LDS addresses: the A -> C transpose XOR-swizzles u (conflict-free for both
+// patterns), the C -> B one pads a word every 8 (C conflict-free, B at most
+// two-way); kTr8 doubles per sub-transform.
+constexpr int kE8 = 8;
+constexpr uint32_t kTr8 = 287;
+
+template <int LAY>
+__device__ __forceinline__ uint32_t u8(uint32_t t, int k)
+{
+    if (LAY == 0) return t + 32u * (uint32_t)k;
+    if (LAY == 1) return ((t >> 2) << 5) | ((uint32_t)k << 2) | (t & 3u);
+    return ((uint32_t)(k >> 2) << 7) | (t << 2) | (uint32_t)(k & 3);
+}
+
+// forward stage S on layout LAY (S in 0-2 for A, 3-5 for C, 6-7 for B)
+template <int LAY, int S>
+__device__ __forceinline__ void fwd8_stage(double (&x)[kE8], const double *tws, uint32_t t, const Ar<true> &ar,
+                                           uint32_t Bm = 1)
+{
+    constexpr int b = 7 - S;
+    constexpr int rb = LAY == 0 ? b - 5 : LAY == 1 ? b - 2 : (b == 7 ? 2 : b);
+    static_assert(rb >= 0 && rb < 3, "stage not in this layout");
+#pragma unroll
+    for (int k = 0; k < kE8; k++) {
+        if (k & (1 << rb)) continue;
+        const double w = tws[(1u << S) * Bm + (u8<LAY>(t, k) >> (b + 1))];
+        ar.ct(x[k], x[k | (1 << rb)], w);
+    }
+}
+
+__device__ __forceinline__ uint32_t pad_ac(uint32_t u) { return u ^ (((u >> 5) & 7u) << 2); }
+__device__ __forceinline__ uint32_t pad_cb(uint32_t u) { return u + (u >> 3); }
+
+// all eight forward stages of the sub-transform held by thread t (layout A in,
+// layout B out); tr: this sub-transform's kTr8 doubles of LDS; every thread of
+// the block must call it (block barriers)
+__device__ __forceinline__ void fwd8_256(double (&x)[kE8], const double *tws, double *tr, uint32_t t,
+                                         const Ar<true> &ar, uint32_t Bm = 1)
+{
+    fwd8_stage<0, 0>(x, tws, t, ar, Bm);
+    fwd8_stage<0, 1>(x, tws, t, ar, Bm);
+    fwd8_stage<0, 2>(x, tws, t, ar, Bm);
+#pragma unroll
+    for (int k = 0; k < kE8; k++) tr[pad_ac(u8<0>(t, k))] = x[k];
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < kE8; k++) x[k] = tr[pad_ac(u8<1>(t, k))];
+    __syncthreads();
+    fwd8_stage<1, 3>(x, tws, t, ar, Bm);
+    fwd8_stage<1, 4>(x, tws, t, ar, Bm);
+    fwd8_stage<1, 5>(x, tws, t, ar, Bm);
+#pragma unroll
+    for (int k = 0; k < kE8; k++) tr[pad_cb(u8<1>(t, k))] = x[k];
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < kE8; k++) x[k] = tr[pad_cb(u8<2>(t, k))];
+    __syncthreads();
+    fwd8_stage<2, 6>(x, tws, t, ar, Bm);
+    fwd8_stage<2, 7>(x, tws, t, ar, Bm);
+}
+
+// layout B -> layout A through LDS (a word of padding every 32), so that
+// consecutive lanes hold consecutive points again
+__device__ __forceinline__ void b_to_a8(double (&x)[kE8], double *tr, uint32_t t)
+{
+#pragma unroll
+    for (int k = 0; k < kE8; k++) tr[u8<2>(t, k) + (u8<2>(t, k) >> 5)] = x[k];
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < kE8; k++) x[k] = tr[u8<0>(t, k) + (u8<0>(t, k) >> 5)];
+    __syncthreads();
+}
+
+// twiddle table of a 256-point sub-transform with base B: tws[2^s + g] = Psi[B 2^s + g]
+// for 1 <= 2^s + g < 256; filled by `nthreads` threads starting at thread `tid`
+__device__ __forceinline__ void stage_twiddles8(double *tws, const double *tw, uint32_t B, uint32_t tid,
+                                                uint32_t nthreads)
+{
+    for (uint32_t e = tid + 1; e < 256; e += nthreads) {
+        const uint32_t m = 1u << (31 - __clz(e));
+        tws[e] = tw[(size_t)B * m + (e - m)];
+    }
+}
+
 }  // namespace nttc

@@ -180,6 +180,80 @@ __global__ __launch_bounds__(64) void k_row_mac(uint64_t *acc, const uint64_t *_
     }
 }
 
+// The same for 256-point rows with 8 residues per thread (nttc::fwd8_256): a
+// block is one wave holding 2 rows, whose twiddle tables are staged in LDS once
+// for all P pairs.  The transform ends in a layout where each lane holds runs of
+// 4 points; one more LDS transpose returns the values to consecutive lanes
+// before xrot is read, since the 16-byte strided reads of that layout measured
+// 30% slower than the extra transpose.  Half the registers of the 16-residue
+// kernel (126 VGPRs): 4 waves per SIMD instead of 3.
+__global__ __launch_bounds__(64) void k_row_mac8(uint64_t *acc, const uint64_t *__restrict__ colout,
+                                                 const double *__restrict__ xrot, uint32_t P, uint32_t jc,
+                                                 uint32_t ib0, uint32_t bcount, uint32_t n1, uint32_t L,
+                                                 uint32_t log_n, int accumulate, const ModQ *__restrict__ mods,
+                                                 const double *__restrict__ twf, uint32_t blocks_per_limb, int xcd)
+{
+    using nttc::kE8;
+    __shared__ double tws[2][257];
+    __shared__ double tr[2][nttc::kTr8];
+    const uint32_t bid = blockIdx.x;
+    uint32_t jj, tile;
+    if (xcd) {
+        const uint32_t k = bid >> 3;
+        jj = k % jc;
+        tile = (k / jc) * 8 + (bid & 7);
+    } else {
+        jj = bid % jc;
+        tile = bid / jc;
+    }
+    const uint32_t l = tile / blocks_per_limb, blk = tile % blocks_per_limb;
+    const nttc::Ar<true> ar(mods[l]);
+    const uint32_t sub = threadIdx.x >> 5, t = threadIdx.x & 31;
+    const uint32_t h = blk * 2 + sub;
+    nttc::stage_twiddles8(tws[sub], twf + ((size_t)l << log_n), (1u << (log_n - 8)) + h, t, 32);
+    __syncthreads();
+    const size_t pt_words = (size_t)L << log_n, ct_words = 2 * pt_words;
+    const size_t row = ((size_t)l << log_n) + (size_t)h * 256;
+    double a0[kE8], a1[kE8];
+#pragma unroll
+    for (int k = 0; k < kE8; k++) a0[k] = a1[k] = 0.0;
+    for (uint32_t p = 0; p < P; p++) {
+        const uint64_t *src = colout + ((size_t)jj * P + p) * pt_words + row;
+        double x[kE8];
+#pragma unroll
+        for (int k = 0; k < kE8; k++) x[k] = nttc::Ar<true>::from_raw(src[nttc::u8<0>(t, k)]);
+        nttc::fwd8_256(x, tws[sub], tr[sub], t, ar);
+        nttc::b_to_a8(x, tr[sub], t);
+        const uint32_t pair = ib0 + p;
+        const double *xr = xrot + (size_t)((pair / bcount) * n1 + pair % bcount) * ct_words + row;
+#pragma unroll
+        for (int k = 0; k < kE8; k++) {
+            a0[k] += ar.mul(x[k], xr[nttc::u8<0>(t, k)]);
+            a1[k] += ar.mul(x[k], xr[pt_words + nttc::u8<0>(t, k)]);
+        }
+        if ((p & 3) == 3) {
+#pragma unroll
+            for (int k = 0; k < kE8; k++) {
+                a0[k] = ar.red(a0[k]);
+                a1[k] = ar.red(a1[k]);
+            }
+        }
+    }
+    const uint64_t q = mods[l].q;
+    uint64_t *dst = acc + (size_t)jj * ct_words + row;
+#pragma unroll
+    for (int k = 0; k < kE8; k++) {
+        const uint32_t u = nttc::u8<0>(t, k);
+        uint64_t r0 = ar.to_canon(a0[k]), r1 = ar.to_canon(a1[k]);
+        if (accumulate) {
+            r0 = addmod(r0, dst[u], q);
+            r1 = addmod(r1, dst[pt_words + u], q);
+        }
+        dst[u] = r0;
+        dst[pt_words + u] = r1;
+    }
+}
+
 // canonical residues -> the same values as doubles (exact below 2^53), in place
 __global__ __launch_bounds__(kThreads) void k_to_f64(uint64_t *v, size_t n)
 {
@@ -216,11 +290,16 @@ ckks_status launch_row_mac(ckks_ctx *ctx, uint64_t *acc, const uint64_t *colout,
     prof_begin(ctx, K_ROW_MAC, w * ((double)jc * P + 2.0 * P + 2.0 * jc * (accumulate ? 2 : 1)),
                res * (kOpsButterflyF64 * s2 / 2 + 15.5));
     hipError_t e = hipErrorInvalidValue;
-    switch (s2) {
+    if (s2 == 8) {
+        const uint32_t bpl = 1u << (ctx->log_n - 9), tiles = L * bpl;  // two rows per block
+        hipLaunchKernelGGL(k_row_mac8, dim3(jc * tiles), dim3(64), 0, ctx->stream, acc, colout, xrot, P, jc, ib0,
+                           bcount, n1, L, ctx->log_n, (int)accumulate, ctx->d_mod, ctx->d_twf, bpl,
+                           (int)(tiles % 8 == 0));
+        e = hipGetLastError();
+    } else switch (s2) {
     case 5: e = launch_row_mac_t<5>(ctx, acc, colout, xrot, P, jc, ib0, bcount, n1, L, accumulate); break;
     case 6: e = launch_row_mac_t<6>(ctx, acc, colout, xrot, P, jc, ib0, bcount, n1, L, accumulate); break;
     case 7: e = launch_row_mac_t<7>(ctx, acc, colout, xrot, P, jc, ib0, bcount, n1, L, accumulate); break;
-    case 8: e = launch_row_mac_t<8>(ctx, acc, colout, xrot, P, jc, ib0, bcount, n1, L, accumulate); break;
     }
     prof_end(ctx, K_ROW_MAC);
     if (e != hipSuccess) return set_error(CKKS_EHIP, "row/mac launch failed: %s", hipGetErrorString(e));

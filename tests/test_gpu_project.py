@@ -9,6 +9,7 @@
   output ciphertexts (a full tile of output blocks and a ragged one) and at most
   seven (input, baby step) pairs per launch, so partial sums are carried across
   launches of unequal sizes;
+* a ring of degree 2^10 (a 64-point second transform pass);
 * the Llama-shaped projection parameters at full ring degree (N = 2^16, 24 + 8
   limbs of 50-bit primes, dnum 3, level 12, 128 tokens x 256 features, n1 = 32,
   n2 = 8 so 31 baby and 7 giant rotations) on a 256 x 512 slice of the weights
@@ -100,6 +101,15 @@ def test_toy_projection_bsgs_tiles_and_carried_sums():
     cfg = dataclasses.replace(TOY, n1=16)
     err = run_case(cfg, 2 * cfg.feats, 17 * cfg.feats, [0, 13, 14, 16], max_pairs=7)
     say("toy BSGS max error vs X@W", err)
+    assert err <= 2.0 ** -12
+
+
+def test_small_ring_projection():
+    # N = 2^10: the transform's row pass has 64 points (the 16-residue fused kernel), other sizes use the
+    # 256-point one
+    cfg = dataclasses.replace(TOY, name="ring10", log_n=10, tokens=4, d_in=256, d_out=384, n1=16)
+    err = run_case(cfg, cfg.d_in, cfg.d_out, [0, 2])
+    say("N=2^10 max error vs X@W", err)
     assert err <= 2.0 ** -12
 
 
