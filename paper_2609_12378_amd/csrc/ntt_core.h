@@ -63,9 +63,10 @@ struct Ar<true> {
     }
     __device__ static E from_raw(uint64_t v) { return __longlong_as_double((long long)v); }
     __device__ static uint64_t to_raw(E x) { return (uint64_t)__double_as_longlong(x); }
-    // |x| < 2^52 -> |result| <= q/2 + 1
+    // |x| < 2^53 -> x mod q, exact, |result| <= q/2 + 2^-52 |x| + 1
     __device__ E red(E x) const { return fma(-rint(x * qinv), q, x); }
-    // |a| < 4q, 0 <= w < q -> a w mod q, exact, |result| < 2q
+    // 0 <= w < q, |a| <= 8q -> a w mod q, exact, |result| <= q/2 + 0.375 |a| (< 2q for |a| < 4q): the
+    // estimate h/q of the quotient is at most |a| in size with relative error 2^-52, and |l| <= ulp(h)/2
     __device__ E mul(E a, E w) const
     {
         const double h = a * w;
@@ -91,11 +92,19 @@ struct Ar<true> {
         const uint64_t r = csub(mag - mulhi64(mag, m.one_s) * m.q, m.q);
         return neg ? -(double)r : (double)r;
     }
-    // |X|, |Y| < 2q -> |X'|, |Y'| < 2q
+    // |X|, |Y| < 2q -> |X'|, |Y'| < 2q; in general |X'|, |Y'| <= q + 0.375 |Y|
     __device__ void ct(E &X, E &Y, W w) const
     {
         const double x = red(X);
         const double r = mul(Y, w);
+        X = x + r;
+        Y = x - r;
+    }
+    // the same without the range reduction of X: |X'|, |Y'| <= |X| + |mul(Y, w)|
+    __device__ void ct_lazy(E &X, E &Y, W w) const
+    {
+        const double r = mul(Y, w);
+        const double x = X;
         X = x + r;
         Y = x - r;
     }
@@ -218,8 +227,21 @@ size_t lds_bytes(uint32_t subs)
 // LDS addresses: the A -> C transpose XOR-swizzles u (conflict-free for both
 // patterns), the C -> B one pads a word every 8 (C conflict-free, B at most
 // two-way); kTr8 doubles per sub-transform.
+//
+// Lazy range reduction: a stage whose bit is clear in RMASK skips the
+// reduction of X (ct_lazy).  Magnitudes, in units of q (q < 2^50): mul(a, w)
+// returns |r| <= 0.5 + 0.375 |a| (the quotient estimate h/q, up to |a| q in
+// size, carries a relative error of 2^-52, and |l| <= ulp(h)/2); red(x) returns
+// <= 0.5 + 2^-52 |x|.  So a reducing stage maps a bound b on its inputs to
+// 1 + 0.375 b and a lazy one to 1.375 b + 0.5.  The projection uses RMASK =
+// 0x50 for the column pass (inputs reduced, <= 0.5; largest value 4.3, output
+// <= 4.3) and 0xAA for the row pass (inputs <= 4.3; largest 3.9, output <= 2.6),
+// then accumulates products of the outputs (each <= 1.5) four at a time onto a
+// reduced sum: every value stays below 6.4 q < 2^53, so all arithmetic is exact
+// integer arithmetic on doubles.
 constexpr int kE8 = 8;
 constexpr uint32_t kTr8 = 287;
+constexpr unsigned kColMask8 = 0x50, kRowMask8 = 0xAA;
 
 template <int LAY>
 __device__ __forceinline__ uint32_t u8(uint32_t t, int k)
@@ -230,7 +252,7 @@ __device__ __forceinline__ uint32_t u8(uint32_t t, int k)
 }
 
 // forward stage S on layout LAY (S in 0-2 for A, 3-5 for C, 6-7 for B)
-template <int LAY, int S>
+template <int LAY, int S, bool RED = true>
 __device__ __forceinline__ void fwd8_stage(double (&x)[kE8], const double *tws, uint32_t t, const Ar<true> &ar,
                                            uint32_t Bm = 1)
 {
@@ -241,7 +263,10 @@ __device__ __forceinline__ void fwd8_stage(double (&x)[kE8], const double *tws, 
     for (int k = 0; k < kE8; k++) {
         if (k & (1 << rb)) continue;
         const double w = tws[(1u << S) * Bm + (u8<LAY>(t, k) >> (b + 1))];
-        ar.ct(x[k], x[k | (1 << rb)], w);
+        if (RED)
+            ar.ct(x[k], x[k | (1 << rb)], w);
+        else
+            ar.ct_lazy(x[k], x[k | (1 << rb)], w);
     }
 }
 
@@ -249,31 +274,32 @@ __device__ __forceinline__ uint32_t pad_ac(uint32_t u) { return u ^ (((u >> 5) &
 __device__ __forceinline__ uint32_t pad_cb(uint32_t u) { return u + (u >> 3); }
 
 // all eight forward stages of the sub-transform held by thread t (layout A in,
-// layout B out); tr: this sub-transform's kTr8 doubles of LDS; every thread of
-// the block must call it (block barriers)
+// layout B out), reducing X at the stages set in RMASK; tr: this sub-transform's
+// kTr8 doubles of LDS; every thread of the block must call it (block barriers)
+template <unsigned RMASK>
 __device__ __forceinline__ void fwd8_256(double (&x)[kE8], const double *tws, double *tr, uint32_t t,
                                          const Ar<true> &ar, uint32_t Bm = 1)
 {
-    fwd8_stage<0, 0>(x, tws, t, ar, Bm);
-    fwd8_stage<0, 1>(x, tws, t, ar, Bm);
-    fwd8_stage<0, 2>(x, tws, t, ar, Bm);
+    fwd8_stage<0, 0, (RMASK >> 0) & 1>(x, tws, t, ar, Bm);
+    fwd8_stage<0, 1, (RMASK >> 1) & 1>(x, tws, t, ar, Bm);
+    fwd8_stage<0, 2, (RMASK >> 2) & 1>(x, tws, t, ar, Bm);
 #pragma unroll
     for (int k = 0; k < kE8; k++) tr[pad_ac(u8<0>(t, k))] = x[k];
     __syncthreads();
 #pragma unroll
     for (int k = 0; k < kE8; k++) x[k] = tr[pad_ac(u8<1>(t, k))];
     __syncthreads();
-    fwd8_stage<1, 3>(x, tws, t, ar, Bm);
-    fwd8_stage<1, 4>(x, tws, t, ar, Bm);
-    fwd8_stage<1, 5>(x, tws, t, ar, Bm);
+    fwd8_stage<1, 3, (RMASK >> 3) & 1>(x, tws, t, ar, Bm);
+    fwd8_stage<1, 4, (RMASK >> 4) & 1>(x, tws, t, ar, Bm);
+    fwd8_stage<1, 5, (RMASK >> 5) & 1>(x, tws, t, ar, Bm);
 #pragma unroll
     for (int k = 0; k < kE8; k++) tr[pad_cb(u8<1>(t, k))] = x[k];
     __syncthreads();
 #pragma unroll
     for (int k = 0; k < kE8; k++) x[k] = tr[pad_cb(u8<2>(t, k))];
     __syncthreads();
-    fwd8_stage<2, 6>(x, tws, t, ar, Bm);
-    fwd8_stage<2, 7>(x, tws, t, ar, Bm);
+    fwd8_stage<2, 6, (RMASK >> 6) & 1>(x, tws, t, ar, Bm);
+    fwd8_stage<2, 7, (RMASK >> 7) & 1>(x, tws, t, ar, Bm);
 }
 
 // layout B -> layout A through LDS (a word of padding every 32), so that

@@ -222,7 +222,7 @@ __global__ __launch_bounds__(64) void k_row_mac8(uint64_t *acc, const uint64_t *
         double x[kE8];
 #pragma unroll
         for (int k = 0; k < kE8; k++) x[k] = nttc::Ar<true>::from_raw(src[nttc::u8<0>(t, k)]);
-        nttc::fwd8_256(x, tws[sub], tr[sub], t, ar);
+        nttc::fwd8_256<nttc::kRowMask8>(x, tws[sub], tr[sub], t, ar);
         nttc::b_to_a8(x, tr[sub], t);
         const uint32_t pair = ib0 + p;
         const double *xr = xrot + (size_t)((pair / bcount) * n1 + pair % bcount) * ct_words + row;
@@ -284,11 +284,13 @@ ckks_status launch_row_mac(ckks_ctx *ctx, uint64_t *acc, const uint64_t *colout,
     ntt_split(ctx->log_n, &s1, &s2);
     // column-pass rows (jc x P), rotated inputs (P ciphertexts), accumulators written (and read when accumulating)
     const double w = 8.0 * L * ctx->n;
-    // per plaintext residue: the row pass's butterflies, two exact products and additions (14), and the range
-    // reduction of both sums every 4 pairs (1.5)
+    // per plaintext residue: the row pass's butterflies (the 8-residue kernel skips the reduction of X in half
+    // of its stages), two exact products and additions (14), and the range reduction of both sums every 4 pairs
+    // (1.5)
     const double res = (double)jc * P * L * ctx->n;
+    const double bf_ops = s2 == 8 ? (4 * kOpsButterflyF64 + 4 * (kOpsButterflyF64 - 3)) / 2 : kOpsButterflyF64 * s2 / 2;
     prof_begin(ctx, K_ROW_MAC, w * ((double)jc * P + 2.0 * P + 2.0 * jc * (accumulate ? 2 : 1)),
-               res * (kOpsButterflyF64 * s2 / 2 + 15.5));
+               res * (bf_ops + 15.5));
     hipError_t e = hipErrorInvalidValue;
     if (s2 == 8) {
         const uint32_t bpl = 1u << (ctx->log_n - 9), tiles = L * bpl;  // two rows per block
