@@ -107,6 +107,117 @@ __global__ __launch_bounds__(kThreads) void k_fft_a(double2 *a, const double2 *_
     }
 }
 
+// Pass A for 2048-point blocks from the projection's diagonal layout, with the
+// butterflies three stages at a time in registers: 256 threads hold 8 points
+// each, in four layouts whose register bits are the position bits of the
+// stages they run (L1: bits 0-2, stages 1-3; L2: bits 3-5; L3: bits 6-8; L4:
+// bits 9, 10 and 0, stages 10-11); three LDS transposes with XOR swizzles
+// (conflict-free for all six access patterns) connect them.  Each butterfly is
+// the same arithmetic as in k_fft_a, so the results are identical.  The
+// plaintext's D weights are read once (one contiguous diagonal of Wd) into LDS
+// and spread over the block's positions through feat_of_pos.
+template <int LAY>
+__device__ __forceinline__ uint32_t posA(uint32_t t, int r)
+{
+    if (LAY == 1) return (t << 3) | (uint32_t)r;
+    if (LAY == 2) return ((t >> 3) << 6) | ((uint32_t)r << 3) | (t & 7u);
+    if (LAY == 3) return ((t >> 6) << 9) | ((uint32_t)r << 6) | (t & 63u);
+    return ((uint32_t)(r >> 1) << 9) | (t << 1) | (uint32_t)(r & 1);
+}
+__device__ __forceinline__ uint32_t swz_a(uint32_t x) { return x ^ ((x >> 3) & 15u); }
+__device__ __forceinline__ uint32_t swz_b(uint32_t x) { return x ^ ((x >> 1) & 15u); }
+
+template <int LAY, int LS>
+__device__ __forceinline__ void fft8_stage(double2 (&v)[8], const double2 *__restrict__ w, uint32_t t, uint32_t logm)
+{
+    constexpr uint32_t half = 1u << (LS - 1);
+    constexpr int xb = LS - 1;
+    constexpr int rb = LAY == 1 ? xb : LAY == 2 ? xb - 3 : LAY == 3 ? xb - 6 : xb - 8;
+    static_assert(rb >= 0 && rb < 3 && (LAY != 4 || xb >= 9), "stage not in this layout");
+    const uint32_t step = (1u << logm) >> LS;
+#pragma unroll
+    for (int r = 0; r < 8; r++) {
+        if (r & (1 << rb)) continue;
+        const uint32_t k = posA<LAY>(t, r) & (half - 1);
+        const double2 tt = cmul(w[k * step], v[r | (1 << rb)]);
+        const double2 u = v[r];
+        v[r] = make_double2(u.x + tt.x, u.y + tt.y);
+        v[r | (1 << rb)] = make_double2(u.x - tt.x, u.y - tt.y);
+    }
+}
+
+template <int LA, int LB, bool SWB>
+__device__ __forceinline__ void fft8_transpose(double2 (&v)[8], double2 *sh, uint32_t t)
+{
+#pragma unroll
+    for (int r = 0; r < 8; r++) {
+        const uint32_t x = posA<LA>(t, r);
+        sh[SWB ? swz_b(x) : swz_a(x)] = v[r];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < 8; r++) {
+        const uint32_t x = posA<LB>(t, r);
+        v[r] = sh[SWB ? swz_b(x) : swz_a(x)];
+    }
+    __syncthreads();
+}
+
+__global__ __launch_bounds__(256) void k_fft_a8(double2 *a, const double2 *__restrict__ w, uint32_t logm, int mode,
+                                                const double2 *__restrict__ twist, double c, int64_t *m,
+                                                SlotSource ss)
+{
+    __shared__ double2 sh[2048];
+    __shared__ double vals[256];
+    const uint32_t M = 1u << logm, blocks_per = M >> 11;
+    const uint32_t p = blockIdx.x / blocks_per, blk = blockIdx.x % blocks_per, t = threadIdx.x;
+    const uint32_t D = ss.feats;
+    const uint32_t jb = ss.j0 + p / ss.pairs, pair = ss.ib0 + p % ss.pairs;
+    const uint32_t i = pair / ss.bcount, b = pair % ss.bcount;
+    const double *dg = ss.Wd + (((size_t)jb * ss.n_in + i) * D + ss.n1g + b) * D;
+    for (uint32_t o = t; o < D; o += 256) vals[o] = dg[o];
+    __syncthreads();
+    // slot f*T + t' holds diagonal entry (f - n1 g) mod D
+    const uint32_t shift = D - ss.n1g % D, mask = D - 1;
+    const uint32_t *fp = ss.feat_of_pos + ((size_t)blk << 11);
+    double2 v[8];
+#pragma unroll
+    for (int r = 0; r < 8; r++) v[r] = make_double2(vals[(fp[posA<1>(t, r)] + shift) & mask], 0.0);
+    fft8_stage<1, 1>(v, w, t, logm);
+    fft8_stage<1, 2>(v, w, t, logm);
+    fft8_stage<1, 3>(v, w, t, logm);
+    fft8_transpose<1, 2, false>(v, sh, t);
+    fft8_stage<2, 4>(v, w, t, logm);
+    fft8_stage<2, 5>(v, w, t, logm);
+    fft8_stage<2, 6>(v, w, t, logm);
+    fft8_transpose<2, 3, false>(v, sh, t);
+    fft8_stage<3, 7>(v, w, t, logm);
+    fft8_stage<3, 8>(v, w, t, logm);
+    fft8_stage<3, 9>(v, w, t, logm);
+    fft8_transpose<3, 4, true>(v, sh, t);
+    fft8_stage<4, 10>(v, w, t, logm);
+    fft8_stage<4, 11>(v, w, t, logm);
+    if (mode == 0) {
+        double2 *dst = a + (size_t)p * M + ((size_t)blk << 11);
+#pragma unroll
+        for (int r = 0; r < 8; r++) dst[posA<4>(t, r)] = v[r];
+    } else {
+#pragma unroll
+        for (int r = 0; r < 8; r++) {
+            const uint32_t x = posA<4>(t, r);
+            round_out(m, (size_t)p * 2 * M, x, M, v[r], twist[x], c);
+        }
+    }
+}
+
+// feat_of_pos[x] = slot index at FFT position x, divided by the token count
+__global__ __launch_bounds__(kThreads) void k_feat_of_pos(uint32_t *out, const uint32_t *__restrict__ slot_of_pos,
+                                                          uint32_t M, uint32_t tokens)
+{
+    const uint32_t x = blockIdx.x * kThreads + threadIdx.x;
+    if (x < M) out[x] = slot_of_pos[x] / tokens;
+}
+
 // Pass B: stages len = 2^(logb+1) .. M; thread owns column c (points h*B + c, h < 2^HB).
 template <int HB>
 __global__ __launch_bounds__(kThreads) void k_fft_b(double2 *a, const double2 *__restrict__ w, uint32_t logm,
@@ -232,9 +343,14 @@ ckks_status fft_passes(ckks_ctx *ctx, double2 *work, uint32_t batch, int mode, d
                                   : bytes;
     SlotSource none;
     prof_begin(ctx, K_FFT_A, bytes_a);
-    hipLaunchKernelGGL(k_fft_a, dim3(batch * (M >> logb)), dim3(kThreads), B * sizeof(double2), ctx->stream, work,
-                       ctx->d_fft_w, logm, logb, single ? mode : 0, ctx->d_fft_twist, c, m, gather ? 1 : 0,
-                       gather ? *gather : none, ctx->d_pos_slot);
+    if (gather && gather->Wd && logb == (uint32_t)kLogBA) {
+        hipLaunchKernelGGL(k_fft_a8, dim3(batch * (M >> logb)), dim3(256), 0, ctx->stream, work, ctx->d_fft_w, logm,
+                           single ? mode : 0, ctx->d_fft_twist, c, m, *gather);
+    } else {
+        hipLaunchKernelGGL(k_fft_a, dim3(batch * (M >> logb)), dim3(kThreads), B * sizeof(double2), ctx->stream,
+                           work, ctx->d_fft_w, logm, logb, single ? mode : 0, ctx->d_fft_twist, c, m, gather ? 1 : 0,
+                           gather ? *gather : none, ctx->d_pos_slot);
+    }
     prof_end(ctx, K_FFT_A);
     if (!single) {
         const uint32_t hb = logm - logb;
@@ -262,6 +378,15 @@ ckks_status enc_coeffs(ckks_ctx *ctx, const SlotSource &src, uint32_t batch, dou
 {
     if (!batch) return CKKS_OK;
     return fft_passes(ctx, work, batch, 1, scale * (2.0 / (double)ctx->n), m_out, &src);
+}
+
+ckks_status enc_feat_of_pos(ckks_ctx *ctx, uint32_t tokens, uint32_t *out)
+{
+    const uint32_t M = ctx->n / 2;
+    hipLaunchKernelGGL(k_feat_of_pos, dim3((M + kThreads - 1) / kThreads), dim3(kThreads), 0, ctx->stream, out,
+                       ctx->d_pos_slot, M, tokens);
+    HIP_TRY(hipGetLastError());
+    return CKKS_OK;
 }
 
 ckks_status enc_to_rns(ckks_ctx *ctx, const int64_t *m, uint32_t batch, uint32_t limbs, uint64_t *out)

@@ -57,10 +57,17 @@ struct SlotSource {
     uint32_t d_out = 0, tokens = 0, feats = 0;
     uint32_t n1g = 0, bcount = 0;
     uint32_t j0 = 0, ib0 = 0, pairs = 1;
+    // optional, for feats <= 256 and N >= 2^12: W re-laid as its cyclic diagonals,
+    // Wd[((jb * n_in + i) * D + k) * D + o] = D_k(A_{jb,i})[o], and feat_of_pos[x] = (slot at FFT position x) / tokens
+    const double *Wd = nullptr;
+    const uint32_t *feat_of_pos = nullptr;
+    uint32_t n_in = 0;
 };
 // m_out: [batch][N] int64 rounded coefficients; work: [batch][N/2] double2
 ckks_status enc_coeffs(ckks_ctx *ctx, const SlotSource &src, uint32_t batch, double scale, double2 *work,
                        int64_t *m_out);
+// out[x] = (slot index held at FFT position x) / tokens, x < N/2
+ckks_status enc_feat_of_pos(ckks_ctx *ctx, uint32_t tokens, uint32_t *out);
 // residues of m ([batch][N]) into out ([batch][limbs][N]), primes 0..limbs-1
 ckks_status enc_to_rns(ckks_ctx *ctx, const int64_t *m, uint32_t batch, uint32_t limbs, uint64_t *out);
 size_t enc_work_bytes(const ckks_ctx *ctx, uint32_t batch);

@@ -254,6 +254,19 @@ __global__ __launch_bounds__(64) void k_row_mac8(uint64_t *acc, const uint64_t *
     }
 }
 
+// W (d_in x d_out, row-major) -> its cyclic diagonals per block pair:
+// Wd[((jb * n_in + i) * D + k) * D + o] = D_k(A_{jb,i})[o] = W[(i D + (k + o) mod D) * d_out + jb D + o]
+__global__ __launch_bounds__(kThreads) void k_diag_layout(double *Wd, const double *__restrict__ W, uint32_t D,
+                                                          uint32_t n_in, uint32_t d_out, size_t total)
+{
+    const size_t e = (size_t)blockIdx.x * kThreads + threadIdx.x;
+    if (e >= total) return;
+    const uint32_t o = (uint32_t)(e % D), k = (uint32_t)((e / D) % D);
+    const size_t bi = e / ((size_t)D * D);
+    const uint32_t i = (uint32_t)(bi % n_in), jb = (uint32_t)(bi / n_in);
+    Wd[e] = W[((size_t)i * D + (k + o) % D) * d_out + (size_t)jb * D + o];
+}
+
 // canonical residues -> the same values as doubles (exact below 2^53), in place
 __global__ __launch_bounds__(kThreads) void k_to_f64(uint64_t *v, size_t n)
 {
@@ -396,7 +409,10 @@ extern "C" ckks_status ckks_linear_project(ckks_ctx *ctx, const ckks_buf *in, co
     const size_t m_w = (size_t)Jt * Pb * N;                       // int64 coefficients
     const size_t fft_w = (size_t)Jt * Pb * (N / 2) * 2;            // double2 per slot
     const size_t ks_w = ks_scratch_words(ctx, level, ks_rot_batch(n1 > 1 ? n1 - 1 : 1));
-    const size_t total = xrot_w + acc_w + tot_w + rot_w + pt_w + m_w + fft_w + ks_w;
+    // W re-laid as its cyclic diagonals, and the feature index of every FFT position, for the radix-8 FFT pass
+    const bool diag = D <= 256 && ctx->log_n >= 12;
+    const size_t wd_w = diag ? (size_t)shape->d_in * shape->d_out : 0, fop_w = diag ? N / 4 : 0;
+    const size_t total = xrot_w + acc_w + tot_w + rot_w + pt_w + m_w + fft_w + ks_w + wd_w + fop_w;
     void *w;
     CK_TRY(ctx_scratch(ctx, total * 8, &w));
     uint64_t *xrot = (uint64_t *)w;
@@ -407,6 +423,17 @@ extern "C" ckks_status ckks_linear_project(ckks_ctx *ctx, const ckks_buf *in, co
     int64_t *mint = (int64_t *)(pts + pt_w);
     double2 *fft = (double2 *)(mint + m_w);
     uint64_t *ksw = (uint64_t *)(fft) + fft_w;
+    double *Wd = (double *)(ksw + ks_w);
+    uint32_t *fop = (uint32_t *)(ksw + ks_w + wd_w);
+    if (diag) {
+        const size_t tot_e = wd_w;
+        prof_begin(ctx, K_ELEM, 16.0 * tot_e);
+        hipLaunchKernelGGL(k_diag_layout, dim3((unsigned)((tot_e + kThreads - 1) / kThreads)), dim3(kThreads), 0,
+                           ctx->stream, Wd, W, D, n_in, shape->d_out, tot_e);
+        prof_end(ctx, K_ELEM);
+        HIP_TRY(hipGetLastError());
+        CK_TRY(enc_feat_of_pos(ctx, T, fop));
+    }
 
     // ---- 1. baby-step rotations, hoisted per input ciphertext
     for (uint32_t i = 0; i < n_in; i++) {
@@ -451,6 +478,11 @@ extern "C" ckks_status ckks_linear_project(ckks_ctx *ctx, const ckks_buf *in, co
                 src.j0 = j0;
                 src.ib0 = pb0;
                 src.pairs = P;
+                if (diag) {
+                    src.Wd = Wd;
+                    src.feat_of_pos = fop;
+                    src.n_in = n_in;
+                }
                 const uint32_t batch = jc * P;
                 CK_TRY(enc_coeffs(ctx, src, batch, delta_w, fft, mint));
                 if (fused) {
