@@ -52,6 +52,9 @@ struct ConvDev {
     uint8_t dst[kMaxPrimes];
     ulonglong2 *d_qhat_inv = nullptr;  // [ns] (value, Shoup companion) mod src_i
     ulonglong2 *d_qhat_mod = nullptr;  // [ns][nt] (value, Shoup companion) mod dst_t
+    bool f64 = false;                  // primes below 2^50, sources below twice the targets: fp64 tables set
+    double *d_qhat_inv_f = nullptr;    // [ns] the values of d_qhat_inv as doubles
+    double *d_qhat_mod_f = nullptr;    // [ns][nt] the values of d_qhat_mod as doubles
 };
 
 // Kernels timed by the optional event profiler.  Each launch is bracketed by
@@ -145,6 +148,9 @@ ckks_status launch_ntt_from_i64(ckks_ctx *ctx, const int64_t *m, uint64_t *out, 
 void ntt_split(uint32_t log_n, int *s1, int *s2);
 // the transforms over primes 0..limbs-1 use the fp64 butterflies
 bool ntt_uses_f64(const ckks_ctx *ctx, uint32_t limbs);
+// column pass only of a forward transform (fp64 primes, two-pass sizes); the rows are left as raw doubles
+ckks_status launch_ntt_fwd_first_pass(ckks_ctx *ctx, uint64_t *data, uint32_t batch, uint32_t bstride,
+                                      const LimbMap &map);
 // column pass only of launch_ntt_from_i64 (two-pass sizes); the rows stay in the inter-pass form
 ckks_status launch_ntt_col_i64(ckks_ctx *ctx, const int64_t *m, uint64_t *out, uint32_t batch, uint32_t limbs);
 // nominal VALU instructions of one radix-2 butterfly: fp64 (product with FMA

@@ -241,6 +241,26 @@ static ckks_status make_conv(ckks_ctx *c, const std::vector<uint32_t> &src, cons
     for (size_t t = 0; t < dst.size(); t++) out->dst[t] = (uint8_t)dst[t];
     CK_TRY(upload((void **)&out->d_qhat_inv, qinv.data(), qinv.size() * sizeof(ulonglong2)));
     CK_TRY(upload((void **)&out->d_qhat_mod, qmod.data(), qmod.size() * sizeof(ulonglong2)));
+    // fp64 conversion: every prime below 2^50 and every source prime below twice every target prime (so the
+    // canonical y_i < 2 q_t and the sums stay exact)
+    out->f64 = true;
+    uint64_t max_src = 0, min_dst = ~0ull;
+    for (uint32_t v : src) {
+        out->f64 = out->f64 && c->f64_ok[v];
+        max_src = std::max(max_src, c->primes[v]);
+    }
+    for (uint32_t v : dst) {
+        out->f64 = out->f64 && c->f64_ok[v];
+        min_dst = std::min(min_dst, c->primes[v]);
+    }
+    out->f64 = out->f64 && !dst.empty() && max_src / 2 < min_dst;
+    if (out->f64) {
+        std::vector<double> fi(qinv.size()), fm(qmod.size());
+        for (size_t k = 0; k < qinv.size(); k++) fi[k] = (double)qinv[k].x;
+        for (size_t k = 0; k < qmod.size(); k++) fm[k] = (double)qmod[k].x;
+        CK_TRY(upload((void **)&out->d_qhat_inv_f, fi.data(), fi.size() * sizeof(double)));
+        CK_TRY(upload((void **)&out->d_qhat_mod_f, fm.data(), fm.size() * sizeof(double)));
+    }
     return CKKS_OK;
 }
 
@@ -403,6 +423,8 @@ void ckks_ctx_destroy(ckks_ctx *c)
     for (auto &kv : c->conv) {
         if (kv.second.d_qhat_inv) (void)hipFree(kv.second.d_qhat_inv);
         if (kv.second.d_qhat_mod) (void)hipFree(kv.second.d_qhat_mod);
+        if (kv.second.d_qhat_inv_f) (void)hipFree(kv.second.d_qhat_inv_f);
+        if (kv.second.d_qhat_mod_f) (void)hipFree(kv.second.d_qhat_mod_f);
     }
     delete c;
 }

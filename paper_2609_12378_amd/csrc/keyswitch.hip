@@ -15,6 +15,7 @@
 // (ns <= 8 at the benchmark parameters) is far too small and too wide-integer
 // for the matrix cores, so it runs on the vector ALUs.
 #include "ckks_internal.h"
+#include "ntt_core.h"
 #include "ops.h"
 
 namespace {
@@ -84,6 +85,55 @@ __global__ __launch_bounds__(kThreads) void k_conv(const uint64_t *in, uint32_t 
     }
 }
 
+// The same conversion in fp64 (every prime below 2^50): y_i = x_i * qhat_inv_i mod s_i is made canonical by
+// adding s_i to a negative result (|mul| < s_i for canonical operands), then each target sums the products
+// y_i * [Qhat_i]_t (each < 1.25 t, since y_i < 2^50 < 2 t) with a range reduction every four terms (sums stay
+// below 5.5 t < 2^53) and writes the canonical residue: the same integers as k_conv.
+template <int NS_MAX>
+__global__ __launch_bounds__(kThreads) void k_conv_f64(const uint64_t *in, uint32_t in_stride, uint64_t *out,
+                                                        uint32_t out_stride, uint32_t split, uint32_t skip,
+                                                        ConvArgs a, const double *__restrict__ qhat_inv,
+                                                        const double *__restrict__ qhat_mod,
+                                                        const ModQ *__restrict__ mods, uint32_t log_n)
+{
+    __shared__ double s_mod[NS_MAX * kMaxPrimes];
+    __shared__ double2 s_tq[kMaxPrimes];
+    const int ns = a.ns, nt = a.nt;
+    for (int k = threadIdx.x; k < ns * nt; k += kThreads) s_mod[k] = qhat_mod[k];
+    for (int k = threadIdx.x; k < nt; k += kThreads) s_tq[k] = make_double2(mods[a.dst[k]].qd, mods[a.dst[k]].qinvd);
+    __syncthreads();
+    const uint32_t n = 1u << log_n;
+    const uint32_t col = blockIdx.x * kThreads + threadIdx.x;
+    const uint32_t poly = blockIdx.y;
+    if (col >= n) return;
+    const uint64_t *src = in + ((size_t)poly * in_stride << log_n) + col;
+    double y[NS_MAX];
+#pragma unroll
+    for (int i = 0; i < NS_MAX; i++) {
+        if (i < ns) {
+            const nttc::Ar<true> ar(mods[a.src[i]]);
+            const double v = ar.mul(nttc::Ar<true>::from_u64(src[(size_t)i << log_n]), qhat_inv[i]);
+            y[i] = v < 0.0 ? v + ar.q : v;
+        }
+    }
+    uint64_t *dst = out + ((size_t)poly * out_stride << log_n) + col;
+    for (int t = 0; t < nt; t++) {
+        nttc::Ar<true> ar;
+        ar.q = s_tq[t].x;
+        ar.qinv = s_tq[t].y;
+        double acc = 0.0;
+#pragma unroll
+        for (int i = 0; i < NS_MAX; i++) {
+            if (i < ns) {
+                acc += ar.mul(y[i], s_mod[i * nt + t]);
+                if ((i & 3) == 3) acc = ar.red(acc);
+            }
+        }
+        const uint32_t row = t < (int)split ? t : t + skip;
+        dst[(size_t)row << log_n] = ar.to_canon(acc);
+    }
+}
+
 // u[k][r][n] = sum_{j<nd} d_j[r][sigma(n)] * key[j][k][krow(r)][n], rows r over Q_level u P
 __global__ __launch_bounds__(kThreads) void k_key_ip(const uint64_t *__restrict__ digits,
                                                       const uint64_t *__restrict__ key, uint64_t *u, uint32_t nd,
@@ -142,15 +192,17 @@ struct RotArgs {
     uint64_t *out[kRotBatch];
 };
 
-// u[r][k][row][n] = sum_j d_j[row][sigma_{g_r}(n)] * key_r[j][k][krow][n]
+// u[r][k][row - row0][n] = sum_j d_j[row][sigma_{g_r}(n)] * key_r[j][k][krow][n] for rows row0 .. row0 + rows - 1
+// of Q_level u P (u holds `rows` rows per polynomial)
 __global__ __launch_bounds__(kThreads) void k_key_ip_batch(const uint64_t *__restrict__ digits, RotArgs ra,
                                                             uint64_t *u, uint32_t nd, uint32_t ext, uint32_t level,
-                                                            uint32_t n_q, uint32_t key_rows,
-                                                            const ModQ *__restrict__ mods, uint32_t log_n)
+                                                            uint32_t n_q, uint32_t key_rows, uint32_t row0,
+                                                            uint32_t rows, const ModQ *__restrict__ mods,
+                                                            uint32_t log_n)
 {
     const uint32_t n = 1u << log_n;
     const uint32_t col = blockIdx.x * kThreads + threadIdx.x;
-    const uint32_t row = blockIdx.y, r = blockIdx.z;
+    const uint32_t row = row0 + blockIdx.y, r = blockIdx.z;
     if (col >= n) return;
     const uint32_t prime = row <= level ? row : n_q + (row - level - 1);
     const ModQ m = mods[prime];
@@ -163,9 +215,75 @@ __global__ __launch_bounds__(kThreads) void k_key_ip_batch(const uint64_t *__res
         mac(a0, d, key[kb + col]);
         mac(a1, d, key[kb + ((size_t)key_rows << log_n) + col]);
     }
-    uint64_t *ur = u + (((size_t)r * 2 * ext + row) << log_n) + col;
+    uint64_t *ur = u + (((size_t)r * 2 * rows + (row - row0)) << log_n) + col;
     ur[0] = reduce128(a0, m);
-    ur[(size_t)ext << log_n] = reduce128(a1, m);
+    ur[(size_t)rows << log_n] = reduce128(a1, m);
+}
+
+// ModDown of a batch of rotations, fused (fp64, 256-point rows): block (r, q-limb i, two rows h) finishes the
+// forward transform of the converted P part cw[r][k][i] (its first pass already done), computes the q-limb part
+// of the key inner product u_k = sum_j sigma_{g_r}(d_j)[i] * key_r[j][k][i] in registers, and writes
+//   out_r[k][i] = (u_k - NTT(cw[r][k][i])) * P^-1 (+ sigma_{g_r}(c0)[i] for k = 0),
+// so neither the q-limb rows of u nor the transformed conversion ever go to HBM.  Magnitudes (units of q):
+// transform outputs <= 2.5 (row pass after a reducing first pass), each product <= 0.875 and the sum range-reduced
+// every 4 digits (<= 4), differences <= 6.5, P^-1 products <= 3, plus c0 < 1: all below 8 q = 2^53.
+__global__ __launch_bounds__(64) void k_ks_finish8(RotArgs ra, const uint64_t *__restrict__ cw,
+                                                   const uint64_t *__restrict__ digits,
+                                                   const uint64_t *__restrict__ c0, uint32_t nd, uint32_t ext,
+                                                   uint32_t L, uint32_t key_rows, const ModQ *__restrict__ mods,
+                                                   const double *__restrict__ twf,
+                                                   const ulonglong2 *__restrict__ pinv, uint32_t log_n,
+                                                   uint32_t blocks_per_limb)
+{
+    using nttc::kE8;
+    __shared__ double tws[2][257];
+    __shared__ double tr[2][nttc::kTr8];
+    const uint32_t per_rot = L * blocks_per_limb;
+    const uint32_t r = blockIdx.x / per_rot, rem = blockIdx.x % per_rot;
+    const uint32_t i = rem / blocks_per_limb, blk = rem % blocks_per_limb;
+    const nttc::Ar<true> ar(mods[i]);
+    const uint32_t sub = threadIdx.x >> 5, t = threadIdx.x & 31;
+    const uint32_t h = blk * 2 + sub;
+    nttc::stage_twiddles8(tws[sub], twf + ((size_t)i << log_n), (1u << (log_n - 8)) + h, t, 32);
+    __syncthreads();
+    const size_t row = ((size_t)i << log_n) + (size_t)h * 256;
+    double v[2][kE8];
+#pragma unroll
+    for (int k = 0; k < 2; k++) {
+        const uint64_t *src = cw + (((size_t)r * 2 + k) * L << log_n) + row;
+        double x[kE8];
+#pragma unroll
+        for (int e = 0; e < kE8; e++) x[e] = nttc::Ar<true>::from_raw(src[nttc::u8<0>(t, e)]);
+        nttc::fwd8_256<nttc::kRowMask8>(x, tws[sub], tr[sub], t, ar);
+        nttc::b_to_a8(x, tr[sub], t);
+#pragma unroll
+        for (int e = 0; e < kE8; e++) v[k][e] = x[e];
+    }
+    const uint32_t g = ra.g[r];
+    const uint64_t *key = ra.key[r];
+    uint64_t *out = ra.out[r];
+    const double pi = (double)pinv[i].x;
+    const size_t kstride = (size_t)key_rows << log_n;
+#pragma unroll
+    for (int e = 0; e < kE8; e++) {
+        const uint32_t pos = h * 256 + nttc::u8<0>(t, e);
+        const uint32_t sc = auto_index(pos, g, log_n);
+        double u0 = 0.0, u1 = 0.0;
+        for (uint32_t j = 0; j < nd; j++) {
+            const double d = nttc::Ar<true>::from_u64(digits[(((size_t)j * ext + i) << log_n) + sc]);
+            const uint64_t *kj = key + (((size_t)j * 2 * key_rows + i) << log_n) + pos;
+            u0 += ar.mul(d, nttc::Ar<true>::from_u64(kj[0]));
+            u1 += ar.mul(d, nttc::Ar<true>::from_u64(kj[kstride]));
+            if ((j & 3) == 3) {
+                u0 = ar.red(u0);
+                u1 = ar.red(u1);
+            }
+        }
+        const double r0 = ar.mul(u0 - v[0][e], pi) + nttc::Ar<true>::from_u64(c0[((size_t)i << log_n) + sc]);
+        const double r1 = ar.mul(u1 - v[1][e], pi);
+        out[((size_t)i << log_n) + pos] = ar.to_canon(r0);
+        out[(((size_t)L + i) << log_n) + pos] = ar.to_canon(r1);
+    }
 }
 
 // out_r[k][i][n] = (u[r][k][i][n] - c[r][k][i][n]) * P^-1 (+ c0[i][sigma_{g_r}(n)] for k = 0)
@@ -198,7 +316,14 @@ ckks_status launch_conv(ckks_ctx *ctx, const ConvDev *cd, const uint64_t *in, ui
     for (int t = 0; t < cd->nt; t++) a.dst[t] = cd->dst[t];
     const dim3 grid((ctx->n + kThreads - 1) / kThreads, polys), block(kThreads);
     prof_begin(ctx, K_CONV, 8.0 * polys * (a.ns + a.nt) * ctx->n);
-    if (a.ns <= 4)
+    if (cd->f64 && !ctx->int_only && a.ns <= 16) {
+        if (a.ns <= 8)
+            hipLaunchKernelGGL(k_conv_f64<8>, grid, block, 0, ctx->stream, in, in_stride, out, out_stride, split,
+                               skip, a, cd->d_qhat_inv_f, cd->d_qhat_mod_f, ctx->d_mod, ctx->log_n);
+        else
+            hipLaunchKernelGGL(k_conv_f64<16>, grid, block, 0, ctx->stream, in, in_stride, out, out_stride, split,
+                               skip, a, cd->d_qhat_inv_f, cd->d_qhat_mod_f, ctx->d_mod, ctx->log_n);
+    } else if (a.ns <= 4)
         hipLaunchKernelGGL(k_conv<4>, grid, block, 0, ctx->stream, in, in_stride, out, out_stride, split, skip, a,
                            cd->d_qhat_inv, cd->d_qhat_mod, ctx->d_mod, ctx->log_n);
     else if (a.ns <= 8)
@@ -246,13 +371,43 @@ ckks_status ks_rotate_batch(ckks_ctx *ctx, const uint64_t *c, uint32_t level, co
         ra.key[r] = keys[r];
         ra.out[r] = outs[r];
     }
+    int s1, s2;
+    ntt_split(ctx->log_n, &s1, &s2);
+    if (s2 == 8 && ntt_uses_f64(ctx, L)) {
+        // fused ModDown: only the P rows of u are formed in HBM
+        uint64_t *up = work;                             // [count][2][K][N]
+        uint64_t *cw = up + (size_t)count * 2 * K * N;   // [count][2][L][N]
+        {
+            const dim3 grid((ctx->n + kThreads - 1) / kThreads, K, count), block(kThreads);
+            prof_begin(ctx, K_KEYIP, 8.0 * ctx->n * K * (count * (2.0 * nd + 2.0) + nd));
+            hipLaunchKernelGGL(k_key_ip_batch, grid, block, 0, ctx->stream, digits, ra, up, nd, ext, level, ctx->n_q,
+                               ctx->n_primes(), L, K, ctx->d_mod, ctx->log_n);
+            prof_end(ctx, K_KEYIP);
+            HIP_TRY(hipGetLastError());
+        }
+        CK_TRY(launch_ntt_strided(ctx, up, 2 * count, K, limb_range(ctx->n_q, K), true));
+        const ConvDev *cd;
+        CK_TRY(ctx_conv(ctx, (int)level, -1, &cd));
+        CK_TRY(launch_conv(ctx, cd, up, K, cw, L, L, 0, 2 * count));
+        CK_TRY(launch_ntt_fwd_first_pass(ctx, cw, 2 * count, L, limb_range(0, L)));
+        const uint32_t bpl = 1u << (ctx->log_n - 9);
+        // cw rows once, the key's q rows, the outputs; digits and c0 are cache-resident gathers
+        const double res = (double)count * L * N;
+        prof_begin(ctx, K_MODDOWN, 8.0 * res * (2.0 + 2.0 * nd + 2.0),
+                   res * (2 * (4 * kOpsButterflyF64 + 4 * (kOpsButterflyF64 - 3)) / 2 + nd * 2 * 10.0 + 40.0));
+        hipLaunchKernelGGL(k_ks_finish8, dim3(count * L * bpl), dim3(64), 0, ctx->stream, ra, cw, digits, c, nd, ext,
+                           L, ctx->n_primes(), ctx->d_mod, ctx->d_twf, ctx->d_pinv, ctx->log_n, bpl);
+        prof_end(ctx, K_MODDOWN);
+        HIP_TRY(hipGetLastError());
+        return CKKS_OK;
+    }
     uint64_t *u = work;                              // [count][2][ext][N]
     uint64_t *cw = u + (size_t)count * 2 * ext * N;  // [count][2][L][N]
     {
         const dim3 grid((ctx->n + kThreads - 1) / kThreads, ext, count), block(kThreads);
         prof_begin(ctx, K_KEYIP, 8.0 * ctx->n * ext * (count * (2.0 * nd + 2.0) + nd));
         hipLaunchKernelGGL(k_key_ip_batch, grid, block, 0, ctx->stream, digits, ra, u, nd, ext, level, ctx->n_q,
-                           ctx->n_primes(), ctx->d_mod, ctx->log_n);
+                           ctx->n_primes(), 0u, ext, ctx->d_mod, ctx->log_n);
         prof_end(ctx, K_KEYIP);
         HIP_TRY(hipGetLastError());
     }

@@ -461,6 +461,23 @@ ckks_status launch_ntt_strided(ckks_ctx *ctx, uint64_t *data, uint32_t batch, ui
 
 void ntt_split(uint32_t log_n, int *s1, int *s2) { split_log((int)log_n, s1, s2); }
 
+// First (column) pass only of the forward transform of `batch` groups of map.n rows, fp64 butterflies; the rows
+// are left as raw doubles for a fused second pass.  Needs a two-pass size and primes below 2^50.
+ckks_status launch_ntt_fwd_first_pass(ckks_ctx *ctx, uint64_t *data, uint32_t batch, uint32_t bstride,
+                                      const LimbMap &map)
+{
+    if (!batch || !map.n) return CKKS_OK;
+    int s1, s2;
+    split_log((int)ctx->log_n, &s1, &s2);
+    CK_REQUIRE(s1 > 0 && use_f64(ctx, map), CKKS_EINVAL, "ntt: first pass alone needs two passes and fp64 primes");
+    const double res = (double)batch * map.n * ctx->n;
+    prof_begin(ctx, K_NTT_FWD_COL, 16.0 * res, res * kOpsButterflyF64 * s1 / 2);
+    const hipError_t e = dispatch_col<false, true>(s1, ctx, data, batch, bstride, map);
+    prof_end(ctx, K_NTT_FWD_COL);
+    if (e != hipSuccess) return set_error(CKKS_EHIP, "ntt launch failed: %s", hipGetErrorString(e));
+    return CKKS_OK;
+}
+
 bool ntt_uses_f64(const ckks_ctx *ctx, uint32_t limbs) { return use_f64(ctx, limb_range(0, limbs)); }
 
 // First (column) pass only of the forward NTT of m[batch][N] into out[batch][limbs][N]; the rows are left in the

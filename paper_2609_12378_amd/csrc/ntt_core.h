@@ -57,6 +57,7 @@ struct Ar<true> {
     using W = double;
     double q, qinv, ninv;
     __device__ explicit Ar(const ModQ &m) : q(m.qd), qinv(m.qinvd), ninv(m.ninvd) {}
+    __device__ Ar() : q(0.0), qinv(0.0), ninv(0.0) {}
     __device__ static E from_u64(uint64_t v)
     {
         return (double)(uint32_t)(v >> 32) * 4294967296.0 + (double)(uint32_t)v;
