@@ -37,9 +37,38 @@ ckks_status rotate_core(ckks_ctx *ctx, const uint64_t *c, uint32_t level, const 
     const uint32_t bs = ks_rot_batch(count);
     std::vector<uint32_t> g(count);
     for (uint32_t r = 0; r < count; r++) g[r] = ckks_galois_elt(ctx, steps[r]);
+    std::vector<const uint64_t *> c0s(count, c), digs(count, digits);
     for (uint32_t r0 = 0; r0 < count; r0 += bs) {
         const uint32_t cnt = count - r0 < bs ? count - r0 : bs;
-        CK_TRY(ks_rotate_batch(ctx, c, level, digits, cnt, g.data() + r0, keys + r0, outs + r0, rw));
+        CK_TRY(ks_rotate_batch(ctx, level, cnt, c0s.data() + r0, digs.data() + r0, g.data() + r0, keys + r0,
+                               outs + r0, rw));
+    }
+    return CKKS_OK;
+}
+
+// The same rotation (steps, key) of `count` ciphertexts: ciphertext r at cs + r * stride (words, [2][level+1][N]),
+// output r at outs[r]; one batched ModUp, key switching in batches of up to 32.
+// work: ks_scratch_words(ctx, level, ks_rot_batch(count), count) words
+ckks_status rotate_many(ckks_ctx *ctx, const uint64_t *cs, size_t stride, uint32_t count, uint32_t level,
+                        int32_t steps, const uint64_t *key, uint64_t *const *outs, uint64_t *work)
+{
+    if (!count) return CKKS_OK;
+    const uint32_t L = level + 1, ext = L + ctx->n_p, nd = n_digits(ctx, level);
+    const size_t N = ctx->n, dig_ct = (size_t)nd * ext * N;
+    uint64_t *digits = work;
+    uint64_t *rw = digits + (size_t)count * (dig_ct + (size_t)ctx->alpha * N);
+    CK_TRY(ks_modup_batch(ctx, cs + (size_t)L * N, stride, count, level, digits));
+    const uint32_t bs = ks_rot_batch(count);
+    std::vector<uint32_t> g(count, ckks_galois_elt(ctx, steps));
+    std::vector<const uint64_t *> keys(count, key), c0s(count), digs(count);
+    for (uint32_t r = 0; r < count; r++) {
+        c0s[r] = cs + (size_t)r * stride;
+        digs[r] = digits + (size_t)r * dig_ct;
+    }
+    for (uint32_t r0 = 0; r0 < count; r0 += bs) {
+        const uint32_t cnt = count - r0 < bs ? count - r0 : bs;
+        CK_TRY(ks_rotate_batch(ctx, level, cnt, c0s.data() + r0, digs.data() + r0, g.data() + r0, keys.data() + r0,
+                               outs + r0, rw));
     }
     return CKKS_OK;
 }

@@ -183,19 +183,22 @@ __global__ __launch_bounds__(kThreads) void k_moddown_finish(uint64_t *out, cons
     out[(((size_t)k * L + i) << log_n) + col] = r;
 }
 
-// Batched rotations (hoisting): rotation r of the batch uses Galois element
-// g[r], key key[r] and writes out[r].
+// Batched rotations: rotation r of the batch uses Galois element g[r], key
+// key[r], the ModUp digits dig[r] and c0[r] of its input, and writes out[r];
+// hoisted rotations of one ciphertext share dig and c0.
 struct RotArgs {
     uint32_t count;
     uint32_t g[kRotBatch];
     const uint64_t *key[kRotBatch];
     uint64_t *out[kRotBatch];
+    const uint64_t *dig[kRotBatch];  // ModUp digits [nd][ext][N] of the rotated ciphertext
+    const uint64_t *c0[kRotBatch];   // its c0 [level+1][N]
 };
 
 // u[r][k][row - row0][n] = sum_j d_j[row][sigma_{g_r}(n)] * key_r[j][k][krow][n] for rows row0 .. row0 + rows - 1
 // of Q_level u P (u holds `rows` rows per polynomial)
-__global__ __launch_bounds__(kThreads) void k_key_ip_batch(const uint64_t *__restrict__ digits, RotArgs ra,
-                                                            uint64_t *u, uint32_t nd, uint32_t ext, uint32_t level,
+__global__ __launch_bounds__(kThreads) void k_key_ip_batch(RotArgs ra, uint64_t *u, uint32_t nd, uint32_t ext,
+                                                            uint32_t level,
                                                             uint32_t n_q, uint32_t key_rows, uint32_t row0,
                                                             uint32_t rows, const ModQ *__restrict__ mods,
                                                             uint32_t log_n)
@@ -208,6 +211,7 @@ __global__ __launch_bounds__(kThreads) void k_key_ip_batch(const uint64_t *__res
     const ModQ m = mods[prime];
     const uint32_t sc = auto_index(col, ra.g[r], log_n);
     const uint64_t *key = ra.key[r];
+    const uint64_t *digits = ra.dig[r];
     acc128 a0{0, 0}, a1{0, 0};
     for (uint32_t j = 0; j < nd; j++) {
         const uint64_t d = digits[(((size_t)j * ext + row) << log_n) + sc];
@@ -227,9 +231,8 @@ __global__ __launch_bounds__(kThreads) void k_key_ip_batch(const uint64_t *__res
 // so neither the q-limb rows of u nor the transformed conversion ever go to HBM.  Magnitudes (units of q):
 // transform outputs <= 2.5 (row pass after a reducing first pass), each product <= 0.875 and the sum range-reduced
 // every 4 digits (<= 4), differences <= 6.5, P^-1 products <= 3, plus c0 < 1: all below 8 q = 2^53.
-__global__ __launch_bounds__(64) void k_ks_finish8(RotArgs ra, const uint64_t *__restrict__ cw,
-                                                   const uint64_t *__restrict__ digits,
-                                                   const uint64_t *__restrict__ c0, uint32_t nd, uint32_t ext,
+__global__ __launch_bounds__(64) void k_ks_finish8(RotArgs ra, const uint64_t *__restrict__ cw, uint32_t nd,
+                                                   uint32_t ext,
                                                    uint32_t L, uint32_t key_rows, const ModQ *__restrict__ mods,
                                                    const double *__restrict__ twf,
                                                    const ulonglong2 *__restrict__ pinv, uint32_t log_n,
@@ -262,6 +265,7 @@ __global__ __launch_bounds__(64) void k_ks_finish8(RotArgs ra, const uint64_t *_
     const uint32_t g = ra.g[r];
     const uint64_t *key = ra.key[r];
     uint64_t *out = ra.out[r];
+    const uint64_t *digits = ra.dig[r], *c0 = ra.c0[r];
     const double pi = (double)pinv[i].x;
     const size_t kstride = (size_t)key_rows << log_n;
 #pragma unroll
@@ -288,7 +292,7 @@ __global__ __launch_bounds__(64) void k_ks_finish8(RotArgs ra, const uint64_t *_
 
 // out_r[k][i][n] = (u[r][k][i][n] - c[r][k][i][n]) * P^-1 (+ c0[i][sigma_{g_r}(n)] for k = 0)
 __global__ __launch_bounds__(kThreads) void k_moddown_finish_batch(RotArgs ra, const uint64_t *u, const uint64_t *c,
-                                                                    const uint64_t *c0, uint32_t ext, uint32_t level,
+                                                                    uint32_t ext, uint32_t level,
                                                                     const ulonglong2 *__restrict__ pinv,
                                                                     const ModQ *__restrict__ mods, uint32_t log_n)
 {
@@ -302,7 +306,7 @@ __global__ __launch_bounds__(kThreads) void k_moddown_finish_batch(RotArgs ra, c
     const uint64_t cv = c[(((size_t)rk * L + i) << log_n) + col];
     const ulonglong2 w = pinv[i];
     uint64_t res = shoup(submod(x, cv, q), w.x, w.y, q);
-    if (k == 0) res = addmod(res, c0[((size_t)i << log_n) + auto_index(col, ra.g[r], log_n)], q);
+    if (k == 0) res = addmod(res, ra.c0[r][((size_t)i << log_n) + auto_index(col, ra.g[r], log_n)], q);
     ra.out[r][(((size_t)k * L + i) << log_n) + col] = res;
 }
 
@@ -348,18 +352,20 @@ ckks_status launch_conv(ckks_ctx *ctx, const ConvDev *cd, const uint64_t *in, ui
 
 uint32_t ks_rot_batch(uint32_t count) { return count < (uint32_t)kRotBatch ? count : (uint32_t)kRotBatch; }
 
-size_t ks_scratch_words(const ckks_ctx *ctx, uint32_t level, uint32_t batch)
+size_t ks_scratch_words(const ckks_ctx *ctx, uint32_t level, uint32_t batch, uint32_t n_ct)
 {
     const size_t ext = level + 1 + ctx->n_p;
     const size_t nd = n_digits(ctx, level);
     if (batch < 1) batch = 1;
-    // digits + INTT staging [alpha] + per rotation: u[2][ext] and the converted rows [2][level+1]
-    return ((nd * ext) + ctx->alpha + (size_t)batch * (2 * ext + 2 * (level + 1))) << ctx->log_n;
+    if (n_ct < 1) n_ct = 1;
+    // per input ciphertext: digits + INTT staging [alpha]; per rotation of a batch: u[2][ext] and the converted
+    // rows [2][level+1]
+    return ((size_t)n_ct * (nd * ext + ctx->alpha) + (size_t)batch * (2 * ext + 2 * (level + 1))) << ctx->log_n;
 }
 
-ckks_status ks_rotate_batch(ckks_ctx *ctx, const uint64_t *c, uint32_t level, const uint64_t *digits,
-                            uint32_t count, const uint32_t *g, const uint64_t *const *keys, uint64_t *const *outs,
-                            uint64_t *work)
+ckks_status ks_rotate_batch(ckks_ctx *ctx, uint32_t level, uint32_t count, const uint64_t *const *c0s,
+                            const uint64_t *const *digs, const uint32_t *g, const uint64_t *const *keys,
+                            uint64_t *const *outs, uint64_t *work)
 {
     CK_REQUIRE(count >= 1 && count <= (uint32_t)kRotBatch, CKKS_EINVAL, "rotation batch of %u", count);
     const uint32_t L = level + 1, K = ctx->n_p, ext = L + K, nd = n_digits(ctx, level);
@@ -370,6 +376,8 @@ ckks_status ks_rotate_batch(ckks_ctx *ctx, const uint64_t *c, uint32_t level, co
         ra.g[r] = g[r];
         ra.key[r] = keys[r];
         ra.out[r] = outs[r];
+        ra.dig[r] = digs[r];
+        ra.c0[r] = c0s[r];
     }
     int s1, s2;
     ntt_split(ctx->log_n, &s1, &s2);
@@ -380,7 +388,7 @@ ckks_status ks_rotate_batch(ckks_ctx *ctx, const uint64_t *c, uint32_t level, co
         {
             const dim3 grid((ctx->n + kThreads - 1) / kThreads, K, count), block(kThreads);
             prof_begin(ctx, K_KEYIP, 8.0 * ctx->n * K * (count * (2.0 * nd + 2.0) + nd));
-            hipLaunchKernelGGL(k_key_ip_batch, grid, block, 0, ctx->stream, digits, ra, up, nd, ext, level, ctx->n_q,
+            hipLaunchKernelGGL(k_key_ip_batch, grid, block, 0, ctx->stream, ra, up, nd, ext, level, ctx->n_q,
                                ctx->n_primes(), L, K, ctx->d_mod, ctx->log_n);
             prof_end(ctx, K_KEYIP);
             HIP_TRY(hipGetLastError());
@@ -395,8 +403,8 @@ ckks_status ks_rotate_batch(ckks_ctx *ctx, const uint64_t *c, uint32_t level, co
         const double res = (double)count * L * N;
         prof_begin(ctx, K_MODDOWN, 8.0 * res * (2.0 + 2.0 * nd + 2.0),
                    res * (2 * (4 * kOpsButterflyF64 + 4 * (kOpsButterflyF64 - 3)) / 2 + nd * 2 * 10.0 + 40.0));
-        hipLaunchKernelGGL(k_ks_finish8, dim3(count * L * bpl), dim3(64), 0, ctx->stream, ra, cw, digits, c, nd, ext,
-                           L, ctx->n_primes(), ctx->d_mod, ctx->d_twf, ctx->d_pinv, ctx->log_n, bpl);
+        hipLaunchKernelGGL(k_ks_finish8, dim3(count * L * bpl), dim3(64), 0, ctx->stream, ra, cw, nd, ext, L,
+                           ctx->n_primes(), ctx->d_mod, ctx->d_twf, ctx->d_pinv, ctx->log_n, bpl);
         prof_end(ctx, K_MODDOWN);
         HIP_TRY(hipGetLastError());
         return CKKS_OK;
@@ -406,7 +414,7 @@ ckks_status ks_rotate_batch(ckks_ctx *ctx, const uint64_t *c, uint32_t level, co
     {
         const dim3 grid((ctx->n + kThreads - 1) / kThreads, ext, count), block(kThreads);
         prof_begin(ctx, K_KEYIP, 8.0 * ctx->n * ext * (count * (2.0 * nd + 2.0) + nd));
-        hipLaunchKernelGGL(k_key_ip_batch, grid, block, 0, ctx->stream, digits, ra, u, nd, ext, level, ctx->n_q,
+        hipLaunchKernelGGL(k_key_ip_batch, grid, block, 0, ctx->stream, ra, u, nd, ext, level, ctx->n_q,
                            ctx->n_primes(), 0u, ext, ctx->d_mod, ctx->log_n);
         prof_end(ctx, K_KEYIP);
         HIP_TRY(hipGetLastError());
@@ -419,7 +427,7 @@ ckks_status ks_rotate_batch(ckks_ctx *ctx, const uint64_t *c, uint32_t level, co
     {
         const dim3 grid((ctx->n + kThreads - 1) / kThreads, L, 2 * count), block(kThreads);
         prof_begin(ctx, K_MODDOWN, 8.0 * ctx->n * L * count * 7.0);
-        hipLaunchKernelGGL(k_moddown_finish_batch, grid, block, 0, ctx->stream, ra, u, cw, c, ext, level,
+        hipLaunchKernelGGL(k_moddown_finish_batch, grid, block, 0, ctx->stream, ra, u, cw, ext, level,
                            ctx->d_pinv, ctx->d_mod, ctx->log_n);
         prof_end(ctx, K_MODDOWN);
         HIP_TRY(hipGetLastError());
@@ -427,31 +435,47 @@ ckks_status ks_rotate_batch(ckks_ctx *ctx, const uint64_t *c, uint32_t level, co
     return CKKS_OK;
 }
 
-ckks_status ks_modup(ckks_ctx *ctx, const uint64_t *c, uint32_t level, uint64_t *digits)
+ckks_status ks_modup_batch(ckks_ctx *ctx, const uint64_t *c1, size_t in_stride, uint32_t count, uint32_t level,
+                           uint64_t *digits)
 {
-    const uint32_t K = ctx->n_p, ext = level + 1 + K, nd = n_digits(ctx, level);
-    const size_t N = ctx->n;
+    if (!count) return CKKS_OK;
+    const uint32_t K = ctx->n_p, ext = level + 1 + K, nd = n_digits(ctx, level), alpha = ctx->alpha;
+    const size_t N = ctx->n, dig_ct = (size_t)nd * ext * N;
+    // coefficient form of a digit's limbs, staged in alpha rows per ciphertext after all the digits
+    uint64_t *coef = digits + (size_t)count * dig_ct;
     for (uint32_t j = 0; j < nd; j++) {
         const uint32_t lo = digit_lo(ctx, j), hi = digit_hi(ctx, j, level), ns = hi - lo;
         uint64_t *dj = digits + (size_t)j * ext * N;
-        // the digit's own limbs keep their NTT-domain values
-        HIP_TRY(hipMemcpyAsync(dj + lo * N, c + lo * N, ns * N * sizeof(uint64_t), hipMemcpyDeviceToDevice,
-                               ctx->stream));
-        // coefficient form of the digit's limbs, staged in the alpha rows after the digits
-        uint64_t *coef = digits + (size_t)nd * ext * N;
-        HIP_TRY(hipMemcpyAsync(coef, c + lo * N, ns * N * sizeof(uint64_t), hipMemcpyDeviceToDevice, ctx->stream));
-        CK_TRY(launch_ntt(ctx, coef, ns, limb_range(lo, ns), true));
+        const size_t width = (size_t)ns * N * sizeof(uint64_t);
+        // the digit's own limbs keep their NTT-domain values; a second copy goes to the staging rows
+        if (count == 1) {
+            HIP_TRY(hipMemcpyAsync(dj + lo * N, c1 + lo * N, width, hipMemcpyDeviceToDevice, ctx->stream));
+            HIP_TRY(hipMemcpyAsync(coef, c1 + lo * N, width, hipMemcpyDeviceToDevice, ctx->stream));
+        } else {
+            HIP_TRY(hipMemcpy2DAsync(dj + lo * N, dig_ct * sizeof(uint64_t), c1 + lo * N,
+                                     in_stride * sizeof(uint64_t), width, count, hipMemcpyDeviceToDevice,
+                                     ctx->stream));
+            HIP_TRY(hipMemcpy2DAsync(coef, (size_t)alpha * N * sizeof(uint64_t), c1 + lo * N,
+                                     in_stride * sizeof(uint64_t), width, count, hipMemcpyDeviceToDevice,
+                                     ctx->stream));
+        }
+        CK_TRY(launch_ntt_strided(ctx, coef, count, alpha, limb_range(lo, ns), true));
         const ConvDev *cd;
         CK_TRY(ctx_conv(ctx, (int)level, (int)j, &cd));
-        CK_TRY(launch_conv(ctx, cd, coef, 0, dj, 0, lo, ns, 1));
+        CK_TRY(launch_conv(ctx, cd, coef, alpha, dj, (uint32_t)(dig_ct / N), lo, ns, count));
         // NTT of the converted rows: [0, lo) and [hi, ext)
-        if (lo) CK_TRY(launch_ntt(ctx, dj, lo, limb_range(0, lo), false));
+        if (lo) CK_TRY(launch_ntt_strided(ctx, dj, count, (uint32_t)(dig_ct / N), limb_range(0, lo), false));
         LimbMap m{};
         m.n = ext - hi;
         for (uint32_t r = hi; r < ext; r++) m.prime[r - hi] = (uint8_t)(r <= level ? r : ctx->n_q + (r - level - 1));
-        CK_TRY(launch_ntt(ctx, dj + (size_t)hi * N, m.n, m, false));
+        CK_TRY(launch_ntt_strided(ctx, dj + (size_t)hi * N, count, (uint32_t)(dig_ct / N), m, false));
     }
     return CKKS_OK;
+}
+
+ckks_status ks_modup(ckks_ctx *ctx, const uint64_t *c, uint32_t level, uint64_t *digits)
+{
+    return ks_modup_batch(ctx, c, 0, 1, level, digits);
 }
 
 ckks_status ks_inner_product(ckks_ctx *ctx, const uint64_t *digits, uint32_t nd, const uint64_t *key,

@@ -27,6 +27,10 @@ ckks_status launch_rescale_finish(ckks_ctx *ctx, uint64_t *out, const uint64_t *
 // digits: [nd][level+1+K][N] from c ([level+1][N]); the buffer must hold alpha more rows
 // after the digits (staging for the INTT of a digit's limbs)
 ckks_status ks_modup(ckks_ctx *ctx, const uint64_t *c, uint32_t level, uint64_t *digits);
+// ModUp of `count` ciphertexts at once: c1 of ciphertext r at c1 + r * in_stride (words); digits: [count][nd][ext][N]
+// followed by count * alpha staging rows
+ckks_status ks_modup_batch(ckks_ctx *ctx, const uint64_t *c1, size_t in_stride, uint32_t count, uint32_t level,
+                           uint64_t *digits);
 // (u0, u1) = sum_j sigma_g(d_j) (b_j, a_j); g = 1 for no automorphism; u: [2][level+1+K][N]
 ckks_status ks_inner_product(ckks_ctx *ctx, const uint64_t *digits, uint32_t nd, const uint64_t *key,
                              uint32_t level, uint32_t g, uint64_t *u);
@@ -36,15 +40,16 @@ ckks_status ks_inner_product(ckks_ctx *ctx, const uint64_t *digits, uint32_t nd,
 ckks_status ks_moddown(ckks_ctx *ctx, uint64_t *u, uint32_t polys, uint32_t level, const uint64_t *add0,
                        uint32_t add0_g, const uint64_t *add1, uint64_t *out, uint64_t *work);
 // scratch words for rotations at `level` processed `batch` at a time (see rotate_core)
-size_t ks_scratch_words(const ckks_ctx *ctx, uint32_t level, uint32_t batch);
+size_t ks_scratch_words(const ckks_ctx *ctx, uint32_t level, uint32_t batch, uint32_t n_ct = 1);
 // rotations per batched launch for `count` requested rotations
 uint32_t ks_rot_batch(uint32_t count);
-// `count` (<= 32) rotations of ciphertext c sharing the ModUp digits: key inner product with the
-// automorphism g[r], ModDown and the sigma_{g_r}(c0) addition, each stage one launch for all r.
+// `count` (<= 32) rotations: rotation r applies the automorphism g[r] with key keys[r] to the ciphertext whose
+// c0 is c0s[r] and whose ModUp digits are digs[r] (hoisted rotations of one ciphertext share both): key inner
+// product, ModDown and the sigma_{g_r}(c0) addition, each stage one launch for all r.
 // work: count * (2 ext + 2 (level+1)) N words
-ckks_status ks_rotate_batch(ckks_ctx *ctx, const uint64_t *c, uint32_t level, const uint64_t *digits,
-                            uint32_t count, const uint32_t *g, const uint64_t *const *keys, uint64_t *const *outs,
-                            uint64_t *work);
+ckks_status ks_rotate_batch(ckks_ctx *ctx, uint32_t level, uint32_t count, const uint64_t *const *c0s,
+                            const uint64_t *const *digs, const uint32_t *g, const uint64_t *const *keys,
+                            uint64_t *const *outs, uint64_t *work);
 
 // encoding (encode.hip)
 struct SlotSource {

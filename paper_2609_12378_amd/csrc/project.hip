@@ -31,6 +31,8 @@
 ckks_status rotate_core(ckks_ctx *ctx, const uint64_t *c, uint32_t level, const int32_t *steps,
                         const uint64_t *const *keys, uint32_t count, uint64_t *const *outs, uint64_t *work);
 ckks_status rescale_core(ckks_ctx *ctx, const uint64_t *c, uint32_t l, uint64_t *out, uint64_t *work);
+ckks_status rotate_many(ckks_ctx *ctx, const uint64_t *cs, size_t stride, uint32_t count, uint32_t level,
+                        int32_t steps, const uint64_t *key, uint64_t *const *outs, uint64_t *work);
 
 namespace {
 
@@ -404,11 +406,13 @@ extern "C" ckks_status ckks_linear_project(ckks_ctx *ctx, const ckks_buf *in, co
     if (ctx->proj_max_pairs) Pmax = std::min(Pmax, ctx->proj_max_pairs);
     const uint32_t Pb = Pmax;
     const size_t xrot_w = (size_t)n_in * n1 * ctw;
-    const size_t acc_w = (size_t)kJ * ctw, tot_w = (size_t)kJ * ctw, rot_w = ctw;
+    const size_t acc_w = (size_t)kJ * ctw, tot_w = (size_t)kJ * ctw, rot_w = (size_t)kJ * ctw;
     const size_t pt_w = (size_t)Jt * Pb * L * N;
     const size_t m_w = (size_t)Jt * Pb * N;                       // int64 coefficients
     const size_t fft_w = (size_t)Jt * Pb * (N / 2) * 2;            // double2 per slot
-    const size_t ks_w = ks_scratch_words(ctx, level, ks_rot_batch(n1 > 1 ? n1 - 1 : 1));
+    // key switching: hoisted baby steps of one input, or the giant step of a tile's kJ partial sums
+    const size_t ks_w = std::max(ks_scratch_words(ctx, level, ks_rot_batch(n1 > 1 ? n1 - 1 : 1)),
+                                 ks_scratch_words(ctx, level, ks_rot_batch(kJ), kJ));
     // W re-laid as its cyclic diagonals, and the feature index of every FFT position, for the radix-8 FFT pass
     const bool diag = D <= 256 && ctx->log_n >= 12;
     const size_t wd_w = diag ? (size_t)shape->d_in * shape->d_out : 0, fop_w = diag ? N / 4 : 0;
@@ -494,17 +498,14 @@ extern "C" ckks_status ckks_linear_project(ckks_ctx *ctx, const ckks_buf *in, co
                 }
                 pb0 += P;
             }
-            for (uint32_t jj = 0; jj < jc; jj++) {
-                uint64_t *a = acc + (size_t)jj * ctw, *t = tot + (size_t)jj * ctw;
-                if (g == 0) {
-                    HIP_TRY(hipMemcpyAsync(t, a, ctw * 8, hipMemcpyDeviceToDevice, ctx->stream));
-                } else {
-                    const int32_t st = (int32_t)(T * n1 * g);
-                    const uint64_t *k = gkeys[g];
-                    uint64_t *o = rot;
-                    CK_TRY(rotate_core(ctx, a, level, &st, &k, 1, &o, ksw));
-                    CK_TRY(launch_binary(ctx, t, t, rot, 2 * L, limb_range(0, L), EW_ADD));
-                }
+            // giant step: the tile's jc partial sums rotated together, then added to the totals
+            if (g == 0) {
+                HIP_TRY(hipMemcpyAsync(tot, acc, jc * ctw * 8, hipMemcpyDeviceToDevice, ctx->stream));
+            } else {
+                std::vector<uint64_t *> outs(jc);
+                for (uint32_t jj = 0; jj < jc; jj++) outs[jj] = rot + (size_t)jj * ctw;
+                CK_TRY(rotate_many(ctx, acc, ctw, jc, level, (int32_t)(T * n1 * g), gkeys[g], outs.data(), ksw));
+                CK_TRY(launch_binary(ctx, tot, tot, rot, jc * 2 * L, limb_range(0, L), EW_ADD));
             }
         }
         for (uint32_t jj = 0; jj < jc; jj++) {
