@@ -25,6 +25,7 @@
 // memory.
 #pragma clang fp contract(off)
 #include "ckks_internal.h"
+#include "ntt_core.h"
 #include "ops.h"
 
 namespace {
@@ -210,6 +211,133 @@ __global__ __launch_bounds__(256) void k_fft_a8(double2 *a, const double2 *__res
     }
 }
 
+// FFT pass B fused with the first NTT pass (N = 2^16: M = 32768 = 16 x 2048, transform columns of 256 points).
+// Block (plaintext b, columns c0..c0+15 of the 256 x 256 coefficient matrix, coefficient n = 256 u + c) needs
+// pass-B outputs v_k, k = 256 u' + c (u' < 128; m_n = round(c Re v_n) for n < M and m_{n+M} = round(c Im v_n)),
+// i.e. pass-B columns c' = k mod 2048 = 256 (u' mod 8) + c at depths h = u' / 8.  Its 512 threads compute those
+// 128 pass-B columns (four threads per column, two stages in registers, an LDS exchange, two more), round into an
+// int64 tile in LDS, and run the 8-residue column transform of every limb from that tile (as ntt_col8_from_i64).
+// The pass-B butterflies, twist and rounding are the same arithmetic as in k_fft_b, so the coefficients are the
+// same integers, and they never go to HBM.
+__global__ __launch_bounds__(512) void ntt_col8_from_fft(const double2 *__restrict__ work, uint64_t *out,
+                                                         uint32_t limbs, const ModQ *__restrict__ mods,
+                                                         const double *__restrict__ twf,
+                                                         const double2 *__restrict__ fw,
+                                                         const double2 *__restrict__ twist, double cs)
+{
+    using nttc::kE8;
+    constexpr uint32_t log_n = 16, M = 1u << 15, MT_PITCH = 17;
+    __shared__ double tws[2][256];
+    __shared__ double tr[16][nttc::kTr8];  // also the pass-B exchange buffer (2048 double2 with padding)
+    __shared__ int64_t mt[256 * MT_PITCH];
+    const uint32_t b = blockIdx.x >> 4, c0 = (blockIdx.x & 15u) << 4, tid = threadIdx.x;
+    // ---- pass B for columns c' = 256 w8 + c0 + cc, ci = 16 w8 + cc, depths h = 4 qq + j
+    {
+        const uint32_t ci = tid >> 2, qq = tid & 3u, cc = ci & 15u, w8 = ci >> 4;
+        const uint32_t cp = (w8 << 8) + c0 + cc;
+        const double2 *src = work + ((size_t)b << 15);
+        double2 x[4];
+#pragma unroll
+        for (int j = 0; j < 4; j++) x[j] = src[((4 * qq + j) << 11) + cp];
+        // stages 1, 2 (pairs h, h + 1 and h, h + 2: h's low bits are j's)
+#pragma unroll
+        for (int st = 1; st <= 2; st++) {
+            const uint32_t half = 1u << (st - 1), step = M >> (11 + st);
+#pragma unroll
+            for (int j = 0; j < 4; j++) {
+                if (j & half) continue;
+                const uint32_t h = 4 * qq + j;
+                const uint32_t k = (h & (half - 1)) * 2048 + cp;
+                const double2 t = cmul(fw[k * step], x[j + half]);
+                const double2 u = x[j];
+                x[j] = make_double2(u.x + t.x, u.y + t.y);
+                x[j + half] = make_double2(u.x - t.x, u.y - t.y);
+            }
+        }
+        double2 *ex = (double2 *)&tr[0][0];  // [16 depths][128 columns + 1]
+#pragma unroll
+        for (int j = 0; j < 4; j++) ex[(4 * qq + j) * 129 + ci] = x[j];
+        __syncthreads();
+#pragma unroll
+        for (int j = 0; j < 4; j++) x[j] = ex[(qq + 4 * j) * 129 + ci];
+        // stages 3, 4: now h = qq + 4 j, so h's bits 2, 3 are j's
+#pragma unroll
+        for (int st = 3; st <= 4; st++) {
+            const uint32_t half = 1u << (st - 1), jh = half >> 2, step = M >> (11 + st);
+#pragma unroll
+            for (int j = 0; j < 4; j++) {
+                if (j & jh) continue;
+                const uint32_t h = qq + 4 * j;
+                const uint32_t k = (h & (half - 1)) * 2048 + cp;
+                const double2 t = cmul(fw[k * step], x[j + jh]);
+                const double2 u = x[j];
+                x[j] = make_double2(u.x + t.x, u.y + t.y);
+                x[j + jh] = make_double2(u.x - t.x, u.y - t.y);
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < 4; j++) {
+            const uint32_t h = qq + 4 * j, k = (h << 11) + cp, u = (h << 3) + w8;
+            const double2 v = cmul(twist[k], x[j]);
+            mt[u * MT_PITCH + cc] = (int64_t)round(cs * v.x);
+            mt[(u + 128) * MT_PITCH + cc] = (int64_t)round(cs * v.y);
+        }
+    }
+    if (tid < 255) tws[0][tid + 1] = twf[tid + 1];
+    __syncthreads();
+    // ---- column transforms (as ntt_col8_from_i64, coefficients from the tile)
+    const uint32_t col = tid & 15u, t = tid >> 4;
+    const size_t coff = c0 + col;
+    double vd[kE8];
+    bool big = false;
+#pragma unroll
+    for (int k = 0; k < kE8; k++) {
+        const int64_t v = mt[nttc::u8<0>(t, k) * MT_PITCH + col];
+        big |= v > (1ll << 52) || v < -(1ll << 52);
+        vd[k] = (double)v;
+    }
+    for (uint32_t l = 0; l < limbs; l++) {
+        const ModQ md = mods[l];
+        const nttc::Ar<true> ar(md);
+        double wnext = 0.0;
+        if (l + 1 < limbs && tid < 255) wnext = twf[((size_t)(l + 1) << log_n) + tid + 1];
+        double x[kE8];
+        if (!big) {
+#pragma unroll
+            for (int k = 0; k < kE8; k++) x[k] = ar.red(vd[k]);
+        } else {
+#pragma unroll
+            for (int k = 0; k < kE8; k++) x[k] = ar.from_i64(mt[nttc::u8<0>(t, k) * MT_PITCH + col], md);
+        }
+        const double *tw = tws[l & 1];
+        double *trc = tr[col];
+        nttc::fwd8_stage<0, 0, (nttc::kColMask8 >> 0) & 1>(x, tw, t, ar);
+        nttc::fwd8_stage<0, 1, (nttc::kColMask8 >> 1) & 1>(x, tw, t, ar);
+        nttc::fwd8_stage<0, 2, (nttc::kColMask8 >> 2) & 1>(x, tw, t, ar);
+#pragma unroll
+        for (int k = 0; k < kE8; k++) trc[nttc::pad_ac(nttc::u8<0>(t, k))] = x[k];
+        __syncthreads();
+        if (l + 1 < limbs && tid < 255) tws[(l + 1) & 1][tid + 1] = wnext;
+#pragma unroll
+        for (int k = 0; k < kE8; k++) x[k] = trc[nttc::pad_ac(nttc::u8<1>(t, k))];
+        __syncthreads();
+        nttc::fwd8_stage<1, 3, (nttc::kColMask8 >> 3) & 1>(x, tw, t, ar);
+        nttc::fwd8_stage<1, 4, (nttc::kColMask8 >> 4) & 1>(x, tw, t, ar);
+        nttc::fwd8_stage<1, 5, (nttc::kColMask8 >> 5) & 1>(x, tw, t, ar);
+#pragma unroll
+        for (int k = 0; k < kE8; k++) trc[nttc::pad_cb(nttc::u8<1>(t, k))] = x[k];
+        __syncthreads();
+#pragma unroll
+        for (int k = 0; k < kE8; k++) x[k] = trc[nttc::pad_cb(nttc::u8<2>(t, k))];
+        __syncthreads();
+        nttc::fwd8_stage<2, 6, (nttc::kColMask8 >> 6) & 1>(x, tw, t, ar);
+        nttc::fwd8_stage<2, 7, (nttc::kColMask8 >> 7) & 1>(x, tw, t, ar);
+        uint64_t *dst = out + (((size_t)b * limbs + l) << log_n) + coff;
+#pragma unroll
+        for (int k = 0; k < kE8; k++) dst[(size_t)nttc::u8<2>(t, k) * 256] = nttc::Ar<true>::to_raw(x[k]);
+    }
+}
+
 // feat_of_pos[x] = slot index at FFT position x, divided by the token count
 __global__ __launch_bounds__(kThreads) void k_feat_of_pos(uint32_t *out, const uint32_t *__restrict__ slot_of_pos,
                                                           uint32_t M, uint32_t tokens)
@@ -330,7 +458,7 @@ __global__ __launch_bounds__(kThreads) void k_decode_out(const double2 *y, const
 size_t enc_work_bytes(const ckks_ctx *ctx, uint32_t batch) { return (size_t)batch * (ctx->n / 2) * sizeof(double2); }
 
 ckks_status fft_passes(ckks_ctx *ctx, double2 *work, uint32_t batch, int mode, double c, int64_t *m,
-                       const SlotSource *gather)
+                       const SlotSource *gather, bool pass_a_only = false)
 {
     const uint32_t logm = ctx->log_n - 1, M = 1u << logm;
     const uint32_t logb = logm < (uint32_t)kLogBA ? logm : (uint32_t)kLogBA;
@@ -352,7 +480,7 @@ ckks_status fft_passes(ckks_ctx *ctx, double2 *work, uint32_t batch, int mode, d
                            gather ? *gather : none, ctx->d_pos_slot);
     }
     prof_end(ctx, K_FFT_A);
-    if (!single) {
+    if (!single && !pass_a_only) {
         const uint32_t hb = logm - logb;
         const dim3 grid(batch * (B / kThreads));
         prof_begin(ctx, K_FFT_B, bytes);
@@ -378,6 +506,26 @@ ckks_status enc_coeffs(ckks_ctx *ctx, const SlotSource &src, uint32_t batch, dou
 {
     if (!batch) return CKKS_OK;
     return fft_passes(ctx, work, batch, 1, scale * (2.0 / (double)ctx->n), m_out, &src);
+}
+
+bool enc_fused_ok(const ckks_ctx *ctx, uint32_t limbs) { return ctx->log_n == 16 && ntt_uses_f64(ctx, limbs); }
+
+ckks_status enc_ntt_first_pass(ckks_ctx *ctx, const SlotSource &src, uint32_t batch, double scale, double2 *work,
+                               uint32_t limbs, uint64_t *out)
+{
+    if (!batch) return CKKS_OK;
+    CK_REQUIRE(enc_fused_ok(ctx, limbs), CKKS_EINVAL, "encode: the fused first pass needs N = 2^16 and fp64 primes");
+    const double c = scale * (2.0 / (double)ctx->n);
+    CK_TRY(fft_passes(ctx, work, batch, 0, c, nullptr, &src, true));
+    // pass B's work array once, the limbs' first-pass rows
+    const double res = (double)batch * limbs * ctx->n;
+    prof_begin(ctx, K_NTT_FWD_COL, batch * 8.0 * ctx->n * (1 + limbs),
+               res * ((2 * kOpsButterflyF64 + 6 * (kOpsButterflyF64 - 3)) / 2 + 3.0));
+    hipLaunchKernelGGL(ntt_col8_from_fft, dim3(batch * 16), dim3(512), 0, ctx->stream, work, out, limbs, ctx->d_mod,
+                       ctx->d_twf, ctx->d_fft_w, ctx->d_fft_twist, c);
+    prof_end(ctx, K_NTT_FWD_COL);
+    HIP_TRY(hipGetLastError());
+    return CKKS_OK;
 }
 
 ckks_status enc_feat_of_pos(ckks_ctx *ctx, uint32_t tokens, uint32_t *out)

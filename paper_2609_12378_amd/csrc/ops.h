@@ -71,6 +71,12 @@ struct SlotSource {
 // m_out: [batch][N] int64 rounded coefficients; work: [batch][N/2] double2
 ckks_status enc_coeffs(ckks_ctx *ctx, const SlotSource &src, uint32_t batch, double scale, double2 *work,
                        int64_t *m_out);
+// encoding of a projection sub-batch fused with the first NTT pass (N = 2^16, fp64 primes 0..limbs-1):
+// FFT pass A into work, then pass B, twist, rounding and the column transforms of every limb in one kernel;
+// out: [batch][limbs][N] in the inter-pass form of launch_ntt_col_i64
+bool enc_fused_ok(const ckks_ctx *ctx, uint32_t limbs);
+ckks_status enc_ntt_first_pass(ckks_ctx *ctx, const SlotSource &src, uint32_t batch, double scale, double2 *work,
+                               uint32_t limbs, uint64_t *out);
 // out[x] = (slot index held at FFT position x) / tokens, x < N/2
 ckks_status enc_feat_of_pos(ckks_ctx *ctx, uint32_t tokens, uint32_t *out);
 // residues of m ([batch][N]) into out ([batch][limbs][N]), primes 0..limbs-1

@@ -488,11 +488,15 @@ extern "C" ckks_status ckks_linear_project(ckks_ctx *ctx, const ckks_buf *in, co
                     src.n_in = n_in;
                 }
                 const uint32_t batch = jc * P;
-                CK_TRY(enc_coeffs(ctx, src, batch, delta_w, fft, mint));
-                if (fused) {
+                if (fused && enc_fused_ok(ctx, L)) {
+                    CK_TRY(enc_ntt_first_pass(ctx, src, batch, delta_w, fft, L, pts));
+                    CK_TRY(launch_row_mac(ctx, acc, pts, (const double *)xrot, P, jc, pb0, bcount, n1, L, pb0 > 0));
+                } else if (fused) {
+                    CK_TRY(enc_coeffs(ctx, src, batch, delta_w, fft, mint));
                     CK_TRY(launch_ntt_col_i64(ctx, mint, pts, batch, L));
                     CK_TRY(launch_row_mac(ctx, acc, pts, (const double *)xrot, P, jc, pb0, bcount, n1, L, pb0 > 0));
                 } else {
+                    CK_TRY(enc_coeffs(ctx, src, batch, delta_w, fft, mint));
                     CK_TRY(launch_ntt_from_i64(ctx, mint, pts, batch, L));
                     CK_TRY(launch_mac(ctx, acc, pts, xrot, P, jc, pb0, bcount, n1, L, pb0 > 0));
                 }
