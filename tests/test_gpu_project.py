@@ -10,6 +10,7 @@
   seven (input, baby step) pairs per launch, so partial sums are carried across
   launches of unequal sizes;
 * a ring of degree 2^10 (a 64-point second transform pass);
+* the same parameters with weights 2^17 times larger (plaintext coefficients beyond 2^52);
 * the Llama-shaped projection parameters at full ring degree (N = 2^16, 24 + 8
   limbs of 50-bit primes, dnum 3, level 12, 128 tokens x 256 features, n1 = 32,
   n2 = 8 so 31 baby and 7 giant rotations) on a 256 x 512 slice of the weights
@@ -32,7 +33,7 @@ def fm_pack(X, T, D, i):
     return X[:, i * D:(i + 1) * D].T.reshape(-1)
 
 
-def run_case(cfg, d_in, d_out, oracle_outputs, arith=0, max_pairs=0):
+def run_case(cfg, d_in, d_out, oracle_outputs, arith=0, max_pairs=0, weight_scale=1.0):
     require_gpu()
     from paper_2609_12378_amd import Context
     ctx = Context(cfg.log_n, cfg.n_q, cfg.n_p, cfg.dnum, q_bits=cfg.q_bits)
@@ -43,7 +44,7 @@ def run_case(cfg, d_in, d_out, oracle_outputs, arith=0, max_pairs=0):
     n2 = -(-D // n1)
     s = ternary_secret(rng(cfg.index, 3), n)
     X = uniform_slots(rng(cfg.index, 1), (T, d_in))
-    W = gaussian_weights(rng(cfg.index, 2), (d_in, d_out))
+    W = gaussian_weights(rng(cfg.index, 2), (d_in, d_out)) * weight_scale
     delta = float(2 ** cfg.scale_log2)
     ge = rng(cfg.index, 4)
     cts_o, cts_g = [], []
@@ -81,7 +82,7 @@ def run_case(cfg, d_in, d_out, oracle_outputs, arith=0, max_pairs=0):
     errs = []
     for j, o in enumerate(outs):
         re, im = ctx.decode(ctx.decrypt(s_dev, o))
-        errs.append(np.max(np.abs(to_host(re) - fm_pack(Y, T, D, j))))
+        errs.append(np.max(np.abs(to_host(re) - fm_pack(Y, T, D, j))) / weight_scale)
     return max(errs)
 
 
@@ -110,6 +111,15 @@ def test_small_ring_projection():
     cfg = dataclasses.replace(TOY, name="ring10", log_n=10, tokens=4, d_in=256, d_out=384, n1=16)
     err = run_case(cfg, cfg.d_in, cfg.d_out, [0, 2])
     say("N=2^10 max error vs X@W", err)
+    assert err <= 2.0 ** -12
+
+
+def test_projection_large_weights_full_degree_slice():
+    # weights 2^17 times larger: rounded plaintext coefficients beyond 2^52 take the exact integer reduction of
+    # the fused first transform pass (error relative to the weight scale)
+    say("full-degree slice, large weights")
+    err = run_case(PROJECTION, 256, 256, [0], weight_scale=2.0 ** 17)
+    say("large-weight slice max error vs X@W / 2^17", err)
     assert err <= 2.0 ** -12
 
 

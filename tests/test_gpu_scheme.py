@@ -116,6 +116,17 @@ def test_encode_large_coefficients(toy):
     eq(pt.data[0], toy.ck.encode(re, im, scale, 4))
 
 
+def test_encode_large_coefficients_full_degree(big):
+    # the same at N = 2^16 (the 8-residue column pass and its exact integer reduction)
+    g = rng(4, 2, extra=10)
+    re = g.uniform(-1, 1, big.n // 2)
+    scale = float(2 ** 61)
+    pt = big.ctx.encode(to_dev(re), None, scale, 4)
+    want = big.ck.encode(re, None, scale, 4)
+    assert np.abs(big.ck.encode_int(re, None, scale)).max() > 2 ** 52
+    eq(pt.data[0], want)
+
+
 def test_encode_many_weight_vectors_full_degree(big):
     # 24 more weight-like vectors at scale q_12: each has tens of coefficients within one ulp
     # of a rounding tie, so any difference in twiddles or operation order shows up here
