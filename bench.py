@@ -131,7 +131,7 @@ def roofline(prof):
 # their hash is unchanged
 KERNEL_SOURCES = {
     "ntt_row_mac": ["project.hip", "ntt_core.h", "modarith.h", "ckks_internal.h"],
-    "ntt_fwd_col": ["ntt.hip", "ntt_core.h", "modarith.h", "ckks_internal.h"],
+    "ntt_fwd_col": ["encode.hip", "ntt.hip", "ntt_core.h", "modarith.h", "ckks_internal.h"],
 }
 
 
