@@ -84,6 +84,7 @@ struct ckks_ctx {
     bool int_only = false;               // force the integer Shoup butterflies
     uint32_t proj_max_pairs = 0;         // projection sub-batch limit (0 = by the staging budget)
     double2 *d_fft_w = nullptr;          // [N/4]  omega^-e, omega = exp(2 pi i/(N/2))
+    double2 *d_fft_wc = nullptr;         // [2048] stage-by-stage copy for 2048-point blocks (N >= 2^12)
     double2 *d_fft_twist = nullptr;      // [N/2]  zeta^-k, zeta = exp(i pi / N)
     uint32_t *d_slot_pos = nullptr;      // [N/2]  bit-reversed FFT position of slot j
     uint32_t *d_pos_slot = nullptr;      // [N/2]  slot index held at FFT position x (inverse of d_slot_pos)

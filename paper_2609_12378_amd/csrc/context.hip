@@ -193,6 +193,13 @@ static ckks_status build_tables(ckks_ctx *c)
         e5 = e5 * 5 % two_n;
     }
     CK_TRY(upload((void **)&c->d_fft_w, w.data(), w.size() * sizeof(double2)));
+    if (M >= 2048) {
+        // the same twiddles, stage by stage for 2048-point blocks: wc[2^(s-1) + k] = w[k * M / 2^s]
+        std::vector<double2> wc(2048, make_double2(0.0, 0.0));
+        for (uint32_t s = 1; s <= 11; s++)
+            for (uint32_t k = 0; k < (1u << (s - 1)); k++) wc[(1u << (s - 1)) + k] = w[(size_t)k * (M >> s)];
+        CK_TRY(upload((void **)&c->d_fft_wc, wc.data(), wc.size() * sizeof(double2)));
+    }
     CK_TRY(upload((void **)&c->d_fft_twist, twist.data(), twist.size() * sizeof(double2)));
     CK_TRY(upload((void **)&c->d_slot_pos, pos.data(), pos.size() * sizeof(uint32_t)));
     std::vector<uint32_t> inv_pos(M);
@@ -415,7 +422,7 @@ void ckks_ctx_destroy(ckks_ctx *c)
     if (!c) return;
     (void)hipDeviceSynchronize();
     (void)prof_collect(c);
-    void *ptrs[] = {c->d_mod, c->d_tw, c->d_itw, c->d_twf, c->d_itwf, c->d_fft_w, c->d_fft_twist, c->d_slot_pos,
+    void *ptrs[] = {c->d_mod, c->d_tw, c->d_itw, c->d_twf, c->d_itwf, c->d_fft_w, c->d_fft_wc, c->d_fft_twist, c->d_slot_pos,
                     c->d_pos_slot,
                     c->d_pinv, c->d_pmodq, c->d_qlinv, c->scratch};
     for (void *p : ptrs)

@@ -128,19 +128,19 @@ __device__ __forceinline__ uint32_t posA(uint32_t t, int r)
 __device__ __forceinline__ uint32_t swz_a(uint32_t x) { return x ^ ((x >> 3) & 15u); }
 __device__ __forceinline__ uint32_t swz_b(uint32_t x) { return x ^ ((x >> 1) & 15u); }
 
+// wc: the stage-by-stage twiddle table, wc[2^(LS-1) + k] = w[k * M / 2^LS] (32 KiB, cache-resident)
 template <int LAY, int LS>
-__device__ __forceinline__ void fft8_stage(double2 (&v)[8], const double2 *__restrict__ w, uint32_t t, uint32_t logm)
+__device__ __forceinline__ void fft8_stage(double2 (&v)[8], const double2 *__restrict__ wc, uint32_t t)
 {
     constexpr uint32_t half = 1u << (LS - 1);
     constexpr int xb = LS - 1;
     constexpr int rb = LAY == 1 ? xb : LAY == 2 ? xb - 3 : LAY == 3 ? xb - 6 : xb - 8;
     static_assert(rb >= 0 && rb < 3 && (LAY != 4 || xb >= 9), "stage not in this layout");
-    const uint32_t step = (1u << logm) >> LS;
 #pragma unroll
     for (int r = 0; r < 8; r++) {
         if (r & (1 << rb)) continue;
         const uint32_t k = posA<LAY>(t, r) & (half - 1);
-        const double2 tt = cmul(w[k * step], v[r | (1 << rb)]);
+        const double2 tt = cmul(wc[half + k], v[r | (1 << rb)]);
         const double2 u = v[r];
         v[r] = make_double2(u.x + tt.x, u.y + tt.y);
         v[r | (1 << rb)] = make_double2(u.x - tt.x, u.y - tt.y);
@@ -164,7 +164,7 @@ __device__ __forceinline__ void fft8_transpose(double2 (&v)[8], double2 *sh, uin
     __syncthreads();
 }
 
-__global__ __launch_bounds__(256) void k_fft_a8(double2 *a, const double2 *__restrict__ w, uint32_t logm, int mode,
+__global__ __launch_bounds__(256) void k_fft_a8(double2 *a, const double2 *__restrict__ wc, uint32_t logm, int mode,
                                                 const double2 *__restrict__ twist, double c, int64_t *m,
                                                 SlotSource ss)
 {
@@ -184,20 +184,20 @@ __global__ __launch_bounds__(256) void k_fft_a8(double2 *a, const double2 *__res
     double2 v[8];
 #pragma unroll
     for (int r = 0; r < 8; r++) v[r] = make_double2(vals[(fp[posA<1>(t, r)] + shift) & mask], 0.0);
-    fft8_stage<1, 1>(v, w, t, logm);
-    fft8_stage<1, 2>(v, w, t, logm);
-    fft8_stage<1, 3>(v, w, t, logm);
+    fft8_stage<1, 1>(v, wc, t);
+    fft8_stage<1, 2>(v, wc, t);
+    fft8_stage<1, 3>(v, wc, t);
     fft8_transpose<1, 2, false>(v, sh, t);
-    fft8_stage<2, 4>(v, w, t, logm);
-    fft8_stage<2, 5>(v, w, t, logm);
-    fft8_stage<2, 6>(v, w, t, logm);
+    fft8_stage<2, 4>(v, wc, t);
+    fft8_stage<2, 5>(v, wc, t);
+    fft8_stage<2, 6>(v, wc, t);
     fft8_transpose<2, 3, false>(v, sh, t);
-    fft8_stage<3, 7>(v, w, t, logm);
-    fft8_stage<3, 8>(v, w, t, logm);
-    fft8_stage<3, 9>(v, w, t, logm);
+    fft8_stage<3, 7>(v, wc, t);
+    fft8_stage<3, 8>(v, wc, t);
+    fft8_stage<3, 9>(v, wc, t);
     fft8_transpose<3, 4, true>(v, sh, t);
-    fft8_stage<4, 10>(v, w, t, logm);
-    fft8_stage<4, 11>(v, w, t, logm);
+    fft8_stage<4, 10>(v, wc, t);
+    fft8_stage<4, 11>(v, wc, t);
     if (mode == 0) {
         double2 *dst = a + (size_t)p * M + ((size_t)blk << 11);
 #pragma unroll
@@ -472,7 +472,7 @@ ckks_status fft_passes(ckks_ctx *ctx, double2 *work, uint32_t batch, int mode, d
     SlotSource none;
     prof_begin(ctx, K_FFT_A, bytes_a);
     if (gather && gather->Wd && logb == (uint32_t)kLogBA) {
-        hipLaunchKernelGGL(k_fft_a8, dim3(batch * (M >> logb)), dim3(256), 0, ctx->stream, work, ctx->d_fft_w, logm,
+        hipLaunchKernelGGL(k_fft_a8, dim3(batch * (M >> logb)), dim3(256), 0, ctx->stream, work, ctx->d_fft_wc, logm,
                            single ? mode : 0, ctx->d_fft_twist, c, m, *gather);
     } else {
         hipLaunchKernelGGL(k_fft_a, dim3(batch * (M >> logb)), dim3(kThreads), B * sizeof(double2), ctx->stream,
