@@ -17,7 +17,7 @@ follows the standard RNS-CKKS literature:
 
 Where the paper is silent the conventions are fixed here (each is a reading
 recorded in the design notes): prime choice, psi, bit-reversed evaluation
-order, round-half-away encode, non-centred uncorrected basis conversion,
+order, round-half-away encode, centred uncorrected basis conversion,
 centred rescale, sigma applied after ModUp, giant-step rotation before the
 rescale, and the feature-major slot map s = f*T + t.
 
@@ -368,8 +368,9 @@ class Ckks:
 
     # ---------------- basis conversion, ModUp, ModDown ----------------
     def conv(self, coef: np.ndarray, src: Sequence[int], dst: Sequence[int]) -> np.ndarray:
-        """Fast basis conversion of coefficient rows from primes src to primes dst (non-centred,
-        no overflow correction): result = x + u * Q_src for some 0 <= u < len(src)."""
+        """Fast basis conversion of coefficient rows from primes src to primes dst (centred digits
+        y_i in (-q_i/2, q_i/2], no overflow correction): result = x + u * Q_src, x the centred
+        representative modulo Q_src and |u| <= len(src) // 2."""
         qs = [self.primes[k] for k in src]
         qt = [self.primes[k] for k in dst]
         Qs = math.prod(qs)

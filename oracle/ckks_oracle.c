@@ -199,8 +199,11 @@ void or_reduce_i64(const int64_t *v, uint64_t *out, int64_t rows, int64_t n, con
 
 /* ------------------------------------------------------------------------ */
 /* Fast basis conversion (Cheon-Han-Kim-Kim-Song 2018, the approximate form  */
-/* without overflow correction):                                             */
-/*   Conv(a)_t = sum_{i in I} [a_i * Qhat_i^-1]_{q_i} * [Qhat_i]_t  (mod t)  */
+/* without overflow correction), with centred digits:                        */
+/*   y_i = [a_i * Qhat_i^-1]_{q_i} taken in (-q_i/2, q_i/2] (q_i odd),       */
+/*   Conv(a)_t = sum_{i in I} y_i * [Qhat_i]_t  (mod t).                     */
+/* The integer sum_i y_i Qhat_i is congruent to a modulo Q_I and has zero    */
+/* mean over uniform inputs, which keeps the key-switching error centred.    */
 /* in: [ni][n] coefficient residues mod qin[i]; out: [nt][n] mod qt[t].      */
 /* qhat_inv[i] = Qhat_i^-1 mod q_i; qhat_mod_t[i*nt + t] = Qhat_i mod qt[t]. */
 /* ------------------------------------------------------------------------ */
@@ -213,7 +216,14 @@ void or_conv(const uint64_t *in, const uint64_t *qin, int64_t ni, uint64_t *out,
             u128 acc = 0;
             for (int64_t i = 0; i < ni; i++) {
                 uint64_t y = mulm(in[i * n + j] % qin[i], qhat_inv[i], qin[i]);
-                acc += (u128)mulm(y, qhat_mod_t[i * nt + t] % qt[t], qt[t]);
+                uint64_t qh = qhat_mod_t[i * nt + t] % qt[t];
+                if (y > qin[i] / 2) {
+                    /* y stands for the negative value -(q_i - y) */
+                    uint64_t m = mulm((qin[i] - y) % qt[t], qh, qt[t]);
+                    acc += m ? qt[t] - m : 0;
+                } else {
+                    acc += (u128)mulm(y % qt[t], qh, qt[t]);
+                }
             }
             out[t * n + j] = (uint64_t)(acc % qt[t]);
         }

@@ -45,13 +45,15 @@ struct LimbMap {
 };
 
 // Device constants of one fast basis conversion, from the primes src[0..ns) to
-// dst[0..nt): y_i = [x_i * qhat_inv_i]_{src_i}, out_t = sum_i y_i [Qhat_i]_t.
+// dst[0..nt): y_i = [x_i * qhat_inv_i]_{src_i} centred in (-src_i/2, src_i/2],
+// out_t = sum_i y_i [Qhat_i]_t.
 struct ConvDev {
     int ns = 0, nt = 0;
     uint8_t src[kMaxPrimes];
     uint8_t dst[kMaxPrimes];
     ulonglong2 *d_qhat_inv = nullptr;  // [ns] (value, Shoup companion) mod src_i
     ulonglong2 *d_qhat_mod = nullptr;  // [ns][nt] (value, Shoup companion) mod dst_t
+    ulonglong2 *d_neg_q = nullptr;     // [nt] (value, Shoup companion) of [-Q_src]_dst_t
     bool f64 = false;                  // primes below 2^50, sources below twice the targets: fp64 tables set
     double *d_qhat_inv_f = nullptr;    // [ns] the values of d_qhat_inv as doubles
     double *d_qhat_mod_f = nullptr;    // [ns][nt] the values of d_qhat_mod as doubles

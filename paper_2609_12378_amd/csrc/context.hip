@@ -245,11 +245,19 @@ static ckks_status make_conv(ckks_ctx *c, const std::vector<uint32_t> &src, cons
             qmod[a * dst.size() + t] = shoup_pair(v, qt);
         }
     }
-    for (size_t t = 0; t < dst.size(); t++) out->dst[t] = (uint8_t)dst[t];
+    std::vector<ulonglong2> negq(dst.size() ? dst.size() : 1);
+    for (size_t t = 0; t < dst.size(); t++) {
+        out->dst[t] = (uint8_t)dst[t];
+        const uint64_t qt = c->primes[dst[t]];
+        uint64_t v = 1;  // Q_src mod q_t
+        for (uint32_t b : src) v = hm::mul(v, c->primes[b] % qt, qt);
+        negq[t] = shoup_pair(v ? qt - v : 0, qt);
+    }
     CK_TRY(upload((void **)&out->d_qhat_inv, qinv.data(), qinv.size() * sizeof(ulonglong2)));
     CK_TRY(upload((void **)&out->d_qhat_mod, qmod.data(), qmod.size() * sizeof(ulonglong2)));
+    CK_TRY(upload((void **)&out->d_neg_q, negq.data(), negq.size() * sizeof(ulonglong2)));
     // fp64 conversion: every prime below 2^50 and every source prime below twice every target prime (so the
-    // canonical y_i < 2 q_t and the sums stay exact)
+    // centred |y_i| < q_t and the sums stay exact)
     out->f64 = true;
     uint64_t max_src = 0, min_dst = ~0ull;
     for (uint32_t v : src) {
@@ -430,6 +438,7 @@ void ckks_ctx_destroy(ckks_ctx *c)
     for (auto &kv : c->conv) {
         if (kv.second.d_qhat_inv) (void)hipFree(kv.second.d_qhat_inv);
         if (kv.second.d_qhat_mod) (void)hipFree(kv.second.d_qhat_mod);
+        if (kv.second.d_neg_q) (void)hipFree(kv.second.d_neg_q);
         if (kv.second.d_qhat_inv_f) (void)hipFree(kv.second.d_qhat_inv_f);
         if (kv.second.d_qhat_mod_f) (void)hipFree(kv.second.d_qhat_mod_f);
     }

@@ -8,10 +8,13 @@
 //                      with the final additions of the rotation or relinearisation.
 //
 // The fast basis conversion (Cheon-Han-Kim-Kim-Song 2018) is
-//   Conv(x)_t = sum_i [x_i * Qhat_i^-1]_{q_i} * [Qhat_i]_t  (mod t),
-// non-centred and without overflow correction.  Every constant multiplier is a
-// Shoup product, so a conversion with ns source limbs and nt targets costs
-// ns + ns*nt Shoup multiplications per coefficient.  The inner dimension
+//   Conv(x)_t = sum_i y_i * [Qhat_i]_t  (mod t),  y_i = [x_i * Qhat_i^-1]_{q_i} in (-q_i/2, q_i/2],
+// without overflow correction.  Centred digits give the ModUp digits and the
+// ModDown rounding a zero mean: with [0, q_i) digits every digit carries a
+// constant offset of about |I|/2 * Q_I whose product with the key error piles
+// up in the slots next to X = +-1.  Every constant multiplier is a Shoup
+// product, so a conversion with ns source limbs and nt targets costs
+// ns + ns*nt + nt Shoup multiplications per coefficient.  The inner dimension
 // (ns <= 8 at the benchmark parameters) is far too small and too wide-integer
 // for the matrix cores, so it runs on the vector ALUs.
 #include "ckks_internal.h"
@@ -39,21 +42,28 @@ struct ConvArgs {
 
 // in: [polys][ns][N] (stride in_stride rows between polys), coefficient form;
 // out row for target ti: out + (poly*out_stride + (ti < split ? ti : ti + skip)) * N.
-// The ns + ns*nt Shoup constants and the target moduli are staged in LDS once per
-// block, so the per-target loop reads them at LDS latency instead of waiting on
-// scalar memory loads.
+// A digit y_i > q_i/2 stands for y_i - q_i, so the centred sum is the sum of the
+// canonical digits plus neg * [-Q_I]_t, neg the number of such digits.  The
+// Shoup constants and the target moduli are staged in LDS once per block, so the
+// per-target loop reads them at LDS latency instead of waiting on scalar memory
+// loads.
 template <int NS_MAX>
 __global__ __launch_bounds__(kThreads) void k_conv(const uint64_t *in, uint32_t in_stride, uint64_t *out,
                                                     uint32_t out_stride, uint32_t split, uint32_t skip, ConvArgs a,
                                                     const ulonglong2 *__restrict__ qhat_inv,
                                                     const ulonglong2 *__restrict__ qhat_mod,
+                                                    const ulonglong2 *__restrict__ neg_q,
                                                     const ModQ *__restrict__ mods, uint32_t log_n)
 {
     __shared__ ulonglong2 s_mod[NS_MAX * kMaxPrimes];
+    __shared__ ulonglong2 s_neg[kMaxPrimes];
     __shared__ uint64_t s_tq[kMaxPrimes];
     const int ns = a.ns, nt = a.nt;
     for (int k = threadIdx.x; k < ns * nt; k += kThreads) s_mod[k] = qhat_mod[k];
-    for (int k = threadIdx.x; k < nt; k += kThreads) s_tq[k] = mods[a.dst[k]].q;
+    for (int k = threadIdx.x; k < nt; k += kThreads) {
+        s_tq[k] = mods[a.dst[k]].q;
+        s_neg[k] = neg_q[k];
+    }
     __syncthreads();
     const uint32_t n = 1u << log_n;
     const uint32_t col = blockIdx.x * kThreads + threadIdx.x;
@@ -61,18 +71,21 @@ __global__ __launch_bounds__(kThreads) void k_conv(const uint64_t *in, uint32_t 
     if (col >= n) return;
     const uint64_t *src = in + ((size_t)poly * in_stride << log_n) + col;
     uint64_t y[NS_MAX];
+    uint64_t neg = 0;
 #pragma unroll
     for (int i = 0; i < NS_MAX; i++) {
         if (i < ns) {
             const uint64_t q = mods[a.src[i]].q;
             const ulonglong2 w = qhat_inv[i];
             y[i] = shoup(src[(size_t)i << log_n], w.x, w.y, q);
+            neg += y[i] > (q >> 1);
         }
     }
     uint64_t *dst = out + ((size_t)poly * out_stride << log_n) + col;
     for (int t = 0; t < nt; t++) {
         const uint64_t qt = s_tq[t], two = 2 * qt;
-        uint64_t acc = 0;
+        const ulonglong2 wn = s_neg[t];
+        uint64_t acc = shoup_lazy(neg, wn.x, wn.y, qt);
 #pragma unroll
         for (int i = 0; i < NS_MAX; i++) {
             if (i < ns) {
@@ -85,10 +98,10 @@ __global__ __launch_bounds__(kThreads) void k_conv(const uint64_t *in, uint32_t 
     }
 }
 
-// The same conversion in fp64 (every prime below 2^50): y_i = x_i * qhat_inv_i mod s_i is made canonical by
-// adding s_i to a negative result (|mul| < s_i for canonical operands), then each target sums the products
-// y_i * [Qhat_i]_t (each < 1.25 t, since y_i < 2^50 < 2 t) with a range reduction every four terms (sums stay
-// below 5.5 t < 2^53) and writes the canonical residue: the same integers as k_conv.
+// The same conversion in fp64 (every prime below 2^50): y_i = x_i * qhat_inv_i mod s_i (|mul| < 0.875 s_i for
+// canonical operands) is moved into (-s_i/2, s_i/2] by one add or subtract of s_i, then each target sums the
+// products y_i * [Qhat_i]_t (each below 0.875 t in magnitude, since |y_i| < s_i/2 < t) with a range reduction
+// every four terms (sums stay below 4 t < 2^53) and writes the canonical residue: the same integers as k_conv.
 template <int NS_MAX>
 __global__ __launch_bounds__(kThreads) void k_conv_f64(const uint64_t *in, uint32_t in_stride, uint64_t *out,
                                                         uint32_t out_stride, uint32_t split, uint32_t skip,
@@ -113,7 +126,8 @@ __global__ __launch_bounds__(kThreads) void k_conv_f64(const uint64_t *in, uint3
         if (i < ns) {
             const nttc::Ar<true> ar(mods[a.src[i]]);
             const double v = ar.mul(nttc::Ar<true>::from_u64(src[(size_t)i << log_n]), qhat_inv[i]);
-            y[i] = v < 0.0 ? v + ar.q : v;
+            const double h = 0.5 * ar.q;
+            y[i] = v > h ? v - ar.q : (v < -h ? v + ar.q : v);
         }
     }
     uint64_t *dst = out + ((size_t)poly * out_stride << log_n) + col;
@@ -329,16 +343,16 @@ ckks_status launch_conv(ckks_ctx *ctx, const ConvDev *cd, const uint64_t *in, ui
                                skip, a, cd->d_qhat_inv_f, cd->d_qhat_mod_f, ctx->d_mod, ctx->log_n);
     } else if (a.ns <= 4)
         hipLaunchKernelGGL(k_conv<4>, grid, block, 0, ctx->stream, in, in_stride, out, out_stride, split, skip, a,
-                           cd->d_qhat_inv, cd->d_qhat_mod, ctx->d_mod, ctx->log_n);
+                           cd->d_qhat_inv, cd->d_qhat_mod, cd->d_neg_q, ctx->d_mod, ctx->log_n);
     else if (a.ns <= 8)
         hipLaunchKernelGGL(k_conv<8>, grid, block, 0, ctx->stream, in, in_stride, out, out_stride, split, skip, a,
-                           cd->d_qhat_inv, cd->d_qhat_mod, ctx->d_mod, ctx->log_n);
+                           cd->d_qhat_inv, cd->d_qhat_mod, cd->d_neg_q, ctx->d_mod, ctx->log_n);
     else if (a.ns <= 16)
         hipLaunchKernelGGL(k_conv<16>, grid, block, 0, ctx->stream, in, in_stride, out, out_stride, split, skip, a,
-                           cd->d_qhat_inv, cd->d_qhat_mod, ctx->d_mod, ctx->log_n);
+                           cd->d_qhat_inv, cd->d_qhat_mod, cd->d_neg_q, ctx->d_mod, ctx->log_n);
     else if (a.ns <= 32)
         hipLaunchKernelGGL(k_conv<32>, grid, block, 0, ctx->stream, in, in_stride, out, out_stride, split, skip, a,
-                           cd->d_qhat_inv, cd->d_qhat_mod, ctx->d_mod, ctx->log_n);
+                           cd->d_qhat_inv, cd->d_qhat_mod, cd->d_neg_q, ctx->d_mod, ctx->log_n);
     else {
         prof_end(ctx, K_CONV);
         return set_error(CKKS_EUNSUPPORTED, "basis conversion from %d limbs (at most 32)", a.ns);

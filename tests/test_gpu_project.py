@@ -14,7 +14,11 @@
 * the Llama-shaped projection parameters at full ring degree (N = 2^16, 24 + 8
   limbs of 50-bit primes, dnum 3, level 12, 128 tokens x 256 features, n1 = 32,
   n2 = 8 so 31 baby and 7 giant rotations) on a 256 x 512 slice of the weights
-  (one input ciphertext, two output ciphertexts), bit for bit.
+  (one input ciphertext, two output ciphertexts), bit for bit, and decrypted
+  within 2^-18 of X @ W.
+
+Every compared output is also decrypted and decoded on both sides: the GPU's
+slots agree with the oracle's within 2^-20 of the scale.
 """
 import dataclasses
 
@@ -78,6 +82,11 @@ def run_case(cfg, d_in, d_out, oracle_outputs, arith=0, max_pairs=0, weight_scal
         bad = np.argwhere(got != wo)
         assert bad.size == 0, "output %d: first mismatches %s" % (j, bad[:5].tolist())
         assert outs[j].scale == delta
+        # decrypted parity in slot units (relative to the scale): the GPU's decrypt + decode against the oracle's
+        re, im = ctx.decode(ctx.decrypt(s_dev, outs[j]))
+        zo = ck.decode(ck.decrypt(s, wo), delta)
+        assert np.max(np.abs(to_host(re) - zo.real)) <= 2.0 ** -20
+        assert np.max(np.abs(to_host(im) - zo.imag)) <= 2.0 ** -20
     Y = X @ W
     errs = []
     for j, o in enumerate(outs):
@@ -127,4 +136,6 @@ def test_projection_parameters_full_degree_slice():
     say("full-degree slice")
     err = run_case(PROJECTION, 256, 512, [0, 1])
     say("slice max error vs X@W", err)
-    assert err <= 2.0 ** -12
+    # fresh noise ~2^-29, one hoisted rotation ~2^-20.5 at most over 32768 slots, 38 rotated terms summed and
+    # one rescale: the oracle measures 2^-22.4 on this slice, the bound leaves a factor of 2^4
+    assert err <= 2.0 ** -18

@@ -1,7 +1,9 @@
 """Pins for the oracle's RNS machinery, checked with Python big integers:
 
 * CRT lift reproduces the integer it came from;
-* fast basis conversion equals x + u*Q_I with 0 <= u < |I| (Cheon-Han-Kim-Kim-Song 2018);
+* fast basis conversion with centred digits equals x + u*Q_I, x the centred
+  representative modulo Q_I and |u| <= |I|//2 (Cheon-Han-Kim-Kim-Song 2018), so
+  one source limb gives the centred lift itself;
 * ModDown(P * c) = c exactly;
 * rescale equals round(c / q_l) coefficient by coefficient;
 * the NTT-domain automorphism sigma_g(a)(X) = a(X^g) agrees with the
@@ -42,18 +44,25 @@ def test_crt_lift_round_trip():
 
 
 @pytest.mark.parametrize("src,dst", [([0, 1, 2], [3, 4, 5, 6, 7, 8]), ([6, 7, 8], [0, 1, 2, 3, 4, 5]),
-                                     ([4], [0, 1, 6])])
+                                     ([0, 1, 2, 3], [6, 7, 8]), ([4], [0, 1, 6])])
 def test_basis_conversion_overflow_form(src, dst):
     ck = _ck()
     a = uniform_residues(rng(3, 1, extra=len(src)), [ck.primes[k] for k in src], ck.n)
     out = ck.conv(a, src, dst)
     qs = [ck.primes[k] for k in src]
     QI = math.prod(qs)
-    for j in range(0, ck.n, 7):
+    half = len(src) // 2
+    seen = set()
+    for j in range(0, ck.n, 3):
         x = _crt([a[r, j] for r in range(len(src))], qs)
-        ok = [u for u in range(len(src))
+        if x > QI // 2:
+            x -= QI
+        ok = [u for u in range(-half, half + 1)
               if all((x + u * QI) % ck.primes[k] == int(out[r, j]) for r, k in enumerate(dst))]
         assert len(ok) == 1, j
+        seen.add(ok[0])
+    # the overflow takes both signs once there are two or more digits (it is centred, not one-sided)
+    assert min(seen) < 0 < max(seen) if half else seen == {0}
 
 
 def test_moddown_of_p_multiple_is_exact():
@@ -81,9 +90,13 @@ def test_moddown_divides_by_p_with_bounded_error():
     for j in range(ck.n):
         X = _crt(xc[:, j], mods_ext)
         Y = _crt(oc[:, j], mods_q)
-        # Y = (X - ([X]_P + u P)) / P mod Q_l for some 0 <= u < K: floor division up to K
-        base = X // ck.P
-        assert any((base - u) % Ql == Y for u in range(ck.n_p)), j
+        # Y = (X - (x_c + u P)) / P mod Q_l, x_c the centred residue of X mod P and |u| <= K // 2:
+        # division rounded to nearest, up to the centred overflow
+        P = ck.P
+        xc_ = (X + (P - 1) // 2) % P - (P - 1) // 2
+        base = (X - xc_) // P
+        half = ck.n_p // 2
+        assert sum((base - u) % Ql == Y for u in range(-half, half + 1)) == 1, j
 
 
 def test_rescale_is_rounded_division():
