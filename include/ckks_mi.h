@@ -19,7 +19,7 @@
  * Layout.  A polynomial is a [limbs][N] array of uint64 residues, limb-major;
  *   limb k of a ciphertext or plaintext is reduced modulo q_k and stored in
  *   the NTT domain: index j holds a(psi_k^(2*brev(j)+1)) mod q_k, where psi_k
- *   is the context's primitive 2N-th root for q_k (ckks_ctx_primes).  Every
+ *   is the context's primitive 2N-th root for q_k (ckks_ctx_tables).  Every
  *   stored residue is canonical, in [0, q_k).  A ciphertext is [2][limbs][N]
  *   (c0 then c1); its level is limbs - 1.
  * Streams.  Calls are asynchronous on the context's HIP stream and validate
@@ -100,7 +100,42 @@ ckks_status ckks_ctx_set_ntt_arith(ckks_ctx *ctx, int mode);
 ckks_status ckks_ctx_set_proj_batch(ckks_ctx *ctx, uint32_t max_pairs);
 /* Host copies of the primes q (n_q), p (n_p) and psi (n_q + n_p, q first);
  * any pointer may be NULL. */
-ckks_status ckks_ctx_primes(const ckks_ctx *ctx, uint64_t *q, uint64_t *p, uint64_t *psi);
+ckks_status ckks_ctx_tables(const ckks_ctx *ctx, uint64_t *q, uint64_t *p, uint64_t *psi);
+
+/* Workspace.  Calls that need device scratch memory take it from the
+ * context's arena, which the library grows with hipMalloc on demand.  A
+ * caller that cannot have the library allocate (graph capture, pooled
+ * allocators) hands it a workspace instead: ckks_set_workspace(ctx, dev,
+ * bytes) makes dev[0, bytes) (device memory, 256-byte aligned, owned by the
+ * caller, which keeps it alive until the context is destroyed or another
+ * workspace is set) the arena; the library frees its own arena and never
+ * allocates scratch again (the basis-conversion tables of every level, which
+ * calls otherwise build on first use, are built here), and a call that needs
+ * more than `bytes` fails with CKKS_ENOMEM before any launch.  ckks_set_workspace(ctx, NULL, 0)
+ * returns to library-managed scratch.  It synchronizes the context stream
+ * first (work in flight may still use the old arena).  All calls on one
+ * context share the workspace, so they must be ordered on its stream.
+ *
+ * ckks_workspace_bytes returns the bytes one call of `op` takes, for the
+ * shape given as shape[] (unused entries may be omitted; shape may be NULL
+ * where noted), or SIZE_MAX for an unknown op or invalid shape.  The figure
+ * for CKKS_OP_LINEAR_PROJECT depends on ckks_ctx_set_proj_batch. */
+typedef enum {
+    CKKS_OP_NONE = 0,           /* ntt, intt, add, mul_plain, automorph: no workspace */
+    CKKS_OP_ENCODE = 1,         /* shape unused */
+    CKKS_OP_DECODE = 2,         /* shape[0] = limbs of the plaintext */
+    CKKS_OP_ENCRYPT = 3,        /* shape[0] = limbs */
+    CKKS_OP_DECRYPT = 4,        /* shape[0] = limbs */
+    CKKS_OP_KEYGEN = 5,         /* Galois and relinearisation keys; shape unused */
+    CKKS_OP_RESCALE = 6,        /* shape[0] = limbs of the input */
+    CKKS_OP_ROTATE = 7,         /* shape[0] = limbs, shape[1] = rotations of one hoisted call (1: ckks_rotate) */
+    CKKS_OP_MUL_RELIN = 8,      /* shape[0] = limbs */
+    CKKS_OP_MODUP = 9,          /* shape[0] = level */
+    CKKS_OP_MODDOWN = 10,       /* shape[0] = level */
+    CKKS_OP_LINEAR_PROJECT = 11 /* shape = {limbs of the inputs, tokens, d_in, d_out, n1} */
+} ckks_op;
+size_t ckks_workspace_bytes(const ckks_ctx *ctx, int op, const uint32_t *shape);
+ckks_status ckks_set_workspace(ckks_ctx *ctx, void *dev, size_t bytes);
 /* Galois element 5^steps mod 2N of a left slot rotation by steps (any sign). */
 uint32_t ckks_galois_elt(const ckks_ctx *ctx, int32_t steps);
 const char *ckks_last_error(void);
@@ -199,7 +234,7 @@ ckks_status ckks_automorph(ckks_ctx *ctx, const uint64_t *dev_in, uint32_t rows,
  * same scale; out: d_out/D ciphertexts with n_limbs = level (the rescale
  * drops q_level) whose scale is set to the input scale (the plaintext scale
  * q_level cancels exactly in the rescale).  Scratch comes from the context's
- * arena (grown with hipMalloc on first use). */
+ * arena or workspace (ckks_workspace_bytes, CKKS_OP_LINEAR_PROJECT). */
 typedef struct {
     uint32_t tokens, d_in, d_out, n1;
 } ckks_proj_shape;

@@ -53,7 +53,9 @@ _SIGS = {
     "ckks_ctx_set_stream": (ctypes.c_int, [_VP, _VP]),
     "ckks_ctx_set_ntt_arith": (ctypes.c_int, [_VP, ctypes.c_int]),
     "ckks_ctx_set_proj_batch": (ctypes.c_int, [_VP, _U32]),
-    "ckks_ctx_primes": (ctypes.c_int, [_VP, _VP, _VP, _VP]),
+    "ckks_ctx_tables": (ctypes.c_int, [_VP, _VP, _VP, _VP]),
+    "ckks_workspace_bytes": (ctypes.c_size_t, [_VP, ctypes.c_int, _VP]),
+    "ckks_set_workspace": (ctypes.c_int, [_VP, _VP, ctypes.c_size_t]),
     "ckks_galois_elt": (_U32, [_VP, _I32]),
     "ckks_last_error": (ctypes.c_char_p, []),
     "ckks_ntt": (ctypes.c_int, [_VP, _VP, _U32, _U32, _U32]),
@@ -172,7 +174,7 @@ class Context:
         qo = (ctypes.c_uint64 * max(n_q, 1))()
         po = (ctypes.c_uint64 * max(n_p, 1))()
         so = (ctypes.c_uint64 * (n_q + n_p))()
-        _check(L.ckks_ctx_primes(h, qo, po, so), "ckks_ctx_primes")
+        _check(L.ckks_ctx_tables(h, qo, po, so), "ckks_ctx_tables")
         self.q = list(qo)[:n_q]
         self.p = list(po)[:n_p]
         self.psi = list(so)
@@ -195,6 +197,27 @@ class Context:
     def set_proj_batch(self, max_pairs: int):
         """Cap the (input, baby step) pairs per projection launch (0 = by the 2 GiB staging budget)."""
         _check(self.lib.ckks_ctx_set_proj_batch(self.h, max_pairs), "ckks_ctx_set_proj_batch")
+
+    # workspace op codes (ckks_op)
+    OP_ENCODE, OP_DECODE, OP_ENCRYPT, OP_DECRYPT, OP_KEYGEN, OP_RESCALE, OP_ROTATE, OP_MUL_RELIN, OP_MODUP, \
+        OP_MODDOWN, OP_LINEAR_PROJECT = range(1, 12)
+
+    def workspace_bytes(self, op: int, shape=()) -> int:
+        """Device bytes one call of `op` takes from the arena or workspace, for the given shape."""
+        arr = (_U32 * max(1, len(shape)))(*shape)
+        b = int(self.lib.ckks_workspace_bytes(self.h, op, arr if shape else None))
+        if b == (1 << 64) - 1:
+            raise CkksError("ckks_workspace_bytes: " + self.lib.ckks_last_error().decode(errors="replace"))
+        return b
+
+    def set_workspace(self, buf: Optional[torch.Tensor]):
+        """Use buf (a device tensor the caller keeps alive) as the scratch arena; None: library-managed."""
+        if buf is None:
+            _check(self.lib.ckks_set_workspace(self.h, None, 0), "ckks_set_workspace")
+        else:
+            _check(self.lib.ckks_set_workspace(self.h, _ptr(buf), buf.numel() * buf.element_size()),
+                   "ckks_set_workspace")
+        self._workspace = buf
 
     def galois_elt(self, steps: int) -> int:
         return int(self.lib.ckks_galois_elt(self.h, steps))

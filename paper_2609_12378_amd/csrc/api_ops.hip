@@ -23,6 +23,49 @@ size_t words(const ckks_ctx *ctx, size_t rows) { return rows << ctx->log_n; }
 
 }  // namespace
 
+// Workspace bytes of one call of `op` (ckks_op) with the given shape; SIZE_MAX for an unknown op or shape.
+// Every call below takes exactly this many bytes from the context's arena.
+size_t op_workspace_bytes(const ckks_ctx *ctx, int op, const uint32_t *shape)
+{
+    const size_t N = ctx->n;
+    const uint32_t a = shape ? shape[0] : 0;
+    switch (op) {
+    case CKKS_OP_NONE: return 0;
+    case CKKS_OP_ENCODE: return enc_work_bytes(ctx, 1) + N * sizeof(int64_t);
+    case CKKS_OP_DECODE:
+        if (a < 1 || a > ctx->n_q) return SIZE_MAX;
+        return words(ctx, a > 1 ? 2 : 1) * 8 + enc_work_bytes(ctx, 1);
+    case CKKS_OP_ENCRYPT:
+        if (a < 1 || a > ctx->n_q) return SIZE_MAX;
+        return words(ctx, 2 * (size_t)a) * 8;
+    case CKKS_OP_DECRYPT:
+        if (a < 1 || a > ctx->n_q) return SIZE_MAX;
+        return words(ctx, a) * 8;
+    case CKKS_OP_KEYGEN: return words(ctx, 3 * (size_t)ctx->n_primes()) * 8;
+    case CKKS_OP_RESCALE:
+        if (a < 2 || a > ctx->n_q) return SIZE_MAX;
+        return words(ctx, 2 + 2 * (size_t)(a - 1)) * 8;
+    case CKKS_OP_ROTATE: {
+        const uint32_t count = shape ? shape[1] : 0;
+        if (a < 1 || a > ctx->n_q || count < 1) return SIZE_MAX;
+        return ks_scratch_words(ctx, a - 1, ks_rot_batch(count)) * 8;
+    }
+    case CKKS_OP_MUL_RELIN:
+        if (a < 1 || a > ctx->n_q) return SIZE_MAX;
+        return (3 * (size_t)a * N + ks_scratch_words(ctx, a - 1, 1)) * 8;
+    case CKKS_OP_MODUP:
+        if (!shape || a >= ctx->n_q) return SIZE_MAX;
+        return ((size_t)n_digits(ctx, a) * (a + 1 + ctx->n_p) + ctx->alpha) * N * 8;
+    case CKKS_OP_MODDOWN:
+        if (!shape || a >= ctx->n_q) return SIZE_MAX;
+        return ((size_t)(a + 1 + ctx->n_p) + (a + 1)) * N * 8;
+    case CKKS_OP_LINEAR_PROJECT:
+        if (!shape) return SIZE_MAX;
+        return proj_workspace_bytes(ctx, shape[0], shape[1], shape[2], shape[3], shape[4]);
+    default: return SIZE_MAX;
+    }
+}
+
 // rotations of one ciphertext sharing a single ModUp (used by the API and the projection),
 // processed in batches of ks_rot_batch(count).  work: ks_scratch_words(level, ks_rot_batch(count)) words
 ckks_status rotate_core(ckks_ctx *ctx, const uint64_t *c, uint32_t level, const int32_t *steps,
@@ -100,7 +143,7 @@ ckks_status ckks_encode(ckks_ctx *ctx, const double *re, const double *im, doubl
     CK_REQUIRE(scale > 0 && std::isfinite(scale), CKKS_EINVAL, "encode: scale must be positive");
     void *w;
     const size_t N = ctx->n;
-    CK_TRY(ctx_scratch(ctx, enc_work_bytes(ctx, 1) + N * sizeof(int64_t), &w));
+    CK_TRY(ctx_scratch(ctx, op_workspace_bytes(ctx, CKKS_OP_ENCODE, nullptr), &w));
     double2 *work = (double2 *)w;
     int64_t *m = (int64_t *)((char *)w + enc_work_bytes(ctx, 1));
     SlotSource src;
@@ -120,7 +163,7 @@ ckks_status ckks_decode(ckks_ctx *ctx, const ckks_buf *pt, double *re, double *i
     CK_REQUIRE(pt->scale > 0, CKKS_ESCALE, "decode: scale must be positive");
     const uint32_t lim = pt->n_limbs > 1 ? 2 : 1;
     void *w;
-    CK_TRY(ctx_scratch(ctx, words(ctx, lim) * 8 + enc_work_bytes(ctx, 1), &w));
+    CK_TRY(ctx_scratch(ctx, op_workspace_bytes(ctx, CKKS_OP_DECODE, &pt->n_limbs), &w));
     uint64_t *coef = (uint64_t *)w;
     double2 *work = (double2 *)(coef + words(ctx, lim));
     HIP_TRY(hipMemcpyAsync(coef, pt->data, words(ctx, lim) * 8, hipMemcpyDeviceToDevice, ctx->stream));
@@ -138,7 +181,7 @@ ckks_status ckks_encrypt_sk(ckks_ctx *ctx, const int8_t *s, const ckks_buf *pt, 
     CK_REQUIRE(ct->n_limbs == pt->n_limbs, CKKS_ELEVEL, "encrypt: limb counts differ");
     const uint32_t L = pt->n_limbs;
     void *w;
-    CK_TRY(ctx_scratch(ctx, words(ctx, 2 * L) * 8, &w));
+    CK_TRY(ctx_scratch(ctx, op_workspace_bytes(ctx, CKKS_OP_ENCRYPT, &L), &w));
     uint64_t *sn = (uint64_t *)w, *en = sn + words(ctx, L);
     const LimbMap map = limb_range(0, L);
     CK_TRY(launch_expand_i8(ctx, sn, s, map));
@@ -158,7 +201,7 @@ ckks_status ckks_decrypt(ckks_ctx *ctx, const int8_t *s, const ckks_buf *ct, ckk
     CK_REQUIRE(ct->n_limbs == pt->n_limbs, CKKS_ELEVEL, "decrypt: limb counts differ");
     const uint32_t L = ct->n_limbs;
     void *w;
-    CK_TRY(ctx_scratch(ctx, words(ctx, L) * 8, &w));
+    CK_TRY(ctx_scratch(ctx, op_workspace_bytes(ctx, CKKS_OP_DECRYPT, &L), &w));
     uint64_t *sn = (uint64_t *)w;
     const LimbMap map = limb_range(0, L);
     CK_TRY(launch_expand_i8(ctx, sn, s, map));
@@ -178,7 +221,7 @@ static ckks_status keygen_common(ckks_ctx *ctx, const int8_t *s, uint32_t g, boo
     const uint32_t R = ctx->n_primes();
     const size_t rows = R;
     void *w;
-    CK_TRY(ctx_scratch(ctx, words(ctx, 3 * rows) * 8, &w));
+    CK_TRY(ctx_scratch(ctx, op_workspace_bytes(ctx, CKKS_OP_KEYGEN, nullptr), &w));
     uint64_t *sn = (uint64_t *)w, *t = sn + words(ctx, rows), *en = t + words(ctx, rows);
     const LimbMap all = limb_range(0, R);
     CK_TRY(launch_expand_i8(ctx, sn, s, all));
@@ -252,7 +295,7 @@ ckks_status ckks_rescale(ckks_ctx *ctx, const ckks_buf *in, ckks_buf *out)
     CK_REQUIRE(out->n_limbs == in->n_limbs - 1, CKKS_ELEVEL, "rescale: output must have one limb fewer");
     const uint32_t l = in->n_limbs - 1;
     void *w;
-    CK_TRY(ctx_scratch(ctx, words(ctx, 2 + 2 * l) * 8, &w));
+    CK_TRY(ctx_scratch(ctx, op_workspace_bytes(ctx, CKKS_OP_RESCALE, &in->n_limbs), &w));
     CK_TRY(rescale_core(ctx, in->data, l, out->data, (uint64_t *)w));
     out->scale = in->scale / (double)ctx->primes[l];
     return CKKS_OK;
@@ -277,7 +320,8 @@ ckks_status ckks_rotate_hoisted(ckks_ctx *ctx, const ckks_buf *in, const int32_t
     }
     const uint32_t level = in->n_limbs - 1;
     void *w;
-    CK_TRY(ctx_scratch(ctx, ks_scratch_words(ctx, level, ks_rot_batch(count)) * 8, &w));
+    const uint32_t shp[2] = {in->n_limbs, count};
+    CK_TRY(ctx_scratch(ctx, op_workspace_bytes(ctx, CKKS_OP_ROTATE, shp), &w));
     CK_TRY(rotate_core(ctx, in->data, level, steps, keys, count, op.data(), (uint64_t *)w));
     for (uint32_t r = 0; r < count; r++) outs[r].scale = in->scale;
     return CKKS_OK;
@@ -302,7 +346,7 @@ ckks_status ckks_mul_relin(ckks_ctx *ctx, const ckks_buf *a, const ckks_buf *b, 
     const uint32_t ext = L + ctx->n_p, nd = n_digits(ctx, level);
     const size_t N = ctx->n;
     void *w;
-    CK_TRY(ctx_scratch(ctx, (3 * (size_t)L * N + ks_scratch_words(ctx, level, 1)) * 8, &w));
+    CK_TRY(ctx_scratch(ctx, op_workspace_bytes(ctx, CKKS_OP_MUL_RELIN, &L), &w));
     uint64_t *d0 = (uint64_t *)w, *d1 = d0 + L * N, *d2 = d1 + L * N;
     uint64_t *digits = d2 + L * N;
     uint64_t *u = digits + ((size_t)nd * ext + ctx->alpha) * N;
@@ -324,7 +368,7 @@ ckks_status ckks_modup(ckks_ctx *ctx, const uint64_t *c, uint32_t level, uint64_
     const uint32_t ext = level + 1 + ctx->n_p, nd = n_digits(ctx, level);
     const size_t N = ctx->n;
     void *w;
-    CK_TRY(ctx_scratch(ctx, ((size_t)nd * ext + ctx->alpha) * N * 8, &w));
+    CK_TRY(ctx_scratch(ctx, op_workspace_bytes(ctx, CKKS_OP_MODUP, &level), &w));
     CK_TRY(ks_modup(ctx, c, level, (uint64_t *)w));
     HIP_TRY(hipMemcpyAsync(digits, w, (size_t)nd * ext * N * 8, hipMemcpyDeviceToDevice, ctx->stream));
     return CKKS_OK;
@@ -339,7 +383,7 @@ ckks_status ckks_moddown(ckks_ctx *ctx, const uint64_t *x, uint32_t level, uint6
     const uint32_t ext = level + 1 + ctx->n_p, L = level + 1;
     const size_t N = ctx->n;
     void *w;
-    CK_TRY(ctx_scratch(ctx, ((size_t)ext + L) * N * 8, &w));
+    CK_TRY(ctx_scratch(ctx, op_workspace_bytes(ctx, CKKS_OP_MODDOWN, &level), &w));
     uint64_t *u = (uint64_t *)w, *cw = u + (size_t)ext * N;
     HIP_TRY(hipMemcpyAsync(u, x, (size_t)ext * N * 8, hipMemcpyDeviceToDevice, ctx->stream));
     return ks_moddown(ctx, u, 1, level, nullptr, 1, nullptr, out, cw);

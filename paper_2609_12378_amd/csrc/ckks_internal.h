@@ -98,6 +98,7 @@ struct ckks_ctx {
     // grow-only scratch arena
     void *scratch = nullptr;
     size_t scratch_bytes = 0;
+    bool scratch_external = false;  // the arena is a caller's workspace (ckks_set_workspace): never reallocated
 
     // optional per-kernel event profiling
     bool profiling = false;
@@ -116,6 +117,8 @@ struct ckks_ctx {
 
 // scratch of at least `bytes` bytes (256-byte aligned), growing the arena
 ckks_status ctx_scratch(ckks_ctx *ctx, size_t bytes, void **out);
+// workspace bytes of one call of a ckks_op (SIZE_MAX: unknown op or invalid shape)
+size_t op_workspace_bytes(const ckks_ctx *ctx, int op, const uint32_t *shape);
 
 // profiler brackets: call prof_begin before a launch and prof_end after;
 // bytes = the launch's algorithmic HBM bytes, ops = its nominal VALU lane

@@ -307,6 +307,10 @@ ckks_status ctx_conv(ckks_ctx *c, int level, int digit, const ConvDev **out)
 
 ckks_status ctx_scratch(ckks_ctx *c, size_t bytes, void **out)
 {
+    if (bytes == SIZE_MAX) return set_error(CKKS_EINVAL, "workspace size of an invalid shape");
+    if (bytes > c->scratch_bytes && c->scratch_external)
+        return set_error(CKKS_ENOMEM, "workspace of %zu bytes is too small: this call needs %zu", c->scratch_bytes,
+                         bytes);
     if (bytes > c->scratch_bytes) {
         if (c->scratch) {
             HIP_TRY(hipStreamSynchronize(c->stream));
@@ -430,6 +434,7 @@ void ckks_ctx_destroy(ckks_ctx *c)
     if (!c) return;
     (void)hipDeviceSynchronize();
     (void)prof_collect(c);
+    if (c->scratch_external) c->scratch = nullptr;  // the caller's workspace
     void *ptrs[] = {c->d_mod, c->d_tw, c->d_itw, c->d_twf, c->d_itwf, c->d_fft_w, c->d_fft_wc, c->d_fft_twist, c->d_slot_pos,
                     c->d_pos_slot,
                     c->d_pinv, c->d_pmodq, c->d_qlinv, c->scratch};
@@ -470,13 +475,48 @@ ckks_status ckks_ctx_set_proj_batch(ckks_ctx *c, uint32_t max_pairs)
     return CKKS_OK;
 }
 
-ckks_status ckks_ctx_primes(const ckks_ctx *c, uint64_t *q, uint64_t *p, uint64_t *psi)
+ckks_status ckks_ctx_tables(const ckks_ctx *c, uint64_t *q, uint64_t *p, uint64_t *psi)
 {
     clear_error();
     CK_REQUIRE(c, CKKS_EINVAL, "null context");
     if (q) memcpy(q, c->primes.data(), c->n_q * sizeof(uint64_t));
     if (p) memcpy(p, c->primes.data() + c->n_q, c->n_p * sizeof(uint64_t));
     if (psi) memcpy(psi, c->psi.data(), c->psi.size() * sizeof(uint64_t));
+    return CKKS_OK;
+}
+
+size_t ckks_workspace_bytes(const ckks_ctx *c, int op, const uint32_t *shape)
+{
+    clear_error();
+    if (!c) {
+        set_error(CKKS_EINVAL, "workspace_bytes: null context");
+        return SIZE_MAX;
+    }
+    const size_t b = op_workspace_bytes(c, op, shape);
+    if (b == SIZE_MAX) set_error(CKKS_EINVAL, "workspace_bytes: unknown op %d or invalid shape", op);
+    return b;
+}
+
+ckks_status ckks_set_workspace(ckks_ctx *c, void *dev, size_t bytes)
+{
+    clear_error();
+    CK_REQUIRE(c, CKKS_EINVAL, "set_workspace: null context");
+    CK_REQUIRE((dev == nullptr) == (bytes == 0), CKKS_EINVAL,
+               "set_workspace: dev and bytes must be both set or both zero");
+    CK_REQUIRE(((uintptr_t)dev & 255) == 0, CKKS_EINVAL, "set_workspace: dev must be 256-byte aligned");
+    HIP_TRY(hipStreamSynchronize(c->stream));
+    if (dev && c->n_p) {
+        // build every level's basis-conversion tables now, so no later call allocates them on first use
+        const ConvDev *cd;
+        for (uint32_t level = 0; level < c->n_q; level++) {
+            CK_TRY(ctx_conv(c, (int)level, -1, &cd));
+            for (uint32_t j = 0; j < n_digits(c, level); j++) CK_TRY(ctx_conv(c, (int)level, (int)j, &cd));
+        }
+    }
+    if (c->scratch && !c->scratch_external) HIP_TRY(hipFree(c->scratch));
+    c->scratch = dev;
+    c->scratch_bytes = bytes;
+    c->scratch_external = dev != nullptr;
     return CKKS_OK;
 }
 

@@ -82,6 +82,8 @@ ckks_status enc_feat_of_pos(ckks_ctx *ctx, uint32_t tokens, uint32_t *out);
 // residues of m ([batch][N]) into out ([batch][limbs][N]), primes 0..limbs-1
 ckks_status enc_to_rns(ckks_ctx *ctx, const int64_t *m, uint32_t batch, uint32_t limbs, uint64_t *out);
 size_t enc_work_bytes(const ckks_ctx *ctx, uint32_t batch);
+size_t proj_workspace_bytes(const ckks_ctx *ctx, uint32_t L, uint32_t tokens, uint32_t d_in, uint32_t d_out,
+                            uint32_t n1);
 // decode: coef = coefficient form of limbs 0..min(limbs,2)-1 ([limbs][N]); writes N/2 slots
 ckks_status dec_slots(ckks_ctx *ctx, const uint64_t *coef, uint32_t limbs, double scale, double2 *work, double *re,
                       double *im);

@@ -347,7 +347,52 @@ ckks_status launch_mac(ckks_ctx *ctx, uint64_t *acc, const uint64_t *pt, const u
     return CKKS_OK;
 }
 
+// Scratch words of one ckks_linear_project call, by region (every region a multiple of N words).
+struct ProjScratch {
+    uint32_t Pb;  // (input, baby step) pairs per plaintext sub-batch
+    bool diag;    // W re-laid as its cyclic diagonals (radix-8 FFT pass A)
+    size_t xrot_w, acc_w, tot_w, rot_w, pt_w, m_w, fft_w, ks_w, wd_w, fop_w, total;
+};
+
+ProjScratch proj_scratch(const ckks_ctx *ctx, uint32_t L, uint32_t D, uint32_t d_in, uint32_t d_out, uint32_t n1)
+{
+    ProjScratch ps{};
+    const uint32_t level = L - 1, n_in = d_in / D;
+    const size_t N = ctx->n, ctw = 2 * (size_t)L * N;
+    const uint32_t maxpairs = n_in * n1;
+    // plaintext sub-batch of at most 2 GiB: kJ output blocks x Pb (i, b) pairs
+    const size_t budget = size_t(1) << 31;
+    uint32_t Pmax = std::min<uint32_t>(maxpairs, std::max<uint32_t>(1, (uint32_t)(budget / ((size_t)kJ * L * N * 8))));
+    if (ctx->proj_max_pairs) Pmax = std::min(Pmax, ctx->proj_max_pairs);
+    ps.Pb = Pmax;
+    ps.xrot_w = (size_t)n_in * n1 * ctw;
+    ps.acc_w = ps.tot_w = ps.rot_w = (size_t)kJ * ctw;
+    ps.pt_w = (size_t)kJ * ps.Pb * L * N;
+    ps.m_w = (size_t)kJ * ps.Pb * N;               // int64 coefficients
+    ps.fft_w = (size_t)kJ * ps.Pb * (N / 2) * 2;   // double2 per slot
+    // key switching: hoisted baby steps of one input, or the giant step of a tile's kJ partial sums
+    ps.ks_w = std::max(ks_scratch_words(ctx, level, ks_rot_batch(n1 > 1 ? n1 - 1 : 1)),
+                       ks_scratch_words(ctx, level, ks_rot_batch(kJ), kJ));
+    // W re-laid as its cyclic diagonals, and the feature index of every FFT position, for the radix-8 FFT pass
+    ps.diag = D <= 256 && ctx->log_n >= 12;
+    ps.wd_w = ps.diag ? (size_t)d_in * d_out : 0;
+    ps.fop_w = ps.diag ? N / 4 : 0;
+    ps.total = ps.xrot_w + ps.acc_w + ps.tot_w + ps.rot_w + ps.pt_w + ps.m_w + ps.fft_w + ps.ks_w + ps.wd_w +
+               ps.fop_w;
+    return ps;
+}
+
 }  // namespace
+
+size_t proj_workspace_bytes(const ckks_ctx *ctx, uint32_t L, uint32_t tokens, uint32_t d_in, uint32_t d_out,
+                            uint32_t n1)
+{
+    const uint32_t slots = ctx->n / 2;
+    if (tokens < 1 || slots % tokens) return SIZE_MAX;
+    const uint32_t D = slots / tokens;
+    if (!d_in || !d_out || d_in % D || d_out % D || n1 < 1 || n1 > D || L < 2 || L > ctx->n_q) return SIZE_MAX;
+    return proj_scratch(ctx, L, D, d_in, d_out, n1).total * 8;
+}
 
 extern "C" ckks_status ckks_linear_project(ckks_ctx *ctx, const ckks_buf *in, const double *W,
                                            const ckks_proj_shape *shape, const int32_t *key_steps,
@@ -398,25 +443,11 @@ extern "C" ckks_status ckks_linear_project(ckks_ctx *ctx, const ckks_buf *in, co
 
     // ---- scratch layout
     const size_t N = ctx->n, ctw = 2 * (size_t)L * N;
-    const uint32_t maxpairs = n_in * n1;
-    // plaintext sub-batch of at most 2 GiB: J output blocks x Pb (i, b) pairs
-    const size_t budget = size_t(1) << 31;
-    const uint32_t Jt = kJ;
-    uint32_t Pmax = std::min<uint32_t>(maxpairs, std::max<uint32_t>(1, (uint32_t)(budget / ((size_t)Jt * L * N * 8))));
-    if (ctx->proj_max_pairs) Pmax = std::min(Pmax, ctx->proj_max_pairs);
-    const uint32_t Pb = Pmax;
-    const size_t xrot_w = (size_t)n_in * n1 * ctw;
-    const size_t acc_w = (size_t)kJ * ctw, tot_w = (size_t)kJ * ctw, rot_w = (size_t)kJ * ctw;
-    const size_t pt_w = (size_t)Jt * Pb * L * N;
-    const size_t m_w = (size_t)Jt * Pb * N;                       // int64 coefficients
-    const size_t fft_w = (size_t)Jt * Pb * (N / 2) * 2;            // double2 per slot
-    // key switching: hoisted baby steps of one input, or the giant step of a tile's kJ partial sums
-    const size_t ks_w = std::max(ks_scratch_words(ctx, level, ks_rot_batch(n1 > 1 ? n1 - 1 : 1)),
-                                 ks_scratch_words(ctx, level, ks_rot_batch(kJ), kJ));
-    // W re-laid as its cyclic diagonals, and the feature index of every FFT position, for the radix-8 FFT pass
-    const bool diag = D <= 256 && ctx->log_n >= 12;
-    const size_t wd_w = diag ? (size_t)shape->d_in * shape->d_out : 0, fop_w = diag ? N / 4 : 0;
-    const size_t total = xrot_w + acc_w + tot_w + rot_w + pt_w + m_w + fft_w + ks_w + wd_w + fop_w;
+    const ProjScratch ps = proj_scratch(ctx, L, D, shape->d_in, shape->d_out, n1);
+    const uint32_t Jt = kJ, Pb = ps.Pb;
+    const size_t xrot_w = ps.xrot_w, acc_w = ps.acc_w, tot_w = ps.tot_w, rot_w = ps.rot_w, pt_w = ps.pt_w;
+    const size_t m_w = ps.m_w, fft_w = ps.fft_w, ks_w = ps.ks_w, wd_w = ps.wd_w, total = ps.total;
+    const bool diag = ps.diag;
     void *w;
     CK_TRY(ctx_scratch(ctx, total * 8, &w));
     uint64_t *xrot = (uint64_t *)w;
