@@ -263,6 +263,30 @@ def bench_tile(torch, np, steps, warmup, calib_mib):
                             "GBps": v[2] / (v[0] * 1e-3) / 1e9} for k, v in prof.items()}}
 
 
+def bench_shapes(torch, np, steps):
+    """The other projection shapes of a Llama-3-8B block (QKV, attention output, down), same ring and level."""
+    from workloads import PROJ_DOWN, PROJ_QKV, PROJ_WO
+    res = {}
+    for cfg in (PROJ_QKV, PROJ_WO, PROJ_DOWN):
+        st = setup_projection(torch, np, cfg)
+        ctx = st["ctx"]
+        outs = ctx.linear_project(st["cts"], st["Wd"], st["T"], st["n1"], st["keys"])
+        with Timer(torch) as t:
+            for _ in range(steps):
+                outs = ctx.linear_project(st["cts"], st["Wd"], st["T"], st["n1"], st["keys"], outs)
+        n_out = cfg.d_out // st["D"]
+        err = check_projection(np, st, outs, blocks=(0, n_out - 1))
+        D, n1 = st["D"], cfg.n1
+        n2 = -(-D // n1)
+        res[cfg.name] = {"workload": "%dx%d, n1=%d n2=%d, %d rotations" % (
+                             cfg.d_in, cfg.d_out, n1, n2, (cfg.d_in // D) * (n1 - 1) + n_out * (n2 - 1)),
+                         "s_per_projection": t.ms / steps / 1e3, "decrypt_max_abs_err": err}
+        log("shape %s: %.1f ms" % (cfg.name, t.ms / steps))
+        del st, outs, ctx
+        torch.cuda.empty_cache()
+    return res
+
+
 def cpu_baseline(np, cfg, budget_s=20.0):
     """The oracle on a bounded sample of the projection, extrapolated to one full projection."""
     from oracle import Ckks, gen_primes
@@ -311,7 +335,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-secondary", action="store_true")
-    ap.add_argument("--only", choices=["keyswitch", "ntt", "tile"], default=None,
+    ap.add_argument("--only", choices=["keyswitch", "ntt", "tile", "shapes"], default=None,
                     help="run only this secondary workload (for profiling); prints its JSON")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also run one plain device copy of this many MiB (for hardware-counter calibration)")
@@ -330,6 +354,9 @@ def main():
         return
     if args.only == "ntt":
         print(json.dumps(bench_ntt(torch, args.steps)), flush=True)
+        return
+    if args.only == "shapes":
+        print(json.dumps(bench_shapes(torch, np, args.steps)), flush=True)
         return
     if args.only == "tile":
         print(json.dumps(bench_tile(torch, np, args.steps, args.warmup, args.calib_copy_mib)), flush=True)
@@ -373,6 +400,8 @@ def main():
         log("ntt microbench")
         secondary["ntt"] = bench_ntt(torch, max(args.steps, 5))
         torch.cuda.empty_cache()
+        log("other projection shapes")
+        secondary["shapes"] = bench_shapes(torch, np, 1)
     cpu = None
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle sample)")

@@ -274,12 +274,19 @@ __device__ __forceinline__ void fwd8_stage(double (&x)[kE8], const double *tws, 
 __device__ __forceinline__ uint32_t pad_ac(uint32_t u) { return u ^ (((u >> 5) & 7u) << 2); }
 __device__ __forceinline__ uint32_t pad_cb(uint32_t u) { return u + (u >> 3); }
 
+struct NoHook {
+    __device__ void operator()() const {}
+};
+
 // all eight forward stages of the sub-transform held by thread t (layout A in,
 // layout B out), reducing X at the stages set in RMASK; tr: this sub-transform's
-// kTr8 doubles of LDS; every thread of the block must call it (block barriers)
-template <unsigned RMASK>
+// kTr8 doubles of LDS; every thread of the block must call it (block barriers).
+// hook() runs right after the first barrier: every thread has then finished the
+// previous call's reads of the twiddle table, so a hook may refill a second
+// table for the next call (three more barriers follow before this call returns).
+template <unsigned RMASK, typename Hook = NoHook>
 __device__ __forceinline__ void fwd8_256(double (&x)[kE8], const double *tws, double *tr, uint32_t t,
-                                         const Ar<true> &ar, uint32_t Bm = 1)
+                                         const Ar<true> &ar, uint32_t Bm = 1, Hook hook = Hook())
 {
     fwd8_stage<0, 0, (RMASK >> 0) & 1>(x, tws, t, ar, Bm);
     fwd8_stage<0, 1, (RMASK >> 1) & 1>(x, tws, t, ar, Bm);
@@ -287,6 +294,7 @@ __device__ __forceinline__ void fwd8_256(double (&x)[kE8], const double *tws, do
 #pragma unroll
     for (int k = 0; k < kE8; k++) tr[pad_ac(u8<0>(t, k))] = x[k];
     __syncthreads();
+    hook();
 #pragma unroll
     for (int k = 0; k < kE8; k++) x[k] = tr[pad_ac(u8<1>(t, k))];
     __syncthreads();

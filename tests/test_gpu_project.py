@@ -17,6 +17,9 @@
   (one input ciphertext, two output ciphertexts), bit for bit, and decrypted
   within 2^-18 of X @ W.
 
+* the down-projection parameters (n1 = 8, n2 = 32: 7 baby and 31 giant rotations) on a
+  512 x 256 slice (two input ciphertexts, one output), bit for bit.
+
 Every compared output is also decrypted and decoded on both sides: the GPU's
 slots agree with the oracle's within 2^-20 of the scale.
 """
@@ -27,7 +30,7 @@ import pytest
 
 from gpu_common import require_gpu, say, to_dev, to_host
 from oracle import Ckks
-from workloads import (PROJECTION, TOY, gaussian_error, gaussian_weights, rng, ternary_secret,
+from workloads import (PROJ_DOWN, PROJECTION, TOY, gaussian_error, gaussian_weights, rng, ternary_secret,
                        uniform_residues, uniform_slots)
 
 pytestmark = pytest.mark.gpu
@@ -138,4 +141,11 @@ def test_projection_parameters_full_degree_slice():
     say("slice max error vs X@W", err)
     # fresh noise ~2^-29, one hoisted rotation ~2^-20.5 at most over 32768 slots, 38 rotated terms summed and
     # one rescale: the oracle measures 2^-22.4 on this slice, the bound leaves a factor of 2^4
+    assert err <= 2.0 ** -18
+
+
+def test_down_projection_parameters_full_degree_slice():
+    say("down-projection slice (n1 = 8)")
+    err = run_case(PROJ_DOWN, 512, 256, [0])
+    say("down slice max error vs X@W", err)
     assert err <= 2.0 ** -18

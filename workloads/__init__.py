@@ -91,3 +91,12 @@ KEYSWITCH = Config("keyswitch", 3, 16, 50, 24, 8, 3, scale_log2=40, level=23, ba
 # Llama-3-8B-shaped projection: 4096 -> 14336 at level 12, 128 tokens x 256 features per ciphertext.
 PROJECTION = Config("projection", 4, 16, 50, 24, 8, 3, scale_log2=40, level=12, tokens=128,
                     d_in=4096, d_out=14336, n1=32)
+# The other projection shapes of a Llama-3-8B block, same ring and level: QKV (4096 -> 4096 + 2 x 1024),
+# attention output (4096 -> 4096) and down (14336 -> 4096; 56 inputs, so n1 = 8, n2 = 32: 392 baby + 496 giant
+# rotations).
+PROJ_QKV = Config("proj_qkv", 5, 16, 50, 24, 8, 3, scale_log2=40, level=12, tokens=128,
+                  d_in=4096, d_out=6144, n1=32)
+PROJ_WO = Config("proj_wo", 6, 16, 50, 24, 8, 3, scale_log2=40, level=12, tokens=128,
+                 d_in=4096, d_out=4096, n1=32)
+PROJ_DOWN = Config("proj_down", 7, 16, 50, 24, 8, 3, scale_log2=40, level=12, tokens=128,
+                   d_in=14336, d_out=4096, n1=8)
