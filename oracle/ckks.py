@@ -283,6 +283,24 @@ class Ckks:
         idx = list(range(n_limbs))
         return self.ntt(self.reduce_int(self.encode_int(zr, zi, delta), idx), idx)
 
+    def encode_periodic(self, u, delta: float, n_limbs: int) -> np.ndarray:
+        """Plaintext (NTT domain, limbs q_0..q_{n_limbs-1}) of the slot vector z[t*D + f] = u[f], period D = len(u).
+
+        A slot vector of period D (a power of two) is fixed by the automorphisms X -> X^a, a = 1 mod 4D, so
+        its encoding is a polynomial in X^(N/2D): m(X) = m'(X^(N/2D)) with m' the encoding of the D values u
+        in the ring of degree 2D (the same fp64 evaluation and rounding rule as encode, run at degree 2D).
+        Zero coefficients stay exactly zero, so the plaintext's NTT values are constant over runs of N/2D
+        consecutive (bit-reversed) indices."""
+        u = np.ascontiguousarray(u, dtype=np.float64)
+        D = u.shape[0]
+        assert D >= 1 and D & (D - 1) == 0 and 2 * D <= self.n
+        mp = np.empty(2 * D, dtype=np.int64)
+        lib().or_encode_round(u, None, 2 * D, float(delta), mp)
+        m = np.zeros(self.n, dtype=np.int64)
+        m[::self.n // (2 * D)] = mp
+        idx = list(range(n_limbs))
+        return self.ntt(self.reduce_int(m, idx), idx)
+
     def lift_centered(self, rows: np.ndarray, idx: Sequence[int]) -> List[int]:
         """Coefficient residues -> the centred integer in (-Q/2, Q/2] by CRT (Python big ints)."""
         mods = [self.primes[k] for k in idx]
@@ -482,6 +500,61 @@ class Ckks:
         o = (f - n1 * g) % D
         vals = W[i * D + (o + k) % D, j * D + o]
         return np.repeat(vals, T)
+
+    @staticmethod
+    def periodic_diag_vectors(W: np.ndarray, D: int, j: int, i: int, n1: int, g: int, b: int):
+        """One period (D values) of the two plaintexts of (j, i, g, b) in the token-major layout s = t*D + f.
+
+        With A = W^T, A_{j,i} = W[iD:(i+1)D, jD:(j+1)D]^T and k = n1 g + b, the diagonal D_k(A)[o] =
+        A[o, (o + k) mod D] splits by whether o + k wraps past D: U_k keeps the entries with o + k < D, V_k
+        the others.  A left rotation by k of a token-major ciphertext moves feature o + k of the same token to
+        feature o only when o + k < D; the wrapped entries need the rotation by k - D instead, so
+            y = sum_k U_k * rho^k(x) + V_k * rho^(k-D)(x).
+        The giant step rho^(n1 g) is factored out as in the feature-major case, which rotates both vectors
+        right by n1 g: returned are U[o] = U_k[(o - n1 g) mod D] and V[o] = V_k[(o - n1 g) mod D]."""
+        k = n1 * g + b
+        o = (np.arange(D) - n1 * g) % D
+        wraps = o + k >= D
+        vals = W[i * D + (o + k) % D, j * D + o]
+        return np.where(wraps, 0.0, vals), np.where(wraps, vals, 0.0)
+
+    def linear_project_tm(self, cts: Sequence[np.ndarray], W: np.ndarray, T: int, n1: int,
+                          keys: Dict[int, np.ndarray], out_blocks: Optional[Sequence[int]] = None):
+        """The projection in the token-major layout s = t*D + f (input i holds features [iD, (i+1)D) of every
+        token):
+            out_j = Rescale( sum_g Rot_{n1 g}( sum_{i,b} U_{j,i,g,b} * Rot_b(x_i) + V_{j,i,g,b} * Rot_{b-D}(x_i) ) )
+        with U, V from periodic_diag_vectors, encoded with encode_periodic at scale q_level.  Keys: steps
+        b (0 < b < n1), b - D (0 <= b < n1) and n1 g (0 < g < n2)."""
+        level = self.level_of(cts[0])
+        D = (self.n // 2) // T
+        d_in, d_out = W.shape
+        n_in, n_out = d_in // D, d_out // D
+        n2 = -(-D // n1)
+        delta_w = float(self.q[level])
+        xr, xw = [], []
+        for i in range(n_in):
+            steps = [b for b in range(1, n1)] + [b - D for b in range(n1)]
+            rots = self.rotate_hoisted(cts[i], steps, [keys[s] for s in steps])
+            xr.append([cts[i]] + rots[:n1 - 1])
+            xw.append(rots[n1 - 1:])
+        outs = []
+        for j in (range(n_out) if out_blocks is None else out_blocks):
+            total = None
+            for g in range(n2):
+                acc = None
+                for i in range(n_in):
+                    for b in range(n1):
+                        if n1 * g + b >= D:
+                            continue
+                        uu, vv = self.periodic_diag_vectors(W, D, j, i, n1, g, b)
+                        for vec, x in ((uu, xr[i][b]), (vv, xw[i][b])):
+                            term = self.ct_mul_plain(x, self.encode_periodic(vec, delta_w, level + 1))
+                            acc = term if acc is None else self.ct_add(acc, term)
+                if g > 0:
+                    acc = self.rotate(acc, n1 * g, keys[n1 * g])
+                total = acc if total is None else self.ct_add(total, acc)
+            outs.append(self.rescale(total))
+        return outs
 
     def linear_project(self, cts: Sequence[np.ndarray], W: np.ndarray, T: int, n1: int,
                        keys: Dict[int, np.ndarray], out_blocks: Optional[Sequence[int]] = None):
