@@ -87,6 +87,77 @@ def setup_projection(torch, np, cfg):
     return dict(ctx=ctx, s=s, X=X, W=W, Wd=Wd, cts=cts, keys=keys, T=T, D=D, n1=n1, delta=delta)
 
 
+def tm_pack(X, T, D, i):
+    return X[:, i * D:(i + 1) * D].reshape(-1)
+
+
+def setup_projection_tm(torch, np, cfg, n1):
+    """Inputs and keys of the token-major projection (slot t*D + f): steps b, b - D (0 <= b < n1) and n1 g."""
+    from paper_2609_12378_amd import Context
+    from workloads import (gaussian_error, gaussian_weights, rng, ternary_secret, uniform_residues,
+                           uniform_slots)
+    ctx = Context(cfg.log_n, cfg.n_q, cfg.n_p, cfg.dnum, q_bits=cfg.q_bits)
+    n, T, level = ctx.n, cfg.tokens, cfg.level
+    D = (n // 2) // T
+    n2 = -(-D // n1)
+    s = torch.from_numpy(ternary_secret(rng(cfg.index, 3), n)).cuda()
+    X = uniform_slots(rng(cfg.index, 1), (T, cfg.d_in))
+    W = gaussian_weights(rng(cfg.index, 2), (cfg.d_in, cfg.d_out))
+    Wd = torch.from_numpy(W).cuda()
+    delta = float(2 ** cfg.scale_log2)
+    ge = rng(cfg.index, 4)
+    cts = []
+    for i in range(cfg.d_in // D):
+        pt = ctx.encode(torch.from_numpy(tm_pack(X, T, D, i)).cuda(), None, delta, level + 1)
+        a = torch.from_numpy(uniform_residues(ge, ctx.q[:level + 1], n)).cuda()
+        e = torch.from_numpy(gaussian_error(ge, n)).cuda()
+        cts.append(ctx.encrypt(s, pt, a, e))
+    steps = [b for b in range(1, n1)] + [b - D for b in range(n1)] + [n1 * g for g in range(1, n2)]
+    gk = rng(cfg.index, 5)
+    keys = {}
+    for st in steps:
+        a = torch.from_numpy(uniform_residues(gk, ctx.primes, n, lead=(cfg.dnum,))).cuda()
+        e = torch.from_numpy(gaussian_error(gk, (cfg.dnum, n))).cuda()
+        keys[st] = ctx.keygen_galois(s, ctx.galois_elt(st), a, e)
+    torch.cuda.synchronize()
+    return dict(ctx=ctx, s=s, X=X, W=W, Wd=Wd, cts=cts, keys=keys, T=T, D=D, n1=n1, delta=delta)
+
+
+def bench_tm(torch, np, steps, warmup, n1s=(16, 32)):
+    """The 4096x14336 projection in the token-major layout (periodic weight plaintexts), per baby-step size."""
+    from workloads import PROJECTION as cfg
+    res = {}
+    for n1 in n1s:
+        st = setup_projection_tm(torch, np, cfg, n1)
+        ctx = st["ctx"]
+        outs = None
+        for _ in range(warmup):
+            outs = ctx.linear_project(st["cts"], st["Wd"], st["T"], n1, st["keys"], outs, layout="tm")
+        ctx.profile(True)
+        ctx.profile_reset()
+        with Timer(torch) as t:
+            for _ in range(steps):
+                outs = ctx.linear_project(st["cts"], st["Wd"], st["T"], n1, st["keys"], outs, layout="tm")
+        prof = ctx.profile_all()
+        ctx.profile(False)
+        T, D = st["T"], st["D"]
+        errs = []
+        for j in (0, 27, 55):
+            re, _ = ctx.decode(ctx.decrypt(st["s"], outs[j]))
+            want = tm_pack(st["X"] @ st["W"][:, j * D:(j + 1) * D], T, D, 0)
+            errs.append(float(np.max(np.abs(re.cpu().numpy() - want))))
+        n2 = -(-D // n1)
+        res["n1=%d" % n1] = {
+            "workload": "4096x14336 token-major (slot t*256 + f), N=2^16, level 12, n1=%d n2=%d, %d rotations"
+                        % (n1, n2, 16 * (2 * n1 - 1) + 56 * (n2 - 1)),
+            "s_per_projection": t.ms / steps / 1e3, "decrypt_max_abs_err": max(errs),
+            "kernels_ms": {k: round(v[0] / steps, 3) for k, v in sorted(prof.items(), key=lambda kv: -kv[1][0])}}
+        log("token-major n1=%d: %.1f ms" % (n1, t.ms / steps))
+        del st, outs, ctx
+        torch.cuda.empty_cache()
+    return res
+
+
 def check_projection(np, st, outs, blocks=(0, 27, 55)):
     """Decrypt sampled outputs and compare with X @ W (property check at full size)."""
     ctx, T, D = st["ctx"], st["T"], st["D"]
@@ -335,7 +406,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-secondary", action="store_true")
-    ap.add_argument("--only", choices=["keyswitch", "ntt", "tile", "shapes"], default=None,
+    ap.add_argument("--only", choices=["keyswitch", "ntt", "tile", "shapes", "tm"], default=None,
                     help="run only this secondary workload (for profiling); prints its JSON")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also run one plain device copy of this many MiB (for hardware-counter calibration)")
@@ -354,6 +425,9 @@ def main():
         return
     if args.only == "ntt":
         print(json.dumps(bench_ntt(torch, args.steps)), flush=True)
+        return
+    if args.only == "tm":
+        print(json.dumps(bench_tm(torch, np, args.steps, args.warmup)), flush=True)
         return
     if args.only == "shapes":
         print(json.dumps(bench_shapes(torch, np, args.steps)), flush=True)
@@ -402,6 +476,9 @@ def main():
         torch.cuda.empty_cache()
         log("other projection shapes")
         secondary["shapes"] = bench_shapes(torch, np, 1)
+        torch.cuda.empty_cache()
+        log("token-major projection")
+        secondary["projection_tm"] = bench_tm(torch, np, 1, 1, n1s=(32,))["n1=32"]
     cpu = None
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle sample)")

@@ -132,7 +132,8 @@ typedef enum {
     CKKS_OP_MUL_RELIN = 8,      /* shape[0] = limbs */
     CKKS_OP_MODUP = 9,          /* shape[0] = level */
     CKKS_OP_MODDOWN = 10,       /* shape[0] = level */
-    CKKS_OP_LINEAR_PROJECT = 11 /* shape = {limbs of the inputs, tokens, d_in, d_out, n1} */
+    CKKS_OP_LINEAR_PROJECT = 11, /* shape = {limbs of the inputs, tokens, d_in, d_out, n1} */
+    CKKS_OP_LINEAR_PROJECT_TM = 12 /* the same shape */
 } ckks_op;
 size_t ckks_workspace_bytes(const ckks_ctx *ctx, int op, const uint32_t *shape);
 ckks_status ckks_set_workspace(ckks_ctx *ctx, void *dev, size_t bytes);
@@ -241,6 +242,28 @@ typedef struct {
 ckks_status ckks_linear_project(ckks_ctx *ctx, const ckks_buf *in, const double *dev_W, const ckks_proj_shape *shape,
                                 const int32_t *key_steps, const uint64_t *const *dev_keys, uint32_t n_keys,
                                 ckks_buf *out);
+
+/* The same projection in the token-major layout: slot t*D + f of input
+ * ciphertext i holds X[t, i*D + f] (D = N/2/tokens features, a power of two
+ * in [4, 256]); output j holds Y[t, j*D + o] at slot t*D + o.  A left
+ * rotation by k then moves feature o + k of the same token to feature o only
+ * while o + k < D, so each cyclic diagonal is split into the entries that do
+ * not wrap (U, multiplying Rot_b(x_i)) and those that do (V, multiplying
+ * Rot_{b-D}(x_i)):
+ *   out_j = Rescale( sum_g Rot_{n1 g}( sum_{i,b<n1} U_{j,i,g,b} * Rot_b(x_i)
+ *                                              + V_{j,i,g,b} * Rot_{b-D}(x_i) ) )
+ * with U_{j,i,g,b}[t*D + o] = A_{j,i}[o', o' + k] if o' + k < D (else 0) and
+ * V_{j,i,g,b}[t*D + o] = A_{j,i}[o', o' + k - D] if o' + k >= D (else 0),
+ * k = n1 g + b, o' = (o - n1 g) mod D.  Every weight plaintext is periodic
+ * in the slots (period D), so it is encoded as m'(X^(N/2D)) with m' the
+ * encoding of one period at ring degree 2D (the encode's own rounding rule).
+ * Keys: steps b (0 < b < n1), b - D (0 <= b < n1) and n1 g (0 < g < n2).
+ * Needs every prime below 2^50.  Arguments, scales and errors as for
+ * ckks_linear_project; scratch: ckks_workspace_bytes with
+ * CKKS_OP_LINEAR_PROJECT_TM. */
+ckks_status ckks_linear_project_tm(ckks_ctx *ctx, const ckks_buf *in, const double *dev_W,
+                                   const ckks_proj_shape *shape, const int32_t *key_steps,
+                                   const uint64_t *const *dev_keys, uint32_t n_keys, ckks_buf *out);
 
 /* ---- measurement helpers ------------------------------------------------- */
 

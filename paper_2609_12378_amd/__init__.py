@@ -76,6 +76,7 @@ _SIGS = {
     "ckks_moddown": (ctypes.c_int, [_VP, _VP, _U32, _VP]),
     "ckks_automorph": (ctypes.c_int, [_VP, _VP, _U32, _U32, _VP]),
     "ckks_linear_project": (ctypes.c_int, [_VP, _BP, _VP, ctypes.POINTER(_ProjShape), _VP, _VP, _U32, _BP]),
+    "ckks_linear_project_tm": (ctypes.c_int, [_VP, _BP, _VP, ctypes.POINTER(_ProjShape), _VP, _VP, _U32, _BP]),
     "ckks_profile_enable": (ctypes.c_int, [_VP, ctypes.c_int]),
     "ckks_profile_read": (ctypes.c_int, [_VP, ctypes.c_char_p, ctypes.POINTER(_DBL), ctypes.POINTER(_U64),
                                          ctypes.POINTER(_DBL), ctypes.POINTER(_DBL)]),
@@ -200,7 +201,7 @@ class Context:
 
     # workspace op codes (ckks_op)
     OP_ENCODE, OP_DECODE, OP_ENCRYPT, OP_DECRYPT, OP_KEYGEN, OP_RESCALE, OP_ROTATE, OP_MUL_RELIN, OP_MODUP, \
-        OP_MODDOWN, OP_LINEAR_PROJECT = range(1, 12)
+        OP_MODDOWN, OP_LINEAR_PROJECT, OP_LINEAR_PROJECT_TM = range(1, 13)
 
     def workspace_bytes(self, op: int, shape=()) -> int:
         """Device bytes one call of `op` takes from the arena or workspace, for the given shape."""
@@ -345,7 +346,9 @@ class Context:
         return out
 
     def linear_project(self, cts: Sequence[Buf], W: torch.Tensor, tokens: int, n1: int,
-                       keys: Dict[int, torch.Tensor], outs: Optional[Sequence[Buf]] = None) -> List[Buf]:
+                       keys: Dict[int, torch.Tensor], outs: Optional[Sequence[Buf]] = None,
+                       layout: str = "fm") -> List[Buf]:
+        """Y = X W on packed ciphertexts; layout "fm" (slot f*tokens + t) or "tm" (slot t*D + f)."""
         d_in, d_out = W.shape
         D = (self.n // 2) // tokens
         n_out = d_out // D
@@ -358,8 +361,10 @@ class Context:
         ks = (ctypes.c_int32 * len(steps))(*steps)
         kp = (ctypes.c_void_p * len(steps))(*[keys[s].data_ptr() for s in steps])
         shape = _ProjShape(tokens, d_in, d_out, n1)
-        _check(self.lib.ckks_linear_project(self.h, inb, _ptr(W), ctypes.byref(shape), ks, kp, len(steps), ob),
-               "ckks_linear_project")
+        if layout not in ("fm", "tm"):
+            raise ValueError("layout must be 'fm' or 'tm'")
+        fn = "ckks_linear_project" if layout == "fm" else "ckks_linear_project_tm"
+        _check(getattr(self.lib, fn)(self.h, inb, _ptr(W), ctypes.byref(shape), ks, kp, len(steps), ob), fn)
         for o, b in zip(outs, ob):
             o.scale = b.scale
         return list(outs)

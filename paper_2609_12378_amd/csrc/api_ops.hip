@@ -62,6 +62,9 @@ size_t op_workspace_bytes(const ckks_ctx *ctx, int op, const uint32_t *shape)
     case CKKS_OP_LINEAR_PROJECT:
         if (!shape) return SIZE_MAX;
         return proj_workspace_bytes(ctx, shape[0], shape[1], shape[2], shape[3], shape[4]);
+    case CKKS_OP_LINEAR_PROJECT_TM:
+        if (!shape) return SIZE_MAX;
+        return proj_tm_workspace_bytes(ctx, shape[0], shape[1], shape[2], shape[3], shape[4]);
     default: return SIZE_MAX;
     }
 }
@@ -142,7 +145,6 @@ ckks_status ckks_encode(ckks_ctx *ctx, const double *re, const double *im, doubl
                "encode: limbs %u (buffer %u) outside [1, %u]", n_limbs, pt->n_limbs, ctx->n_q);
     CK_REQUIRE(scale > 0 && std::isfinite(scale), CKKS_EINVAL, "encode: scale must be positive");
     void *w;
-    const size_t N = ctx->n;
     CK_TRY(ctx_scratch(ctx, op_workspace_bytes(ctx, CKKS_OP_ENCODE, nullptr), &w));
     double2 *work = (double2 *)w;
     int64_t *m = (int64_t *)((char *)w + enc_work_bytes(ctx, 1));
@@ -380,7 +382,7 @@ ckks_status ckks_moddown(ckks_ctx *ctx, const uint64_t *x, uint32_t level, uint6
     CK_REQUIRE(ctx && x && out, CKKS_EINVAL, "moddown: null argument");
     CK_REQUIRE(level < ctx->n_q, CKKS_ELEVEL, "moddown: level %u >= n_q", level);
     CK_REQUIRE(ctx->n_p > 0, CKKS_EUNSUPPORTED, "moddown: the context has no special primes");
-    const uint32_t ext = level + 1 + ctx->n_p, L = level + 1;
+    const uint32_t ext = level + 1 + ctx->n_p;
     const size_t N = ctx->n;
     void *w;
     CK_TRY(ctx_scratch(ctx, op_workspace_bytes(ctx, CKKS_OP_MODDOWN, &level), &w));

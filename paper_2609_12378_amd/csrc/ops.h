@@ -84,6 +84,25 @@ ckks_status enc_to_rns(ckks_ctx *ctx, const int64_t *m, uint32_t batch, uint32_t
 size_t enc_work_bytes(const ckks_ctx *ctx, uint32_t batch);
 size_t proj_workspace_bytes(const ckks_ctx *ctx, uint32_t L, uint32_t tokens, uint32_t d_in, uint32_t d_out,
                             uint32_t n1);
+size_t proj_tm_workspace_bytes(const ckks_ctx *ctx, uint32_t L, uint32_t tokens, uint32_t d_in, uint32_t d_out,
+                               uint32_t n1);
+
+// projection helpers (project.hip): W's cyclic diagonals Wd[((jb * n_in + i) * D + k) * D + o] =
+// W[(i D + (k + o) mod D) * d_out + jb D + o]; canonical residues -> the same integers as doubles, in place
+ckks_status launch_diag_layout(ckks_ctx *ctx, double *Wd, const double *W, uint32_t D, uint32_t n_in,
+                               uint32_t d_out);
+ckks_status launch_to_f64(ckks_ctx *ctx, uint64_t *v, size_t words);
+
+// ciphertext-level steps shared by the API calls and the projections (api_ops.hip)
+// rotations of one ciphertext sharing a single ModUp; work: ks_scratch_words(level, ks_rot_batch(count))
+ckks_status rotate_core(ckks_ctx *ctx, const uint64_t *c, uint32_t level, const int32_t *steps,
+                        const uint64_t *const *keys, uint32_t count, uint64_t *const *outs, uint64_t *work);
+// rescale of one ciphertext at level l; work: (2 + 2 l) N words
+ckks_status rescale_core(ckks_ctx *ctx, const uint64_t *c, uint32_t l, uint64_t *out, uint64_t *work);
+// `count` ciphertexts (at cs + r * stride) rotated by the same step; work: ks_scratch_words(level,
+// ks_rot_batch(count), count)
+ckks_status rotate_many(ckks_ctx *ctx, const uint64_t *cs, size_t stride, uint32_t count, uint32_t level,
+                        int32_t steps, const uint64_t *key, uint64_t *const *outs, uint64_t *work);
 // decode: coef = coefficient form of limbs 0..min(limbs,2)-1 ([limbs][N]); writes N/2 slots
 ckks_status dec_slots(ckks_ctx *ctx, const uint64_t *coef, uint32_t limbs, double scale, double2 *work, double *re,
                       double *im);

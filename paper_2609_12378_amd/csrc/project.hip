@@ -28,12 +28,6 @@
 #include "ntt_core.h"
 #include "ops.h"
 
-ckks_status rotate_core(ckks_ctx *ctx, const uint64_t *c, uint32_t level, const int32_t *steps,
-                        const uint64_t *const *keys, uint32_t count, uint64_t *const *outs, uint64_t *work);
-ckks_status rescale_core(ckks_ctx *ctx, const uint64_t *c, uint32_t l, uint64_t *out, uint64_t *work);
-ckks_status rotate_many(ckks_ctx *ctx, const uint64_t *cs, size_t stride, uint32_t count, uint32_t level,
-                        int32_t steps, const uint64_t *key, uint64_t *const *outs, uint64_t *work);
-
 namespace {
 
 constexpr int kThreads = 256;
@@ -384,6 +378,28 @@ ProjScratch proj_scratch(const ckks_ctx *ctx, uint32_t L, uint32_t D, uint32_t d
 
 }  // namespace
 
+ckks_status launch_diag_layout(ckks_ctx *ctx, double *Wd, const double *W, uint32_t D, uint32_t n_in,
+                               uint32_t d_out)
+{
+    const size_t tot_e = (size_t)n_in * D * d_out;
+    prof_begin(ctx, K_ELEM, 16.0 * tot_e);
+    hipLaunchKernelGGL(k_diag_layout, dim3((unsigned)((tot_e + kThreads - 1) / kThreads)), dim3(kThreads), 0,
+                       ctx->stream, Wd, W, D, n_in, d_out, tot_e);
+    prof_end(ctx, K_ELEM);
+    HIP_TRY(hipGetLastError());
+    return CKKS_OK;
+}
+
+ckks_status launch_to_f64(ckks_ctx *ctx, uint64_t *v, size_t words)
+{
+    prof_begin(ctx, K_ELEM, 16.0 * words);
+    hipLaunchKernelGGL(k_to_f64, dim3((unsigned)((words + kThreads - 1) / kThreads)), dim3(kThreads), 0, ctx->stream,
+                       v, words);
+    prof_end(ctx, K_ELEM);
+    HIP_TRY(hipGetLastError());
+    return CKKS_OK;
+}
+
 size_t proj_workspace_bytes(const ckks_ctx *ctx, uint32_t L, uint32_t tokens, uint32_t d_in, uint32_t d_out,
                             uint32_t n1)
 {
@@ -461,12 +477,7 @@ extern "C" ckks_status ckks_linear_project(ckks_ctx *ctx, const ckks_buf *in, co
     double *Wd = (double *)(ksw + ks_w);
     uint32_t *fop = (uint32_t *)(ksw + ks_w + wd_w);
     if (diag) {
-        const size_t tot_e = wd_w;
-        prof_begin(ctx, K_ELEM, 16.0 * tot_e);
-        hipLaunchKernelGGL(k_diag_layout, dim3((unsigned)((tot_e + kThreads - 1) / kThreads)), dim3(kThreads), 0,
-                           ctx->stream, Wd, W, D, n_in, shape->d_out, tot_e);
-        prof_end(ctx, K_ELEM);
-        HIP_TRY(hipGetLastError());
+        CK_TRY(launch_diag_layout(ctx, Wd, W, D, n_in, shape->d_out));
         CK_TRY(enc_feat_of_pos(ctx, T, fop));
     }
 
@@ -484,13 +495,7 @@ extern "C" ckks_status ckks_linear_project(ckks_ctx *ctx, const ckks_buf *in, co
     int s1, s2;
     ntt_split(ctx->log_n, &s1, &s2);
     const bool fused = s1 > 0 && ntt_uses_f64(ctx, L);
-    if (fused) {
-        prof_begin(ctx, K_ELEM, 16.0 * xrot_w);
-        hipLaunchKernelGGL(k_to_f64, dim3((unsigned)((xrot_w + kThreads - 1) / kThreads)), dim3(kThreads), 0,
-                           ctx->stream, xrot, xrot_w);
-        prof_end(ctx, K_ELEM);
-        HIP_TRY(hipGetLastError());
-    }
+    if (fused) CK_TRY(launch_to_f64(ctx, xrot, xrot_w));
 
     // ---- 2./3. tiles of output blocks
     const double delta_w = (double)ctx->primes[level];

@@ -1,0 +1,402 @@
+// The packed projection Y = X W in the token-major layout s = t*D + f: input ciphertext i holds features
+// [iD, (i+1)D) of all T = N/2D tokens, output j features [jD, (j+1)D).
+//
+// A left rotation by k moves feature o + k of a token to feature o only while o + k < D; the entries of the
+// cyclic diagonal D_k(A_{j,i})[o] = A[o, (o + k) mod D] (A = W^T) that wrap past D need the rotation by k - D
+// instead.  Splitting each diagonal into U_k (no wrap) and V_k (wrap) and factoring out the giant steps as in
+// the feature-major case (Section "Matrix Representations and Linear Computation in CKKS", Eq.
+// slot-diagonal-matvec, with baby-step/giant-step reuse):
+//   out_j = Rescale( sum_g Rot_{n1 g}( sum_{i,b} U_{j,i,g,b} * Rot_b(x_i) + V_{j,i,g,b} * Rot_{b-D}(x_i) ) ),
+// U / V the vectors U_k / V_k (k = n1 g + b) shifted right by n1 g, the same for every token.
+//
+// Why this layout is cheap to encode: a slot vector of period D (a power of two) is fixed by X -> X^a for
+// every a = 1 mod 4D, so its encoding is m'(X^T) with m' the encoding of one period in the ring of degree 2D,
+// and its NTT value at (bit-reversed) index x is Q[x >> log2 T], Q the 2D-point negacyclic NTT of m' with
+// psi^T, whose twiddles psi^(T brev_9(e)) = psi^(brev_16(e)) are the first 2D entries of the ring's table.
+// A weight plaintext therefore costs one D-point FFT and one 2D-point NTT per limb instead of an N-point
+// encode, and in the multiply-accumulate every run of T consecutive ciphertext values meets one scalar.
+//
+// The D-point FFT is the encode's own evaluation (radix-2 decimation in time from bit-reversed input,
+// butterfly t = w a[hi], complex products without fused multiply-add) at M' = D: its twiddles and twist
+// factors are the ring's tables at stride T (the angles 2 pi e T / (D T) and pi k T / (2 D T) differ from
+// 2 pi e / D and pi k / 2D by exact powers of two), and the scale is Delta * (2 / 2D), so the rounded
+// coefficients are the ones the degree-2D encode gives.
+#pragma clang fp contract(off)
+#include <vector>
+
+#include "ckks_internal.h"
+#include "ntt_core.h"
+#include "ops.h"
+
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kPE = 8;        // plaintexts per encode block: 8 consecutive doubles per table row (64 B)
+constexpr int kMaxD = 256;    // features per ciphertext handled by the encode kernel
+constexpr int kJT = 32;       // output ciphertexts per multiply-accumulate tile
+
+__device__ __forceinline__ double2 cmul(double2 a, double2 b)
+{
+    const double p1 = a.x * b.x, p2 = a.y * b.y, p3 = a.x * b.y, p4 = a.y * b.x;
+    return make_double2(p1 - p2, p3 + p4);
+}
+
+struct TmArgs {
+    const double *Wd;   // W's cyclic diagonals [jb][i][k][o]
+    uint32_t D, logD, n_in, n1g, bcount;
+    uint32_t j0, jc;    // first output of the tile, outputs in the tile
+    uint32_t pb0, P;    // first (input, baby step) pair of the sub-batch, pairs in it
+    uint32_t npt;       // plaintexts in the sub-batch: P * 2 * jc, index (p * 2 + uv) * jc + jj
+};
+
+// Encode kPE periodic weight plaintexts per block and transform them: Q[l][x][pt] (x < 2D) holds the
+// canonical residue of plaintext pt's NTT values x*T .. x*T + T - 1 modulo q_l, as a double.
+__global__ __launch_bounds__(kThreads) void k_enc_periodic(TmArgs a, const double2 *__restrict__ fft_w,
+                                                           const double2 *__restrict__ twist, uint32_t T,
+                                                           double c, uint32_t L, const ModQ *__restrict__ mods,
+                                                           const double *__restrict__ twf, uint32_t log_n,
+                                                           double *Q)
+{
+    __shared__ double2 buf[kPE * kMaxD];        // FFT, then the transform's working rows (kPE x 2D doubles)
+    __shared__ int64_t mq[kPE * 2 * kMaxD];     // rounded coefficients m'
+    __shared__ double tws[2 * kMaxD];
+    const uint32_t D = a.D, logD = a.logD, D2 = 2 * D;
+    const uint32_t pt0 = blockIdx.x * kPE;
+    // 1. one period of each plaintext's slot vector, at its bit-reversed FFT position
+    for (uint32_t e = threadIdx.x; e < kPE * D; e += kThreads) {
+        const uint32_t p = e / D, j = e % D, pt = pt0 + p;
+        double v = 0.0;
+        if (pt < a.npt) {
+            const uint32_t jj = pt % a.jc, uv = (pt / a.jc) & 1, pr = a.pb0 + pt / (2 * a.jc);
+            const uint32_t i = pr / a.bcount, b = pr % a.bcount, k = a.n1g + b;
+            const uint32_t o = (j + D - a.n1g % D) % D;   // feature before the giant-step shift
+            const bool wraps = o + k >= D;
+            if (wraps == (uv == 1))
+                v = a.Wd[(((size_t)(a.j0 + jj) * a.n_in + i) * D + k) * D + o];
+        }
+        // slot j sits at FFT position brev((5^j mod 4D - 1) / 4)
+        uint32_t e5 = 1, base = 5, ex = j;
+        while (ex) {
+            if (ex & 1) e5 = (e5 * base) & (4 * D - 1);
+            base = (base * base) & (4 * D - 1);
+            ex >>= 1;
+        }
+        const uint32_t s = (e5 - 1) >> 2;
+        const uint32_t pos = logD ? __brev(s) >> (32 - logD) : 0;
+        buf[p * D + pos] = make_double2(v, 0.0);
+    }
+    __syncthreads();
+    // 2. radix-2 stages len = 2 .. D
+    for (uint32_t len = 2; len <= D; len <<= 1) {
+        const uint32_t half = len >> 1, step = D / len;
+        for (uint32_t e = threadIdx.x; e < kPE * (D / 2); e += kThreads) {
+            const uint32_t p = e / (D / 2), bf = e % (D / 2);
+            const uint32_t blk = bf / half, k = bf % half;
+            double2 *row = buf + p * D + blk * len;
+            const double2 w = fft_w[(size_t)k * step * T];
+            const double2 t = cmul(w, row[k + half]);
+            const double2 lo = row[k];
+            row[k + half] = make_double2(lo.x - t.x, lo.y - t.y);
+            row[k] = make_double2(lo.x + t.x, lo.y + t.y);
+        }
+        __syncthreads();
+    }
+    // 3. twist, scale and round: m'[k] = round(c Re v_k), m'[k + D] = round(c Im v_k)
+    for (uint32_t e = threadIdx.x; e < kPE * D; e += kThreads) {
+        const uint32_t p = e / D, k = e % D;
+        const double2 v = cmul(twist[(size_t)k * T], buf[p * D + k]);
+        mq[p * D2 + k] = (int64_t)round(c * v.x);
+        mq[p * D2 + k + D] = (int64_t)round(c * v.y);
+    }
+    double *xs = (double *)buf;  // kPE rows of 2D doubles
+    // 4. per limb: the 2D-point negacyclic NTT (Cooley-Tukey, group i of stage m takes Psi[m + i])
+    for (uint32_t l = 0; l < L; l++) {
+        const ModQ md = mods[l];
+        const nttc::Ar<true> ar(md);
+        __syncthreads();
+        for (uint32_t e = threadIdx.x; e < D2; e += kThreads) tws[e] = twf[((size_t)l << log_n) + e];
+        for (uint32_t e = threadIdx.x; e < kPE * D2; e += kThreads) xs[e] = ar.from_i64(mq[e], md);
+        __syncthreads();
+        for (uint32_t m = 1, t = D; m < D2; m <<= 1, t >>= 1) {
+            for (uint32_t e = threadIdx.x; e < kPE * D; e += kThreads) {
+                const uint32_t p = e / D, bf = e % D;
+                const uint32_t g = bf / t, j = bf % t;
+                double *row = xs + p * D2 + 2 * g * t + j;
+                double x0 = row[0], x1 = row[t];
+                ar.ct(x0, x1, tws[m + g]);
+                row[0] = x0;
+                row[t] = x1;
+            }
+            __syncthreads();
+        }
+        // rows of Q: for each x, kPE consecutive plaintexts
+        for (uint32_t e = threadIdx.x; e < kPE * D2; e += kThreads) {
+            const uint32_t p = e % kPE, x = e / kPE, pt = pt0 + p;
+            if (pt < a.npt) Q[((size_t)l * D2 + x) * a.npt + pt] = (double)ar.to_canon(xs[p * D2 + x]);
+        }
+    }
+}
+
+// Multiply-accumulate of one sub-batch: block (limb l, 128 positions) holds, per thread (polynomial, position),
+// the tile's jc accumulators and runs over the sub-batch's pairs:
+//   acc_jj += Q_U[jj][pair] * xr[pair] + Q_V[jj][pair] * xw[pair]   (mod q_l),
+// the Q values of a position being those of its run x = pos >> log2 T.  With T >= 128 (UNIF) the block lies in
+// one run, so its Q values are the same for every lane and are read with scalar loads.  Products (|x| < q,
+// 0 <= Q < q) are below 0.875 q, and the sum is range-reduced after every pair (at most 0.5 q + 1.75 q): every
+// value is an exact integer below 2^53.  acc ([jc][2][L][N], canonical) is written, or added to when
+// `accumulate`.
+template <int JT, bool UNIF>
+__global__ __launch_bounds__(kThreads) void k_mac_tm(uint64_t *acc, const double *__restrict__ x2,
+                                                     const double *__restrict__ Q, TmArgs a, uint32_t n1, uint32_t L,
+                                                     uint32_t logT, uint32_t log_n, int accumulate,
+                                                     const ModQ *__restrict__ mods)
+{
+    const uint32_t blocks_per_limb = 1u << (log_n - 7);
+    const uint32_t l = blockIdx.x / blocks_per_limb, pb = blockIdx.x % blocks_per_limb;
+    const uint32_t poly = threadIdx.x >> 7, pos = (pb << 7) + (threadIdx.x & 127);
+    const nttc::Ar<true> ar(mods[l]);
+    const uint32_t x = UNIF ? (pb << 7) >> logT : pos >> logT, D2 = 2 * a.D;
+    const size_t n = (size_t)1 << log_n, ctw = 2 * (size_t)L * n;
+    const double *qrow = Q + ((size_t)l * D2 + x) * a.npt;
+    double s[JT];
+#pragma unroll
+    for (int jj = 0; jj < JT; jj++) s[jj] = 0.0;
+    const size_t off = ((size_t)poly * L + l) * n + pos;
+    for (uint32_t p = 0; p < a.P; p++) {
+        const uint32_t pr = a.pb0 + p, i = pr / a.bcount, b = pr % a.bcount;
+        const double *xp = x2 + (size_t)(i * n1 + b) * 2 * ctw + off;
+        const double xr = xp[0], xw = xp[ctw];
+        const double *qu = qrow + (size_t)p * 2 * a.jc, *qv = qu + a.jc;
+#pragma unroll
+        for (int jj = 0; jj < JT; jj++) {
+            if (jj < (int)a.jc) s[jj] = ar.red(s[jj] + ar.mul(xr, qu[jj]) + ar.mul(xw, qv[jj]));
+        }
+    }
+    const uint64_t q = mods[l].q;
+#pragma unroll
+    for (int jj = 0; jj < JT; jj++) {
+        if (jj < (int)a.jc) {
+            uint64_t *dst = acc + (size_t)jj * ctw + off;
+            uint64_t r = ar.to_canon(s[jj]);
+            if (accumulate) r = addmod(r, *dst, q);
+            *dst = r;
+        }
+    }
+}
+
+struct TmScratch {
+    uint32_t Jt, Pb;
+    size_t x2_w, acc_w, tot_w, rot_w, q_w, ks_w, wd_w, total;
+};
+
+TmScratch tm_scratch(const ckks_ctx *ctx, uint32_t L, uint32_t D, uint32_t d_in, uint32_t d_out, uint32_t n1)
+{
+    TmScratch ts{};
+    const uint32_t level = L - 1, n_in = d_in / D, n_out = d_out / D;
+    const size_t N = ctx->n, ctw = 2 * (size_t)L * N;
+    // output tiles of at most kJT, balanced
+    const uint32_t tiles = (n_out + kJT - 1) / kJT;
+    ts.Jt = (n_out + tiles - 1) / tiles;
+    // pairs per sub-batch: the tile's weight tables within 1 GiB
+    const size_t per_pair = (size_t)2 * ts.Jt * L * 2 * D * sizeof(double);
+    const uint32_t maxpairs = n_in * n1;
+    uint32_t Pb = (uint32_t)std::max<size_t>(1, ((size_t)1 << 30) / per_pair);
+    if (ctx->proj_max_pairs) Pb = std::min(Pb, ctx->proj_max_pairs);
+    ts.Pb = std::min(Pb, maxpairs);
+    ts.x2_w = (size_t)n_in * n1 * 2 * ctw;
+    ts.acc_w = ts.tot_w = ts.rot_w = (size_t)ts.Jt * ctw;
+    ts.q_w = (size_t)ts.Pb * 2 * ts.Jt * L * 2 * D;
+    ts.ks_w = std::max(ks_scratch_words(ctx, level, ks_rot_batch(2 * n1 - 1)),
+                       ks_scratch_words(ctx, level, ks_rot_batch(ts.Jt), ts.Jt));
+    ts.wd_w = (size_t)d_in * d_out;
+    ts.total = ts.x2_w + ts.acc_w + ts.tot_w + ts.rot_w + ts.q_w + ts.ks_w + ts.wd_w;
+    return ts;
+}
+
+ckks_status launch_mac_tm(ckks_ctx *ctx, uint64_t *acc, const double *x2, const double *Q, const TmArgs &a,
+                          uint32_t n1, uint32_t L, uint32_t logT, bool accumulate)
+{
+    const uint32_t blocks = L << (ctx->log_n - 7);
+    const double res = (double)a.jc * 2 * L * ctx->n;
+    // the pairs' two ciphertexts once, the accumulators once (read when accumulating) and written
+    prof_begin(ctx, K_MAC_TM, 8.0 * (double)a.P * 2 * 2 * L * ctx->n + 8.0 * res * (accumulate ? 2 : 1),
+               res * a.P * 2 * 8.0);
+    const bool unif = logT >= 7;
+#define CK_MAC_TM(J, U)                                                                                          \
+    hipLaunchKernelGGL((k_mac_tm<J, U>), dim3(blocks), dim3(kThreads), 0, ctx->stream, acc, x2, Q, a, n1, L, logT, \
+                       ctx->log_n, (int)accumulate, ctx->d_mod)
+    if (a.jc <= 8) {
+        if (unif) CK_MAC_TM(8, true); else CK_MAC_TM(8, false);
+    } else if (a.jc <= 16) {
+        if (unif) CK_MAC_TM(16, true); else CK_MAC_TM(16, false);
+    } else {
+        if (unif) CK_MAC_TM(kJT, true); else CK_MAC_TM(kJT, false);
+    }
+#undef CK_MAC_TM
+    prof_end(ctx, K_MAC_TM);
+    HIP_TRY(hipGetLastError());
+    return CKKS_OK;
+}
+
+ckks_status launch_enc_periodic(ckks_ctx *ctx, const TmArgs &a, double delta, uint32_t L, double *Q)
+{
+    const uint32_t T = (uint32_t)(ctx->n / (2 * a.D));
+    const double c = delta * (2.0 / (double)(2 * a.D));
+    const double pts = (double)a.npt;
+    // W's diagonals in, the tables out; FFT and transforms (D/2 log D + L D log 2D butterflies per plaintext)
+    prof_begin(ctx, K_ENC_TM, 8.0 * pts * a.D + 8.0 * pts * L * 2 * a.D,
+               pts * (a.D / 2.0 * a.logD * 10.0 + L * (double)a.D * (a.logD + 1) * kOpsButterflyF64));
+    hipLaunchKernelGGL(k_enc_periodic, dim3((a.npt + kPE - 1) / kPE), dim3(kThreads), 0, ctx->stream, a,
+                       (const double2 *)ctx->d_fft_w, (const double2 *)ctx->d_fft_twist, T, c, L, ctx->d_mod,
+                       ctx->d_twf, ctx->log_n, Q);
+    prof_end(ctx, K_ENC_TM);
+    HIP_TRY(hipGetLastError());
+    return CKKS_OK;
+}
+
+ckks_status tm_check_shape(const ckks_ctx *ctx, uint32_t L, uint32_t T, uint32_t d_in, uint32_t d_out, uint32_t n1,
+                           uint32_t *Dout)
+{
+    const uint32_t slots = ctx->n / 2;
+    CK_REQUIRE(T >= 1 && slots % T == 0, CKKS_EINVAL, "linear_project_tm: %u tokens do not divide %u slots", T,
+               slots);
+    const uint32_t D = slots / T;
+    CK_REQUIRE(D >= 4 && D <= (uint32_t)kMaxD && (D & (D - 1)) == 0 && T >= 2, CKKS_EUNSUPPORTED,
+               "linear_project_tm: %u features per ciphertext (a power of two in [4, %d], at least 2 tokens)", D,
+               kMaxD);
+    CK_REQUIRE(d_in > 0 && d_out > 0 && d_in % D == 0 && d_out % D == 0, CKKS_EINVAL,
+               "linear_project_tm: d_in %u and d_out %u must be positive multiples of %u", d_in, d_out, D);
+    CK_REQUIRE(n1 >= 1 && n1 <= D, CKKS_EINVAL, "linear_project_tm: n1 %u outside [1, %u]", n1, D);
+    CK_REQUIRE(L >= 2 && L <= ctx->n_q, CKKS_ELEVEL, "linear_project_tm: inputs need 2..%u limbs", ctx->n_q);
+    CK_REQUIRE(ntt_uses_f64(ctx, L), CKKS_EUNSUPPORTED, "linear_project_tm: needs primes below 2^50");
+    CK_REQUIRE(ctx->log_n >= 8, CKKS_EUNSUPPORTED, "linear_project_tm: needs N >= 256");
+    *Dout = D;
+    return CKKS_OK;
+}
+
+}  // namespace
+
+size_t proj_tm_workspace_bytes(const ckks_ctx *ctx, uint32_t L, uint32_t tokens, uint32_t d_in, uint32_t d_out,
+                               uint32_t n1)
+{
+    uint32_t D;
+    if (tm_check_shape(ctx, L, tokens, d_in, d_out, n1, &D) != CKKS_OK) {
+        clear_error();
+        return SIZE_MAX;
+    }
+    return tm_scratch(ctx, L, D, d_in, d_out, n1).total * 8;
+}
+
+extern "C" ckks_status ckks_linear_project_tm(ckks_ctx *ctx, const ckks_buf *in, const double *W,
+                                              const ckks_proj_shape *shape, const int32_t *key_steps,
+                                              const uint64_t *const *keys, uint32_t n_keys, ckks_buf *out)
+{
+    clear_error();
+    CK_REQUIRE(ctx && in && W && shape && out, CKKS_EINVAL, "linear_project_tm: null argument");
+    CK_REQUIRE(ctx->n_p > 0, CKKS_EUNSUPPORTED, "linear_project_tm: the context has no special primes");
+    const uint32_t T = shape->tokens, n1 = shape->n1;
+    const uint32_t L = in[0].n_limbs, level = L - 1;
+    uint32_t D;
+    CK_TRY(tm_check_shape(ctx, L, T, shape->d_in, shape->d_out, n1, &D));
+    const uint32_t n_in = shape->d_in / D, n_out = shape->d_out / D, n2 = (D + n1 - 1) / n1;
+    for (uint32_t i = 0; i < n_in; i++) {
+        CK_REQUIRE(in[i].data && in[i].n_polys == 2, CKKS_EINVAL, "linear_project_tm: input %u is not a ciphertext",
+                   i);
+        CK_REQUIRE(in[i].n_limbs == L, CKKS_ELEVEL, "linear_project_tm: input %u has %u limbs, expected %u", i,
+                   in[i].n_limbs, L);
+        CK_REQUIRE(in[i].scale == in[0].scale, CKKS_ESCALE, "linear_project_tm: input scales differ");
+    }
+    for (uint32_t j = 0; j < n_out; j++)
+        CK_REQUIRE(out[j].data && out[j].n_polys == 2 && out[j].n_limbs == level, CKKS_EINVAL,
+                   "linear_project_tm: output %u must be a ciphertext with %u limbs", j, level);
+    auto find_key = [&](int32_t st) -> const uint64_t * {
+        for (uint32_t r = 0; r < n_keys; r++)
+            if (key_steps[r] == st) return keys[r];
+        return nullptr;
+    };
+    // baby steps b (0 < b < n1) then the wrapped ones b - D (0 <= b < n1), all hoisted from one ModUp
+    std::vector<int32_t> bsteps;
+    std::vector<const uint64_t *> bkeys;
+    for (uint32_t b = 1; b < n1; b++) bsteps.push_back((int32_t)b);
+    for (uint32_t b = 0; b < n1; b++) bsteps.push_back((int32_t)b - (int32_t)D);
+    for (int32_t st : bsteps) {
+        const uint64_t *k = find_key(st);
+        CK_REQUIRE(k, CKKS_ENOKEY, "linear_project_tm: no key for step %d", st);
+        bkeys.push_back(k);
+    }
+    std::vector<const uint64_t *> gkeys(n2, nullptr);
+    for (uint32_t g = 1; g < n2; g++) {
+        gkeys[g] = find_key((int32_t)(n1 * g));
+        CK_REQUIRE(gkeys[g], CKKS_ENOKEY, "linear_project_tm: no key for giant step %u", n1 * g);
+    }
+
+    const size_t N = ctx->n, ctw = 2 * (size_t)L * N;
+    const TmScratch ts = tm_scratch(ctx, L, D, shape->d_in, shape->d_out, n1);
+    void *w;
+    CK_TRY(ctx_scratch(ctx, ts.total * 8, &w));
+    uint64_t *x2 = (uint64_t *)w;  // [n_in][n1][xr, xw][2][L][N]
+    uint64_t *acc = x2 + ts.x2_w;
+    uint64_t *tot = acc + ts.acc_w;
+    uint64_t *rot = tot + ts.tot_w;
+    double *Q = (double *)(rot + ts.rot_w);
+    uint64_t *ksw = (uint64_t *)(Q + ts.q_w);
+    double *Wd = (double *)(ksw + ts.ks_w);
+    CK_TRY(launch_diag_layout(ctx, Wd, W, D, n_in, shape->d_out));
+
+    // 1. Rot_b(x_i) and Rot_{b-D}(x_i), hoisted per input
+    for (uint32_t i = 0; i < n_in; i++) {
+        uint64_t *xi = x2 + (size_t)i * n1 * 2 * ctw;
+        HIP_TRY(hipMemcpyAsync(xi, in[i].data, ctw * 8, hipMemcpyDeviceToDevice, ctx->stream));
+        std::vector<uint64_t *> outs;
+        for (uint32_t b = 1; b < n1; b++) outs.push_back(xi + (size_t)b * 2 * ctw);
+        for (uint32_t b = 0; b < n1; b++) outs.push_back(xi + ((size_t)b * 2 + 1) * ctw);
+        CK_TRY(rotate_core(ctx, in[i].data, level, bsteps.data(), bkeys.data(), (uint32_t)bsteps.size(),
+                           outs.data(), ksw));
+    }
+    CK_TRY(launch_to_f64(ctx, x2, ts.x2_w));
+
+    // 2./3. tiles of output ciphertexts, giant steps, sub-batches of pairs
+    const double delta_w = (double)ctx->primes[level];
+    uint32_t logT = 0;
+    while ((1u << logT) < T) logT++;
+    uint32_t logD = 0;
+    while ((1u << logD) < D) logD++;
+    for (uint32_t j0 = 0; j0 < n_out; j0 += ts.Jt) {
+        const uint32_t jc = std::min(ts.Jt, n_out - j0);
+        for (uint32_t g = 0; g < n2; g++) {
+            const uint32_t bcount = std::min(n1, D - n1 * g);
+            const uint32_t pairs = n_in * bcount;
+            const uint32_t nsub = (pairs + ts.Pb - 1) / ts.Pb;
+            for (uint32_t sb = 0, pb0 = 0; sb < nsub; sb++) {
+                TmArgs a{};
+                a.Wd = Wd;
+                a.D = D;
+                a.logD = logD;
+                a.n_in = n_in;
+                a.n1g = n1 * g;
+                a.bcount = bcount;
+                a.j0 = j0;
+                a.jc = jc;
+                a.pb0 = pb0;
+                a.P = pairs / nsub + (sb < pairs % nsub ? 1 : 0);
+                a.npt = a.P * 2 * jc;
+                CK_TRY(launch_enc_periodic(ctx, a, delta_w, L, Q));
+                CK_TRY(launch_mac_tm(ctx, acc, (const double *)x2, Q, a, n1, L, logT, pb0 > 0));
+                pb0 += a.P;
+            }
+            if (g == 0) {
+                HIP_TRY(hipMemcpyAsync(tot, acc, jc * ctw * 8, hipMemcpyDeviceToDevice, ctx->stream));
+            } else {
+                std::vector<uint64_t *> outs(jc);
+                for (uint32_t jj = 0; jj < jc; jj++) outs[jj] = rot + (size_t)jj * ctw;
+                CK_TRY(rotate_many(ctx, acc, ctw, jc, level, (int32_t)(n1 * g), gkeys[g], outs.data(), ksw));
+                CK_TRY(launch_binary(ctx, tot, tot, rot, jc * 2 * L, limb_range(0, L), EW_ADD));
+            }
+        }
+        for (uint32_t jj = 0; jj < jc; jj++) {
+            CK_TRY(rescale_core(ctx, tot + (size_t)jj * ctw, level, out[j0 + jj].data, rot));
+            out[j0 + jj].scale = in[0].scale;
+        }
+    }
+    return CKKS_OK;
+}

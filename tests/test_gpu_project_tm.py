@@ -1,0 +1,111 @@
+"""GPU parity of the token-major (periodic) projection against the oracle.
+
+Every output ciphertext compared is identical bit for bit to the oracle's, its
+decrypted slots agree with the oracle's within 2^-20 of the scale, and with X @ W
+within the stated bound:
+
+* toy ring (N = 2^12, 16 tokens x 128 features), n1 = 16, two inputs and three
+  outputs, at most five (input, baby step) pairs per launch so the sums are
+  carried across launches;
+* toy ring with the plain diagonal split (n1 = 128, no giant step);
+* a ring of degree 2^10 with 4 tokens (runs of four equal plaintext values, so one
+  multiply-accumulate block meets many of them);
+* the projection parameters at full degree (N = 2^16, 24 + 8 limbs, level 12, 128
+  tokens x 256 features, n1 = 32: 31 + 32 baby and 7 giant rotations) on a
+  256 x 512 slice.
+"""
+import dataclasses
+
+import numpy as np
+import pytest
+
+from gpu_common import require_gpu, say, to_dev, to_host
+from oracle import Ckks
+from workloads import (PROJECTION, TOY, gaussian_error, gaussian_weights, rng, ternary_secret,
+                       uniform_residues, uniform_slots)
+
+pytestmark = pytest.mark.gpu
+
+
+def tm_pack(X, T, D, i):
+    return X[:, i * D:(i + 1) * D].reshape(-1)
+
+
+def run_case(cfg, d_in, d_out, n1, oracle_outputs, max_pairs=0):
+    require_gpu()
+    from paper_2609_12378_amd import Context
+    ctx = Context(cfg.log_n, cfg.n_q, cfg.n_p, cfg.dnum, q_bits=cfg.q_bits)
+    ctx.set_proj_batch(max_pairs)
+    ck = Ckks(cfg.log_n, ctx.q, ctx.p, cfg.dnum)
+    n, T, level = ctx.n, cfg.tokens, cfg.level
+    D = (n // 2) // T
+    n2 = -(-D // n1)
+    s = ternary_secret(rng(cfg.index, 3, extra=40), n)
+    X = uniform_slots(rng(cfg.index, 1, extra=40), (T, d_in))
+    W = gaussian_weights(rng(cfg.index, 2, extra=40), (d_in, d_out))
+    delta = float(2 ** cfg.scale_log2)
+    ge = rng(cfg.index, 4, extra=40)
+    s_dev = to_dev(s)
+    cts_o, cts_g = [], []
+    for i in range(d_in // D):
+        x = tm_pack(X, T, D, i)
+        a = uniform_residues(ge, ctx.q[:level + 1], n)
+        e = gaussian_error(ge, n)
+        cts_o.append(ck.encrypt(s, ck.encode(x, None, delta, level + 1), a, e))
+        cts_g.append(ctx.encrypt(s_dev, ctx.encode(to_dev(x), None, delta, level + 1), to_dev(a), to_dev(e)))
+    steps = [b for b in range(1, n1)] + [b - D for b in range(n1)] + [n1 * g for g in range(1, n2)]
+    gk = rng(cfg.index, 5, extra=40)
+    keys_o, keys_g = {}, {}
+    for st in steps:
+        a = uniform_residues(gk, ctx.primes, n, lead=(cfg.dnum,))
+        e = gaussian_error(gk, (cfg.dnum, n))
+        g = ck.galois_elt(st)
+        keys_o[st] = ck.keygen_galois(s, g, a, e)
+        keys_g[st] = ctx.keygen_galois(s_dev, g, to_dev(a), to_dev(e))
+    say("keys ready", len(steps))
+    outs = ctx.linear_project(cts_g, to_dev(W), T, n1, keys_g, layout="tm")
+    say("gpu projection done")
+    want = ck.linear_project_tm(cts_o, W, T, n1, keys_o, out_blocks=oracle_outputs)
+    say("oracle projection done")
+    for j, wo in zip(oracle_outputs, want):
+        got = to_host(outs[j].data)
+        assert got.shape == wo.shape
+        bad = np.argwhere(got != wo)
+        assert bad.size == 0, "output %d: first mismatches %s" % (j, bad[:5].tolist())
+        assert outs[j].scale == delta
+        re, im = ctx.decode(ctx.decrypt(s_dev, outs[j]))
+        zo = ck.decode(ck.decrypt(s, wo), delta)
+        assert np.max(np.abs(to_host(re) - zo.real)) <= 2.0 ** -20
+        assert np.max(np.abs(to_host(im) - zo.imag)) <= 2.0 ** -20
+    Y = X @ W
+    errs = []
+    for j, o in enumerate(outs):
+        re, _ = ctx.decode(ctx.decrypt(s_dev, o))
+        errs.append(np.max(np.abs(to_host(re) - tm_pack(Y, T, D, j))))
+    return max(errs)
+
+
+def test_toy_tm_projection_carried_sums():
+    err = run_case(TOY, 2 * TOY.feats, 3 * TOY.feats, 16, [0, 2], max_pairs=5)
+    say("toy tm max error vs X@W", err)
+    assert err <= 2.0 ** -12
+
+
+def test_toy_tm_projection_plain_diagonals():
+    err = run_case(TOY, TOY.feats, TOY.feats, TOY.feats, [0])
+    say("toy tm (n1 = D) max error vs X@W", err)
+    assert err <= 2.0 ** -12
+
+
+def test_small_ring_tm_projection_short_runs():
+    cfg = dataclasses.replace(TOY, name="ring10", log_n=10, tokens=4)
+    err = run_case(cfg, 256, 384, 16, [0, 2])
+    say("N=2^10 tm max error vs X@W", err)
+    assert err <= 2.0 ** -12
+
+
+def test_tm_projection_parameters_full_degree_slice():
+    say("full-degree tm slice")
+    err = run_case(PROJECTION, 256, 512, 32, [0, 1])
+    say("tm slice max error vs X@W", err)
+    assert err <= 2.0 ** -18
