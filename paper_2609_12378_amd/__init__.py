@@ -355,8 +355,12 @@ class Context:
         level = cts[0].level
         if outs is None:
             outs = [Buf(self.zeros(2, level), cts[0].scale) for _ in range(n_out)]
+        # the library reads d_in/D input and d_out/D output descriptors: never hand it shorter arrays
+        if D > 0 and d_in % D == 0 and d_out % D == 0 and (len(cts) < d_in // D or len(outs) < n_out):
+            raise ValueError("linear_project: %d inputs and %d outputs given, the shape needs %d and %d"
+                             % (len(cts), len(outs), d_in // D, n_out))
         inb = (_Buf * len(cts))(*[c.c() for c in cts])
-        ob = (_Buf * n_out)(*[o.c() for o in outs])
+        ob = (_Buf * max(1, len(outs)))(*[o.c() for o in outs])
         steps = sorted(keys)
         ks = (ctypes.c_int32 * len(steps))(*steps)
         kp = (ctypes.c_void_p * len(steps))(*[keys[s].data_ptr() for s in steps])

@@ -109,3 +109,58 @@ def test_tm_projection_parameters_full_degree_slice():
     err = run_case(PROJECTION, 256, 512, 32, [0, 1])
     say("tm slice max error vs X@W", err)
     assert err <= 2.0 ** -18
+
+
+def test_tm_projection_rejects_bad_shapes_and_missing_keys():
+    """Host-side validation fails before any launch; the output buffers keep their contents."""
+    require_gpu()
+    from paper_2609_12378_amd import Buf, CkksError, Context
+    cfg = TOY
+    ctx = Context(cfg.log_n, cfg.n_q, cfg.n_p, cfg.dnum, q_bits=cfg.q_bits)
+    n, L = ctx.n, cfg.level + 1
+    ct = Buf(ctx.zeros(2, L), 2.0 ** 30)
+    W = to_dev(np.zeros((128, 128)))
+    key = ctx.keygen_galois(to_dev(ternary_secret(rng(1, 3), n)), ctx.galois_elt(1),
+                            to_dev(uniform_residues(rng(1, 5), ctx.primes, n, lead=(cfg.dnum,))),
+                            to_dev(gaussian_error(rng(1, 5), (cfg.dnum, n))))
+    out = Buf(ctx.zeros(2, L - 1), 1.0)
+    # 3 tokens do not divide the 2048 slots
+    with pytest.raises(CkksError, match="tokens"):
+        ctx.linear_project([ct], W, 3, 4, {1: key}, outs=[out], layout="tm")
+    # 4 tokens give 512 features per ciphertext, above the periodic encode's limit
+    with pytest.raises(CkksError, match="features"):
+        ctx.linear_project([ct], to_dev(np.zeros((512, 512))), 4, 4, {1: key}, outs=[out], layout="tm")
+    # n1 = 2 needs the steps 1, -128, -127 and the giant steps 2g
+    with pytest.raises(CkksError, match="no key"):
+        ctx.linear_project([ct], W, 16, 2, {1: key}, outs=[out], layout="tm")
+    assert not to_host(out.data).any()
+    assert ctx.workspace_bytes(ctx.OP_LINEAR_PROJECT_TM, (L, 16, 128, 128, 2)) > 0
+    with pytest.raises(CkksError):
+        ctx.workspace_bytes(ctx.OP_LINEAR_PROJECT_TM, (L, 4, 512, 512, 2))
+
+
+def test_tm_projection_with_exact_workspace():
+    require_gpu()
+    import torch
+    from paper_2609_12378_amd import Context
+    cfg = TOY
+    ctx = Context(cfg.log_n, cfg.n_q, cfg.n_p, cfg.dnum, q_bits=cfg.q_bits)
+    n, T, L, n1 = ctx.n, cfg.tokens, cfg.level + 1, 16
+    D = (n // 2) // T
+    s = to_dev(ternary_secret(rng(1, 3, extra=41), n))
+    X = uniform_slots(rng(1, 1, extra=41), (T, 2 * D))
+    W = to_dev(gaussian_weights(rng(1, 2, extra=41), (2 * D, D)))
+    ge = rng(1, 4, extra=41)
+    cts = [ctx.encrypt(s, ctx.encode(to_dev(tm_pack(X, T, D, i)), None, 2.0 ** 30, L),
+                       to_dev(uniform_residues(ge, ctx.q[:L], n)), to_dev(gaussian_error(ge, n))) for i in range(2)]
+    gk = rng(1, 5, extra=41)
+    keys = {}
+    for st in [b for b in range(1, n1)] + [b - D for b in range(n1)] + [n1 * g for g in range(1, D // n1)]:
+        keys[st] = ctx.keygen_galois(s, ctx.galois_elt(st), to_dev(uniform_residues(gk, ctx.primes, n, lead=(2,))),
+                                     to_dev(gaussian_error(gk, (2, n))))
+    want = to_host(ctx.linear_project(cts, W, T, n1, keys, layout="tm")[0].data)
+    nbytes = ctx.workspace_bytes(ctx.OP_LINEAR_PROJECT_TM, (L, T, 2 * D, D, n1))
+    ctx.set_workspace(torch.empty(nbytes // 8, dtype=torch.uint64, device="cuda"))
+    got = to_host(ctx.linear_project(cts, W, T, n1, keys, layout="tm")[0].data)
+    ctx.set_workspace(None)
+    assert np.array_equal(got, want)
