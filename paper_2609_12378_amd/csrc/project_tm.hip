@@ -184,9 +184,145 @@ __global__ __launch_bounds__(kThreads) void k_mac_tm(uint64_t *acc, const double
     }
 }
 
+// ---- the multiply-accumulate on the matrix cores ----------------------------------------------------------
+//
+// Per (limb l, run x) the sub-batch's sum is a dense product: acc[jj][c] = sum_kappa Q[jj][kappa] X[kappa][c]
+// (kappa = 2 pair + uv over the sub-batch, c a position of the run in one polynomial), over residues below
+// 2^50.  Each residue is written in seven balanced base-256 digits (v = sum_a d_a 256^a, d_a in [-128, 127]),
+// so that with C_s = sum_{a + b = s} sum_kappa Qd_a Xd_b (13 groups, each a sum of int8 x int8 products that
+// v_mfma_i32_16x16x64_i8 accumulates exactly in int32 while K <= 4096: |C_s| < 7 * 4096 * 2^14 < 2^31)
+//   sum_kappa Q X = sum_s 256^s C_s   (an integer identity, reduced mod q_l in the epilogue).
+// The ciphertext digits are laid out once per projection as Xd[digit][l][poly N + pos][kappa] (kappa
+// contiguous, 16 bytes per MFMA lane); the plaintext digits of a 64-kappa block are formed in LDS from Q.
+// Operand layouts (checked on the hardware): A 16x64, lane i holds row i % 16, bytes k = 16 (i / 16) + 0..15;
+// B 64x16, lane i holds column i % 16, the same k; C 16x16, lane i holds column i % 16, rows 4 (i / 16) + r.
+typedef int v4i __attribute__((ext_vector_type(4)));
+constexpr int kDig = 7, kGroups = 2 * kDig - 1, kKB = 64;
+
+__device__ __forceinline__ void digits7(uint64_t v, int8_t *d, size_t stride)
+{
+#pragma unroll
+    for (int a = 0; a < kDig; a++) {
+        int t = (int)(v & 255u);
+        v >>= 8;
+        if (t >= 128) {
+            t -= 256;
+            v += 1;
+        }
+        d[(size_t)a * stride] = (int8_t)t;
+    }
+}
+
+// x2 ([n_in][n1][xr, xw][2][L][N] canonical) -> Xd[a][l][poly N + pos][kappa], kappa = 2 (i n1 + b) + uv < kt
+// (rows padded to kt_pad bytes with zeros).  Block: (l, 64 columns, 64 kappa), staged through LDS.
+__global__ __launch_bounds__(kThreads) void k_xdigits(const uint64_t *__restrict__ x2, int8_t *Xd, uint32_t L,
+                                                      uint32_t log_n, uint32_t kt, uint32_t kt_pad)
+{
+    __shared__ uint64_t tile[64][65];
+    const uint32_t cols = 2u << log_n, cblocks = cols / 64, kblocks = kt_pad / 64;
+    const uint32_t kb = blockIdx.x % kblocks, rest = blockIdx.x / kblocks;
+    const uint32_t cb = rest % cblocks, l = rest / cblocks;
+    const size_t n = (size_t)1 << log_n, ctw = 2 * (size_t)L * n;
+    const uint32_t c0 = cb * 64, k0 = kb * 64;
+    for (uint32_t e = threadIdx.x; e < 64 * 64; e += kThreads) {
+        const uint32_t kk = e / 64, cc = e % 64, kappa = k0 + kk, c = c0 + cc;
+        uint64_t v = 0;
+        if (kappa < kt) {
+            const uint32_t poly = c >> log_n, pos = c & ((1u << log_n) - 1);
+            v = x2[(size_t)kappa * ctw + ((size_t)poly * L + l) * n + pos];
+        }
+        tile[kk][cc] = v;
+    }
+    __syncthreads();
+    const size_t plane = (size_t)L * cols * kt_pad;
+    for (uint32_t e = threadIdx.x; e < 64 * 64; e += kThreads) {
+        const uint32_t cc = e / 64, kk = e % 64;
+        digits7(tile[kk][cc], Xd + ((size_t)l * cols + c0 + cc) * kt_pad + k0 + kk, plane);
+    }
+}
+
+// Block (limb l, run x, polynomial): T / 16 waves, wave w holds positions x T + 16 w .. + 15 of the polynomial
+// and the tile's jc <= 32 outputs (two 16-row MFMA tiles).  Q ([L][2D][npt], npt = K jc, kappa-major) gives the
+// plaintext digits of each 64-kappa block (rows jj >= jc and kappa >= K are zero); Xd the ciphertext digits from
+// kappa_base on (16-byte aligned, rows padded so a block never reads past them).
+template <int NW>
+__global__ __launch_bounds__(64 * NW) void k_mac_tm_mfma(uint64_t *acc, const int8_t *__restrict__ Xd,
+                                                           const double *__restrict__ Q, uint32_t jc, uint32_t K,
+                                                           uint32_t kappa_base, uint32_t kt_pad, uint32_t D2,
+                                                           uint32_t L, uint32_t logT, uint32_t log_n,
+                                                           int accumulate, const ModQ *__restrict__ mods)
+{
+    __shared__ __attribute__((aligned(16))) int8_t A[kDig][32][kKB];
+    const uint32_t runs = D2, poly = blockIdx.x & 1, x = (blockIdx.x >> 1) % runs, l = (blockIdx.x >> 1) / runs;
+    const uint32_t lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const uint32_t pos = (x << logT) + 16 * w + (lane & 15);
+    const size_t n = (size_t)1 << log_n, cols = 2 * n;
+    const size_t plane = (size_t)L * cols * kt_pad;
+    const int8_t *xb = Xd + ((size_t)l * cols + (size_t)poly * n + (x << logT) + 16 * w + (lane & 15)) * kt_pad +
+                       kappa_base + 16 * (lane >> 4);
+    const double *qx = Q + ((size_t)l * D2 + x) * (size_t)K * jc;
+    v4i c[2][kGroups];
+#pragma unroll
+    for (int m = 0; m < 2; m++)
+#pragma unroll
+        for (int g = 0; g < kGroups; g++) c[m][g] = v4i{0, 0, 0, 0};
+    for (uint32_t k0 = 0; k0 < K; k0 += kKB) {
+        __syncthreads();
+        for (uint32_t e = threadIdx.x; e < 32 * kKB; e += 64 * NW) {
+            const uint32_t kk = e / 32, jj = e % 32, kappa = k0 + kk;
+            uint64_t v = 0;
+            if (jj < jc && kappa < K) v = (uint64_t)qx[(size_t)kappa * jc + jj];
+            digits7(v, &A[0][jj][kk], 32 * kKB);
+        }
+        __syncthreads();
+        v4i b[kDig];
+#pragma unroll
+        for (int d = 0; d < kDig; d++) b[d] = *(const v4i *)(xb + (size_t)d * plane + k0);
+#pragma unroll
+        for (int m = 0; m < 2; m++) {
+#pragma unroll
+            for (int a = 0; a < kDig; a++) {
+                const v4i av = *(const v4i *)&A[a][16 * m + (lane & 15)][16 * (lane >> 4)];
+#pragma unroll
+                for (int d = 0; d < kDig; d++)
+                    c[m][a + d] = __builtin_amdgcn_mfma_i32_16x16x64_i8(av, b[d], c[m][a + d], 0, 0, 0);
+            }
+        }
+    }
+    // epilogue: sum_s 256^s C_s mod q_l, canonical, added to the stored sums when accumulating
+    const ModQ md = mods[l];
+    const nttc::Ar<true> ar(md);
+    double w256[kGroups];
+    w256[0] = 1.0;
+#pragma unroll
+    for (int g = 1; g < kGroups; g++) w256[g] = (double)ar.to_canon(ar.mul(w256[g - 1], 256.0));
+    const size_t ctw = 2 * (size_t)L * n;
+#pragma unroll
+    for (int m = 0; m < 2; m++) {
+#pragma unroll
+        for (int r = 0; r < 4; r++) {
+            const uint32_t jj = 16 * m + 4 * (lane >> 4) + r;
+            double sum = 0.0;
+#pragma unroll
+            for (int g = 0; g < kGroups; g++) {
+                sum += ar.mul((double)c[m][g][r], w256[g]);
+                if ((g & 3) == 3) sum = ar.red(sum);
+            }
+            if (jj < jc) {
+                uint64_t *dst = acc + (size_t)jj * ctw + ((size_t)poly * L + l) * n + pos;
+                uint64_t v = ar.to_canon(sum);
+                if (accumulate) v = addmod(v, *dst, md.q);
+                *dst = v;
+            }
+        }
+    }
+}
+
 struct TmScratch {
     uint32_t Jt, Pb;
-    size_t x2_w, acc_w, tot_w, rot_w, q_w, ks_w, wd_w, total;
+    bool mfma;             // the multiply-accumulate runs on the matrix cores
+    uint32_t kt, kt_pad;   // kappa count (2 n_in n1) and the padded digit-row length in bytes
+    size_t x2_w, acc_w, tot_w, rot_w, q_w, ks_w, wd_w, xd_w, total;
 };
 
 TmScratch tm_scratch(const ckks_ctx *ctx, uint32_t L, uint32_t D, uint32_t d_in, uint32_t d_out, uint32_t n1)
@@ -194,23 +330,78 @@ TmScratch tm_scratch(const ckks_ctx *ctx, uint32_t L, uint32_t D, uint32_t d_in,
     TmScratch ts{};
     const uint32_t level = L - 1, n_in = d_in / D, n_out = d_out / D;
     const size_t N = ctx->n, ctw = 2 * (size_t)L * N;
+    const uint32_t T = (uint32_t)(N / (2 * D));
     // output tiles of at most kJT, balanced
     const uint32_t tiles = (n_out + kJT - 1) / kJT;
     ts.Jt = (n_out + tiles - 1) / tiles;
-    // pairs per sub-batch: the tile's weight tables within 1 GiB
+    // pairs per sub-batch: the tile's weight tables within 2 GiB, a multiple of 8 (16-byte aligned digit rows),
+    // at most 2048 (int32 digit sums stay exact)
     const size_t per_pair = (size_t)2 * ts.Jt * L * 2 * D * sizeof(double);
     const uint32_t maxpairs = n_in * n1;
-    uint32_t Pb = (uint32_t)std::max<size_t>(1, ((size_t)1 << 30) / per_pair);
-    if (ctx->proj_max_pairs) Pb = std::min(Pb, ctx->proj_max_pairs);
+    uint32_t Pb = (uint32_t)std::min<size_t>(2048, std::max<size_t>(8, ((size_t)1 << 31) / per_pair));
+    if (ctx->proj_max_pairs) Pb = std::min(Pb, std::max<uint32_t>(8, ctx->proj_max_pairs));
+    Pb &= ~7u;
     ts.Pb = std::min(Pb, maxpairs);
+    // the matrix-core path needs runs of 16..128 positions (a 16-column tile inside one run, one block per run)
+    // and every giant step over the same n1 baby steps (D a multiple of n1)
+    ts.mfma = T >= 16 && T <= 128 && D % n1 == 0;
+    ts.kt = 2 * n_in * n1;
+    ts.kt_pad = ((ts.kt + 63) & ~63u) + 64;
     ts.x2_w = (size_t)n_in * n1 * 2 * ctw;
     ts.acc_w = ts.tot_w = ts.rot_w = (size_t)ts.Jt * ctw;
     ts.q_w = (size_t)ts.Pb * 2 * ts.Jt * L * 2 * D;
     ts.ks_w = std::max(ks_scratch_words(ctx, level, ks_rot_batch(2 * n1 - 1)),
                        ks_scratch_words(ctx, level, ks_rot_batch(ts.Jt), ts.Jt));
     ts.wd_w = (size_t)d_in * d_out;
-    ts.total = ts.x2_w + ts.acc_w + ts.tot_w + ts.rot_w + ts.q_w + ts.ks_w + ts.wd_w;
+    ts.xd_w = ts.mfma ? ((size_t)kDig * L * 2 * N * ts.kt_pad + 7) / 8 : 0;
+    ts.total = ts.x2_w + ts.acc_w + ts.tot_w + ts.rot_w + ts.q_w + ts.ks_w + ts.wd_w + ts.xd_w;
     return ts;
+}
+
+ckks_status launch_xdigits(ckks_ctx *ctx, const uint64_t *x2, int8_t *Xd, uint32_t L, uint32_t kt, uint32_t kt_pad)
+{
+    const uint32_t blocks = L * (uint32_t)((2 * ctx->n) / 64) * (kt_pad / 64);
+    prof_begin(ctx, K_ELEM, 8.0 * kt * 2 * L * ctx->n + (double)kDig * kt_pad * 2 * L * ctx->n);
+    hipLaunchKernelGGL(k_xdigits, dim3(blocks), dim3(kThreads), 0, ctx->stream, x2, Xd, L, ctx->log_n, kt, kt_pad);
+    prof_end(ctx, K_ELEM);
+    HIP_TRY(hipGetLastError());
+    return CKKS_OK;
+}
+
+ckks_status launch_mac_tm_mfma(ckks_ctx *ctx, uint64_t *acc, const int8_t *Xd, const double *Q, const TmArgs &a,
+                               uint32_t kt_pad, uint32_t L, uint32_t logT, bool accumulate)
+{
+    const uint32_t K = 2 * a.P, kbase = 2 * a.pb0, D2 = 2 * a.D, nw = 1u << (logT - 4);
+    CK_REQUIRE(a.jc <= 32 && kbase % 16 == 0 && K <= 4096 && nw >= 1 && nw <= 8, CKKS_EINVAL,
+               "token-major multiply-accumulate: unsupported tile (jc %u, kappa base %u, K %u, T %u)", a.jc, kbase,
+               K, 1u << logT);
+    const uint32_t blocks = L * D2 * 2;
+    const double res = (double)a.jc * 2 * L * ctx->n;
+    // the digits of the pairs' ciphertexts once per launch, the tables once, the accumulators
+    prof_begin(ctx, K_MAC_TM, (double)kDig * K * 2 * L * ctx->n + 8.0 * (double)K * a.jc * L * D2 +
+                                  8.0 * res * (accumulate ? 2 : 1),
+               0.0);
+    switch (nw) {
+    case 1:
+        hipLaunchKernelGGL(k_mac_tm_mfma<1>, dim3(blocks), dim3(64), 0, ctx->stream, acc, Xd, Q, a.jc, K, kbase,
+                           kt_pad, D2, L, logT, ctx->log_n, (int)accumulate, ctx->d_mod);
+        break;
+    case 2:
+        hipLaunchKernelGGL(k_mac_tm_mfma<2>, dim3(blocks), dim3(128), 0, ctx->stream, acc, Xd, Q, a.jc, K, kbase,
+                           kt_pad, D2, L, logT, ctx->log_n, (int)accumulate, ctx->d_mod);
+        break;
+    case 4:
+        hipLaunchKernelGGL(k_mac_tm_mfma<4>, dim3(blocks), dim3(256), 0, ctx->stream, acc, Xd, Q, a.jc, K, kbase,
+                           kt_pad, D2, L, logT, ctx->log_n, (int)accumulate, ctx->d_mod);
+        break;
+    default:
+        hipLaunchKernelGGL(k_mac_tm_mfma<8>, dim3(blocks), dim3(512), 0, ctx->stream, acc, Xd, Q, a.jc, K, kbase,
+                           kt_pad, D2, L, logT, ctx->log_n, (int)accumulate, ctx->d_mod);
+        break;
+    }
+    prof_end(ctx, K_MAC_TM);
+    HIP_TRY(hipGetLastError());
+    return CKKS_OK;
 }
 
 ckks_status launch_mac_tm(ckks_ctx *ctx, uint64_t *acc, const double *x2, const double *Q, const TmArgs &a,
@@ -341,6 +532,7 @@ extern "C" ckks_status ckks_linear_project_tm(ckks_ctx *ctx, const ckks_buf *in,
     double *Q = (double *)(rot + ts.rot_w);
     uint64_t *ksw = (uint64_t *)(Q + ts.q_w);
     double *Wd = (double *)(ksw + ts.ks_w);
+    int8_t *Xd = (int8_t *)(Wd + ts.wd_w);
     CK_TRY(launch_diag_layout(ctx, Wd, W, D, n_in, shape->d_out));
 
     // 1. Rot_b(x_i) and Rot_{b-D}(x_i), hoisted per input
@@ -353,7 +545,10 @@ extern "C" ckks_status ckks_linear_project_tm(ckks_ctx *ctx, const ckks_buf *in,
         CK_TRY(rotate_core(ctx, in[i].data, level, bsteps.data(), bkeys.data(), (uint32_t)bsteps.size(),
                            outs.data(), ksw));
     }
-    CK_TRY(launch_to_f64(ctx, x2, ts.x2_w));
+    if (ts.mfma)
+        CK_TRY(launch_xdigits(ctx, x2, Xd, L, ts.kt, ts.kt_pad));
+    else
+        CK_TRY(launch_to_f64(ctx, x2, ts.x2_w));
 
     // 2./3. tiles of output ciphertexts, giant steps, sub-batches of pairs
     const double delta_w = (double)ctx->primes[level];
@@ -368,6 +563,7 @@ extern "C" ckks_status ckks_linear_project_tm(ckks_ctx *ctx, const ckks_buf *in,
             const uint32_t pairs = n_in * bcount;
             const uint32_t nsub = (pairs + ts.Pb - 1) / ts.Pb;
             for (uint32_t sb = 0, pb0 = 0; sb < nsub; sb++) {
+                // sub-batches of Pb pairs (a multiple of 8), the last one shorter
                 TmArgs a{};
                 a.Wd = Wd;
                 a.D = D;
@@ -378,10 +574,13 @@ extern "C" ckks_status ckks_linear_project_tm(ckks_ctx *ctx, const ckks_buf *in,
                 a.j0 = j0;
                 a.jc = jc;
                 a.pb0 = pb0;
-                a.P = pairs / nsub + (sb < pairs % nsub ? 1 : 0);
+                a.P = std::min(ts.Pb, pairs - pb0);
                 a.npt = a.P * 2 * jc;
                 CK_TRY(launch_enc_periodic(ctx, a, delta_w, L, Q));
-                CK_TRY(launch_mac_tm(ctx, acc, (const double *)x2, Q, a, n1, L, logT, pb0 > 0));
+                if (ts.mfma)
+                    CK_TRY(launch_mac_tm_mfma(ctx, acc, Xd, Q, a, ts.kt_pad, L, logT, pb0 > 0));
+                else
+                    CK_TRY(launch_mac_tm(ctx, acc, (const double *)x2, Q, a, n1, L, logT, pb0 > 0));
                 pb0 += a.P;
             }
             if (g == 0) {

@@ -7,12 +7,14 @@ within the stated bound:
 * toy ring (N = 2^12, 16 tokens x 128 features), n1 = 16, two inputs and three
   outputs, at most five (input, baby step) pairs per launch so the sums are
   carried across launches;
-* toy ring with the plain diagonal split (n1 = 128, no giant step);
-* a ring of degree 2^10 with 4 tokens (runs of four equal plaintext values, so one
-  multiply-accumulate block meets many of them);
+* toy ring with the plain diagonal split (n1 = 128, no giant step), and with n1 = 24,
+  which does not divide D (runs of 16 values: the matrix-core multiply-accumulate
+  except for n1 = 24, which takes the vector-ALU one);
+* a ring of degree 2^10 with 4 tokens (runs of four equal plaintext values: the
+  vector-ALU multiply-accumulate, one block meeting many runs);
 * the projection parameters at full degree (N = 2^16, 24 + 8 limbs, level 12, 128
   tokens x 256 features, n1 = 32: 31 + 32 baby and 7 giant rotations) on a
-  256 x 512 slice.
+  256 x 512 slice (runs of 128 values: the matrix-core multiply-accumulate).
 """
 import dataclasses
 
@@ -94,6 +96,13 @@ def test_toy_tm_projection_carried_sums():
 def test_toy_tm_projection_plain_diagonals():
     err = run_case(TOY, TOY.feats, TOY.feats, TOY.feats, [0])
     say("toy tm (n1 = D) max error vs X@W", err)
+    assert err <= 2.0 ** -12
+
+
+def test_toy_tm_projection_uneven_baby_steps():
+    # n1 = 24 does not divide D = 128 (the last giant step has 8 baby steps): the vector-ALU multiply-accumulate
+    err = run_case(TOY, 2 * TOY.feats, TOY.feats, 24, [0])
+    say("toy tm (n1 = 24) max error vs X@W", err)
     assert err <= 2.0 ** -12
 
 
