@@ -33,7 +33,8 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kPE = 8;        // plaintexts per encode block: 8 consecutive doubles per table row (64 B)
 constexpr int kMaxD = 256;    // features per ciphertext handled by the encode kernel
-constexpr int kJT = 32;       // output ciphertexts per multiply-accumulate tile
+constexpr int kJT = 32;       // output ciphertexts per vector-ALU multiply-accumulate tile
+constexpr int kMaxJtMfma = 32; // and per matrix-core one (64 outputs need 452 VGPRs, one wave per SIMD: slower)
 
 __device__ __forceinline__ double2 cmul(double2 a, double2 b)
 {
@@ -197,7 +198,7 @@ __global__ __launch_bounds__(kThreads) void k_mac_tm(uint64_t *acc, const double
 // Operand layouts (checked on the hardware): A 16x64, lane i holds row i % 16, bytes k = 16 (i / 16) + 0..15;
 // B 64x16, lane i holds column i % 16, the same k; C 16x16, lane i holds column i % 16, rows 4 (i / 16) + r.
 typedef int v4i __attribute__((ext_vector_type(4)));
-constexpr int kDig = 7, kGroups = 2 * kDig - 1, kKB = 64;
+constexpr int kDig = 7, kGroups = 2 * kDig - 1, kKB = 64, kRowW = 20;
 
 __device__ __forceinline__ void digits7(uint64_t v, int8_t *d, size_t stride)
 {
@@ -241,48 +242,94 @@ __global__ __launch_bounds__(kThreads) void k_xdigits(const uint64_t *__restrict
     }
 }
 
-// Block (limb l, run x, polynomial): T / 16 waves, wave w holds positions x T + 16 w .. + 15 of the polynomial
-// and the tile's jc <= 32 outputs (two 16-row MFMA tiles).  Q ([L][2D][npt], npt = K jc, kappa-major) gives the
-// plaintext digits of each 64-kappa block (rows jj >= jc and kappa >= K are zero); Xd the ciphertext digits from
-// kappa_base on (16-byte aligned, rows padded so a block never reads past them).
-template <int NW>
+// Block (limb l, run x, polynomial, part): NW waves, wave w holds 16 positions of the run (x T + 16 (part NW + w)
+// + 0..15) of the polynomial and the tile's jc <= 16 MT outputs (MT 16-row MFMA tiles).  Q ([L][2D][npt],
+// npt = K jc, kappa-major) gives the plaintext digits of each 64-kappa block (rows jj >= jc and kappa >= K are
+// zero); Xd the ciphertext digits from kappa_base on (16-byte aligned, rows padded so a block never reads past
+// them).
+template <int NW, int MT>
 __global__ __launch_bounds__(64 * NW) void k_mac_tm_mfma(uint64_t *acc, const int8_t *__restrict__ Xd,
                                                            const double *__restrict__ Q, uint32_t jc, uint32_t K,
                                                            uint32_t kappa_base, uint32_t kt_pad, uint32_t D2,
                                                            uint32_t L, uint32_t logT, uint32_t log_n,
                                                            int accumulate, const ModQ *__restrict__ mods)
 {
-    __shared__ __attribute__((aligned(16))) int8_t A[kDig][32][kKB];
-    const uint32_t runs = D2, poly = blockIdx.x & 1, x = (blockIdx.x >> 1) % runs, l = (blockIdx.x >> 1) / runs;
+    constexpr int R = 16 * MT;
+    // plaintext digits of the 64-kappa block: row jj of digit a holds 64 bytes, padded to 80 so that both the
+    // packed 4-byte writes (lanes along jj) and the 16-byte MFMA reads spread over the banks
+    __shared__ __attribute__((aligned(16))) uint32_t A[kDig][R][kRowW];
+    const uint32_t parts = (1u << (logT - 4)) / NW;
+    uint32_t bid = blockIdx.x;
+    const uint32_t part = bid % parts;
+    bid /= parts;
+    const uint32_t poly = bid & 1, x = (bid >> 1) % D2, l = (bid >> 1) / D2;
     const uint32_t lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    const uint32_t pos = (x << logT) + 16 * w + (lane & 15);
+    const uint32_t pos = (x << logT) + 16 * (part * NW + w) + (lane & 15);
     const size_t n = (size_t)1 << log_n, cols = 2 * n;
     const size_t plane = (size_t)L * cols * kt_pad;
-    const int8_t *xb = Xd + ((size_t)l * cols + (size_t)poly * n + (x << logT) + 16 * w + (lane & 15)) * kt_pad +
-                       kappa_base + 16 * (lane >> 4);
+    const int8_t *xb = Xd + ((size_t)l * cols + (size_t)poly * n + pos) * kt_pad + kappa_base + 16 * (lane >> 4);
     const double *qx = Q + ((size_t)l * D2 + x) * (size_t)K * jc;
-    v4i c[2][kGroups];
+    v4i c[MT][kGroups];
 #pragma unroll
-    for (int m = 0; m < 2; m++)
+    for (int m = 0; m < MT; m++)
 #pragma unroll
         for (int g = 0; g < kGroups; g++) c[m][g] = v4i{0, 0, 0, 0};
+    // software pipeline: the next block's ciphertext digits and plaintext values are loaded into registers
+    // while the current block's products run
+    constexpr int QPT = (R * (kKB / 4) + 64 * NW - 1) / (64 * NW);  // packed table entries per thread
+    auto load_q = [&](uint32_t k0, double (&qv)[QPT][4]) {
+#pragma unroll
+        for (int i = 0; i < QPT; i++) {
+            const uint32_t e = threadIdx.x + i * 64 * NW, jj = e % R, k4 = e / R;
+#pragma unroll
+            for (int t = 0; t < 4; t++) {
+                const uint32_t kappa = k0 + 4 * k4 + t;
+                qv[i][t] = (e < R * (kKB / 4) && jj < jc && kappa < K) ? qx[(size_t)kappa * jc + jj] : 0.0;
+            }
+        }
+    };
+    v4i bn[kDig];
+    double qn[QPT][4];
+#pragma unroll
+    for (int d = 0; d < kDig; d++) bn[d] = *(const v4i *)(xb + (size_t)d * plane);
+    load_q(0, qn);
     for (uint32_t k0 = 0; k0 < K; k0 += kKB) {
-        __syncthreads();
-        for (uint32_t e = threadIdx.x; e < 32 * kKB; e += 64 * NW) {
-            const uint32_t kk = e / 32, jj = e % 32, kappa = k0 + kk;
-            uint64_t v = 0;
-            if (jj < jc && kappa < K) v = (uint64_t)qx[(size_t)kappa * jc + jj];
-            digits7(v, &A[0][jj][kk], 32 * kKB);
+        v4i b[kDig];
+        double qc[QPT][4];
+#pragma unroll
+        for (int d = 0; d < kDig; d++) b[d] = bn[d];
+#pragma unroll
+        for (int i = 0; i < QPT; i++)
+#pragma unroll
+            for (int t = 0; t < 4; t++) qc[i][t] = qn[i][t];
+        if (k0 + kKB < K) {
+#pragma unroll
+            for (int d = 0; d < kDig; d++) bn[d] = *(const v4i *)(xb + (size_t)d * plane + k0 + kKB);
+            load_q(k0 + kKB, qn);
         }
         __syncthreads();
-        v4i b[kDig];
 #pragma unroll
-        for (int d = 0; d < kDig; d++) b[d] = *(const v4i *)(xb + (size_t)d * plane + k0);
+        for (int i = 0; i < QPT; i++) {
+            const uint32_t e = threadIdx.x + i * 64 * NW, jj = e % R, k4 = e / R;
+            if (e < R * (kKB / 4)) {
+                uint32_t packed[kDig] = {0, 0, 0, 0, 0, 0, 0};
 #pragma unroll
-        for (int m = 0; m < 2; m++) {
+                for (int t = 0; t < 4; t++) {
+                    int8_t d[kDig];
+                    digits7((uint64_t)qc[i][t], d, 1);
+#pragma unroll
+                    for (int a = 0; a < kDig; a++) packed[a] |= (uint32_t)(uint8_t)d[a] << (8 * t);
+                }
+#pragma unroll
+                for (int a = 0; a < kDig; a++) A[a][jj][k4] = packed[a];
+            }
+        }
+        __syncthreads();
+#pragma unroll
+        for (int m = 0; m < MT; m++) {
 #pragma unroll
             for (int a = 0; a < kDig; a++) {
-                const v4i av = *(const v4i *)&A[a][16 * m + (lane & 15)][16 * (lane >> 4)];
+                const v4i av = *(const v4i *)&A[a][16 * m + (lane & 15)][4 * (lane >> 4)];
 #pragma unroll
                 for (int d = 0; d < kDig; d++)
                     c[m][a + d] = __builtin_amdgcn_mfma_i32_16x16x64_i8(av, b[d], c[m][a + d], 0, 0, 0);
@@ -298,7 +345,7 @@ __global__ __launch_bounds__(64 * NW) void k_mac_tm_mfma(uint64_t *acc, const in
     for (int g = 1; g < kGroups; g++) w256[g] = (double)ar.to_canon(ar.mul(w256[g - 1], 256.0));
     const size_t ctw = 2 * (size_t)L * n;
 #pragma unroll
-    for (int m = 0; m < 2; m++) {
+    for (int m = 0; m < MT; m++) {
 #pragma unroll
         for (int r = 0; r < 4; r++) {
             const uint32_t jj = 16 * m + 4 * (lane >> 4) + r;
@@ -331,8 +378,12 @@ TmScratch tm_scratch(const ckks_ctx *ctx, uint32_t L, uint32_t D, uint32_t d_in,
     const uint32_t level = L - 1, n_in = d_in / D, n_out = d_out / D;
     const size_t N = ctx->n, ctw = 2 * (size_t)L * N;
     const uint32_t T = (uint32_t)(N / (2 * D));
-    // output tiles of at most kJT, balanced
-    const uint32_t tiles = (n_out + kJT - 1) / kJT;
+    // the matrix-core path needs runs of 16..128 positions (a 16-column tile inside one run, at most 8 tiles per
+    // block) and every giant step over the same n1 baby steps (D a multiple of n1)
+    ts.mfma = T >= 16 && T <= 128 && D % n1 == 0;
+    // output tiles of at most kJT (vector ALU) or kMaxJtMfma (matrix cores), balanced
+    const uint32_t jmax = ts.mfma ? kMaxJtMfma : kJT;
+    const uint32_t tiles = (n_out + jmax - 1) / jmax;
     ts.Jt = (n_out + tiles - 1) / tiles;
     // pairs per sub-batch: the tile's weight tables within 2 GiB, a multiple of 8 (16-byte aligned digit rows),
     // at most 2048 (int32 digit sums stay exact)
@@ -342,9 +393,6 @@ TmScratch tm_scratch(const ckks_ctx *ctx, uint32_t L, uint32_t D, uint32_t d_in,
     if (ctx->proj_max_pairs) Pb = std::min(Pb, std::max<uint32_t>(8, ctx->proj_max_pairs));
     Pb &= ~7u;
     ts.Pb = std::min(Pb, maxpairs);
-    // the matrix-core path needs runs of 16..128 positions (a 16-column tile inside one run, one block per run)
-    // and every giant step over the same n1 baby steps (D a multiple of n1)
-    ts.mfma = T >= 16 && T <= 128 && D % n1 == 0;
     ts.kt = 2 * n_in * n1;
     ts.kt_pad = ((ts.kt + 63) & ~63u) + 64;
     ts.x2_w = (size_t)n_in * n1 * 2 * ctw;
@@ -371,34 +419,26 @@ ckks_status launch_xdigits(ckks_ctx *ctx, const uint64_t *x2, int8_t *Xd, uint32
 ckks_status launch_mac_tm_mfma(ckks_ctx *ctx, uint64_t *acc, const int8_t *Xd, const double *Q, const TmArgs &a,
                                uint32_t kt_pad, uint32_t L, uint32_t logT, bool accumulate)
 {
-    const uint32_t K = 2 * a.P, kbase = 2 * a.pb0, D2 = 2 * a.D, nw = 1u << (logT - 4);
-    CK_REQUIRE(a.jc <= 32 && kbase % 16 == 0 && K <= 4096 && nw >= 1 && nw <= 8, CKKS_EINVAL,
+    const uint32_t K = 2 * a.P, kbase = 2 * a.pb0, D2 = 2 * a.D, tiles16 = 1u << (logT - 4);
+    CK_REQUIRE(a.jc <= kMaxJtMfma && kbase % 16 == 0 && K <= 4096 && logT >= 4 && logT <= 7, CKKS_EINVAL,
                "token-major multiply-accumulate: unsupported tile (jc %u, kappa base %u, K %u, T %u)", a.jc, kbase,
                K, 1u << logT);
-    const uint32_t blocks = L * D2 * 2;
     const double res = (double)a.jc * 2 * L * ctx->n;
     // the digits of the pairs' ciphertexts once per launch, the tables once, the accumulators
     prof_begin(ctx, K_MAC_TM, (double)kDig * K * 2 * L * ctx->n + 8.0 * (double)K * a.jc * L * D2 +
                                   8.0 * res * (accumulate ? 2 : 1),
                0.0);
-    switch (nw) {
-    case 1:
-        hipLaunchKernelGGL(k_mac_tm_mfma<1>, dim3(blocks), dim3(64), 0, ctx->stream, acc, Xd, Q, a.jc, K, kbase,
-                           kt_pad, D2, L, logT, ctx->log_n, (int)accumulate, ctx->d_mod);
-        break;
-    case 2:
-        hipLaunchKernelGGL(k_mac_tm_mfma<2>, dim3(blocks), dim3(128), 0, ctx->stream, acc, Xd, Q, a.jc, K, kbase,
-                           kt_pad, D2, L, logT, ctx->log_n, (int)accumulate, ctx->d_mod);
-        break;
-    case 4:
-        hipLaunchKernelGGL(k_mac_tm_mfma<4>, dim3(blocks), dim3(256), 0, ctx->stream, acc, Xd, Q, a.jc, K, kbase,
-                           kt_pad, D2, L, logT, ctx->log_n, (int)accumulate, ctx->d_mod);
-        break;
-    default:
-        hipLaunchKernelGGL(k_mac_tm_mfma<8>, dim3(blocks), dim3(512), 0, ctx->stream, acc, Xd, Q, a.jc, K, kbase,
-                           kt_pad, D2, L, logT, ctx->log_n, (int)accumulate, ctx->d_mod);
-        break;
+#define CK_MFMA(NWV, MTV)                                                                                          \
+    hipLaunchKernelGGL((k_mac_tm_mfma<NWV, MTV>), dim3(L * D2 * 2 * (tiles16 / NWV)), dim3(64 * NWV), 0,           \
+                       ctx->stream, acc, Xd, Q, a.jc, K, kbase, kt_pad, D2, L, logT, ctx->log_n, (int)accumulate,   \
+                       ctx->d_mod)
+    switch (tiles16) {
+    case 1: CK_MFMA(1, 2); break;
+    case 2: CK_MFMA(2, 2); break;
+    case 4: CK_MFMA(4, 2); break;
+    default: CK_MFMA(8, 2); break;
     }
+#undef CK_MFMA
     prof_end(ctx, K_MAC_TM);
     HIP_TRY(hipGetLastError());
     return CKKS_OK;
