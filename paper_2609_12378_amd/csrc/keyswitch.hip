@@ -101,8 +101,9 @@ __global__ __launch_bounds__(kThreads) void k_conv(const uint64_t *in, uint32_t 
 // The same conversion in fp64 (every prime below 2^50): y_i = x_i * qhat_inv_i mod s_i (|mul| < 0.875 s_i for
 // canonical operands) is moved into (-s_i/2, s_i/2] by one add or subtract of s_i, then each target sums the
 // products y_i * [Qhat_i]_t (each below 0.875 t in magnitude, since |y_i| < s_i/2 < t) with a range reduction
-// every four terms (sums stay below 4 t < 2^53) and writes the canonical residue: the same integers as k_conv.
-template <int NS_MAX>
+// every four terms (sums stay below 4 t < 2^53) and writes the canonical residue: the same integers as k_conv
+// (RAW: the reduced value, |x| <= t/2, as raw double bits, for a following fp64 transform pass).
+template <int NS_MAX, bool RAW>
 __global__ __launch_bounds__(kThreads) void k_conv_f64(const uint64_t *in, uint32_t in_stride, uint64_t *out,
                                                         uint32_t out_stride, uint32_t split, uint32_t skip,
                                                         ConvArgs a, const double *__restrict__ qhat_inv,
@@ -144,85 +145,34 @@ __global__ __launch_bounds__(kThreads) void k_conv_f64(const uint64_t *in, uint3
             }
         }
         const uint32_t row = t < (int)split ? t : t + skip;
-        dst[(size_t)row << log_n] = ar.to_canon(acc);
+        dst[(size_t)row << log_n] = RAW ? nttc::Ar<true>::to_raw(ar.red(acc)) : ar.to_canon(acc);
     }
 }
 
-// The conversion fused with the first (column) pass of the forward transform of its outputs (fp64, 256-point
-// columns, every prime below 2^50).  Block (poly p, 16 columns, target group) loads the ns source rows of its
-// 16 x 256 positions once and keeps the centred digits y_s (|y_s| < s_s/2 < t) in registers; for each target t of
-// its group it forms sum_s y_s [Qhat_s]_t (range-reduced every four terms and once at the end, so |x| <= q/2 as the
-// column pass with kColMask8 expects), runs the eight column stages and writes raw doubles in layout B, the
-// inter-pass form the fused row passes read.  The digits are the same integers as k_conv_f64's, so the finished
-// transforms are identical.
-template <int NS>
-__global__ __launch_bounds__(512) void k_conv_col8(const uint64_t *__restrict__ in, uint32_t in_stride,
-                                                    uint64_t *out, uint32_t out_stride, ConvArgs a,
-                                                    uint32_t tgroup, uint32_t groups,
-                                                    const double *__restrict__ qhat_inv,
-                                                    const double *__restrict__ qhat_mod,
-                                                    const ModQ *__restrict__ mods, const double *__restrict__ twf,
-                                                    uint32_t log_n, uint32_t blocks_per_row)
+// First (column) pass of the forward transform over rows of raw doubles (|x| <= q/2, the reduced conversion
+// output), in place, 8 residues per thread: block (row, 16 columns), 512 threads; row r uses prime map[r % n].
+// Leaves the rows as raw doubles in the inter-pass form the fused row passes read.
+__global__ __launch_bounds__(512) void k_col8_rows(uint64_t *data, LimbMap map, const ModQ *__restrict__ mods,
+                                                   const double *__restrict__ twf, uint32_t log_n,
+                                                   uint32_t blocks_per_row)
 {
     using nttc::kE8;
-    __shared__ double tws[2][256];
+    __shared__ double tws[256];
     __shared__ double tr[16][nttc::kTr8];
-    __shared__ double s_mod[NS * kMaxPrimes];
-    // the groups of one tile run on one XCD (blocks are dealt to the 8 XCDs in turn), back to back, so the
-    // tile's source rows come from that XCD's L2 after the first read; the tile count is a multiple of 8
-    const uint32_t span = 8 * groups, rem8 = blockIdx.x % span;
-    const uint32_t grp = rem8 >> 3, tile = (blockIdx.x / span) * 8 + (rem8 & 7);
-    const uint32_t p = tile / blocks_per_row, blk = tile % blocks_per_row;
-    const uint32_t i0 = grp * tgroup, i1 = min((uint32_t)a.nt, i0 + tgroup), ng = i1 - i0;
+    const uint32_t row = blockIdx.x / blocks_per_row, blk = blockIdx.x % blocks_per_row;
+    const uint32_t prime = map.prime[row % map.n];
+    const nttc::Ar<true> ar(mods[prime]);
     const uint32_t n2 = 1u << (log_n - 8);
     const uint32_t col = threadIdx.x & 15, t = threadIdx.x >> 4;
-    const size_t coff = (size_t)blk * 16 + col;
-    const int ns = a.ns;
-    for (uint32_t e = threadIdx.x; e < (uint32_t)ns * ng; e += 512)
-        s_mod[e] = qhat_mod[(e / ng) * a.nt + i0 + e % ng];
-    if (threadIdx.x < 255) tws[0][threadIdx.x + 1] = twf[((size_t)a.dst[i0] << log_n) + threadIdx.x + 1];
-    const uint64_t *src = in + ((size_t)p * in_stride << log_n) + coff;
-    double y[NS][kE8];
+    if (threadIdx.x < 255) tws[threadIdx.x + 1] = twf[((size_t)prime << log_n) + threadIdx.x + 1];
+    uint64_t *base = data + ((size_t)row << log_n) + (size_t)blk * 16 + col;
+    double x[kE8];
 #pragma unroll
-    for (int s = 0; s < NS; s++) {
-        if (s < ns) {
-            const nttc::Ar<true> ar(mods[a.src[s]]);
-            const double h = 0.5 * ar.q;
-#pragma unroll
-            for (int k = 0; k < kE8; k++) {
-                const double v = ar.mul(nttc::Ar<true>::from_u64(src[((size_t)s << log_n) +
-                                                                     (size_t)nttc::u8<0>(t, k) * n2]),
-                                        qhat_inv[s]);
-                y[s][k] = v > h ? v - ar.q : (v < -h ? v + ar.q : v);
-            }
-        }
-    }
+    for (int k = 0; k < kE8; k++) x[k] = nttc::Ar<true>::from_raw(base[(size_t)nttc::u8<0>(t, k) * n2]);
     __syncthreads();
-    for (uint32_t i = i0; i < i1; i++) {
-        const nttc::Ar<true> ar(mods[a.dst[i]]);
-        double wnext = 0.0;
-        if (i + 1 < i1 && threadIdx.x < 255) wnext = twf[((size_t)a.dst[i + 1] << log_n) + threadIdx.x + 1];
-        double x[kE8];
+    nttc::fwd8_256<nttc::kColMask8>(x, tws, tr[col], t, ar);
 #pragma unroll
-        for (int k = 0; k < kE8; k++) {
-            double acc = 0.0;
-#pragma unroll
-            for (int s = 0; s < NS; s++) {
-                if (s < ns) {
-                    acc += ar.mul(y[s][k], s_mod[s * ng + (i - i0)]);
-                    if ((s & 3) == 3) acc = ar.red(acc);
-                }
-            }
-            x[k] = ar.red(acc);
-        }
-        const uint32_t nb = (i - i0 + 1) & 1;
-        nttc::fwd8_256<nttc::kColMask8>(x, tws[(i - i0) & 1], tr[col], t, ar, 1, [&]() {
-            if (i + 1 < i1 && threadIdx.x < 255) tws[nb][threadIdx.x + 1] = wnext;
-        });
-        uint64_t *dst = out + (((size_t)p * out_stride + i) << log_n) + coff;
-#pragma unroll
-        for (int k = 0; k < kE8; k++) dst[(size_t)nttc::u8<2>(t, k) * n2] = nttc::Ar<true>::to_raw(x[k]);
-    }
+    for (int k = 0; k < kE8; k++) base[(size_t)nttc::u8<2>(t, k) * n2] = nttc::Ar<true>::to_raw(x[k]);
 }
 
 // u[k][r][n] = sum_{j<nd} d_j[r][sigma(n)] * key[j][k][krow(r)][n], rows r over Q_level u P
@@ -402,7 +352,7 @@ __global__ __launch_bounds__(kThreads) void k_moddown_finish_batch(RotArgs ra, c
 }
 
 ckks_status launch_conv(ckks_ctx *ctx, const ConvDev *cd, const uint64_t *in, uint32_t in_stride, uint64_t *out,
-                        uint32_t out_stride, uint32_t split, uint32_t skip, uint32_t polys)
+                        uint32_t out_stride, uint32_t split, uint32_t skip, uint32_t polys, bool raw = false)
 {
     ConvArgs a;
     a.ns = cd->ns;
@@ -411,13 +361,17 @@ ckks_status launch_conv(ckks_ctx *ctx, const ConvDev *cd, const uint64_t *in, ui
     for (int t = 0; t < cd->nt; t++) a.dst[t] = cd->dst[t];
     const dim3 grid((ctx->n + kThreads - 1) / kThreads, polys), block(kThreads);
     prof_begin(ctx, K_CONV, 8.0 * polys * (a.ns + a.nt) * ctx->n);
-    if (cd->f64 && !ctx->int_only && a.ns <= 16) {
+    if (raw) {
+        CK_REQUIRE(cd->f64 && !ctx->int_only && a.ns <= 8, CKKS_EINVAL, "raw conversion needs the fp64 tables");
+        hipLaunchKernelGGL((k_conv_f64<8, true>), grid, block, 0, ctx->stream, in, in_stride, out, out_stride, split,
+                           skip, a, cd->d_qhat_inv_f, cd->d_qhat_mod_f, ctx->d_mod, ctx->log_n);
+    } else if (cd->f64 && !ctx->int_only && a.ns <= 16) {
         if (a.ns <= 8)
-            hipLaunchKernelGGL(k_conv_f64<8>, grid, block, 0, ctx->stream, in, in_stride, out, out_stride, split,
-                               skip, a, cd->d_qhat_inv_f, cd->d_qhat_mod_f, ctx->d_mod, ctx->log_n);
+            hipLaunchKernelGGL((k_conv_f64<8, false>), grid, block, 0, ctx->stream, in, in_stride, out, out_stride,
+                               split, skip, a, cd->d_qhat_inv_f, cd->d_qhat_mod_f, ctx->d_mod, ctx->log_n);
         else
-            hipLaunchKernelGGL(k_conv_f64<16>, grid, block, 0, ctx->stream, in, in_stride, out, out_stride, split,
-                               skip, a, cd->d_qhat_inv_f, cd->d_qhat_mod_f, ctx->d_mod, ctx->log_n);
+            hipLaunchKernelGGL((k_conv_f64<16, false>), grid, block, 0, ctx->stream, in, in_stride, out, out_stride,
+                               split, skip, a, cd->d_qhat_inv_f, cd->d_qhat_mod_f, ctx->d_mod, ctx->log_n);
     } else if (a.ns <= 4)
         hipLaunchKernelGGL(k_conv<4>, grid, block, 0, ctx->stream, in, in_stride, out, out_stride, split, skip, a,
                            cd->d_qhat_inv, cd->d_qhat_mod, cd->d_neg_q, ctx->d_mod, ctx->log_n);
@@ -439,28 +393,15 @@ ckks_status launch_conv(ckks_ctx *ctx, const ConvDev *cd, const uint64_t *in, ui
     return CKKS_OK;
 }
 
-// Conversion + first forward column pass of `polys` polynomials (in: ns rows at in_stride rows per polynomial,
-// coefficient form; out: nt rows at out_stride, raw doubles after the column pass).  Needs s1 == 8, the fp64
-// tables and ns <= 8.  Targets are split into groups of at most 8 so that a launch has enough blocks.
-ckks_status launch_conv_col8(ckks_ctx *ctx, const ConvDev *cd, const uint64_t *in, uint32_t in_stride,
-                             uint64_t *out, uint32_t out_stride, uint32_t polys)
+// First forward column pass of `rows` rows of raw doubles (row r with prime map.prime[r % map.n]), N = 2^16.
+ckks_status launch_col8_rows(ckks_ctx *ctx, uint64_t *data, uint32_t rows, const LimbMap &map)
 {
-    ConvArgs a;
-    a.ns = cd->ns;
-    a.nt = cd->nt;
-    for (int i = 0; i < cd->ns; i++) a.src[i] = cd->src[i];
-    for (int t = 0; t < cd->nt; t++) a.dst[t] = cd->dst[t];
-    const uint32_t bpr = 1u << (ctx->log_n - 12);  // 16 of the 256 columns per block
-    const uint32_t tgroup = 8, groups = (a.nt + tgroup - 1) / tgroup;
-    CK_REQUIRE((polys * bpr) % 8 == 0, CKKS_EINVAL, "conversion + column pass: %u tiles, not a multiple of 8",
-               polys * bpr);
-    const double res = (double)polys * ctx->n;
-    prof_begin(ctx, K_CONV, 8.0 * res * (a.ns + a.nt),
-               res * (6.0 * a.ns + a.nt * (6.0 * a.ns + 8.0 + 4.0 * kOpsButterflyF64)));
-    hipLaunchKernelGGL(k_conv_col8<8>, dim3(polys * bpr * groups), dim3(512), 0, ctx->stream, in, in_stride, out,
-                       out_stride, a, tgroup, groups, cd->d_qhat_inv_f, cd->d_qhat_mod_f, ctx->d_mod, ctx->d_twf,
+    const uint32_t bpr = 1u << (ctx->log_n - 12);
+    const double res = (double)rows * ctx->n;
+    prof_begin(ctx, K_NTT_FWD_COL, 16.0 * res, res * kOpsButterflyF64 * 4);
+    hipLaunchKernelGGL(k_col8_rows, dim3(rows * bpr), dim3(512), 0, ctx->stream, data, map, ctx->d_mod, ctx->d_twf,
                        ctx->log_n, bpr);
-    prof_end(ctx, K_CONV);
+    prof_end(ctx, K_NTT_FWD_COL);
     HIP_TRY(hipGetLastError());
     return CKKS_OK;
 }
@@ -514,7 +455,9 @@ ckks_status ks_rotate_batch(ckks_ctx *ctx, uint32_t level, uint32_t count, const
         const ConvDev *cd;
         CK_TRY(ctx_conv(ctx, (int)level, -1, &cd));
         if (s1 == 8 && cd->f64 && !ctx->int_only && cd->ns <= 8) {
-            CK_TRY(launch_conv_col8(ctx, cd, up, K, cw, L, 2 * count));
+            // the conversion writes reduced raw doubles; the 8-residue column pass takes them as they are
+            CK_TRY(launch_conv(ctx, cd, up, K, cw, L, L, 0, 2 * count, true));
+            CK_TRY(launch_col8_rows(ctx, cw, 2 * count * L, limb_range(0, L)));
         } else {
             CK_TRY(launch_conv(ctx, cd, up, K, cw, L, L, 0, 2 * count));
             CK_TRY(launch_ntt_fwd_first_pass(ctx, cw, 2 * count, L, limb_range(0, L)));
