@@ -51,20 +51,25 @@ struct TmArgs {
 };
 
 // Encode kPE periodic weight plaintexts per block and transform them: Q[l][x][pt] (x < 2D) holds the
-// canonical residue of plaintext pt's NTT values x*T .. x*T + T - 1 modulo q_l, as a double.
-__global__ __launch_bounds__(kThreads) void k_enc_periodic(TmArgs a, const double2 *__restrict__ fft_w,
-                                                           const double2 *__restrict__ twist, uint32_t T,
-                                                           double c, uint32_t L, const ModQ *__restrict__ mods,
-                                                           const double *__restrict__ twf, uint32_t log_n,
-                                                           double *Q)
+// canonical residue of plaintext pt's NTT values x*T .. x*T + T - 1 modulo q_l, as a double.  512 threads.
+// For 2D = 512 and 256 the transform runs on the register-resident 8-residue stages: for 512 points the first
+// stage (pairs j, j + 256, twiddle Psi[1]) is applied while the values are loaded, leaving two 256-point
+// sub-transforms with bases 2 and 3 (group g of their stage S takes Psi[(2 + i) 2^S + g]); every stage
+// reduces, so all values stay below 2q.  Other sizes use plain LDS stages.
+__global__ __launch_bounds__(512) void k_enc_periodic(TmArgs a, const double2 *__restrict__ fft_w,
+                                                      const double2 *__restrict__ twist, uint32_t T, double c,
+                                                      uint32_t L, const ModQ *__restrict__ mods,
+                                                      const double *__restrict__ twf, uint32_t log_n, double *Q)
 {
-    __shared__ double2 buf[kPE * kMaxD];        // FFT, then the transform's working rows (kPE x 2D doubles)
+    constexpr uint32_t kBT = 512;
+    __shared__ double2 buf[kPE * kMaxD];        // FFT, then the transform's outputs (kPE x 2D doubles)
     __shared__ int64_t mq[kPE * 2 * kMaxD];     // rounded coefficients m'
-    __shared__ double tws[2 * kMaxD];
+    __shared__ double tws[2][256];
+    __shared__ double tr[2 * kPE][nttc::kTr8];
     const uint32_t D = a.D, logD = a.logD, D2 = 2 * D;
     const uint32_t pt0 = blockIdx.x * kPE;
     // 1. one period of each plaintext's slot vector, at its bit-reversed FFT position
-    for (uint32_t e = threadIdx.x; e < kPE * D; e += kThreads) {
+    for (uint32_t e = threadIdx.x; e < kPE * D; e += kBT) {
         const uint32_t p = e / D, j = e % D, pt = pt0 + p;
         double v = 0.0;
         if (pt < a.npt) {
@@ -90,7 +95,7 @@ __global__ __launch_bounds__(kThreads) void k_enc_periodic(TmArgs a, const doubl
     // 2. radix-2 stages len = 2 .. D
     for (uint32_t len = 2; len <= D; len <<= 1) {
         const uint32_t half = len >> 1, step = D / len;
-        for (uint32_t e = threadIdx.x; e < kPE * (D / 2); e += kThreads) {
+        for (uint32_t e = threadIdx.x; e < kPE * (D / 2); e += kBT) {
             const uint32_t p = e / (D / 2), bf = e % (D / 2);
             const uint32_t blk = bf / half, k = bf % half;
             double2 *row = buf + p * D + blk * len;
@@ -103,35 +108,73 @@ __global__ __launch_bounds__(kThreads) void k_enc_periodic(TmArgs a, const doubl
         __syncthreads();
     }
     // 3. twist, scale and round: m'[k] = round(c Re v_k), m'[k + D] = round(c Im v_k)
-    for (uint32_t e = threadIdx.x; e < kPE * D; e += kThreads) {
+    for (uint32_t e = threadIdx.x; e < kPE * D; e += kBT) {
         const uint32_t p = e / D, k = e % D;
         const double2 v = cmul(twist[(size_t)k * T], buf[p * D + k]);
         mq[p * D2 + k] = (int64_t)round(c * v.x);
         mq[p * D2 + k + D] = (int64_t)round(c * v.y);
     }
     double *xs = (double *)buf;  // kPE rows of 2D doubles
+    const bool regs = D2 == 512 || D2 == 256;
+    const uint32_t nsub = D2 / 256;
     // 4. per limb: the 2D-point negacyclic NTT (Cooley-Tukey, group i of stage m takes Psi[m + i])
     for (uint32_t l = 0; l < L; l++) {
         const ModQ md = mods[l];
         const nttc::Ar<true> ar(md);
+        const double *tw = twf + ((size_t)l << log_n);
         __syncthreads();
-        for (uint32_t e = threadIdx.x; e < D2; e += kThreads) tws[e] = twf[((size_t)l << log_n) + e];
-        for (uint32_t e = threadIdx.x; e < kPE * D2; e += kThreads) xs[e] = ar.from_i64(mq[e], md);
-        __syncthreads();
-        for (uint32_t m = 1, t = D; m < D2; m <<= 1, t >>= 1) {
-            for (uint32_t e = threadIdx.x; e < kPE * D; e += kThreads) {
-                const uint32_t p = e / D, bf = e % D;
-                const uint32_t g = bf / t, j = bf % t;
-                double *row = xs + p * D2 + 2 * g * t + j;
-                double x0 = row[0], x1 = row[t];
-                ar.ct(x0, x1, tws[m + g]);
-                row[0] = x0;
-                row[t] = x1;
+        if (regs) {
+            for (uint32_t e = threadIdx.x; e < nsub * 255; e += kBT) {
+                const uint32_t si = e / 255, ee = e % 255 + 1, m = 1u << (31 - __clz(ee));
+                tws[si][ee] = tw[(size_t)(nsub == 2 ? 2 + si : 1) * m + (ee - m)];
             }
             __syncthreads();
+            const uint32_t sub = threadIdx.x >> 5, t = threadIdx.x & 31;
+            const uint32_t p = sub / nsub, si = sub % nsub;
+            const bool live = p < (uint32_t)kPE;
+            double x[nttc::kE8];
+            if (nsub == 2) {
+                const double w0 = tw[1];
+#pragma unroll
+                for (int k = 0; k < nttc::kE8; k++) {
+                    const uint32_t u = nttc::u8<0>(t, k);
+                    double xo = 0.0;
+                    if (live) {
+                        const double X = ar.from_i64(mq[p * D2 + u], md), Y = ar.from_i64(mq[p * D2 + u + 256], md);
+                        const double r = ar.mul(Y, w0);
+                        xo = si == 0 ? X + r : X - r;
+                    }
+                    x[k] = xo;
+                }
+            } else {
+#pragma unroll
+                for (int k = 0; k < nttc::kE8; k++)
+                    x[k] = live ? ar.from_i64(mq[p * D2 + nttc::u8<0>(t, k)], md) : 0.0;
+            }
+            nttc::fwd8_256<0xFFu>(x, tws[si], tr[sub], t, ar);
+            if (live) {
+#pragma unroll
+                for (int k = 0; k < nttc::kE8; k++) xs[p * D2 + 256 * si + nttc::u8<2>(t, k)] = x[k];
+            }
+            __syncthreads();
+        } else {
+            for (uint32_t e = threadIdx.x; e < kPE * D2; e += kBT) xs[e] = ar.from_i64(mq[e], md);
+            __syncthreads();
+            for (uint32_t m = 1, t = D; m < D2; m <<= 1, t >>= 1) {
+                for (uint32_t e = threadIdx.x; e < kPE * D; e += kBT) {
+                    const uint32_t p = e / D, bf = e % D;
+                    const uint32_t g = bf / t, j = bf % t;
+                    double *row = xs + p * D2 + 2 * g * t + j;
+                    double x0 = row[0], x1 = row[t];
+                    ar.ct(x0, x1, tw[m + g]);
+                    row[0] = x0;
+                    row[t] = x1;
+                }
+                __syncthreads();
+            }
         }
         // rows of Q: for each x, kPE consecutive plaintexts
-        for (uint32_t e = threadIdx.x; e < kPE * D2; e += kThreads) {
+        for (uint32_t e = threadIdx.x; e < kPE * D2; e += kBT) {
             const uint32_t p = e % kPE, x = e / kPE, pt = pt0 + p;
             if (pt < a.npt) Q[((size_t)l * D2 + x) * a.npt + pt] = (double)ar.to_canon(xs[p * D2 + x]);
         }
@@ -477,7 +520,7 @@ ckks_status launch_enc_periodic(ckks_ctx *ctx, const TmArgs &a, double delta, ui
     // W's diagonals in, the tables out; FFT and transforms (D/2 log D + L D log 2D butterflies per plaintext)
     prof_begin(ctx, K_ENC_TM, 8.0 * pts * a.D + 8.0 * pts * L * 2 * a.D,
                pts * (a.D / 2.0 * a.logD * 10.0 + L * (double)a.D * (a.logD + 1) * kOpsButterflyF64));
-    hipLaunchKernelGGL(k_enc_periodic, dim3((a.npt + kPE - 1) / kPE), dim3(kThreads), 0, ctx->stream, a,
+    hipLaunchKernelGGL(k_enc_periodic, dim3((a.npt + kPE - 1) / kPE), dim3(512), 0, ctx->stream, a,
                        (const double2 *)ctx->d_fft_w, (const double2 *)ctx->d_fft_twist, T, c, L, ctx->d_mod,
                        ctx->d_twf, ctx->log_n, Q);
     prof_end(ctx, K_ENC_TM);
