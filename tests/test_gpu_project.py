@@ -149,3 +149,11 @@ def test_down_projection_parameters_full_degree_slice():
     err = run_case(PROJ_DOWN, 512, 256, [0])
     say("down slice max error vs X@W", err)
     assert err <= 2.0 ** -18
+
+
+def test_toy_projection_lowest_level():
+    # inputs with two limbs (level 1): the outputs keep one limb after the rescale
+    cfg = dataclasses.replace(TOY, level=1, n1=8)
+    err = run_case(cfg, TOY.feats, TOY.feats, [0])
+    say("toy level-1 max error vs X@W", err)
+    assert err <= 2.0 ** -10

@@ -173,3 +173,10 @@ def test_tm_projection_with_exact_workspace():
     got = to_host(ctx.linear_project(cts, W, T, n1, keys, layout="tm")[0].data)
     ctx.set_workspace(None)
     assert np.array_equal(got, want)
+
+
+def test_toy_tm_projection_lowest_level():
+    cfg = dataclasses.replace(TOY, level=1)
+    err = run_case(cfg, TOY.feats, TOY.feats, 8, [0])
+    say("toy tm level-1 max error vs X@W", err)
+    assert err <= 2.0 ** -10

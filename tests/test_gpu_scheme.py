@@ -244,3 +244,39 @@ def test_decrypted_rotation_is_slot_shift(toy):
     dre, dim = toy.ctx.decode(toy.ctx.decrypt(toy.s_dev, out))
     z = to_host(dre) + 1j * to_host(dim)
     assert np.max(np.abs(z - np.roll(re + 1j * im, -5))) < 1e-2
+
+
+@pytest.mark.parametrize("steps", [0, 2048])
+def test_rotate_identity_steps(toy, steps):
+    # steps 0 and N/2 (the slot count) both give the Galois element 1: a key switch from s to s (the output
+    # differs from the input by the key-switching noise only), bit for bit as the oracle
+    cto, ctg, _ = toy.encrypt_both(17, 4, 2.0 ** 30)
+    assert toy.ctx.galois_elt(steps) == 1
+    ko, kg = toy.galois_keys(80 + steps, steps)
+    eq(toy.ctx.rotate(ctg, steps, kg).data, toy.ck.rotate(cto, steps, ko))
+
+
+def test_lowest_level_operations(toy):
+    # one limb: rotation (a single partial digit), relinearised product; two limbs -> one: rescale
+    c1o, c1g, _ = toy.encrypt_both(18, 1, 2.0 ** 20)
+    c2o, c2g, _ = toy.encrypt_both(19, 1, 2.0 ** 10)
+    ko, kg = toy.galois_keys(90, 3)
+    eq(toy.ctx.rotate(c1g, 3, kg).data, toy.ck.rotate(c1o, 3, ko))
+    a, e = toy.key_randomness(91)
+    rlk_o = toy.ck.keygen_relin(toy.s, a, e)
+    rlk_g = toy.ctx.keygen_relin(toy.s_dev, to_dev(a), to_dev(e))
+    eq(toy.ctx.mul_relin(c1g, c2g, rlk_g).data, toy.ck.mul_relin(c1o, c2o, rlk_o))
+    c3o, c3g, _ = toy.encrypt_both(20, 2, 2.0 ** 30)
+    eq(toy.ctx.rescale(c3g).data, toy.ck.rescale(c3o))
+
+
+@pytest.mark.parametrize("count", [33, 40])
+def test_rotate_hoisted_beyond_one_batch(toy, count):
+    # more rotations than one key-switching launch takes (32): a second, ragged batch
+    cto, ctg, _ = toy.encrypt_both(21, 4, 2.0 ** 30)
+    steps = [s + 1 for s in range(count)]
+    keys = [toy.galois_keys(100 + s, s) for s in steps]
+    outs_g = toy.ctx.rotate_hoisted(ctg, steps, [k[1] for k in keys])
+    outs_o = toy.ck.rotate_hoisted(cto, steps, [k[0] for k in keys])
+    for og, oo in zip(outs_g, outs_o):
+        eq(og.data, oo)
