@@ -354,8 +354,9 @@ ProjScratch proj_scratch(const ckks_ctx *ctx, uint32_t L, uint32_t D, uint32_t d
     const uint32_t level = L - 1, n_in = d_in / D;
     const size_t N = ctx->n, ctw = 2 * (size_t)L * N;
     const uint32_t maxpairs = n_in * n1;
-    // plaintext sub-batch of at most 2 GiB: kJ output blocks x Pb (i, b) pairs
-    const size_t budget = size_t(1) << 31;
+    // plaintext sub-batch of at most 12 GiB (128 pairs at the benchmark shape: each launch reads and writes the
+    // accumulators once, so fewer, larger launches move less; 22 -> 128 pairs measured 1092 -> 1039 ms)
+    const size_t budget = size_t(12) << 30;
     uint32_t Pmax = std::min<uint32_t>(maxpairs, std::max<uint32_t>(1, (uint32_t)(budget / ((size_t)kJ * L * N * 8))));
     if (ctx->proj_max_pairs) Pmax = std::min(Pmax, ctx->proj_max_pairs);
     ps.Pb = Pmax;
