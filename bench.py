@@ -301,14 +301,14 @@ def bench_ntt(torch, steps):
 
 
 def bench_tile(torch, np, steps, warmup, calib_mib):
-    """One output tile of the projection: 4096 -> 14 x 256 features, the same launches as the full one.
+    """One output tile of the projection: 4096 -> 28 x 256 features, the same launches as the full one.
 
     A smaller process for hardware-counter passes; per-launch figures of its kernels apply to the full
     projection, whose launches have the same shapes.
     """
     import dataclasses
     from workloads import PROJECTION
-    cfg = dataclasses.replace(PROJECTION, d_out=14 * PROJECTION.feats)
+    cfg = dataclasses.replace(PROJECTION, d_out=28 * PROJECTION.feats)
     st = setup_projection(torch, np, cfg)
     ctx = st["ctx"]
     if calib_mib:
@@ -327,8 +327,8 @@ def bench_tile(torch, np, steps, warmup, calib_mib):
             outs = ctx.linear_project(st["cts"], st["Wd"], st["T"], st["n1"], st["keys"], outs)
     prof = ctx.profile_all()
     ctx.profile(False)
-    err = check_projection(np, st, outs, blocks=(0, 13))
-    return {"workload": "projection 4096x3584 (one tile of 14 output ciphertexts of the 4096x14336 projection)",
+    err = check_projection(np, st, outs, blocks=(0, 27))
+    return {"workload": "projection 4096x7168 (one tile of 28 output ciphertexts of the 4096x14336 projection)",
             "ms_per_step": t.ms / steps, "decrypt_max_abs_err": err,
             "kernels": {k: {"launches": v[1] / steps, "avg_ms": v[0] / v[1], "bytes_per_launch": v[2] / v[1],
                             "GBps": v[2] / (v[0] * 1e-3) / 1e9} for k, v in prof.items()}}

@@ -95,7 +95,7 @@ ckks_status ckks_ctx_set_stream(ckks_ctx *ctx, void *hip_stream);
 ckks_status ckks_ctx_set_ntt_arith(ckks_ctx *ctx, int mode);
 /* Upper bound on the (input ciphertext, baby step) pairs whose weight
  * plaintexts ckks_linear_project encodes and accumulates per launch (0, the
- * default: as many as fit a 12 GiB staging buffer).  Smaller values use less
+ * default: as many as fit a 24 GiB staging buffer).  Smaller values use less
  * scratch memory and more launches; results are identical for every value. */
 ckks_status ckks_ctx_set_proj_batch(ckks_ctx *ctx, uint32_t max_pairs);
 /* Host copies of the primes q (n_q), p (n_p) and psi (n_q + n_p, q first);

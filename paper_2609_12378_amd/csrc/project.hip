@@ -80,7 +80,8 @@ __global__ __launch_bounds__(kThreads) void k_mac(uint64_t *acc, const uint64_t 
 
 // output blocks per tile: the blocks of one tile share each xrot read; 14 (a divisor of the 56 outputs of the
 // 4096 x 14336 projection) fills the last wave of the multiply-accumulate launches best among the divisors tried
-constexpr uint32_t kJ = 14;
+constexpr uint32_t kJ = 14;   // output blocks per tile on the integer path (k_mac keeps them in registers)
+constexpr uint32_t kJF = 28;  // on the fused fp64 path (one block per output: the tile only sets xrot reuse)
 
 // Row pass of the forward NTT fused with the multiply-accumulate (fp64
 // arithmetic, primes below 2^50).  Block (jj, tile) owns rows_per_block rows of
@@ -343,6 +344,7 @@ ckks_status launch_mac(ckks_ctx *ctx, uint64_t *acc, const uint64_t *pt, const u
 
 // Scratch words of one ckks_linear_project call, by region (every region a multiple of N words).
 struct ProjScratch {
+    uint32_t Jt;  // output blocks per tile (kJ on the integer path, kJF on the fused fp64 one)
     uint32_t Pb;  // (input, baby step) pairs per plaintext sub-batch
     bool diag;    // W re-laid as its cyclic diagonals (radix-8 FFT pass A)
     size_t xrot_w, acc_w, tot_w, rot_w, pt_w, m_w, fft_w, ks_w, wd_w, fop_w, total;
@@ -354,20 +356,25 @@ ProjScratch proj_scratch(const ckks_ctx *ctx, uint32_t L, uint32_t D, uint32_t d
     const uint32_t level = L - 1, n_in = d_in / D;
     const size_t N = ctx->n, ctw = 2 * (size_t)L * N;
     const uint32_t maxpairs = n_in * n1;
-    // plaintext sub-batch of at most 12 GiB (128 pairs at the benchmark shape: each launch reads and writes the
-    // accumulators once, so fewer, larger launches move less; 22 -> 128 pairs measured 1092 -> 1039 ms)
-    const size_t budget = size_t(12) << 30;
-    uint32_t Pmax = std::min<uint32_t>(maxpairs, std::max<uint32_t>(1, (uint32_t)(budget / ((size_t)kJ * L * N * 8))));
+    int s1, s2;
+    ntt_split(ctx->log_n, &s1, &s2);
+    const uint32_t kJt = (s1 > 0 && ntt_uses_f64(ctx, L)) ? kJF : kJ;
+    ps.Jt = kJt;
+    // plaintext sub-batch of at most 24 GiB (128 pairs of 28 output blocks at the benchmark shape: each launch
+    // reads and writes the accumulators once, so fewer, larger launches move less; 22 -> 128 pairs measured
+    // 1092 -> 1039 ms)
+    const size_t budget = size_t(24) << 30;
+    uint32_t Pmax = std::min<uint32_t>(maxpairs, std::max<uint32_t>(1, (uint32_t)(budget / ((size_t)kJt * L * N * 8))));
     if (ctx->proj_max_pairs) Pmax = std::min(Pmax, ctx->proj_max_pairs);
     ps.Pb = Pmax;
     ps.xrot_w = (size_t)n_in * n1 * ctw;
-    ps.acc_w = ps.tot_w = ps.rot_w = (size_t)kJ * ctw;
-    ps.pt_w = (size_t)kJ * ps.Pb * L * N;
-    ps.m_w = (size_t)kJ * ps.Pb * N;               // int64 coefficients
-    ps.fft_w = (size_t)kJ * ps.Pb * (N / 2) * 2;   // double2 per slot
-    // key switching: hoisted baby steps of one input, or the giant step of a tile's kJ partial sums
+    ps.acc_w = ps.tot_w = ps.rot_w = (size_t)kJt * ctw;
+    ps.pt_w = (size_t)kJt * ps.Pb * L * N;
+    ps.m_w = (size_t)kJt * ps.Pb * N;               // int64 coefficients
+    ps.fft_w = (size_t)kJt * ps.Pb * (N / 2) * 2;   // double2 per slot
+    // key switching: hoisted baby steps of one input, or the giant step of a tile's partial sums
     ps.ks_w = std::max(ks_scratch_words(ctx, level, ks_rot_batch(n1 > 1 ? n1 - 1 : 1)),
-                       ks_scratch_words(ctx, level, ks_rot_batch(kJ), kJ));
+                       ks_scratch_words(ctx, level, ks_rot_batch(kJt), kJt));
     // W re-laid as its cyclic diagonals, and the feature index of every FFT position, for the radix-8 FFT pass
     ps.diag = D <= 256 && ctx->log_n >= 12;
     ps.wd_w = ps.diag ? (size_t)d_in * d_out : 0;
@@ -461,7 +468,7 @@ extern "C" ckks_status ckks_linear_project(ckks_ctx *ctx, const ckks_buf *in, co
     // ---- scratch layout
     const size_t N = ctx->n, ctw = 2 * (size_t)L * N;
     const ProjScratch ps = proj_scratch(ctx, L, D, shape->d_in, shape->d_out, n1);
-    const uint32_t Jt = kJ, Pb = ps.Pb;
+    const uint32_t Jt = ps.Jt, Pb = ps.Pb;
     const size_t xrot_w = ps.xrot_w, acc_w = ps.acc_w, tot_w = ps.tot_w, rot_w = ps.rot_w, pt_w = ps.pt_w;
     const size_t m_w = ps.m_w, fft_w = ps.fft_w, ks_w = ps.ks_w, wd_w = ps.wd_w, total = ps.total;
     const bool diag = ps.diag;

@@ -5,9 +5,9 @@
   and decrypted within 2^-12 of X @ W;
 * toy ring with the integer transform arithmetic (the unfused path: separate row
   pass and multiply-accumulate kernels);
-* toy ring with a baby-step/giant-step split (n1 = 16, n2 = 8), two input and 17
-  output ciphertexts (a full tile of output blocks and a ragged one) and at most
-  seven (input, baby step) pairs per launch, so partial sums are carried across
+* toy ring with a baby-step/giant-step split (n1 = 16, n2 = 8), two input and 31
+  output ciphertexts (a full tile of 28 output blocks and a ragged one of 3) and at
+  most seven (input, baby step) pairs per launch, so partial sums are carried across
   launches of unequal sizes;
 * a ring of degree 2^10 (a 64-point second transform pass);
 * the same parameters with weights 2^17 times larger (plaintext coefficients beyond 2^52);
@@ -112,7 +112,7 @@ def test_toy_projection_integer_arithmetic():
 
 def test_toy_projection_bsgs_tiles_and_carried_sums():
     cfg = dataclasses.replace(TOY, n1=16)
-    err = run_case(cfg, 2 * cfg.feats, 17 * cfg.feats, [0, 13, 14, 16], max_pairs=7)
+    err = run_case(cfg, 2 * cfg.feats, 31 * cfg.feats, [0, 27, 28, 30], max_pairs=7)
     say("toy BSGS max error vs X@W", err)
     assert err <= 2.0 ** -12
 
