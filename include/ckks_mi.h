@@ -209,7 +209,7 @@ ckks_status ckks_rotate_hoisted(ckks_ctx *ctx, const ckks_buf *in, const int32_t
 
 /* ModUp of dev_c ([level+1][N], NTT domain): for each digit j meeting
  * [0, level], INTT of its limbs, fast basis conversion to the other q-limbs
- * and P (non-centred, uncorrected), NTT.  dev_digits: [n_digits][level+1+n_p][N]
+ * and P (centred digits, uncorrected), NTT.  dev_digits: [n_digits][level+1+n_p][N]
  * (q-limbs 0..level then p-limbs); n_digits = digits with a limb <= level. */
 ckks_status ckks_modup(ckks_ctx *ctx, const uint64_t *dev_c, uint32_t level, uint64_t *dev_digits);
 /* ModDown of dev_x ([level+1+n_p][N]): (x - NTT(Conv_{P->Q}(INTT([x]_P)))) * P^-1. */

@@ -196,7 +196,7 @@ class Context:
         _check(self.lib.ckks_ctx_set_ntt_arith(self.h, mode), "ckks_ctx_set_ntt_arith")
 
     def set_proj_batch(self, max_pairs: int):
-        """Cap the (input, baby step) pairs per projection launch (0 = by the 2 GiB staging budget)."""
+        """Cap the (input, baby step) pairs per projection launch (0 = by the library's staging budget)."""
         _check(self.lib.ckks_ctx_set_proj_batch(self.h, max_pairs), "ckks_ctx_set_proj_batch")
 
     # workspace op codes (ckks_op)

@@ -9,7 +9,7 @@
 // Schedule on the GPU:
 //  1. hoisted baby-step rotations: one ModUp per input ciphertext, n1 - 1
 //     key switches each, into xrot[i][b] (b = 0 is a copy of x_i);
-//  2. for a tile of J = 8 output blocks and one giant step g, the weight
+//  2. for a tile of J output blocks (28 on the fp64 path, 14 on the integer one) and one giant step g, the weight
 //     plaintexts of a sub-batch of (i, b) pairs are encoded on the fly from W
 //     (slot generation fused into the fp64 FFT -> round -> NTT column pass with
 //     the RNS reduction fused in) and consumed by k_row_mac, which finishes

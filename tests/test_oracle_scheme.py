@@ -3,11 +3,14 @@ stand for (Background, "The CKKS Computation Model": Add, PCMult, Mult, Rot_k, K
 Rescale), plus the definitional identity hoisted == one-at-a-time rotation.
 
 Error bounds: a fresh encryption error e (|e_i| <= 19) moves a decoded slot by at
-most N*19/Delta.  Key switching adds E = sum_j d_j e_j / P.  The digits d_j are
-non-centred (uniform on [0, Q_j), mean Q_j/2), so d_j carries (Q_j/2) times the
-all-ones polynomial, whose value at zeta^k is 2/(1 - zeta^k): up to 2N/pi at the
-slots with 5^j = +-1 mod 2N.  With |e_j(zeta^k)| <= 6 sigma sqrt(N) this gives
-|E| <= n_digits * (Q_j / P) * (2N/pi) * 6 * 3.2 * sqrt(N) / Delta  (ks_bound).
+most N*19/Delta.  Key switching adds E = sum_j d_j e_j / P.  The digits d_j come
+from the centred basis conversion: each coefficient is Q_j times a sum of alpha
+independent values uniform on (-1/2, 1/2), zero mean and variance alpha/12, so
+d_j(zeta) has standard deviation Q_j sqrt(alpha N / 12) and e_j(zeta) 3.2 sqrt(N).
+Six standard deviations of each give
+|E| <= n_digits * (Q_j / P) * 6 sqrt(alpha N / 12) * 6 * 3.2 * sqrt(N) / Delta  (ks_bound).
+(Digits in [0, Q_j) instead carry a mean offset of about Q_j (alpha + 1)/2 times
+the all-ones polynomial, whose value at zeta^k reaches 2N/pi, and break it.)
 """
 import math
 
@@ -50,7 +53,8 @@ def _z(ck, seed):
 
 def ks_bound(ck, level, delta):
     qj = max(math.prod(ck.q[i] for i in ck.digit_limbs(j, level)) for j in range(ck.n_digits(level)))
-    return ck.n_digits(level) * (qj / ck.P) * (2 * ck.n / math.pi) * 6 * 3.2 * math.sqrt(ck.n) / delta
+    return (ck.n_digits(level) * (qj / ck.P) * 6 * math.sqrt(ck.alpha * ck.n / 12) * 6 * 3.2 * math.sqrt(ck.n)
+            / delta)
 
 
 def _dec(ck, s, ct, scale):
