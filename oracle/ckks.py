@@ -480,14 +480,23 @@ class Ckks:
             outs.append(np.stack([self.add(self.automorph(ct[0], g), u0, idx), u1]))
         return outs
 
-    def mul_relin(self, a: np.ndarray, b: np.ndarray, rlk: np.ndarray) -> np.ndarray:
-        level = self.level_of(a)
-        idx = self.level_primes(level)
+    def tensor(self, a: np.ndarray, b: np.ndarray) -> np.ndarray:
+        """(d0, d1, d2) = (a0 b0, a0 b1 + a1 b0, a1 b1): the product decrypting under (1, s, s^2)."""
+        idx = self.level_primes(self.level_of(a))
         d0 = self.mul(a[0], b[0], idx)
         d1 = self.add(self.mul(a[0], b[1], idx), self.mul(a[1], b[0], idx), idx)
         d2 = self.mul(a[1], b[1], idx)
-        u0, u1 = self.keyswitch_digits(self.modup(d2, level), rlk, level, None)
-        return np.stack([self.add(d0, u0, idx), self.add(d1, u1, idx)])
+        return np.stack([d0, d1, d2])
+
+    def relin(self, d: np.ndarray, rlk: np.ndarray) -> np.ndarray:
+        """Key switching of d2 from s^2 to s: (d0 + u0, d1 + u1)."""
+        level = d.shape[1] - 1
+        idx = self.level_primes(level)
+        u0, u1 = self.keyswitch_digits(self.modup(d[2], level), rlk, level, None)
+        return np.stack([self.add(d[0], u0, idx), self.add(d[1], u1, idx)])
+
+    def mul_relin(self, a: np.ndarray, b: np.ndarray, rlk: np.ndarray) -> np.ndarray:
+        return self.relin(self.tensor(a, b), rlk)
 
     # ---------------- the projection ----------------
     @staticmethod
@@ -554,6 +563,106 @@ class Ckks:
                     acc = self.rotate(acc, n1 * g, keys[n1 * g])
                 total = acc if total is None else self.ct_add(total, acc)
             outs.append(self.rescale(total))
+        return outs
+
+    # ---------------- the attention block (token-major) ----------------
+    @staticmethod
+    def attention_mask(D: int, hd: int, c: int) -> np.ndarray:
+        """One period (D features) of the mask M_c: 1 at the features f = c mod hd, position c of every head."""
+        u = np.zeros(D)
+        u[c::hd] = 1.0
+        return u
+
+    def attention_scores(self, q_cts: Sequence[np.ndarray], k_cts: Sequence[np.ndarray], k_of_q: Sequence[int],
+                         T: int, hd: int, rlk: np.ndarray, keys: Dict[int, np.ndarray]):
+        """Scores of one attention block in the token-major layout s = t*D + f, heads of hd features.
+
+        Query ciphertext c holds D/hd heads, slot t*D + h*hd + d = Q[t, h, d]; key ciphertext k_of_q[c] holds
+        one key head repeated in every head position, K'[t*D + h*hd + d] = K[t, d].  The output holds the
+        scores on cyclic token diagonals: slot t*D + h*hd + delta = sum_d Q[t, h, d] K[(t + delta) mod T, d]
+        for delta < T, 0 for T <= delta < hd (the paper's QK^T as Mult plus rotation sums; the packing is this
+        construction's own, see the design notes):
+            P_delta = Rescale(Relin(Rot_{-delta}(Q) x Rot_{delta (D-1)}(K')))        (0 <= delta < T)
+            out     = Rescale( sum_k Rot_k( sum_delta M_{(delta + k) mod hd} * P_delta ) )   (0 <= k < hd)
+        With the left rotation (Rot_k x)[s] = x[s + k], slot t*D + h*hd + delta + d of P_delta holds
+        Q[t, h, d] K[t + delta, d]; M_c selects head position c, so the term k brings position delta + k of
+        P_delta to position delta: the sum over k is the dot product over d, placed at position delta.
+        The masks are periodic plaintexts encoded at scale q_(level-1), so the output scale is
+        scale(Q) scale(K) / q_level.  Keys: -delta and delta (D - 1) (0 < delta < T), k (0 < k < hd)."""
+        level = self.level_of(q_cts[0])
+        D = (self.n // 2) // T
+        assert T <= hd and D % hd == 0 and level >= 2
+        masks = [self.encode_periodic(self.attention_mask(D, hd, c), float(self.q[level - 1]), level)
+                 for c in range(hd)]
+        bcache = {}
+        outs = []
+        for c, q in enumerate(q_cts):
+            kk = k_of_q[c]
+            if kk not in bcache:
+                st = [d * (D - 1) for d in range(1, T)]
+                bcache[kk] = [k_cts[kk]] + self.rotate_hoisted(k_cts[kk], st, [keys[s] for s in st])
+            B = bcache[kk]
+            st = [-d for d in range(1, T)]
+            A = [q] + self.rotate_hoisted(q, st, [keys[s] for s in st])
+            P = [self.rescale(self.mul_relin(A[d], B[d], rlk)) for d in range(T)]
+            total = None
+            for k in range(hd):
+                U = None
+                for d in range(T):
+                    term = self.ct_mul_plain(P[d], masks[(d + k) % hd])
+                    U = term if U is None else self.ct_add(U, term)
+                if k > 0:
+                    U = self.rotate(U, k, keys[k])
+                total = U if total is None else self.ct_add(total, U)
+            outs.append(self.rescale(total))
+        return outs
+
+    def attention_apply(self, p_cts: Sequence[np.ndarray], v_cts: Sequence[np.ndarray], v_of_p: Sequence[int],
+                        T: int, hd: int, rlk: np.ndarray, keys: Dict[int, np.ndarray]):
+        """Weighted sums of values consuming scores in the layout attention_scores writes.
+
+        p_cts[c] holds P[t, h, delta] at slot t*D + h*hd + delta (delta < T; the positions delta >= T are not
+        read); value ciphertext v_of_p[c] holds one value head repeated in every head position, V'[t*D + h*hd
+        + d] = V[t, d].  The output holds O[t, h, d] = sum_delta P[t, h, delta] V[(t + delta) mod T, d] at slot
+        t*D + h*hd + d.  Broadcasting position delta over a head is sum_d M_d * Rot_(delta - d)(P); with
+        j = delta - d:
+            R_delta = Rot_{delta D}(V')                                                (0 <= delta < T)
+            C_j     = Rescale( sum_delta M_{delta - j} * R_delta )  over 0 <= delta - j < hd  (-hd < j < T)
+            out     = Rescale(Relin( sum_j Rot_j(P) x C_j ))
+        C_j is computed at the value ciphertexts' level, rescaled (masks at scale q_(level of V)) and then
+        reduced to the scores' limbs (the scores' level must be below the values'); out has scale
+        scale(P) scale(V) / q_(level of P).  Keys: delta D (0 < delta < T), j (-hd < j < T, j != 0)."""
+        lp, lv = self.level_of(p_cts[0]), self.level_of(v_cts[0])
+        D = (self.n // 2) // T
+        assert T <= hd and D % hd == 0 and 1 <= lp <= lv - 1
+        masks = [self.encode_periodic(self.attention_mask(D, hd, c), float(self.q[lv]), lv + 1) for c in range(hd)]
+        js = list(range(-(hd - 1), T))
+        ccache = {}
+        outs = []
+        for c, p in enumerate(p_cts):
+            kk = v_of_p[c]
+            if kk not in ccache:
+                st = [d * D for d in range(1, T)]
+                R = [v_cts[kk]] + self.rotate_hoisted(v_cts[kk], st, [keys[s] for s in st])
+                C = {}
+                for j in js:
+                    acc = None
+                    for d in range(T):
+                        if 0 <= d - j < hd:
+                            term = self.ct_mul_plain(R[d], masks[d - j])
+                            acc = term if acc is None else self.ct_add(acc, term)
+                    C[j] = np.ascontiguousarray(self.rescale(acc)[:, :lp + 1])
+                ccache[kk] = C
+            C = ccache[kk]
+            st = [j for j in js if j != 0]
+            E = dict(zip(st, self.rotate_hoisted(p, st, [keys[s] for s in st])))
+            E[0] = p
+            idx = self.level_primes(lp)
+            acc = None
+            for j in js:
+                d = self.tensor(E[j], C[j])
+                acc = d if acc is None else np.stack([self.add(acc[i], d[i], idx) for i in range(3)])
+            outs.append(self.rescale(self.relin(acc, rlk)))
         return outs
 
     def linear_project(self, cts: Sequence[np.ndarray], W: np.ndarray, T: int, n1: int,

@@ -70,6 +70,9 @@ class Config:
     d_out: int = 0
     n1: int = 0                           # baby-step count
     batch: int = 0                        # polynomials per NTT batch / rotations per hoisted batch
+    head_dim: int = 0                     # attention: features per head
+    heads: int = 0                        # attention: query heads
+    kv_heads: int = 0                     # attention: key/value heads (grouped-query attention)
     notes: str = ""
 
     @property
@@ -100,3 +103,14 @@ PROJ_WO = Config("proj_wo", 6, 16, 50, 24, 8, 3, scale_log2=40, level=12, tokens
                  d_in=4096, d_out=4096, n1=32)
 PROJ_DOWN = Config("proj_down", 7, 16, 50, 24, 8, 3, scale_log2=40, level=12, tokens=128,
                    d_in=14336, d_out=4096, n1=8)
+# Attention block, toy ring: N = 2^12, 6 + 2 limbs of 50-bit primes, scale 2^50 (close to the primes, so a
+# ciphertext product rescaled by one prime keeps it), 16 tokens x 128 features = two heads of 64 per
+# ciphertext, inputs at level 5.
+ATTN_TOY = Config("attn_toy", 8, 12, 50, 6, 2, 3, scale_log2=50, level=5, tokens=16, head_dim=64, heads=4,
+                  kv_heads=2)
+# One Llama-3-8B attention block's ciphertext work: 128 tokens x 256 features (two heads of 128) per
+# ciphertext, 32 query heads (16 ciphertexts) and 8 key/value heads (each repeated in both head positions of
+# its own ciphertext: 8 key and 8 value ciphertexts), projections 4096 -> 4096 (Q, O) and 4096 -> 2 x 1024
+# (K, V, each head written twice), token-major layout, inputs at level 12, scale 2^50.
+ATTENTION = Config("attention", 9, 16, 50, 24, 8, 3, scale_log2=50, level=12, tokens=128, d_in=4096,
+                   d_out=4096, n1=32, head_dim=128, heads=32, kv_heads=8)
