@@ -133,7 +133,9 @@ typedef enum {
     CKKS_OP_MODUP = 9,          /* shape[0] = level */
     CKKS_OP_MODDOWN = 10,       /* shape[0] = level */
     CKKS_OP_LINEAR_PROJECT = 11, /* shape = {limbs of the inputs, tokens, d_in, d_out, n1} */
-    CKKS_OP_LINEAR_PROJECT_TM = 12 /* the same shape */
+    CKKS_OP_LINEAR_PROJECT_TM = 12, /* the same shape */
+    CKKS_OP_ATTN_SCORES = 13,   /* shape = {limbs of the inputs, tokens, head_dim} */
+    CKKS_OP_ATTN_APPLY = 14     /* shape = {limbs of the scores, limbs of the values, tokens, head_dim} */
 } ckks_op;
 size_t ckks_workspace_bytes(const ckks_ctx *ctx, int op, const uint32_t *shape);
 ckks_status ckks_set_workspace(ckks_ctx *ctx, void *dev, size_t bytes);
@@ -264,6 +266,61 @@ ckks_status ckks_linear_project(ckks_ctx *ctx, const ckks_buf *in, const double 
 ckks_status ckks_linear_project_tm(ckks_ctx *ctx, const ckks_buf *in, const double *dev_W,
                                    const ckks_proj_shape *shape, const int32_t *key_steps,
                                    const uint64_t *const *dev_keys, uint32_t n_keys, ckks_buf *out);
+
+/* ---- attention block (token-major layout) --------------------------------- */
+
+/* Shape of the attention calls: `tokens` tokens per ciphertext (T, a power of
+ * two in [16, 128]) and heads of `head_dim` features (hd, a power of two with
+ * T <= hd <= D, where D = N/2/T <= 256 features per ciphertext).  Slot
+ * t*D + h*hd + d of a ciphertext holds feature d of head h of token t. */
+typedef struct {
+    uint32_t tokens, head_dim;
+} ckks_attn_shape;
+
+/* Attention scores on token diagonals (the scores S_Delta that QK^T produces
+ * in the paper's C-Delta layout, Section "C--Delta Attention Layout and
+ * Computation" and Table ccmm-performance; the paper gives no construction,
+ * this one is QK^T as Mult plus rotation sums).  q: n_q query ciphertexts
+ * (D/hd heads each); k: n_k key ciphertexts, each holding one key head
+ * repeated in every head position (slot t*D + h*hd + d = K[t, d] for all h);
+ * query c uses key k_of_q[c].  Output c holds, at slot t*D + h*hd + delta,
+ *   S[t, h, delta] = sum_d Q[t, h, d] K[(t + delta) mod T, d]   (delta < T)
+ * and 0 for T <= delta < hd, computed as
+ *   P_delta = Rescale(Relin(Rot_{-delta}(Q) x Rot_{delta(D-1)}(K')))
+ *   out = Rescale(sum_{k<hd} Rot_k(sum_delta M_{(delta+k) mod hd} * P_delta))
+ * with M_c the 0/1 mask of head position c, a periodic plaintext at scale
+ * q_(level-1).  Inputs: n_limbs = level + 1 >= 3, equal within q and within k,
+ * equal scales within each; out[c]: n_limbs = level - 1, scale set to
+ * scale(q) scale(k) / q_level.  Keys (Galois, key_steps[r] -> dev_keys[r]):
+ * steps -delta and delta (D-1) for 0 < delta < T, and 1 .. hd-1; dev_rlk: the
+ * relinearisation key.  All device memory is the caller's; scratch from the
+ * arena or workspace (CKKS_OP_ATTN_SCORES).  Errors: CKKS_EINVAL (shapes,
+ * k_of_q out of range, output descriptors), CKKS_EUNSUPPORTED (token count,
+ * primes of 50 bits or more, no special primes), CKKS_ELEVEL, CKKS_ESCALE,
+ * CKKS_ENOKEY; all checked before any launch. */
+ckks_status ckks_attention_scores(ckks_ctx *ctx, const ckks_buf *q, uint32_t n_q, const ckks_buf *k, uint32_t n_k,
+                                  const uint32_t *k_of_q, const ckks_attn_shape *shape, const uint64_t *dev_rlk,
+                                  const int32_t *key_steps, const uint64_t *const *dev_keys, uint32_t n_keys,
+                                  ckks_buf *out);
+
+/* Weighted sums of values consuming scores in the layout ckks_attention_scores
+ * writes (the paper's PV consuming P_Delta, same sections).  p: n_p score
+ * ciphertexts (slot t*D + h*hd + delta = P[t, h, delta] for delta < T; the
+ * positions delta >= T are not read); v: n_v value ciphertexts, each holding
+ * one value head repeated in every head position; scores c use value
+ * v_of_p[c].  Output c holds, at slot t*D + h*hd + d,
+ *   O[t, h, d] = sum_{delta<T} P[t, h, delta] V[(t + delta) mod T, d]
+ * computed as C_j = Rescale(sum_delta M_{delta-j} * Rot_{delta D}(V')) over
+ * 0 <= delta - j < hd (masks at scale q_(level of v), C_j then kept on the
+ * scores' limbs) and out = Rescale(Relin(sum_{-hd<j<T} Rot_j(P) x C_j)).
+ * The scores' level must be below the values': 2 <= p.n_limbs < v.n_limbs;
+ * out[c]: n_limbs = p.n_limbs - 1, scale set to scale(p) scale(v) / q_(level
+ * of p).  Keys: steps delta D (0 < delta < T) and j (-hd < j < T, j != 0);
+ * dev_rlk as above; scratch: CKKS_OP_ATTN_APPLY; errors as above. */
+ckks_status ckks_attention_apply(ckks_ctx *ctx, const ckks_buf *p, uint32_t n_p, const ckks_buf *v, uint32_t n_v,
+                                 const uint32_t *v_of_p, const ckks_attn_shape *shape, const uint64_t *dev_rlk,
+                                 const int32_t *key_steps, const uint64_t *const *dev_keys, uint32_t n_keys,
+                                 ckks_buf *out);
 
 /* ---- measurement helpers ------------------------------------------------- */
 

@@ -580,8 +580,9 @@ class Ckks:
         Query ciphertext c holds D/hd heads, slot t*D + h*hd + d = Q[t, h, d]; key ciphertext k_of_q[c] holds
         one key head repeated in every head position, K'[t*D + h*hd + d] = K[t, d].  The output holds the
         scores on cyclic token diagonals: slot t*D + h*hd + delta = sum_d Q[t, h, d] K[(t + delta) mod T, d]
-        for delta < T, 0 for T <= delta < hd (the paper's QK^T as Mult plus rotation sums; the packing is this
-        construction's own, see the design notes):
+        for delta < T, 0 for T <= delta < hd: the scores on token diagonals (the S_Delta of Section "C--Delta
+        Attention Layout and Computation", for which the paper gives no construction; this one is QK^T as Mult
+        plus rotation sums):
             P_delta = Rescale(Relin(Rot_{-delta}(Q) x Rot_{delta (D-1)}(K')))        (0 <= delta < T)
             out     = Rescale( sum_k Rot_k( sum_delta M_{(delta + k) mod hd} * P_delta ) )   (0 <= k < hd)
         With the left rotation (Rot_k x)[s] = x[s + k], slot t*D + h*hd + delta + d of P_delta holds

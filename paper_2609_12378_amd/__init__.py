@@ -41,6 +41,10 @@ class _ProjShape(ctypes.Structure):
                 ("n1", ctypes.c_uint32)]
 
 
+class _AttnShape(ctypes.Structure):
+    _fields_ = [("tokens", ctypes.c_uint32), ("head_dim", ctypes.c_uint32)]
+
+
 _LIB = None
 
 # name -> (restype, argtypes)
@@ -77,6 +81,10 @@ _SIGS = {
     "ckks_automorph": (ctypes.c_int, [_VP, _VP, _U32, _U32, _VP]),
     "ckks_linear_project": (ctypes.c_int, [_VP, _BP, _VP, ctypes.POINTER(_ProjShape), _VP, _VP, _U32, _BP]),
     "ckks_linear_project_tm": (ctypes.c_int, [_VP, _BP, _VP, ctypes.POINTER(_ProjShape), _VP, _VP, _U32, _BP]),
+    "ckks_attention_scores": (ctypes.c_int, [_VP, _BP, _U32, _BP, _U32, _VP, ctypes.POINTER(_AttnShape), _VP, _VP,
+                                             _VP, _U32, _BP]),
+    "ckks_attention_apply": (ctypes.c_int, [_VP, _BP, _U32, _BP, _U32, _VP, ctypes.POINTER(_AttnShape), _VP, _VP,
+                                            _VP, _U32, _BP]),
     "ckks_profile_enable": (ctypes.c_int, [_VP, ctypes.c_int]),
     "ckks_profile_read": (ctypes.c_int, [_VP, ctypes.c_char_p, ctypes.POINTER(_DBL), ctypes.POINTER(_U64),
                                          ctypes.POINTER(_DBL), ctypes.POINTER(_DBL)]),
@@ -201,7 +209,7 @@ class Context:
 
     # workspace op codes (ckks_op)
     OP_ENCODE, OP_DECODE, OP_ENCRYPT, OP_DECRYPT, OP_KEYGEN, OP_RESCALE, OP_ROTATE, OP_MUL_RELIN, OP_MODUP, \
-        OP_MODDOWN, OP_LINEAR_PROJECT, OP_LINEAR_PROJECT_TM = range(1, 13)
+        OP_MODDOWN, OP_LINEAR_PROJECT, OP_LINEAR_PROJECT_TM, OP_ATTN_SCORES, OP_ATTN_APPLY = range(1, 15)
 
     def workspace_bytes(self, op: int, shape=()) -> int:
         """Device bytes one call of `op` takes from the arena or workspace, for the given shape."""
@@ -372,6 +380,49 @@ class Context:
         for o, b in zip(outs, ob):
             o.scale = b.scale
         return list(outs)
+
+    def _attention(self, fn: str, a_cts: Sequence[Buf], b_cts: Sequence[Buf], b_of_a: Sequence[int], tokens: int,
+                   head_dim: int, rlk: torch.Tensor, keys: Dict[int, torch.Tensor], outs: Optional[Sequence[Buf]]):
+        if len(b_of_a) != len(a_cts):
+            raise ValueError("%s: %d ciphertexts but %d indices" % (fn, len(a_cts), len(b_of_a)))
+        if outs is None:
+            outs = [Buf(self.zeros(2, a_cts[0].n_limbs - (2 if fn == "ckks_attention_scores" else 1)), 0.0)
+                    for _ in a_cts]
+        if len(outs) < len(a_cts):
+            raise ValueError("%s: %d outputs for %d inputs" % (fn, len(outs), len(a_cts)))
+        ab = (_Buf * len(a_cts))(*[c.c() for c in a_cts])
+        bb = (_Buf * len(b_cts))(*[c.c() for c in b_cts])
+        ob = (_Buf * len(a_cts))(*[o.c() for o in outs[:len(a_cts)]])
+        idx = (_U32 * len(a_cts))(*b_of_a)
+        steps = sorted(keys)
+        ks = (ctypes.c_int32 * max(1, len(steps)))(*steps)
+        kp = (ctypes.c_void_p * max(1, len(steps)))(*[keys[s].data_ptr() for s in steps])
+        shape = _AttnShape(tokens, head_dim)
+        _check(getattr(self.lib, fn)(self.h, ab, len(a_cts), bb, len(b_cts), idx, ctypes.byref(shape), _ptr(rlk), ks,
+                                     kp, len(steps), ob), fn)
+        for o, b in zip(outs, ob):
+            o.scale = b.scale
+        return list(outs[:len(a_cts)])
+
+    def attention_scores(self, q_cts: Sequence[Buf], k_cts: Sequence[Buf], k_of_q: Sequence[int], tokens: int,
+                         head_dim: int, rlk: torch.Tensor, keys: Dict[int, torch.Tensor],
+                         outs: Optional[Sequence[Buf]] = None) -> List[Buf]:
+        """Scores on token diagonals: out[c] slot t*D + h*hd + delta = sum_d Q_c[t, h, d] K[(t + delta) mod T, d]."""
+        return self._attention("ckks_attention_scores", q_cts, k_cts, k_of_q, tokens, head_dim, rlk, keys, outs)
+
+    def attention_apply(self, p_cts: Sequence[Buf], v_cts: Sequence[Buf], v_of_p: Sequence[int], tokens: int,
+                        head_dim: int, rlk: torch.Tensor, keys: Dict[int, torch.Tensor],
+                        outs: Optional[Sequence[Buf]] = None) -> List[Buf]:
+        """Weighted sums: out[c] slot t*D + h*hd + d = sum_delta P_c[t, h, delta] V[(t + delta) mod T, d]."""
+        return self._attention("ckks_attention_apply", p_cts, v_cts, v_of_p, tokens, head_dim, rlk, keys, outs)
+
+    @staticmethod
+    def attention_steps(slots: int, tokens: int, head_dim: int) -> List[int]:
+        """Every rotation step the two attention calls need for this shape."""
+        D = slots // tokens
+        st = set(-d for d in range(1, tokens)) | set(d * (D - 1) for d in range(1, tokens)) | set(range(1, head_dim))
+        st |= set(d * D for d in range(1, tokens)) | set(j for j in range(-head_dim + 1, tokens) if j)
+        return sorted(st)
 
     # ---------------- measurement ----------------
     def profile(self, on: bool = True):

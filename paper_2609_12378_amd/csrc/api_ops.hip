@@ -65,6 +65,12 @@ size_t op_workspace_bytes(const ckks_ctx *ctx, int op, const uint32_t *shape)
     case CKKS_OP_LINEAR_PROJECT_TM:
         if (!shape) return SIZE_MAX;
         return proj_tm_workspace_bytes(ctx, shape[0], shape[1], shape[2], shape[3], shape[4]);
+    case CKKS_OP_ATTN_SCORES:
+        if (!shape) return SIZE_MAX;
+        return attn_scores_workspace_bytes(ctx, shape[0], shape[1], shape[2]);
+    case CKKS_OP_ATTN_APPLY:
+        if (!shape) return SIZE_MAX;
+        return attn_apply_workspace_bytes(ctx, shape[0], shape[1], shape[2], shape[3]);
     default: return SIZE_MAX;
     }
 }
@@ -117,6 +123,47 @@ ckks_status rotate_many(ckks_ctx *ctx, const uint64_t *cs, size_t stride, uint32
                                outs + r0, rw));
     }
     return CKKS_OK;
+}
+
+ckks_status rotate_each(ckks_ctx *ctx, const uint64_t *cs, size_t stride, uint32_t count, uint32_t level,
+                        const int32_t *steps, const uint64_t *const *keys, uint64_t *const *outs, uint64_t *work)
+{
+    if (!count) return CKKS_OK;
+    const uint32_t L = level + 1, ext = L + ctx->n_p, nd = n_digits(ctx, level);
+    const size_t N = ctx->n, dig_ct = (size_t)nd * ext * N;
+    uint64_t *digits = work;
+    uint64_t *rw = digits + (size_t)count * (dig_ct + (size_t)ctx->alpha * N);
+    CK_TRY(ks_modup_batch(ctx, cs + (size_t)L * N, stride, count, level, digits));
+    const uint32_t bs = ks_rot_batch(count);
+    std::vector<uint32_t> g(count);
+    std::vector<const uint64_t *> c0s(count), digs(count);
+    for (uint32_t r = 0; r < count; r++) {
+        g[r] = ckks_galois_elt(ctx, steps[r]);
+        c0s[r] = cs + (size_t)r * stride;
+        digs[r] = digits + (size_t)r * dig_ct;
+    }
+    for (uint32_t r0 = 0; r0 < count; r0 += bs) {
+        const uint32_t cnt = count - r0 < bs ? count - r0 : bs;
+        CK_TRY(ks_rotate_batch(ctx, level, cnt, c0s.data() + r0, digs.data() + r0, g.data() + r0, keys + r0,
+                               outs + r0, rw));
+    }
+    return CKKS_OK;
+}
+
+ckks_status rescale_many(ckks_ctx *ctx, const uint64_t *c, uint32_t count, uint32_t l, uint64_t *out,
+                         uint64_t *work)
+{
+    if (!count) return CKKS_OK;
+    const size_t N = ctx->n;
+    const uint32_t polys = 2 * count;
+    uint64_t *top = work, *r = top + (size_t)polys * N;
+    // the top limb of every polynomial, then the same steps as one rescale over all of them
+    HIP_TRY(hipMemcpy2DAsync(top, N * 8, c + (size_t)l * N, (size_t)(l + 1) * N * 8, N * 8, polys,
+                             hipMemcpyDeviceToDevice, ctx->stream));
+    CK_TRY(launch_ntt(ctx, top, polys, limb_range(l, 1), true));
+    CK_TRY(launch_rescale_spread(ctx, r, top, polys, l));
+    CK_TRY(launch_ntt(ctx, r, polys * l, limb_range(0, l), false));
+    return launch_rescale_finish(ctx, out, c, r, polys, l);
 }
 
 // c ([2][l+1][N]) -> out ([2][l][N]) = round(c / q_l); work: (2 + 2l) N words

@@ -86,6 +86,8 @@ size_t proj_workspace_bytes(const ckks_ctx *ctx, uint32_t L, uint32_t tokens, ui
                             uint32_t n1);
 size_t proj_tm_workspace_bytes(const ckks_ctx *ctx, uint32_t L, uint32_t tokens, uint32_t d_in, uint32_t d_out,
                                uint32_t n1);
+size_t attn_scores_workspace_bytes(const ckks_ctx *ctx, uint32_t L, uint32_t tokens, uint32_t head_dim);
+size_t attn_apply_workspace_bytes(const ckks_ctx *ctx, uint32_t Lp, uint32_t Lv, uint32_t tokens, uint32_t head_dim);
 
 // projection helpers (project.hip): W's cyclic diagonals Wd[((jb * n_in + i) * D + k) * D + o] =
 // W[(i D + (k + o) mod D) * d_out + jb D + o]; canonical residues -> the same integers as doubles, in place
@@ -103,6 +105,30 @@ ckks_status rescale_core(ckks_ctx *ctx, const uint64_t *c, uint32_t l, uint64_t 
 // ks_rot_batch(count), count)
 ckks_status rotate_many(ckks_ctx *ctx, const uint64_t *cs, size_t stride, uint32_t count, uint32_t level,
                         int32_t steps, const uint64_t *key, uint64_t *const *outs, uint64_t *work);
+// `count` ciphertexts (at cs + r * stride) each rotated by its own step with its own key; one batched ModUp.
+// work: ks_scratch_words(ctx, level, ks_rot_batch(count), count) words
+ckks_status rotate_each(ckks_ctx *ctx, const uint64_t *cs, size_t stride, uint32_t count, uint32_t level,
+                        const int32_t *steps, const uint64_t *const *keys, uint64_t *const *outs, uint64_t *work);
+// rescale of `count` contiguous ciphertexts c ([count][2][l+1][N]) into out ([count][2][l][N]);
+// work: 2 count (1 + l) N words
+ckks_status rescale_many(ckks_ctx *ctx, const uint64_t *c, uint32_t count, uint32_t l, uint64_t *out,
+                         uint64_t *work);
+
+// matrix-core multiply-accumulate over residues (project_tm.hip): acc[jj] (+)= sum_kappa Q[kappa][jj] x_kappa for
+// jj < jc and the K ciphertexts kappa_base .. kappa_base + K - 1 of a digit layout Xd, per limb l and run x of
+// 2^logT positions: Q is [L][D2][K][jc] canonical residues as doubles (D2 runs), acc [jc][2][L][N] canonical.
+uint32_t mac_kt_pad(uint32_t kt);
+size_t mac_digit_bytes(const ckks_ctx *ctx, uint32_t L, uint32_t kt_pad);
+uint32_t mac_max_outputs();
+// x2 ([kt][2][L][N] canonical) -> Xd, the digit layout of kt ciphertexts (mac_digit_bytes bytes)
+ckks_status launch_xdigits(ckks_ctx *ctx, const uint64_t *x2, int8_t *Xd, uint32_t L, uint32_t kt, uint32_t kt_pad);
+ckks_status launch_mac_mfma(ckks_ctx *ctx, uint64_t *acc, const int8_t *Xd, const double *Q, uint32_t jc, uint32_t K,
+                            uint32_t kbase, uint32_t kt_pad, uint32_t D2, uint32_t L, uint32_t logT, bool accumulate);
+// periodic plaintexts of `count` explicit period vectors U ([count][D]) at scale delta: Q[l][x][pt] (x < 2D) holds
+// plaintext pt's NTT values on run x (positions x N/2D ..) modulo q_l, l < L, as doubles
+ckks_status launch_enc_vectors(ckks_ctx *ctx, const double *U, uint32_t D, uint32_t count, double delta, uint32_t L,
+                               double *Q);
+
 // decode: coef = coefficient form of limbs 0..min(limbs,2)-1 ([limbs][N]); writes N/2 slots
 ckks_status dec_slots(ckks_ctx *ctx, const uint64_t *coef, uint32_t limbs, double scale, double2 *work, double *re,
                       double *im);

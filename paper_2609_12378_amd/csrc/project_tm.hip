@@ -44,6 +44,7 @@ __device__ __forceinline__ double2 cmul(double2 a, double2 b)
 
 struct TmArgs {
     const double *Wd;   // W's cyclic diagonals [jb][i][k][o]
+    const double *U;    // or explicit period vectors: plaintext pt's D values at U[pt D ..] (then Wd is unused)
     uint32_t D, logD, n_in, n1g, bcount;
     uint32_t j0, jc;    // first output of the tile, outputs in the tile
     uint32_t pb0, P;    // first (input, baby step) pair of the sub-batch, pairs in it
@@ -72,7 +73,9 @@ __global__ __launch_bounds__(512) void k_enc_periodic(TmArgs a, const double2 *_
     for (uint32_t e = threadIdx.x; e < kPE * D; e += kBT) {
         const uint32_t p = e / D, j = e % D, pt = pt0 + p;
         double v = 0.0;
-        if (pt < a.npt) {
+        if (pt < a.npt && a.U) {
+            v = a.U[(size_t)pt * D + j];
+        } else if (pt < a.npt) {
             const uint32_t jj = pt % a.jc, uv = (pt / a.jc) & 1, pr = a.pb0 + pt / (2 * a.jc);
             const uint32_t i = pr / a.bcount, b = pr % a.bcount, k = a.n1g + b;
             const uint32_t o = (j + D - a.n1g % D) % D;   // feature before the giant-step shift
@@ -449,42 +452,10 @@ TmScratch tm_scratch(const ckks_ctx *ctx, uint32_t L, uint32_t D, uint32_t d_in,
     return ts;
 }
 
-ckks_status launch_xdigits(ckks_ctx *ctx, const uint64_t *x2, int8_t *Xd, uint32_t L, uint32_t kt, uint32_t kt_pad)
-{
-    const uint32_t blocks = L * (uint32_t)((2 * ctx->n) / 64) * (kt_pad / 64);
-    prof_begin(ctx, K_ELEM, 8.0 * kt * 2 * L * ctx->n + (double)kDig * kt_pad * 2 * L * ctx->n);
-    hipLaunchKernelGGL(k_xdigits, dim3(blocks), dim3(kThreads), 0, ctx->stream, x2, Xd, L, ctx->log_n, kt, kt_pad);
-    prof_end(ctx, K_ELEM);
-    HIP_TRY(hipGetLastError());
-    return CKKS_OK;
-}
-
 ckks_status launch_mac_tm_mfma(ckks_ctx *ctx, uint64_t *acc, const int8_t *Xd, const double *Q, const TmArgs &a,
                                uint32_t kt_pad, uint32_t L, uint32_t logT, bool accumulate)
 {
-    const uint32_t K = 2 * a.P, kbase = 2 * a.pb0, D2 = 2 * a.D, tiles16 = 1u << (logT - 4);
-    CK_REQUIRE(a.jc <= kMaxJtMfma && kbase % 16 == 0 && K <= 4096 && logT >= 4 && logT <= 7, CKKS_EINVAL,
-               "token-major multiply-accumulate: unsupported tile (jc %u, kappa base %u, K %u, T %u)", a.jc, kbase,
-               K, 1u << logT);
-    const double res = (double)a.jc * 2 * L * ctx->n;
-    // the digits of the pairs' ciphertexts once per launch, the tables once, the accumulators
-    prof_begin(ctx, K_MAC_TM, (double)kDig * K * 2 * L * ctx->n + 8.0 * (double)K * a.jc * L * D2 +
-                                  8.0 * res * (accumulate ? 2 : 1),
-               0.0);
-#define CK_MFMA(NWV, MTV)                                                                                          \
-    hipLaunchKernelGGL((k_mac_tm_mfma<NWV, MTV>), dim3(L * D2 * 2 * (tiles16 / NWV)), dim3(64 * NWV), 0,           \
-                       ctx->stream, acc, Xd, Q, a.jc, K, kbase, kt_pad, D2, L, logT, ctx->log_n, (int)accumulate,   \
-                       ctx->d_mod)
-    switch (tiles16) {
-    case 1: CK_MFMA(1, 2); break;
-    case 2: CK_MFMA(2, 2); break;
-    case 4: CK_MFMA(4, 2); break;
-    default: CK_MFMA(8, 2); break;
-    }
-#undef CK_MFMA
-    prof_end(ctx, K_MAC_TM);
-    HIP_TRY(hipGetLastError());
-    return CKKS_OK;
+    return launch_mac_mfma(ctx, acc, Xd, Q, a.jc, 2 * a.P, 2 * a.pb0, kt_pad, 2 * a.D, L, logT, accumulate);
 }
 
 ckks_status launch_mac_tm(ckks_ctx *ctx, uint64_t *acc, const double *x2, const double *Q, const TmArgs &a,
@@ -549,6 +520,69 @@ ckks_status tm_check_shape(const ckks_ctx *ctx, uint32_t L, uint32_t T, uint32_t
 }
 
 }  // namespace
+
+uint32_t mac_kt_pad(uint32_t kt) { return ((kt + 63) & ~63u) + 64; }
+
+size_t mac_digit_bytes(const ckks_ctx *ctx, uint32_t L, uint32_t kt_pad)
+{
+    return (size_t)kDig * L * 2 * ctx->n * kt_pad;
+}
+
+uint32_t mac_max_outputs() { return kMaxJtMfma; }
+
+ckks_status launch_xdigits(ckks_ctx *ctx, const uint64_t *x2, int8_t *Xd, uint32_t L, uint32_t kt, uint32_t kt_pad)
+{
+    const uint32_t blocks = L * (uint32_t)((2 * ctx->n) / 64) * (kt_pad / 64);
+    prof_begin(ctx, K_ELEM, 8.0 * kt * 2 * L * ctx->n + (double)kDig * kt_pad * 2 * L * ctx->n);
+    hipLaunchKernelGGL(k_xdigits, dim3(blocks), dim3(kThreads), 0, ctx->stream, x2, Xd, L, ctx->log_n, kt, kt_pad);
+    prof_end(ctx, K_ELEM);
+    HIP_TRY(hipGetLastError());
+    return CKKS_OK;
+}
+
+ckks_status launch_mac_mfma(ckks_ctx *ctx, uint64_t *acc, const int8_t *Xd, const double *Q, uint32_t jc, uint32_t K,
+                            uint32_t kbase, uint32_t kt_pad, uint32_t D2, uint32_t L, uint32_t logT, bool accumulate)
+{
+    const uint32_t tiles16 = 1u << (logT - 4);
+    CK_REQUIRE(jc >= 1 && jc <= (uint32_t)kMaxJtMfma && kbase % 16 == 0 && K >= 1 && K <= 4096 && logT >= 4 &&
+                   logT <= 7 && kbase + ((K + 63) & ~63u) <= kt_pad,
+               CKKS_EINVAL, "matrix-core multiply-accumulate: unsupported tile (jc %u, kappa base %u, K %u, T %u)",
+               jc, kbase, K, 1u << logT);
+    const double res = (double)jc * 2 * L * ctx->n;
+    // the digits of the K ciphertexts once per launch, the tables once, the accumulators
+    prof_begin(ctx, K_MAC_TM, (double)kDig * K * 2 * L * ctx->n + 8.0 * (double)K * jc * L * D2 +
+                                  8.0 * res * (accumulate ? 2 : 1),
+               0.0);
+#define CK_MFMA(NWV, MTV)                                                                                          \
+    hipLaunchKernelGGL((k_mac_tm_mfma<NWV, MTV>), dim3(L * D2 * 2 * (tiles16 / NWV)), dim3(64 * NWV), 0,           \
+                       ctx->stream, acc, Xd, Q, jc, K, kbase, kt_pad, D2, L, logT, ctx->log_n, (int)accumulate,     \
+                       ctx->d_mod)
+    switch (tiles16) {
+    case 1: CK_MFMA(1, 2); break;
+    case 2: CK_MFMA(2, 2); break;
+    case 4: CK_MFMA(4, 2); break;
+    default: CK_MFMA(8, 2); break;
+    }
+#undef CK_MFMA
+    prof_end(ctx, K_MAC_TM);
+    HIP_TRY(hipGetLastError());
+    return CKKS_OK;
+}
+
+ckks_status launch_enc_vectors(ckks_ctx *ctx, const double *U, uint32_t D, uint32_t count, double delta, uint32_t L,
+                               double *Q)
+{
+    CK_REQUIRE(D >= 4 && D <= (uint32_t)kMaxD && (D & (D - 1)) == 0 && 2 * D <= ctx->n && count >= 1, CKKS_EINVAL,
+               "periodic encode: period %u outside [4, %d] or not a power of two", D, kMaxD);
+    TmArgs a{};
+    a.U = U;
+    a.D = D;
+    while ((1u << a.logD) < D) a.logD++;
+    a.jc = 1;
+    a.bcount = 1;
+    a.npt = count;
+    return launch_enc_periodic(ctx, a, delta, L, Q);
+}
 
 size_t proj_tm_workspace_bytes(const ckks_ctx *ctx, uint32_t L, uint32_t tokens, uint32_t d_in, uint32_t d_out,
                                uint32_t n1)
