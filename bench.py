@@ -158,6 +158,134 @@ def bench_tm(torch, np, steps, warmup, n1s=(16, 32)):
     return res
 
 
+def device_keys(torch, ctx, s, steps, seed):
+    """Galois keys for `steps` and the relinearisation key from device randomness (uniform residues, rounded
+    Gaussian errors): generating the attention block's ~550 keys from host randomness would take minutes."""
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(seed)
+    n, dnum = ctx.n, ctx.dnum
+
+    def rand_a():
+        rows = [torch.randint(0, p, (dnum, 1, n), generator=gen, device="cuda", dtype=torch.int64)
+                for p in ctx.primes]
+        return torch.cat(rows, dim=1).view(torch.uint64).contiguous()
+
+    def rand_e():
+        e = torch.round(torch.randn((dnum, n), generator=gen, device="cuda", dtype=torch.float64) * 3.2)
+        return e.clamp(-19, 19).to(torch.int32).contiguous()
+
+    keys = {st: ctx.keygen_galois(s, ctx.galois_elt(st), rand_a(), rand_e()) for st in steps}
+    return keys, ctx.keygen_relin(s, rand_a(), rand_e())
+
+
+def attention_plain(np, X, Wq, Wk, Wv, Wo, T, hd, heads, kv_heads):
+    """The block in fp64 on the host, scores on cyclic token diagonals (no Softmax: P = S)."""
+    Q, K, V = X @ Wq, X @ Wk, X @ Wv
+    O = np.zeros((T, heads * hd))
+    grp = heads // kv_heads
+    for h in range(heads):
+        q, k, v = Q[:, h * hd:(h + 1) * hd], K[:, (h // grp) * hd:(h // grp + 1) * hd], \
+            V[:, (h // grp) * hd:(h // grp + 1) * hd]
+        S = np.stack([np.sum(q * np.roll(k, -d, axis=0), axis=1) for d in range(T)], axis=1)  # [t][delta]
+        for d in range(T):
+            O[:, h * hd:(h + 1) * hd] += S[:, d:d + 1] * np.roll(v, -d, axis=0)
+    return O @ Wo
+
+
+def bench_attention(torch, np, steps, warmup):
+    """One Llama-3-8B attention block's ciphertext work in the token-major layout: Q, K, V projections, scores
+    on token diagonals, weighted sums of values (consuming the scores: Softmax is outside this build) and the
+    output projection, timed as one step."""
+    from paper_2609_12378_amd import Context
+    from workloads import ATTENTION as cfg, gaussian_error, gaussian_weights, rng, ternary_secret, \
+        uniform_residues, uniform_slots
+    ctx = Context(cfg.log_n, cfg.n_q, cfg.n_p, cfg.dnum, q_bits=cfg.q_bits)
+    n, T, hd, level, n1 = ctx.n, cfg.tokens, cfg.head_dim, cfg.level, cfg.n1
+    D = (n // 2) // T
+    hpc = D // hd
+    d_kv = cfg.kv_heads * hd
+    s = torch.from_numpy(ternary_secret(rng(cfg.index, 3), n)).cuda()
+    X = uniform_slots(rng(cfg.index, 1), (T, cfg.d_in))
+    gw = rng(cfg.index, 2)
+    # 1/sqrt(hd) folded into W_Q, as the block scales its scores
+    Wq = gaussian_weights(gw, (cfg.d_in, cfg.heads * hd)) / np.sqrt(hd)
+    Wk = gaussian_weights(gw, (cfg.d_in, d_kv))
+    Wv = gaussian_weights(gw, (cfg.d_in, d_kv))
+    Wo = gaussian_weights(gw, (cfg.heads * hd, cfg.d_out))
+    # K and V projections emit each head in every head position of its own ciphertext
+    dup = np.concatenate([np.arange(m * hd, (m + 1) * hd) for m in range(cfg.kv_heads) for _ in range(hpc)])
+    Wk2, Wv2 = np.ascontiguousarray(Wk[:, dup]), np.ascontiguousarray(Wv[:, dup])
+    # one projection for Q, K' and V' (one set of baby-step rotations of the inputs, full output tiles)
+    Wqkv = np.ascontiguousarray(np.concatenate([Wq, Wk2, Wv2], axis=1))
+    Wd = {k: torch.from_numpy(v).cuda() for k, v in (("qkv", Wqkv), ("o", Wo))}
+    delta = float(2 ** cfg.scale_log2)
+    ge = rng(cfg.index, 4)
+    cts = []
+    for i in range(cfg.d_in // D):
+        pt = ctx.encode(torch.from_numpy(tm_pack(X, T, D, i)).cuda(), None, delta, level + 1)
+        a = torch.from_numpy(uniform_residues(ge, ctx.q[:level + 1], n)).cuda()
+        e = torch.from_numpy(gaussian_error(ge, n)).cuda()
+        cts.append(ctx.encrypt(s, pt, a, e))
+    n2 = -(-D // n1)
+    steps_p = [b for b in range(1, n1)] + [b - D for b in range(n1)] + [n1 * g for g in range(1, n2)]
+    all_steps = sorted(set(steps_p) | set(Context.attention_steps(n // 2, T, hd)))
+    keys, rlk = device_keys(torch, ctx, s, all_steps, cfg.index)
+    torch.cuda.synchronize()
+    log("attention: %d keys ready" % len(keys))
+    n_q, n_kv = cfg.heads * hd // D, cfg.kv_heads
+    grp = cfg.heads // cfg.kv_heads
+    kv_of_q = [c * hpc // grp for c in range(n_q)]
+    ev = {k: torch.cuda.Event(enable_timing=True) for k in ("a", "b", "c", "d", "e")}
+
+    def step():
+        ev["a"].record()
+        QKV = ctx.linear_project(cts, Wd["qkv"], T, n1, keys, layout="tm")
+        Q, K, V = QKV[:n_q], QKV[n_q:n_q + n_kv], QKV[n_q + n_kv:]
+        ev["b"].record()
+        S = ctx.attention_scores(Q, K, kv_of_q, T, hd, rlk, keys)
+        ev["c"].record()
+        O = ctx.attention_apply(S, V, kv_of_q, T, hd, rlk, keys)
+        ev["d"].record()
+        Y = ctx.linear_project(O, Wd["o"], T, n1, keys, layout="tm")
+        ev["e"].record()
+        return Y
+
+    for w in range(warmup):
+        Y = step()
+        torch.cuda.synchronize()
+        log("attention warmup", w, "done")
+    ctx.profile(True)
+    ctx.profile_reset()
+    phase = {"qkv_projection": 0.0, "scores": 0.0, "weighted_sums": 0.0, "output_projection": 0.0}
+    with Timer(torch) as t:
+        for _ in range(steps):
+            Y = step()
+            torch.cuda.synchronize()
+            for name, (a, b) in zip(phase, (("a", "b"), ("b", "c"), ("c", "d"), ("d", "e"))):
+                phase[name] += ev[a].elapsed_time(ev[b]) / steps
+    prof = ctx.profile_all()
+    ctx.profile(False)
+    want = attention_plain(np, X, Wq, Wk, Wv, Wo, T, hd, cfg.heads, cfg.kv_heads)
+    errs = []
+    for j in (0, 7, 15):
+        re, _ = ctx.decode(ctx.decrypt(s, Y[j]))
+        errs.append(float(np.max(np.abs(re.cpu().numpy() - tm_pack(want, T, D, j)))))
+    res = {
+        "workload": "one Llama-3-8B attention block, token-major (slot t*256 + f): 128 tokens, 32 query / 8 key-value "
+                    "heads of 128, N=2^16, 24+8 x 50-bit primes, dnum 3, scale 2^50, inputs at level 12; Q/K/V/O "
+                    "projections (n1=32; Q, K, V as one 4096x8192 projection, K and V heads written twice), scores on token "
+                    "diagonals, weighted sums consuming them (no Softmax)",
+        "s_per_block": t.ms / steps / 1e3,
+        "phases_ms": {k: round(v, 3) for k, v in phase.items()},
+        "decrypt_max_abs_err": max(errs), "output_max_abs": float(np.max(np.abs(want))),
+        "keys": len(keys),
+        "kernels_ms": {k: round(v[0] / steps, 3) for k, v in sorted(prof.items(), key=lambda kv: -kv[1][0])}}
+    log("attention block: %.1f ms (%s), max err %.3g" % (t.ms / steps, res["phases_ms"], max(errs)))
+    del keys, rlk, cts, ctx
+    torch.cuda.empty_cache()
+    return res
+
+
 def check_projection(np, st, outs, blocks=(0, 27, 55)):
     """Decrypt sampled outputs and compare with X @ W (property check at full size)."""
     ctx, T, D = st["ctx"], st["T"], st["D"]
@@ -406,7 +534,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-secondary", action="store_true")
-    ap.add_argument("--only", choices=["keyswitch", "ntt", "tile", "shapes", "tm"], default=None,
+    ap.add_argument("--only", choices=["keyswitch", "ntt", "tile", "shapes", "tm", "attention"], default=None,
                     help="run only this secondary workload (for profiling); prints its JSON")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also run one plain device copy of this many MiB (for hardware-counter calibration)")
@@ -428,6 +556,9 @@ def main():
         return
     if args.only == "tm":
         print(json.dumps(bench_tm(torch, np, args.steps, args.warmup)), flush=True)
+        return
+    if args.only == "attention":
+        print(json.dumps(bench_attention(torch, np, args.steps, args.warmup)), flush=True)
         return
     if args.only == "shapes":
         print(json.dumps(bench_shapes(torch, np, args.steps)), flush=True)
@@ -479,6 +610,9 @@ def main():
         torch.cuda.empty_cache()
         log("token-major projection")
         secondary["projection_tm"] = bench_tm(torch, np, 1, 1, n1s=(32,))["n1=32"]
+        torch.cuda.empty_cache()
+        log("attention block")
+        secondary["attention"] = bench_attention(torch, np, 1, 1)
     cpu = None
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle sample)")

@@ -12,24 +12,30 @@
 //   out     = Rescale( sum_k Rot_k( U_k ) ),  U_k = sum_delta M_{(delta + k) mod hd} * P_delta    0 <= k < hd
 // and slot t*D + h*hd + delta of out holds sum_d Q[t, h, d] K[(t + delta) mod T, d] (zero for delta >= T).
 // The masks M_c (1 on head position c) are slot vectors of period D, so their plaintexts are constant on
-// runs of T consecutive NTT positions; each U_k over all delta is a dense residue contraction per run —
-// the token-major projection's matrix-core multiply-accumulate, with a mask table in place of the weights.
+// runs of T consecutive NTT positions, with values m[c] on a run.  At one NTT position the sums over delta are
+// then a cyclic correlation of the ciphertext values x[delta] with m: U_k = sum_delta m[(delta + k) mod hd]
+// x[delta] = z[-k], z = x (*) m_r (cyclic convolution of length hd, m_r[v] = m[-v]), evaluated exactly mod
+// q_l as INTT(NTT(x) NTT(m_r)) with a cyclic NTT along delta (root psi^(2N/n)) — O(hd log hd) per position
+// instead of hd T products.
 //
 // Weighted sums.  Scores P in that layout, a value ciphertext V' with one value head in every position:
 //   R_delta = Rot_{delta D}(V'),  C_j = Rescale( sum_delta M_{delta - j} * R_delta )   (0 <= delta - j < hd)
 //   out     = Rescale(Relin( sum_j Rot_j(P) x C_j ))                                   -hd < j < T
 // so that out[t*D + h*hd + d] = sum_delta P[t, h, delta] V[(t + delta) mod T, d].  The C_j depend only on the
 // value ciphertext and are shared by every score ciphertext that uses it; the products are summed before
-// the single relinearisation.
+// the single relinearisation.  C_j = z[j mod 2hd] for the same correlation at length 2hd with m zero past hd:
+// delta - j spans T + hd - 1 <= 2hd values, so no two of them meet modulo 2hd.
 #include <algorithm>
 #include <vector>
 
 #include "ckks_internal.h"
+#include "ntt_core.h"
 #include "ops.h"
 
 namespace {
 
 constexpr int kThreads = 256;
+constexpr uint32_t kRotChunk = 32;  // outputs rotated (or rescaled) per batch
 
 // U[c][f] = 1 if f = c (mod hd), else 0; c < hd, f < D
 __global__ __launch_bounds__(kThreads) void k_attn_masks(double *U, uint32_t D, uint32_t hd)
@@ -40,29 +46,129 @@ __global__ __launch_bounds__(kThreads) void k_attn_masks(double *U, uint32_t D, 
     U[i] = (f & (hd - 1)) == c ? 1.0 : 0.0;
 }
 
-// The multiply-accumulate table of one output tile: Qt[l][x][kappa][jj] = MQ[l][x][c] with
-//   scores (wrap = 1): c = (kappa + o0 + jj) mod hd;
-//   sums   (wrap = 0): c = kappa - (o0 + jj) if it lies in [0, hd), else the entry is 0.
-// MQ: [L][D2][hd] (the mask plaintexts on each run), Qt: [L][D2][K][jc].
-__global__ __launch_bounds__(kThreads) void k_attn_table(double *Qt, const double *__restrict__ MQ, uint32_t L,
-                                                         uint32_t D2, uint32_t K, uint32_t jc, uint32_t hd, int o0,
-                                                         int wrap)
+// Cyclic NTT of length n = 2^LOGN along the first index of s ([n][P] doubles in LDS, |values| < 2q): the
+// Cooley-Tukey loop with natural-order input and bit-reversed output, group i of stage m taking om[m + i] =
+// w_(2m)^brev_(log m)(i) (w_(2m) a primitive 2m-th root of unity).  Every value stays below 2q.
+template <int LOGN, int P, int NT>
+__device__ __forceinline__ void corr_fwd(double *s, const double *om, const nttc::Ar<true> &ar)
 {
-    const size_t i = (size_t)blockIdx.x * kThreads + threadIdx.x;
-    const size_t total = (size_t)L * D2 * K * jc;
-    if (i >= total) return;
-    const uint32_t jj = (uint32_t)(i % jc);
-    const uint32_t kappa = (uint32_t)((i / jc) % K);
-    const size_t lx = i / ((size_t)jc * K);  // l * D2 + x
-    double v = 0.0;
-    if (wrap) {
-        const uint32_t c = (uint32_t)((int)kappa + o0 + (int)jj) & (hd - 1);
-        v = MQ[lx * hd + c];
-    } else {
-        const int c = (int)kappa - (o0 + (int)jj);
-        if (c >= 0 && c < (int)hd) v = MQ[lx * hd + (uint32_t)c];
+    constexpr int n = 1 << LOGN;
+    for (int m = 1, t = n / 2; m < n; m <<= 1, t >>= 1) {
+        for (int b = threadIdx.x; b < (n / 2) * P; b += NT) {
+            const int p = b % P, bi = b / P, i = bi / t, j = 2 * i * t + bi % t;
+            double X = s[j * P + p], Y = s[(j + t) * P + p];
+            ar.ct(X, Y, om[m + i]);
+            s[j * P + p] = X;
+            s[(j + t) * P + p] = Y;
+        }
+        __syncthreads();
     }
-    Qt[i] = v;
+}
+
+// Its inverse without the 1/n (Gentleman-Sande, bit-reversed input, natural output, omi[m + i] = om[m + i]^-1).
+template <int LOGN, int P, int NT>
+__device__ __forceinline__ void corr_inv(double *s, const double *omi, const nttc::Ar<true> &ar)
+{
+    constexpr int n = 1 << LOGN;
+    for (int m = n / 2, t = 1; m >= 1; m >>= 1, t <<= 1) {
+        for (int b = threadIdx.x; b < (n / 2) * P; b += NT) {
+            const int p = b % P, bi = b / P, i = bi / t, j = 2 * i * t + bi % t;
+            double X = s[j * P + p], Y = s[(j + t) * P + p];
+            ar.gs(X, Y, omi[m + i]);
+            s[j * P + p] = X;
+            s[(j + t) * P + p] = Y;
+        }
+        __syncthreads();
+    }
+}
+
+// Twiddles of the cyclic NTT of length n for limbs l < L: om[l][m + i] = psi^e, e = N brev_(log m)(i) / m < N
+// (psi^e = twf[brev(e)], the ring's table), omi the inverses from the inverse table.
+__global__ __launch_bounds__(kThreads) void k_attn_tw(double *om, double *omi, uint32_t n, uint32_t L,
+                                                      const double *__restrict__ twf, const double *__restrict__ itwf,
+                                                      uint32_t log_n)
+{
+    const uint32_t i = blockIdx.x * kThreads + threadIdx.x;
+    if (i >= L * n) return;
+    const uint32_t l = i / n, k = i % n;
+    double w = 1.0, wi = 1.0;
+    if (k > 0) {
+        const uint32_t logm = 31 - __clz(k), ii = k - (1u << logm);
+        const uint32_t br = logm ? __brev(ii) >> (32 - logm) : 0;
+        const uint32_t e = (br << log_n) >> logm;
+        if (e) {
+            const uint32_t idx = __brev(e) >> (32 - log_n);
+            w = twf[((size_t)l << log_n) + idx];
+            wi = itwf[((size_t)l << log_n) + idx];
+        }
+    }
+    om[i] = w;
+    omi[i] = wi;
+}
+
+// The transformed masks of one (limb l, run): Mh[l][run][f] = NTT(m_r)[f] / n, m_r[v] = m[(n - v) mod n] with
+// m[c] = MQ[l][run][c] for c < hd and 0 for hd <= c < n.  One block per (l, run).
+template <int LOGN>
+__global__ __launch_bounds__(kThreads) void k_attn_mhat(double *Mh, const double *__restrict__ MQ, uint32_t hd,
+                                                        uint32_t D2, const double *__restrict__ Om,
+                                                        const ModQ *__restrict__ mods)
+{
+    constexpr int n = 1 << LOGN;
+    __shared__ double s[n], om[n];
+    const uint32_t bid = blockIdx.x, l = bid / D2;
+    const nttc::Ar<true> ar(mods[l]);
+    for (int i = threadIdx.x; i < n; i += kThreads) {
+        om[i] = Om[(size_t)l * n + i];
+        const uint32_t c = (uint32_t)(n - i) & (n - 1);
+        s[i] = c < hd ? MQ[(size_t)bid * hd + c] : 0.0;
+    }
+    __syncthreads();
+    corr_fwd<LOGN, 1, kThreads>(s, om, ar);
+    const double q = mods[l].qd;
+    const double ninv = q - (q - 1.0) / (double)n;  // n divides q - 1
+    for (int f = threadIdx.x; f < n; f += kThreads) Mh[(size_t)bid * n + f] = (double)ar.to_canon(ar.mul(s[f], ninv));
+}
+
+// z = x (*) m_r at P consecutive positions of one (limb, polynomial): x[delta] is position p of input ciphertext
+// delta < T (x + delta ctw, [2][L][N] each; zero for T <= delta < n), Mh the transformed masks of each position's
+// run (p >> logT).  Output e < nout is z[(sgn e + off) mod n], written canonical to out + e ctw.
+template <int LOGN, int P>
+__global__ __launch_bounds__(kThreads) void k_attn_corr(uint64_t *out, const uint64_t *__restrict__ x, uint32_t T,
+                                                        uint32_t nout, int sgn, int off, size_t ctw, uint32_t L,
+                                                        uint32_t log_n, uint32_t logT, uint32_t D2,
+                                                        const double *__restrict__ Om, const double *__restrict__ Omi,
+                                                        const double *__restrict__ Mh, const ModQ *__restrict__ mods)
+{
+    constexpr int n = 1 << LOGN;
+    __shared__ double s[n * P];
+    __shared__ double om[n], omi[n];
+    const uint32_t groups = (1u << log_n) / P;
+    const uint32_t pg = blockIdx.x % groups, rest = blockIdx.x / groups;
+    const uint32_t poly = rest & 1, l = rest >> 1;
+    const uint32_t p0 = pg * P;
+    const nttc::Ar<true> ar(mods[l]);
+    for (int i = threadIdx.x; i < n; i += kThreads) {
+        om[i] = Om[(size_t)l * n + i];
+        omi[i] = Omi[(size_t)l * n + i];
+    }
+    const size_t row = (((size_t)poly * L + l) << log_n) + p0;
+    for (int i = threadIdx.x; i < n * P; i += kThreads) {
+        const uint32_t d = i / P, p = i % P;
+        s[i] = d < T ? (double)x[(size_t)d * ctw + row + p] : 0.0;
+    }
+    __syncthreads();
+    corr_fwd<LOGN, P, kThreads>(s, om, ar);
+    for (int i = threadIdx.x; i < n * P; i += kThreads) {
+        const uint32_t f = i / P, p = i % P, run = (p0 + p) >> logT;
+        s[i] = ar.mul(s[i], Mh[((size_t)l * D2 + run) * n + f]);
+    }
+    __syncthreads();
+    corr_inv<LOGN, P, kThreads>(s, omi, ar);
+    for (int i = threadIdx.x; i < (int)nout * P; i += kThreads) {
+        const uint32_t e = i / P, p = i % P;
+        const uint32_t f = (uint32_t)(sgn * (int)e + off) & (n - 1);
+        out[(size_t)e * ctw + row + p] = ar.to_canon(s[f * P + p]);
+    }
 }
 
 // out[w] = (accumulate ? out[w] : 0) + sum_{r < count} src[r * stride + w] mod q, w < 2 L N (one ciphertext).
@@ -105,6 +211,13 @@ __global__ __launch_bounds__(kThreads) void k_tensor_acc(uint64_t *d, const uint
     d[2 * ew + i] = reduce128(a2, m);
 }
 
+uint32_t log2u(uint32_t v)
+{
+    uint32_t r = 0;
+    while ((1u << r) < v) r++;
+    return r;
+}
+
 inline dim3 grid_of(size_t total) { return dim3((unsigned)((total + kThreads - 1) / kThreads)); }
 
 ckks_status launch_masks(ckks_ctx *ctx, double *U, double *MQ, uint32_t D, uint32_t hd, double delta, uint32_t L)
@@ -114,14 +227,56 @@ ckks_status launch_masks(ckks_ctx *ctx, double *U, double *MQ, uint32_t D, uint3
     return launch_enc_vectors(ctx, U, D, hd, delta, L, MQ);
 }
 
-ckks_status launch_table(ckks_ctx *ctx, double *Qt, const double *MQ, uint32_t L, uint32_t D2, uint32_t K,
-                         uint32_t jc, uint32_t hd, int o0, bool wrap)
+constexpr int kCorrP = 32;  // positions per correlation block
+
+// twiddles and transformed masks for the correlation of length n over L limbs: Om, Omi [L][n]; Mh [L][D2][n]
+ckks_status launch_corr_tables(ckks_ctx *ctx, uint32_t logn, uint32_t L, uint32_t D2, uint32_t hd, const double *MQ,
+                               double *Om, double *Omi, double *Mh)
 {
-    const size_t total = (size_t)L * D2 * K * jc;
-    prof_begin(ctx, K_ELEM, 8.0 * total + 8.0 * (double)L * D2 * hd);
-    hipLaunchKernelGGL(k_attn_table, grid_of(total), dim3(kThreads), 0, ctx->stream, Qt, MQ, L, D2, K, jc, hd, o0,
-                       (int)wrap);
-    prof_end(ctx, K_ELEM);
+    const uint32_t n = 1u << logn;
+    hipLaunchKernelGGL(k_attn_tw, grid_of((size_t)L * n), dim3(kThreads), 0, ctx->stream, Om, Omi, n, L,
+                       (const double *)ctx->d_twf, (const double *)ctx->d_itwf, ctx->log_n);
+    HIP_TRY(hipGetLastError());
+    if (logn == 7)
+        hipLaunchKernelGGL(k_attn_mhat<7>, dim3(L * D2), dim3(kThreads), 0, ctx->stream, Mh, MQ, hd, D2, Om, ctx->d_mod);
+    else if (logn == 8)
+        hipLaunchKernelGGL(k_attn_mhat<8>, dim3(L * D2), dim3(kThreads), 0, ctx->stream, Mh, MQ, hd, D2, Om, ctx->d_mod);
+    else if (logn == 6)
+        hipLaunchKernelGGL(k_attn_mhat<6>, dim3(L * D2), dim3(kThreads), 0, ctx->stream, Mh, MQ, hd, D2, Om, ctx->d_mod);
+    else if (logn == 5)
+        hipLaunchKernelGGL(k_attn_mhat<5>, dim3(L * D2), dim3(kThreads), 0, ctx->stream, Mh, MQ, hd, D2, Om, ctx->d_mod);
+    else if (logn == 4)
+        hipLaunchKernelGGL(k_attn_mhat<4>, dim3(L * D2), dim3(kThreads), 0, ctx->stream, Mh, MQ, hd, D2, Om, ctx->d_mod);
+    else
+        return set_error(CKKS_EUNSUPPORTED, "attention: correlation length 2^%u outside [16, 256]", logn);
+    HIP_TRY(hipGetLastError());
+    return CKKS_OK;
+}
+
+// out[e] (e < nout, stride ctw) = z[(sgn e + off) mod n] of the T inputs x (stride ctw), L limbs
+ckks_status launch_corr(ckks_ctx *ctx, uint64_t *out, const uint64_t *x, uint32_t T, uint32_t nout, int sgn, int off,
+                        uint32_t L, uint32_t logn, uint32_t logT, uint32_t D2, const double *Om, const double *Omi,
+                        const double *Mh)
+{
+    const size_t ctw = 2 * (size_t)L * ctx->n;
+    const uint32_t n = 1u << logn;
+    const dim3 grid(L * 2 * (uint32_t)(ctx->n / kCorrP));
+    const double res = 2.0 * L * ctx->n;
+    // the inputs once, the outputs once; two transforms and a product per position
+    prof_begin(ctx, K_ATTN_CORR, 8.0 * res * (T + nout), res * (n * logn * 11.0 + 8.0 * n));
+#define CK_CORR(LG)                                                                                                \
+    hipLaunchKernelGGL((k_attn_corr<LG, kCorrP>), grid, dim3(kThreads), 0, ctx->stream, out, x, T, nout, sgn, off, \
+                       ctw, L, ctx->log_n, logT, D2, Om, Omi, Mh, ctx->d_mod)
+    switch (logn) {
+    case 4: CK_CORR(4); break;
+    case 5: CK_CORR(5); break;
+    case 6: CK_CORR(6); break;
+    case 7: CK_CORR(7); break;
+    case 8: CK_CORR(8); break;
+    default: prof_end(ctx, K_ATTN_CORR); return set_error(CKKS_EUNSUPPORTED, "attention: correlation length %u", n);
+    }
+#undef CK_CORR
+    prof_end(ctx, K_ATTN_CORR);
     HIP_TRY(hipGetLastError());
     return CKKS_OK;
 }
@@ -151,32 +306,30 @@ ckks_status launch_tensor_acc(ckks_ctx *ctx, uint64_t *d, const uint64_t *E, con
     return CKKS_OK;
 }
 
-// Shape checks shared by both calls: T tokens (a power of two in [16, 128]: the runs of the mask plaintexts
-// are T positions long, the matrix-core tile's range), head dimension hd (a power of two, T <= hd <= D,
-// dividing D), D <= 256 features (the periodic encode's limit).
+// Shape checks shared by both calls: T tokens (a power of two, at most 128), head dimension hd (a power of
+// two with max(T, 16) <= hd <= 128, dividing D: the correlations have length hd and 2hd <= 256), D <= 256
+// features (the periodic encode's limit).
 ckks_status attn_check_shape(const ckks_ctx *ctx, const ckks_attn_shape *shape, const char *what, uint32_t *Dout,
                              uint32_t *logTout)
 {
     CK_REQUIRE(shape, CKKS_EINVAL, "%s: null shape", what);
     const uint32_t T = shape->tokens, hd = shape->head_dim, slots = (uint32_t)(ctx->n / 2);
-    CK_REQUIRE(T >= 16 && T <= 128 && (T & (T - 1)) == 0 && slots % T == 0, CKKS_EUNSUPPORTED,
-               "%s: %u tokens (a power of two in [16, 128] dividing %u slots)", what, T, slots);
+    CK_REQUIRE(T >= 2 && T <= 128 && (T & (T - 1)) == 0 && slots % T == 0, CKKS_EUNSUPPORTED,
+               "%s: %u tokens (a power of two in [2, 128] dividing %u slots)", what, T, slots);
     const uint32_t D = slots / T;
     CK_REQUIRE(D <= 256, CKKS_EUNSUPPORTED, "%s: %u features per ciphertext (at most 256)", what, D);
-    CK_REQUIRE(hd >= T && hd <= D && (hd & (hd - 1)) == 0, CKKS_EINVAL,
-               "%s: head dimension %u (a power of two with %u <= hd <= %u)", what, hd, T, D);
+    CK_REQUIRE(hd >= T && hd >= 16 && hd <= 128 && hd <= D && (hd & (hd - 1)) == 0, CKKS_EINVAL,
+               "%s: head dimension %u (a power of two with max(%u, 16) <= hd <= min(%u, 128))", what, hd, T, D);
     CK_REQUIRE(ctx->n_p > 0, CKKS_EUNSUPPORTED, "%s: the context has no special primes", what);
-    uint32_t logT = 0;
-    while ((1u << logT) < T) logT++;
     *Dout = D;
-    *logTout = logT;
+    *logTout = log2u(T);
     return CKKS_OK;
 }
 
 // Scratch of the scores call for inputs of L limbs (words)
 struct ScoreScratch {
-    uint32_t Jt, kt_pad;
-    size_t u_w, mq_w, b_w, a_w, d_w, pr_w, xd_w, qt_w, acc_w, rot_w, tot_w, work_w, total;
+    uint32_t Jt, logn;
+    size_t u_w, mq_w, tw_w, mh_w, b_w, a_w, d_w, pr_w, ub_w, rot_w, tot_w, work_w, total;
 };
 
 ScoreScratch score_scratch(const ckks_ctx *ctx, uint32_t L, uint32_t D, uint32_t T, uint32_t hd)
@@ -184,29 +337,30 @@ ScoreScratch score_scratch(const ckks_ctx *ctx, uint32_t L, uint32_t D, uint32_t
     ScoreScratch s{};
     const size_t N = ctx->n, ctw = 2 * (size_t)L * N, ctw1 = 2 * (size_t)(L - 1) * N;
     const uint32_t level = L - 1;
-    s.Jt = std::min(hd, mac_max_outputs());
-    s.kt_pad = mac_kt_pad(T);
+    s.Jt = kRotChunk;
+    s.logn = log2u(hd);
     s.u_w = (size_t)hd * D;
     s.mq_w = (size_t)(L - 1) * 2 * D * hd;
+    s.tw_w = (size_t)2 * (L - 1) * hd;
+    s.mh_w = (size_t)(L - 1) * 2 * D * hd;
     s.b_w = s.a_w = s.pr_w = (size_t)T * ctw;
     s.d_w = (size_t)T * 3 * L * N;
-    s.xd_w = (mac_digit_bytes(ctx, L - 1, s.kt_pad) + 7) / 8;
-    s.qt_w = (size_t)(L - 1) * 2 * D * T * s.Jt;
-    s.acc_w = s.rot_w = (size_t)s.Jt * ctw1;
+    s.ub_w = (size_t)hd * ctw1;
+    s.rot_w = (size_t)s.Jt * ctw1;
     s.tot_w = ctw1;
     s.work_w = std::max({ks_scratch_words(ctx, level, ks_rot_batch(T - 1)),
                          ks_scratch_words(ctx, level, ks_rot_batch(T), T),
                          ks_scratch_words(ctx, level - 1, ks_rot_batch(s.Jt), s.Jt),
                          (size_t)2 * T * (1 + level) * N});
-    s.total = s.u_w + s.mq_w + s.b_w + s.a_w + s.d_w + s.pr_w + s.xd_w + s.qt_w + s.acc_w + s.rot_w + s.tot_w +
+    s.total = s.u_w + s.mq_w + s.tw_w + s.mh_w + s.b_w + s.a_w + s.d_w + s.pr_w + s.ub_w + s.rot_w + s.tot_w +
               s.work_w;
     return s;
 }
 
 // Scratch of the weighted-sum call for scores of Lp limbs and values of Lv limbs (words)
 struct ApplyScratch {
-    uint32_t Jt, kt_pad, nj;
-    size_t u_w, mq_w, r_w, xd_w, qt_w, cacc_w, ctmp_w, c_w, e_w, d_w, o_w, work_w, total;
+    uint32_t Jt, nj, logn;
+    size_t u_w, mq_w, tw_w, mh_w, r_w, cb_w, ctmp_w, c_w, e_w, d_w, o_w, work_w, total;
 };
 
 ApplyScratch apply_scratch(const ckks_ctx *ctx, uint32_t Lp, uint32_t Lv, uint32_t D, uint32_t T, uint32_t hd)
@@ -214,15 +368,15 @@ ApplyScratch apply_scratch(const ckks_ctx *ctx, uint32_t Lp, uint32_t Lv, uint32
     ApplyScratch s{};
     const size_t N = ctx->n;
     const uint32_t lv = Lv - 1, lp = Lp - 1;
-    s.Jt = std::min(hd + T - 1, mac_max_outputs());
-    s.kt_pad = mac_kt_pad(T);
+    s.Jt = kRotChunk;
     s.nj = hd + T - 1;
+    s.logn = log2u(2 * hd);
     s.u_w = (size_t)hd * D;
     s.mq_w = (size_t)Lv * 2 * D * hd;
+    s.tw_w = (size_t)2 * Lv * 2 * hd;
+    s.mh_w = (size_t)Lv * 2 * D * 2 * hd;
     s.r_w = (size_t)T * 2 * Lv * N;
-    s.xd_w = (mac_digit_bytes(ctx, Lv, s.kt_pad) + 7) / 8;
-    s.qt_w = (size_t)Lv * 2 * D * T * s.Jt;
-    s.cacc_w = (size_t)s.Jt * 2 * Lv * N;
+    s.cb_w = (size_t)s.nj * 2 * Lv * N;
     s.ctmp_w = (size_t)s.Jt * 2 * (Lv - 1) * N;
     s.c_w = s.e_w = (size_t)s.nj * 2 * Lp * N;
     s.d_w = (size_t)3 * Lp * N;
@@ -232,7 +386,7 @@ ApplyScratch apply_scratch(const ckks_ctx *ctx, uint32_t Lp, uint32_t Lv, uint32
     s.work_w = std::max({ks_scratch_words(ctx, lv, ks_rot_batch(T - 1)),
                          ks_scratch_words(ctx, lp, ks_rot_batch(s.nj - 1)), (size_t)2 * s.Jt * (1 + lv) * N,
                          relin_w, (size_t)2 * (1 + lp) * N});
-    s.total = s.u_w + s.mq_w + s.r_w + s.xd_w + s.qt_w + s.cacc_w + s.ctmp_w + s.c_w + s.e_w + s.d_w + s.o_w +
+    s.total = s.u_w + s.mq_w + s.tw_w + s.mh_w + s.r_w + s.cb_w + s.ctmp_w + s.c_w + s.e_w + s.d_w + s.o_w +
               s.work_w;
     return s;
 }
@@ -330,24 +484,26 @@ extern "C" ckks_status ckks_attention_scores(ckks_ctx *ctx, const ckks_buf *q, u
     CK_TRY(ctx_scratch(ctx, ss.total * 8, &w));
     double *U = (double *)w;
     double *MQ = U + ss.u_w;
-    uint64_t *B = (uint64_t *)(MQ + ss.mq_w);   // [T][2][L][N] rotated keys
-    uint64_t *A = B + ss.b_w;                   // [T][2][L][N] rotated queries, then P_delta ([T][2][L-1][N])
-    uint64_t *Dt = A + ss.a_w;                  // [T][3][L][N] products
-    uint64_t *Pr = Dt + ss.d_w;                 // [T][2][L][N] relinearised products
-    int8_t *Xd = (int8_t *)(Pr + ss.pr_w);
-    double *Qt = (double *)((uint64_t *)Xd + ss.xd_w);
-    uint64_t *acc = (uint64_t *)(Qt + ss.qt_w);  // [Jt][2][L-1][N]
-    uint64_t *rot = acc + ss.acc_w;
+    double *Om = MQ + ss.mq_w, *Omi = Om + ss.tw_w / 2;
+    double *Mh = Om + ss.tw_w;
+    uint64_t *B = (uint64_t *)(Mh + ss.mh_w);  // [T][2][L][N] rotated keys
+    uint64_t *A = B + ss.b_w;                  // [T][2][L][N] rotated queries, then P_delta ([T][2][L-1][N])
+    uint64_t *Dt = A + ss.a_w;                 // [T][3][L][N] products
+    uint64_t *Pr = Dt + ss.d_w;                // [T][2][L][N] relinearised products
+    uint64_t *Ub = Pr + ss.pr_w;               // [hd][2][L-1][N] U_k
+    uint64_t *rot = Ub + ss.ub_w;              // [Jt][2][L-1][N]
     uint64_t *tot = rot + ss.rot_w;
     uint64_t *work = tot + ss.tot_w;
 
-    // the masks at scale q_(level-1): the products are multiplied by them after their first rescale
+    // the masks at scale q_(level-1) (the products are multiplied by them after their first rescale), and
+    // their correlation form
     CK_TRY(launch_masks(ctx, U, MQ, D, hd, (double)ctx->primes[level - 1], L - 1));
+    CK_TRY(launch_corr_tables(ctx, ss.logn, L - 1, 2 * D, hd, MQ, Om, Omi, Mh));
     // queries grouped by key: each key's rotations are computed once
     std::vector<uint32_t> order(n_q);
     for (uint32_t c = 0; c < n_q; c++) order[c] = c;
     std::stable_sort(order.begin(), order.end(), [&](uint32_t a, uint32_t b) { return k_of_q[a] < k_of_q[b]; });
-    std::vector<uint64_t *> outs(T);
+    std::vector<uint64_t *> outs(std::max(T, ss.Jt));
     uint32_t cur_k = UINT32_MAX;
     for (uint32_t c : order) {
         const uint32_t kk = k_of_q[c];
@@ -393,20 +549,16 @@ extern "C" ckks_status ckks_attention_scores(ckks_ctx *ctx, const ckks_buf *q, u
         }
         uint64_t *Pd = A;  // [T][2][L-1][N]
         CK_TRY(rescale_many(ctx, Pr, T, level, Pd, work));
-        // 3. U_k = sum_delta M_{(delta + k) mod hd} P_delta on the matrix cores, tiles of Jt values of k; each
-        //    tile rotated by its k and summed
-        CK_TRY(launch_xdigits(ctx, Pd, Xd, L - 1, T, ss.kt_pad));
-        for (uint32_t k0 = 0; k0 < hd; k0 += ss.Jt) {
-            const uint32_t jc = std::min(ss.Jt, hd - k0);
-            CK_TRY(launch_table(ctx, Qt, MQ, L - 1, 2 * D, T, jc, hd, (int)k0, true));
-            CK_TRY(launch_mac_mfma(ctx, acc, Xd, Qt, jc, T, 0, ss.kt_pad, 2 * D, L - 1, logT, false));
-            const uint32_t first = k0 == 0 ? 1 : 0;  // k = 0 needs no rotation
-            std::vector<uint64_t *> ro(jc);
-            for (uint32_t jj = 0; jj < jc; jj++) ro[jj] = rot + (size_t)jj * ctw1;
-            CK_TRY(rotate_each(ctx, acc + (size_t)first * ctw1, ctw1, jc - first, level - 1,
-                               osteps.data() + (k0 + first - 1), okeys.data() + (k0 + first - 1), ro.data(), work));
-            if (k0 == 0) CK_TRY(launch_sum_cts(ctx, tot, acc, 1, ctw1, L - 1, false));
-            CK_TRY(launch_sum_cts(ctx, tot, rot, jc - first, ctw1, L - 1, true));
+        // 3. U_k = sum_delta M_{(delta + k) mod hd} P_delta = z[-k mod hd] for every k, then each rotated by k
+        //    (in chunks) and summed
+        CK_TRY(launch_corr(ctx, Ub, Pd, T, hd, -1, 0, L - 1, ss.logn, logT, 2 * D, Om, Omi, Mh));
+        CK_TRY(launch_sum_cts(ctx, tot, Ub, 1, ctw1, L - 1, false));
+        for (uint32_t k0 = 1; k0 < hd; k0 += ss.Jt) {
+            const uint32_t cnt = std::min(ss.Jt, hd - k0);
+            for (uint32_t r = 0; r < cnt; r++) outs[r] = rot + (size_t)r * ctw1;
+            CK_TRY(rotate_each(ctx, Ub + (size_t)k0 * ctw1, ctw1, cnt, level - 1, osteps.data() + (k0 - 1),
+                               okeys.data() + (k0 - 1), outs.data(), work));
+            CK_TRY(launch_sum_cts(ctx, tot, rot, cnt, ctw1, L - 1, true));
         }
         // 4. the final rescale
         CK_TRY(rescale_core(ctx, tot, level - 1, out[c].data, work));
@@ -462,19 +614,20 @@ extern "C" ckks_status ckks_attention_apply(ckks_ctx *ctx, const ckks_buf *p, ui
     CK_TRY(ctx_scratch(ctx, ss.total * 8, &w));
     double *U = (double *)w;
     double *MQ = U + ss.u_w;
-    uint64_t *R = (uint64_t *)(MQ + ss.mq_w);    // [T][2][Lv][N]
-    int8_t *Xd = (int8_t *)(R + ss.r_w);
-    double *Qt = (double *)((uint64_t *)Xd + ss.xd_w);
-    uint64_t *cacc = (uint64_t *)(Qt + ss.qt_w);  // [Jt][2][Lv][N]
-    uint64_t *ctmp = cacc + ss.cacc_w;            // [Jt][2][Lv-1][N]
-    uint64_t *C = ctmp + ss.ctmp_w;               // [nj][2][Lp][N], index j + hd - 1
-    uint64_t *E = C + ss.c_w;                     // [nj][2][Lp][N]
-    uint64_t *Dacc = E + ss.e_w;                  // [3][Lp][N]
-    uint64_t *O = Dacc + ss.d_w;                  // [2][Lp][N]
+    double *Om = MQ + ss.mq_w, *Omi = Om + ss.tw_w / 2;
+    double *Mh = Om + ss.tw_w;
+    uint64_t *R = (uint64_t *)(Mh + ss.mh_w);  // [T][2][Lv][N]
+    uint64_t *Cb = R + ss.r_w;                 // [nj][2][Lv][N] C_j before the rescale
+    uint64_t *ctmp = Cb + ss.cb_w;             // [Jt][2][Lv-1][N]
+    uint64_t *C = ctmp + ss.ctmp_w;            // [nj][2][Lp][N], index j + hd - 1
+    uint64_t *E = C + ss.c_w;                  // [nj][2][Lp][N]
+    uint64_t *Dacc = E + ss.e_w;               // [3][Lp][N]
+    uint64_t *O = Dacc + ss.d_w;               // [2][Lp][N]
     uint64_t *work = O + ss.o_w;
 
     // masks at scale q_(level of the values): C_j is rescaled by that prime
     CK_TRY(launch_masks(ctx, U, MQ, D, hd, (double)ctx->primes[lv], Lv));
+    CK_TRY(launch_corr_tables(ctx, ss.logn, Lv, 2 * D, hd, MQ, Om, Omi, Mh));
     std::vector<uint32_t> order(n_p);
     for (uint32_t c = 0; c < n_p; c++) order[c] = c;
     std::stable_sort(order.begin(), order.end(), [&](uint32_t a, uint32_t b) { return v_of_p[a] < v_of_p[b]; });
@@ -487,20 +640,17 @@ extern "C" ckks_status ckks_attention_apply(ckks_ctx *ctx, const ckks_buf *p, ui
             HIP_TRY(hipMemcpyAsync(R, v[vv].data, ctwv * 8, hipMemcpyDeviceToDevice, ctx->stream));
             for (uint32_t d = 1; d < T; d++) outs[d - 1] = R + (size_t)d * ctwv;
             CK_TRY(rotate_core(ctx, v[vv].data, lv, vsteps.data(), vkeys.data(), T - 1, outs.data(), work));
-            // 2. C_j on the matrix cores in tiles of Jt values of j, rescaled, kept on the scores' limbs
-            CK_TRY(launch_xdigits(ctx, R, Xd, Lv, T, ss.kt_pad));
-            for (uint32_t j0 = 0; j0 < ss.nj; j0 += ss.Jt) {
-                const uint32_t jc = std::min(ss.Jt, ss.nj - j0);
-                const int o0 = (int)j0 - (int)hd + 1;
-                CK_TRY(launch_table(ctx, Qt, MQ, Lv, 2 * D, T, jc, hd, o0, false));
-                CK_TRY(launch_mac_mfma(ctx, cacc, Xd, Qt, jc, T, 0, ss.kt_pad, 2 * D, Lv, logT, false));
-                uint64_t *dst = C + (size_t)j0 * ctwp;
+            // 2. C_j (index e = j + hd - 1) = z[j mod 2hd], rescaled in chunks and kept on the scores' limbs
+            CK_TRY(launch_corr(ctx, Cb, R, T, ss.nj, 1, -(int)(hd - 1), Lv, ss.logn, logT, 2 * D, Om, Omi, Mh));
+            for (uint32_t e0 = 0; e0 < ss.nj; e0 += ss.Jt) {
+                const uint32_t cnt = std::min(ss.Jt, ss.nj - e0);
+                uint64_t *dst = C + (size_t)e0 * ctwp;
                 if (Lp == Lv - 1) {
-                    CK_TRY(rescale_many(ctx, cacc, jc, lv, dst, work));
+                    CK_TRY(rescale_many(ctx, Cb + (size_t)e0 * ctwv, cnt, lv, dst, work));
                 } else {
-                    CK_TRY(rescale_many(ctx, cacc, jc, lv, ctmp, work));
+                    CK_TRY(rescale_many(ctx, Cb + (size_t)e0 * ctwv, cnt, lv, ctmp, work));
                     HIP_TRY(hipMemcpy2DAsync(dst, (size_t)Lp * N * 8, ctmp, (size_t)(Lv - 1) * N * 8,
-                                             (size_t)Lp * N * 8, 2 * jc, hipMemcpyDeviceToDevice, ctx->stream));
+                                             (size_t)Lp * N * 8, 2 * cnt, hipMemcpyDeviceToDevice, ctx->stream));
                 }
             }
             cur_v = vv;

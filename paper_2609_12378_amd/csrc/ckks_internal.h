@@ -65,7 +65,7 @@ struct ConvDev {
 // and constant tables, which stay cache-resident, are not counted).
 enum KClass {
     K_NTT_FWD_COL = 0, K_NTT_FWD_ROW, K_NTT_INV_ROW, K_NTT_INV_COL, K_FFT_A, K_FFT_B, K_GATHER, K_TO_RNS,
-    K_MAC, K_KEYIP, K_CONV, K_MODDOWN, K_ELEM, K_ROW_MAC, K_ENC_TM, K_MAC_TM, K_NCLASS
+    K_MAC, K_KEYIP, K_CONV, K_MODDOWN, K_ELEM, K_ROW_MAC, K_ENC_TM, K_MAC_TM, K_ATTN_CORR, K_NCLASS
 };
 extern const char *const kKClassNames[K_NCLASS];
 

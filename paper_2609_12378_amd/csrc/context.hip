@@ -32,7 +32,7 @@ extern "C" const char *ckks_last_error(void) { return g_err; }
 const char *const kKClassNames[K_NCLASS] = {"ntt_fwd_col", "ntt_fwd_row", "ntt_inv_row", "ntt_inv_col", "fft_a",
                                             "fft_b",       "gather",      "to_rns",      "mac",         "key_ip",
                                             "conv",        "moddown",     "elementwise", "ntt_row_mac",
-                                            "encode_tm",   "mac_tm"};
+                                            "encode_tm",   "mac_tm",     "attn_corr"};
 
 // --------------------------------------------------------------- host math --
 namespace hm {

@@ -6,7 +6,8 @@ and O[t, h, d] = sum_delta S[t, h, delta] V[(t + delta) mod T, d] within the sta
 
 * toy ring (N = 2^12, 16 tokens, two heads of 64 per ciphertext, inputs at level 5): three query
   ciphertexts on two key and two value ciphertexts, named out of order (the calls group them);
-* a ring of degree 2^13 with 32 tokens and four heads of 32 per ciphertext (another matrix-core tile shape);
+* a ring of degree 2^13 with 32 tokens and four heads of 32 per ciphertext, and the toy ring with 8 tokens
+  and four heads of 64 (several mask runs per correlation block);
 * the attention parameters at full degree (N = 2^16, 24 + 8 limbs, 128 tokens, two heads of 128 per
   ciphertext, inputs at level 11, scale 2^50: the launch shapes of the benchmark), two query ciphertexts on
   one key and one value ciphertext: decrypted results against the definitions (the oracle is too slow for
@@ -125,6 +126,15 @@ def test_attention_parity_ring13_four_heads():
     assert eo <= 2.0 ** -26
 
 
+def test_attention_parity_eight_tokens():
+    # 8 tokens x 256 features (four heads of 64): runs of 8 NTT positions, several per correlation block
+    cfg = dataclasses.replace(ATTN_TOY, name="attn8", tokens=8, head_dim=64)
+    es, eo = run_parity(cfg, 1, 1, [0])
+    say("8-token attention max error: scores %.3g, sums %.3g" % (es, eo))
+    assert es <= 2.0 ** -30
+    assert eo <= 2.0 ** -28
+
+
 def _dev_keys(ctx, s_dev, steps, seed):
     """Galois and relinearisation keys from device randomness (no oracle at this degree)."""
     import torch
@@ -230,7 +240,7 @@ def test_attention_rejects_bad_arguments(toy_env):
     ctx, q, k, v, keys, rlk, T, hd, L = (t[x] for x in ("ctx", "q", "k", "v", "keys", "rlk", "T", "hd", "L"))
     out = Buf(ctx.zeros(2, L - 2), 1.0)
     with pytest.raises(CkksError, match="tokens"):
-        ctx.attention_scores([q], [k], [0], 8, hd, rlk, keys, outs=[out])
+        ctx.attention_scores([q], [k], [0], 3, hd, rlk, keys, outs=[out])
     with pytest.raises(CkksError, match="head dimension"):
         ctx.attention_scores([q], [k], [0], T, 8, rlk, keys, outs=[out])
     with pytest.raises(CkksError, match="names key"):
@@ -246,7 +256,7 @@ def test_attention_rejects_bad_arguments(toy_env):
         ctx.attention_apply([q], [v], [0], T, hd, rlk, keys, outs=[out1])
     assert not to_host(out.data).any() and not to_host(out1.data).any()
     with pytest.raises(CkksError):
-        ctx.workspace_bytes(ctx.OP_ATTN_SCORES, (L, 8, hd))
+        ctx.workspace_bytes(ctx.OP_ATTN_SCORES, (L, 3, hd))
     with pytest.raises(CkksError):
         ctx.workspace_bytes(ctx.OP_ATTN_APPLY, (L, L, T, hd))
 
