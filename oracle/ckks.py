@@ -426,8 +426,8 @@ class Ckks:
     def _key_rows(self, key: np.ndarray, level: int) -> np.ndarray:
         return key[:, :, self.ext_primes(level), :]
 
-    def keyswitch_digits(self, digits: np.ndarray, key: np.ndarray, level: int, g: Optional[int]):
-        """(u0, u1) = sum_j sigma_g(d_j) * (b_j, a_j), then ModDown of each (g None: no sigma)."""
+    def key_inner(self, digits: np.ndarray, key: np.ndarray, level: int, g: Optional[int]):
+        """(u0, u1) = sum_j sigma_g(d_j) * (b_j, a_j) over Q_level u P (g None: no sigma)."""
         ext = self.ext_primes(level)
         kr = self._key_rows(key, level)
         u = [np.zeros((len(ext), self.n), dtype=np.uint64) for _ in range(2)]
@@ -435,7 +435,32 @@ class Ckks:
             d = digits[j] if g is None else self.automorph(digits[j], g)
             for k in range(2):
                 u[k] = self.add(u[k], self.mul(d, kr[j, k], ext), ext)
+        return u
+
+    def keyswitch_digits(self, digits: np.ndarray, key: np.ndarray, level: int, g: Optional[int]):
+        """(u0, u1) = sum_j sigma_g(d_j) * (b_j, a_j), then ModDown of each (g None: no sigma)."""
+        u = self.key_inner(digits, key, level, g)
         return self.moddown(u[0], level), self.moddown(u[1], level)
+
+    def rotate_sum_lazy(self, cts: Sequence[np.ndarray], steps: Sequence[int], keys: Sequence[np.ndarray]):
+        """sum_r Rot_{steps[r]}(cts[r]) with one ModDown: the key-switching inner products of all terms are summed
+        over Q_level u P together with P * sigma_r(c0_r) (zero modulo P), and the sum is divided by P once.
+        ModDown(x + P y) = ModDown(x) + y exactly, so one term gives the rotation bit for bit; with several
+        terms only the rounding of the division differs from summing separately rotated ciphertexts (the lazy
+        ModDown across a sum of rotations of the key-switching literature, e.g. Bossuat et al. 2021)."""
+        level = self.level_of(cts[0])
+        ext = self.ext_primes(level)
+        ql = self.level_primes(level)
+        u = [np.zeros((len(ext), self.n), dtype=np.uint64) for _ in range(2)]
+        pq = [self.P % self.q[i] for i in ql]
+        for ct, st, key in zip(cts, steps, keys):
+            g = self.galois_elt(st)
+            t = self.key_inner(self.modup(ct[1], level), key, level, g)
+            c0 = self.mul_scalar(self.automorph(ct[0], g), pq, ql)
+            u[0] = self.add(u[0], t[0], ext)
+            u[1] = self.add(u[1], t[1], ext)
+            u[0][:level + 1] = self.add(u[0][:level + 1], c0, ql)
+        return np.stack([self.moddown(u[0], level), self.moddown(u[1], level)])
 
     # ---------------- ciphertext operations ----------------
     @staticmethod
@@ -528,7 +553,8 @@ class Ckks:
         return np.where(wraps, 0.0, vals), np.where(wraps, vals, 0.0)
 
     def linear_project_tm(self, cts: Sequence[np.ndarray], W: np.ndarray, T: int, n1: int,
-                          keys: Dict[int, np.ndarray], out_blocks: Optional[Sequence[int]] = None):
+                          keys: Dict[int, np.ndarray], out_blocks: Optional[Sequence[int]] = None,
+                          lazy: bool = False):
         """The projection in the token-major layout s = t*D + f (input i holds features [iD, (i+1)D) of every
         token):
             out_j = Rescale( sum_g Rot_{n1 g}( sum_{i,b} U_{j,i,g,b} * Rot_b(x_i) + V_{j,i,g,b} * Rot_{b-D}(x_i) ) )
@@ -559,10 +585,8 @@ class Ckks:
                         for vec, x in ((uu, xr[i][b]), (vv, xw[i][b])):
                             term = self.ct_mul_plain(x, self.encode_periodic(vec, delta_w, level + 1))
                             acc = term if acc is None else self.ct_add(acc, term)
-                if g > 0:
-                    acc = self.rotate(acc, n1 * g, keys[n1 * g])
-                total = acc if total is None else self.ct_add(total, acc)
-            outs.append(self.rescale(total))
+                total = self._giant_step(total, acc, g, n1 * g, keys, lazy)
+            outs.append(self.rescale(self._giant_finish(total, lazy)))
         return outs
 
     # ---------------- the attention block (token-major) ----------------
@@ -574,7 +598,7 @@ class Ckks:
         return u
 
     def attention_scores(self, q_cts: Sequence[np.ndarray], k_cts: Sequence[np.ndarray], k_of_q: Sequence[int],
-                         T: int, hd: int, rlk: np.ndarray, keys: Dict[int, np.ndarray]):
+                         T: int, hd: int, rlk: np.ndarray, keys: Dict[int, np.ndarray], lazy: bool = False):
         """Scores of one attention block in the token-major layout s = t*D + f, heads of hd features.
 
         Query ciphertext c holds D/hd heads, slot t*D + h*hd + d = Q[t, h, d]; key ciphertext k_of_q[c] holds
@@ -589,7 +613,8 @@ class Ckks:
         Q[t, h, d] K[t + delta, d]; M_c selects head position c, so the term k brings position delta + k of
         P_delta to position delta: the sum over k is the dot product over d, placed at position delta.
         The masks are periodic plaintexts encoded at scale q_(level-1), so the output scale is
-        scale(Q) scale(K) / q_level.  Keys: -delta and delta (D - 1) (0 < delta < T), k (0 < k < hd)."""
+        scale(Q) scale(K) / q_level.  Keys: -delta and delta (D - 1) (0 < delta < T), k (0 < k < hd).  With `lazy`
+        the hd - 1 rotations of the outer sum share one ModDown (rotate_sum_lazy)."""
         level = self.level_of(q_cts[0])
         D = (self.n // 2) // T
         assert T <= hd and D % hd == 0 and level >= 2
@@ -612,10 +637,8 @@ class Ckks:
                 for d in range(T):
                     term = self.ct_mul_plain(P[d], masks[(d + k) % hd])
                     U = term if U is None else self.ct_add(U, term)
-                if k > 0:
-                    U = self.rotate(U, k, keys[k])
-                total = U if total is None else self.ct_add(total, U)
-            outs.append(self.rescale(total))
+                total = self._giant_step(total, U, k, k, keys, lazy)
+            outs.append(self.rescale(self._giant_finish(total, lazy)))
         return outs
 
     def attention_apply(self, p_cts: Sequence[np.ndarray], v_cts: Sequence[np.ndarray], v_of_p: Sequence[int],
@@ -667,11 +690,13 @@ class Ckks:
         return outs
 
     def linear_project(self, cts: Sequence[np.ndarray], W: np.ndarray, T: int, n1: int,
-                       keys: Dict[int, np.ndarray], out_blocks: Optional[Sequence[int]] = None):
+                       keys: Dict[int, np.ndarray], out_blocks: Optional[Sequence[int]] = None,
+                       lazy: bool = False):
         """out_j = Rescale( sum_g Rot_{T n1 g}( sum_{i,b} pt_{j,i,g,b} * Rot_{T b}(x_i) ) ).
 
         Plaintext scale is q_level, so the rescale returns the ciphertext scale unchanged.
-        `out_blocks` restricts the computation to the listed output ciphertexts."""
+        `out_blocks` restricts the computation to the listed output ciphertexts; `lazy` sums the giant-step
+        rotations with one ModDown (rotate_sum_lazy)."""
         level = self.level_of(cts[0])
         idx = self.level_primes(level)
         D = (self.n // 2) // T
@@ -697,8 +722,26 @@ class Ckks:
                         pt = self.encode(z, None, delta_w, level + 1)
                         term = self.ct_mul_plain(xrot[i][b], pt)
                         acc = term if acc is None else self.ct_add(acc, term)
-                if g > 0:
-                    acc = self.rotate(acc, T * n1 * g, keys[T * n1 * g])
-                total = acc if total is None else self.ct_add(total, acc)
-            outs.append(self.rescale(total))
+                total = self._giant_step(total, acc, g, T * n1 * g, keys, lazy)
+            outs.append(self.rescale(self._giant_finish(total, lazy)))
         return outs
+
+    def _giant_step(self, total, acc, g: int, step: int, keys, lazy: bool):
+        """Add the giant-step partial sum acc (rotated by step for g > 0) to total; with lazy, total is
+        (partial sum of g = 0, [rotated terms]) and the rotations are summed by _giant_finish."""
+        if lazy:
+            if g == 0:
+                return (acc, [], [], [])
+            total[1].append(acc)
+            total[2].append(step)
+            total[3].append(keys[step])
+            return total
+        if g > 0:
+            acc = self.rotate(acc, step, keys[step])
+        return acc if total is None else self.ct_add(total, acc)
+
+    def _giant_finish(self, total, lazy: bool):
+        if not lazy:
+            return total
+        base, terms, steps, ks = total
+        return self.ct_add(base, self.rotate_sum_lazy(terms, steps, ks)) if terms else base

@@ -158,7 +158,8 @@ def toy_attention():
     keys, rlk = attn_keys(ck, s, T, D, hd, rng(cfg.index, 5))
     S = ck.attention_scores([q_ct], [k_ct], [0], T, hd, rlk, keys)[0]
     O = ck.attention_apply([S], [v_ct], [0], T, hd, rlk, keys)[0]
-    return dict(ck=ck, s=s, Q=Q, K=K, V=V, S=S, O=O, delta=delta, T=T, D=D, hd=hd)
+    S_lazy = ck.attention_scores([q_ct], [k_ct], [0], T, hd, rlk, keys, lazy=True)[0]
+    return dict(ck=ck, s=s, Q=Q, K=K, V=V, S=S, O=O, S_lazy=S_lazy, delta=delta, T=T, D=D, hd=hd)
 
 
 def test_toy_attention_scores_accuracy(toy_attention):
@@ -185,3 +186,16 @@ def test_toy_attention_apply_accuracy(toy_attention):
     want = apply_def(S, t["V"], T, D, hd)
     err = np.max(np.abs(z.real.reshape(T, D) - want))
     assert err < 2.0 ** -28, err
+
+
+def test_toy_attention_scores_lazy_outer_sum(toy_attention):
+    """The outer sum's hd - 1 rotations with one ModDown: before the final rescale the sum differs from the eager
+    one by a few units per coefficient (the conversion digits' wrap), which the division by q rounds away except
+    within a few units of a rounding boundary; the accuracy is the same."""
+    t = toy_attention
+    ck, T, D, hd = t["ck"], t["T"], t["D"], t["hd"]
+    assert t["S_lazy"].shape == t["S"].shape
+    scale = t["delta"] * t["delta"] / ck.q[ATTN_TOY.level]
+    z = ck.decode(ck.decrypt(t["s"], t["S_lazy"]), scale)
+    err = np.max(np.abs(z.real.reshape(T, D) - scores_def(t["Q"], t["K"], T, D, hd)))
+    assert err < 2.0 ** -30, err

@@ -152,11 +152,12 @@ def toy_tm_projection():
         e = gaussian_error(gk, (ck.dnum, ck.n))
         keys[st] = ck.keygen_galois(s, ck.galois_elt(st), a, e)
     outs = ck.linear_project_tm(cts, W, T, n1, keys, out_blocks=[0, 2])
-    return ck, s, X, W, outs, delta
+    lazy = ck.linear_project_tm(cts, W, T, n1, keys, out_blocks=[0], lazy=True)
+    return ck, s, X, W, outs, delta, lazy
 
 
 def test_toy_tm_projection_accuracy(toy_tm_projection):
-    ck, s, X, W, outs, delta = toy_tm_projection
+    ck, s, X, W, outs, delta, _ = toy_tm_projection
     T, D = TOY.tokens, TOY.feats
     Y = X @ W
     for j, ct in zip([0, 2], outs):
@@ -165,3 +166,13 @@ def test_toy_tm_projection_accuracy(toy_tm_projection):
         err = np.max(np.abs(z.real - tm_pack(Y, T, D, j)))
         assert err <= 2.0 ** -12, err
         assert np.max(np.abs(z.imag)) <= 2.0 ** -12
+
+
+def test_toy_tm_projection_lazy_giant_steps(toy_tm_projection):
+    """The giant-step rotations summed with one ModDown (the division by P rounds once instead of per rotation;
+    the final rescale absorbs the difference except near a rounding boundary): the same accuracy."""
+    ck, s, X, W, outs, delta, lazy = toy_tm_projection
+    T, D = TOY.tokens, TOY.feats
+    assert lazy[0].shape == outs[0].shape
+    z = ck.decode(ck.decrypt(s, lazy[0]), delta)
+    assert np.max(np.abs(z.real - tm_pack(X @ W, T, D, 0))) <= 2.0 ** -12

@@ -121,6 +121,38 @@ def test_hoisted_equals_single_rotations(toy):
         assert np.array_equal(h, ck.rotate(ct, r, k))
 
 
+def test_lazy_rotation_sum_single_term_is_the_rotation(toy):
+    # ModDown(x + P y) = ModDown(x) + y exactly: one term of the lazy sum is the rotation bit for bit
+    ck, s = toy
+    for lvl, st in ((3, 5), (2, -3)):
+        ct = _enc(ck, s, _z(ck, 40 + lvl), DELTA, 40 + lvl, level=lvl)
+        a, e = _keys(ck, s, 41 + lvl)
+        key = ck.keygen_galois(s, ck.galois_elt(st), a, e)
+        assert np.array_equal(ck.rotate_sum_lazy([ct], [st], [key]), ck.rotate(ct, st, key))
+
+
+def test_lazy_rotation_sum_decrypts_to_the_sum(toy):
+    ck, s = toy
+    steps = [1, 7, -16, 300]
+    zs = [_z(ck, 50 + i) for i in range(len(steps))]
+    cts = [_enc(ck, s, z, DELTA, 50 + i) for i, z in enumerate(zs)]
+    keys = []
+    for i, r in enumerate(steps):
+        a, e = _keys(ck, s, 60 + i)
+        keys.append(ck.keygen_galois(s, ck.galois_elt(r), a, e))
+    lazy = ck.rotate_sum_lazy(cts, steps, keys)
+    want = sum(np.roll(z, -r) for z, r in zip(zs, steps))
+    # the encryption errors of four inputs and four key-switching errors, one rounding of the division
+    bound = 4 * ck.n * 20 / DELTA + 4 * ks_bound(ck, 3, DELTA)
+    assert np.max(np.abs(_dec(ck, s, lazy, DELTA) - want)) < bound
+    eager = ck.rotate(cts[0], steps[0], keys[0])
+    for ct, r, k in zip(cts[1:], steps[1:], keys[1:]):
+        eager = ck.ct_add(eager, ck.rotate(ct, r, k))
+    # the two forms differ only in the rounding of the divisions by P
+    assert not np.array_equal(lazy, eager)
+    assert np.max(np.abs(_dec(ck, s, lazy, DELTA) - _dec(ck, s, eager, DELTA))) < 4 * ks_bound(ck, 3, DELTA)
+
+
 def test_rotation_composes(toy):
     ck, s = toy
     z = _z(ck, 8)
