@@ -27,6 +27,16 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 METRIC = "rotations/s at N=2^16 (keyswitch) and s per 4096x14336 ct-pt projection"
+# sums of rotations (giant steps, the attention outer sum) with one ModDown per output (--lazy-moddown)
+LAZY = {"on": False}
+
+
+def make_context(cfg, n_p=None, dnum=None):
+    from paper_2609_12378_amd import Context
+    ctx = Context(cfg.log_n, cfg.n_q, cfg.n_p if n_p is None else n_p, cfg.dnum if dnum is None else dnum,
+                  q_bits=cfg.q_bits)
+    ctx.set_lazy_moddown(LAZY["on"])
+    return ctx
 HBM_PEAK_GBS = 8000.0
 # 256 CUs x 64 lanes x 2.4 GHz of VALU issue (fp64 FMA and 32-bit integer ops are full rate)
 LANE_OPS = 256 * 64 * 2.4e9
@@ -58,10 +68,9 @@ class Timer:
 
 
 def setup_projection(torch, np, cfg):
-    from paper_2609_12378_amd import Context
     from workloads import (gaussian_error, gaussian_weights, rng, ternary_secret, uniform_residues,
                            uniform_slots)
-    ctx = Context(cfg.log_n, cfg.n_q, cfg.n_p, cfg.dnum, q_bits=cfg.q_bits)
+    ctx = make_context(cfg)
     n, T, D, level, n1 = ctx.n, cfg.tokens, cfg.feats, cfg.level, cfg.n1
     n2 = -(-D // n1)
     s = torch.from_numpy(ternary_secret(rng(cfg.index, 3), n)).cuda()
@@ -93,10 +102,9 @@ def tm_pack(X, T, D, i):
 
 def setup_projection_tm(torch, np, cfg, n1):
     """Inputs and keys of the token-major projection (slot t*D + f): steps b, b - D (0 <= b < n1) and n1 g."""
-    from paper_2609_12378_amd import Context
     from workloads import (gaussian_error, gaussian_weights, rng, ternary_secret, uniform_residues,
                            uniform_slots)
-    ctx = Context(cfg.log_n, cfg.n_q, cfg.n_p, cfg.dnum, q_bits=cfg.q_bits)
+    ctx = make_context(cfg)
     n, T, level = ctx.n, cfg.tokens, cfg.level
     D = (n // 2) // T
     n2 = -(-D // n1)
@@ -199,7 +207,7 @@ def bench_attention(torch, np, steps, warmup):
     from paper_2609_12378_amd import Context
     from workloads import ATTENTION as cfg, gaussian_error, gaussian_weights, rng, ternary_secret, \
         uniform_residues, uniform_slots
-    ctx = Context(cfg.log_n, cfg.n_q, cfg.n_p, cfg.dnum, q_bits=cfg.q_bits)
+    ctx = make_context(cfg)
     n, T, hd, level, n1 = ctx.n, cfg.tokens, cfg.head_dim, cfg.level, cfg.n1
     D = (n // 2) // T
     hpc = D // hd
@@ -363,9 +371,8 @@ def load_traffic(kernel):
 
 
 def bench_keyswitch(torch, np, steps, warmup):
-    from paper_2609_12378_amd import Context
     from workloads import KEYSWITCH as cfg, gaussian_error, rng, ternary_secret, uniform_residues, uniform_slots
-    ctx = Context(cfg.log_n, cfg.n_q, cfg.n_p, cfg.dnum, q_bits=cfg.q_bits)
+    ctx = make_context(cfg)
     n, L = ctx.n, cfg.level + 1
     s = torch.from_numpy(ternary_secret(rng(cfg.index, 3), n)).cuda()
     z = uniform_slots(rng(cfg.index, 1), n // 2)
@@ -401,9 +408,8 @@ def bench_keyswitch(torch, np, steps, warmup):
 
 
 def bench_ntt(torch, steps):
-    from paper_2609_12378_amd import Context
     from workloads import NTT_BENCH as cfg
-    ctx = Context(cfg.log_n, cfg.n_q, 0, 1, q_bits=cfg.q_bits)
+    ctx = make_context(cfg, 0, 1)
     g = torch.Generator(device="cuda").manual_seed(202)
     x = torch.randint(0, 1 << 49, (cfg.batch, cfg.n_q, ctx.n), generator=g, device="cuda",
                       dtype=torch.int64).view(torch.uint64)
@@ -536,9 +542,13 @@ def main():
     ap.add_argument("--no-secondary", action="store_true")
     ap.add_argument("--only", choices=["keyswitch", "ntt", "tile", "shapes", "tm", "attention"], default=None,
                     help="run only this secondary workload (for profiling); prints its JSON")
+    ap.add_argument("--lazy-moddown", type=int, default=1, choices=[0, 1],
+                    help="1 (default): sums of rotations with one ModDown per output (the library's lazy mode); "
+                         "0: one ModDown per rotation")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also run one plain device copy of this many MiB (for hardware-counter calibration)")
     args = ap.parse_args()
+    LAZY["on"] = bool(args.lazy_moddown)
     if args.gpus != 1:
         print("bench.py runs on one GPU: the projection path is single-GPU in this build (--gpus %d requested)"
               % args.gpus, file=sys.stderr)

@@ -98,6 +98,17 @@ ckks_status ckks_ctx_set_ntt_arith(ckks_ctx *ctx, int mode);
  * default: as many as fit a 24 GiB staging buffer).  Smaller values use less
  * scratch memory and more launches; results are identical for every value. */
 ckks_status ckks_ctx_set_proj_batch(ckks_ctx *ctx, uint32_t max_pairs);
+/* Lazy ModDown (on = 1; off, the default, = 0): the giant-step rotations of
+ * ckks_linear_project and ckks_linear_project_tm and the outer rotation sum of
+ * ckks_attention_scores sum their key-switching inner products over Q u P
+ * (with P * sigma(c0)) and divide by P once per output instead of once per
+ * rotation (the lazy ModDown of a sum of key switches, e.g. Bossuat et al.
+ * 2021).  The division rounds once instead of per rotation, so sums before the
+ * final rescale differ by small integers per coefficient (at most n_p times
+ * half the number of rotations); the outputs, after it, agree with the eager
+ * ones except where such a difference crosses a rounding boundary.  Scratch
+ * sizes (ckks_workspace_bytes) depend on this setting. */
+ckks_status ckks_ctx_set_lazy_moddown(ckks_ctx *ctx, int on);
 /* Host copies of the primes q (n_q), p (n_p) and psi (n_q + n_p, q first);
  * any pointer may be NULL. */
 ckks_status ckks_ctx_tables(const ckks_ctx *ctx, uint64_t *q, uint64_t *p, uint64_t *psi);
@@ -119,7 +130,9 @@ ckks_status ckks_ctx_tables(const ckks_ctx *ctx, uint64_t *q, uint64_t *p, uint6
  * ckks_workspace_bytes returns the bytes one call of `op` takes, for the
  * shape given as shape[] (unused entries may be omitted; shape may be NULL
  * where noted), or SIZE_MAX for an unknown op or invalid shape.  The figure
- * for CKKS_OP_LINEAR_PROJECT depends on ckks_ctx_set_proj_batch. */
+ * for CKKS_OP_LINEAR_PROJECT depends on ckks_ctx_set_proj_batch, and the
+ * figures of the projections and the attention scores on
+ * ckks_ctx_set_lazy_moddown. */
 typedef enum {
     CKKS_OP_NONE = 0,           /* ntt, intt, add, mul_plain, automorph: no workspace */
     CKKS_OP_ENCODE = 1,         /* shape unused */

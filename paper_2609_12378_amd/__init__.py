@@ -57,6 +57,7 @@ _SIGS = {
     "ckks_ctx_set_stream": (ctypes.c_int, [_VP, _VP]),
     "ckks_ctx_set_ntt_arith": (ctypes.c_int, [_VP, ctypes.c_int]),
     "ckks_ctx_set_proj_batch": (ctypes.c_int, [_VP, _U32]),
+    "ckks_ctx_set_lazy_moddown": (ctypes.c_int, [_VP, ctypes.c_int]),
     "ckks_ctx_tables": (ctypes.c_int, [_VP, _VP, _VP, _VP]),
     "ckks_workspace_bytes": (ctypes.c_size_t, [_VP, ctypes.c_int, _VP]),
     "ckks_set_workspace": (ctypes.c_int, [_VP, _VP, ctypes.c_size_t]),
@@ -206,6 +207,10 @@ class Context:
     def set_proj_batch(self, max_pairs: int):
         """Cap the (input, baby step) pairs per projection launch (0 = by the library's staging budget)."""
         _check(self.lib.ckks_ctx_set_proj_batch(self.h, max_pairs), "ckks_ctx_set_proj_batch")
+
+    def set_lazy_moddown(self, on: bool):
+        """Sum the rotations of the projections' giant steps and of the attention outer sum with one ModDown."""
+        _check(self.lib.ckks_ctx_set_lazy_moddown(self.h, int(bool(on))), "ckks_ctx_set_lazy_moddown")
 
     # workspace op codes (ckks_op)
     OP_ENCODE, OP_DECODE, OP_ENCRYPT, OP_DECRYPT, OP_KEYGEN, OP_RESCALE, OP_ROTATE, OP_MUL_RELIN, OP_MODUP, \

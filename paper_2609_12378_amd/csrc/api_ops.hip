@@ -150,6 +150,56 @@ ckks_status rotate_each(ckks_ctx *ctx, const uint64_t *cs, size_t stride, uint32
     return CKKS_OK;
 }
 
+size_t lazy_work_words(const ckks_ctx *ctx, uint32_t level, uint32_t count)
+{
+    const size_t ext = level + 1 + ctx->n_p;
+    return (size_t)count * ((size_t)n_digits(ctx, level) * ext + ctx->alpha) << ctx->log_n;
+}
+
+namespace {
+
+ckks_status rotate_lazy(ckks_ctx *ctx, const uint64_t *cs, size_t stride, uint32_t count, uint32_t level,
+                        const int32_t *steps, const uint64_t *const *keys, bool same_step, uint64_t *uacc,
+                        bool sum_all, bool accumulate, uint64_t *work)
+{
+    if (!count) return CKKS_OK;
+    const uint32_t L = level + 1, ext = L + ctx->n_p, nd = n_digits(ctx, level);
+    const size_t N = ctx->n, dig_ct = (size_t)nd * ext * N;
+    CK_TRY(ks_modup_batch(ctx, cs + (size_t)L * N, stride, count, level, work));
+    std::vector<uint32_t> g(count);
+    std::vector<const uint64_t *> c0s(count), digs(count), ks(count);
+    std::vector<uint64_t *> accs(count);
+    for (uint32_t r = 0; r < count; r++) {
+        g[r] = ckks_galois_elt(ctx, same_step ? steps[0] : steps[r]);
+        ks[r] = same_step ? keys[0] : keys[r];
+        c0s[r] = cs + (size_t)r * stride;
+        digs[r] = work + (size_t)r * dig_ct;
+        accs[r] = uacc + (sum_all ? 0 : (size_t)r * 2 * ext * N);
+    }
+    const uint32_t bs = ks_rot_batch(count);
+    for (uint32_t r0 = 0; r0 < count; r0 += bs) {
+        const uint32_t cnt = count - r0 < bs ? count - r0 : bs;
+        CK_TRY(ks_ip_accumulate(ctx, level, cnt, c0s.data() + r0, digs.data() + r0, g.data() + r0, ks.data() + r0,
+                                accs.data() + r0, sum_all, accumulate || (sum_all && r0 > 0)));
+    }
+    return CKKS_OK;
+}
+
+}  // namespace
+
+ckks_status rotate_many_lazy(ckks_ctx *ctx, const uint64_t *cs, size_t stride, uint32_t count, uint32_t level,
+                             int32_t steps, const uint64_t *key, uint64_t *uacc, bool accumulate, uint64_t *work)
+{
+    return rotate_lazy(ctx, cs, stride, count, level, &steps, &key, true, uacc, false, accumulate, work);
+}
+
+ckks_status rotate_each_lazy(ckks_ctx *ctx, const uint64_t *cs, size_t stride, uint32_t count, uint32_t level,
+                             const int32_t *steps, const uint64_t *const *keys, uint64_t *uacc, bool accumulate,
+                             uint64_t *work)
+{
+    return rotate_lazy(ctx, cs, stride, count, level, steps, keys, false, uacc, true, accumulate, work);
+}
+
 ckks_status rescale_many(ckks_ctx *ctx, const uint64_t *c, uint32_t count, uint32_t l, uint64_t *out,
                          uint64_t *work)
 {

@@ -329,7 +329,7 @@ ckks_status attn_check_shape(const ckks_ctx *ctx, const ckks_attn_shape *shape, 
 // Scratch of the scores call for inputs of L limbs (words)
 struct ScoreScratch {
     uint32_t Jt, logn;
-    size_t u_w, mq_w, tw_w, mh_w, b_w, a_w, d_w, pr_w, ub_w, rot_w, tot_w, work_w, total;
+    size_t u_w, mq_w, tw_w, mh_w, b_w, a_w, d_w, pr_w, ub_w, rot_w, tot_w, ua_w, work_w, total;
 };
 
 ScoreScratch score_scratch(const ckks_ctx *ctx, uint32_t L, uint32_t D, uint32_t T, uint32_t hd)
@@ -348,12 +348,13 @@ ScoreScratch score_scratch(const ckks_ctx *ctx, uint32_t L, uint32_t D, uint32_t
     s.ub_w = (size_t)hd * ctw1;
     s.rot_w = (size_t)s.Jt * ctw1;
     s.tot_w = ctw1;
+    s.ua_w = (size_t)2 * (L - 1 + ctx->n_p) * N;  // the outer sum over Q u P (lazy ModDown)
     s.work_w = std::max({ks_scratch_words(ctx, level, ks_rot_batch(T - 1)),
                          ks_scratch_words(ctx, level, ks_rot_batch(T), T),
                          ks_scratch_words(ctx, level - 1, ks_rot_batch(s.Jt), s.Jt),
                          (size_t)2 * T * (1 + level) * N});
     s.total = s.u_w + s.mq_w + s.tw_w + s.mh_w + s.b_w + s.a_w + s.d_w + s.pr_w + s.ub_w + s.rot_w + s.tot_w +
-              s.work_w;
+              s.ua_w + s.work_w;
     return s;
 }
 
@@ -493,7 +494,8 @@ extern "C" ckks_status ckks_attention_scores(ckks_ctx *ctx, const ckks_buf *q, u
     uint64_t *Ub = Pr + ss.pr_w;               // [hd][2][L-1][N] U_k
     uint64_t *rot = Ub + ss.ub_w;              // [Jt][2][L-1][N]
     uint64_t *tot = rot + ss.rot_w;
-    uint64_t *work = tot + ss.tot_w;
+    uint64_t *uacc = tot + ss.tot_w;           // [2][L-1+K][N]
+    uint64_t *work = uacc + ss.ua_w;
 
     // the masks at scale q_(level-1) (the products are multiplied by them after their first rescale), and
     // their correlation form
@@ -552,13 +554,23 @@ extern "C" ckks_status ckks_attention_scores(ckks_ctx *ctx, const ckks_buf *q, u
         // 3. U_k = sum_delta M_{(delta + k) mod hd} P_delta = z[-k mod hd] for every k, then each rotated by k
         //    (in chunks) and summed
         CK_TRY(launch_corr(ctx, Ub, Pd, T, hd, -1, 0, L - 1, ss.logn, logT, 2 * D, Om, Omi, Mh));
-        CK_TRY(launch_sum_cts(ctx, tot, Ub, 1, ctw1, L - 1, false));
-        for (uint32_t k0 = 1; k0 < hd; k0 += ss.Jt) {
-            const uint32_t cnt = std::min(ss.Jt, hd - k0);
-            for (uint32_t r = 0; r < cnt; r++) outs[r] = rot + (size_t)r * ctw1;
-            CK_TRY(rotate_each(ctx, Ub + (size_t)k0 * ctw1, ctw1, cnt, level - 1, osteps.data() + (k0 - 1),
-                               okeys.data() + (k0 - 1), outs.data(), work));
-            CK_TRY(launch_sum_cts(ctx, tot, rot, cnt, ctw1, L - 1, true));
+        if (ctx->lazy_moddown) {
+            // the hd - 1 key-switching sums accumulated over Q u P, one ModDown, U_0 added in it
+            for (uint32_t k0 = 1; k0 < hd; k0 += ss.Jt) {
+                const uint32_t cnt = std::min(ss.Jt, hd - k0);
+                CK_TRY(rotate_each_lazy(ctx, Ub + (size_t)k0 * ctw1, ctw1, cnt, level - 1, osteps.data() + (k0 - 1),
+                                        okeys.data() + (k0 - 1), uacc, k0 > 1, work));
+            }
+            CK_TRY(ks_moddown(ctx, uacc, 2, level - 1, Ub, 1, Ub + (size_t)(L - 1) * N, tot, work));
+        } else {
+            CK_TRY(launch_sum_cts(ctx, tot, Ub, 1, ctw1, L - 1, false));
+            for (uint32_t k0 = 1; k0 < hd; k0 += ss.Jt) {
+                const uint32_t cnt = std::min(ss.Jt, hd - k0);
+                for (uint32_t r = 0; r < cnt; r++) outs[r] = rot + (size_t)r * ctw1;
+                CK_TRY(rotate_each(ctx, Ub + (size_t)k0 * ctw1, ctw1, cnt, level - 1, osteps.data() + (k0 - 1),
+                                   okeys.data() + (k0 - 1), outs.data(), work));
+                CK_TRY(launch_sum_cts(ctx, tot, rot, cnt, ctw1, L - 1, true));
+            }
         }
         // 4. the final rescale
         CK_TRY(rescale_core(ctx, tot, level - 1, out[c].data, work));

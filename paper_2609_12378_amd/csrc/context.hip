@@ -476,6 +476,14 @@ ckks_status ckks_ctx_set_proj_batch(ckks_ctx *c, uint32_t max_pairs)
     return CKKS_OK;
 }
 
+ckks_status ckks_ctx_set_lazy_moddown(ckks_ctx *c, int on)
+{
+    clear_error();
+    CK_REQUIRE(c, CKKS_EINVAL, "null context");
+    c->lazy_moddown = on != 0;
+    return CKKS_OK;
+}
+
 ckks_status ckks_ctx_tables(const ckks_ctx *c, uint64_t *q, uint64_t *p, uint64_t *psi)
 {
     clear_error();

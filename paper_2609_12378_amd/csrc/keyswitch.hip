@@ -265,6 +265,49 @@ __global__ __launch_bounds__(kThreads) void k_key_ip_batch(RotArgs ra, uint64_t 
     ur[(size_t)rows << log_n] = reduce128(a1, m);
 }
 
+// Lazy ModDown: the key inner products of several rotations summed over Q_level u P before one division by P.
+// For rotation r: t_k = sum_j sigma_{g_r}(d_j) * key_r[j][k] on every row, plus P * sigma_{g_r}(c0_r) on the q rows of
+// component 0 (P is 0 modulo the special primes, and ModDown(x + P y) = ModDown(x) + y, so the c0 term passes the
+// division unchanged).  sum_all: one accumulator ra.out[0] takes the sum over all r of the batch; else ra.out[r]
+// takes rotation r's.  Accumulators [2][ext][N], added to when `accumulate`.  The 128-bit sums hold at most
+// 32 (nd + 1) products below 2^100.
+__global__ __launch_bounds__(kThreads) void k_key_ip_acc(RotArgs ra, uint32_t nd, uint32_t ext, uint32_t level,
+                                                         uint32_t n_q, uint32_t key_rows,
+                                                         const ulonglong2 *__restrict__ pmodq,
+                                                         const ModQ *__restrict__ mods, uint32_t log_n, int sum_all,
+                                                         int accumulate)
+{
+    const uint32_t n = 1u << log_n;
+    const uint32_t col = blockIdx.x * kThreads + threadIdx.x;
+    const uint32_t row = blockIdx.y;
+    if (col >= n) return;
+    const uint32_t r0 = sum_all ? 0 : blockIdx.z, r1 = sum_all ? ra.count : blockIdx.z + 1;
+    const uint32_t prime = row <= level ? row : n_q + (row - level - 1);
+    const ModQ m = mods[prime];
+    const uint64_t pq = row <= level ? pmodq[row].x : 0;
+    acc128 a0{0, 0}, a1{0, 0};
+    for (uint32_t r = r0; r < r1; r++) {
+        const uint32_t sc = auto_index(col, ra.g[r], log_n);
+        const uint64_t *key = ra.key[r];
+        const uint64_t *digits = ra.dig[r];
+        for (uint32_t j = 0; j < nd; j++) {
+            const uint64_t d = digits[(((size_t)j * ext + row) << log_n) + sc];
+            const size_t kb = ((size_t)j * 2 * key_rows + prime) << log_n;
+            mac(a0, d, key[kb + col]);
+            mac(a1, d, key[kb + ((size_t)key_rows << log_n) + col]);
+        }
+        if (pq) mac(a0, ra.c0[r][((size_t)row << log_n) + sc], pq);
+    }
+    uint64_t *u = ra.out[r0] + ((size_t)row << log_n) + col;
+    uint64_t v0 = reduce128(a0, m), v1 = reduce128(a1, m);
+    if (accumulate) {
+        v0 = addmod(v0, u[0], m.q);
+        v1 = addmod(v1, u[(size_t)ext << log_n], m.q);
+    }
+    u[0] = v0;
+    u[(size_t)ext << log_n] = v1;
+}
+
 // ModDown of a batch of rotations, fused (fp64, 256-point rows): block (r, q-limb i, two rows h) finishes the
 // forward transform of the converted P part cw[r][k][i] (its first pass already done), computes the q-limb part
 // of the key inner product u_k = sum_j sigma_{g_r}(d_j)[i] * key_r[j][k][i] in registers, and writes
@@ -496,6 +539,33 @@ ckks_status ks_rotate_batch(ckks_ctx *ctx, uint32_t level, uint32_t count, const
         prof_end(ctx, K_MODDOWN);
         HIP_TRY(hipGetLastError());
     }
+    return CKKS_OK;
+}
+
+ckks_status ks_ip_accumulate(ckks_ctx *ctx, uint32_t level, uint32_t count, const uint64_t *const *c0s,
+                             const uint64_t *const *digs, const uint32_t *g, const uint64_t *const *keys,
+                             uint64_t *const *accs, bool sum_all, bool accumulate)
+{
+    CK_REQUIRE(count >= 1 && count <= (uint32_t)kRotBatch, CKKS_EINVAL, "rotation batch of %u", count);
+    const uint32_t L = level + 1, ext = L + ctx->n_p, nd = n_digits(ctx, level);
+    RotArgs ra{};
+    ra.count = count;
+    for (uint32_t r = 0; r < count; r++) {
+        ra.g[r] = g[r];
+        ra.key[r] = keys[r];
+        ra.out[r] = accs[sum_all ? 0 : r];
+        ra.dig[r] = digs[r];
+        ra.c0[r] = c0s[r];
+    }
+    const dim3 grid((ctx->n + kThreads - 1) / kThreads, ext, sum_all ? 1 : count), block(kThreads);
+    const double outs = sum_all ? 1.0 : count;
+    // digits and keys of every rotation, c0, the accumulators read (when accumulating) and written
+    prof_begin(ctx, K_KEYIP, 8.0 * ctx->n * ext * (count * (3.0 * nd) + (double)L / ext * count +
+                                                   outs * 2.0 * (accumulate ? 2 : 1)));
+    hipLaunchKernelGGL(k_key_ip_acc, grid, block, 0, ctx->stream, ra, nd, ext, level, ctx->n_q, ctx->n_primes(),
+                       ctx->d_pmodq, ctx->d_mod, ctx->log_n, (int)sum_all, (int)accumulate);
+    prof_end(ctx, K_KEYIP);
+    HIP_TRY(hipGetLastError());
     return CKKS_OK;
 }
 

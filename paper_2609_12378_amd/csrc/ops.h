@@ -51,6 +51,13 @@ ckks_status ks_rotate_batch(ckks_ctx *ctx, uint32_t level, uint32_t count, const
                             const uint64_t *const *digs, const uint32_t *g, const uint64_t *const *keys,
                             uint64_t *const *outs, uint64_t *work);
 
+// lazy ModDown: accs[r] (or accs[0] for all r when sum_all; [2][level+1+K][N]) (+)= the key inner product of
+// rotation r over Q_level u P plus P * sigma_{g_r}(c0_r) on the q rows; count <= 32.  ks_moddown of the accumulator
+// then gives the sum of the rotations.
+ckks_status ks_ip_accumulate(ckks_ctx *ctx, uint32_t level, uint32_t count, const uint64_t *const *c0s,
+                             const uint64_t *const *digs, const uint32_t *g, const uint64_t *const *keys,
+                             uint64_t *const *accs, bool sum_all, bool accumulate);
+
 // encoding (encode.hip)
 struct SlotSource {
     // explicit slots: re/im [batch][N/2] (im may be null)
@@ -128,6 +135,17 @@ ckks_status launch_mac_mfma(ckks_ctx *ctx, uint64_t *acc, const int8_t *Xd, cons
 // plaintext pt's NTT values on run x (positions x N/2D ..) modulo q_l, l < L, as doubles
 ckks_status launch_enc_vectors(ckks_ctx *ctx, const double *U, uint32_t D, uint32_t count, double delta, uint32_t L,
                                double *Q);
+
+// Lazy sums of rotations (one ModDown per output).  rotate_many_lazy: ciphertext r (at cs + r * stride) rotated by
+// `steps` is added to accumulator uacc + r * 2 ext N; rotate_each_lazy: ciphertext r rotated by steps[r], all
+// added to the one accumulator uacc.  accumulate = false starts the accumulators.
+// work: count * (nd ext + alpha) N words (the ModUp digits)
+ckks_status rotate_many_lazy(ckks_ctx *ctx, const uint64_t *cs, size_t stride, uint32_t count, uint32_t level,
+                             int32_t steps, const uint64_t *key, uint64_t *uacc, bool accumulate, uint64_t *work);
+ckks_status rotate_each_lazy(ckks_ctx *ctx, const uint64_t *cs, size_t stride, uint32_t count, uint32_t level,
+                             const int32_t *steps, const uint64_t *const *keys, uint64_t *uacc, bool accumulate,
+                             uint64_t *work);
+size_t lazy_work_words(const ckks_ctx *ctx, uint32_t level, uint32_t count);
 
 // decode: coef = coefficient form of limbs 0..min(limbs,2)-1 ([limbs][N]); writes N/2 slots
 ckks_status dec_slots(ckks_ctx *ctx, const uint64_t *coef, uint32_t limbs, double scale, double2 *work, double *re,

@@ -347,7 +347,7 @@ struct ProjScratch {
     uint32_t Jt;  // output blocks per tile (kJ on the integer path, kJF on the fused fp64 one)
     uint32_t Pb;  // (input, baby step) pairs per plaintext sub-batch
     bool diag;    // W re-laid as its cyclic diagonals (radix-8 FFT pass A)
-    size_t xrot_w, acc_w, tot_w, rot_w, pt_w, m_w, fft_w, ks_w, wd_w, fop_w, total;
+    size_t xrot_w, acc_w, tot_w, rot_w, pt_w, m_w, fft_w, ks_w, wd_w, fop_w, ua_w, total;
 };
 
 ProjScratch proj_scratch(const ckks_ctx *ctx, uint32_t L, uint32_t D, uint32_t d_in, uint32_t d_out, uint32_t n1)
@@ -379,8 +379,10 @@ ProjScratch proj_scratch(const ckks_ctx *ctx, uint32_t L, uint32_t D, uint32_t d
     ps.diag = D <= 256 && ctx->log_n >= 12;
     ps.wd_w = ps.diag ? (size_t)d_in * d_out : 0;
     ps.fop_w = ps.diag ? N / 4 : 0;
+    // lazy ModDown: the tile's key-switching sums over Q u P
+    ps.ua_w = ctx->lazy_moddown ? (size_t)kJt * 2 * (L + ctx->n_p) * N : 0;
     ps.total = ps.xrot_w + ps.acc_w + ps.tot_w + ps.rot_w + ps.pt_w + ps.m_w + ps.fft_w + ps.ks_w + ps.wd_w +
-               ps.fop_w;
+               ps.fop_w + ps.ua_w;
     return ps;
 }
 
@@ -484,6 +486,8 @@ extern "C" ckks_status ckks_linear_project(ckks_ctx *ctx, const ckks_buf *in, co
     uint64_t *ksw = (uint64_t *)(fft) + fft_w;
     double *Wd = (double *)(ksw + ks_w);
     uint32_t *fop = (uint32_t *)(ksw + ks_w + wd_w);
+    uint64_t *uacc = ksw + ks_w + wd_w + ps.fop_w;  // [Jt][2][L + K][N] when the ModDown is lazy
+    const bool lazy = ctx->lazy_moddown;
     if (diag) {
         CK_TRY(launch_diag_layout(ctx, Wd, W, D, n_in, shape->d_out));
         CK_TRY(enc_feat_of_pos(ctx, T, fop));
@@ -546,15 +550,22 @@ extern "C" ckks_status ckks_linear_project(ckks_ctx *ctx, const ckks_buf *in, co
                 }
                 pb0 += P;
             }
-            // giant step: the tile's jc partial sums rotated together, then added to the totals
+            // giant step: the tile's jc partial sums rotated together, then added to the totals (lazy: their
+            // key-switching sums accumulated over Q u P, divided by P once after the last giant step)
             if (g == 0) {
                 HIP_TRY(hipMemcpyAsync(tot, acc, jc * ctw * 8, hipMemcpyDeviceToDevice, ctx->stream));
+            } else if (lazy) {
+                CK_TRY(rotate_many_lazy(ctx, acc, ctw, jc, level, (int32_t)(T * n1 * g), gkeys[g], uacc, g > 1, ksw));
             } else {
                 std::vector<uint64_t *> outs(jc);
                 for (uint32_t jj = 0; jj < jc; jj++) outs[jj] = rot + (size_t)jj * ctw;
                 CK_TRY(rotate_many(ctx, acc, ctw, jc, level, (int32_t)(T * n1 * g), gkeys[g], outs.data(), ksw));
                 CK_TRY(launch_binary(ctx, tot, tot, rot, jc * 2 * L, limb_range(0, L), EW_ADD));
             }
+        }
+        if (lazy && n2 > 1) {
+            CK_TRY(ks_moddown(ctx, uacc, 2 * jc, level, nullptr, 1, nullptr, rot, ksw));
+            CK_TRY(launch_binary(ctx, tot, tot, rot, jc * 2 * L, limb_range(0, L), EW_ADD));
         }
         for (uint32_t jj = 0; jj < jc; jj++) {
             CK_TRY(rescale_core(ctx, tot + (size_t)jj * ctw, level, out[j0 + jj].data, rot));

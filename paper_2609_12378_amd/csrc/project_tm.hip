@@ -415,7 +415,7 @@ struct TmScratch {
     uint32_t Jt, Pb;
     bool mfma;             // the multiply-accumulate runs on the matrix cores
     uint32_t kt, kt_pad;   // kappa count (2 n_in n1) and the padded digit-row length in bytes
-    size_t x2_w, acc_w, tot_w, rot_w, q_w, ks_w, wd_w, xd_w, total;
+    size_t x2_w, acc_w, tot_w, rot_w, q_w, ks_w, wd_w, xd_w, ua_w, total;
 };
 
 TmScratch tm_scratch(const ckks_ctx *ctx, uint32_t L, uint32_t D, uint32_t d_in, uint32_t d_out, uint32_t n1)
@@ -448,7 +448,8 @@ TmScratch tm_scratch(const ckks_ctx *ctx, uint32_t L, uint32_t D, uint32_t d_in,
                        ks_scratch_words(ctx, level, ks_rot_batch(ts.Jt), ts.Jt));
     ts.wd_w = (size_t)d_in * d_out;
     ts.xd_w = ts.mfma ? ((size_t)kDig * L * 2 * N * ts.kt_pad + 7) / 8 : 0;
-    ts.total = ts.x2_w + ts.acc_w + ts.tot_w + ts.rot_w + ts.q_w + ts.ks_w + ts.wd_w + ts.xd_w;
+    ts.ua_w = ctx->lazy_moddown ? (size_t)ts.Jt * 2 * (L + ctx->n_p) * N : 0;
+    ts.total = ts.x2_w + ts.acc_w + ts.tot_w + ts.rot_w + ts.q_w + ts.ks_w + ts.wd_w + ts.xd_w + ts.ua_w;
     return ts;
 }
 
@@ -650,6 +651,8 @@ extern "C" ckks_status ckks_linear_project_tm(ckks_ctx *ctx, const ckks_buf *in,
     uint64_t *ksw = (uint64_t *)(Q + ts.q_w);
     double *Wd = (double *)(ksw + ts.ks_w);
     int8_t *Xd = (int8_t *)(Wd + ts.wd_w);
+    uint64_t *uacc = (uint64_t *)(Wd + ts.wd_w) + ts.xd_w;  // [Jt][2][L + K][N] when the ModDown is lazy
+    const bool lazy = ctx->lazy_moddown;
     CK_TRY(launch_diag_layout(ctx, Wd, W, D, n_in, shape->d_out));
 
     // 1. Rot_b(x_i) and Rot_{b-D}(x_i), hoisted per input
@@ -702,12 +705,18 @@ extern "C" ckks_status ckks_linear_project_tm(ckks_ctx *ctx, const ckks_buf *in,
             }
             if (g == 0) {
                 HIP_TRY(hipMemcpyAsync(tot, acc, jc * ctw * 8, hipMemcpyDeviceToDevice, ctx->stream));
+            } else if (lazy) {
+                CK_TRY(rotate_many_lazy(ctx, acc, ctw, jc, level, (int32_t)(n1 * g), gkeys[g], uacc, g > 1, ksw));
             } else {
                 std::vector<uint64_t *> outs(jc);
                 for (uint32_t jj = 0; jj < jc; jj++) outs[jj] = rot + (size_t)jj * ctw;
                 CK_TRY(rotate_many(ctx, acc, ctw, jc, level, (int32_t)(n1 * g), gkeys[g], outs.data(), ksw));
                 CK_TRY(launch_binary(ctx, tot, tot, rot, jc * 2 * L, limb_range(0, L), EW_ADD));
             }
+        }
+        if (lazy && n2 > 1) {
+            CK_TRY(ks_moddown(ctx, uacc, 2 * jc, level, nullptr, 1, nullptr, rot, ksw));
+            CK_TRY(launch_binary(ctx, tot, tot, rot, jc * 2 * L, limb_range(0, L), EW_ADD));
         }
         for (uint32_t jj = 0; jj < jc; jj++) {
             CK_TRY(rescale_core(ctx, tot + (size_t)jj * ctw, level, out[j0 + jj].data, rot));

@@ -47,10 +47,11 @@ def rep(Kh, D, hd):
     return np.tile(Kh, (1, D // hd))
 
 
-def run_parity(cfg, n_q, n_kv, kv_of_q):
+def run_parity(cfg, n_q, n_kv, kv_of_q, lazy=False):
     require_gpu()
     from paper_2609_12378_amd import Context
     ctx = Context(cfg.log_n, cfg.n_q, cfg.n_p, cfg.dnum, q_bits=cfg.q_bits)
+    ctx.set_lazy_moddown(lazy)
     ck = Ckks(cfg.log_n, ctx.q, ctx.p, cfg.dnum)
     n, T, hd, level = ctx.n, cfg.tokens, cfg.head_dim, cfg.level
     D = (n // 2) // T
@@ -86,10 +87,20 @@ def run_parity(cfg, n_q, n_kv, kv_of_q):
     rlk_o = ck.keygen_relin(s, a, e)
     rlk_g = ctx.keygen_relin(s_dev, to_dev(a), to_dev(e))
     say("keys ready", len(keys_g))
+    ctx.profile(True)
+    ctx.profile_reset()
     S_g = ctx.attention_scores(list(q_g), list(k_g), kv_of_q, T, hd, rlk_g, keys_g)
+    moddowns = ctx.profile_read("moddown")[1]
+    ctx.profile(False)
+    if lazy:
+        # the keys' rotations (per key ciphertext used), then per query ciphertext its pre-rotations and the
+        # batched relinearisation (batches of 32) and one ModDown for the whole outer sum
+        b32 = -(-(T - 1) // 32)
+        expect = len(set(kv_of_q)) * b32 + n_q * (b32 + -(-T // 32) + 1)
+        assert moddowns == expect, (moddowns, expect)
     O_g = ctx.attention_apply(S_g, list(v_g), kv_of_q, T, hd, rlk_g, keys_g)
     say("gpu attention done")
-    S_o = ck.attention_scores(list(q_o), list(k_o), kv_of_q, T, hd, rlk_o, keys_o)
+    S_o = ck.attention_scores(list(q_o), list(k_o), kv_of_q, T, hd, rlk_o, keys_o, lazy=lazy)
     O_o = ck.attention_apply(S_o, list(v_o), kv_of_q, T, hd, rlk_o, keys_o)
     say("oracle attention done")
     s_scale = delta * delta / ctx.q[level]
@@ -114,6 +125,13 @@ def run_parity(cfg, n_q, n_kv, kv_of_q):
 def test_toy_attention_parity_grouped():
     es, eo = run_parity(ATTN_TOY, 3, 2, [1, 0, 1])
     say("toy attention max error: scores %.3g, sums %.3g" % (es, eo))
+    assert es <= 2.0 ** -30
+    assert eo <= 2.0 ** -28
+
+
+def test_toy_attention_parity_lazy_moddown():
+    es, eo = run_parity(ATTN_TOY, 2, 1, [0, 0], lazy=True)
+    say("toy attention (lazy ModDown) max error: scores %.3g, sums %.3g" % (es, eo))
     assert es <= 2.0 ** -30
     assert eo <= 2.0 ** -28
 

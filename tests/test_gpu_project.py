@@ -40,12 +40,13 @@ def fm_pack(X, T, D, i):
     return X[:, i * D:(i + 1) * D].T.reshape(-1)
 
 
-def run_case(cfg, d_in, d_out, oracle_outputs, arith=0, max_pairs=0, weight_scale=1.0):
+def run_case(cfg, d_in, d_out, oracle_outputs, arith=0, max_pairs=0, weight_scale=1.0, lazy=False):
     require_gpu()
     from paper_2609_12378_amd import Context
     ctx = Context(cfg.log_n, cfg.n_q, cfg.n_p, cfg.dnum, q_bits=cfg.q_bits)
     ctx.set_ntt_arith(arith)
     ctx.set_proj_batch(max_pairs)
+    ctx.set_lazy_moddown(lazy)
     ck = Ckks(cfg.log_n, ctx.q, ctx.p, cfg.dnum)
     n, T, D, n1, level = ctx.n, cfg.tokens, cfg.feats, cfg.n1, cfg.level
     n2 = -(-D // n1)
@@ -75,9 +76,18 @@ def run_case(cfg, d_in, d_out, oracle_outputs, arith=0, max_pairs=0, weight_scal
         keys_g[st] = ctx.keygen_galois(s_dev, g, to_dev(a), to_dev(e))
     say("keys ready", len(steps))
     Wd = to_dev(W)
+    ctx.profile(True)
+    ctx.profile_reset()
     outs = ctx.linear_project(cts_g, Wd, T, n1, keys_g)
-    say("gpu projection done")
-    want = ck.linear_project(cts_o, W, T, n1, keys_o, out_blocks=oracle_outputs)
+    moddowns = ctx.profile_read("moddown")[1]
+    ctx.profile(False)
+    say("gpu projection done; ModDown launches", moddowns)
+    if lazy and n2 > 1:
+        # the hoisted baby steps (batches of 32 per input), then one ModDown per output tile of 28 instead of
+        # one per giant step
+        expect = (d_in // D) * -(-(n1 - 1) // 32) + -(-(d_out // D) // 28)
+        assert moddowns == expect, (moddowns, expect)
+    want = ck.linear_project(cts_o, W, T, n1, keys_o, out_blocks=oracle_outputs, lazy=lazy)
     say("oracle projection done")
     for j, wo in zip(oracle_outputs, want):
         got = to_host(outs[j].data)
@@ -148,6 +158,21 @@ def test_down_projection_parameters_full_degree_slice():
     say("down-projection slice (n1 = 8)")
     err = run_case(PROJ_DOWN, 512, 256, [0])
     say("down slice max error vs X@W", err)
+    assert err <= 2.0 ** -18
+
+
+def test_toy_projection_lazy_moddown():
+    # the eight giant steps of each output summed with one ModDown (output tiles of 28 and a short one)
+    cfg = dataclasses.replace(TOY, n1=16)
+    err = run_case(cfg, 2 * cfg.feats, 31 * cfg.feats, [0, 28, 30], lazy=True)
+    say("toy lazy-ModDown max error vs X@W", err)
+    assert err <= 2.0 ** -12
+
+
+def test_projection_lazy_moddown_full_degree_slice():
+    say("full-degree slice, lazy ModDown")
+    err = run_case(PROJECTION, 256, 512, [1], lazy=True)
+    say("lazy slice max error vs X@W", err)
     assert err <= 2.0 ** -18
 
 

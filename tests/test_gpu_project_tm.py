@@ -33,11 +33,12 @@ def tm_pack(X, T, D, i):
     return X[:, i * D:(i + 1) * D].reshape(-1)
 
 
-def run_case(cfg, d_in, d_out, n1, oracle_outputs, max_pairs=0):
+def run_case(cfg, d_in, d_out, n1, oracle_outputs, max_pairs=0, lazy=False):
     require_gpu()
     from paper_2609_12378_amd import Context
     ctx = Context(cfg.log_n, cfg.n_q, cfg.n_p, cfg.dnum, q_bits=cfg.q_bits)
     ctx.set_proj_batch(max_pairs)
+    ctx.set_lazy_moddown(lazy)
     ck = Ckks(cfg.log_n, ctx.q, ctx.p, cfg.dnum)
     n, T, level = ctx.n, cfg.tokens, cfg.level
     D = (n // 2) // T
@@ -65,9 +66,17 @@ def run_case(cfg, d_in, d_out, n1, oracle_outputs, max_pairs=0):
         keys_o[st] = ck.keygen_galois(s, g, a, e)
         keys_g[st] = ctx.keygen_galois(s_dev, g, to_dev(a), to_dev(e))
     say("keys ready", len(steps))
+    ctx.profile(True)
+    ctx.profile_reset()
     outs = ctx.linear_project(cts_g, to_dev(W), T, n1, keys_g, layout="tm")
-    say("gpu projection done")
-    want = ck.linear_project_tm(cts_o, W, T, n1, keys_o, out_blocks=oracle_outputs)
+    moddowns = ctx.profile_read("moddown")[1]
+    ctx.profile(False)
+    say("gpu projection done; ModDown launches", moddowns)
+    if lazy and n2 > 1:
+        # the hoisted baby steps b and b - D (batches of 32 per input), then one ModDown per output tile of 32
+        expect = (d_in // D) * -(-(2 * n1 - 1) // 32) + -(-(d_out // D) // 32)
+        assert moddowns == expect, (moddowns, expect)
+    want = ck.linear_project_tm(cts_o, W, T, n1, keys_o, out_blocks=oracle_outputs, lazy=lazy)
     say("oracle projection done")
     for j, wo in zip(oracle_outputs, want):
         got = to_host(outs[j].data)
@@ -173,6 +182,12 @@ def test_tm_projection_with_exact_workspace():
     got = to_host(ctx.linear_project(cts, W, T, n1, keys, layout="tm")[0].data)
     ctx.set_workspace(None)
     assert np.array_equal(got, want)
+
+
+def test_toy_tm_projection_lazy_moddown():
+    err = run_case(TOY, 2 * TOY.feats, 3 * TOY.feats, 16, [0, 2], lazy=True)
+    say("toy tm lazy-ModDown max error vs X@W", err)
+    assert err <= 2.0 ** -12
 
 
 def test_toy_tm_projection_lowest_level():
