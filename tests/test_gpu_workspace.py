@@ -134,15 +134,20 @@ def test_projection_with_exact_workspace(env):
     n2 = -(-D // n1)
     keys = {st: ctx.keygen_galois(s, ctx.galois_elt(st), env["ka"], env["ke"])
             for st in [T * b for b in range(1, n1)] + [T * n1 * g for g in range(1, n2)]}
-    want = [to_host(o.data) for o in ctx.linear_project(cts, W, T, n1, keys)]
-    for max_pairs in (0, 5):
-        ctx.set_proj_batch(max_pairs)
-        nbytes = ctx.workspace_bytes(ctx.OP_LINEAR_PROJECT, (L, T, d_in, d_out, n1))
-        say("projection workspace bytes", nbytes, "max pairs", max_pairs)
-        ctx.set_workspace(_ws(env, nbytes))
-        got = [to_host(o.data) for o in ctx.linear_project(cts, W, T, n1, keys)]
-        ctx.set_workspace(None)
-        for g, w in zip(got, want):
-            assert np.array_equal(g, w)
+    # the lazy ModDown's accumulators make the scratch larger: both modes, each against its own arena result
+    for lazy in (False, True):
+        ctx.set_lazy_moddown(lazy)
+        ctx.set_proj_batch(0)
+        want = [to_host(o.data) for o in ctx.linear_project(cts, W, T, n1, keys)]
+        for max_pairs in (0, 5):
+            ctx.set_proj_batch(max_pairs)
+            nbytes = ctx.workspace_bytes(ctx.OP_LINEAR_PROJECT, (L, T, d_in, d_out, n1))
+            say("projection workspace bytes", nbytes, "max pairs", max_pairs, "lazy", lazy)
+            ctx.set_workspace(_ws(env, nbytes))
+            got = [to_host(o.data) for o in ctx.linear_project(cts, W, T, n1, keys)]
+            ctx.set_workspace(None)
+            for g, w in zip(got, want):
+                assert np.array_equal(g, w)
     ctx.set_proj_batch(0)
+    ctx.set_lazy_moddown(False)
     torch.cuda.synchronize()
