@@ -48,35 +48,79 @@ __global__ __launch_bounds__(kThreads) void k_attn_masks(double *U, uint32_t D, 
 
 // Cyclic NTT of length n = 2^LOGN along the first index of s ([n][P] doubles in LDS, |values| < 2q): the
 // Cooley-Tukey loop with natural-order input and bit-reversed output, group i of stage m taking om[m + i] =
-// w_(2m)^brev_(log m)(i) (w_(2m) a primitive 2m-th root of unity).  Every value stays below 2q.
+// w_(2m)^brev_(log m)(i) (w_(2m) a primitive 2m-th root of unity).  Stages run in pairs (m, 2m) with four points
+// per thread (one LDS round trip and one barrier per pair), an odd last stage alone.  Every butterfly keeps its
+// values below 2q.
 template <int LOGN, int P, int NT>
 __device__ __forceinline__ void corr_fwd(double *s, const double *om, const nttc::Ar<true> &ar)
 {
     constexpr int n = 1 << LOGN;
-    for (int m = 1, t = n / 2; m < n; m <<= 1, t >>= 1) {
+#pragma unroll
+    for (int st = 0; st + 1 < LOGN; st += 2) {
+        // stage m (stride t) on (j, j + t), (j + t/2, j + 3t/2); stage 2m (stride t/2) on (j, j + t/2), (j + t, j + 3t/2)
+        const int m = 1 << st, lt = LOGN - 1 - st, t = 1 << lt, h = t >> 1;
+        for (int b = threadIdx.x; b < (n / 4) * P; b += NT) {
+            const int p = b % P, bi = b / P, i = bi >> (lt - 1), j = (i << (lt + 1)) + (bi & (h - 1));
+            double x0 = s[j * P + p], x1 = s[(j + h) * P + p], x2 = s[(j + t) * P + p], x3 = s[(j + t + h) * P + p];
+            const double w = om[m + i];
+            ar.ct(x0, x2, w);
+            ar.ct(x1, x3, w);
+            ar.ct(x0, x1, om[2 * m + 2 * i]);
+            ar.ct(x2, x3, om[2 * m + 2 * i + 1]);
+            s[j * P + p] = x0;
+            s[(j + h) * P + p] = x1;
+            s[(j + t) * P + p] = x2;
+            s[(j + t + h) * P + p] = x3;
+        }
+        __syncthreads();
+    }
+    if (LOGN & 1) {
+        constexpr int m = n / 2;
         for (int b = threadIdx.x; b < (n / 2) * P; b += NT) {
-            const int p = b % P, bi = b / P, i = bi / t, j = 2 * i * t + bi % t;
-            double X = s[j * P + p], Y = s[(j + t) * P + p];
+            const int p = b % P, i = b / P, j = 2 * i;
+            double X = s[j * P + p], Y = s[(j + 1) * P + p];
             ar.ct(X, Y, om[m + i]);
             s[j * P + p] = X;
-            s[(j + t) * P + p] = Y;
+            s[(j + 1) * P + p] = Y;
         }
         __syncthreads();
     }
 }
 
-// Its inverse without the 1/n (Gentleman-Sande, bit-reversed input, natural output, omi[m + i] = om[m + i]^-1).
+// Its inverse without the 1/n (Gentleman-Sande, bit-reversed input, natural output, omi[m + i] = om[m + i]^-1):
+// stages m = n/2 .. 1, an odd first stage alone, then pairs (m, m/2) with four points per thread.
 template <int LOGN, int P, int NT>
 __device__ __forceinline__ void corr_inv(double *s, const double *omi, const nttc::Ar<true> &ar)
 {
     constexpr int n = 1 << LOGN;
-    for (int m = n / 2, t = 1; m >= 1; m >>= 1, t <<= 1) {
+    if (LOGN & 1) {
+        constexpr int m = n / 2;
         for (int b = threadIdx.x; b < (n / 2) * P; b += NT) {
-            const int p = b % P, bi = b / P, i = bi / t, j = 2 * i * t + bi % t;
-            double X = s[j * P + p], Y = s[(j + t) * P + p];
+            const int p = b % P, i = b / P, j = 2 * i;
+            double X = s[j * P + p], Y = s[(j + 1) * P + p];
             ar.gs(X, Y, omi[m + i]);
             s[j * P + p] = X;
-            s[(j + t) * P + p] = Y;
+            s[(j + 1) * P + p] = Y;
+        }
+        __syncthreads();
+    }
+#pragma unroll
+    for (int st = LOGN - 1 - (LOGN & 1); st >= 1; st -= 2) {
+        // stage m (stride t) on (a, a + t), (a + 2t, a + 3t); stage m/2 (stride 2t) on (a, a + 2t), (a + t, a + 3t)
+        const int m = 1 << st, lt = LOGN - 1 - st, t = 1 << lt;
+        for (int b = threadIdx.x; b < (n / 4) * P; b += NT) {
+            const int p = b % P, bi = b / P, i2 = bi >> lt, a = (i2 << (lt + 2)) + (bi & (t - 1));
+            double x0 = s[a * P + p], x1 = s[(a + t) * P + p], x2 = s[(a + 2 * t) * P + p],
+                   x3 = s[(a + 3 * t) * P + p];
+            ar.gs(x0, x1, omi[m + 2 * i2]);
+            ar.gs(x2, x3, omi[m + 2 * i2 + 1]);
+            const double w = omi[m / 2 + i2];
+            ar.gs(x0, x2, w);
+            ar.gs(x1, x3, w);
+            s[a * P + p] = x0;
+            s[(a + t) * P + p] = x1;
+            s[(a + 2 * t) * P + p] = x2;
+            s[(a + 3 * t) * P + p] = x3;
         }
         __syncthreads();
     }
@@ -227,7 +271,8 @@ ckks_status launch_masks(ckks_ctx *ctx, double *U, double *MQ, uint32_t D, uint3
     return launch_enc_vectors(ctx, U, D, hd, delta, L, MQ);
 }
 
-constexpr int kCorrP = 32;  // positions per correlation block
+// positions per correlation block: 32 (n <= 128: 34 KB of LDS, four blocks per CU) or 16 (n = 256)
+constexpr int corr_positions(uint32_t logn) { return logn >= 8 ? 16 : 32; }
 
 // twiddles and transformed masks for the correlation of length n over L limbs: Om, Omi [L][n]; Mh [L][D2][n]
 ckks_status launch_corr_tables(ckks_ctx *ctx, uint32_t logn, uint32_t L, uint32_t D2, uint32_t hd, const double *MQ,
@@ -260,13 +305,14 @@ ckks_status launch_corr(ckks_ctx *ctx, uint64_t *out, const uint64_t *x, uint32_
 {
     const size_t ctw = 2 * (size_t)L * ctx->n;
     const uint32_t n = 1u << logn;
-    const dim3 grid(L * 2 * (uint32_t)(ctx->n / kCorrP));
+    const uint32_t P = (uint32_t)corr_positions(logn);
+    const dim3 grid(L * 2 * (uint32_t)(ctx->n / P));
     const double res = 2.0 * L * ctx->n;
     // the inputs once, the outputs once; two transforms and a product per position
     prof_begin(ctx, K_ATTN_CORR, 8.0 * res * (T + nout), res * (n * logn * 11.0 + 8.0 * n));
 #define CK_CORR(LG)                                                                                                \
-    hipLaunchKernelGGL((k_attn_corr<LG, kCorrP>), grid, dim3(kThreads), 0, ctx->stream, out, x, T, nout, sgn, off, \
-                       ctw, L, ctx->log_n, logT, D2, Om, Omi, Mh, ctx->d_mod)
+    hipLaunchKernelGGL((k_attn_corr<LG, corr_positions(LG)>), grid, dim3(kThreads), 0, ctx->stream, out, x, T, nout, \
+                       sgn, off, ctw, L, ctx->log_n, logT, D2, Om, Omi, Mh, ctx->d_mod)
     switch (logn) {
     case 4: CK_CORR(4); break;
     case 5: CK_CORR(5); break;
