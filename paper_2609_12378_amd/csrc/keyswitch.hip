@@ -103,7 +103,10 @@ __global__ __launch_bounds__(kThreads) void k_conv(const uint64_t *in, uint32_t 
 // products y_i * [Qhat_i]_t (each below 0.875 t in magnitude, since |y_i| < s_i/2 < t) with a range reduction
 // every four terms (sums stay below 4 t < 2^53) and writes the canonical residue: the same integers as k_conv
 // (RAW: the reduced value, |x| <= t/2, as raw double bits, for a following fp64 transform pass).
-template <int NS_MAX, bool RAW>
+// C coefficients per thread (kThreads apart, so every load and store stays coalesced): the per-target constants
+// come from LDS once for all C, and the C product chains are independent.  EXACT: ns == NS_MAX, so the source
+// loop has no guards and all source loads issue before the first is used.
+template <int NS_MAX, bool RAW, int C, bool EXACT = false>
 __global__ __launch_bounds__(kThreads) void k_conv_f64(const uint64_t *in, uint32_t in_stride, uint64_t *out,
                                                         uint32_t out_stride, uint32_t split, uint32_t skip,
                                                         ConvArgs a, const double *__restrict__ qhat_inv,
@@ -112,23 +115,44 @@ __global__ __launch_bounds__(kThreads) void k_conv_f64(const uint64_t *in, uint3
 {
     __shared__ double s_mod[NS_MAX * kMaxPrimes];
     __shared__ double2 s_tq[kMaxPrimes];
-    const int ns = a.ns, nt = a.nt;
+    const int ns = EXACT ? NS_MAX : a.ns, nt = a.nt;
     for (int k = threadIdx.x; k < ns * nt; k += kThreads) s_mod[k] = qhat_mod[k];
     for (int k = threadIdx.x; k < nt; k += kThreads) s_tq[k] = make_double2(mods[a.dst[k]].qd, mods[a.dst[k]].qinvd);
     __syncthreads();
     const uint32_t n = 1u << log_n;
-    const uint32_t col = blockIdx.x * kThreads + threadIdx.x;
+    const uint32_t col = blockIdx.x * (kThreads * C) + threadIdx.x;
     const uint32_t poly = blockIdx.y;
-    if (col >= n) return;
+    if (col >= n) return;  // n is a multiple of kThreads * C
     const uint64_t *src = in + ((size_t)poly * in_stride << log_n) + col;
-    double y[NS_MAX];
+    double y[C][NS_MAX];
+    if (EXACT) {
+        uint64_t raw[C][NS_MAX];
+#pragma unroll
+        for (int i = 0; i < NS_MAX; i++)
+#pragma unroll
+            for (int c = 0; c < C; c++) raw[c][i] = src[((size_t)i << log_n) + c * kThreads];
+#pragma unroll
+        for (int i = 0; i < NS_MAX; i++) {
+            const nttc::Ar<true> ar(mods[a.src[i]]);
+            const double h = 0.5 * ar.q;
+#pragma unroll
+            for (int c = 0; c < C; c++) {
+                const double v = ar.mul(nttc::Ar<true>::from_u64(raw[c][i]), qhat_inv[i]);
+                y[c][i] = v > h ? v - ar.q : (v < -h ? v + ar.q : v);
+            }
+        }
+    }
 #pragma unroll
     for (int i = 0; i < NS_MAX; i++) {
-        if (i < ns) {
+        if (!EXACT && i < ns) {
             const nttc::Ar<true> ar(mods[a.src[i]]);
-            const double v = ar.mul(nttc::Ar<true>::from_u64(src[(size_t)i << log_n]), qhat_inv[i]);
             const double h = 0.5 * ar.q;
-            y[i] = v > h ? v - ar.q : (v < -h ? v + ar.q : v);
+#pragma unroll
+            for (int c = 0; c < C; c++) {
+                const double v = ar.mul(nttc::Ar<true>::from_u64(src[((size_t)i << log_n) + c * kThreads]),
+                                        qhat_inv[i]);
+                y[c][i] = v > h ? v - ar.q : (v < -h ? v + ar.q : v);
+            }
         }
     }
     uint64_t *dst = out + ((size_t)poly * out_stride << log_n) + col;
@@ -136,16 +160,25 @@ __global__ __launch_bounds__(kThreads) void k_conv_f64(const uint64_t *in, uint3
         nttc::Ar<true> ar;
         ar.q = s_tq[t].x;
         ar.qinv = s_tq[t].y;
-        double acc = 0.0;
+        double acc[C];
+#pragma unroll
+        for (int c = 0; c < C; c++) acc[c] = 0.0;
 #pragma unroll
         for (int i = 0; i < NS_MAX; i++) {
-            if (i < ns) {
-                acc += ar.mul(y[i], s_mod[i * nt + t]);
-                if ((i & 3) == 3) acc = ar.red(acc);
+            if (EXACT || i < ns) {
+                const double w = s_mod[i * nt + t];
+#pragma unroll
+                for (int c = 0; c < C; c++) {
+                    acc[c] += ar.mul(y[c][i], w);
+                    if ((i & 3) == 3) acc[c] = ar.red(acc[c]);
+                }
             }
         }
         const uint32_t row = t < (int)split ? t : t + skip;
-        dst[(size_t)row << log_n] = RAW ? nttc::Ar<true>::to_raw(ar.red(acc)) : ar.to_canon(acc);
+#pragma unroll
+        for (int c = 0; c < C; c++)
+            dst[((size_t)row << log_n) + c * kThreads] =
+                RAW ? nttc::Ar<true>::to_raw(ar.red(acc[c])) : ar.to_canon(acc[c]);
     }
 }
 
@@ -403,18 +436,33 @@ ckks_status launch_conv(ckks_ctx *ctx, const ConvDev *cd, const uint64_t *in, ui
     for (int i = 0; i < cd->ns; i++) a.src[i] = cd->src[i];
     for (int t = 0; t < cd->nt; t++) a.dst[t] = cd->dst[t];
     const dim3 grid((ctx->n + kThreads - 1) / kThreads, polys), block(kThreads);
+    // fp64 kernels: two coefficients per thread where the ring has at least 512 of them
+    const bool two = ctx->n % (2 * kThreads) == 0;
+    const dim3 grid2(two ? (uint32_t)(ctx->n / (2 * kThreads)) : grid.x, polys);
     prof_begin(ctx, K_CONV, 8.0 * polys * (a.ns + a.nt) * ctx->n);
+#define CK_CONVF(NSM, RAWV)                                                                                        \
+    do {                                                                                                           \
+        if (two && a.ns == NSM)                                                                                    \
+            hipLaunchKernelGGL((k_conv_f64<NSM, RAWV, 2, true>), grid2, block, 0, ctx->stream, in, in_stride, out,  \
+                               out_stride, split, skip, a, cd->d_qhat_inv_f, cd->d_qhat_mod_f, ctx->d_mod,          \
+                               ctx->log_n);                                                                        \
+        else if (two)                                                                                              \
+            hipLaunchKernelGGL((k_conv_f64<NSM, RAWV, 2>), grid2, block, 0, ctx->stream, in, in_stride, out,        \
+                               out_stride, split, skip, a, cd->d_qhat_inv_f, cd->d_qhat_mod_f, ctx->d_mod,          \
+                               ctx->log_n);                                                                        \
+        else                                                                                                       \
+            hipLaunchKernelGGL((k_conv_f64<NSM, RAWV, 1>), grid, block, 0, ctx->stream, in, in_stride, out,         \
+                               out_stride, split, skip, a, cd->d_qhat_inv_f, cd->d_qhat_mod_f, ctx->d_mod,          \
+                               ctx->log_n);                                                                        \
+    } while (0)
     if (raw) {
         CK_REQUIRE(cd->f64 && !ctx->int_only && a.ns <= 8, CKKS_EINVAL, "raw conversion needs the fp64 tables");
-        hipLaunchKernelGGL((k_conv_f64<8, true>), grid, block, 0, ctx->stream, in, in_stride, out, out_stride, split,
-                           skip, a, cd->d_qhat_inv_f, cd->d_qhat_mod_f, ctx->d_mod, ctx->log_n);
+        CK_CONVF(8, true);
     } else if (cd->f64 && !ctx->int_only && a.ns <= 16) {
         if (a.ns <= 8)
-            hipLaunchKernelGGL((k_conv_f64<8, false>), grid, block, 0, ctx->stream, in, in_stride, out, out_stride,
-                               split, skip, a, cd->d_qhat_inv_f, cd->d_qhat_mod_f, ctx->d_mod, ctx->log_n);
+            CK_CONVF(8, false);
         else
-            hipLaunchKernelGGL((k_conv_f64<16, false>), grid, block, 0, ctx->stream, in, in_stride, out, out_stride,
-                               split, skip, a, cd->d_qhat_inv_f, cd->d_qhat_mod_f, ctx->d_mod, ctx->log_n);
+            CK_CONVF(16, false);
     } else if (a.ns <= 4)
         hipLaunchKernelGGL(k_conv<4>, grid, block, 0, ctx->stream, in, in_stride, out, out_stride, split, skip, a,
                            cd->d_qhat_inv, cd->d_qhat_mod, cd->d_neg_q, ctx->d_mod, ctx->log_n);
@@ -431,6 +479,7 @@ ckks_status launch_conv(ckks_ctx *ctx, const ConvDev *cd, const uint64_t *in, ui
         prof_end(ctx, K_CONV);
         return set_error(CKKS_EUNSUPPORTED, "basis conversion from %d limbs (at most 32)", a.ns);
     }
+#undef CK_CONVF
     prof_end(ctx, K_CONV);
     HIP_TRY(hipGetLastError());
     return CKKS_OK;
