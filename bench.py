@@ -307,6 +307,31 @@ def check_projection(np, st, outs, blocks=(0, 27, 55)):
     return max(errs) if errs else None
 
 
+COPY = {"GBps": None}
+
+
+def measure_copy(torch, ctx, mib=1024, reps=3):
+    """Measured HBM rate of a plain device copy (read + write bytes over time) of a buffer far larger than the
+    caches: the practical ceiling next to the nominal 8 TB/s."""
+    src = torch.ones(mib << 17, dtype=torch.uint64, device="cuda")
+    dst = torch.empty_like(src)
+    ctx.calib_copy(dst, src)
+    with Timer(torch) as t:
+        for _ in range(reps):
+            ctx.calib_copy(dst, src)
+    del src, dst
+    COPY["GBps"] = 2.0 * (mib << 20) * reps / (t.ms * 1e-3) / 1e9
+    return COPY["GBps"]
+
+
+def hbm_fracs(gbs):
+    out = {"frac": gbs / HBM_PEAK_GBS}
+    if COPY["GBps"]:
+        out["copy_GBps"] = COPY["GBps"]
+        out["frac_of_copy"] = gbs / COPY["GBps"]
+    return out
+
+
 def roofline(prof):
     """The kernel with the most total time, against the HBM roof and the VALU issue roof.
 
@@ -318,7 +343,7 @@ def roofline(prof):
     name, (ms, cnt, by, ops) = max(prof.items(), key=lambda kv: kv[1][0])
     sec = ms * 1e-3
     gbs = by / sec / 1e9
-    hbm = {"achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": gbs / HBM_PEAK_GBS}
+    hbm = {"achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s", **hbm_fracs(gbs)}
     out = {"kernel": name, "launches": cnt, "avg_ms": ms / cnt, "bytes_per_launch": by / cnt}
     alu = None
     if ops:
@@ -408,8 +433,8 @@ def bench_keyswitch(torch, np, steps, warmup):
     res = {"workload": "32 hoisted rotations by 1..32 of one level-23 ciphertext, N=2^16, L=24+K=8, dnum=3",
            "ms_per_batch": ms, "rotations_per_s": cfg.batch / (ms * 1e-3), "decrypt_err_last": err,
            "roofline": {"bound": "hbm", "algorithmic_bytes_per_batch": kbytes,
-                        "achieved": kbytes / (kms * 1e-3) / 1e9, "peak": 8000.0, "unit": "GB/s",
-                        "frac": kbytes / (kms * 1e-3) / 1e9 / 8000.0},
+                        "achieved": kbytes / (kms * 1e-3) / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                        **hbm_fracs(kbytes / (kms * 1e-3) / 1e9)},
            "kernels_ms": {k: v[0] / steps for k, v in prof.items()},
            "kernels_GBps": {k: v[2] / (v[0] * 1e-3) / 1e9 for k, v in prof.items() if v[0] > 0}}
     del keys, outs, ct, ctx
@@ -439,10 +464,10 @@ def bench_ntt(torch, steps):
            "algorithmic_bytes_per_direction": algo,
            "fwd_GBps": algo / (tf.ms / steps * 1e-3) / 1e9, "inv_GBps": algo / (ti.ms / steps * 1e-3) / 1e9,
            "kernels": {k: {"avg_ms": v[0] / v[1], "GBps": v[2] / (v[0] * 1e-3) / 1e9,
-                           "hbm_frac": v[2] / (v[0] * 1e-3) / 1e9 / 8000.0} for k, v in prof.items()}}
+                           **hbm_fracs(v[2] / (v[0] * 1e-3) / 1e9)} for k, v in prof.items()}}
     # per transform (one read and one write of every residue) against 8 TB/s; each two-pass transform moves twice that
-    res["fwd_hbm_frac"] = res["fwd_GBps"] / 8000.0
-    res["inv_hbm_frac"] = res["inv_GBps"] / 8000.0
+    res["fwd_hbm"] = hbm_fracs(res["fwd_GBps"])
+    res["inv_hbm"] = hbm_fracs(res["inv_GBps"])
     del x, ctx
     return res
 
@@ -546,6 +571,50 @@ def cpu_baseline(np, cfg, budget_s=20.0):
                       "56 rescales" % (n_pts, t_pt, t_rot, t_rs)}
 
 
+def cpu_oracle_secondary(np):
+    """The oracle's rates on the NTT and key-switching workloads, from small samples (threads as for the
+    projection baseline): one 2^16-point negacyclic NTT row, and a one- and a two-rotation hoisted call at the
+    key-switching parameters (their difference is one rotation's inner product and ModDown, the rest the shared
+    ModUp), extrapolated to 64 x 36 rows and to 32 hoisted rotations."""
+    from oracle import Ckks, gen_primes
+    from workloads import KEYSWITCH as kcfg, NTT_BENCH as ncfg, gaussian_error, rng, ternary_secret, \
+        uniform_residues, uniform_slots
+    out = {}
+    pr = gen_primes(ncfg.q_bits, 2 * ncfg.n, 1)
+    ck = Ckks(ncfg.log_n, pr)
+    a = uniform_residues(rng(ncfg.index, 1), pr, ck.n)
+    t0 = time.time()
+    reps = 0
+    while time.time() - t0 < 2.0 or reps < 2:
+        ck.ntt(a, [0])
+        reps += 1
+    t_row = (time.time() - t0) / reps
+    out["ntt"] = {"s_per_direction": t_row * ncfg.batch * ncfg.n_q, "row_s": t_row,
+                  "sample": "%d forward NTT rows of 2^16 residues, scaled by 64 x 36 rows" % reps}
+    pr = gen_primes(kcfg.q_bits, 2 * kcfg.n, kcfg.n_q + kcfg.n_p)
+    ck = Ckks(kcfg.log_n, pr[:kcfg.n_q], pr[kcfg.n_q:], kcfg.dnum)
+    n, L = ck.n, kcfg.level + 1
+    s = ternary_secret(rng(kcfg.index, 3), n)
+    ge = rng(kcfg.index, 4)
+    ct = ck.encrypt(s, ck.encode(uniform_slots(rng(kcfg.index, 1), n // 2), None, 2.0 ** 40, L),
+                    uniform_residues(ge, ck.q[:L], n), gaussian_error(ge, n))
+    gk = rng(kcfg.index, 5)
+    keys = [ck.keygen_galois(s, ck.galois_elt(r), uniform_residues(gk, ck.primes, n, lead=(kcfg.dnum,)),
+                             gaussian_error(gk, (kcfg.dnum, n))) for r in (1, 2)]
+    t0 = time.time()
+    ck.rotate_hoisted(ct, [1], keys[:1])
+    t1 = time.time() - t0
+    t0 = time.time()
+    ck.rotate_hoisted(ct, [1, 2], keys)
+    t2 = time.time() - t0
+    per_rot = max(t2 - t1, 1e-9)
+    batch = max(t1 - per_rot, 0.0) + kcfg.batch * per_rot
+    out["keyswitch"] = {"rotations_per_s": kcfg.batch / batch, "s_per_batch": batch,
+                        "sample": "hoisted calls of 1 and 2 rotations at level 23 (%.2f s, %.2f s), scaled to 32"
+                                  % (t1, t2)}
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -592,6 +661,7 @@ def main():
     log("setup: projection 4096 -> 14336")
     st = setup_projection(torch, np, cfg)
     ctx = st["ctx"]
+    log("copy calibration: %.0f GB/s" % measure_copy(torch, ctx))
     if args.calib_copy_mib:
         src = torch.ones(args.calib_copy_mib << 17, dtype=torch.uint64, device="cuda")
         dst = torch.empty_like(src)
@@ -640,6 +710,11 @@ def main():
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle sample)")
         cpu = cpu_baseline(np, cfg)
+        if secondary:
+            log("oracle samples: NTT and key switching")
+            for k, v in cpu_oracle_secondary(np).items():
+                v["cores"] = cpu["cores"]
+                secondary[k]["cpu_oracle"] = v
     line = {
         "metric": METRIC,
         "value": ms / 1e3,
@@ -659,6 +734,7 @@ def main():
         "roofline": roof,
         "cpu_baseline": cpu,
         "decrypt_max_abs_err": err,
+        "copy_GBps": COPY["GBps"],
         "kernels_ms_per_step": kernels_ms,
         "secondary": secondary,
     }
