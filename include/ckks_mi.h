@@ -299,12 +299,12 @@ typedef struct {
  * query c uses key k_of_q[c].  Output c holds, at slot t*D + h*hd + delta,
  *   S[t, h, delta] = sum_d Q[t, h, d] K[(t + delta) mod T, d]   (delta < T)
  * and 0 for T <= delta < hd, computed as
- *   P_delta = Rescale(Relin(Rot_{-delta}(Q) x Rot_{delta(D-1)}(K')))
- *   out = Rescale(sum_{k<hd} Rot_k(sum_delta M_{(delta+k) mod hd} * P_delta))
+ *   P_delta = Relin(Rot_{-delta}(Q) x Rot_{delta(D-1)}(K'))
+ *   out = Rescale(Rescale(sum_{k<hd} Rot_k(sum_delta M_{(delta+k) mod hd} * P_delta)))
  * with M_c the 0/1 mask of head position c, a periodic plaintext at scale
- * q_(level-1).  Inputs: n_limbs = level + 1 >= 3, equal within q and within k,
+ * q_level.  Inputs: n_limbs = level + 1 >= 3, equal within q and within k,
  * equal scales within each; out[c]: n_limbs = level - 1, scale set to
- * scale(q) scale(k) / q_level.  Keys (Galois, key_steps[r] -> dev_keys[r]):
+ * scale(q) scale(k) / q_(level-1).  Keys (Galois, key_steps[r] -> dev_keys[r]):
  * steps -delta and delta (D-1) for 0 < delta < T, and 1 .. hd-1; dev_rlk: the
  * relinearisation key.  All device memory is the caller's; scratch from the
  * arena or workspace (CKKS_OP_ATTN_SCORES).  Errors: CKKS_EINVAL (shapes,

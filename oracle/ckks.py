@@ -607,18 +607,19 @@ class Ckks:
         for delta < T, 0 for T <= delta < hd: the scores on token diagonals (the S_Delta of Section "C--Delta
         Attention Layout and Computation", for which the paper gives no construction; this one is QK^T as Mult
         plus rotation sums):
-            P_delta = Rescale(Relin(Rot_{-delta}(Q) x Rot_{delta (D-1)}(K')))        (0 <= delta < T)
-            out     = Rescale( sum_k Rot_k( sum_delta M_{(delta + k) mod hd} * P_delta ) )   (0 <= k < hd)
+            P_delta = Relin(Rot_{-delta}(Q) x Rot_{delta (D-1)}(K'))                  (0 <= delta < T)
+            out     = Rescale(Rescale( sum_k Rot_k( sum_delta M_{(delta + k) mod hd} * P_delta ) ))  (0 <= k < hd)
         With the left rotation (Rot_k x)[s] = x[s + k], slot t*D + h*hd + delta + d of P_delta holds
         Q[t, h, d] K[t + delta, d]; M_c selects head position c, so the term k brings position delta + k of
         P_delta to position delta: the sum over k is the dot product over d, placed at position delta.
-        The masks are periodic plaintexts encoded at scale q_(level-1), so the output scale is
-        scale(Q) scale(K) / q_level.  Keys: -delta and delta (D - 1) (0 < delta < T), k (0 < k < hd).  With `lazy`
-        the hd - 1 rotations of the outer sum share one ModDown (rotate_sum_lazy)."""
+        The masks are periodic plaintexts encoded at scale q_level and multiply the products at the inputs' level
+        (no rescale in between); the two rescales at the end divide by q_level and q_(level-1), so the output
+        scale is scale(Q) scale(K) / q_(level-1).  Keys: -delta and delta (D - 1) (0 < delta < T), k (0 < k < hd).
+        With `lazy` the hd - 1 rotations of the outer sum share one ModDown (rotate_sum_lazy)."""
         level = self.level_of(q_cts[0])
         D = (self.n // 2) // T
         assert T <= hd and D % hd == 0 and level >= 2
-        masks = [self.encode_periodic(self.attention_mask(D, hd, c), float(self.q[level - 1]), level)
+        masks = [self.encode_periodic(self.attention_mask(D, hd, c), float(self.q[level]), level + 1)
                  for c in range(hd)]
         bcache = {}
         outs = []
@@ -630,7 +631,7 @@ class Ckks:
             B = bcache[kk]
             st = [-d for d in range(1, T)]
             A = [q] + self.rotate_hoisted(q, st, [keys[s] for s in st])
-            P = [self.rescale(self.mul_relin(A[d], B[d], rlk)) for d in range(T)]
+            P = [self.mul_relin(A[d], B[d], rlk) for d in range(T)]
             total = None
             for k in range(hd):
                 U = None
@@ -638,7 +639,7 @@ class Ckks:
                     term = self.ct_mul_plain(P[d], masks[(d + k) % hd])
                     U = term if U is None else self.ct_add(U, term)
                 total = self._giant_step(total, U, k, k, keys, lazy)
-            outs.append(self.rescale(self._giant_finish(total, lazy)))
+            outs.append(self.rescale(self.rescale(self._giant_finish(total, lazy))))
         return outs
 
     def attention_apply(self, p_cts: Sequence[np.ndarray], v_cts: Sequence[np.ndarray], v_of_p: Sequence[int],

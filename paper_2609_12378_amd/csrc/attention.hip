@@ -8,8 +8,8 @@
 //
 // Scores.  Query ciphertext c holds D/hd heads (slot t*D + h*hd + d = Q[t, h, d]); its key ciphertext holds
 // one key head repeated in every head position.  With the left rotation (Rot_k x)[s] = x[s + k]:
-//   P_delta = Rescale(Relin(Rot_{-delta}(Q) x Rot_{delta (D-1)}(K')))                       0 <= delta < T
-//   out     = Rescale( sum_k Rot_k( U_k ) ),  U_k = sum_delta M_{(delta + k) mod hd} * P_delta    0 <= k < hd
+//   P_delta = Relin(Rot_{-delta}(Q) x Rot_{delta (D-1)}(K'))                                 0 <= delta < T
+//   out     = Rescale(Rescale( sum_k Rot_k( U_k ) )),  U_k = sum_delta M_{(delta + k) mod hd} * P_delta  0 <= k < hd
 // and slot t*D + h*hd + delta of out holds sum_d Q[t, h, d] K[(t + delta) mod T, d] (zero for delta >= T).
 // The masks M_c (1 on head position c) are slot vectors of period D, so their plaintexts are constant on
 // runs of T consecutive NTT positions, with values m[c] on a run.  At one NTT position the sums over delta are
@@ -381,24 +381,23 @@ struct ScoreScratch {
 ScoreScratch score_scratch(const ckks_ctx *ctx, uint32_t L, uint32_t D, uint32_t T, uint32_t hd)
 {
     ScoreScratch s{};
-    const size_t N = ctx->n, ctw = 2 * (size_t)L * N, ctw1 = 2 * (size_t)(L - 1) * N;
+    const size_t N = ctx->n, ctw = 2 * (size_t)L * N;
     const uint32_t level = L - 1;
     s.Jt = kRotChunk;
     s.logn = log2u(hd);
     s.u_w = (size_t)hd * D;
-    s.mq_w = (size_t)(L - 1) * 2 * D * hd;
-    s.tw_w = (size_t)2 * (L - 1) * hd;
-    s.mh_w = (size_t)(L - 1) * 2 * D * hd;
+    s.mq_w = (size_t)L * 2 * D * hd;
+    s.tw_w = (size_t)2 * L * hd;
+    s.mh_w = (size_t)L * 2 * D * hd;
     s.b_w = s.a_w = s.pr_w = (size_t)T * ctw;
     s.d_w = (size_t)T * 3 * L * N;
-    s.ub_w = (size_t)hd * ctw1;
-    s.rot_w = (size_t)s.Jt * ctw1;
-    s.tot_w = ctw1;
-    s.ua_w = (size_t)2 * (L - 1 + ctx->n_p) * N;  // the outer sum over Q u P (lazy ModDown)
+    s.ub_w = (size_t)hd * ctw;
+    s.rot_w = (size_t)s.Jt * ctw;
+    s.tot_w = ctw;
+    s.ua_w = (size_t)2 * (L + ctx->n_p) * N;  // the outer sum over Q u P (lazy ModDown)
     s.work_w = std::max({ks_scratch_words(ctx, level, ks_rot_batch(T - 1)),
                          ks_scratch_words(ctx, level, ks_rot_batch(T), T),
-                         ks_scratch_words(ctx, level - 1, ks_rot_batch(s.Jt), s.Jt),
-                         (size_t)2 * T * (1 + level) * N});
+                         ks_scratch_words(ctx, level, ks_rot_batch(s.Jt), s.Jt), (size_t)2 * (1 + level) * N});
     s.total = s.u_w + s.mq_w + s.tw_w + s.mh_w + s.b_w + s.a_w + s.d_w + s.pr_w + s.ub_w + s.rot_w + s.tot_w +
               s.ua_w + s.work_w;
     return s;
@@ -525,7 +524,7 @@ extern "C" ckks_status ckks_attention_scores(ckks_ctx *ctx, const ckks_buf *q, u
         }
     }
 
-    const size_t N = ctx->n, ctw = 2 * (size_t)L * N, ctw1 = 2 * (size_t)(L - 1) * N;
+    const size_t N = ctx->n, ctw = 2 * (size_t)L * N;
     const ScoreScratch ss = score_scratch(ctx, L, D, T, hd);
     void *w;
     CK_TRY(ctx_scratch(ctx, ss.total * 8, &w));
@@ -534,19 +533,18 @@ extern "C" ckks_status ckks_attention_scores(ckks_ctx *ctx, const ckks_buf *q, u
     double *Om = MQ + ss.mq_w, *Omi = Om + ss.tw_w / 2;
     double *Mh = Om + ss.tw_w;
     uint64_t *B = (uint64_t *)(Mh + ss.mh_w);  // [T][2][L][N] rotated keys
-    uint64_t *A = B + ss.b_w;                  // [T][2][L][N] rotated queries, then P_delta ([T][2][L-1][N])
+    uint64_t *A = B + ss.b_w;                  // [T][2][L][N] rotated queries
     uint64_t *Dt = A + ss.a_w;                 // [T][3][L][N] products
-    uint64_t *Pr = Dt + ss.d_w;                // [T][2][L][N] relinearised products
-    uint64_t *Ub = Pr + ss.pr_w;               // [hd][2][L-1][N] U_k
-    uint64_t *rot = Ub + ss.ub_w;              // [Jt][2][L-1][N]
+    uint64_t *Pr = Dt + ss.d_w;                // [T][2][L][N] relinearised products P_delta
+    uint64_t *Ub = Pr + ss.pr_w;               // [hd][2][L][N] U_k
+    uint64_t *rot = Ub + ss.ub_w;              // [Jt][2][L][N]
     uint64_t *tot = rot + ss.rot_w;
-    uint64_t *uacc = tot + ss.tot_w;           // [2][L-1+K][N]
+    uint64_t *uacc = tot + ss.tot_w;           // [2][L+K][N]
     uint64_t *work = uacc + ss.ua_w;
 
-    // the masks at scale q_(level-1) (the products are multiplied by them after their first rescale), and
-    // their correlation form
-    CK_TRY(launch_masks(ctx, U, MQ, D, hd, (double)ctx->primes[level - 1], L - 1));
-    CK_TRY(launch_corr_tables(ctx, ss.logn, L - 1, 2 * D, hd, MQ, Om, Omi, Mh));
+    // the masks at scale q_level (they multiply the products at the inputs' level), and their correlation form
+    CK_TRY(launch_masks(ctx, U, MQ, D, hd, (double)ctx->primes[level], L));
+    CK_TRY(launch_corr_tables(ctx, ss.logn, L, 2 * D, hd, MQ, Om, Omi, Mh));
     // queries grouped by key: each key's rotations are computed once
     std::vector<uint32_t> order(n_q);
     for (uint32_t c = 0; c < n_q; c++) order[c] = c;
@@ -566,7 +564,7 @@ extern "C" ckks_status ckks_attention_scores(ckks_ctx *ctx, const ckks_buf *q, u
         for (uint32_t d = 1; d < T; d++) outs[d - 1] = A + (size_t)d * ctw;
         CK_TRY(rotate_core(ctx, q[c].data, level, qsteps.data(), qkeys.data(), T - 1, outs.data(), work));
         // 2. products, relinearised in one batch (key switching with sigma = identity and the relinearisation
-        //    key: (d0 + u0, u1), then d1 added), rescaled
+        //    key: (d0 + u0, u1), then d1 added)
         for (uint32_t d = 0; d < T; d++) {
             uint64_t *dd = Dt + (size_t)d * 3 * L * N;
             CK_TRY(launch_tensor(ctx, dd, dd + L * N, dd + 2 * L * N, A + (size_t)d * ctw, B + (size_t)d * ctw, L));
@@ -595,32 +593,31 @@ extern "C" ckks_status ckks_attention_scores(ckks_ctx *ctx, const ckks_buf *q, u
                 CK_TRY(launch_binary(ctx, po[d] + (size_t)L * N, po[d] + (size_t)L * N, c0s[d] + (size_t)L * N, L,
                                      limb_range(0, L), EW_ADD));
         }
-        uint64_t *Pd = A;  // [T][2][L-1][N]
-        CK_TRY(rescale_many(ctx, Pr, T, level, Pd, work));
         // 3. U_k = sum_delta M_{(delta + k) mod hd} P_delta = z[-k mod hd] for every k, then each rotated by k
         //    (in chunks) and summed
-        CK_TRY(launch_corr(ctx, Ub, Pd, T, hd, -1, 0, L - 1, ss.logn, logT, 2 * D, Om, Omi, Mh));
+        CK_TRY(launch_corr(ctx, Ub, Pr, T, hd, -1, 0, L, ss.logn, logT, 2 * D, Om, Omi, Mh));
         if (ctx->lazy_moddown) {
             // the hd - 1 key-switching sums accumulated over Q u P, one ModDown, U_0 added in it
             for (uint32_t k0 = 1; k0 < hd; k0 += ss.Jt) {
                 const uint32_t cnt = std::min(ss.Jt, hd - k0);
-                CK_TRY(rotate_each_lazy(ctx, Ub + (size_t)k0 * ctw1, ctw1, cnt, level - 1, osteps.data() + (k0 - 1),
+                CK_TRY(rotate_each_lazy(ctx, Ub + (size_t)k0 * ctw, ctw, cnt, level, osteps.data() + (k0 - 1),
                                         okeys.data() + (k0 - 1), uacc, k0 > 1, work));
             }
-            CK_TRY(ks_moddown(ctx, uacc, 2, level - 1, Ub, 1, Ub + (size_t)(L - 1) * N, tot, work));
+            CK_TRY(ks_moddown(ctx, uacc, 2, level, Ub, 1, Ub + (size_t)L * N, tot, work));
         } else {
-            CK_TRY(launch_sum_cts(ctx, tot, Ub, 1, ctw1, L - 1, false));
+            CK_TRY(launch_sum_cts(ctx, tot, Ub, 1, ctw, L, false));
             for (uint32_t k0 = 1; k0 < hd; k0 += ss.Jt) {
                 const uint32_t cnt = std::min(ss.Jt, hd - k0);
-                for (uint32_t r = 0; r < cnt; r++) outs[r] = rot + (size_t)r * ctw1;
-                CK_TRY(rotate_each(ctx, Ub + (size_t)k0 * ctw1, ctw1, cnt, level - 1, osteps.data() + (k0 - 1),
+                for (uint32_t r = 0; r < cnt; r++) outs[r] = rot + (size_t)r * ctw;
+                CK_TRY(rotate_each(ctx, Ub + (size_t)k0 * ctw, ctw, cnt, level, osteps.data() + (k0 - 1),
                                    okeys.data() + (k0 - 1), outs.data(), work));
-                CK_TRY(launch_sum_cts(ctx, tot, rot, cnt, ctw1, L - 1, true));
+                CK_TRY(launch_sum_cts(ctx, tot, rot, cnt, ctw, L, true));
             }
         }
-        // 4. the final rescale
-        CK_TRY(rescale_core(ctx, tot, level - 1, out[c].data, work));
-        out[c].scale = q[c].scale * k[kk].scale / (double)ctx->primes[level];
+        // 4. the two rescales (by q_level, the masks' scale, and by q_(level-1))
+        CK_TRY(rescale_core(ctx, tot, level, rot, work));
+        CK_TRY(rescale_core(ctx, rot, level - 1, out[c].data, work));
+        out[c].scale = q[c].scale * k[kk].scale / (double)ctx->primes[level - 1];
     }
     return CKKS_OK;
 }

@@ -103,7 +103,7 @@ def run_parity(cfg, n_q, n_kv, kv_of_q, lazy=False):
     S_o = ck.attention_scores(list(q_o), list(k_o), kv_of_q, T, hd, rlk_o, keys_o, lazy=lazy)
     O_o = ck.attention_apply(S_o, list(v_o), kv_of_q, T, hd, rlk_o, keys_o)
     say("oracle attention done")
-    s_scale = delta * delta / ctx.q[level]
+    s_scale = delta * delta / ctx.q[level - 1]
     o_scale = s_scale * delta / ctx.q[level - 2]
     errs_s, errs_o = [], []
     for c in range(n_q):

@@ -166,7 +166,7 @@ def test_toy_attention_scores_accuracy(toy_attention):
     t = toy_attention
     ck, T, D, hd = t["ck"], t["T"], t["D"], t["hd"]
     assert t["S"].shape == (2, ATTN_TOY.level - 1, ck.n)
-    scale = t["delta"] * t["delta"] / ck.q[ATTN_TOY.level]
+    scale = t["delta"] * t["delta"] / ck.q[ATTN_TOY.level - 1]
     z = ck.decode(ck.decrypt(t["s"], t["S"]), scale)
     want = scores_def(t["Q"], t["K"], T, D, hd)
     err = np.max(np.abs(z.real.reshape(T, D) - want))
@@ -179,7 +179,7 @@ def test_toy_attention_apply_accuracy(toy_attention):
     ck, T, D, hd = t["ck"], t["T"], t["D"], t["hd"]
     ls = ATTN_TOY.level - 2
     assert t["O"].shape == (2, ls, ck.n)
-    s_scale = t["delta"] * t["delta"] / ck.q[ATTN_TOY.level]
+    s_scale = t["delta"] * t["delta"] / ck.q[ATTN_TOY.level - 1]
     o_scale = s_scale * t["delta"] / ck.q[ls]
     z = ck.decode(ck.decrypt(t["s"], t["O"]), o_scale)
     S = scores_def(t["Q"], t["K"], T, D, hd)
@@ -195,7 +195,7 @@ def test_toy_attention_scores_lazy_outer_sum(toy_attention):
     t = toy_attention
     ck, T, D, hd = t["ck"], t["T"], t["D"], t["hd"]
     assert t["S_lazy"].shape == t["S"].shape
-    scale = t["delta"] * t["delta"] / ck.q[ATTN_TOY.level]
+    scale = t["delta"] * t["delta"] / ck.q[ATTN_TOY.level - 1]
     z = ck.decode(ck.decrypt(t["s"], t["S_lazy"]), scale)
     err = np.max(np.abs(z.real.reshape(T, D) - scores_def(t["Q"], t["K"], T, D, hd)))
     assert err < 2.0 ** -30, err
