@@ -415,16 +415,19 @@ def bench_keyswitch(torch, np, steps, warmup):
     outs = ctx.rotate_hoisted(ct, rsteps, keys)
     for _ in range(warmup):
         ctx.rotate_hoisted(ct, rsteps, keys, outs)
+    # each batch bracketed by its own events: the median over the runs, and the kernels' profile over all
     ctx.profile(True)
     ctx.profile_reset()
-    with Timer(torch) as t:
-        for _ in range(steps):
+    runs = []
+    for _ in range(steps):
+        with Timer(torch) as t:
             ctx.rotate_hoisted(ct, rsteps, keys, outs)
+        runs.append(t.ms)
     prof = ctx.profile_all()
     ctx.profile(False)
     re, _ = ctx.decode(ctx.decrypt(s, outs[-1]))
     err = float(np.max(np.abs(re.cpu().numpy() - np.roll(z, -rsteps[-1]))))
-    ms = t.ms / steps
+    ms = float(np.median(runs))
     # HBM roofline of the batch: the algorithmic bytes the library's profiler tags on every key-switching launch
     # (each input and output word once per launch; cache-resident gathers of the shared digits and c0 not
     # counted), over the kernels' summed time
@@ -432,6 +435,7 @@ def bench_keyswitch(torch, np, steps, warmup):
     kms = sum(v[0] for v in prof.values()) / steps
     res = {"workload": "32 hoisted rotations by 1..32 of one level-23 ciphertext, N=2^16, L=24+K=8, dnum=3",
            "ms_per_batch": ms, "rotations_per_s": cfg.batch / (ms * 1e-3), "decrypt_err_last": err,
+           "runs": steps, "warmup": warmup, "ms_min": min(runs), "ms_max": max(runs),
            "roofline": {"bound": "hbm", "algorithmic_bytes_per_batch": kbytes,
                         "achieved": kbytes / (kms * 1e-3) / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                         **hbm_fracs(kbytes / (kms * 1e-3) / 1e9)},
@@ -442,6 +446,7 @@ def bench_keyswitch(torch, np, steps, warmup):
 
 
 def bench_ntt(torch, steps):
+    import numpy as np
     from workloads import NTT_BENCH as cfg
     ctx = make_context(cfg, 0, 1)
     g = torch.Generator(device="cuda").manual_seed(202)
@@ -449,20 +454,26 @@ def bench_ntt(torch, steps):
                       dtype=torch.int64).view(torch.uint64)
     ctx.ntt(x)
     ctx.intt(x)
+    for _ in range(2):
+        ctx.ntt(x)
+        ctx.intt(x)
     ctx.profile(True)
     ctx.profile_reset()
-    with Timer(torch) as tf:
-        for _ in range(steps):
+    fwd, inv = [], []
+    for _ in range(steps):
+        with Timer(torch) as tf:
             ctx.ntt(x)
-    with Timer(torch) as ti:
-        for _ in range(steps):
+        fwd.append(tf.ms)
+        with Timer(torch) as ti:
             ctx.intt(x)
+        inv.append(ti.ms)
     prof = ctx.profile_all()
     ctx.profile(False)
+    fms, ims = float(np.median(fwd)), float(np.median(inv))
     algo = 16.0 * cfg.batch * cfg.n_q * ctx.n
-    res = {"workload": "64 polys x 36 limbs x 2^16, 50-bit primes", "fwd_ms": tf.ms / steps, "inv_ms": ti.ms / steps,
-           "algorithmic_bytes_per_direction": algo,
-           "fwd_GBps": algo / (tf.ms / steps * 1e-3) / 1e9, "inv_GBps": algo / (ti.ms / steps * 1e-3) / 1e9,
+    res = {"workload": "64 polys x 36 limbs x 2^16, 50-bit primes", "fwd_ms": fms, "inv_ms": ims,
+           "runs": steps, "warmup": 3, "algorithmic_bytes_per_direction": algo,
+           "fwd_GBps": algo / (fms * 1e-3) / 1e9, "inv_GBps": algo / (ims * 1e-3) / 1e9,
            "kernels": {k: {"avg_ms": v[0] / v[1], "GBps": v[2] / (v[0] * 1e-3) / 1e9,
                            **hbm_fracs(v[2] / (v[0] * 1e-3) / 1e9)} for k, v in prof.items()}}
     # per transform (one read and one write of every residue) against 8 TB/s; each two-pass transform moves twice that
@@ -693,10 +704,10 @@ def main():
     secondary = {}
     if not args.no_secondary:
         log("keyswitch batch")
-        secondary["keyswitch"] = bench_keyswitch(torch, np, max(args.steps, 3), 1)
+        secondary["keyswitch"] = bench_keyswitch(torch, np, max(args.steps, 10), 3)
         torch.cuda.empty_cache()
         log("ntt microbench")
-        secondary["ntt"] = bench_ntt(torch, max(args.steps, 5))
+        secondary["ntt"] = bench_ntt(torch, max(args.steps, 10))
         torch.cuda.empty_cache()
         log("other projection shapes")
         secondary["shapes"] = bench_shapes(torch, np, 1)
