@@ -281,8 +281,8 @@ def bench_attention(torch, np, steps, warmup):
     res = {
         "workload": "one Llama-3-8B attention block, token-major (slot t*256 + f): 128 tokens, 32 query / 8 key-value "
                     "heads of 128, N=2^16, 24+8 x 50-bit primes, dnum 3, scale 2^50, inputs at level 12; Q/K/V/O "
-                    "projections (n1=32; Q, K, V as one 4096x8192 projection, K and V heads written twice), scores on token "
-                    "diagonals, weighted sums consuming them (no Softmax)",
+                    "projections (n1=%d; Q, K, V as one 4096x8192 projection, K and V heads written twice), scores on token "
+                    "diagonals, weighted sums consuming them (no Softmax)" % n1,
         "s_per_block": t.ms / steps / 1e3,
         "phases_ms": {k: round(v, 3) for k, v in phase.items()},
         "decrypt_max_abs_err": max(errs), "output_max_abs": float(np.max(np.abs(want))),

@@ -111,6 +111,7 @@ ATTN_TOY = Config("attn_toy", 8, 12, 50, 6, 2, 3, scale_log2=50, level=5, tokens
 # One Llama-3-8B attention block's ciphertext work: 128 tokens x 256 features (two heads of 128) per
 # ciphertext, 32 query heads (16 ciphertexts) and 8 key/value heads (each repeated in both head positions of
 # its own ciphertext: 8 key and 8 value ciphertexts), projections 4096 -> 4096 (Q, O) and 4096 -> 2 x 1024
-# (K, V, each head written twice), token-major layout, inputs at level 12, scale 2^50.
+# (K, V, each head written twice), token-major layout, inputs at level 12, scale 2^50; the projections use n1 = 16
+# (with 32 and 16 outputs, half the hoisted baby steps of n1 = 32 save more than the extra giant steps cost).
 ATTENTION = Config("attention", 9, 16, 50, 24, 8, 3, scale_log2=50, level=12, tokens=128, d_in=4096,
-                   d_out=4096, n1=32, head_dim=128, heads=32, kv_heads=8)
+                   d_out=4096, n1=16, head_dim=128, heads=32, kv_heads=8)
