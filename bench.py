@@ -324,6 +324,28 @@ def measure_copy(torch, ctx, mib=1024, reps=3):
     return COPY["GBps"]
 
 
+def measure_modmul(torch, ctx, lanes=1 << 21, iters=512):
+    """Measured fp64 modular-multiply rate (the library's probe: eight independent product chains per lane,
+    exact FMA products, q < 2^50), the ALU reference for the projection's modmul-class work."""
+    out = torch.empty(lanes, dtype=torch.uint64, device="cuda")
+    ctx.calib_modmul(out, iters, 1)
+    with Timer(torch) as t:
+        ctx.calib_modmul(out, iters, 1)
+    del out
+    return lanes * iters * 8 / (t.ms * 1e-3)
+
+
+def projection_modmuls(cfg, ks_rotations):
+    """Modmul-class operations of one projection: one modular product per encode-NTT butterfly (every weight
+    plaintext, every limb), two per multiply-accumulated residue, and about 2.5e7 per key-switched rotation at
+    level 12 (inner product, conversions and the ModDown transforms)."""
+    D = cfg.feats
+    plaintexts = (cfg.d_out // D) * (cfg.d_in // D) * D
+    limbs = cfg.level + 1
+    n, log_n = 1 << cfg.log_n, cfg.log_n
+    return plaintexts * limbs * (n // 2) * log_n + plaintexts * limbs * n * 2 + ks_rotations * 2.5e7
+
+
 def hbm_fracs(gbs):
     out = {"frac": gbs / HBM_PEAK_GBS}
     if COPY["GBps"]:
@@ -673,6 +695,8 @@ def main():
     st = setup_projection(torch, np, cfg)
     ctx = st["ctx"]
     log("copy calibration: %.0f GB/s" % measure_copy(torch, ctx))
+    modmul_peak = measure_modmul(torch, ctx)
+    log("modmul calibration: %.2f T/s" % (modmul_peak / 1e12))
     if args.calib_copy_mib:
         src = torch.ones(args.calib_copy_mib << 17, dtype=torch.uint64, device="cuda")
         dst = torch.empty_like(src)
@@ -746,6 +770,12 @@ def main():
         "cpu_baseline": cpu,
         "decrypt_max_abs_err": err,
         "copy_GBps": COPY["GBps"],
+        "modmul": {"ops_per_projection": projection_modmuls(cfg, 888),
+                   "achieved_per_s": projection_modmuls(cfg, 888) / (ms * 1e-3),
+                   "measured_peak_per_s": modmul_peak,
+                   "frac": projection_modmuls(cfg, 888) / (ms * 1e-3) / modmul_peak,
+                   "note": "encode-NTT butterflies + multiply-accumulate products + key switching, against the "
+                           "library's fp64 modmul probe (8 independent chains per lane)"},
         "kernels_ms_per_step": kernels_ms,
         "secondary": secondary,
     }
