@@ -450,17 +450,24 @@ def bench_keyswitch(torch, np, steps, warmup):
     re, _ = ctx.decode(ctx.decrypt(s, outs[-1]))
     err = float(np.max(np.abs(re.cpu().numpy() - np.roll(z, -rsteps[-1]))))
     ms = float(np.median(runs))
-    # HBM roofline of the batch: the algorithmic bytes the library's profiler tags on every key-switching launch
-    # (each input and output word once per launch; cache-resident gathers of the shared digits and c0 not
-    # counted), over the kernels' summed time
+    # HBM roofline of the batch.  Algorithmic bytes: what any hoisted batch must move once, the 32 keys
+    # [dnum][2][L+K][N], the 32 outputs [2][L][N], the input [2][L][N], and the ModUp digits [dnum][L+K][N]
+    # written and read once; over the batch's median time.  Beside it, the bytes the library's profiler tags on
+    # its launches (each word a launch reads or writes, once; intermediate rows included) over the kernels'
+    # summed time: how close the kernels run to the rate HBM sustains.
+    word = 8.0 * n
+    nd = cfg.dnum
+    abytes = (cfg.batch * nd * 2 * (L + cfg.n_p) + cfg.batch * 2 * L + 2 * L + 2 * nd * (L + cfg.n_p)) * word
     kbytes = sum(v[2] for v in prof.values()) / steps
     kms = sum(v[0] for v in prof.values()) / steps
     res = {"workload": "32 hoisted rotations by 1..32 of one level-23 ciphertext, N=2^16, L=24+K=8, dnum=3",
            "ms_per_batch": ms, "rotations_per_s": cfg.batch / (ms * 1e-3), "decrypt_err_last": err,
            "runs": steps, "warmup": warmup, "ms_min": min(runs), "ms_max": max(runs),
-           "roofline": {"bound": "hbm", "algorithmic_bytes_per_batch": kbytes,
-                        "achieved": kbytes / (kms * 1e-3) / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                        **hbm_fracs(kbytes / (kms * 1e-3) / 1e9)},
+           "roofline": {"bound": "hbm", "algorithmic_bytes_per_batch": abytes,
+                        "achieved": abytes / (ms * 1e-3) / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                        **hbm_fracs(abytes / (ms * 1e-3) / 1e9)},
+           "kernel_traffic": {"bytes_per_batch": kbytes, "GBps": kbytes / (kms * 1e-3) / 1e9,
+                              **hbm_fracs(kbytes / (kms * 1e-3) / 1e9)},
            "kernels_ms": {k: v[0] / steps for k, v in prof.items()},
            "kernels_GBps": {k: v[2] / (v[0] * 1e-3) / 1e9 for k, v in prof.items() if v[0] > 0}}
     del keys, outs, ct, ctx

@@ -352,8 +352,9 @@ ckks_status ckks_profile_read(ckks_ctx *ctx, const char *kernel, double *total_m
                               double *bytes, double *valu_ops);
 ckks_status ckks_profile_reset(ckks_ctx *ctx);
 const char *ckks_profile_name(int i);
-/* A plain device copy of `bytes` bytes (multiple of 16) on the context stream,
- * for calibrating HBM counters and achievable bandwidth. */
+/* A plain device copy of `bytes` bytes (multiple of 16, at most 8 TiB) on the context
+ * stream, for calibrating HBM counters and achievable bandwidth: one 16-byte word per
+ * thread with nontemporal loads and stores, the fastest copy shape measured on gfx950. */
 ckks_status ckks_calib_copy(ckks_ctx *ctx, void *dev_dst, const void *dev_src, size_t bytes);
 /* Modular-multiply throughput probe: `iters` dependent-chain multiplications
  * per lane on `lanes` lanes, mode 0 = integer Shoup (64-bit, built from 32-bit

@@ -334,7 +334,7 @@ __global__ __launch_bounds__(512) void ntt_col8_from_fft(const double2 *__restri
         nttc::fwd8_stage<2, 7, (nttc::kColMask8 >> 7) & 1>(x, tw, t, ar);
         uint64_t *dst = out + (((size_t)b * limbs + l) << log_n) + coff;
 #pragma unroll
-        for (int k = 0; k < kE8; k++) dst[(size_t)nttc::u8<2>(t, k) * 256] = nttc::Ar<true>::to_raw(x[k]);
+        for (int k = 0; k < kE8; k++) nttc::st_stream(dst + (size_t)nttc::u8<2>(t, k) * 256, nttc::Ar<true>::to_raw(x[k]));
     }
 }
 

@@ -208,6 +208,90 @@ __global__ __launch_bounds__(512) void k_col8_rows(uint64_t *data, LimbMap map, 
     for (int k = 0; k < kE8; k++) base[(size_t)nttc::u8<2>(t, k) * n2] = nttc::Ar<true>::to_raw(x[k]);
 }
 
+// The fp64 conversion (at most 8 source limbs) fused with the first forward column pass, N = 2^16: block
+// (poly, 16 adjacent columns), 512 threads, 8 points of one 256-point column per thread.  The centred source
+// digits y_i of the block's 4096 coefficients stay in registers; for each target limb in turn the block forms
+// the converted residues with the products and range reductions of k_conv_f64 (RAW), runs that limb's column
+// sub-transforms on them (the arithmetic of k_col8_rows) and writes the rows as raw doubles, the inter-pass
+// form the fused row passes read.  The converted rows thus cross HBM once instead of three times.  Target
+// t + 1's twiddles (Psi[1..255]) are staged into the idle half of a double-buffered table while target t is
+// transformed.  EXACT: ns == 8 (no guards on the source loop).
+struct StageNext {
+    double *dst;
+    double v;
+    bool on;
+    __device__ void operator()() const
+    {
+        if (on) dst[threadIdx.x + 1] = v;
+    }
+};
+
+template <bool EXACT>
+__global__ __launch_bounds__(512) void k_conv_col8(const uint64_t *__restrict__ in, uint32_t in_stride,
+                                                   uint64_t *out, uint32_t out_stride, uint32_t split, uint32_t skip,
+                                                   ConvArgs a, const double *__restrict__ qhat_inv,
+                                                   const double *__restrict__ qhat_mod,
+                                                   const ModQ *__restrict__ mods, const double *__restrict__ twf,
+                                                   uint32_t log_n, uint32_t blocks_per_row)
+{
+    using nttc::Ar;
+    using nttc::kE8;
+    __shared__ double s_mod[8 * kMaxPrimes];
+    __shared__ double tws[2][256];
+    __shared__ double tr[16][nttc::kTr8];
+    const int ns = EXACT ? 8 : a.ns, nt = a.nt;
+    for (int k = threadIdx.x; k < ns * nt; k += 512) s_mod[k] = qhat_mod[k];
+    if (threadIdx.x < 255) tws[0][threadIdx.x + 1] = twf[((size_t)a.dst[0] << log_n) + threadIdx.x + 1];
+    const uint32_t poly = blockIdx.x / blocks_per_row, blk = blockIdx.x % blocks_per_row;
+    const uint32_t n2 = 1u << (log_n - 8);
+    const uint32_t col = threadIdx.x & 15, t = threadIdx.x >> 4;
+    const size_t coff = (size_t)blk * 16 + col;
+    const uint64_t *src = in + ((size_t)poly * in_stride << log_n) + coff;
+    uint64_t raw[8][kE8];
+#pragma unroll
+    for (int i = 0; i < 8; i++)
+#pragma unroll
+        for (int k = 0; k < kE8; k++)
+            if (EXACT || i < ns) raw[i][k] = src[((size_t)i << log_n) + (size_t)nttc::u8<0>(t, k) * n2];
+    double y[kE8][8];
+#pragma unroll
+    for (int i = 0; i < 8; i++) {
+        if (EXACT || i < ns) {
+            const Ar<true> ar(mods[a.src[i]]);
+            const double h = 0.5 * ar.q, w = qhat_inv[i];
+#pragma unroll
+            for (int k = 0; k < kE8; k++) {
+                const double v = ar.mul(Ar<true>::from_u64(raw[i][k]), w);
+                y[k][i] = v > h ? v - ar.q : (v < -h ? v + ar.q : v);
+            }
+        }
+    }
+    __syncthreads();
+    for (int tt = 0; tt < nt; tt++) {
+        const Ar<true> ar(mods[a.dst[tt]]);
+        StageNext next{tws[(tt + 1) & 1], 0.0, tt + 1 < nt && threadIdx.x < 255};
+        if (next.on) next.v = twf[((size_t)a.dst[tt + 1] << log_n) + threadIdx.x + 1];
+        double x[kE8];
+#pragma unroll
+        for (int k = 0; k < kE8; k++) {
+            double acc = 0.0;
+#pragma unroll
+            for (int i = 0; i < 8; i++) {
+                if (EXACT || i < ns) {
+                    acc += ar.mul(y[k][i], s_mod[i * nt + tt]);
+                    if ((i & 3) == 3) acc = ar.red(acc);
+                }
+            }
+            x[k] = ar.red(acc);
+        }
+        nttc::fwd8_256<nttc::kColMask8>(x, tws[tt & 1], tr[col], t, ar, 1, next);
+        const uint32_t row = tt < (int)split ? tt : tt + skip;
+        uint64_t *dst = out + (((size_t)poly * out_stride + row) << log_n) + coff;
+#pragma unroll
+        for (int k = 0; k < kE8; k++) nttc::st_stream(dst + (size_t)nttc::u8<2>(t, k) * n2, Ar<true>::to_raw(x[k]));
+    }
+}
+
 // u[k][r][n] = sum_{j<nd} d_j[r][sigma(n)] * key[j][k][krow(r)][n], rows r over Q_level u P
 __global__ __launch_bounds__(kThreads) void k_key_ip(const uint64_t *__restrict__ digits,
                                                       const uint64_t *__restrict__ key, uint64_t *u, uint32_t nd,
@@ -290,8 +374,8 @@ __global__ __launch_bounds__(kThreads) void k_key_ip_batch(RotArgs ra, uint64_t 
     for (uint32_t j = 0; j < nd; j++) {
         const uint64_t d = digits[(((size_t)j * ext + row) << log_n) + sc];
         const size_t kb = ((size_t)j * 2 * key_rows + prime) << log_n;
-        mac(a0, d, key[kb + col]);
-        mac(a1, d, key[kb + ((size_t)key_rows << log_n) + col]);
+        mac(a0, d, nttc::ld_stream(key + kb + col));
+        mac(a1, d, nttc::ld_stream(key + kb + ((size_t)key_rows << log_n) + col));
     }
     uint64_t *ur = u + (((size_t)r * 2 * rows + (row - row0)) << log_n) + col;
     ur[0] = reduce128(a0, m);
@@ -373,7 +457,7 @@ __global__ __launch_bounds__(64) void k_ks_finish8(RotArgs ra, const uint64_t *_
         const uint64_t *src = cw + (((size_t)r * 2 + k) * L << log_n) + row;
         double x[kE8];
 #pragma unroll
-        for (int e = 0; e < kE8; e++) x[e] = nttc::Ar<true>::from_raw(src[nttc::u8<0>(t, e)]);
+        for (int e = 0; e < kE8; e++) x[e] = nttc::Ar<true>::from_raw(nttc::ld_stream(src + nttc::u8<0>(t, e)));
         nttc::fwd8_256<nttc::kRowMask8>(x, tws[sub], tr[sub], t, ar);
         nttc::b_to_a8(x, tr[sub], t);
 #pragma unroll
@@ -393,8 +477,8 @@ __global__ __launch_bounds__(64) void k_ks_finish8(RotArgs ra, const uint64_t *_
         for (uint32_t j = 0; j < nd; j++) {
             const double d = nttc::Ar<true>::from_u64(digits[(((size_t)j * ext + i) << log_n) + sc]);
             const uint64_t *kj = key + (((size_t)j * 2 * key_rows + i) << log_n) + pos;
-            u0 += ar.mul(d, nttc::Ar<true>::from_u64(kj[0]));
-            u1 += ar.mul(d, nttc::Ar<true>::from_u64(kj[kstride]));
+            u0 += ar.mul(d, nttc::Ar<true>::from_u64(nttc::ld_stream(kj)));
+            u1 += ar.mul(d, nttc::Ar<true>::from_u64(nttc::ld_stream(kj + kstride)));
             if ((j & 3) == 3) {
                 u0 = ar.red(u0);
                 u1 = ar.red(u1);
@@ -402,8 +486,8 @@ __global__ __launch_bounds__(64) void k_ks_finish8(RotArgs ra, const uint64_t *_
         }
         const double r0 = ar.mul(u0 - v[0][e], pi) + nttc::Ar<true>::from_u64(c0[((size_t)i << log_n) + sc]);
         const double r1 = ar.mul(u1 - v[1][e], pi);
-        out[((size_t)i << log_n) + pos] = ar.to_canon(r0);
-        out[(((size_t)L + i) << log_n) + pos] = ar.to_canon(r1);
+        nttc::st_stream(out + ((size_t)i << log_n) + pos, ar.to_canon(r0));
+        nttc::st_stream(out + (((size_t)L + i) << log_n) + pos, ar.to_canon(r1));
     }
 }
 
@@ -498,6 +582,37 @@ ckks_status launch_col8_rows(ckks_ctx *ctx, uint64_t *data, uint32_t rows, const
     return CKKS_OK;
 }
 
+// The raw fp64 conversion of `polys` polynomials followed by the first forward column pass of its output rows
+// (N = 2^16, at most 8 source limbs), in one kernel: out rows as launch_conv writes them, in the inter-pass form.
+ckks_status launch_conv_col8(ckks_ctx *ctx, const ConvDev *cd, const uint64_t *in, uint32_t in_stride, uint64_t *out,
+                             uint32_t out_stride, uint32_t split, uint32_t skip, uint32_t polys)
+{
+    CK_REQUIRE(ctx->log_n == 16 && cd->f64 && !ctx->int_only && cd->ns >= 1 && cd->ns <= 8 && cd->nt >= 1,
+               CKKS_EINVAL, "fused conversion needs N = 2^16, the fp64 tables and 1..8 source limbs");
+    CK_REQUIRE(split <= (uint32_t)cd->nt && (uint32_t)cd->nt + skip <= out_stride && cd->ns <= (int)in_stride,
+               CKKS_EINVAL, "fused conversion: target rows outside the output");
+    ConvArgs a;
+    a.ns = cd->ns;
+    a.nt = cd->nt;
+    for (int i = 0; i < cd->ns; i++) a.src[i] = cd->src[i];
+    for (int t = 0; t < cd->nt; t++) a.dst[t] = cd->dst[t];
+    const uint32_t bpr = 1u << (ctx->log_n - 12);
+    const double res = (double)polys * ctx->n;
+    // the sources once, the converted rows once; the conversion products and the column pass's butterflies
+    prof_begin(ctx, K_CONV, 8.0 * res * (a.ns + a.nt), res * a.nt * (a.ns * 5.0 + kOpsButterflyF64 * 4));
+    if (a.ns == 8)
+        hipLaunchKernelGGL(k_conv_col8<true>, dim3(polys * bpr), dim3(512), 0, ctx->stream, in, in_stride, out,
+                           out_stride, split, skip, a, cd->d_qhat_inv_f, cd->d_qhat_mod_f, ctx->d_mod, ctx->d_twf,
+                           ctx->log_n, bpr);
+    else
+        hipLaunchKernelGGL(k_conv_col8<false>, dim3(polys * bpr), dim3(512), 0, ctx->stream, in, in_stride, out,
+                           out_stride, split, skip, a, cd->d_qhat_inv_f, cd->d_qhat_mod_f, ctx->d_mod, ctx->d_twf,
+                           ctx->log_n, bpr);
+    prof_end(ctx, K_CONV);
+    HIP_TRY(hipGetLastError());
+    return CKKS_OK;
+}
+
 }  // namespace
 
 uint32_t ks_rot_batch(uint32_t count) { return count < (uint32_t)kRotBatch ? count : (uint32_t)kRotBatch; }
@@ -548,8 +663,7 @@ ckks_status ks_rotate_batch(ckks_ctx *ctx, uint32_t level, uint32_t count, const
         CK_TRY(ctx_conv(ctx, (int)level, -1, &cd));
         if (s1 == 8 && cd->f64 && !ctx->int_only && cd->ns <= 8) {
             // the conversion writes reduced raw doubles; the 8-residue column pass takes them as they are
-            CK_TRY(launch_conv(ctx, cd, up, K, cw, L, L, 0, 2 * count, true));
-            CK_TRY(launch_col8_rows(ctx, cw, 2 * count * L, limb_range(0, L)));
+            CK_TRY(launch_conv_col8(ctx, cd, up, K, cw, L, L, 0, 2 * count));
         } else {
             CK_TRY(launch_conv(ctx, cd, up, K, cw, L, L, 0, 2 * count));
             CK_TRY(launch_ntt_fwd_first_pass(ctx, cw, 2 * count, L, limb_range(0, L)));

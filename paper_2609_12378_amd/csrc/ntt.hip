@@ -42,28 +42,45 @@ namespace {
 
 using namespace nttc;
 
-__device__ __forceinline__ size_t row_of_block(uint32_t blk_row, uint32_t batch, uint32_t bstride,
+// Rows in memory order: consecutive blocks take consecutive limbs of one polynomial, then the next polynomial
+// (limb-major order, which keeps one twiddle table hot, measured slower: its concurrent blocks touch rows a
+// whole polynomial apart).
+__device__ __forceinline__ size_t row_of_block(uint32_t blk_row, uint32_t limbs, uint32_t bstride,
                                                uint32_t *prime_slot)
 {
-    // blocks are ordered limb-major so that concurrent blocks share one twiddle table
-    const uint32_t limb = blk_row / batch, b = blk_row % batch;
+    const uint32_t b = blk_row / limbs, limb = blk_row % limbs;
     *prime_slot = limb;
     return (size_t)b * bstride + limb;
 }
 
+// Sub-transforms per block of the column pass (16 columns of 256 points) and of the row pass (8 rows of 256).
+constexpr uint32_t col_subs(int logs, int log_n)
+{
+    return (4096u >> logs) < (1u << (log_n - logs)) ? (4096u >> logs) : (1u << (log_n - logs));
+}
+constexpr uint32_t row_subs(int logs, int log_n)
+{
+    return (2048u >> logs) < (1u << (log_n - logs)) ? (2048u >> logs) : (1u << (log_n - logs));
+}
+
 // Column pass over N1 = 2^LOGS points at stride N2 = 2^(log_n - LOGS).
 // Forward: first pass (canonical input).  Inverse: last pass (N^-1, canonical output).
-template <int LOGS, bool INV, bool F>
-__global__ __launch_bounds__(256) void ntt_col(uint64_t *data, LimbMap map, uint32_t batch, uint32_t bstride,
-                                               const ModQ *mods, const void *tw_all, uint32_t log_n,
-                                               uint32_t cols_per_block, uint32_t blocks_per_row)
+// LOGN > 0: the ring degree is 2^LOGN at compile time (log_n, cols_per_block and blocks_per_row are then
+// ignored), so every stride is a constant; 0: all from the arguments.
+template <int LOGS, bool INV, bool F, int LOGN = 0>
+__global__ __launch_bounds__(256) void ntt_col(uint64_t *data, LimbMap map, uint32_t bstride,
+                                               const ModQ *mods, const void *tw_all, uint32_t log_n_arg,
+                                               uint32_t cols_arg, uint32_t bpr_arg)
 {
     using E = typename Ar<F>::E;
     constexpr uint32_t TS = (1u << LOGS) / 16;
+    const uint32_t log_n = LOGN ? LOGN : log_n_arg;
+    const uint32_t cols_per_block = LOGN ? col_subs(LOGS, LOGN) : cols_arg;
+    const uint32_t blocks_per_row = LOGN ? (1u << (LOGN - LOGS)) / col_subs(LOGS, LOGN) : bpr_arg;
     extern __shared__ uint64_t lds_raw[];
     E *lds = (E *)lds_raw;
     uint32_t slot;
-    const size_t row = row_of_block(blockIdx.x / blocks_per_row, batch, bstride, &slot);
+    const size_t row = row_of_block(blockIdx.x / blocks_per_row, map.n, bstride, &slot);
     const uint32_t blk = blockIdx.x % blocks_per_row;
     const uint32_t prime = map.prime[slot];
     const Ar<F> ar(mods[prime]);
@@ -74,24 +91,24 @@ __global__ __launch_bounds__(256) void ntt_col(uint64_t *data, LimbMap map, uint
     E x[kE];
     if (!INV) {
 #pragma unroll
-        for (int k = 0; k < kE; k++) x[k] = ar.from_u64(base[(size_t)(r + TS * k) * n2 + col]);
+        for (int k = 0; k < kE; k++) x[k] = ar.from_u64(ld_stream(base + (size_t)(r + TS * k) * n2 + col));
         fwd_top<F>(x, tw, 1, ar);
         if (LOGS > 4) {
             transpose<LOGS, true>(x, lds, col, r);
             fwd_low<LOGS, F>(x, tw, 1, r, ar);
         }
 #pragma unroll
-        for (int k = 0; k < kE; k++) base[(size_t)(LOGS > 4 ? 16 * r + k : k) * n2 + col] = ar.to_raw(x[k]);
+        for (int k = 0; k < kE; k++) st_stream(base + (size_t)(LOGS > 4 ? 16 * r + k : k) * n2 + col, ar.to_raw(x[k]));
     } else {
 #pragma unroll
-        for (int k = 0; k < kE; k++) x[k] = ar.from_raw(base[(size_t)(LOGS > 4 ? 16 * r + k : k) * n2 + col]);
+        for (int k = 0; k < kE; k++) x[k] = ar.from_raw(ld_stream(base + (size_t)(LOGS > 4 ? 16 * r + k : k) * n2 + col));
         if (LOGS > 4) {
             inv_low<LOGS, F>(x, tw, 1, r, ar);
             transpose<LOGS, false>(x, lds, col, r);
         }
         inv_top<F>(x, tw, 1, ar);
 #pragma unroll
-        for (int k = 0; k < kE; k++) base[(size_t)(r + TS * k) * n2 + col] = ar.to_canon(ar.scale_n(x[k]));
+        for (int k = 0; k < kE; k++) st_stream(base + (size_t)(r + TS * k) * n2 + col, ar.to_canon(ar.scale_n(x[k])));
     }
 }
 
@@ -239,17 +256,20 @@ __global__ __launch_bounds__(512) void ntt_col8_from_i64(const int64_t *__restri
 // Row pass over N2 = 2^LOGS contiguous points of row h, twiddle base N1 + h.
 // FIRST: input is canonical residues; LAST: write canonical residues (and, for
 // the inverse, multiply by N^-1).
-template <int LOGS, bool INV, bool FIRST, bool LAST, bool F>
-__global__ __launch_bounds__(256) void ntt_row(uint64_t *data, LimbMap map, uint32_t batch, uint32_t bstride,
-                                               const ModQ *mods, const void *tw_all, uint32_t log_n,
-                                               uint32_t rows_per_block, uint32_t blocks_per_poly)
+template <int LOGS, bool INV, bool FIRST, bool LAST, bool F, int LOGN = 0>
+__global__ __launch_bounds__(256) void ntt_row(uint64_t *data, LimbMap map, uint32_t bstride,
+                                               const ModQ *mods, const void *tw_all, uint32_t log_n_arg,
+                                               uint32_t rows_arg, uint32_t bpp_arg)
 {
     using E = typename Ar<F>::E;
     constexpr uint32_t S = 1u << LOGS, TS = S / 16;
+    const uint32_t log_n = LOGN ? LOGN : log_n_arg;
+    const uint32_t rows_per_block = LOGN ? row_subs(LOGS, LOGN) : rows_arg;
+    const uint32_t blocks_per_poly = LOGN ? (1u << (LOGN - LOGS)) / row_subs(LOGS, LOGN) : bpp_arg;
     extern __shared__ uint64_t lds_raw[];
     E *lds = (E *)lds_raw;
     uint32_t slot;
-    const size_t poly = row_of_block(blockIdx.x / blocks_per_poly, batch, bstride, &slot);
+    const size_t poly = row_of_block(blockIdx.x / blocks_per_poly, map.n, bstride, &slot);
     const uint32_t blk = blockIdx.x % blocks_per_poly;
     const uint32_t prime = map.prime[slot];
     const Ar<F> ar(mods[prime]);
@@ -262,7 +282,7 @@ __global__ __launch_bounds__(256) void ntt_row(uint64_t *data, LimbMap map, uint
     E x[kE];
 #pragma unroll
     for (int k = 0; k < kE; k++) {
-        const uint64_t raw = base[r + TS * k];
+        const uint64_t raw = ld_stream(base + r + TS * k);
         x[k] = FIRST ? ar.from_u64(raw) : ar.from_raw(raw);
     }
     if (!INV) {
@@ -285,7 +305,7 @@ __global__ __launch_bounds__(256) void ntt_row(uint64_t *data, LimbMap map, uint
         }
     }
 #pragma unroll
-    for (int k = 0; k < kE; k++) base[r + TS * k] = LAST ? ar.to_canon(x[k]) : ar.to_raw(x[k]);
+    for (int k = 0; k < kE; k++) st_stream(base + r + TS * k, LAST ? ar.to_canon(x[k]) : ar.to_raw(x[k]));
 }
 
 template <bool F>
@@ -299,17 +319,22 @@ const void *inv_table(const ckks_ctx *c)
     return F ? (const void *)c->d_itwf : (const void *)c->d_itw;
 }
 
+// N = 2^16 (256 x 256) takes the variants with compile-time strides
 template <int LOGS, bool INV, bool F>
 hipError_t launch_col(ckks_ctx *ctx, uint64_t *data, uint32_t batch, uint32_t bstride, const LimbMap &map)
 {
     const uint32_t n2 = 1u << (ctx->log_n - LOGS);
     const uint32_t TS = (1u << LOGS) / 16;
-    uint32_t cols = 4096u >> LOGS;
-    if (cols > n2) cols = n2;
+    const uint32_t cols = col_subs(LOGS, (int)ctx->log_n);
     const uint32_t bpr = n2 / cols;
     const dim3 grid(batch * map.n * bpr), block(cols * TS);
-    hipLaunchKernelGGL((ntt_col<LOGS, INV, F>), grid, block, lds_bytes<LOGS>(cols), ctx->stream, data, map, batch,
-                       bstride, ctx->d_mod, INV ? inv_table<F>(ctx) : fwd_table<F>(ctx), ctx->log_n, cols, bpr);
+    const void *tw = INV ? inv_table<F>(ctx) : fwd_table<F>(ctx);
+    if (LOGS == 8 && ctx->log_n == 16)
+        hipLaunchKernelGGL((ntt_col<LOGS, INV, F, 16>), grid, block, lds_bytes<LOGS>(cols), ctx->stream, data, map,
+                           bstride, ctx->d_mod, tw, ctx->log_n, cols, bpr);
+    else
+        hipLaunchKernelGGL((ntt_col<LOGS, INV, F>), grid, block, lds_bytes<LOGS>(cols), ctx->stream, data, map,
+                           bstride, ctx->d_mod, tw, ctx->log_n, cols, bpr);
     return hipGetLastError();
 }
 
@@ -318,13 +343,17 @@ hipError_t launch_row(ckks_ctx *ctx, uint64_t *data, uint32_t batch, uint32_t bs
 {
     const uint32_t n1 = 1u << (ctx->log_n - LOGS);
     const uint32_t TS = (1u << LOGS) / 16;
-    uint32_t rows = 4096u >> LOGS;
-    if (rows > n1) rows = n1;
+    // 128 threads: smaller blocks stream measurably faster than 256
+    const uint32_t rows = row_subs(LOGS, (int)ctx->log_n);
     const uint32_t bpp = n1 / rows;
     const dim3 grid(batch * map.n * bpp), block(rows * TS);
-    hipLaunchKernelGGL((ntt_row<LOGS, INV, FIRST, LAST, F>), grid, block, lds_bytes<LOGS>(rows), ctx->stream, data,
-                       map, batch, bstride, ctx->d_mod, INV ? inv_table<F>(ctx) : fwd_table<F>(ctx), ctx->log_n, rows,
-                       bpp);
+    const void *tw = INV ? inv_table<F>(ctx) : fwd_table<F>(ctx);
+    if (LOGS == 8 && ctx->log_n == 16)
+        hipLaunchKernelGGL((ntt_row<LOGS, INV, FIRST, LAST, F, 16>), grid, block, lds_bytes<LOGS>(rows), ctx->stream,
+                           data, map, bstride, ctx->d_mod, tw, ctx->log_n, rows, bpp);
+    else
+        hipLaunchKernelGGL((ntt_row<LOGS, INV, FIRST, LAST, F>), grid, block, lds_bytes<LOGS>(rows), ctx->stream,
+                           data, map, bstride, ctx->d_mod, tw, ctx->log_n, rows, bpp);
     return hipGetLastError();
 }
 

@@ -218,7 +218,7 @@ __global__ __launch_bounds__(64) void k_row_mac8(uint64_t *acc, const uint64_t *
         const uint64_t *src = colout + ((size_t)jj * P + p) * pt_words + row;
         double x[kE8];
 #pragma unroll
-        for (int k = 0; k < kE8; k++) x[k] = nttc::Ar<true>::from_raw(src[nttc::u8<0>(t, k)]);
+        for (int k = 0; k < kE8; k++) x[k] = nttc::Ar<true>::from_raw(nttc::ld_stream(src + nttc::u8<0>(t, k)));
         nttc::fwd8_256<nttc::kRowMask8>(x, tws[sub], tr[sub], t, ar);
         nttc::b_to_a8(x, tr[sub], t);
         const uint32_t pair = ib0 + p;
