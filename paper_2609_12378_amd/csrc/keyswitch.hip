@@ -101,12 +101,11 @@ __global__ __launch_bounds__(kThreads) void k_conv(const uint64_t *in, uint32_t 
 // The same conversion in fp64 (every prime below 2^50): y_i = x_i * qhat_inv_i mod s_i (|mul| < 0.875 s_i for
 // canonical operands) is moved into (-s_i/2, s_i/2] by one add or subtract of s_i, then each target sums the
 // products y_i * [Qhat_i]_t (each below 0.875 t in magnitude, since |y_i| < s_i/2 < t) with a range reduction
-// every four terms (sums stay below 4 t < 2^53) and writes the canonical residue: the same integers as k_conv
-// (RAW: the reduced value, |x| <= t/2, as raw double bits, for a following fp64 transform pass).
+// every four terms (sums stay below 4 t < 2^53) and writes the canonical residue: the same integers as k_conv.
 // C coefficients per thread (kThreads apart, so every load and store stays coalesced): the per-target constants
 // come from LDS once for all C, and the C product chains are independent.  EXACT: ns == NS_MAX, so the source
 // loop has no guards and all source loads issue before the first is used.
-template <int NS_MAX, bool RAW, int C, bool EXACT = false>
+template <int NS_MAX, int C, bool EXACT = false>
 __global__ __launch_bounds__(kThreads) void k_conv_f64(const uint64_t *in, uint32_t in_stride, uint64_t *out,
                                                         uint32_t out_stride, uint32_t split, uint32_t skip,
                                                         ConvArgs a, const double *__restrict__ qhat_inv,
@@ -176,46 +175,20 @@ __global__ __launch_bounds__(kThreads) void k_conv_f64(const uint64_t *in, uint3
         }
         const uint32_t row = t < (int)split ? t : t + skip;
 #pragma unroll
-        for (int c = 0; c < C; c++)
-            dst[((size_t)row << log_n) + c * kThreads] =
-                RAW ? nttc::Ar<true>::to_raw(ar.red(acc[c])) : ar.to_canon(acc[c]);
+        for (int c = 0; c < C; c++) dst[((size_t)row << log_n) + c * kThreads] = ar.to_canon(acc[c]);
     }
-}
-
-// First (column) pass of the forward transform over rows of raw doubles (|x| <= q/2, the reduced conversion
-// output), in place, 8 residues per thread: block (row, 16 columns), 512 threads; row r uses prime map[r % n].
-// Leaves the rows as raw doubles in the inter-pass form the fused row passes read.
-__global__ __launch_bounds__(512) void k_col8_rows(uint64_t *data, LimbMap map, const ModQ *__restrict__ mods,
-                                                   const double *__restrict__ twf, uint32_t log_n,
-                                                   uint32_t blocks_per_row)
-{
-    using nttc::kE8;
-    __shared__ double tws[256];
-    __shared__ double tr[16][nttc::kTr8];
-    const uint32_t row = blockIdx.x / blocks_per_row, blk = blockIdx.x % blocks_per_row;
-    const uint32_t prime = map.prime[row % map.n];
-    const nttc::Ar<true> ar(mods[prime]);
-    const uint32_t n2 = 1u << (log_n - 8);
-    const uint32_t col = threadIdx.x & 15, t = threadIdx.x >> 4;
-    if (threadIdx.x < 255) tws[threadIdx.x + 1] = twf[((size_t)prime << log_n) + threadIdx.x + 1];
-    uint64_t *base = data + ((size_t)row << log_n) + (size_t)blk * 16 + col;
-    double x[kE8];
-#pragma unroll
-    for (int k = 0; k < kE8; k++) x[k] = nttc::Ar<true>::from_raw(base[(size_t)nttc::u8<0>(t, k) * n2]);
-    __syncthreads();
-    nttc::fwd8_256<nttc::kColMask8>(x, tws, tr[col], t, ar);
-#pragma unroll
-    for (int k = 0; k < kE8; k++) base[(size_t)nttc::u8<2>(t, k) * n2] = nttc::Ar<true>::to_raw(x[k]);
 }
 
 // The fp64 conversion (at most 8 source limbs) fused with the first forward column pass, N = 2^16: block
 // (poly, 16 adjacent columns), 512 threads, 8 points of one 256-point column per thread.  The centred source
 // digits y_i of the block's 4096 coefficients stay in registers; for each target limb in turn the block forms
-// the converted residues with the products and range reductions of k_conv_f64 (RAW), runs that limb's column
-// sub-transforms on them (the arithmetic of k_col8_rows) and writes the rows as raw doubles, the inter-pass
-// form the fused row passes read.  The converted rows thus cross HBM once instead of three times.  Target
-// t + 1's twiddles (Psi[1..255]) are staged into the idle half of a double-buffered table while target t is
-// transformed.  EXACT: ns == 8 (no guards on the source loop).
+// the converted residues with the products and range reductions of k_conv_f64 (reduced to |x| <= t/2 rather
+// than made canonical), runs that limb's column sub-transforms on them (nttc::fwd8_256 with the column pass's
+// lazy-reduction mask) and writes the rows as raw doubles, the inter-pass form the fused row passes read.  The
+// converted rows thus cross HBM once instead of three times (written, read and written by a separate column
+// pass, read by the ModDown).  Target t + 1's twiddles (Psi[1..255]) are staged into the idle half of a
+// double-buffered table while target t is transformed.  EXACT: ns == 8 (no guards on the source loop, all
+// source loads issued first).
 struct StageNext {
     double *dst;
     double v;
@@ -512,7 +485,7 @@ __global__ __launch_bounds__(kThreads) void k_moddown_finish_batch(RotArgs ra, c
 }
 
 ckks_status launch_conv(ckks_ctx *ctx, const ConvDev *cd, const uint64_t *in, uint32_t in_stride, uint64_t *out,
-                        uint32_t out_stride, uint32_t split, uint32_t skip, uint32_t polys, bool raw = false)
+                        uint32_t out_stride, uint32_t split, uint32_t skip, uint32_t polys)
 {
     ConvArgs a;
     a.ns = cd->ns;
@@ -524,29 +497,24 @@ ckks_status launch_conv(ckks_ctx *ctx, const ConvDev *cd, const uint64_t *in, ui
     const bool two = ctx->n % (2 * kThreads) == 0;
     const dim3 grid2(two ? (uint32_t)(ctx->n / (2 * kThreads)) : grid.x, polys);
     prof_begin(ctx, K_CONV, 8.0 * polys * (a.ns + a.nt) * ctx->n);
-#define CK_CONVF(NSM, RAWV)                                                                                        \
+#define CK_CONVF(NSM)                                                                                              \
     do {                                                                                                           \
         if (two && a.ns == NSM)                                                                                    \
-            hipLaunchKernelGGL((k_conv_f64<NSM, RAWV, 2, true>), grid2, block, 0, ctx->stream, in, in_stride, out,  \
+            hipLaunchKernelGGL((k_conv_f64<NSM, 2, true>), grid2, block, 0, ctx->stream, in, in_stride, out,        \
                                out_stride, split, skip, a, cd->d_qhat_inv_f, cd->d_qhat_mod_f, ctx->d_mod,          \
                                ctx->log_n);                                                                        \
         else if (two)                                                                                              \
-            hipLaunchKernelGGL((k_conv_f64<NSM, RAWV, 2>), grid2, block, 0, ctx->stream, in, in_stride, out,        \
-                               out_stride, split, skip, a, cd->d_qhat_inv_f, cd->d_qhat_mod_f, ctx->d_mod,          \
-                               ctx->log_n);                                                                        \
+            hipLaunchKernelGGL((k_conv_f64<NSM, 2>), grid2, block, 0, ctx->stream, in, in_stride, out, out_stride,  \
+                               split, skip, a, cd->d_qhat_inv_f, cd->d_qhat_mod_f, ctx->d_mod, ctx->log_n);        \
         else                                                                                                       \
-            hipLaunchKernelGGL((k_conv_f64<NSM, RAWV, 1>), grid, block, 0, ctx->stream, in, in_stride, out,         \
-                               out_stride, split, skip, a, cd->d_qhat_inv_f, cd->d_qhat_mod_f, ctx->d_mod,          \
-                               ctx->log_n);                                                                        \
+            hipLaunchKernelGGL((k_conv_f64<NSM, 1>), grid, block, 0, ctx->stream, in, in_stride, out, out_stride,   \
+                               split, skip, a, cd->d_qhat_inv_f, cd->d_qhat_mod_f, ctx->d_mod, ctx->log_n);        \
     } while (0)
-    if (raw) {
-        CK_REQUIRE(cd->f64 && !ctx->int_only && a.ns <= 8, CKKS_EINVAL, "raw conversion needs the fp64 tables");
-        CK_CONVF(8, true);
-    } else if (cd->f64 && !ctx->int_only && a.ns <= 16) {
+    if (cd->f64 && !ctx->int_only && a.ns <= 16) {
         if (a.ns <= 8)
-            CK_CONVF(8, false);
+            CK_CONVF(8);
         else
-            CK_CONVF(16, false);
+            CK_CONVF(16);
     } else if (a.ns <= 4)
         hipLaunchKernelGGL(k_conv<4>, grid, block, 0, ctx->stream, in, in_stride, out, out_stride, split, skip, a,
                            cd->d_qhat_inv, cd->d_qhat_mod, cd->d_neg_q, ctx->d_mod, ctx->log_n);
@@ -565,19 +533,6 @@ ckks_status launch_conv(ckks_ctx *ctx, const ConvDev *cd, const uint64_t *in, ui
     }
 #undef CK_CONVF
     prof_end(ctx, K_CONV);
-    HIP_TRY(hipGetLastError());
-    return CKKS_OK;
-}
-
-// First forward column pass of `rows` rows of raw doubles (row r with prime map.prime[r % map.n]), N = 2^16.
-ckks_status launch_col8_rows(ckks_ctx *ctx, uint64_t *data, uint32_t rows, const LimbMap &map)
-{
-    const uint32_t bpr = 1u << (ctx->log_n - 12);
-    const double res = (double)rows * ctx->n;
-    prof_begin(ctx, K_NTT_FWD_COL, 16.0 * res, res * kOpsButterflyF64 * 4);
-    hipLaunchKernelGGL(k_col8_rows, dim3(rows * bpr), dim3(512), 0, ctx->stream, data, map, ctx->d_mod, ctx->d_twf,
-                       ctx->log_n, bpr);
-    prof_end(ctx, K_NTT_FWD_COL);
     HIP_TRY(hipGetLastError());
     return CKKS_OK;
 }
