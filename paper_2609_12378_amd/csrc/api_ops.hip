@@ -208,8 +208,7 @@ ckks_status rescale_many(ckks_ctx *ctx, const uint64_t *c, uint32_t count, uint3
     const uint32_t polys = 2 * count;
     uint64_t *top = work, *r = top + (size_t)polys * N;
     // the top limb of every polynomial, then the same steps as one rescale over all of them
-    HIP_TRY(hipMemcpy2DAsync(top, N * 8, c + (size_t)l * N, (size_t)(l + 1) * N * 8, N * 8, polys,
-                             hipMemcpyDeviceToDevice, ctx->stream));
+    CK_TRY(launch_copy_rows(ctx, top, N, nullptr, 0, c + (size_t)l * N, (size_t)(l + 1) * N, N, polys));
     CK_TRY(launch_ntt(ctx, top, polys, limb_range(l, 1), true));
     CK_TRY(launch_rescale_spread(ctx, r, top, polys, l));
     CK_TRY(launch_ntt(ctx, r, polys * l, limb_range(0, l), false));

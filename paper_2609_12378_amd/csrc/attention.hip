@@ -704,8 +704,8 @@ extern "C" ckks_status ckks_attention_apply(ckks_ctx *ctx, const ckks_buf *p, ui
                     CK_TRY(rescale_many(ctx, Cb + (size_t)e0 * ctwv, cnt, lv, dst, work));
                 } else {
                     CK_TRY(rescale_many(ctx, Cb + (size_t)e0 * ctwv, cnt, lv, ctmp, work));
-                    HIP_TRY(hipMemcpy2DAsync(dst, (size_t)Lp * N * 8, ctmp, (size_t)(Lv - 1) * N * 8,
-                                             (size_t)Lp * N * 8, 2 * cnt, hipMemcpyDeviceToDevice, ctx->stream));
+                    CK_TRY(launch_copy_rows(ctx, dst, (size_t)Lp * N, nullptr, 0, ctmp, (size_t)(Lv - 1) * N,
+                                            (size_t)Lp * N, 2 * cnt));
                 }
             }
             cur_v = vv;

@@ -19,6 +19,11 @@ ckks_status launch_encrypt(ckks_ctx *ctx, uint64_t *c0, uint64_t *c1, const uint
 ckks_status launch_keygen_digit(ckks_ctx *ctx, uint64_t *b_out, uint64_t *a_out, const uint64_t *a,
                                 const uint64_t *s, const uint64_t *e, const uint64_t *t, uint32_t dig_lo,
                                 uint32_t dig_hi);
+// count entries of `words` contiguous words: entry b at src + b src_stride copied to dst_a + b a_stride and, when
+// dst_b is not null, to dst_b + b b_stride (strides in words; 16-byte accesses where every pointer and stride
+// allows them); count <= 65535
+ckks_status launch_copy_rows(ckks_ctx *ctx, uint64_t *dst_a, size_t a_stride, uint64_t *dst_b, size_t b_stride,
+                             const uint64_t *src, size_t src_stride, size_t words, uint32_t count);
 ckks_status launch_rescale_spread(ckks_ctx *ctx, uint64_t *out, const uint64_t *top, uint32_t polys, uint32_t l);
 ckks_status launch_rescale_finish(ckks_ctx *ctx, uint64_t *out, const uint64_t *c, const uint64_t *r,
                                   uint32_t polys, uint32_t l);

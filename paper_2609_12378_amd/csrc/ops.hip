@@ -169,6 +169,23 @@ __global__ __launch_bounds__(kThreads) void k_rescale_finish(uint64_t *out, cons
     out[i] = shoup(submod(ci, r[i], q), w.x, w.y, q);
 }
 
+// Entry b (b = blockIdx.y) of src, `words` contiguous words at src + b * src_stride, copied to
+// dst_a + b * a_stride and, when dst_b is set, to dst_b + b * b_stride: one read and one or two writes per word.
+// V: ulonglong2 (every pointer and stride 16-byte aligned, words even) or uint64_t.
+template <typename V>
+__global__ __launch_bounds__(kThreads) void k_copy_rows(uint64_t *dst_a, size_t a_stride, uint64_t *dst_b,
+                                                        size_t b_stride, const uint64_t *__restrict__ src,
+                                                        size_t src_stride, size_t words)
+{
+    constexpr size_t W = sizeof(V) / 8;
+    const size_t i = (size_t)blockIdx.x * kThreads + threadIdx.x;
+    const size_t b = blockIdx.y;
+    if (i * W >= words) return;
+    const V v = ((const V *)(src + b * src_stride))[i];
+    ((V *)(dst_a + b * a_stride))[i] = v;
+    if (dst_b) ((V *)(dst_b + b * b_stride))[i] = v;
+}
+
 }  // namespace
 
 ckks_status launch_binary(ckks_ctx *ctx, uint64_t *out, const uint64_t *a, const uint64_t *b, uint32_t rows,
@@ -268,6 +285,28 @@ ckks_status launch_rescale_finish(ckks_ctx *ctx, uint64_t *out, const uint64_t *
     const size_t total = ((size_t)polys * l) << ctx->log_n;
     hipLaunchKernelGGL(k_rescale_finish, grid_for(total), dim3(kThreads), 0, ctx->stream, out, c, r, total,
                        ctx->log_n, l, ctx->d_qlinv + (size_t)l * ctx->n_q, ctx->d_mod);
+    HIP_TRY(hipGetLastError());
+    return CKKS_OK;
+}
+
+ckks_status launch_copy_rows(ckks_ctx *ctx, uint64_t *dst_a, size_t a_stride, uint64_t *dst_b, size_t b_stride,
+                             const uint64_t *src, size_t src_stride, size_t words, uint32_t count)
+{
+    if (!count || !words) return CKKS_OK;
+    CK_REQUIRE(count <= 65535, CKKS_EINVAL, "row copy of %u entries in one launch (at most 65535)", count);
+    auto al16 = [](const void *p) { return ((uintptr_t)p & 15) == 0; };
+    const bool wide = words % 2 == 0 && a_stride % 2 == 0 && b_stride % 2 == 0 && src_stride % 2 == 0 &&
+                      al16(dst_a) && al16(src) && (!dst_b || al16(dst_b));
+    const size_t per = wide ? words / 2 : words;
+    const dim3 grid((unsigned)((per + kThreads - 1) / kThreads), count);
+    prof_begin(ctx, K_ELEM, 8.0 * words * count * (dst_b ? 3 : 2));
+    if (wide)
+        hipLaunchKernelGGL(k_copy_rows<ulonglong2>, grid, dim3(kThreads), 0, ctx->stream, dst_a, a_stride, dst_b,
+                           b_stride, src, src_stride, words);
+    else
+        hipLaunchKernelGGL(k_copy_rows<uint64_t>, grid, dim3(kThreads), 0, ctx->stream, dst_a, a_stride, dst_b,
+                           b_stride, src, src_stride, words);
+    prof_end(ctx, K_ELEM);
     HIP_TRY(hipGetLastError());
     return CKKS_OK;
 }

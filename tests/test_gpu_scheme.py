@@ -5,6 +5,8 @@ Two parameter sets: the toy ring (N = 2^12, 4 + 2 limbs of 36-bit primes, dnum 2
 and the key-switching / projection chain at full degree (N = 2^16, 24 + 8 limbs of
 50-bit primes, dnum 3) at level 12 (partial second digit) and level 23.
 """
+import dataclasses
+
 import numpy as np
 import pytest
 
@@ -211,6 +213,19 @@ def test_rotate_toy(toy, steps):
     eq(toy.ctx.rotate(ctg, steps, kg).data, toy.ck.rotate(cto, steps, ko))
 
 
+def test_rotate_buffer_off_16_byte_boundary(toy):
+    """A ciphertext whose data starts 8 bytes past a 16-byte boundary: ModUp's row copies take their 8-byte form."""
+    import torch
+    from paper_2609_12378_amd import Buf
+    cto, ctg, _ = toy.encrypt_both(17, 4, 2.0 ** 30)
+    flat = torch.zeros(ctg.data.numel() + 1, dtype=torch.uint64, device="cuda")
+    view = flat[1:].view(ctg.data.shape)
+    view.copy_(ctg.data)
+    assert view.data_ptr() % 16 == 8
+    ko, kg = toy.galois_keys(27, 7)
+    eq(toy.ctx.rotate(Buf(view, ctg.scale), 7, kg).data, toy.ck.rotate(cto, 7, ko))
+
+
 def test_rotate_hoisted_toy_lower_level(toy):
     cto, ctg, _ = toy.encrypt_both(12, 3, 2.0 ** 30)   # level 2: partial second digit
     steps = [1, 2, 16, 100]
@@ -226,6 +241,21 @@ def test_rotate_full_degree(big):
     cto, ctg, _ = big.encrypt_both(13, 13, 2.0 ** 40)
     ko, kg = big.galois_keys(50, 3)
     eq(big.ctx.rotate(ctg, 3, kg).data, big.ck.rotate(cto, 3, ko))
+
+
+def test_rotate_hoisted_full_degree_few_special_primes():
+    """N = 2^16 with 6 + 3 limbs and dnum 2: the ModDown's fused conversion and first forward pass take 3 source
+    limbs (the guarded variant; the benchmark parameters have 8), ModUp digits of 3 limbs, bit for bit."""
+    cfg = dataclasses.replace(KEYSWITCH, n_q=6, n_p=3, dnum=2, level=5, batch=3)
+    env = Env(cfg, 3)
+    say("rotate hoisted, 6 + 3 limbs at N = 2^16")
+    cto, ctg, _ = env.encrypt_both(31, 6, 2.0 ** 40)
+    steps = [1, 5, -3]
+    keys = [env.galois_keys(70 + i, st) for i, st in enumerate(steps)]
+    outs_g = env.ctx.rotate_hoisted(ctg, steps, [k[1] for k in keys])
+    outs_o = env.ck.rotate_hoisted(cto, steps, [k[0] for k in keys])
+    for og, oo in zip(outs_g, outs_o):
+        eq(og.data, oo)
 
 
 def test_mul_relin(toy):
