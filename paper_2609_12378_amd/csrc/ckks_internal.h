@@ -158,6 +158,10 @@ bool ntt_uses_f64(const ckks_ctx *ctx, uint32_t limbs);
 // column pass only of a forward transform (fp64 primes, two-pass sizes); the rows are left as raw doubles
 ckks_status launch_ntt_fwd_first_pass(ckks_ctx *ctx, uint64_t *data, uint32_t batch, uint32_t bstride,
                                       const LimbMap &map);
+// column pass only of an inverse transform whose row pass a fused kernel ran (rows as raw doubles below 2q; fp64
+// primes, two-pass sizes): canonical coefficients out
+ckks_status launch_ntt_inv_second_pass(ckks_ctx *ctx, uint64_t *data, uint32_t batch, uint32_t bstride,
+                                       const LimbMap &map);
 // column pass only of launch_ntt_from_i64 (two-pass sizes); the rows stay in the inter-pass form
 ckks_status launch_ntt_col_i64(ckks_ctx *ctx, const int64_t *m, uint64_t *out, uint32_t batch, uint32_t limbs);
 // nominal VALU instructions of one radix-2 butterfly: fp64 (product with FMA

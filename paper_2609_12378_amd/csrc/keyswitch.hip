@@ -398,7 +398,66 @@ __global__ __launch_bounds__(kThreads) void k_key_ip_acc(RotArgs ra, uint32_t nd
     u[(size_t)ext << log_n] = v1;
 }
 
-// ModDown of a batch of rotations, fused (fp64, 256-point rows): block (r, q-limb i, two rows h) finishes the
+// The key inner products of a rotation batch's P rows fused with the first (row) pass of their inverse
+// transform (fp64, 256-point rows): block (r, P limb i, two rows h), one wave, 8 positions per thread as in
+// k_ks_finish8.  u_k = sum_j sigma_{g_r}(d_j)[L + i] * key_r[j][k][n_q + i] (the products and range reductions
+// of k_ks_finish8's inner product), reduced below q/2 + 1, then the row's Gentleman-Sande stages with its inverse
+// twiddles; written as raw doubles below 2q to up[r][k][i], the inter-pass form the inverse column pass reads.
+// The P rows of u thus never go to HBM in canonical form to be read back by a separate row pass.
+__global__ __launch_bounds__(64) void k_key_ip_intt8(RotArgs ra, uint64_t *up, uint32_t nd, uint32_t ext,
+                                                     uint32_t L, uint32_t K, uint32_t n_q, uint32_t key_rows,
+                                                     const ModQ *__restrict__ mods, const double *__restrict__ itwf,
+                                                     uint32_t log_n, uint32_t blocks_per_limb)
+{
+    using nttc::kE8;
+    __shared__ double tws[2][257];
+    __shared__ double tr[2][nttc::kTr8];
+    const uint32_t per_rot = K * blocks_per_limb;
+    const uint32_t r = blockIdx.x / per_rot, rem = blockIdx.x % per_rot;
+    const uint32_t i = rem / blocks_per_limb, blk = rem % blocks_per_limb;
+    const uint32_t prime = n_q + i, row = L + i;
+    const nttc::Ar<true> ar(mods[prime]);
+    const uint32_t sub = threadIdx.x >> 5, t = threadIdx.x & 31;
+    const uint32_t h = blk * 2 + sub;
+    nttc::stage_twiddles8(tws[sub], itwf + ((size_t)prime << log_n), (1u << (log_n - 8)) + h, t, 32);
+    const uint32_t g = ra.g[r];
+    const uint64_t *key = ra.key[r];
+    const uint64_t *digits = ra.dig[r];
+    const size_t kstride = (size_t)key_rows << log_n;
+    double u[2][kE8];
+#pragma unroll
+    for (int e = 0; e < kE8; e++) {
+        const uint32_t pos = h * 256 + nttc::u8<0>(t, e);
+        const uint32_t sc = auto_index(pos, g, log_n);
+        double u0 = 0.0, u1 = 0.0;
+        for (uint32_t j = 0; j < nd; j++) {
+            const double d = nttc::Ar<true>::from_u64(digits[(((size_t)j * ext + row) << log_n) + sc]);
+            const uint64_t *kj = key + (((size_t)j * 2 * key_rows + prime) << log_n) + pos;
+            u0 += ar.mul(d, nttc::Ar<true>::from_u64(nttc::ld_stream(kj)));
+            u1 += ar.mul(d, nttc::Ar<true>::from_u64(nttc::ld_stream(kj + kstride)));
+            if ((j & 3) == 3) {
+                u0 = ar.red(u0);
+                u1 = ar.red(u1);
+            }
+        }
+        u[0][e] = ar.red(u0);
+        u[1][e] = ar.red(u1);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < 2; k++) {
+        double x[kE8];
+#pragma unroll
+        for (int e = 0; e < kE8; e++) x[e] = u[k][e];
+        nttc::a_to_b8(x, tr[sub], t);
+        nttc::inv8_256(x, tws[sub], tr[sub], t, ar);
+        uint64_t *out = up + ((((size_t)r * 2 + k) * K + i) << log_n) + (size_t)h * 256;
+#pragma unroll
+        for (int e = 0; e < kE8; e++) nttc::st_stream(out + nttc::u8<0>(t, e), nttc::Ar<true>::to_raw(x[e]));
+    }
+}
+
+// ModDown of a batch of rotations, fused (fp64, 256-point rows)// ModDown of a batch of rotations, fused (fp64, 256-point rows): block (r, q-limb i, two rows h) finishes the
 // forward transform of the converted P part cw[r][k][i] (its first pass already done), computes the q-limb part
 // of the key inner product u_k = sum_j sigma_{g_r}(d_j)[i] * key_r[j][k][i] in registers, and writes
 //   out_r[k][i] = (u_k - NTT(cw[r][k][i])) * P^-1 (+ sigma_{g_r}(c0)[i] for k = 0),
@@ -605,19 +664,32 @@ ckks_status ks_rotate_batch(ckks_ctx *ctx, uint32_t level, uint32_t count, const
         // fused ModDown: only the P rows of u are formed in HBM
         uint64_t *up = work;                             // [count][2][K][N]
         uint64_t *cw = up + (size_t)count * 2 * K * N;   // [count][2][L][N]
-        {
+        bool p_f64 = !ctx->int_only;
+        for (uint32_t i = 0; i < K; i++) p_f64 = p_f64 && ctx->f64_ok[ctx->n_q + i];
+        if (s1 == 8 && p_f64) {
+            // the P rows' inner products with the first pass of their inverse transform, then its second pass
+            const uint32_t bpl = 1u << (ctx->log_n - 9);
+            const double res = (double)count * 2 * K * N;
+            prof_begin(ctx, K_KEYIP, 8.0 * res * (nd + 1.0) + 8.0 * (double)nd * K * N,
+                       res * (nd * 10.0 + 4 * kOpsButterflyF64 + 8.0));
+            hipLaunchKernelGGL(k_key_ip_intt8, dim3(count * K * bpl), dim3(64), 0, ctx->stream, ra, up, nd, ext, L,
+                               K, ctx->n_q, ctx->n_primes(), ctx->d_mod, ctx->d_itwf, ctx->log_n, bpl);
+            prof_end(ctx, K_KEYIP);
+            HIP_TRY(hipGetLastError());
+            CK_TRY(launch_ntt_inv_second_pass(ctx, up, 2 * count, K, limb_range(ctx->n_q, K)));
+        } else {
             const dim3 grid((ctx->n + kThreads - 1) / kThreads, K, count), block(kThreads);
             prof_begin(ctx, K_KEYIP, 8.0 * ctx->n * K * (count * (2.0 * nd + 2.0) + nd));
             hipLaunchKernelGGL(k_key_ip_batch, grid, block, 0, ctx->stream, ra, up, nd, ext, level, ctx->n_q,
                                ctx->n_primes(), L, K, ctx->d_mod, ctx->log_n);
             prof_end(ctx, K_KEYIP);
             HIP_TRY(hipGetLastError());
+            CK_TRY(launch_ntt_strided(ctx, up, 2 * count, K, limb_range(ctx->n_q, K), true));
         }
-        CK_TRY(launch_ntt_strided(ctx, up, 2 * count, K, limb_range(ctx->n_q, K), true));
         const ConvDev *cd;
         CK_TRY(ctx_conv(ctx, (int)level, -1, &cd));
         if (s1 == 8 && cd->f64 && !ctx->int_only && cd->ns <= 8) {
-            // the conversion writes reduced raw doubles; the 8-residue column pass takes them as they are
+            // the conversion and the first forward pass of the converted rows in one kernel
             CK_TRY(launch_conv_col8(ctx, cd, up, K, cw, L, L, 0, 2 * count));
         } else {
             CK_TRY(launch_conv(ctx, cd, up, K, cw, L, L, 0, 2 * count));

@@ -507,6 +507,23 @@ ckks_status launch_ntt_fwd_first_pass(ckks_ctx *ctx, uint64_t *data, uint32_t ba
     return CKKS_OK;
 }
 
+// Second (column) pass only of the inverse transform of `batch` groups of map.n rows left by a fused first pass
+// as raw doubles below 2q (fp64 primes, two-pass size): canonical coefficients out.
+ckks_status launch_ntt_inv_second_pass(ckks_ctx *ctx, uint64_t *data, uint32_t batch, uint32_t bstride,
+                                       const LimbMap &map)
+{
+    if (!batch || !map.n) return CKKS_OK;
+    int s1, s2;
+    split_log((int)ctx->log_n, &s1, &s2);
+    CK_REQUIRE(s1 > 0 && use_f64(ctx, map), CKKS_EINVAL, "ntt: second pass alone needs two passes and fp64 primes");
+    const double res = (double)batch * map.n * ctx->n;
+    prof_begin(ctx, K_NTT_INV_COL, 16.0 * res, res * kOpsButterflyF64 * s1 / 2);
+    const hipError_t e = dispatch_col<true, true>(s1, ctx, data, batch, bstride, map);
+    prof_end(ctx, K_NTT_INV_COL);
+    if (e != hipSuccess) return set_error(CKKS_EHIP, "ntt launch failed: %s", hipGetErrorString(e));
+    return CKKS_OK;
+}
+
 bool ntt_uses_f64(const ckks_ctx *ctx, uint32_t limbs) { return use_f64(ctx, limb_range(0, limbs)); }
 
 // First (column) pass only of the forward NTT of m[batch][N] into out[batch][limbs][N]; the rows are left in the

@@ -329,6 +329,58 @@ __device__ __forceinline__ void b_to_a8(double (&x)[kE8], double *tr, uint32_t t
     __syncthreads();
 }
 
+// layout A -> layout B through LDS (the padding of b_to_a8)
+__device__ __forceinline__ void a_to_b8(double (&x)[kE8], double *tr, uint32_t t)
+{
+#pragma unroll
+    for (int k = 0; k < kE8; k++) tr[u8<0>(t, k) + (u8<0>(t, k) >> 5)] = x[k];
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < kE8; k++) x[k] = tr[u8<2>(t, k) + (u8<2>(t, k) >> 5)];
+    __syncthreads();
+}
+
+// The inverse of fwd8_256 without the factor 1/256: Gentleman-Sande butterflies with a staged table of inverse
+// twiddles (itws[2^s + g], as fwd8_256's table), stages 7 .. 0; layout B in, layout A out; every stage reduces,
+// so inputs below 2q stay below 2q.  Every thread of the block must call it (block barriers).
+template <int LAY, int S>
+__device__ __forceinline__ void inv8_stage(double (&x)[kE8], const double *itws, uint32_t t, const Ar<true> &ar)
+{
+    constexpr int b = 7 - S;
+    constexpr int rb = LAY == 0 ? b - 5 : LAY == 1 ? b - 2 : (b == 7 ? 2 : b);
+    static_assert(rb >= 0 && rb < 3, "stage not in this layout");
+#pragma unroll
+    for (int k = 0; k < kE8; k++) {
+        if (k & (1 << rb)) continue;
+        ar.gs(x[k], x[k | (1 << rb)], itws[(1u << S) + (u8<LAY>(t, k) >> (b + 1))]);
+    }
+}
+
+__device__ __forceinline__ void inv8_256(double (&x)[kE8], const double *itws, double *tr, uint32_t t,
+                                         const Ar<true> &ar)
+{
+    inv8_stage<2, 7>(x, itws, t, ar);
+    inv8_stage<2, 6>(x, itws, t, ar);
+#pragma unroll
+    for (int k = 0; k < kE8; k++) tr[pad_cb(u8<2>(t, k))] = x[k];
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < kE8; k++) x[k] = tr[pad_cb(u8<1>(t, k))];
+    __syncthreads();
+    inv8_stage<1, 5>(x, itws, t, ar);
+    inv8_stage<1, 4>(x, itws, t, ar);
+    inv8_stage<1, 3>(x, itws, t, ar);
+#pragma unroll
+    for (int k = 0; k < kE8; k++) tr[pad_ac(u8<1>(t, k))] = x[k];
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < kE8; k++) x[k] = tr[pad_ac(u8<0>(t, k))];
+    __syncthreads();
+    inv8_stage<0, 2>(x, itws, t, ar);
+    inv8_stage<0, 1>(x, itws, t, ar);
+    inv8_stage<0, 0>(x, itws, t, ar);
+}
+
 // twiddle table of a 256-point sub-transform with base B: tws[2^s + g] = Psi[B 2^s + g]
 // for 1 <= 2^s + g < 256; filled by `nthreads` threads starting at thread `tid`
 __device__ __forceinline__ void stage_twiddles8(double *tws, const double *tw, uint32_t B, uint32_t tid,
