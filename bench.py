@@ -141,11 +141,15 @@ def bench_tm(torch, np, steps, warmup, n1s=(16, 32)):
         outs = None
         for _ in range(warmup):
             outs = ctx.linear_project(st["cts"], st["Wd"], st["T"], n1, st["keys"], outs, layout="tm")
-        ctx.profile(True)
-        ctx.profile_reset()
+        # timed with the library's profiler off; the per-kernel figures from as many profiled steps afterwards
         with Timer(torch) as t:
             for _ in range(steps):
                 outs = ctx.linear_project(st["cts"], st["Wd"], st["T"], n1, st["keys"], outs, layout="tm")
+        ctx.profile(True)
+        ctx.profile_reset()
+        for _ in range(steps):
+            outs = ctx.linear_project(st["cts"], st["Wd"], st["T"], n1, st["keys"], outs, layout="tm")
+        torch.cuda.synchronize()
         prof = ctx.profile_all()
         ctx.profile(False)
         T, D = st["T"], st["D"]
@@ -262,8 +266,7 @@ def bench_attention(torch, np, steps, warmup):
         Y = step()
         torch.cuda.synchronize()
         log("attention warmup", w, "done")
-    ctx.profile(True)
-    ctx.profile_reset()
+    # timed with the library's profiler off; the per-kernel figures from as many profiled steps afterwards
     phase = {"qkv_projection": 0.0, "scores": 0.0, "weighted_sums": 0.0, "output_projection": 0.0}
     with Timer(torch) as t:
         for _ in range(steps):
@@ -271,6 +274,11 @@ def bench_attention(torch, np, steps, warmup):
             torch.cuda.synchronize()
             for name, (a, b) in zip(phase, (("a", "b"), ("b", "c"), ("c", "d"), ("d", "e"))):
                 phase[name] += ev[a].elapsed_time(ev[b]) / steps
+    ctx.profile(True)
+    ctx.profile_reset()
+    for _ in range(steps):
+        Y = step()
+    torch.cuda.synchronize()
     prof = ctx.profile_all()
     ctx.profile(False)
     want = attention_plain(np, X, Wq, Wk, Wv, Wo, T, hd, cfg.heads, cfg.kv_heads)
@@ -437,14 +445,18 @@ def bench_keyswitch(torch, np, steps, warmup):
     outs = ctx.rotate_hoisted(ct, rsteps, keys)
     for _ in range(warmup):
         ctx.rotate_hoisted(ct, rsteps, keys, outs)
-    # each batch bracketed by its own events: the median over the runs, and the kernels' profile over all
-    ctx.profile(True)
-    ctx.profile_reset()
+    # each batch bracketed by its own events, the library's profiler off: the median over the runs; then the same
+    # number of batches again with the profiler on (two events around every launch) for the per-kernel figures
     runs = []
     for _ in range(steps):
         with Timer(torch) as t:
             ctx.rotate_hoisted(ct, rsteps, keys, outs)
         runs.append(t.ms)
+    ctx.profile(True)
+    ctx.profile_reset()
+    for _ in range(steps):
+        ctx.rotate_hoisted(ct, rsteps, keys, outs)
+    torch.cuda.synchronize()
     prof = ctx.profile_all()
     ctx.profile(False)
     re, _ = ctx.decode(ctx.decrypt(s, outs[-1]))
@@ -486,8 +498,7 @@ def bench_ntt(torch, steps):
     for _ in range(2):
         ctx.ntt(x)
         ctx.intt(x)
-    ctx.profile(True)
-    ctx.profile_reset()
+    # timed with the library's profiler off; the per-kernel figures from as many profiled runs afterwards
     fwd, inv = [], []
     for _ in range(steps):
         with Timer(torch) as tf:
@@ -496,6 +507,12 @@ def bench_ntt(torch, steps):
         with Timer(torch) as ti:
             ctx.intt(x)
         inv.append(ti.ms)
+    ctx.profile(True)
+    ctx.profile_reset()
+    for _ in range(steps):
+        ctx.ntt(x)
+        ctx.intt(x)
+    torch.cuda.synchronize()
     prof = ctx.profile_all()
     ctx.profile(False)
     fms, ims = float(np.median(fwd)), float(np.median(inv))
