@@ -257,17 +257,20 @@ __global__ __launch_bounds__(512) void ntt_col8_from_i64(const int64_t *__restri
 // FIRST: input is canonical residues; LAST: write canonical residues (and, for
 // the inverse, multiply by N^-1).
 template <int LOGS, bool INV, bool FIRST, bool LAST, bool F, int LOGN = 0>
-__global__ __launch_bounds__(256) void ntt_row(uint64_t *data, LimbMap map, uint32_t bstride,
-                                               const ModQ *mods, const void *tw_all, uint32_t log_n_arg,
-                                               uint32_t rows_arg, uint32_t bpp_arg)
+__global__ __launch_bounds__(LOGN ? 128 : 256) void ntt_row(uint64_t *data, LimbMap map, uint32_t bstride,
+                                                             const ModQ *mods, const void *tw_all,
+                                                             uint32_t log_n_arg, uint32_t rows_arg, uint32_t bpp_arg)
 {
     using E = typename Ar<F>::E;
     constexpr uint32_t S = 1u << LOGS, TS = S / 16;
     const uint32_t log_n = LOGN ? LOGN : log_n_arg;
     const uint32_t rows_per_block = LOGN ? row_subs(LOGS, LOGN) : rows_arg;
     const uint32_t blocks_per_poly = LOGN ? (1u << (LOGN - LOGS)) / row_subs(LOGS, LOGN) : bpp_arg;
+    // compile-time ring degree: the LDS of the block's rows is static (row_subs rows, padded)
+    constexpr uint32_t kStatic = LOGN ? row_subs(LOGS, LOGN) * (S + S / 16 + 1) : 1;
+    __shared__ E lds_static[kStatic];
     extern __shared__ uint64_t lds_raw[];
-    E *lds = (E *)lds_raw;
+    E *lds = LOGN ? lds_static : (E *)lds_raw;
     uint32_t slot;
     const size_t poly = row_of_block(blockIdx.x / blocks_per_poly, map.n, bstride, &slot);
     const uint32_t blk = blockIdx.x % blocks_per_poly;
@@ -349,8 +352,8 @@ hipError_t launch_row(ckks_ctx *ctx, uint64_t *data, uint32_t batch, uint32_t bs
     const dim3 grid(batch * map.n * bpp), block(rows * TS);
     const void *tw = INV ? inv_table<F>(ctx) : fwd_table<F>(ctx);
     if (LOGS == 8 && ctx->log_n == 16)
-        hipLaunchKernelGGL((ntt_row<LOGS, INV, FIRST, LAST, F, 16>), grid, block, lds_bytes<LOGS>(rows), ctx->stream,
-                           data, map, bstride, ctx->d_mod, tw, ctx->log_n, rows, bpp);
+        hipLaunchKernelGGL((ntt_row<LOGS, INV, FIRST, LAST, F, 16>), grid, block, 0, ctx->stream, data, map, bstride,
+                           ctx->d_mod, tw, ctx->log_n, rows, bpp);
     else
         hipLaunchKernelGGL((ntt_row<LOGS, INV, FIRST, LAST, F>), grid, block, lds_bytes<LOGS>(rows), ctx->stream,
                            data, map, bstride, ctx->d_mod, tw, ctx->log_n, rows, bpp);
