@@ -383,8 +383,8 @@ __global__ __launch_bounds__(kThreads) void k_key_ip_acc(RotArgs ra, uint32_t nd
         for (uint32_t j = 0; j < nd; j++) {
             const uint64_t d = digits[(((size_t)j * ext + row) << log_n) + sc];
             const size_t kb = ((size_t)j * 2 * key_rows + prime) << log_n;
-            mac(a0, d, key[kb + col]);
-            mac(a1, d, key[kb + ((size_t)key_rows << log_n) + col]);
+            mac(a0, d, nttc::ld_stream(key + kb + col));
+            mac(a1, d, nttc::ld_stream(key + kb + ((size_t)key_rows << log_n) + col));
         }
         if (pq) mac(a0, ra.c0[r][((size_t)row << log_n) + sc], pq);
     }
