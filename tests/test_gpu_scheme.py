@@ -258,6 +258,36 @@ def test_rotate_hoisted_full_degree_few_special_primes():
         eq(og.data, oo)
 
 
+def test_rotate_hoisted_full_degree_wide_special_primes():
+    """N = 2^16 with 50-bit q primes and 55-bit special primes: the batched ModDown keeps the fp64 finish over the
+    q rows but takes the integer transforms and conversion for the P rows (no fp64-exact product there)."""
+    require_gpu()
+    from paper_2609_12378_amd import Context
+    ctx = Context(16, 4, 2, 2, q_bits=50, p_bits=55)
+    assert all(p >= 1 << 54 for p in ctx.p)
+    ck = Ckks(16, ctx.q, ctx.p, 2)
+    n = ctx.n
+    s = ternary_secret(rng(3, 3, extra=55), n)
+    re = uniform_slots(rng(3, 1, extra=55), n // 2)
+    g = rng(3, 4, extra=55)
+    a, e = uniform_residues(g, ctx.q, n), gaussian_error(g, n)
+    cto = ck.encrypt(s, ck.encode(re, None, 2.0 ** 40, 4), a, e)
+    ctg = ctx.encrypt(to_dev(s), ctx.encode(to_dev(re), None, 2.0 ** 40, 4), to_dev(a), to_dev(e))
+    steps = [1, -4]
+    keys_o, keys_g = [], []
+    for i, st in enumerate(steps):
+        gk = rng(3, 5, extra=550 + i)
+        ka, ke = uniform_residues(gk, ctx.primes, n, lead=(2,)), gaussian_error(gk, (2, n))
+        gel = ck.galois_elt(st)
+        keys_o.append(ck.keygen_galois(s, gel, ka, ke))
+        keys_g.append(ctx.keygen_galois(to_dev(s), gel, to_dev(ka), to_dev(ke)))
+    say("rotate hoisted, 55-bit special primes at N = 2^16")
+    outs_g = ctx.rotate_hoisted(ctg, steps, keys_g)
+    outs_o = ck.rotate_hoisted(cto, steps, keys_o)
+    for og, oo in zip(outs_g, outs_o):
+        eq(og.data, oo)
+
+
 def test_mul_relin(toy):
     c1o, c1g, _ = toy.encrypt_both(14, 4, 2.0 ** 30)
     c2o, c2g, _ = toy.encrypt_both(15, 4, 2.0 ** 30)
