@@ -206,7 +206,7 @@ def attention_plain(np, X, Wq, Wk, Wv, Wo, T, hd, heads, kv_heads):
 
 def bench_attention(torch, np, steps, warmup):
     """One Llama-3-8B attention block's ciphertext work in the token-major layout: Q, K, V projections, scores
-    on token diagonals, weighted sums of values (consuming the scores: Softmax is outside this build) and the
+    on token diagonals, weighted sums of values (consuming the scores; the Softmax between them is not part of this library) and the
     output projection, timed as one step."""
     from paper_2609_12378_amd import Context
     from workloads import ATTENTION as cfg, gaussian_error, gaussian_weights, rng, ternary_secret, \
@@ -689,7 +689,7 @@ def main():
     args = ap.parse_args()
     LAZY["on"] = bool(args.lazy_moddown)
     if args.gpus != 1:
-        print("bench.py runs on one GPU: the projection path is single-GPU in this build (--gpus %d requested)"
+        print("bench.py runs on one GPU: the library drives a single GPU (--gpus %d requested)"
               % args.gpus, file=sys.stderr)
         sys.exit(2)
     import numpy as np
