@@ -206,8 +206,8 @@ def attention_plain(np, X, Wq, Wk, Wv, Wo, T, hd, heads, kv_heads):
 
 def bench_attention(torch, np, steps, warmup):
     """One Llama-3-8B attention block's ciphertext work in the token-major layout: Q, K, V projections, scores
-    on token diagonals, weighted sums of values (consuming the scores; the Softmax between them is not part of this library) and the
-    output projection, timed as one step."""
+    on token diagonals, weighted sums of values (consuming the scores; the Softmax between them is not part of
+    this library) and the output projection, timed as one step."""
     from paper_2609_12378_amd import Context
     from workloads import ATTENTION as cfg, gaussian_error, gaussian_weights, rng, ternary_secret, \
         uniform_residues, uniform_slots
