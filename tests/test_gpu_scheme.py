@@ -288,6 +288,27 @@ def test_rotate_hoisted_full_degree_wide_special_primes():
         eq(og.data, oo)
 
 
+def test_keyswitch_benchmark_batch_sampled(big):
+    """The key-switching benchmark's own launch: 32 hoisted rotations by 1..32 of one level-23 ciphertext in one
+    batch; rotations 1, 17 and 32 against the oracle bit for bit (a hoisted batch equals the same rotations made
+    alone, so the oracle computes only those three)."""
+    say("keyswitch benchmark batch: 32 hoisted rotations at level 23")
+    cto, ctg, _ = big.encrypt_both(90, 24, 2.0 ** 40)
+    steps = list(range(1, 33))
+    keys_g, keys_o = [], {}
+    for st in steps:
+        a, e = big.key_randomness(200 + st)
+        gel = big.ctx.galois_elt(st)
+        keys_g.append(big.ctx.keygen_galois(big.s_dev, gel, to_dev(a), to_dev(e)))
+        if st in (1, 17, 32):
+            keys_o[st] = big.ck.keygen_galois(big.s, gel, a, e)
+    outs_g = big.ctx.rotate_hoisted(ctg, steps, keys_g)
+    sample = [1, 17, 32]
+    outs_o = big.ck.rotate_hoisted(cto, sample, [keys_o[st] for st in sample])
+    for st, oo in zip(sample, outs_o):
+        eq(outs_g[st - 1].data, oo)
+
+
 def test_mul_relin(toy):
     c1o, c1g, _ = toy.encrypt_both(14, 4, 2.0 ** 30)
     c2o, c2g, _ = toy.encrypt_both(15, 4, 2.0 ** 30)
