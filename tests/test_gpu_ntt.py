@@ -52,6 +52,22 @@ def test_ntt_n16_parity(ctx16, batch, limb0, n_limbs, arith):
     ctx16.set_ntt_arith(0)
 
 
+def test_ntt_benchmark_shape_sampled(ctx16):
+    """The NTT benchmark's own launch: 64 polynomials x 36 limbs x 2^16 in one call. Sampled rows bit for bit
+    against the oracle's transform; the round trip INTT(NTT(x)) == x on every row."""
+    say("ntt benchmark shape 64 x 36 x 2^16")
+    ck = Ckks(16, ctx16.q)
+    batch = NTT_BENCH.batch
+    a = uniform_residues(rng(2, 1, extra=640), ctx16.q, 1 << 16, lead=(batch,))
+    t = to_dev(a)
+    ctx16.ntt(t)
+    got = to_host(t)
+    for b, l in ((0, 0), (17, 35), (batch - 1, 18)):
+        assert np.array_equal(got[b, l], ck.ntt(a[b, l:l + 1], [l])[0]), (b, l)
+    ctx16.intt(t)
+    assert np.array_equal(to_host(t), a)
+
+
 @pytest.mark.parametrize("arith", [0, 1], ids=["fp64", "int"])
 @pytest.mark.parametrize("log_n", list(range(4, 16)))
 def test_ntt_all_degrees(log_n, arith):
