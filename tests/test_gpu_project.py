@@ -154,6 +154,48 @@ def test_projection_parameters_full_degree_slice():
     assert err <= 2.0 ** -18
 
 
+def test_projection_benchmark_shape_decrypted():
+    """The projection benchmark's own call: 4096 x 14336 weights, 16 input ciphertexts at level 12, n1 = 32, the
+    lazy ModDown and the default sub-batching, with the benchmark's seeded inputs. Too large for the oracle (4096
+    plaintexts per output block); the decrypted outputs 0, 27 and 55 must agree with X @ W within 2^-20, the
+    tolerance stated for decrypted projection results."""
+    require_gpu()
+    from paper_2609_12378_amd import Context
+    cfg = PROJECTION
+    ctx = Context(cfg.log_n, cfg.n_q, cfg.n_p, cfg.dnum, q_bits=cfg.q_bits)
+    ctx.set_lazy_moddown(True)
+    n, T, D, n1, level = ctx.n, cfg.tokens, cfg.feats, cfg.n1, cfg.level
+    n2 = -(-D // n1)
+    s_dev = to_dev(ternary_secret(rng(cfg.index, 3), n))
+    X = uniform_slots(rng(cfg.index, 1), (T, cfg.d_in))
+    W = gaussian_weights(rng(cfg.index, 2), (cfg.d_in, cfg.d_out))
+    delta = float(2 ** cfg.scale_log2)
+    ge = rng(cfg.index, 4)
+    cts = []
+    for i in range(cfg.d_in // D):
+        pt = ctx.encode(to_dev(fm_pack(X, T, D, i)), None, delta, level + 1)
+        a = uniform_residues(ge, ctx.q[:level + 1], n)
+        e = gaussian_error(ge, n)
+        cts.append(ctx.encrypt(s_dev, pt, to_dev(a), to_dev(e)))
+    steps = [T * b for b in range(1, n1)] + [T * n1 * g for g in range(1, n2)]
+    gk = rng(cfg.index, 5)
+    keys = {}
+    for st in steps:
+        a = uniform_residues(gk, ctx.primes, n, lead=(cfg.dnum,))
+        e = gaussian_error(gk, (cfg.dnum, n))
+        keys[st] = ctx.keygen_galois(s_dev, ctx.galois_elt(st), to_dev(a), to_dev(e))
+    say("benchmark-shape projection: keys ready", len(steps))
+    outs = ctx.linear_project(cts, to_dev(W), T, n1, keys)
+    assert len(outs) == cfg.d_out // D
+    for j in (0, 27, 55):
+        assert outs[j].scale == delta and outs[j].n_limbs == level
+        re, _ = ctx.decode(ctx.decrypt(s_dev, outs[j]))
+        want = fm_pack(X @ W[:, j * D:(j + 1) * D], T, D, 0)
+        err = float(np.max(np.abs(to_host(re) - want)))
+        say("output", j, "max error vs X@W", err)
+        assert err <= 2.0 ** -20
+
+
 def test_down_projection_parameters_full_degree_slice():
     say("down-projection slice (n1 = 8)")
     err = run_case(PROJ_DOWN, 512, 256, [0])
