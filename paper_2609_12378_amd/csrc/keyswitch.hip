@@ -765,25 +765,42 @@ ckks_status ks_modup_batch(ckks_ctx *ctx, const uint64_t *c1, size_t in_stride, 
     if (!count) return CKKS_OK;
     const uint32_t K = ctx->n_p, ext = level + 1 + K, nd = n_digits(ctx, level), alpha = ctx->alpha;
     const size_t N = ctx->n, dig_ct = (size_t)nd * ext * N;
+    const size_t cstride = count == 1 ? 0 : in_stride;
+    // A few ciphertexts leave each digit's transforms of its converted rows too small to fill the chip: then one
+    // forward transform runs over all ext rows of every digit (each digit's own rows are transformed along and
+    // overwritten with their NTT-domain values afterwards): 2 launches in place of 2 nd.  With more ciphertexts
+    // the per-digit launches are large, and transforming the own rows too would only add work.
+    const bool one_ntt = count < 4;
     // coefficient form of a digit's limbs, staged in alpha rows per ciphertext after all the digits
     uint64_t *coef = digits + (size_t)count * dig_ct;
+    LimbMap m{};
     for (uint32_t j = 0; j < nd; j++) {
         const uint32_t lo = digit_lo(ctx, j), hi = digit_hi(ctx, j, level), ns = hi - lo;
         uint64_t *dj = digits + (size_t)j * ext * N;
-        // the digit's own limbs keep their NTT-domain values; a second copy goes to the staging rows (one kernel
-        // reading them once: the runtime's strided copy moved them at under 1 TB/s)
-        CK_TRY(launch_copy_rows(ctx, dj + lo * N, dig_ct, coef, (size_t)alpha * N, c1 + lo * N,
-                                count == 1 ? 0 : in_stride, (size_t)ns * N, count));
+        // the digit's own limbs to the staging rows (and, unless they are written after the transform, into the
+        // digit with their NTT-domain values), read once
+        CK_TRY(launch_copy_rows(ctx, coef, (size_t)alpha * N, one_ntt ? nullptr : dj + lo * N, dig_ct, c1 + lo * N,
+                                cstride, (size_t)ns * N, count));
         CK_TRY(launch_ntt_strided(ctx, coef, count, alpha, limb_range(lo, ns), true));
         const ConvDev *cd;
         CK_TRY(ctx_conv(ctx, (int)level, (int)j, &cd));
         CK_TRY(launch_conv(ctx, cd, coef, alpha, dj, (uint32_t)(dig_ct / N), lo, ns, count));
+        if (one_ntt) continue;
         // NTT of the converted rows: [0, lo) and [hi, ext)
         if (lo) CK_TRY(launch_ntt_strided(ctx, dj, count, (uint32_t)(dig_ct / N), limb_range(0, lo), false));
-        LimbMap m{};
         m.n = ext - hi;
         for (uint32_t r = hi; r < ext; r++) m.prime[r - hi] = (uint8_t)(r <= level ? r : ctx->n_q + (r - level - 1));
         CK_TRY(launch_ntt_strided(ctx, dj + (size_t)hi * N, count, (uint32_t)(dig_ct / N), m, false));
+    }
+    if (one_ntt) {
+        m.n = ext;
+        for (uint32_t r = 0; r < ext; r++) m.prime[r] = (uint8_t)(r <= level ? r : ctx->n_q + (r - level - 1));
+        CK_TRY(launch_ntt_strided(ctx, digits, nd * count, ext, m, false));
+        for (uint32_t j = 0; j < nd; j++) {
+            const uint32_t lo = digit_lo(ctx, j), hi = digit_hi(ctx, j, level);
+            CK_TRY(launch_copy_rows(ctx, digits + ((size_t)j * ext + lo) * N, dig_ct, nullptr, 0, c1 + lo * N,
+                                    cstride, (size_t)(hi - lo) * N, count));
+        }
     }
     return CKKS_OK;
 }
