@@ -6,6 +6,9 @@
   on plain slot vectors, equals X @ W for every baby-step size n1.
 * End to end on the toy ring (N = 2^12, 16 tokens x 128 features, 127
   rotations): decrypt(linear_project(Enc(X), W)) is within 2^-12 of X @ W.
+* The same ring with giant steps (n1 = 16, n2 = 8; two inputs, three outputs),
+  eager and with the lazy ModDown: every output within 2^-12 of X @ W, so the
+  giant-step rotation Rot_{T n1 g} and the plaintexts' shift by n1 g are pinned.
 """
 import numpy as np
 import pytest
@@ -93,3 +96,49 @@ def test_toy_projection_accuracy(toy_projection):
         err = np.max(np.abs(z.real - fm_pack(Y, T, D, j)))
         assert err <= 2.0 ** -12, err
         assert np.max(np.abs(z.imag)) <= 2.0 ** -12
+
+
+@pytest.fixture(scope="module")
+def toy_bsgs_setup():
+    """The toy ring with a baby-step/giant-step split n1 = 16, n2 = 8: two input and three output ciphertexts."""
+    cfg = TOY
+    qs = gen_primes(cfg.q_bits, 2 * cfg.n, cfg.n_q + cfg.n_p)
+    ck = Ckks(cfg.log_n, qs[:cfg.n_q], qs[cfg.n_q:], cfg.dnum)
+    T, D, n1, level = cfg.tokens, cfg.feats, 16, cfg.level
+    n2 = D // n1
+    d_in, d_out = 2 * D, 3 * D
+    s = ternary_secret(rng(cfg.index, ROLE_SECRET, extra=7), ck.n)
+    X = uniform_slots(rng(cfg.index, ROLE_DATA, extra=7), (T, d_in))
+    W = gaussian_weights(rng(cfg.index, ROLE_WEIGHTS, extra=7), (d_in, d_out))
+    delta = float(2 ** cfg.scale_log2)
+    ge = rng(cfg.index, ROLE_ENC, extra=7)
+    cts = []
+    for i in range(d_in // D):
+        pt = ck.encode(fm_pack(X, T, D, i), None, delta, level + 1)
+        cts.append(ck.encrypt(s, pt, uniform_residues(ge, ck.q[:level + 1], ck.n), gaussian_error(ge, ck.n)))
+    gk = rng(cfg.index, ROLE_KEYS, extra=7)
+    keys = {}
+    for st in [T * b for b in range(1, n1)] + [T * n1 * g for g in range(1, n2)]:
+        a = uniform_residues(gk, ck.primes, ck.n, lead=(ck.dnum,))
+        e = gaussian_error(gk, (ck.dnum, ck.n))
+        keys[st] = ck.keygen_galois(s, ck.galois_elt(st), a, e)
+    return ck, s, X, W, cts, keys, delta, n1
+
+
+@pytest.mark.parametrize("lazy", [False, True])
+def test_toy_projection_giant_steps(toy_bsgs_setup, lazy):
+    """Seven giant-step rotations by T*n1*g per output (Eq. slot-diagonal-matvec with BSGS reuse): a wrong
+    giant-step shift, plaintext shift or rotation direction leaves an O(1) error, far above 2^-12."""
+    ck, s, X, W, cts, keys, delta, n1 = toy_bsgs_setup
+    T, D = TOY.tokens, TOY.feats
+    blocks = [1] if lazy else [0, 2]
+    outs = ck.linear_project(cts, W, T, n1, keys, out_blocks=blocks, lazy=lazy)
+    Y = X @ W
+    assert len(outs) == len(blocks)
+    for j, ct in zip(blocks, outs):
+        assert ct.shape == (2, TOY.level, ck.n)
+        z = ck.decode(ck.decrypt(s, ct), delta)
+        err = np.max(np.abs(z.real - fm_pack(Y, T, D, j)))
+        assert err <= 2.0 ** -12, (lazy, j, err)
+        assert np.max(np.abs(z.imag)) <= 2.0 ** -12
+

@@ -115,3 +115,46 @@ ATTN_TOY = Config("attn_toy", 8, 12, 50, 6, 2, 3, scale_log2=50, level=5, tokens
 # (with 32 and 16 outputs, half the hoisted baby steps of n1 = 32 save more than the extra giant steps cost).
 ATTENTION = Config("attention", 9, 16, 50, 24, 8, 3, scale_log2=50, level=12, tokens=128, d_in=4096,
                    d_out=4096, n1=16, head_dim=128, heads=32, kv_heads=8)
+
+
+def fm_pack(X: np.ndarray, tokens: int, feats: int, i: int) -> np.ndarray:
+    """Slot vector of input ciphertext i in the feature-major layout: slot f*tokens + t holds X[t, i*feats + f]."""
+    return X[:, i * feats:(i + 1) * feats].T.reshape(-1)
+
+
+@dataclass
+class ProjectionInputs:
+    """Every random quantity one feature-major projection workload draws, in the order the tests and the stored
+    expected values draw them: the secret, X, W, per input ciphertext the encryption randomness (a, e), and per
+    rotation step the key randomness (a, e) of its Galois key."""
+    s: np.ndarray
+    X: np.ndarray
+    W: np.ndarray
+    enc: list                      # [(a [level+1][N] uint64, e [N] int32)] per input ciphertext
+    keys: dict                     # step -> (a [dnum][n_q+n_p][N] uint64, e [dnum][N] int32)
+    steps: list
+
+
+def projection_inputs(cfg: Config, q: Sequence[int], primes: Sequence[int], d_in: Optional[int] = None,
+                      d_out: Optional[int] = None) -> ProjectionInputs:
+    """Seeded inputs of a feature-major projection with cfg's ring, level, tokens and n1 (d_in x d_out weights,
+    default cfg's): rotation steps T*b (0 < b < n1) then T*n1*g (0 < g < n2)."""
+    d_in = cfg.d_in if d_in is None else d_in
+    d_out = cfg.d_out if d_out is None else d_out
+    n, T, D, n1, level = cfg.n, cfg.tokens, cfg.feats, cfg.n1, cfg.level
+    n2 = -(-D // n1)
+    s = ternary_secret(rng(cfg.index, ROLE_SECRET), n)
+    X = uniform_slots(rng(cfg.index, ROLE_DATA), (T, d_in))
+    W = gaussian_weights(rng(cfg.index, ROLE_WEIGHTS), (d_in, d_out))
+    ge = rng(cfg.index, ROLE_ENC)
+    enc = []
+    for _ in range(d_in // D):
+        a = uniform_residues(ge, q[:level + 1], n)
+        enc.append((a, gaussian_error(ge, n)))
+    steps = [T * b for b in range(1, n1)] + [T * n1 * g for g in range(1, n2)]
+    gk = rng(cfg.index, ROLE_KEYS)
+    keys = {}
+    for st in steps:
+        a = uniform_residues(gk, primes, n, lead=(cfg.dnum,))
+        keys[st] = (a, gaussian_error(gk, (cfg.dnum, n)))
+    return ProjectionInputs(s, X, W, enc, keys, steps)
