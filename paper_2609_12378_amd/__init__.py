@@ -129,11 +129,31 @@ def _check(st: int, what: str):
 def _ptr(t: Optional[torch.Tensor]):
     if t is None:
         return None
+    if not isinstance(t, torch.Tensor):
+        raise CkksError("expected a torch tensor, got %s" % type(t).__name__)
     if not t.is_cuda:
         raise CkksError("expected a device tensor")
     if not t.is_contiguous():
         raise CkksError("expected a contiguous tensor")
     return ctypes.c_void_p(t.data_ptr())
+
+
+def _arg(t, what: str, dtype: torch.dtype, shape=None, numel: Optional[int] = None):
+    """Device pointer of t after checking what the kernels will assume of it: dtype, then shape (a tuple, or
+    only the element count), then device residency and contiguity.  A wrong host tensor, dtype or size would
+    otherwise be read out of bounds by a kernel, which the C ABI cannot detect."""
+    if not isinstance(t, torch.Tensor):
+        raise CkksError("%s: expected a torch tensor, got %s" % (what, type(t).__name__))
+    if t.dtype != dtype:
+        raise CkksError("%s: dtype %s, expected %s" % (what, t.dtype, dtype))
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise CkksError("%s: shape %s, expected %s" % (what, tuple(t.shape), tuple(shape)))
+    if numel is not None and t.numel() != numel:
+        raise CkksError("%s: %d elements, expected %d" % (what, t.numel(), numel))
+    try:
+        return _ptr(t)
+    except CkksError as e:
+        raise CkksError("%s: %s" % (what, e)) from None
 
 
 @dataclass
@@ -154,10 +174,15 @@ class Buf:
     def level(self) -> int:
         return self.n_limbs - 1
 
-    def c(self) -> _Buf:
+    def c(self, n: Optional[int] = None) -> _Buf:
+        """The C descriptor; with n, the ring degree the rows must have."""
         d = self.data
-        if d.dtype != torch.uint64 or d.dim() != 3:
+        if not isinstance(d, torch.Tensor) or d.dtype != torch.uint64 or d.dim() != 3:
             raise CkksError("buffer must be a 3-d uint64 tensor")
+        if n is not None and d.shape[2] != n:
+            raise CkksError("buffer rows have %d entries, the ring degree is %d" % (d.shape[2], n))
+        if not 1 <= d.shape[0] <= 3 or d.shape[1] < 1:
+            raise CkksError("buffer shape %s: 1-3 polynomials of at least one limb expected" % (tuple(d.shape),))
         return _Buf(_ptr(d), d.shape[0], d.shape[1], float(self.scale))
 
 
@@ -245,10 +270,13 @@ class Context:
     # ---------------- transforms ----------------
     def ntt(self, t: torch.Tensor, limb0: int = 0, inverse: bool = False):
         """In-place (inverse) NTT of t viewed as [batch][limbs][N]; limbs use primes limb0.."""
+        if t.dim() < 2 or t.shape[-1] != self.n:
+            raise CkksError("ntt: rows of %d residues expected, shape %s" % (self.n, tuple(t.shape)))
         nl = t.shape[-2]
         batch = t.numel() // (nl * self.n)
+        ptr = _arg(t, "ntt input", torch.uint64)
         fn = self.lib.ckks_intt if inverse else self.lib.ckks_ntt
-        _check(fn(self.h, _ptr(t), batch, limb0, nl), "ckks_intt" if inverse else "ckks_ntt")
+        _check(fn(self.h, ptr, batch, limb0, nl), "ckks_intt" if inverse else "ckks_ntt")
         return t
 
     def intt(self, t: torch.Tensor, limb0: int = 0):
@@ -259,30 +287,36 @@ class Context:
                out: Optional[torch.Tensor] = None) -> Buf:
         out = self.zeros(1, n_limbs) if out is None else out
         b = Buf(out, scale)
-        cb = b.c()
-        _check(self.lib.ckks_encode(self.h, _ptr(re), _ptr(im), float(scale), n_limbs, ctypes.byref(cb)),
-               "ckks_encode")
+        cb = b.c(self.n)
+        if out.shape[1] != n_limbs or out.shape[0] != 1:
+            raise CkksError("encode: output shape %s, expected (1, %d, %d)" % (tuple(out.shape), n_limbs, self.n))
+        pr = _arg(re, "encode re", torch.float64, numel=self.n // 2)
+        pi = None if im is None else _arg(im, "encode im", torch.float64, numel=self.n // 2)
+        _check(self.lib.ckks_encode(self.h, pr, pi, float(scale), n_limbs, ctypes.byref(cb)), "ckks_encode")
         return b
 
     def decode(self, pt: Buf):
         re = torch.empty(self.n // 2, dtype=torch.float64, device="cuda")
         im = torch.empty(self.n // 2, dtype=torch.float64, device="cuda")
-        cb = pt.c()
+        cb = pt.c(self.n)
         _check(self.lib.ckks_decode(self.h, ctypes.byref(cb), _ptr(re), _ptr(im)), "ckks_decode")
         return re, im
 
     # ---------------- encryption ----------------
     def encrypt(self, s: torch.Tensor, pt: Buf, a: torch.Tensor, e: torch.Tensor) -> Buf:
         out = Buf(self.zeros(2, pt.n_limbs), pt.scale)
-        cp, co = pt.c(), out.c()
-        _check(self.lib.ckks_encrypt_sk(self.h, _ptr(s), ctypes.byref(cp), _ptr(a), _ptr(e), ctypes.byref(co)),
-               "ckks_encrypt_sk")
+        cp, co = pt.c(self.n), out.c(self.n)
+        ps = _arg(s, "secret", torch.int8, numel=self.n)
+        pa = _arg(a, "encryption a", torch.uint64, numel=pt.n_limbs * self.n)
+        pe = _arg(e, "encryption error", torch.int32, numel=self.n)
+        _check(self.lib.ckks_encrypt_sk(self.h, ps, ctypes.byref(cp), pa, pe, ctypes.byref(co)), "ckks_encrypt_sk")
         return out
 
     def decrypt(self, s: torch.Tensor, ct: Buf) -> Buf:
         out = Buf(self.zeros(1, ct.n_limbs), ct.scale)
-        ci, co = ct.c(), out.c()
-        _check(self.lib.ckks_decrypt(self.h, _ptr(s), ctypes.byref(ci), ctypes.byref(co)), "ckks_decrypt")
+        ci, co = ct.c(self.n), out.c(self.n)
+        ps = _arg(s, "secret", torch.int8, numel=self.n)
+        _check(self.lib.ckks_decrypt(self.h, ps, ctypes.byref(ci), ctypes.byref(co)), "ckks_decrypt")
         return out
 
     def key_shape(self):
@@ -290,18 +324,30 @@ class Context:
 
     def keygen_galois(self, s, g: int, a, e, out=None) -> torch.Tensor:
         out = torch.empty(self.key_shape(), dtype=torch.uint64, device="cuda") if out is None else out
-        _check(self.lib.ckks_keygen_galois(self.h, _ptr(s), g, _ptr(a), _ptr(e), _ptr(out)), "ckks_keygen_galois")
+        ps, pa, pe, pk = self._keygen_args(s, a, e, out)
+        _check(self.lib.ckks_keygen_galois(self.h, ps, g, pa, pe, pk), "ckks_keygen_galois")
         return out
 
     def keygen_relin(self, s, a, e, out=None) -> torch.Tensor:
         out = torch.empty(self.key_shape(), dtype=torch.uint64, device="cuda") if out is None else out
-        _check(self.lib.ckks_keygen_relin(self.h, _ptr(s), _ptr(a), _ptr(e), _ptr(out)), "ckks_keygen_relin")
+        _check(self.lib.ckks_keygen_relin(self.h, *self._keygen_args(s, a, e, out)), "ckks_keygen_relin")
         return out
+
+    def _keygen_args(self, s, a, e, out):
+        ext = self.n_q + self.n_p
+        return (_arg(s, "secret", torch.int8, numel=self.n),
+                _arg(a, "key randomness a", torch.uint64, shape=(self.dnum, ext, self.n)),
+                _arg(e, "key error", torch.int32, numel=self.dnum * self.n),
+                self._key(out, "key output"))
+
+    def _key(self, k, what: str = "switching key"):
+        """Pointer of a switching key after checking it is a [dnum][2][n_q+n_p][N] uint64 device tensor."""
+        return _arg(k, what, torch.uint64, shape=self.key_shape())
 
     # ---------------- ciphertext operations ----------------
     def _binop(self, name, a: Buf, b: Buf, out_scale: float, out_limbs: int) -> Buf:
         out = Buf(self.zeros(2, out_limbs), out_scale)
-        ca, cb, co = a.c(), b.c(), out.c()
+        ca, cb, co = a.c(self.n), b.c(self.n), out.c(self.n)
         _check(getattr(self.lib, name)(self.h, ctypes.byref(ca), ctypes.byref(cb), ctypes.byref(co)), name)
         return out
 
@@ -313,56 +359,68 @@ class Context:
 
     def mul_relin(self, a: Buf, b: Buf, rlk: torch.Tensor) -> Buf:
         out = Buf(self.zeros(2, a.n_limbs), a.scale * b.scale)
-        ca, cb, co = a.c(), b.c(), out.c()
-        _check(self.lib.ckks_mul_relin(self.h, ctypes.byref(ca), ctypes.byref(cb), _ptr(rlk), ctypes.byref(co)),
-               "ckks_mul_relin")
+        ca, cb, co = a.c(self.n), b.c(self.n), out.c(self.n)
+        _check(self.lib.ckks_mul_relin(self.h, ctypes.byref(ca), ctypes.byref(cb), self._key(rlk, "relinearisation key"),
+                                       ctypes.byref(co)), "ckks_mul_relin")
         return out
 
     def rescale(self, ct: Buf) -> Buf:
         out = Buf(self.zeros(2, ct.n_limbs - 1), ct.scale / self.q[ct.level])
-        ci, co = ct.c(), out.c()
+        ci, co = ct.c(self.n), out.c(self.n)
         _check(self.lib.ckks_rescale(self.h, ctypes.byref(ci), ctypes.byref(co)), "ckks_rescale")
         return out
 
     def rotate(self, ct: Buf, steps: int, key: torch.Tensor) -> Buf:
         out = Buf(self.zeros(2, ct.n_limbs), ct.scale)
-        ci, co = ct.c(), out.c()
-        _check(self.lib.ckks_rotate(self.h, ctypes.byref(ci), steps, _ptr(key), ctypes.byref(co)), "ckks_rotate")
+        ci, co = ct.c(self.n), out.c(self.n)
+        _check(self.lib.ckks_rotate(self.h, ctypes.byref(ci), steps, self._key(key), ctypes.byref(co)), "ckks_rotate")
         return out
 
     def rotate_hoisted(self, ct: Buf, steps: Sequence[int], keys: Sequence[torch.Tensor],
                        outs: Optional[Sequence[Buf]] = None) -> List[Buf]:
         cnt = len(steps)
+        if len(keys) != cnt:
+            raise CkksError("rotate_hoisted: %d steps but %d keys" % (cnt, len(keys)))
+        if outs is not None and len(outs) < cnt:
+            raise CkksError("rotate_hoisted: %d outputs for %d steps" % (len(outs), cnt))
         if outs is None:
             outs = [Buf(self.zeros(2, ct.n_limbs), ct.scale) for _ in range(cnt)]
         st = (ctypes.c_int32 * cnt)(*steps)
-        kp = (ctypes.c_void_p * cnt)(*[k.data_ptr() for k in keys])
-        ob = (_Buf * cnt)(*[o.c() for o in outs])
-        ci = ct.c()
+        kp = (ctypes.c_void_p * cnt)(*[self._key(k).value for k in keys])
+        ob = (_Buf * cnt)(*[o.c(self.n) for o in outs])
+        ci = ct.c(self.n)
         _check(self.lib.ckks_rotate_hoisted(self.h, ctypes.byref(ci), st, cnt, kp, ob), "ckks_rotate_hoisted")
         return list(outs)
 
     def modup(self, c: torch.Tensor, level: int) -> torch.Tensor:
+        pc = _arg(c, "modup input", torch.uint64, numel=(level + 1) * self.n)
         out = torch.empty((self.n_digits(level), level + 1 + self.n_p, self.n), dtype=torch.uint64, device="cuda")
-        _check(self.lib.ckks_modup(self.h, _ptr(c), level, _ptr(out)), "ckks_modup")
+        _check(self.lib.ckks_modup(self.h, pc, level, _ptr(out)), "ckks_modup")
         return out
 
     def moddown(self, x: torch.Tensor, level: int) -> torch.Tensor:
+        px = _arg(x, "moddown input", torch.uint64, numel=(level + 1 + self.n_p) * self.n)
         out = torch.empty((level + 1, self.n), dtype=torch.uint64, device="cuda")
-        _check(self.lib.ckks_moddown(self.h, _ptr(x), level, _ptr(out)), "ckks_moddown")
+        _check(self.lib.ckks_moddown(self.h, px, level, _ptr(out)), "ckks_moddown")
         return out
 
     def automorph(self, x: torch.Tensor, g: int) -> torch.Tensor:
+        if x.numel() % self.n:
+            raise CkksError("automorph: %d residues is not a whole number of rows of %d" % (x.numel(), self.n))
+        px = _arg(x, "automorph input", torch.uint64)
         out = torch.empty_like(x)
         rows = x.numel() // self.n
-        _check(self.lib.ckks_automorph(self.h, _ptr(x), rows, g, _ptr(out)), "ckks_automorph")
+        _check(self.lib.ckks_automorph(self.h, px, rows, g, _ptr(out)), "ckks_automorph")
         return out
 
     def linear_project(self, cts: Sequence[Buf], W: torch.Tensor, tokens: int, n1: int,
                        keys: Dict[int, torch.Tensor], outs: Optional[Sequence[Buf]] = None,
                        layout: str = "fm") -> List[Buf]:
         """Y = X W on packed ciphertexts; layout "fm" (slot f*tokens + t) or "tm" (slot t*D + f)."""
+        if not isinstance(W, torch.Tensor) or W.dim() != 2:
+            raise CkksError("linear_project: W must be a 2-d (d_in, d_out) tensor")
         d_in, d_out = W.shape
+        pw = _arg(W, "weights W", torch.float64)
         D = (self.n // 2) // tokens
         n_out = d_out // D
         level = cts[0].level
@@ -372,16 +430,16 @@ class Context:
         if D > 0 and d_in % D == 0 and d_out % D == 0 and (len(cts) < d_in // D or len(outs) < n_out):
             raise ValueError("linear_project: %d inputs and %d outputs given, the shape needs %d and %d"
                              % (len(cts), len(outs), d_in // D, n_out))
-        inb = (_Buf * len(cts))(*[c.c() for c in cts])
-        ob = (_Buf * max(1, len(outs)))(*[o.c() for o in outs])
+        inb = (_Buf * len(cts))(*[c.c(self.n) for c in cts])
+        ob = (_Buf * max(1, len(outs)))(*[o.c(self.n) for o in outs])
         steps = sorted(keys)
         ks = (ctypes.c_int32 * len(steps))(*steps)
-        kp = (ctypes.c_void_p * len(steps))(*[keys[s].data_ptr() for s in steps])
+        kp = (ctypes.c_void_p * len(steps))(*[self._key(keys[s], "key for step %d" % s).value for s in steps])
         shape = _ProjShape(tokens, d_in, d_out, n1)
         if layout not in ("fm", "tm"):
             raise ValueError("layout must be 'fm' or 'tm'")
         fn = "ckks_linear_project" if layout == "fm" else "ckks_linear_project_tm"
-        _check(getattr(self.lib, fn)(self.h, inb, _ptr(W), ctypes.byref(shape), ks, kp, len(steps), ob), fn)
+        _check(getattr(self.lib, fn)(self.h, inb, pw, ctypes.byref(shape), ks, kp, len(steps), ob), fn)
         for o, b in zip(outs, ob):
             o.scale = b.scale
         return list(outs)
@@ -395,15 +453,17 @@ class Context:
                     for _ in a_cts]
         if len(outs) < len(a_cts):
             raise ValueError("%s: %d outputs for %d inputs" % (fn, len(outs), len(a_cts)))
-        ab = (_Buf * len(a_cts))(*[c.c() for c in a_cts])
-        bb = (_Buf * len(b_cts))(*[c.c() for c in b_cts])
-        ob = (_Buf * len(a_cts))(*[o.c() for o in outs[:len(a_cts)]])
+        ab = (_Buf * len(a_cts))(*[c.c(self.n) for c in a_cts])
+        bb = (_Buf * len(b_cts))(*[c.c(self.n) for c in b_cts])
+        ob = (_Buf * len(a_cts))(*[o.c(self.n) for o in outs[:len(a_cts)]])
         idx = (_U32 * len(a_cts))(*b_of_a)
         steps = sorted(keys)
         ks = (ctypes.c_int32 * max(1, len(steps)))(*steps)
-        kp = (ctypes.c_void_p * max(1, len(steps)))(*[keys[s].data_ptr() for s in steps])
+        kp = (ctypes.c_void_p * max(1, len(steps)))(*[self._key(keys[s], "key for step %d" % s).value
+                                                       for s in steps])
         shape = _AttnShape(tokens, head_dim)
-        _check(getattr(self.lib, fn)(self.h, ab, len(a_cts), bb, len(b_cts), idx, ctypes.byref(shape), _ptr(rlk), ks,
+        prlk = self._key(rlk, "relinearisation key")
+        _check(getattr(self.lib, fn)(self.h, ab, len(a_cts), bb, len(b_cts), idx, ctypes.byref(shape), prlk, ks,
                                      kp, len(steps), ob), fn)
         for o, b in zip(outs, ob):
             o.scale = b.scale

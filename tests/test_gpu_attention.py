@@ -8,6 +8,8 @@ and O[t, h, d] = sum_delta S[t, h, delta] V[(t + delta) mod T, d] within the sta
   ciphertexts on two key and two value ciphertexts, named out of order (the calls group them);
 * a ring of degree 2^13 with 32 tokens and four heads of 32 per ciphertext, and the toy ring with 8 tokens
   and four heads of 64 (several mask runs per correlation block);
+* a ring of degree 2^13 with 16 tokens and two heads of 128 per ciphertext: the correlation lengths of the
+  benchmark (128 and 256), eager and lazy;
 * the attention parameters at full degree (N = 2^16, 24 + 8 limbs, 128 tokens, two heads of 128 per
   ciphertext, inputs at level 11, scale 2^50: the launch shapes of the benchmark), two query ciphertexts on
   one key and one value ciphertext: decrypted results against the definitions (the oracle is too slow for
@@ -21,7 +23,8 @@ import pytest
 
 from gpu_common import require_gpu, say, to_dev, to_host
 from oracle import Ckks
-from workloads import (ATTENTION, ATTN_TOY, gaussian_error, rng, ternary_secret, uniform_residues)
+from workloads import (ATTENTION, ATTN_HD128, ATTN_TOY, attention_inputs, gaussian_error, rng, ternary_secret,
+                       uniform_residues)
 
 pytestmark = pytest.mark.gpu
 
@@ -47,49 +50,24 @@ def rep(Kh, D, hd):
     return np.tile(Kh, (1, D // hd))
 
 
-def run_parity(cfg, n_q, n_kv, kv_of_q, lazy=False):
-    require_gpu()
-    from paper_2609_12378_amd import Context
-    ctx = Context(cfg.log_n, cfg.n_q, cfg.n_p, cfg.dnum, q_bits=cfg.q_bits)
-    ctx.set_lazy_moddown(lazy)
-    ck = Ckks(cfg.log_n, ctx.q, ctx.p, cfg.dnum)
+def gpu_attention(ctx, cfg, inp, kv_of_q, lazy):
+    """Encrypt the inputs and generate the keys on the GPU, then run the scores and the weighted sums."""
     n, T, hd, level = ctx.n, cfg.tokens, cfg.head_dim, cfg.level
     D = (n // 2) // T
     delta = float(2 ** cfg.scale_log2)
-    s = ternary_secret(rng(cfg.index, 3, extra=50), n)
-    s_dev = to_dev(s)
-    g = rng(cfg.index, 1, extra=50)
-    Qs = [g.uniform(-1, 1, (T, D)) for _ in range(n_q)]
-    Ks = [g.uniform(-1, 1, (T, hd)) for _ in range(n_kv)]
-    Vs = [g.uniform(-1, 1, (T, hd)) for _ in range(n_kv)]
-    ge = rng(cfg.index, 4, extra=50)
-
-    def enc(x):
-        a = uniform_residues(ge, ctx.q[:level + 1], n)
-        e = gaussian_error(ge, n)
-        co = ck.encrypt(s, ck.encode(x.reshape(-1), None, delta, level + 1), a, e)
-        cg = ctx.encrypt(s_dev, ctx.encode(to_dev(x.reshape(-1)), None, delta, level + 1), to_dev(a), to_dev(e))
-        return co, cg
-
-    q_o, q_g = zip(*[enc(Q) for Q in Qs])
-    k_o, k_g = zip(*[enc(rep(K, D, hd)) for K in Ks])
-    v_o, v_g = zip(*[enc(rep(V, D, hd)) for V in Vs])
-    gk = rng(cfg.index, 5, extra=50)
-    keys_o, keys_g = {}, {}
-    for st in Context.attention_steps(n // 2, T, hd):
-        a = uniform_residues(gk, ctx.primes, n, lead=(cfg.dnum,))
-        e = gaussian_error(gk, (cfg.dnum, n))
-        gel = ck.galois_elt(st)
-        keys_o[st] = ck.keygen_galois(s, gel, a, e)
-        keys_g[st] = ctx.keygen_galois(s_dev, gel, to_dev(a), to_dev(e))
-    a = uniform_residues(gk, ctx.primes, n, lead=(cfg.dnum,))
-    e = gaussian_error(gk, (cfg.dnum, n))
-    rlk_o = ck.keygen_relin(s, a, e)
-    rlk_g = ctx.keygen_relin(s_dev, to_dev(a), to_dev(e))
+    s_dev = to_dev(inp.s)
+    plain = list(inp.Q) + [rep(K, D, hd) for K in inp.K] + [rep(V, D, hd) for V in inp.V]
+    cts = [ctx.encrypt(s_dev, ctx.encode(to_dev(x.reshape(-1)), None, delta, level + 1), to_dev(a), to_dev(e))
+           for x, (a, e) in zip(plain, inp.enc)]
+    n_q, n_kv = len(inp.Q), len(inp.K)
+    q_g, k_g, v_g = cts[:n_q], cts[n_q:n_q + n_kv], cts[n_q + n_kv:]
+    keys_g = {st: ctx.keygen_galois(s_dev, ctx.galois_elt(st), to_dev(a), to_dev(e)) for st, (a, e) in inp.keys.items()}
+    rlk_g = ctx.keygen_relin(s_dev, to_dev(inp.rlk[0]), to_dev(inp.rlk[1]))
     say("keys ready", len(keys_g))
+    ctx.set_lazy_moddown(lazy)
     ctx.profile(True)
     ctx.profile_reset()
-    S_g = ctx.attention_scores(list(q_g), list(k_g), kv_of_q, T, hd, rlk_g, keys_g)
+    S_g = ctx.attention_scores(q_g, k_g, kv_of_q, T, hd, rlk_g, keys_g)
     moddowns = ctx.profile_read("moddown")[1]
     ctx.profile(False)
     if lazy:
@@ -98,14 +76,47 @@ def run_parity(cfg, n_q, n_kv, kv_of_q, lazy=False):
         b32 = -(-(T - 1) // 32)
         expect = len(set(kv_of_q)) * b32 + n_q * (b32 + -(-T // 32) + 1)
         assert moddowns == expect, (moddowns, expect)
-    O_g = ctx.attention_apply(S_g, list(v_g), kv_of_q, T, hd, rlk_g, keys_g)
+    O_g = ctx.attention_apply(S_g, v_g, kv_of_q, T, hd, rlk_g, keys_g)
     say("gpu attention done")
-    S_o = ck.attention_scores(list(q_o), list(k_o), kv_of_q, T, hd, rlk_o, keys_o, lazy=lazy)
-    O_o = ck.attention_apply(S_o, list(v_o), kv_of_q, T, hd, rlk_o, keys_o)
+    return S_g, O_g, s_dev
+
+
+def decrypted_errors(ctx, cfg, inp, kv_of_q, S_g, O_g, s_dev):
+    """Max decrypted error of the scores and the sums against the plain definitions."""
+    T, hd = cfg.tokens, cfg.head_dim
+    D = (ctx.n // 2) // T
+    errs_s, errs_o = [], []
+    for c in range(len(S_g)):
+        Sd = scores_def(inp.Q[c], inp.K[kv_of_q[c]], T, D, hd)
+        re, _ = ctx.decode(ctx.decrypt(s_dev, S_g[c]))
+        errs_s.append(np.max(np.abs(to_host(re).reshape(T, D) - Sd)))
+        Od = apply_def(Sd, inp.V[kv_of_q[c]], T, D, hd)
+        re, _ = ctx.decode(ctx.decrypt(s_dev, O_g[c]))
+        errs_o.append(np.max(np.abs(to_host(re).reshape(T, D) - Od)))
+    return max(errs_s), max(errs_o)
+
+
+def run_parity(cfg, n_q, n_kv, kv_of_q, lazy=False):
+    require_gpu()
+    from paper_2609_12378_amd import Context
+    ctx = Context(cfg.log_n, cfg.n_q, cfg.n_p, cfg.dnum, q_bits=cfg.q_bits)
+    ck = Ckks(cfg.log_n, ctx.q, ctx.p, cfg.dnum)
+    n, T, hd, level = ctx.n, cfg.tokens, cfg.head_dim, cfg.level
+    D = (n // 2) // T
+    delta = float(2 ** cfg.scale_log2)
+    inp = attention_inputs(cfg, ctx.q, ctx.primes, n_q, n_kv)
+    S_g, O_g, s_dev = gpu_attention(ctx, cfg, inp, kv_of_q, lazy)
+    plain = list(inp.Q) + [rep(K, D, hd) for K in inp.K] + [rep(V, D, hd) for V in inp.V]
+    cts = [ck.encrypt(inp.s, ck.encode(x.reshape(-1), None, delta, level + 1), a, e)
+           for x, (a, e) in zip(plain, inp.enc)]
+    q_o, k_o, v_o = cts[:n_q], cts[n_q:n_q + n_kv], cts[n_q + n_kv:]
+    keys_o = {st: ck.keygen_galois(inp.s, ck.galois_elt(st), a, e) for st, (a, e) in inp.keys.items()}
+    rlk_o = ck.keygen_relin(inp.s, *inp.rlk)
+    S_o = ck.attention_scores(q_o, k_o, kv_of_q, T, hd, rlk_o, keys_o, lazy=lazy)
+    O_o = ck.attention_apply(S_o, v_o, kv_of_q, T, hd, rlk_o, keys_o)
     say("oracle attention done")
     s_scale = delta * delta / ctx.q[level - 1]
     o_scale = s_scale * delta / ctx.q[level - 2]
-    errs_s, errs_o = [], []
     for c in range(n_q):
         for got, want, scale, name in ((S_g[c], S_o[c], s_scale, "scores"), (O_g[c], O_o[c], o_scale, "sums")):
             gh = to_host(got.data)
@@ -113,13 +124,7 @@ def run_parity(cfg, n_q, n_kv, kv_of_q, lazy=False):
             bad = np.argwhere(gh != want)
             assert bad.size == 0, "%s %d: first mismatches %s" % (name, c, bad[:5].tolist())
             assert got.scale == scale, (name, got.scale, scale)
-        Sd = scores_def(Qs[c], Ks[kv_of_q[c]], T, D, hd)
-        re, _ = ctx.decode(ctx.decrypt(s_dev, S_g[c]))
-        errs_s.append(np.max(np.abs(to_host(re).reshape(T, D) - Sd)))
-        Od = apply_def(Sd, Vs[kv_of_q[c]], T, D, hd)
-        re, _ = ctx.decode(ctx.decrypt(s_dev, O_g[c]))
-        errs_o.append(np.max(np.abs(to_host(re).reshape(T, D) - Od)))
-    return max(errs_s), max(errs_o)
+    return decrypted_errors(ctx, cfg, inp, kv_of_q, S_g, O_g, s_dev)
 
 
 def test_toy_attention_parity_grouped():
@@ -151,6 +156,41 @@ def test_attention_parity_eight_tokens():
     say("8-token attention max error: scores %.3g, sums %.3g" % (es, eo))
     assert es <= 2.0 ** -30
     assert eo <= 2.0 ** -28
+
+
+@pytest.mark.parametrize("mode", ["eager", "lazy"])
+def test_attention_parity_bench_correlation_lengths(mode):
+    """Heads of 128 with 16 tokens at N = 2^13 (256 features, two heads per ciphertext): the correlations run at
+    the benchmark's lengths (128 for the scores, 256 for the weighted sums) with its positions per block.  The
+    oracle's outputs for these seeded inputs are stored as SHA-256 digests (with 32 residues per row to locate a
+    mismatch) by tests/golden/make_attention_golden.py; both outputs must match them bit for bit, with the
+    oracle's scales, eager and with the lazy ModDown of the outer sum."""
+    require_gpu()
+    import hashlib
+    import json
+    import os
+    from paper_2609_12378_amd import Context
+    with open(os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden",
+                           "attention_n13_hd128_outputs.json")) as f:
+        golden = json.load(f)
+    cfg = ATTN_HD128
+    ctx = Context(cfg.log_n, cfg.n_q, cfg.n_p, cfg.dnum, q_bits=cfg.q_bits)
+    inp = attention_inputs(cfg, ctx.q, ctx.primes, 1, 1)
+    S_g, O_g, s_dev = gpu_attention(ctx, cfg, inp, [0], mode == "lazy")
+    pos = golden["positions"]
+    for got, name in ((S_g[0], "scores"), (O_g[0], "sums")):
+        rec = golden["modes"][mode][name]
+        gh = to_host(got.data)
+        assert list(gh.shape) == rec["shape"], name
+        samples = np.array([gh[c, r, pos] for c in range(gh.shape[0]) for r in range(gh.shape[1])], dtype=np.uint64)
+        bad = np.argwhere(samples != np.array(rec["samples"], dtype=np.uint64))
+        assert bad.size == 0, "%s: sampled residues differ at (row, sample) %s" % (name, bad[:5].tolist())
+        assert hashlib.sha256(np.ascontiguousarray(gh, dtype="<u8").tobytes()).hexdigest() == rec["sha256"], name
+        assert got.scale == rec["scale"], (name, got.scale, rec["scale"])
+    es, eo = decrypted_errors(ctx, cfg, inp, [0], S_g, O_g, s_dev)
+    say("N=2^13, hd=128 attention (%s) max error: scores %.3g, sums %.3g" % (mode, es, eo))
+    assert es <= 2.0 ** -28
+    assert eo <= 2.0 ** -26
 
 
 def _dev_keys(ctx, s_dev, steps, seed):

@@ -18,7 +18,9 @@
   within 2^-18 of X @ W.
 
 * the down-projection parameters (n1 = 8, n2 = 32: 7 baby and 31 giant rotations) on a
-  512 x 256 slice (two input ciphertexts, one output), bit for bit.
+  512 x 256 slice (two input ciphertexts, one output), bit for bit;
+* the projection benchmark's own 4096 x 14336 call in its launch configuration:
+  outputs 0, 27 and 55 bit for bit against the oracle's stored digests.
 
 Every compared output is also decrypted and decoded on both sides: the GPU's
 slots agree with the oracle's within 2^-20 of the scale.
@@ -154,45 +156,53 @@ def test_projection_parameters_full_degree_slice():
     assert err <= 2.0 ** -18
 
 
-def test_projection_benchmark_shape_decrypted():
+def test_projection_benchmark_shape_bit_exact():
     """The projection benchmark's own call: 4096 x 14336 weights, 16 input ciphertexts at level 12, n1 = 32, the
-    lazy ModDown and the default sub-batching, with the benchmark's seeded inputs. Too large for the oracle (4096
-    plaintexts per output block); the decrypted outputs 0, 27 and 55 must agree with X @ W within 2^-20, the
-    tolerance stated for decrypted projection results."""
+    lazy ModDown and the default sub-batching (28-output tiles, 128 pairs per launch), with the benchmark's seeded
+    inputs.  Output ciphertexts 0, 27 and 55 are compared in full against the oracle's, stored as SHA-256
+    digests (with 32 residues per row to locate a mismatch) by tests/golden/make_projection_golden.py; their
+    decrypted slots must also agree with X @ W within 2^-20, the tolerance stated for decrypted projection
+    results."""
     require_gpu()
+    import hashlib
+    import json
+    import os
     from paper_2609_12378_amd import Context
+    from workloads import projection_inputs
+    golden_path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden",
+                               "projection_4096x14336_outputs.json")
+    with open(golden_path) as f:
+        golden = json.load(f)
     cfg = PROJECTION
     ctx = Context(cfg.log_n, cfg.n_q, cfg.n_p, cfg.dnum, q_bits=cfg.q_bits)
     ctx.set_lazy_moddown(True)
     n, T, D, n1, level = ctx.n, cfg.tokens, cfg.feats, cfg.n1, cfg.level
-    n2 = -(-D // n1)
-    s_dev = to_dev(ternary_secret(rng(cfg.index, 3), n))
-    X = uniform_slots(rng(cfg.index, 1), (T, cfg.d_in))
-    W = gaussian_weights(rng(cfg.index, 2), (cfg.d_in, cfg.d_out))
+    inp = projection_inputs(cfg, ctx.q, ctx.primes)
+    s_dev = to_dev(inp.s)
     delta = float(2 ** cfg.scale_log2)
-    ge = rng(cfg.index, 4)
     cts = []
-    for i in range(cfg.d_in // D):
-        pt = ctx.encode(to_dev(fm_pack(X, T, D, i)), None, delta, level + 1)
-        a = uniform_residues(ge, ctx.q[:level + 1], n)
-        e = gaussian_error(ge, n)
+    for i, (a, e) in enumerate(inp.enc):
+        pt = ctx.encode(to_dev(fm_pack(inp.X, T, D, i)), None, delta, level + 1)
         cts.append(ctx.encrypt(s_dev, pt, to_dev(a), to_dev(e)))
-    steps = [T * b for b in range(1, n1)] + [T * n1 * g for g in range(1, n2)]
-    gk = rng(cfg.index, 5)
-    keys = {}
-    for st in steps:
-        a = uniform_residues(gk, ctx.primes, n, lead=(cfg.dnum,))
-        e = gaussian_error(gk, (cfg.dnum, n))
-        keys[st] = ctx.keygen_galois(s_dev, ctx.galois_elt(st), to_dev(a), to_dev(e))
-    say("benchmark-shape projection: keys ready", len(steps))
-    outs = ctx.linear_project(cts, to_dev(W), T, n1, keys)
+    keys = {st: ctx.keygen_galois(s_dev, ctx.galois_elt(st), to_dev(a), to_dev(e)) for st, (a, e) in inp.keys.items()}
+    say("benchmark-shape projection: keys ready", len(keys))
+    outs = ctx.linear_project(cts, to_dev(inp.W), T, n1, keys)
     assert len(outs) == cfg.d_out // D
+    pos = golden["positions"]
     for j in (0, 27, 55):
+        rec = golden["outputs"][str(j)]
         assert outs[j].scale == delta and outs[j].n_limbs == level
+        got = to_host(outs[j].data)
+        assert list(got.shape) == rec["shape"]
+        samples = np.array([got[c, r, pos] for c in range(2) for r in range(level)], dtype=np.uint64)
+        bad = np.argwhere(samples != np.array(rec["samples"], dtype=np.uint64))
+        assert bad.size == 0, "output %d: sampled residues differ at (row, sample) %s" % (j, bad[:5].tolist())
+        digest = hashlib.sha256(np.ascontiguousarray(got, dtype="<u8").tobytes()).hexdigest()
+        assert digest == rec["sha256"], "output %d: full ciphertext differs from the oracle's" % j
         re, _ = ctx.decode(ctx.decrypt(s_dev, outs[j]))
-        want = fm_pack(X @ W[:, j * D:(j + 1) * D], T, D, 0)
+        want = fm_pack(inp.X @ inp.W[:, j * D:(j + 1) * D], T, D, 0)
         err = float(np.max(np.abs(to_host(re) - want)))
-        say("output", j, "max error vs X@W", err)
+        say("output", j, "bit-exact against the oracle; max error vs X@W", err)
         assert err <= 2.0 ** -20
 
 

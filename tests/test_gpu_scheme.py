@@ -318,6 +318,24 @@ def test_mul_relin(toy):
     eq(toy.ctx.mul_relin(c1g, c2g, rlk_g).data, toy.ck.mul_relin(c1o, c2o, rlk_o))
 
 
+@pytest.mark.parametrize("limbs", [24, 13])
+def test_mul_relin_full_degree(big, limbs):
+    """Mult + relinearisation at N = 2^16 (24 + 8 limbs of 50-bit primes, dnum 3): at level 23 (three full digits)
+    and level 12 (a partial second digit), bit for bit, and decrypted close to the slot-wise product."""
+    say("mul_relin at N = 2^16 with", limbs, "limbs")
+    c1o, c1g, (r1, i1) = big.encrypt_both(30 + limbs, limbs, 2.0 ** 40)
+    c2o, c2g, (r2, i2) = big.encrypt_both(31 + limbs, limbs, 2.0 ** 40)
+    a, e = big.key_randomness(61)
+    rlk_o = big.ck.keygen_relin(big.s, a, e)
+    rlk_g = big.ctx.keygen_relin(big.s_dev, to_dev(a), to_dev(e))
+    out = big.ctx.mul_relin(c1g, c2g, rlk_g)
+    eq(out.data, big.ck.mul_relin(c1o, c2o, rlk_o))
+    assert out.scale == 2.0 ** 80
+    dre, dim = big.ctx.decode(big.ctx.decrypt(big.s_dev, out))
+    z = to_host(dre) + 1j * to_host(dim)
+    assert np.max(np.abs(z - (r1 + 1j * i1) * (r2 + 1j * i2))) < 2.0 ** -20
+
+
 def test_decrypted_rotation_is_slot_shift(toy):
     cto, ctg, (re, im) = toy.encrypt_both(16, 4, 2.0 ** 30)
     _, kg = toy.galois_keys(70, 5)

@@ -158,3 +158,57 @@ def projection_inputs(cfg: Config, q: Sequence[int], primes: Sequence[int], d_in
         a = uniform_residues(gk, primes, n, lead=(cfg.dnum,))
         keys[st] = (a, gaussian_error(gk, (cfg.dnum, n)))
     return ProjectionInputs(s, X, W, enc, keys, steps)
+
+
+@dataclass
+class AttentionInputs:
+    """Every random quantity of one attention-block parity workload, in the order the tests and the stored
+    expected values draw them: the secret; the query blocks Q [T][D], key and value heads K, V [T][hd]; per
+    ciphertext (queries, then keys, then values) its encryption randomness (a, e); per rotation step (ascending)
+    the Galois-key randomness (a, e); last the relinearisation-key randomness."""
+    s: np.ndarray
+    Q: list
+    K: list
+    V: list
+    enc: list
+    keys: dict
+    rlk: tuple
+
+
+def attention_steps(slots: int, tokens: int, head_dim: int) -> list:
+    """Every rotation step of the scores and weighted sums for T tokens and heads of hd (D = slots / T): -delta
+    and delta (D - 1), 1 .. hd - 1, delta D (0 < delta < T), and j (-hd < j < T, j != 0)."""
+    D = slots // tokens
+    st = set(-d for d in range(1, tokens)) | set(d * (D - 1) for d in range(1, tokens)) | set(range(1, head_dim))
+    st |= set(d * D for d in range(1, tokens)) | set(j for j in range(-head_dim + 1, tokens) if j)
+    return sorted(st)
+
+
+def attention_inputs(cfg: Config, q: Sequence[int], primes: Sequence[int], n_q: int, n_kv: int,
+                     extra: int = 50) -> AttentionInputs:
+    n, T, hd, level = cfg.n, cfg.tokens, cfg.head_dim, cfg.level
+    D = (n // 2) // T
+    s = ternary_secret(rng(cfg.index, ROLE_SECRET, extra=extra), n)
+    g = rng(cfg.index, ROLE_DATA, extra=extra)
+    Q = [g.uniform(-1, 1, (T, D)) for _ in range(n_q)]
+    K = [g.uniform(-1, 1, (T, hd)) for _ in range(n_kv)]
+    V = [g.uniform(-1, 1, (T, hd)) for _ in range(n_kv)]
+    ge = rng(cfg.index, ROLE_ENC, extra=extra)
+    enc = []
+    for _ in range(n_q + 2 * n_kv):
+        a = uniform_residues(ge, q[:level + 1], n)
+        enc.append((a, gaussian_error(ge, n)))
+    gk = rng(cfg.index, ROLE_KEYS, extra=extra)
+    keys = {}
+    for st in attention_steps(n // 2, T, hd):
+        a = uniform_residues(gk, primes, n, lead=(cfg.dnum,))
+        keys[st] = (a, gaussian_error(gk, (cfg.dnum, n)))
+    a = uniform_residues(gk, primes, n, lead=(cfg.dnum,))
+    return AttentionInputs(s, Q, K, V, enc, keys, (a, gaussian_error(gk, (cfg.dnum, n))))
+
+
+# The attention parity case at the benchmark's correlation lengths: N = 2^13, 6 + 2 limbs of 50-bit primes, 16 tokens
+# x 256 features = two heads of 128 per ciphertext (scores correlate over 128 positions, the weighted sums over 256),
+# inputs at level 5, scale 2^50, one query, key and value ciphertext.
+ATTN_HD128 = Config("attn13_hd128", 8, 13, 50, 6, 2, 3, scale_log2=50, level=5, tokens=16, head_dim=128, heads=2,
+                    kv_heads=1)
