@@ -82,7 +82,8 @@ typedef struct {
 
 /* Create a context on the current HIP device: generates or checks primes,
  * finds psi_k (x^((q-1)/2N) for the smallest x >= 2 with psi^N = -1), and
- * uploads twiddle, Shoup-companion, FFT and basis-conversion tables.
+ * uploads twiddle, Shoup-companion, FFT and basis-conversion tables (the
+ * latter for ModUp and ModDown at every level).
  * hip_stream: the hipStream_t all calls are enqueued on (NULL = default). */
 ckks_status ckks_ctx_create(const ckks_params *params, void *hip_stream, ckks_ctx **out);
 void ckks_ctx_destroy(ckks_ctx *ctx);
@@ -120,9 +121,9 @@ ckks_status ckks_ctx_tables(const ckks_ctx *ctx, uint64_t *q, uint64_t *p, uint6
  * bytes) makes dev[0, bytes) (device memory, 256-byte aligned, owned by the
  * caller, which keeps it alive until the context is destroyed or another
  * workspace is set) the arena; the library frees its own arena and never
- * allocates scratch again (the basis-conversion tables of every level, which
- * calls otherwise build on first use, are built here), and a call that needs
- * more than `bytes` fails with CKKS_ENOMEM before any launch.  ckks_set_workspace(ctx, NULL, 0)
+ * allocates scratch again (every table, including each level's
+ * basis-conversion constants, is built by ckks_ctx_create), and a call that
+ * needs more than `bytes` fails with CKKS_ENOMEM before any launch.  ckks_set_workspace(ctx, NULL, 0)
  * returns to library-managed scratch.  It synchronizes the context stream
  * first (work in flight may still use the old arena).  All calls on one
  * context share the workspace, so they must be ordered on its stream.
@@ -219,6 +220,23 @@ ckks_status ckks_rotate(ckks_ctx *ctx, const ckks_buf *in, int32_t steps, const 
  * Result r equals ckks_rotate(in, steps[r], dev_keys[r]) bit for bit. */
 ckks_status ckks_rotate_hoisted(ckks_ctx *ctx, const ckks_buf *in, const int32_t *steps, uint32_t count,
                                 const uint64_t *const *dev_keys, ckks_buf *outs);
+
+/* Allocation-free rotation, for callers that cannot allocate device memory:
+ * code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc.  The operation, arguments and errors are those of ckks_rotate,
+ * and the output equals ckks_rotate's bit for bit; this call takes nothing
+ * from the context's arena or workspace and calls no allocating routine.
+ * Its scratch is a static device buffer of 128 MiB that each device the
+ * library runs on holds until the process ends (located when a context is
+ * created on that device).  A rotation whose scratch,
+ * ckks_workspace_bytes(ctx, CKKS_OP_ROTATE, {limbs, 1}), exceeds 128 MiB fails
+ * with CKKS_ENOMEM before any launch (at N = 2^16: up to 256 rows of N words,
+ * e.g. 24 + 8 limbs with dnum 3 at every level).  All calls on one device
+ * share the buffer, which keeps the last call's contents: calls that overlap
+ * on one device (several streams, contexts or threads) race, so the caller
+ * orders them.  The library's event profiler does not record this call. */
+ckks_status ckks_rotate_noalloc(ckks_ctx *ctx, const ckks_buf *in, int32_t steps, const uint64_t *dev_key,
+                                ckks_buf *out);
 
 /* ---- key-switching stages (exposed for per-stage checks) ----------------- */
 

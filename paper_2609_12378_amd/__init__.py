@@ -77,6 +77,7 @@ _SIGS = {
     "ckks_rescale": (ctypes.c_int, [_VP, _BP, _BP]),
     "ckks_rotate": (ctypes.c_int, [_VP, _BP, _I32, _VP, _BP]),
     "ckks_rotate_hoisted": (ctypes.c_int, [_VP, _BP, _VP, _U32, _VP, _BP]),
+    "ckks_rotate_noalloc": (ctypes.c_int, [_VP, _BP, _I32, _VP, _BP]),
     "ckks_modup": (ctypes.c_int, [_VP, _VP, _U32, _VP]),
     "ckks_moddown": (ctypes.c_int, [_VP, _VP, _U32, _VP]),
     "ckks_automorph": (ctypes.c_int, [_VP, _VP, _U32, _U32, _VP]),
@@ -374,6 +375,14 @@ class Context:
         out = Buf(self.zeros(2, ct.n_limbs), ct.scale)
         ci, co = ct.c(self.n), out.c(self.n)
         _check(self.lib.ckks_rotate(self.h, ctypes.byref(ci), steps, self._key(key), ctypes.byref(co)), "ckks_rotate")
+        return out
+
+    def rotate_noalloc(self, ct: Buf, steps: int, key: torch.Tensor, out: Buf) -> Buf:
+        """ckks_rotate without any device allocation by the library (static scratch); out is the caller's."""
+        ci, co = ct.c(self.n), out.c(self.n)
+        _check(self.lib.ckks_rotate_noalloc(self.h, ctypes.byref(ci), steps, self._key(key), ctypes.byref(co)),
+               "ckks_rotate_noalloc")
+        out.scale = co.scale
         return out
 
     def rotate_hoisted(self, ct: Buf, steps: Sequence[int], keys: Sequence[torch.Tensor],

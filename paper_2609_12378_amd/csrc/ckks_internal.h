@@ -118,6 +118,8 @@ struct ckks_ctx {
 
 // scratch of at least `bytes` bytes (256-byte aligned), growing the arena
 ckks_status ctx_scratch(ckks_ctx *ctx, size_t bytes, void **out);
+// once per device, with that device current: locate the allocation-free calls' static scratch on it
+void noalloc_setup(int device);
 // workspace bytes of one call of a ckks_op (SIZE_MAX: unknown op or invalid shape)
 size_t op_workspace_bytes(const ckks_ctx *ctx, int op, const uint32_t *shape);
 

@@ -306,6 +306,19 @@ ckks_status ctx_conv(ckks_ctx *c, int level, int digit, const ConvDev **out)
     return CKKS_OK;
 }
 
+// Every level's basis-conversion tables (ModUp of each digit, ModDown), built when the context is created so that
+// no later call allocates them on first use.
+static ckks_status build_all_conv(ckks_ctx *c)
+{
+    if (!c->n_p) return CKKS_OK;
+    const ConvDev *cd;
+    for (uint32_t level = 0; level < c->n_q; level++) {
+        CK_TRY(ctx_conv(c, (int)level, -1, &cd));
+        for (uint32_t j = 0; j < n_digits(c, level); j++) CK_TRY(ctx_conv(c, (int)level, (int)j, &cd));
+    }
+    return CKKS_OK;
+}
+
 ckks_status ctx_scratch(ckks_ctx *c, size_t bytes, void **out)
 {
     if (bytes == SIZE_MAX) return set_error(CKKS_EINVAL, "workspace size of an invalid shape");
@@ -422,6 +435,8 @@ ckks_status ckks_ctx_create(const ckks_params *p, void *stream, ckks_ctx **out)
         if (e != hipSuccess) st = set_error(CKKS_EHIP, "hipGetDevice: %s", hipGetErrorString(e));
     }
     if (st == CKKS_OK) st = build_tables(c);
+    if (st == CKKS_OK) st = build_all_conv(c);
+    if (st == CKKS_OK) noalloc_setup(c->device);
     if (st != CKKS_OK) {
         ckks_ctx_destroy(c);
         return st;
@@ -514,14 +529,6 @@ ckks_status ckks_set_workspace(ckks_ctx *c, void *dev, size_t bytes)
                "set_workspace: dev and bytes must be both set or both zero");
     CK_REQUIRE(((uintptr_t)dev & 255) == 0, CKKS_EINVAL, "set_workspace: dev must be 256-byte aligned");
     HIP_TRY(hipStreamSynchronize(c->stream));
-    if (dev && c->n_p) {
-        // build every level's basis-conversion tables now, so no later call allocates them on first use
-        const ConvDev *cd;
-        for (uint32_t level = 0; level < c->n_q; level++) {
-            CK_TRY(ctx_conv(c, (int)level, -1, &cd));
-            for (uint32_t j = 0; j < n_digits(c, level); j++) CK_TRY(ctx_conv(c, (int)level, (int)j, &cd));
-        }
-    }
     if (c->scratch && !c->scratch_external) HIP_TRY(hipFree(c->scratch));
     c->scratch = dev;
     c->scratch_bytes = bytes;
