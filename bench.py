@@ -604,28 +604,60 @@ def cpu_baseline(np, cfg, budget_s=20.0):
     key = ck.keygen_galois(s, ck.galois_elt(T), uniform_residues(gk, ck.primes, n, lead=(cfg.dnum,)),
                            gaussian_error(gk, (cfg.dnum, n)))
     qd = float(ck.q[level])
-    t0 = time.time()
-    n_pts, acc = 0, None
-    while time.time() - t0 < budget_s * 0.6 or n_pts < 2:
-        z = Ckks.diag_slot_vector(W, T, D, 0, 0, n1, 0, n_pts % n1)
-        term = ck.ct_mul_plain(ct, ck.encode(z, None, qd, level + 1))
-        acc = term if acc is None else ck.ct_add(acc, term)
-        n_pts += 1
-    t_pt = (time.time() - t0) / n_pts
-    t1 = time.time()
-    ck.rotate(ct, T, key)
-    t_rot = time.time() - t1
-    t2 = time.time()
-    ck.rescale(acc)
-    t_rs = time.time() - t2
     n_in, n_out = cfg.d_in // D, cfg.d_out // D
     n2 = -(-D // n1)
-    total = (n_out * n_in * D) * t_pt + (n_in * (n1 - 1) + n_out * (n2 - 1)) * t_rot + n_out * t_rs
-    cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
-    return {"value": total, "unit": "s/projection (extrapolated)", "cores": cores, "kind": "oracle",
+
+    def sample(budget, min_pts):
+        t0 = time.time()
+        n_pts, acc = 0, None
+        while time.time() - t0 < budget or n_pts < min_pts:
+            z = Ckks.diag_slot_vector(W, T, D, 0, 0, n1, 0, n_pts % n1)
+            term = ck.ct_mul_plain(ct, ck.encode(z, None, qd, level + 1))
+            acc = term if acc is None else ck.ct_add(acc, term)
+            n_pts += 1
+        t_pt = (time.time() - t0) / n_pts
+        t1 = time.time()
+        ck.rotate(ct, T, key)
+        t_rot = time.time() - t1
+        t2 = time.time()
+        ck.rescale(acc)
+        t_rs = time.time() - t2
+        total = (n_out * n_in * D) * t_pt + (n_in * (n1 - 1) + n_out * (n2 - 1)) * t_rot + n_out * t_rs
+        return total, n_pts, t_pt, t_rot, t_rs
+
+    L = oracle_lib()
+    threads = L.or_threads()
+    total, n_pts, t_pt, t_rot, t_rs = sample(budget_s * 0.5, 2)
+    # the same sample on one thread (the oracle's loops run over limb rows, so this is its serial rate)
+    L.or_set_threads(1)
+    try:
+        total1, n1_pts, t_pt1, t_rot1, _ = sample(budget_s * 0.15, 2)
+    finally:
+        L.or_set_threads(threads)
+    return {"value": total, "unit": "s/projection (extrapolated)", "cores": threads, "kind": "oracle",
+            "cpu_model": cpu_model(), "host_threads": os.cpu_count(),
+            "single_thread": {"value": total1, "unit": "s/projection (extrapolated)",
+                              "sample": "%d plaintexts (%.3f s each), 1 rotation (%.2f s)" % (n1_pts, t_pt1, t_rot1)},
             "sample": "%d weight plaintexts encoded+multiplied+accumulated (%.3f s each), 1 rotation (%.2f s), "
-                      "1 rescale (%.2f s) at N=2^16 level 12; scaled by 229376 plaintexts, 888 rotations, "
-                      "56 rescales" % (n_pts, t_pt, t_rot, t_rs)}
+                      "1 rescale (%.2f s) at N=2^16 level 12, %d threads; scaled by 229376 plaintexts, 888 rotations, "
+                      "56 rescales" % (n_pts, t_pt, t_rot, t_rs, threads)}
+
+
+def oracle_lib():
+    from oracle.ckks import lib
+    return lib()
+
+
+def cpu_model():
+    """The host CPU's model name (/proc/cpuinfo, as lscpu reports it)."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
 
 
 def cpu_oracle_secondary(np):
@@ -733,20 +765,26 @@ def main():
         outs = ctx.linear_project(st["cts"], st["Wd"], st["T"], st["n1"], st["keys"], outs)
         torch.cuda.synchronize()
         log("warmup", w, "done")
-    ctx.profile(True)
-    ctx.profile_reset()
+    # the timed steps run with the library's event profiler off; one more step with it on gives the per-kernel
+    # figures and the roofline of the dominant kernel
     with Timer(torch) as t:
         for _ in range(args.steps):
             outs = ctx.linear_project(st["cts"], st["Wd"], st["T"], st["n1"], st["keys"], outs)
-    prof = ctx.profile_all()
-    ctx.profile(False)
     ms = t.ms / args.steps
     log("projection: %.1f ms/step" % ms)
+    ctx.profile(True)
+    ctx.profile_reset()
+    with Timer(torch) as tp:
+        outs = ctx.linear_project(st["cts"], st["Wd"], st["T"], st["n1"], st["keys"], outs)
+    prof = ctx.profile_all()
+    ctx.profile(False)
+    log("profiled step: %.1f ms" % tp.ms)
     err = check_projection(np, st, outs)
     log("decrypted outputs 0/27/55: max |err| vs X@W = %.3g" % err)
     roof = roofline(prof)
     roof["traffic"] = load_traffic(roof["kernel"])
-    kernels_ms = {k: round(v[0] / args.steps, 3) for k, v in sorted(prof.items(), key=lambda kv: -kv[1][0])}
+    roof["profiled_step_ms"] = tp.ms
+    kernels_ms = {k: round(v[0], 3) for k, v in sorted(prof.items(), key=lambda kv: -kv[1][0])}
     del st, outs, ctx
     torch.cuda.empty_cache()
     secondary = {}
@@ -773,6 +811,7 @@ def main():
             log("oracle samples: NTT and key switching")
             for k, v in cpu_oracle_secondary(np).items():
                 v["cores"] = cpu["cores"]
+                v["cpu_model"] = cpu["cpu_model"]
                 secondary[k]["cpu_oracle"] = v
     line = {
         "metric": METRIC,

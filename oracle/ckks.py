@@ -61,6 +61,10 @@ def lib():
         L.or_encode_round.argtypes = [f64p, ctypes.c_void_p, i64, f64, i64p]
         L.or_encode_def_round.argtypes = [f64p, ctypes.c_void_p, i64, f64, i64p, f64p]
         L.or_encode_unrounded.argtypes = [f64p, ctypes.c_void_p, i64, f64, f64p]
+        L.or_threads.argtypes = []
+        L.or_threads.restype = ctypes.c_int
+        L.or_set_threads.argtypes = [ctypes.c_int]
+        L.or_set_threads.restype = None
         for name in ("or_ntt", "or_intt", "or_ntt_rows", "or_mul", "or_add", "or_sub", "or_mul_scalar",
                      "or_reduce_i64", "or_conv", "or_encode_round", "or_encode_def_round",
                      "or_encode_unrounded"):

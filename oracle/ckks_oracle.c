@@ -19,6 +19,7 @@
  */
 #define _GNU_SOURCE /* sincos */
 #include <math.h>
+#include <omp.h>
 #include <stddef.h>
 #include <stdint.h>
 #include <stdlib.h>
@@ -49,6 +50,11 @@ static uint64_t powm(uint64_t b, uint64_t e, uint64_t q)
     }
     return r;
 }
+/* The threads the parallel loops below use, and a way to change them: the benchmark times the oracle with all
+ * host threads and with one. */
+int or_threads(void) { return omp_get_max_threads(); }
+void or_set_threads(int n) { omp_set_num_threads(n > 0 ? n : 1); }
+
 /* q is prime, so a^(q-2) is the inverse (Fermat). */
 static uint64_t invm(uint64_t a, uint64_t q) { return powm(a, q - 2, q); }
 
