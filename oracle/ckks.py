@@ -61,6 +61,10 @@ def lib():
         L.or_encode_round.argtypes = [f64p, ctypes.c_void_p, i64, f64, i64p]
         L.or_encode_def_round.argtypes = [f64p, ctypes.c_void_p, i64, f64, i64p, f64p]
         L.or_encode_unrounded.argtypes = [f64p, ctypes.c_void_p, i64, f64, f64p]
+        L.or_philox4x64_10.argtypes = [u64p, u64p, u64p]
+        L.or_philox4x64_10.restype = None
+        L.or_expand_key_a.argtypes = [u64p, i64, u64p, i64, i64, u64p]
+        L.or_expand_key_a.restype = None
         L.or_threads.argtypes = []
         L.or_threads.restype = ctypes.c_int
         L.or_set_threads.argtypes = [ctypes.c_int]
@@ -381,6 +385,31 @@ class Ckks:
         """Switching key from sigma_g(s) to s."""
         idx = list(range(self.n_q + self.n_p))
         return self._keygen(s, self.automorph(self.secret_ntt(s, idx), g), a, e)
+
+    # ---------------- seed-expanded keys ----------------
+    @staticmethod
+    def philox(ctr: Sequence[int], key: Sequence[int]) -> List[int]:
+        """One Philox-4x64-10 block (Salmon et al., SC 2011) of counter ctr (4 words) under key (2 words)."""
+        out = np.empty(4, dtype=np.uint64)
+        lib().or_philox4x64_10(_u64(ctr), _u64(key), out)
+        return [int(x) for x in out]
+
+    def expand_key_a(self, seed: Sequence[int]) -> np.ndarray:
+        """The uniform half [dnum][n_q+n_p][N] (NTT domain) that the 128-bit seed stands for: residue n of prime k in
+        digit j is the first w >> (64 - b) below q over the words j mod 4 of the blocks Philox-4x64-10((n, k, j/4, t),
+        seed), t = 0, 1, ... (b = bit length of q; after 64 rejections w mod q)."""
+        out = np.empty((self.dnum, len(self.primes), self.n), dtype=np.uint64)
+        lib().or_expand_key_a(_u64(seed), self.dnum, _u64(self.primes), len(self.primes), self.n, out.reshape(-1))
+        return out
+
+    def keygen_galois_seeded(self, s, g: int, seed: Sequence[int], e: np.ndarray) -> np.ndarray:
+        """The b half [dnum][n_q+n_p][N] of the Galois key for g whose a half is expand_key_a(seed)."""
+        return np.ascontiguousarray(self.keygen_galois(s, g, self.expand_key_a(seed), e)[:, 0])
+
+    def seeded_key(self, b: np.ndarray, seed: Sequence[int]) -> np.ndarray:
+        """The full key (b_j, a_j) a seeded key (b half, seed) stands for: the oracle's seeded mode is the plain key
+        switching with this key."""
+        return np.ascontiguousarray(np.stack([b, self.expand_key_a(seed)], axis=1))
 
     def keygen_relin(self, s, a: np.ndarray, e: np.ndarray) -> np.ndarray:
         """Switching key from s^2 to s."""

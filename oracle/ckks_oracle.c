@@ -370,3 +370,67 @@ void or_encode_def_round(const double *zr, const double *zi, int64_t n, double d
     }
     free(x);
 }
+
+/* ------------------------------------------------------------------------ */
+/* Seed-expanded switching keys.                                            */
+/* A key's uniform half a_j need not be stored: it is a deterministic       */
+/* function of a 128-bit seed.  The generator is Philox-4x64-10 (Salmon,   */
+/* Moraes, Dror and Shaw, "Parallel random numbers: as easy as 1, 2, 3",    */
+/* SC 2011): ten rounds of two 64x64 -> 128-bit products with the constants */
+/* M0, M1, the key bumped by the Weyl constants W0, W1 between rounds.      */
+/* ------------------------------------------------------------------------ */
+void or_philox4x64_10(const uint64_t ctr[4], const uint64_t key[2], uint64_t out[4])
+{
+    const uint64_t M0 = 0xD2E7470EE14C6C93ull, M1 = 0xCA5A826395121157ull;
+    const uint64_t W0 = 0x9E3779B97F4A7C15ull, W1 = 0xBB67AE8584CAA73Bull;
+    uint64_t x0 = ctr[0], x1 = ctr[1], x2 = ctr[2], x3 = ctr[3], k0 = key[0], k1 = key[1];
+    for (int r = 0; r < 10; r++) {
+        if (r > 0) {
+            k0 += W0;
+            k1 += W1;
+        }
+        const u128 p0 = (u128)M0 * x0, p1 = (u128)M1 * x2;
+        const uint64_t y0 = (uint64_t)(p1 >> 64) ^ x1 ^ k0, y1 = (uint64_t)p1;
+        const uint64_t y2 = (uint64_t)(p0 >> 64) ^ x3 ^ k1, y3 = (uint64_t)p0;
+        x0 = y0;
+        x1 = y1;
+        x2 = y2;
+        x3 = y3;
+    }
+    out[0] = x0;
+    out[1] = x1;
+    out[2] = x2;
+    out[3] = x3;
+}
+
+/* The uniform half of a seed-expanded key: out[j][k][n] for digit j < dnum, prime index k < n_primes (modulus
+ * qs[k]) and NTT-domain position n < N.  With b the bit length of q: attempt t = 0, 1, ... draws the block
+ * Philox-4x64-10(counter (n, k, j / 4, t), key seed) and takes its word j mod 4, w; the residue is w >> (64 - b)
+ * if that is below q (rejection sampling: uniform on [0, q)), else the next attempt; after 64 rejections (each
+ * has probability 1 - q/2^b < 1/2) the residue is w mod q. */
+void or_expand_key_a(const uint64_t seed[2], int64_t dnum, const uint64_t *qs, int64_t n_primes, int64_t n,
+                     uint64_t *out)
+{
+#pragma omp parallel for collapse(2)
+    for (int64_t j = 0; j < dnum; j++)
+        for (int64_t k = 0; k < n_primes; k++) {
+            const uint64_t q = qs[k];
+            int b = 0;
+            while (b < 64 && (q >> b) != 0) b++;
+            for (int64_t i = 0; i < n; i++) {
+                uint64_t blk[4], v = 0;
+                for (uint64_t t = 0; t < 64; t++) {
+                    const uint64_t ctr[4] = {(uint64_t)i, (uint64_t)k, (uint64_t)(j / 4), t};
+                    or_philox4x64_10(ctr, seed, blk);
+                    const uint64_t w = blk[j % 4];
+                    const uint64_t x = w >> (64 - b);
+                    if (x < q) {
+                        v = x;
+                        break;
+                    }
+                    if (t == 63) v = w % q;
+                }
+                out[(j * n_primes + k) * n + i] = v;
+            }
+        }
+}
