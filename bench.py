@@ -425,7 +425,8 @@ def load_traffic(kernel):
     return None
 
 
-def bench_keyswitch(torch, np, steps, warmup):
+def bench_keyswitch(torch, np, steps, warmup, seeded=False):
+    """The hoisted batch; with `seeded`, seed-expanded keys (b halves in HBM, the a halves generated in the kernels)."""
     from workloads import KEYSWITCH as cfg, gaussian_error, rng, ternary_secret, uniform_residues, uniform_slots
     ctx = make_context(cfg)
     n, L = ctx.n, cfg.level + 1
@@ -437,25 +438,36 @@ def bench_keyswitch(torch, np, steps, warmup):
                      torch.from_numpy(gaussian_error(ge, n)).cuda())
     rsteps = list(range(1, cfg.batch + 1))
     gk = rng(cfg.index, 5)
-    keys = []
+    keys, seeds = [], []
     for r in rsteps:
-        a = torch.from_numpy(uniform_residues(gk, ctx.primes, n, lead=(cfg.dnum,))).cuda()
-        e = torch.from_numpy(gaussian_error(gk, (cfg.dnum, n))).cuda()
-        keys.append(ctx.keygen_galois(s, ctx.galois_elt(r), a, e))
-    outs = ctx.rotate_hoisted(ct, rsteps, keys)
+        if seeded:
+            seeds.append([int(x) for x in gk.integers(0, 1 << 63, 2)])
+            e = torch.from_numpy(gaussian_error(gk, (cfg.dnum, n))).cuda()
+            keys.append(ctx.keygen_galois_seeded(s, ctx.galois_elt(r), seeds[-1], e))
+        else:
+            a = torch.from_numpy(uniform_residues(gk, ctx.primes, n, lead=(cfg.dnum,))).cuda()
+            e = torch.from_numpy(gaussian_error(gk, (cfg.dnum, n))).cuda()
+            keys.append(ctx.keygen_galois(s, ctx.galois_elt(r), a, e))
+
+    def batch(outs=None):
+        if seeded:
+            return ctx.rotate_hoisted_seeded(ct, rsteps, keys, seeds, outs)
+        return ctx.rotate_hoisted(ct, rsteps, keys, outs)
+
+    outs = batch()
     for _ in range(warmup):
-        ctx.rotate_hoisted(ct, rsteps, keys, outs)
+        batch(outs)
     # each batch bracketed by its own events, the library's profiler off: the median over the runs; then the same
     # number of batches again with the profiler on (two events around every launch) for the per-kernel figures
     runs = []
     for _ in range(steps):
         with Timer(torch) as t:
-            ctx.rotate_hoisted(ct, rsteps, keys, outs)
+            batch(outs)
         runs.append(t.ms)
     ctx.profile(True)
     ctx.profile_reset()
     for _ in range(steps):
-        ctx.rotate_hoisted(ct, rsteps, keys, outs)
+        batch(outs)
     torch.cuda.synchronize()
     prof = ctx.profile_all()
     ctx.profile(False)
@@ -469,10 +481,13 @@ def bench_keyswitch(torch, np, steps, warmup):
     # summed time: how close the kernels run to the rate HBM sustains.
     word = 8.0 * n
     nd = cfg.dnum
-    abytes = (cfg.batch * nd * 2 * (L + cfg.n_p) + cfg.batch * 2 * L + 2 * L + 2 * nd * (L + cfg.n_p)) * word
+    # keys: both halves, or the b half of a seeded key
+    khalves = 1 if seeded else 2
+    abytes = (cfg.batch * nd * khalves * (L + cfg.n_p) + cfg.batch * 2 * L + 2 * L + 2 * nd * (L + cfg.n_p)) * word
     kbytes = sum(v[2] for v in prof.values()) / steps
     kms = sum(v[0] for v in prof.values()) / steps
-    res = {"workload": "32 hoisted rotations by 1..32 of one level-23 ciphertext, N=2^16, L=24+K=8, dnum=3",
+    res = {"workload": "32 hoisted rotations by 1..32 of one level-23 ciphertext, N=2^16, L=24+K=8, dnum=3"
+                       + (", seed-expanded keys" if seeded else ""),
            "ms_per_batch": ms, "rotations_per_s": cfg.batch / (ms * 1e-3), "decrypt_err_last": err,
            "runs": steps, "warmup": warmup, "ms_min": min(runs), "ms_max": max(runs),
            "roofline": {"bound": "hbm", "algorithmic_bytes_per_batch": abytes,
@@ -711,7 +726,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-secondary", action="store_true")
-    ap.add_argument("--only", choices=["keyswitch", "ntt", "tile", "shapes", "tm", "attention"], default=None,
+    ap.add_argument("--only", choices=["keyswitch", "keyswitch_seeded", "ntt", "tile", "shapes", "tm", "attention"],
+                    default=None,
                     help="run only this secondary workload (for profiling); prints its JSON")
     ap.add_argument("--lazy-moddown", type=int, default=1, choices=[0, 1],
                     help="1 (default): sums of rotations with one ModDown per output (the library's lazy mode); "
@@ -731,6 +747,9 @@ def main():
     torch.cuda.set_device(0)
     if args.only == "keyswitch":
         print(json.dumps(bench_keyswitch(torch, np, args.steps, args.warmup)), flush=True)
+        return
+    if args.only == "keyswitch_seeded":
+        print(json.dumps(bench_keyswitch(torch, np, args.steps, args.warmup, seeded=True)), flush=True)
         return
     if args.only == "ntt":
         print(json.dumps(bench_ntt(torch, args.steps)), flush=True)
@@ -791,6 +810,9 @@ def main():
     if not args.no_secondary:
         log("keyswitch batch")
         secondary["keyswitch"] = bench_keyswitch(torch, np, max(args.steps, 10), 3)
+        torch.cuda.empty_cache()
+        log("keyswitch batch, seed-expanded keys")
+        secondary["keyswitch_seeded"] = bench_keyswitch(torch, np, max(args.steps, 10), 3, seeded=True)
         torch.cuda.empty_cache()
         log("ntt microbench")
         secondary["ntt"] = bench_ntt(torch, max(args.steps, 10))

@@ -140,7 +140,7 @@ typedef enum {
     CKKS_OP_DECODE = 2,         /* shape[0] = limbs of the plaintext */
     CKKS_OP_ENCRYPT = 3,        /* shape[0] = limbs */
     CKKS_OP_DECRYPT = 4,        /* shape[0] = limbs */
-    CKKS_OP_KEYGEN = 5,         /* Galois and relinearisation keys; shape unused */
+    CKKS_OP_KEYGEN = 5,         /* Galois, relinearisation and seeded keys; shape unused */
     CKKS_OP_RESCALE = 6,        /* shape[0] = limbs of the input */
     CKKS_OP_ROTATE = 7,         /* shape[0] = limbs, shape[1] = rotations of one hoisted call (1: ckks_rotate) */
     CKKS_OP_MUL_RELIN = 8,      /* shape[0] = limbs */
@@ -199,6 +199,33 @@ ckks_status ckks_keygen_galois(ckks_ctx *ctx, const int8_t *dev_s, uint32_t galo
                                const int32_t *dev_e, uint64_t *dev_key);
 ckks_status ckks_keygen_relin(ckks_ctx *ctx, const int8_t *dev_s, const uint64_t *dev_a, const int32_t *dev_e,
                               uint64_t *dev_key);
+
+/* Seed-expanded switching keys.  The uniform half a_j of a key need not be
+ * stored: a seeded key is its b half [dnum][n_q + n_p][N] plus a 128-bit seed
+ * (two uint64 words, host memory) from which a is regenerated where it is
+ * needed, which halves the key bytes a key switch streams from HBM (the key
+ * format of the paper's Background, "The CKKS Computation Model", KeySwitch,
+ * with a compressed a half).  Residue n (NTT-domain position) of prime index k
+ * (q_0..q_{n_q-1}, then p_0..) in digit j: over the attempts t = 0, 1, ..., the
+ * word j mod 4 of the Philox-4x64-10 block (Salmon, Moraes, Dror and Shaw, SC
+ * 2011) of counter (n, k, j / 4, t) under the key `seed`, w, gives the
+ * candidate w >> (64 - b), b the bit length of the modulus; the first candidate
+ * below the modulus is the residue, and after 64 rejections it is w mod the
+ * modulus.
+ *
+ * ckks_expand_key_a writes that a half, [dnum][n_q + n_p][N], to dev_a.
+ * ckks_keygen_galois_seeded writes the b half of the Galois key for galois_elt
+ * whose a half is the seed's (b_j as in ckks_keygen_galois) to dev_key_b,
+ * [dnum][n_q + n_p][N]; scratch as CKKS_OP_KEYGEN.
+ * ckks_rotate_hoisted_seeded is ckks_rotate_hoisted with seeded keys:
+ * dev_key_b[r] is the b half and seeds[2r], seeds[2r + 1] (host) the seed of
+ * rotation r's key; the results equal ckks_rotate_hoisted's with the keys
+ * (b, ckks_expand_key_a(seed)) bit for bit.  Errors as for the unseeded calls. */
+ckks_status ckks_expand_key_a(ckks_ctx *ctx, const uint64_t *seed, uint64_t *dev_a);
+ckks_status ckks_keygen_galois_seeded(ckks_ctx *ctx, const int8_t *dev_s, uint32_t galois_elt, const uint64_t *seed,
+                                      const int32_t *dev_e, uint64_t *dev_key_b);
+ckks_status ckks_rotate_hoisted_seeded(ckks_ctx *ctx, const ckks_buf *in, const int32_t *steps, uint32_t count,
+                                       const uint64_t *const *dev_key_b, const uint64_t *seeds, ckks_buf *outs);
 
 /* ---- homomorphic operations ---------------------------------------------- */
 

@@ -78,6 +78,9 @@ _SIGS = {
     "ckks_rotate": (ctypes.c_int, [_VP, _BP, _I32, _VP, _BP]),
     "ckks_rotate_hoisted": (ctypes.c_int, [_VP, _BP, _VP, _U32, _VP, _BP]),
     "ckks_rotate_noalloc": (ctypes.c_int, [_VP, _BP, _I32, _VP, _BP]),
+    "ckks_expand_key_a": (ctypes.c_int, [_VP, _VP, _VP]),
+    "ckks_keygen_galois_seeded": (ctypes.c_int, [_VP, _VP, _U32, _VP, _VP, _VP]),
+    "ckks_rotate_hoisted_seeded": (ctypes.c_int, [_VP, _BP, _VP, _U32, _VP, _VP, _BP]),
     "ckks_modup": (ctypes.c_int, [_VP, _VP, _U32, _VP]),
     "ckks_moddown": (ctypes.c_int, [_VP, _VP, _U32, _VP]),
     "ckks_automorph": (ctypes.c_int, [_VP, _VP, _U32, _U32, _VP]),
@@ -328,6 +331,56 @@ class Context:
         ps, pa, pe, pk = self._keygen_args(s, a, e, out)
         _check(self.lib.ckks_keygen_galois(self.h, ps, g, pa, pe, pk), "ckks_keygen_galois")
         return out
+
+    # ---------------- seed-expanded keys ----------------
+    def key_b_shape(self):
+        return (self.dnum, self.n_q + self.n_p, self.n)
+
+    @staticmethod
+    def _seed(seed):
+        if len(seed) != 2:
+            raise CkksError("a key seed is two 64-bit words")
+        return (ctypes.c_uint64 * 2)(*[int(x) & ((1 << 64) - 1) for x in seed])
+
+    def expand_key_a(self, seed, out=None) -> torch.Tensor:
+        """The a half [dnum][n_q+n_p][N] a seed stands for."""
+        out = torch.empty(self.key_b_shape(), dtype=torch.uint64, device="cuda") if out is None else out
+        po = _arg(out, "expanded a", torch.uint64, shape=self.key_b_shape())
+        _check(self.lib.ckks_expand_key_a(self.h, self._seed(seed), po), "ckks_expand_key_a")
+        return out
+
+    def keygen_galois_seeded(self, s, g: int, seed, e, out=None) -> torch.Tensor:
+        """The b half [dnum][n_q+n_p][N] of the Galois key for g whose a half is expand_key_a(seed)."""
+        out = torch.empty(self.key_b_shape(), dtype=torch.uint64, device="cuda") if out is None else out
+        ps = _arg(s, "secret", torch.int8, numel=self.n)
+        pe = _arg(e, "key error", torch.int32, numel=self.dnum * self.n)
+        pk = _arg(out, "key b half", torch.uint64, shape=self.key_b_shape())
+        _check(self.lib.ckks_keygen_galois_seeded(self.h, ps, g, self._seed(seed), pe, pk), "ckks_keygen_galois_seeded")
+        return out
+
+    def rotate_hoisted_seeded(self, ct: Buf, steps: Sequence[int], keys_b: Sequence[torch.Tensor], seeds,
+                              outs: Optional[Sequence[Buf]] = None) -> List[Buf]:
+        """rotate_hoisted with seeded keys: keys_b[r] the b half, seeds[r] the seed of rotation r's key."""
+        cnt = len(steps)
+        if len(keys_b) != cnt or len(seeds) != cnt:
+            raise CkksError("rotate_hoisted_seeded: %d steps, %d keys, %d seeds" % (cnt, len(keys_b), len(seeds)))
+        if outs is not None and len(outs) < cnt:
+            raise CkksError("rotate_hoisted_seeded: %d outputs for %d steps" % (len(outs), cnt))
+        kp = (ctypes.c_void_p * max(1, cnt))(*[_arg(k, "key b half", torch.uint64, shape=self.key_b_shape()).value
+                                               for k in keys_b])
+        sd = (ctypes.c_uint64 * max(2, 2 * cnt))(*[int(w) & ((1 << 64) - 1) for sd_ in seeds for w in sd_])
+        if any(len(sd_) != 2 for sd_ in seeds):
+            raise CkksError("a key seed is two 64-bit words")
+        if outs is None:
+            outs = [Buf(self.zeros(2, ct.n_limbs), ct.scale) for _ in range(cnt)]
+        st = (ctypes.c_int32 * max(1, cnt))(*steps)
+        ob = (_Buf * max(1, cnt))(*[o.c(self.n) for o in outs])
+        ci = ct.c(self.n)
+        _check(self.lib.ckks_rotate_hoisted_seeded(self.h, ctypes.byref(ci), st, cnt, kp, sd, ob),
+               "ckks_rotate_hoisted_seeded")
+        for o, b in zip(outs, ob):
+            o.scale = b.scale
+        return list(outs[:cnt])
 
     def keygen_relin(self, s, a, e, out=None) -> torch.Tensor:
         out = torch.empty(self.key_shape(), dtype=torch.uint64, device="cuda") if out is None else out

@@ -41,7 +41,7 @@ size_t op_workspace_bytes(const ckks_ctx *ctx, int op, const uint32_t *shape)
     case CKKS_OP_DECRYPT:
         if (a < 1 || a > ctx->n_q) return SIZE_MAX;
         return words(ctx, a) * 8;
-    case CKKS_OP_KEYGEN: return words(ctx, 3 * (size_t)ctx->n_primes()) * 8;
+    case CKKS_OP_KEYGEN: return words(ctx, (3 + (size_t)ctx->dnum) * ctx->n_primes()) * 8;
     case CKKS_OP_RESCALE:
         if (a < 2 || a > ctx->n_q) return SIZE_MAX;
         return words(ctx, 2 + 2 * (size_t)(a - 1)) * 8;
@@ -78,7 +78,8 @@ size_t op_workspace_bytes(const ckks_ctx *ctx, int op, const uint32_t *shape)
 // rotations of one ciphertext sharing a single ModUp (used by the API and the projection),
 // processed in batches of ks_rot_batch(count).  work: ks_scratch_words(level, ks_rot_batch(count)) words
 ckks_status rotate_core(ckks_ctx *ctx, const uint64_t *c, uint32_t level, const int32_t *steps,
-                        const uint64_t *const *keys, uint32_t count, uint64_t *const *outs, uint64_t *work)
+                        const uint64_t *const *keys, uint32_t count, uint64_t *const *outs, uint64_t *work,
+                        const uint64_t *seeds)
 {
     if (!count) return CKKS_OK;
     const uint32_t L = level + 1, ext = L + ctx->n_p, nd = n_digits(ctx, level);
@@ -93,7 +94,7 @@ ckks_status rotate_core(ckks_ctx *ctx, const uint64_t *c, uint32_t level, const 
     for (uint32_t r0 = 0; r0 < count; r0 += bs) {
         const uint32_t cnt = count - r0 < bs ? count - r0 : bs;
         CK_TRY(ks_rotate_batch(ctx, level, cnt, c0s.data() + r0, digs.data() + r0, g.data() + r0, keys + r0,
-                               outs + r0, rw));
+                               outs + r0, rw, seeds ? seeds + 2 * (size_t)r0 : nullptr));
     }
     return CKKS_OK;
 }
@@ -310,16 +311,17 @@ ckks_status ckks_decrypt(ckks_ctx *ctx, const int8_t *s, const ckks_buf *ct, ckk
     return CKKS_OK;
 }
 
+// key: [dnum][2][R][N] (b and a), or with b_only the b halves [dnum][R][N] of a seed-expanded key
 static ckks_status keygen_common(ckks_ctx *ctx, const int8_t *s, uint32_t g, bool relin, const uint64_t *a,
-                                 const int32_t *e, uint64_t *key)
+                                 const int32_t *e, uint64_t *key, bool b_only = false, uint64_t *w_given = nullptr)
 {
     CK_REQUIRE(ctx && s && a && e && key, CKKS_EINVAL, "keygen: null argument");
     CK_REQUIRE(ctx->n_p > 0, CKKS_EUNSUPPORTED, "keygen: the context has no special primes");
     CK_REQUIRE(relin || (g & 1u), CKKS_EINVAL, "keygen: Galois element %u is even", g);
     const uint32_t R = ctx->n_primes();
     const size_t rows = R;
-    void *w;
-    CK_TRY(ctx_scratch(ctx, op_workspace_bytes(ctx, CKKS_OP_KEYGEN, nullptr), &w));
+    void *w = w_given;
+    if (!w) CK_TRY(ctx_scratch(ctx, op_workspace_bytes(ctx, CKKS_OP_KEYGEN, nullptr), &w));
     uint64_t *sn = (uint64_t *)w, *t = sn + words(ctx, rows), *en = t + words(ctx, rows);
     const LimbMap all = limb_range(0, R);
     CK_TRY(launch_expand_i8(ctx, sn, s, all));
@@ -329,12 +331,12 @@ static ckks_status keygen_common(ckks_ctx *ctx, const int8_t *s, uint32_t g, boo
     for (uint32_t j = 0; j < ctx->dnum; j++) {
         CK_TRY(launch_expand_i32(ctx, en, e + (size_t)j * ctx->n, all));
         CK_TRY(launch_ntt(ctx, en, R, all, false));
-        uint64_t *kb = key + (size_t)j * 2 * words(ctx, rows);
+        uint64_t *kb = key + (size_t)j * (b_only ? 1 : 2) * words(ctx, rows);
         const uint32_t lo = digit_lo(ctx, j);
         uint32_t hi = lo + ctx->alpha;
         if (hi > ctx->n_q) hi = ctx->n_q;
-        CK_TRY(launch_keygen_digit(ctx, kb, kb + words(ctx, rows), a + (size_t)j * words(ctx, rows), sn, en, t,
-                                   lo, hi));
+        CK_TRY(launch_keygen_digit(ctx, kb, b_only ? nullptr : kb + words(ctx, rows), a + (size_t)j * words(ctx, rows),
+                                   sn, en, t, lo, hi));
     }
     return CKKS_OK;
 }
@@ -352,6 +354,27 @@ ckks_status ckks_keygen_relin(ckks_ctx *ctx, const int8_t *s, const uint64_t *a,
 {
     clear_error();
     return keygen_common(ctx, s, 1, true, a, e, key);
+}
+
+ckks_status ckks_expand_key_a(ckks_ctx *ctx, const uint64_t *seed, uint64_t *a)
+{
+    clear_error();
+    CK_REQUIRE(ctx && seed && a, CKKS_EINVAL, "expand_key_a: null argument");
+    return launch_expand_key_a(ctx, seed[0], seed[1], a);
+}
+
+ckks_status ckks_keygen_galois_seeded(ckks_ctx *ctx, const int8_t *s, uint32_t g, const uint64_t *seed,
+                                      const int32_t *e, uint64_t *key_b)
+{
+    clear_error();
+    CK_REQUIRE(ctx && seed, CKKS_EINVAL, "keygen (seeded): null argument");
+    CK_REQUIRE(g < 2 * ctx->n, CKKS_EINVAL, "keygen: Galois element %u >= 2N", g);
+    // scratch: the key generation's own rows, then the expanded a half
+    void *w;
+    CK_TRY(ctx_scratch(ctx, op_workspace_bytes(ctx, CKKS_OP_KEYGEN, nullptr), &w));
+    uint64_t *a = (uint64_t *)w + words(ctx, 3 * (size_t)ctx->n_primes());
+    CK_TRY(launch_expand_key_a(ctx, seed[0], seed[1], a));
+    return keygen_common(ctx, s, g, false, a, e, key_b, true, (uint64_t *)w);
 }
 
 ckks_status ckks_add(ckks_ctx *ctx, const ckks_buf *a, const ckks_buf *b, ckks_buf *out)
@@ -399,10 +422,9 @@ ckks_status ckks_rescale(ckks_ctx *ctx, const ckks_buf *in, ckks_buf *out)
     return CKKS_OK;
 }
 
-ckks_status ckks_rotate_hoisted(ckks_ctx *ctx, const ckks_buf *in, const int32_t *steps, uint32_t count,
-                                const uint64_t *const *keys, ckks_buf *outs)
+static ckks_status rotate_hoisted_api(ckks_ctx *ctx, const ckks_buf *in, const int32_t *steps, uint32_t count,
+                                      const uint64_t *const *keys, const uint64_t *seeds, ckks_buf *outs)
 {
-    clear_error();
     CK_REQUIRE(ctx, CKKS_EINVAL, "rotate: null context");
     CK_TRY(check_buf(ctx, in, 2, "rotate (in)"));
     if (count == 0) return CKKS_OK;
@@ -420,9 +442,24 @@ ckks_status ckks_rotate_hoisted(ckks_ctx *ctx, const ckks_buf *in, const int32_t
     void *w;
     const uint32_t shp[2] = {in->n_limbs, count};
     CK_TRY(ctx_scratch(ctx, op_workspace_bytes(ctx, CKKS_OP_ROTATE, shp), &w));
-    CK_TRY(rotate_core(ctx, in->data, level, steps, keys, count, op.data(), (uint64_t *)w));
+    CK_TRY(rotate_core(ctx, in->data, level, steps, keys, count, op.data(), (uint64_t *)w, seeds));
     for (uint32_t r = 0; r < count; r++) outs[r].scale = in->scale;
     return CKKS_OK;
+}
+
+ckks_status ckks_rotate_hoisted(ckks_ctx *ctx, const ckks_buf *in, const int32_t *steps, uint32_t count,
+                                const uint64_t *const *keys, ckks_buf *outs)
+{
+    clear_error();
+    return rotate_hoisted_api(ctx, in, steps, count, keys, nullptr, outs);
+}
+
+ckks_status ckks_rotate_hoisted_seeded(ckks_ctx *ctx, const ckks_buf *in, const int32_t *steps, uint32_t count,
+                                       const uint64_t *const *key_b, const uint64_t *seeds, ckks_buf *outs)
+{
+    clear_error();
+    CK_REQUIRE(count == 0 || seeds, CKKS_EINVAL, "rotate (seeded): null seeds");
+    return rotate_hoisted_api(ctx, in, steps, count, key_b, seeds, outs);
 }
 
 ckks_status ckks_rotate(ckks_ctx *ctx, const ckks_buf *in, int32_t steps, const uint64_t *key, ckks_buf *out)

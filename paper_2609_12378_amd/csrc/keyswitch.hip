@@ -20,6 +20,7 @@
 #include "ckks_internal.h"
 #include "ntt_core.h"
 #include "ops.h"
+#include "philox.h"
 
 namespace {
 
@@ -324,10 +325,42 @@ struct RotArgs {
     uint64_t *out[kRotBatch];
     const uint64_t *dig[kRotBatch];  // ModUp digits [nd][ext][N] of the rotated ciphertext
     const uint64_t *c0[kRotBatch];   // its c0 [level+1][N]
+    // seed-expanded keys (the SEEDED kernels): key[r] is the b half [nd][key_rows][N] and seed[r] the seed of a
+    uint64_t seed[kRotBatch][2];
+};
+
+// Where rotation r's key words for digit j, key row `krow`, position `pos` come from: b (and, stored, a) from the
+// key; a seed-expanded key computes a (q = the row's modulus) from its seed, four digits per Philox block.
+template <bool SEEDED>
+struct KeyRow {
+    const uint64_t *key;
+    size_t kstride;      // words between the b and a halves (stored keys)
+    uint32_t key_rows, log_n, prime, pos, shift;
+    uint64_t q, s0, s1;
+    uint64_t blk[4];
+    __device__ KeyRow(const RotArgs &ra, uint32_t r, uint32_t key_rows_, uint32_t log_n_, uint32_t prime_,
+                      uint32_t pos_, uint64_t q_)
+        : key(ra.key[r]), kstride((size_t)key_rows_ << log_n_), key_rows(key_rows_), log_n(log_n_), prime(prime_),
+          pos(pos_), shift(seedk::shift_of(q_)), q(q_), s0(ra.seed[r][0]), s1(ra.seed[r][1])
+    {
+    }
+    __device__ uint64_t b(uint32_t j) const
+    {
+        const size_t row = SEEDED ? (size_t)j * key_rows + prime : (size_t)j * 2 * key_rows + prime;
+        return nttc::ld_stream(key + (row << log_n) + pos);
+    }
+    __device__ uint64_t a(uint32_t j)
+    {
+        if (!SEEDED) return nttc::ld_stream(key + (((size_t)j * 2 * key_rows + prime) << log_n) + kstride + pos);
+        const uint32_t m = j & 3;
+        if (m == 0) seedk::block_residues(s0, s1, pos, prime, j >> 2, q, shift, blk);
+        return m == 0 ? blk[0] : m == 1 ? blk[1] : m == 2 ? blk[2] : blk[3];
+    }
 };
 
 // u[r][k][row - row0][n] = sum_j d_j[row][sigma_{g_r}(n)] * key_r[j][k][krow][n] for rows row0 .. row0 + rows - 1
 // of Q_level u P (u holds `rows` rows per polynomial)
+template <bool SEEDED>
 __global__ __launch_bounds__(kThreads) void k_key_ip_batch(RotArgs ra, uint64_t *u, uint32_t nd, uint32_t ext,
                                                             uint32_t level,
                                                             uint32_t n_q, uint32_t key_rows, uint32_t row0,
@@ -341,14 +374,13 @@ __global__ __launch_bounds__(kThreads) void k_key_ip_batch(RotArgs ra, uint64_t 
     const uint32_t prime = row <= level ? row : n_q + (row - level - 1);
     const ModQ m = mods[prime];
     const uint32_t sc = auto_index(col, ra.g[r], log_n);
-    const uint64_t *key = ra.key[r];
+    KeyRow<SEEDED> kr(ra, r, key_rows, log_n, prime, col, m.q);
     const uint64_t *digits = ra.dig[r];
     acc128 a0{0, 0}, a1{0, 0};
     for (uint32_t j = 0; j < nd; j++) {
         const uint64_t d = digits[(((size_t)j * ext + row) << log_n) + sc];
-        const size_t kb = ((size_t)j * 2 * key_rows + prime) << log_n;
-        mac(a0, d, nttc::ld_stream(key + kb + col));
-        mac(a1, d, nttc::ld_stream(key + kb + ((size_t)key_rows << log_n) + col));
+        mac(a0, d, kr.b(j));
+        mac(a1, d, kr.a(j));
     }
     uint64_t *ur = u + (((size_t)r * 2 * rows + (row - row0)) << log_n) + col;
     ur[0] = reduce128(a0, m);
@@ -404,6 +436,7 @@ __global__ __launch_bounds__(kThreads) void k_key_ip_acc(RotArgs ra, uint32_t nd
 // of k_ks_finish8's inner product), reduced below q/2 + 1, then the row's Gentleman-Sande stages with its inverse
 // twiddles; written as raw doubles below 2q to up[r][k][i], the inter-pass form the inverse column pass reads.
 // The P rows of u thus never go to HBM in canonical form to be read back by a separate row pass.
+template <bool SEEDED>
 __global__ __launch_bounds__(64) void k_key_ip_intt8(RotArgs ra, uint64_t *up, uint32_t nd, uint32_t ext,
                                                      uint32_t L, uint32_t K, uint32_t n_q, uint32_t key_rows,
                                                      const ModQ *__restrict__ mods, const double *__restrict__ itwf,
@@ -421,20 +454,19 @@ __global__ __launch_bounds__(64) void k_key_ip_intt8(RotArgs ra, uint64_t *up, u
     const uint32_t h = blk * 2 + sub;
     nttc::stage_twiddles8(tws[sub], itwf + ((size_t)prime << log_n), (1u << (log_n - 8)) + h, t, 32);
     const uint32_t g = ra.g[r];
-    const uint64_t *key = ra.key[r];
     const uint64_t *digits = ra.dig[r];
-    const size_t kstride = (size_t)key_rows << log_n;
+    const uint64_t qk = mods[prime].q;
     double u[2][kE8];
 #pragma unroll
     for (int e = 0; e < kE8; e++) {
         const uint32_t pos = h * 256 + nttc::u8<0>(t, e);
         const uint32_t sc = auto_index(pos, g, log_n);
+        KeyRow<SEEDED> kr(ra, r, key_rows, log_n, prime, pos, qk);
         double u0 = 0.0, u1 = 0.0;
         for (uint32_t j = 0; j < nd; j++) {
             const double d = nttc::Ar<true>::from_u64(digits[(((size_t)j * ext + row) << log_n) + sc]);
-            const uint64_t *kj = key + (((size_t)j * 2 * key_rows + prime) << log_n) + pos;
-            u0 += ar.mul(d, nttc::Ar<true>::from_u64(nttc::ld_stream(kj)));
-            u1 += ar.mul(d, nttc::Ar<true>::from_u64(nttc::ld_stream(kj + kstride)));
+            u0 += ar.mul(d, nttc::Ar<true>::from_u64(kr.b(j)));
+            u1 += ar.mul(d, nttc::Ar<true>::from_u64(kr.a(j)));
             if ((j & 3) == 3) {
                 u0 = ar.red(u0);
                 u1 = ar.red(u1);
@@ -464,6 +496,7 @@ __global__ __launch_bounds__(64) void k_key_ip_intt8(RotArgs ra, uint64_t *up, u
 // so neither the q-limb rows of u nor the transformed conversion ever go to HBM.  Magnitudes (units of q):
 // transform outputs <= 2.5 (row pass after a reducing first pass), each product <= 0.875 and the sum range-reduced
 // every 4 digits (<= 4), differences <= 6.5, P^-1 products <= 3, plus c0 < 1: all below 8 q = 2^53.
+template <bool SEEDED>
 __global__ __launch_bounds__(64) void k_ks_finish8(RotArgs ra, const uint64_t *__restrict__ cw, uint32_t nd,
                                                    uint32_t ext,
                                                    uint32_t L, uint32_t key_rows, const ModQ *__restrict__ mods,
@@ -496,21 +529,20 @@ __global__ __launch_bounds__(64) void k_ks_finish8(RotArgs ra, const uint64_t *_
         for (int e = 0; e < kE8; e++) v[k][e] = x[e];
     }
     const uint32_t g = ra.g[r];
-    const uint64_t *key = ra.key[r];
     uint64_t *out = ra.out[r];
     const uint64_t *digits = ra.dig[r], *c0 = ra.c0[r];
     const double pi = (double)pinv[i].x;
-    const size_t kstride = (size_t)key_rows << log_n;
+    const uint64_t qi = mods[i].q;
 #pragma unroll
     for (int e = 0; e < kE8; e++) {
         const uint32_t pos = h * 256 + nttc::u8<0>(t, e);
         const uint32_t sc = auto_index(pos, g, log_n);
+        KeyRow<SEEDED> kr(ra, r, key_rows, log_n, i, pos, qi);
         double u0 = 0.0, u1 = 0.0;
         for (uint32_t j = 0; j < nd; j++) {
             const double d = nttc::Ar<true>::from_u64(digits[(((size_t)j * ext + i) << log_n) + sc]);
-            const uint64_t *kj = key + (((size_t)j * 2 * key_rows + i) << log_n) + pos;
-            u0 += ar.mul(d, nttc::Ar<true>::from_u64(nttc::ld_stream(kj)));
-            u1 += ar.mul(d, nttc::Ar<true>::from_u64(nttc::ld_stream(kj + kstride)));
+            u0 += ar.mul(d, nttc::Ar<true>::from_u64(kr.b(j)));
+            u1 += ar.mul(d, nttc::Ar<true>::from_u64(kr.a(j)));
             if ((j & 3) == 3) {
                 u0 = ar.red(u0);
                 u1 = ar.red(u1);
@@ -627,7 +659,35 @@ ckks_status launch_conv_col8(ckks_ctx *ctx, const ConvDev *cd, const uint64_t *i
     return CKKS_OK;
 }
 
+// The a half [dnum][R][N] of a seed-expanded key: thread (prime k, position n) draws the Philox blocks of every
+// group of four digits (philox.h).
+__global__ __launch_bounds__(256) void k_expand_key_a(uint64_t *a, uint64_t s0, uint64_t s1, uint32_t dnum,
+                                                      uint32_t R, const ModQ *__restrict__ mods, uint32_t log_n)
+{
+    const uint32_t col = blockIdx.x * 256 + threadIdx.x, k = blockIdx.y;
+    if (col >= (1u << log_n)) return;
+    const uint64_t q = mods[k].q;
+    const uint32_t shift = seedk::shift_of(q);
+    uint64_t blk[4];
+    for (uint32_t j = 0; j < dnum; j++) {
+        const uint32_t m = j & 3;
+        if (m == 0) seedk::block_residues(s0, s1, col, k, j >> 2, q, shift, blk);
+        a[(((size_t)j * R + k) << log_n) + col] = m == 0 ? blk[0] : m == 1 ? blk[1] : m == 2 ? blk[2] : blk[3];
+    }
+}
+
 }  // namespace
+
+ckks_status launch_expand_key_a(ckks_ctx *ctx, uint64_t s0, uint64_t s1, uint64_t *a)
+{
+    const uint32_t R = ctx->n_primes();
+    const dim3 grid((ctx->n + 255) / 256, R), block(256);
+    prof_begin(ctx, K_ELEM, 8.0 * ctx->dnum * R * ctx->n);
+    hipLaunchKernelGGL(k_expand_key_a, grid, block, 0, ctx->stream, a, s0, s1, ctx->dnum, R, ctx->d_mod, ctx->log_n);
+    prof_end(ctx, K_ELEM);
+    HIP_TRY(hipGetLastError());
+    return CKKS_OK;
+}
 
 uint32_t ks_rot_batch(uint32_t count) { return count < (uint32_t)kRotBatch ? count : (uint32_t)kRotBatch; }
 
@@ -644,11 +704,12 @@ size_t ks_scratch_words(const ckks_ctx *ctx, uint32_t level, uint32_t batch, uin
 
 ckks_status ks_rotate_batch(ckks_ctx *ctx, uint32_t level, uint32_t count, const uint64_t *const *c0s,
                             const uint64_t *const *digs, const uint32_t *g, const uint64_t *const *keys,
-                            uint64_t *const *outs, uint64_t *work)
+                            uint64_t *const *outs, uint64_t *work, const uint64_t *seeds)
 {
     CK_REQUIRE(count >= 1 && count <= (uint32_t)kRotBatch, CKKS_EINVAL, "rotation batch of %u", count);
     const uint32_t L = level + 1, K = ctx->n_p, ext = L + K, nd = n_digits(ctx, level);
     const size_t N = ctx->n;
+    const bool seeded = seeds != nullptr;
     RotArgs ra{};
     ra.count = count;
     for (uint32_t r = 0; r < count; r++) {
@@ -657,7 +718,13 @@ ckks_status ks_rotate_batch(ckks_ctx *ctx, uint32_t level, uint32_t count, const
         ra.out[r] = outs[r];
         ra.dig[r] = digs[r];
         ra.c0[r] = c0s[r];
+        if (seeded) {
+            ra.seed[r][0] = seeds[2 * r];
+            ra.seed[r][1] = seeds[2 * r + 1];
+        }
     }
+    // a seeded key holds its b half only: key_rows rows per digit instead of 2 key_rows
+    const uint32_t kp = ctx->n_primes();
     int s1, s2;
     ntt_split(ctx->log_n, &s1, &s2);
     if (s2 == 8 && ntt_uses_f64(ctx, L)) {
@@ -672,16 +739,24 @@ ckks_status ks_rotate_batch(ckks_ctx *ctx, uint32_t level, uint32_t count, const
             const double res = (double)count * 2 * K * N;
             prof_begin(ctx, K_KEYIP, 8.0 * res * (nd + 1.0) + 8.0 * (double)nd * K * N,
                        res * (nd * 10.0 + 4 * kOpsButterflyF64 + 8.0));
-            hipLaunchKernelGGL(k_key_ip_intt8, dim3(count * K * bpl), dim3(64), 0, ctx->stream, ra, up, nd, ext, L,
-                               K, ctx->n_q, ctx->n_primes(), ctx->d_mod, ctx->d_itwf, ctx->log_n, bpl);
+            if (seeded)
+                hipLaunchKernelGGL(k_key_ip_intt8<true>, dim3(count * K * bpl), dim3(64), 0, ctx->stream, ra, up, nd,
+                                   ext, L, K, ctx->n_q, kp, ctx->d_mod, ctx->d_itwf, ctx->log_n, bpl);
+            else
+                hipLaunchKernelGGL(k_key_ip_intt8<false>, dim3(count * K * bpl), dim3(64), 0, ctx->stream, ra, up, nd,
+                                   ext, L, K, ctx->n_q, kp, ctx->d_mod, ctx->d_itwf, ctx->log_n, bpl);
             prof_end(ctx, K_KEYIP);
             HIP_TRY(hipGetLastError());
             CK_TRY(launch_ntt_inv_second_pass(ctx, up, 2 * count, K, limb_range(ctx->n_q, K)));
         } else {
             const dim3 grid((ctx->n + kThreads - 1) / kThreads, K, count), block(kThreads);
             prof_begin(ctx, K_KEYIP, 8.0 * ctx->n * K * (count * (2.0 * nd + 2.0) + nd));
-            hipLaunchKernelGGL(k_key_ip_batch, grid, block, 0, ctx->stream, ra, up, nd, ext, level, ctx->n_q,
-                               ctx->n_primes(), L, K, ctx->d_mod, ctx->log_n);
+            if (seeded)
+                hipLaunchKernelGGL(k_key_ip_batch<true>, grid, block, 0, ctx->stream, ra, up, nd, ext, level,
+                                   ctx->n_q, kp, L, K, ctx->d_mod, ctx->log_n);
+            else
+                hipLaunchKernelGGL(k_key_ip_batch<false>, grid, block, 0, ctx->stream, ra, up, nd, ext, level,
+                                   ctx->n_q, kp, L, K, ctx->d_mod, ctx->log_n);
             prof_end(ctx, K_KEYIP);
             HIP_TRY(hipGetLastError());
             CK_TRY(launch_ntt_strided(ctx, up, 2 * count, K, limb_range(ctx->n_q, K), true));
@@ -700,8 +775,12 @@ ckks_status ks_rotate_batch(ckks_ctx *ctx, uint32_t level, uint32_t count, const
         const double res = (double)count * L * N;
         prof_begin(ctx, K_MODDOWN, 8.0 * res * (2.0 + 2.0 * nd + 2.0),
                    res * (2 * (4 * kOpsButterflyF64 + 4 * (kOpsButterflyF64 - 3)) / 2 + nd * 2 * 10.0 + 40.0));
-        hipLaunchKernelGGL(k_ks_finish8, dim3(count * L * bpl), dim3(64), 0, ctx->stream, ra, cw, nd, ext, L,
-                           ctx->n_primes(), ctx->d_mod, ctx->d_twf, ctx->d_pinv, ctx->log_n, bpl);
+        if (seeded)
+            hipLaunchKernelGGL(k_ks_finish8<true>, dim3(count * L * bpl), dim3(64), 0, ctx->stream, ra, cw, nd, ext,
+                               L, kp, ctx->d_mod, ctx->d_twf, ctx->d_pinv, ctx->log_n, bpl);
+        else
+            hipLaunchKernelGGL(k_ks_finish8<false>, dim3(count * L * bpl), dim3(64), 0, ctx->stream, ra, cw, nd, ext,
+                               L, kp, ctx->d_mod, ctx->d_twf, ctx->d_pinv, ctx->log_n, bpl);
         prof_end(ctx, K_MODDOWN);
         HIP_TRY(hipGetLastError());
         return CKKS_OK;
@@ -711,8 +790,12 @@ ckks_status ks_rotate_batch(ckks_ctx *ctx, uint32_t level, uint32_t count, const
     {
         const dim3 grid((ctx->n + kThreads - 1) / kThreads, ext, count), block(kThreads);
         prof_begin(ctx, K_KEYIP, 8.0 * ctx->n * ext * (count * (2.0 * nd + 2.0) + nd));
-        hipLaunchKernelGGL(k_key_ip_batch, grid, block, 0, ctx->stream, ra, u, nd, ext, level, ctx->n_q,
-                           ctx->n_primes(), 0u, ext, ctx->d_mod, ctx->log_n);
+        if (seeded)
+            hipLaunchKernelGGL(k_key_ip_batch<true>, grid, block, 0, ctx->stream, ra, u, nd, ext, level, ctx->n_q,
+                               kp, 0u, ext, ctx->d_mod, ctx->log_n);
+        else
+            hipLaunchKernelGGL(k_key_ip_batch<false>, grid, block, 0, ctx->stream, ra, u, nd, ext, level, ctx->n_q,
+                               kp, 0u, ext, ctx->d_mod, ctx->log_n);
         prof_end(ctx, K_KEYIP);
         HIP_TRY(hipGetLastError());
     }

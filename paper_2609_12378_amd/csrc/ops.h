@@ -48,13 +48,16 @@ ckks_status ks_moddown(ckks_ctx *ctx, uint64_t *u, uint32_t polys, uint32_t leve
 size_t ks_scratch_words(const ckks_ctx *ctx, uint32_t level, uint32_t batch, uint32_t n_ct = 1);
 // rotations per batched launch for `count` requested rotations
 uint32_t ks_rot_batch(uint32_t count);
+// the a half [dnum][n_q + n_p][N] of the seed-expanded key with seed (s0, s1) (philox.h)
+ckks_status launch_expand_key_a(ckks_ctx *ctx, uint64_t s0, uint64_t s1, uint64_t *a);
 // `count` (<= 32) rotations: rotation r applies the automorphism g[r] with key keys[r] to the ciphertext whose
 // c0 is c0s[r] and whose ModUp digits are digs[r] (hoisted rotations of one ciphertext share both): key inner
 // product, ModDown and the sigma_{g_r}(c0) addition, each stage one launch for all r.
-// work: count * (2 ext + 2 (level+1)) N words
+// work: count * (2 ext + 2 (level+1)) N words.  seeds (nullable, [count][2]): seed-expanded keys, keys[r] then holds
+// the b half [dnum][n_q + n_p][N] and the a half comes from seeds[2r], seeds[2r + 1] (philox.h)
 ckks_status ks_rotate_batch(ckks_ctx *ctx, uint32_t level, uint32_t count, const uint64_t *const *c0s,
                             const uint64_t *const *digs, const uint32_t *g, const uint64_t *const *keys,
-                            uint64_t *const *outs, uint64_t *work);
+                            uint64_t *const *outs, uint64_t *work, const uint64_t *seeds = nullptr);
 
 // lazy ModDown: accs[r] (or accs[0] for all r when sum_all; [2][level+1+K][N]) (+)= the key inner product of
 // rotation r over Q_level u P plus P * sigma_{g_r}(c0_r) on the q rows; count <= 32.  ks_moddown of the accumulator
@@ -110,7 +113,8 @@ ckks_status launch_to_f64(ckks_ctx *ctx, uint64_t *v, size_t words);
 // ciphertext-level steps shared by the API calls and the projections (api_ops.hip)
 // rotations of one ciphertext sharing a single ModUp; work: ks_scratch_words(level, ks_rot_batch(count))
 ckks_status rotate_core(ckks_ctx *ctx, const uint64_t *c, uint32_t level, const int32_t *steps,
-                        const uint64_t *const *keys, uint32_t count, uint64_t *const *outs, uint64_t *work);
+                        const uint64_t *const *keys, uint32_t count, uint64_t *const *outs, uint64_t *work,
+                        const uint64_t *seeds = nullptr);
 // rescale of one ciphertext at level l; work: (2 + 2 l) N words
 ckks_status rescale_core(ckks_ctx *ctx, const uint64_t *c, uint32_t l, uint64_t *out, uint64_t *work);
 // `count` ciphertexts (at cs + r * stride) rotated by the same step; work: ks_scratch_words(level,

@@ -132,7 +132,7 @@ __global__ __launch_bounds__(kThreads) void k_keygen(uint64_t *b_out, uint64_t *
         r = addmod(r, shoup(t[i], P.x, P.y, md.q), md.q);
     }
     b_out[i] = r;
-    a_out[i] = a[i];
+    if (a_out) a_out[i] = a[i];
 }
 
 // Rescale, step 1: top-limb coefficients t (mod q_l) -> centred -> residues mod q_i, i < l.
