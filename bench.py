@@ -425,10 +425,26 @@ def load_traffic(kernel):
     return None
 
 
-def bench_keyswitch(torch, np, steps, warmup, seeded=False):
-    """The hoisted batch; with `seeded`, seed-expanded keys (b halves in HBM, the a halves generated in the kernels)."""
-    from workloads import KEYSWITCH as cfg, gaussian_error, rng, ternary_secret, uniform_residues, uniform_slots
-    ctx = make_context(cfg)
+def paper_context(cfg):
+    """A context with the paper's chain (q_0 of 60 bits, q_1.. of 59 bits, special primes of 60 bits), the prime
+    lists taken from the library's own generator."""
+    from paper_2609_12378_amd import Context
+    from workloads import paper_chain
+    p60 = Context(cfg.log_n, 1 + cfg.n_p, 0, 1, q_bits=60).q
+    p59 = Context(cfg.log_n, cfg.n_q - 1, 0, 1, q_bits=59).q
+    q, p = paper_chain(p60, p59, cfg.n_q, cfg.n_p)
+    ctx = Context(cfg.log_n, cfg.n_q, cfg.n_p, cfg.dnum, q=q, p=p)
+    ctx.set_lazy_moddown(LAZY["on"])
+    return ctx
+
+
+def bench_keyswitch(torch, np, steps, warmup, seeded=False, paper=False):
+    """The hoisted batch; with `seeded`, seed-expanded keys (b halves in HBM, the a halves generated in the kernels);
+    with `paper`, the paper's parameters (N = 2^16, 37 limbs of 60/59 bits + 8 of 60 bits, dnum 5, level 36)."""
+    from workloads import KEYSWITCH, KEYSWITCH_PAPER, gaussian_error, rng, ternary_secret, uniform_residues, \
+        uniform_slots
+    cfg = KEYSWITCH_PAPER if paper else KEYSWITCH
+    ctx = paper_context(cfg) if paper else make_context(cfg)
     n, L = ctx.n, cfg.level + 1
     s = torch.from_numpy(ternary_secret(rng(cfg.index, 3), n)).cuda()
     z = uniform_slots(rng(cfg.index, 1), n // 2)
@@ -486,7 +502,9 @@ def bench_keyswitch(torch, np, steps, warmup, seeded=False):
     abytes = (cfg.batch * nd * khalves * (L + cfg.n_p) + cfg.batch * 2 * L + 2 * L + 2 * nd * (L + cfg.n_p)) * word
     kbytes = sum(v[2] for v in prof.values()) / steps
     kms = sum(v[0] for v in prof.values()) / steps
-    res = {"workload": "32 hoisted rotations by 1..32 of one level-23 ciphertext, N=2^16, L=24+K=8, dnum=3"
+    res = {"workload": ("32 hoisted rotations by 1..32 of one level-36 ciphertext, N=2^16, L=37 (60/59-bit) + K=8 "
+                        "(60-bit), dnum=5 (the paper's parameters)" if paper else
+                        "32 hoisted rotations by 1..32 of one level-23 ciphertext, N=2^16, L=24+K=8, dnum=3")
                        + (", seed-expanded keys" if seeded else ""),
            "ms_per_batch": ms, "rotations_per_s": cfg.batch / (ms * 1e-3), "decrypt_err_last": err,
            "runs": steps, "warmup": warmup, "ms_min": min(runs), "ms_max": max(runs),
@@ -501,12 +519,15 @@ def bench_keyswitch(torch, np, steps, warmup, seeded=False):
     return res
 
 
-def bench_ntt(torch, steps):
+def bench_ntt(torch, steps, bits=50):
+    """The batched NTT microbenchmark; bits = 59: the same shape over 59-bit primes (the paper's size; integer
+    butterflies)."""
     import numpy as np
+    from paper_2609_12378_amd import Context
     from workloads import NTT_BENCH as cfg
-    ctx = make_context(cfg, 0, 1)
+    ctx = Context(cfg.log_n, cfg.n_q, 0, 1, q_bits=bits)
     g = torch.Generator(device="cuda").manual_seed(202)
-    x = torch.randint(0, 1 << 49, (cfg.batch, cfg.n_q, ctx.n), generator=g, device="cuda",
+    x = torch.randint(0, 1 << (bits - 1), (cfg.batch, cfg.n_q, ctx.n), generator=g, device="cuda",
                       dtype=torch.int64).view(torch.uint64)
     ctx.ntt(x)
     ctx.intt(x)
@@ -532,7 +553,7 @@ def bench_ntt(torch, steps):
     ctx.profile(False)
     fms, ims = float(np.median(fwd)), float(np.median(inv))
     algo = 16.0 * cfg.batch * cfg.n_q * ctx.n
-    res = {"workload": "64 polys x 36 limbs x 2^16, 50-bit primes", "fwd_ms": fms, "inv_ms": ims,
+    res = {"workload": "64 polys x 36 limbs x 2^16, %d-bit primes" % bits, "fwd_ms": fms, "inv_ms": ims,
            "runs": steps, "warmup": 3, "algorithmic_bytes_per_direction": algo,
            "fwd_GBps": algo / (fms * 1e-3) / 1e9, "inv_GBps": algo / (ims * 1e-3) / 1e9,
            "kernels": {k: {"avg_ms": v[0] / v[1], "GBps": v[2] / (v[0] * 1e-3) / 1e9,
@@ -726,7 +747,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-secondary", action="store_true")
-    ap.add_argument("--only", choices=["keyswitch", "keyswitch_seeded", "ntt", "tile", "shapes", "tm", "attention"],
+    ap.add_argument("--only", choices=["keyswitch", "keyswitch_seeded", "paper", "ntt", "tile", "shapes", "tm",
+                                       "attention"],
                     default=None,
                     help="run only this secondary workload (for profiling); prints its JSON")
     ap.add_argument("--lazy-moddown", type=int, default=1, choices=[0, 1],
@@ -750,6 +772,10 @@ def main():
         return
     if args.only == "keyswitch_seeded":
         print(json.dumps(bench_keyswitch(torch, np, args.steps, args.warmup, seeded=True)), flush=True)
+        return
+    if args.only == "paper":
+        print(json.dumps({"keyswitch": bench_keyswitch(torch, np, args.steps, args.warmup, paper=True),
+                          "ntt": bench_ntt(torch, args.steps, bits=59)}), flush=True)
         return
     if args.only == "ntt":
         print(json.dumps(bench_ntt(torch, args.steps)), flush=True)
@@ -816,6 +842,11 @@ def main():
         torch.cuda.empty_cache()
         log("ntt microbench")
         secondary["ntt"] = bench_ntt(torch, max(args.steps, 10))
+        torch.cuda.empty_cache()
+        log("the paper's parameters: keyswitch batch and 59-bit NTT")
+        secondary["keyswitch_paper_params"] = bench_keyswitch(torch, np, max(args.steps, 10), 3, paper=True)
+        torch.cuda.empty_cache()
+        secondary["ntt_59bit"] = bench_ntt(torch, max(args.steps, 10), bits=59)
         torch.cuda.empty_cache()
         log("other projection shapes")
         secondary["shapes"] = bench_shapes(torch, np, 1)

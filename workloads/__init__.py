@@ -212,3 +212,17 @@ def attention_inputs(cfg: Config, q: Sequence[int], primes: Sequence[int], n_q: 
 # inputs at level 5, scale 2^50, one query, key and value ciphertext.
 ATTN_HD128 = Config("attn13_hd128", 8, 13, 50, 6, 2, 3, scale_log2=50, level=5, tokens=16, head_dim=128, heads=2,
                     kv_heads=1)
+
+
+# The paper's own CKKS parameters (Evaluation, "Experimental Setup"): N = 2^16, modulus depth 37 with a 60-bit
+# first modulus and 59-bit others, dnum = 5; here with 8 special primes of 60 bits (alpha = 8).  Every prime is at
+# least 2^50, so every transform, inner product and conversion takes the integer (64-bit Shoup) path.  The
+# hoisted batch at the top level: 32 rotations by 1..32 of a level-36 ciphertext.
+KEYSWITCH_PAPER = Config("keyswitch_paper", 10, 16, 59, 37, 8, 5, scale_log2=40, level=36, batch=32,
+                         notes="q_0 60-bit, q_1..q_36 59-bit, p 60-bit")
+
+
+def paper_chain(primes60: Sequence[int], primes59: Sequence[int], n_q: int, n_p: int):
+    """(q, p) of the paper's chain from the descending 60- and 59-bit prime lists: q_0 the largest 60-bit prime,
+    q_1.. the 59-bit ones, p the next 60-bit primes."""
+    return [primes60[0]] + list(primes59[:n_q - 1]), list(primes60[1:1 + n_p])
