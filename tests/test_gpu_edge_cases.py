@@ -1,0 +1,111 @@
+"""Degenerate and boundary cases of the GPU path, against the oracle where there is a result to compare.
+
+* BSGS splits at their ends: n1 = 1 (no baby steps; D - 1 giant rotations of the partial sums) and a baby-step
+  count that does not divide the features (n1 = 24 for D = 128: the last giant step holds 8 diagonals), on the toy
+  ring, bit for bit, eager and lazy.
+* Empty calls: an NTT of zero polynomials and a hoisted rotation of zero steps do nothing and succeed.
+* An all-zero slot vector encodes to the zero plaintext; a zero weight matrix projects an encryption to a
+  ciphertext that decrypts to zero within the noise.
+"""
+import dataclasses
+
+import numpy as np
+import pytest
+
+from gpu_common import require_gpu, say, to_dev, to_host
+from oracle import Ckks
+from workloads import (TOY, fm_pack, gaussian_error, gaussian_weights, rng, ternary_secret, uniform_residues,
+                       uniform_slots)
+
+pytestmark = pytest.mark.gpu
+
+
+def toy_ctx():
+    from paper_2609_12378_amd import Context
+    ctx = Context(TOY.log_n, TOY.n_q, TOY.n_p, TOY.dnum, q_bits=TOY.q_bits)
+    return ctx, Ckks(TOY.log_n, ctx.q, ctx.p, TOY.dnum)
+
+
+def projection_case(n1, d_in, d_out, lazy, blocks, tag, zero_weights=False):
+    require_gpu()
+    ctx, ck = toy_ctx()
+    ctx.set_lazy_moddown(lazy)
+    n, T, D, level = ctx.n, TOY.tokens, TOY.feats, TOY.level
+    n2 = -(-D // n1)
+    s = ternary_secret(rng(1, 3, extra=tag), n)
+    X = uniform_slots(rng(1, 1, extra=tag), (T, d_in))
+    W = np.zeros((d_in, d_out)) if zero_weights else gaussian_weights(rng(1, 2, extra=tag), (d_in, d_out))
+    delta = float(2 ** TOY.scale_log2)
+    g = rng(1, 4, extra=tag)
+    cts_o, cts_g = [], []
+    for i in range(d_in // D):
+        x = fm_pack(X, T, D, i)
+        a, e = uniform_residues(g, ctx.q[:level + 1], n), gaussian_error(g, n)
+        cts_o.append(ck.encrypt(s, ck.encode(x, None, delta, level + 1), a, e))
+        cts_g.append(ctx.encrypt(to_dev(s), ctx.encode(to_dev(x), None, delta, level + 1), to_dev(a), to_dev(e)))
+    gk = rng(1, 5, extra=tag)
+    keys_o, keys_g = {}, {}
+    for st in [T * b for b in range(1, n1)] + [T * n1 * gg for gg in range(1, n2)]:
+        ka, ke = uniform_residues(gk, ctx.primes, n, lead=(TOY.dnum,)), gaussian_error(gk, (TOY.dnum, n))
+        gel = ck.galois_elt(st)
+        keys_o[st] = ck.keygen_galois(s, gel, ka, ke)
+        keys_g[st] = ctx.keygen_galois(to_dev(s), gel, to_dev(ka), to_dev(ke))
+    say("projection n1=%d (n2=%d), %d keys, lazy=%s" % (n1, n2, len(keys_g), lazy))
+    outs = ctx.linear_project(cts_g, to_dev(W), T, n1, keys_g)
+    want = ck.linear_project(cts_o, W, T, n1, keys_o, out_blocks=blocks, lazy=lazy)
+    for j, w in zip(blocks, want):
+        got = to_host(outs[j].data)
+        bad = np.argwhere(got != w)
+        assert bad.size == 0, "output %d: first mismatches %s" % (j, bad[:5].tolist())
+    Y = X @ W
+    errs = []
+    for j in range(d_out // D):
+        re, _ = ctx.decode(ctx.decrypt(to_dev(s), outs[j]))
+        errs.append(float(np.max(np.abs(to_host(re) - fm_pack(Y, T, D, j)))))
+    return max(errs)
+
+
+@pytest.mark.parametrize("lazy", [False, True])
+def test_projection_no_baby_steps(lazy):
+    err = projection_case(1, TOY.feats, TOY.feats, lazy, [0], 40)
+    say("n1 = 1: max error vs X@W", err)
+    assert err <= 2.0 ** -12
+
+
+@pytest.mark.parametrize("lazy", [False, True])
+def test_projection_ragged_giant_step(lazy):
+    err = projection_case(24, TOY.feats, 2 * TOY.feats, lazy, [0, 1], 41)
+    say("n1 = 24 (last giant step partial): max error vs X@W", err)
+    assert err <= 2.0 ** -12
+
+
+def test_projection_zero_weights():
+    err = projection_case(16, TOY.feats, TOY.feats, False, [0], 42, zero_weights=True)
+    say("zero weights: max decrypted magnitude", err)
+    assert err <= 2.0 ** -12
+
+
+def test_empty_calls():
+    require_gpu()
+    import torch
+    ctx, ck = toy_ctx()
+    t = torch.zeros((0, TOY.n_q, ctx.n), dtype=torch.uint64, device="cuda")
+    ctx.ntt(t)
+    ctx.intt(t)
+    s = ternary_secret(rng(1, 3, extra=43), ctx.n)
+    z = uniform_slots(rng(1, 1, extra=43), ctx.n // 2)
+    g = rng(1, 4, extra=43)
+    ct = ctx.encrypt(to_dev(s), ctx.encode(to_dev(z), None, 2.0 ** 30, TOY.n_q),
+                     to_dev(uniform_residues(g, ctx.q, ctx.n)), to_dev(gaussian_error(g, ctx.n)))
+    before = to_host(ct.data).copy()
+    assert ctx.rotate_hoisted(ct, [], []) == []
+    assert np.array_equal(to_host(ct.data), before)
+
+
+def test_zero_slots_encode_to_zero():
+    require_gpu()
+    ctx, ck = toy_ctx()
+    z = np.zeros(ctx.n // 2)
+    pt = ctx.encode(to_dev(z), None, 2.0 ** 30, TOY.n_q)
+    assert not np.any(to_host(pt.data))
+    assert np.array_equal(to_host(pt.data)[0], ck.encode(z, None, 2.0 ** 30, TOY.n_q))
