@@ -67,10 +67,10 @@ class Timer:
         self.ms = self.a.elapsed_time(self.b)
 
 
-def setup_projection(torch, np, cfg):
+def setup_projection(torch, np, cfg, ctx=None):
     from workloads import (gaussian_error, gaussian_weights, rng, ternary_secret, uniform_residues,
                            uniform_slots)
-    ctx = make_context(cfg)
+    ctx = make_context(cfg) if ctx is None else ctx
     n, T, D, level, n1 = ctx.n, cfg.tokens, cfg.feats, cfg.level, cfg.n1
     n2 = -(-D // n1)
     s = torch.from_numpy(ternary_secret(rng(cfg.index, 3), n)).cuda()
@@ -89,8 +89,8 @@ def setup_projection(torch, np, cfg):
     gk = rng(cfg.index, 5)
     keys = {}
     for st in steps:
-        a = torch.from_numpy(uniform_residues(gk, ctx.primes, n, lead=(cfg.dnum,))).cuda()
-        e = torch.from_numpy(gaussian_error(gk, (cfg.dnum, n))).cuda()
+        a = torch.from_numpy(uniform_residues(gk, ctx.primes, n, lead=(ctx.dnum,))).cuda()
+        e = torch.from_numpy(gaussian_error(gk, (ctx.dnum, n))).cuda()
         keys[st] = ctx.keygen_galois(s, ctx.galois_elt(st), a, e)
     torch.cuda.synchronize()
     return dict(ctx=ctx, s=s, X=X, W=W, Wd=Wd, cts=cts, keys=keys, T=T, D=D, n1=n1, delta=delta)
@@ -124,8 +124,8 @@ def setup_projection_tm(torch, np, cfg, n1):
     gk = rng(cfg.index, 5)
     keys = {}
     for st in steps:
-        a = torch.from_numpy(uniform_residues(gk, ctx.primes, n, lead=(cfg.dnum,))).cuda()
-        e = torch.from_numpy(gaussian_error(gk, (cfg.dnum, n))).cuda()
+        a = torch.from_numpy(uniform_residues(gk, ctx.primes, n, lead=(ctx.dnum,))).cuda()
+        e = torch.from_numpy(gaussian_error(gk, (ctx.dnum, n))).cuda()
         keys[st] = ctx.keygen_galois(s, ctx.galois_elt(st), a, e)
     torch.cuda.synchronize()
     return dict(ctx=ctx, s=s, X=X, W=W, Wd=Wd, cts=cts, keys=keys, T=T, D=D, n1=n1, delta=delta)
@@ -519,6 +519,31 @@ def bench_keyswitch(torch, np, steps, warmup, seeded=False, paper=False):
     return res
 
 
+def bench_projection_paper(torch, np):
+    """The 4096x14336 projection (its shapes, level 12, n1 = 32) with the paper's modulus chain (60/59-bit q, 60-bit
+    special primes, dnum 5): every prime is at least 2^50, so the encode transforms, the multiply-accumulate (128-bit
+    integer sums) and the key switching run on the integer path.  One timed step after one warm-up."""
+    from workloads import KEYSWITCH_PAPER, PROJECTION
+    st = setup_projection(torch, np, PROJECTION, ctx=paper_context(KEYSWITCH_PAPER))
+    ctx = st["ctx"]
+    outs = ctx.linear_project(st["cts"], st["Wd"], st["T"], st["n1"], st["keys"])
+    with Timer(torch) as t:
+        outs = ctx.linear_project(st["cts"], st["Wd"], st["T"], st["n1"], st["keys"], outs)
+    ctx.profile(True)
+    ctx.profile_reset()
+    outs = ctx.linear_project(st["cts"], st["Wd"], st["T"], st["n1"], st["keys"], outs)
+    prof = ctx.profile_all()
+    ctx.profile(False)
+    err = check_projection(np, st, outs)
+    res = {"workload": "4096x14336 feature-major projection, N=2^16, level 12 of the paper's chain (q_0 60-bit, "
+                       "q_1.. 59-bit, 8 x 60-bit special primes, dnum 5), n1 = 32: the integer path",
+           "s_per_projection": t.ms / 1e3, "decrypt_max_abs_err": err,
+           "kernels_ms": {k: round(v[0], 2) for k, v in sorted(prof.items(), key=lambda kv: -kv[1][0])}}
+    del st, outs, ctx
+    torch.cuda.empty_cache()
+    return res
+
+
 def bench_ntt(torch, steps, bits=50):
     """The batched NTT microbenchmark; bits = 59: the same shape over 59-bit primes (the paper's size; integer
     butterflies)."""
@@ -775,7 +800,8 @@ def main():
         return
     if args.only == "paper":
         print(json.dumps({"keyswitch": bench_keyswitch(torch, np, args.steps, args.warmup, paper=True),
-                          "ntt": bench_ntt(torch, args.steps, bits=59)}), flush=True)
+                          "ntt": bench_ntt(torch, args.steps, bits=59),
+                          "projection": bench_projection_paper(torch, np)}), flush=True)
         return
     if args.only == "ntt":
         print(json.dumps(bench_ntt(torch, args.steps)), flush=True)
@@ -848,6 +874,8 @@ def main():
         torch.cuda.empty_cache()
         secondary["ntt_59bit"] = bench_ntt(torch, max(args.steps, 10), bits=59)
         torch.cuda.empty_cache()
+        log("the paper's parameters: 4096x14336 projection (integer path)")
+        secondary["projection_paper_params"] = bench_projection_paper(torch, np)
         log("other projection shapes")
         secondary["shapes"] = bench_shapes(torch, np, 1)
         torch.cuda.empty_cache()
