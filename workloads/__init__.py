@@ -135,10 +135,16 @@ class ProjectionInputs:
     steps: list
 
 
+def tm_pack(X: np.ndarray, tokens: int, feats: int, i: int) -> np.ndarray:
+    """Slot vector of input ciphertext i in the token-major layout: slot t*feats + f holds X[t, i*feats + f]."""
+    return X[:, i * feats:(i + 1) * feats].reshape(-1)
+
+
 def projection_inputs(cfg: Config, q: Sequence[int], primes: Sequence[int], d_in: Optional[int] = None,
-                      d_out: Optional[int] = None) -> ProjectionInputs:
-    """Seeded inputs of a feature-major projection with cfg's ring, level, tokens and n1 (d_in x d_out weights,
-    default cfg's): rotation steps T*b (0 < b < n1) then T*n1*g (0 < g < n2)."""
+                      d_out: Optional[int] = None, layout: str = "fm") -> ProjectionInputs:
+    """Seeded inputs of a projection with cfg's ring, level, tokens and n1 (d_in x d_out weights, default cfg's).
+    Rotation steps, in drawing order: feature-major ("fm") T*b (0 < b < n1) then T*n1*g (0 < g < n2); token-major
+    ("tm") b (0 < b < n1), b - D (0 <= b < n1), then n1*g (0 < g < n2)."""
     d_in = cfg.d_in if d_in is None else d_in
     d_out = cfg.d_out if d_out is None else d_out
     n, T, D, n1, level = cfg.n, cfg.tokens, cfg.feats, cfg.n1, cfg.level
@@ -151,7 +157,10 @@ def projection_inputs(cfg: Config, q: Sequence[int], primes: Sequence[int], d_in
     for _ in range(d_in // D):
         a = uniform_residues(ge, q[:level + 1], n)
         enc.append((a, gaussian_error(ge, n)))
-    steps = [T * b for b in range(1, n1)] + [T * n1 * g for g in range(1, n2)]
+    if layout == "fm":
+        steps = [T * b for b in range(1, n1)] + [T * n1 * g for g in range(1, n2)]
+    else:
+        steps = [b for b in range(1, n1)] + [b - D for b in range(n1)] + [n1 * g for g in range(1, n2)]
     gk = rng(cfg.index, ROLE_KEYS)
     keys = {}
     for st in steps:
