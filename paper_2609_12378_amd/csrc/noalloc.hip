@@ -2,6 +2,7 @@
 // capture, tight serving loops, harnesses that forbid hipMalloc).  Its scratch is a file-scope static device
 // array; each device's copy is located once, when a context is created on that device (noalloc_setup), and only
 // that address is ever handed to kernels, copies or fills.
+#include <atomic>
 #include <mutex>
 
 #include "ckks_internal.h"
@@ -15,7 +16,8 @@ static constexpr int kMaxDevices = 64;
 static __device__ __align__(256) uint64_t scratch[kScratchWords];
 
 static std::mutex g_setup_mu;
-static uint64_t *g_scratch_ptr[kMaxDevices] = {};   // the device address of `scratch` on each device
+// the device address of `scratch` on each device: written once under the lock, read by calls on any thread
+static std::atomic<uint64_t *> g_scratch_ptr[kMaxDevices] = {};
 static hipError_t g_setup_err[kMaxDevices] = {};    // why it could not be located (hipSuccess: not tried or found)
 
 // Called by ckks_ctx_create with `device` current.  A failure here leaves every other call working: only
@@ -24,7 +26,7 @@ void noalloc_setup(int device)
 {
     if (device < 0 || device >= kMaxDevices) return;
     std::lock_guard<std::mutex> lock(g_setup_mu);
-    if (g_scratch_ptr[device]) return;
+    if (g_scratch_ptr[device].load(std::memory_order_acquire)) return;
     void *p = nullptr;
     const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
     if (e != hipSuccess || !p || ((uintptr_t)p & 255)) {
@@ -32,7 +34,7 @@ void noalloc_setup(int device)
         (void)hipGetLastError();   // do not leave the failure for the next runtime call to report
         return;
     }
-    g_scratch_ptr[device] = (uint64_t *)p;
+    g_scratch_ptr[device].store((uint64_t *)p, std::memory_order_release);
 }
 
 extern "C" ckks_status ckks_rotate_noalloc(ckks_ctx *ctx, const ckks_buf *in, int32_t steps, const uint64_t *key,
@@ -49,8 +51,9 @@ extern "C" ckks_status ckks_rotate_noalloc(ckks_ctx *ctx, const ckks_buf *in, in
     CK_REQUIRE(ctx->n_p > 0, CKKS_EUNSUPPORTED, "rotate_noalloc: the context has no special primes");
     CK_REQUIRE(ctx->device >= 0 && ctx->device < kMaxDevices, CKKS_EUNSUPPORTED,
                "rotate_noalloc: device index %d outside [0, %d)", ctx->device, kMaxDevices);
-    CK_REQUIRE(g_scratch_ptr[ctx->device], CKKS_EHIP, "rotate_noalloc: static scratch not located on device %d: %s",
-               ctx->device, hipGetErrorString(g_setup_err[ctx->device]));
+    uint64_t *const scratch_ptr = g_scratch_ptr[ctx->device].load(std::memory_order_acquire);
+    CK_REQUIRE(scratch_ptr, CKKS_EHIP, "rotate_noalloc: static scratch not located on device %d: %s", ctx->device,
+               hipGetErrorString(g_setup_err[ctx->device]));
     const uint32_t level = in->n_limbs - 1, L = in->n_limbs;
     const size_t words = ks_scratch_words(ctx, level, 1);
     CK_REQUIRE(words <= kScratchWords, CKKS_ENOMEM,
@@ -65,7 +68,7 @@ extern "C" ckks_status ckks_rotate_noalloc(ckks_ctx *ctx, const ckks_buf *in, in
     // the event profiler creates runtime objects per launch: off for this call
     const bool profiling = ctx->profiling;
     ctx->profiling = false;
-    uint64_t *digits = g_scratch_ptr[ctx->device];
+    uint64_t *digits = scratch_ptr;
     uint64_t *rw = digits + ((size_t)n_digits(ctx, level) * (L + ctx->n_p) + ctx->alpha) * ctx->n;
     const uint64_t *c0 = in->data, *dig = digits;
     const uint32_t g = ckks_galois_elt(ctx, steps);
