@@ -358,6 +358,73 @@ struct KeyRow {
     }
 };
 
+// The key inner products of the 8 positions pos[e] of one thread (fp64, primes below 2^50):
+//   u0[e], u1[e] = sum_j sigma_{g_r}(d_j)[row][pos[e]] * (b_j, a_j)[prime][pos[e]],  sc[e] = sigma^-1 position,
+// each product reduced to <= 0.875 q and the sums range-reduced every 4 digits (so |u| <= 4 q).  With stored keys
+// the gathers and key words of one digit for all 8 positions are issued together (24 loads in flight), so a wave
+// waits on memory once per digit rather than once per digit and position; ND > 0 fixes the digit count at compile
+// time (fully unrolled), ND = 0 takes nd.  Sums are formed in the same order either way.
+template <bool SEEDED, int ND>
+__device__ __forceinline__ void key_ip8(const RotArgs &ra, uint32_t r, uint32_t nd, uint32_t ext, uint32_t row,
+                                        uint32_t prime, uint32_t key_rows, uint32_t log_n, uint64_t q,
+                                        const nttc::Ar<true> &ar, const uint32_t (&pos)[nttc::kE8],
+                                        const uint32_t (&sc)[nttc::kE8], double (&u0)[nttc::kE8],
+                                        double (&u1)[nttc::kE8])
+{
+    using nttc::kE8;
+    using A = nttc::Ar<true>;
+    const uint32_t ndv = ND > 0 ? (uint32_t)ND : nd;
+    constexpr int kUnroll = ND > 0 ? ND : 1;
+    const uint64_t *dig = ra.dig[r] + ((size_t)row << log_n);
+    const size_t dstride = (size_t)ext << log_n;
+#pragma unroll
+    for (int e = 0; e < kE8; e++) u0[e] = u1[e] = 0.0;
+    if constexpr (!SEEDED) {
+        const size_t kstride = (size_t)key_rows << log_n;   // from a digit's b rows to its a rows
+        const uint64_t *key = ra.key[r] + ((size_t)prime << log_n);
+#pragma unroll kUnroll
+        for (uint32_t j = 0; j < ndv; j++) {
+            const uint64_t *dj = dig + j * dstride, *kb = key + 2 * j * kstride, *ka = kb + kstride;
+            uint64_t dv[kE8], bv[kE8], av[kE8];
+#pragma unroll
+            for (int e = 0; e < kE8; e++) {
+                dv[e] = dj[sc[e]];
+                bv[e] = nttc::ld_stream(kb + pos[e]);
+                av[e] = nttc::ld_stream(ka + pos[e]);
+            }
+#pragma unroll
+            for (int e = 0; e < kE8; e++) {
+                const double d = A::from_u64(dv[e]);
+                u0[e] += ar.mul(d, A::from_u64(bv[e]));
+                u1[e] += ar.mul(d, A::from_u64(av[e]));
+            }
+            if ((j & 3) == 3) {
+#pragma unroll
+                for (int e = 0; e < kE8; e++) {
+                    u0[e] = ar.red(u0[e]);
+                    u1[e] = ar.red(u1[e]);
+                }
+            }
+        }
+    } else {
+        // a regenerated per position (one Philox block per 4 digits), so positions run one after another
+#pragma unroll
+        for (int e = 0; e < kE8; e++) {
+            KeyRow<true> kr(ra, r, key_rows, log_n, prime, pos[e], q);
+#pragma unroll kUnroll
+            for (uint32_t j = 0; j < ndv; j++) {
+                const double d = A::from_u64(dig[j * dstride + sc[e]]);
+                u0[e] += ar.mul(d, A::from_u64(kr.b(j)));
+                u1[e] += ar.mul(d, A::from_u64(kr.a(j)));
+                if ((j & 3) == 3) {
+                    u0[e] = ar.red(u0[e]);
+                    u1[e] = ar.red(u1[e]);
+                }
+            }
+        }
+    }
+}
+
 // u[r][k][row - row0][n] = sum_j d_j[row][sigma_{g_r}(n)] * key_r[j][k][krow][n] for rows row0 .. row0 + rows - 1
 // of Q_level u P (u holds `rows` rows per polynomial)
 template <bool SEEDED>
@@ -393,6 +460,7 @@ __global__ __launch_bounds__(kThreads) void k_key_ip_batch(RotArgs ra, uint64_t 
 // division unchanged).  sum_all: one accumulator ra.out[0] takes the sum over all r of the batch; else ra.out[r]
 // takes rotation r's.  Accumulators [2][ext][N], added to when `accumulate`.  The 128-bit sums hold at most
 // 32 (nd + 1) products below 2^100.
+template <int ND>
 __global__ __launch_bounds__(kThreads) void k_key_ip_acc(RotArgs ra, uint32_t nd, uint32_t ext, uint32_t level,
                                                          uint32_t n_q, uint32_t key_rows,
                                                          const ulonglong2 *__restrict__ pmodq,
@@ -408,17 +476,66 @@ __global__ __launch_bounds__(kThreads) void k_key_ip_acc(RotArgs ra, uint32_t nd
     const ModQ m = mods[prime];
     const uint64_t pq = row <= level ? pmodq[row].x : 0;
     acc128 a0{0, 0}, a1{0, 0};
-    for (uint32_t r = r0; r < r1; r++) {
-        const uint32_t sc = auto_index(col, ra.g[r], log_n);
-        const uint64_t *key = ra.key[r];
-        const uint64_t *digits = ra.dig[r];
-        for (uint32_t j = 0; j < nd; j++) {
-            const uint64_t d = digits[(((size_t)j * ext + row) << log_n) + sc];
-            const size_t kb = ((size_t)j * 2 * key_rows + prime) << log_n;
-            mac(a0, d, nttc::ld_stream(key + kb + col));
-            mac(a1, d, nttc::ld_stream(key + kb + ((size_t)key_rows << log_n) + col));
+    if constexpr (ND > 0) {
+        // every word rotation r needs (its digits' gathers, key words and c0) loaded in one go, and rotation
+        // r + 1's loads issued before rotation r's products: one memory wait per rotation, overlapped
+        struct Words {
+            uint64_t d[ND], b[ND], a[ND], c;
+        };
+        const size_t kstride = (size_t)key_rows << log_n;
+        auto load = [&](uint32_t r, Words &w) {
+            const uint32_t sc = auto_index(col, ra.g[r], log_n);
+            const uint64_t *key = ra.key[r] + ((size_t)prime << log_n) + col;
+            const uint64_t *digits = ra.dig[r] + ((size_t)row << log_n) + sc;
+#pragma unroll
+            for (int j = 0; j < ND; j++) {
+                w.d[j] = digits[(size_t)j * ext << log_n];
+                w.b[j] = nttc::ld_stream(key + 2 * j * kstride);
+                w.a[j] = nttc::ld_stream(key + (2 * j + 1) * kstride);
+            }
+            // loaded on every row (row 0 of c0 for the P rows, unused there) so that every path issues the same
+            // loads and the waits stay partial
+            w.c = ra.c0[r][((size_t)(pq ? row : 0) << log_n) + sc];
+        };
+        auto use = [&](const Words &w) {
+#pragma unroll
+            for (int j = 0; j < ND; j++) {
+                mac(a0, w.d[j], w.b[j]);
+                mac(a1, w.d[j], w.a[j]);
+            }
+            if (pq) mac(a0, w.c, pq);
+        };
+        // two register sets used in turn, with no copies between them and no loads under a condition inside the
+        // loop: either would make the compiler wait for the newer loads as well
+        Words w0, w1;
+        load(r0, w0);
+        uint32_t r = r0;
+        for (; r + 2 < r1; r += 2) {
+            load(r + 1, w1);
+            use(w0);
+            load(r + 2, w0);
+            use(w1);
         }
-        if (pq) mac(a0, ra.c0[r][((size_t)row << log_n) + sc], pq);
+        if (r + 1 < r1) {
+            load(r + 1, w1);
+            use(w0);
+            use(w1);
+        } else {
+            use(w0);
+        }
+    } else {
+        for (uint32_t r = r0; r < r1; r++) {
+            const uint32_t sc = auto_index(col, ra.g[r], log_n);
+            const uint64_t *key = ra.key[r];
+            const uint64_t *digits = ra.dig[r];
+            for (uint32_t j = 0; j < nd; j++) {
+                const uint64_t d = digits[(((size_t)j * ext + row) << log_n) + sc];
+                const size_t kb = ((size_t)j * 2 * key_rows + prime) << log_n;
+                mac(a0, d, nttc::ld_stream(key + kb + col));
+                mac(a1, d, nttc::ld_stream(key + kb + ((size_t)key_rows << log_n) + col));
+            }
+            if (pq) mac(a0, ra.c0[r][((size_t)row << log_n) + sc], pq);
+        }
     }
     uint64_t *u = ra.out[r0] + ((size_t)row << log_n) + col;
     uint64_t v0 = reduce128(a0, m), v1 = reduce128(a1, m);
@@ -436,7 +553,7 @@ __global__ __launch_bounds__(kThreads) void k_key_ip_acc(RotArgs ra, uint32_t nd
 // of k_ks_finish8's inner product), reduced below q/2 + 1, then the row's Gentleman-Sande stages with its inverse
 // twiddles; written as raw doubles below 2q to up[r][k][i], the inter-pass form the inverse column pass reads.
 // The P rows of u thus never go to HBM in canonical form to be read back by a separate row pass.
-template <bool SEEDED>
+template <bool SEEDED, int ND>
 __global__ __launch_bounds__(64) void k_key_ip_intt8(RotArgs ra, uint64_t *up, uint32_t nd, uint32_t ext,
                                                      uint32_t L, uint32_t K, uint32_t n_q, uint32_t key_rows,
                                                      const ModQ *__restrict__ mods, const double *__restrict__ itwf,
@@ -454,26 +571,18 @@ __global__ __launch_bounds__(64) void k_key_ip_intt8(RotArgs ra, uint64_t *up, u
     const uint32_t h = blk * 2 + sub;
     nttc::stage_twiddles8(tws[sub], itwf + ((size_t)prime << log_n), (1u << (log_n - 8)) + h, t, 32);
     const uint32_t g = ra.g[r];
-    const uint64_t *digits = ra.dig[r];
-    const uint64_t qk = mods[prime].q;
-    double u[2][kE8];
+    uint32_t pos[kE8], sc[kE8];
 #pragma unroll
     for (int e = 0; e < kE8; e++) {
-        const uint32_t pos = h * 256 + nttc::u8<0>(t, e);
-        const uint32_t sc = auto_index(pos, g, log_n);
-        KeyRow<SEEDED> kr(ra, r, key_rows, log_n, prime, pos, qk);
-        double u0 = 0.0, u1 = 0.0;
-        for (uint32_t j = 0; j < nd; j++) {
-            const double d = nttc::Ar<true>::from_u64(digits[(((size_t)j * ext + row) << log_n) + sc]);
-            u0 += ar.mul(d, nttc::Ar<true>::from_u64(kr.b(j)));
-            u1 += ar.mul(d, nttc::Ar<true>::from_u64(kr.a(j)));
-            if ((j & 3) == 3) {
-                u0 = ar.red(u0);
-                u1 = ar.red(u1);
-            }
-        }
-        u[0][e] = ar.red(u0);
-        u[1][e] = ar.red(u1);
+        pos[e] = h * 256 + nttc::u8<0>(t, e);
+        sc[e] = auto_index(pos[e], g, log_n);
+    }
+    double u[2][kE8];
+    key_ip8<SEEDED, ND>(ra, r, nd, ext, row, prime, key_rows, log_n, mods[prime].q, ar, pos, sc, u[0], u[1]);
+#pragma unroll
+    for (int e = 0; e < kE8; e++) {
+        u[0][e] = ar.red(u[0][e]);
+        u[1][e] = ar.red(u[1][e]);
     }
     __syncthreads();
 #pragma unroll
@@ -496,7 +605,6 @@ __global__ __launch_bounds__(64) void k_key_ip_intt8(RotArgs ra, uint64_t *up, u
 // so neither the q-limb rows of u nor the transformed conversion ever go to HBM.  Magnitudes (units of q):
 // transform outputs <= 2.5 (row pass after a reducing first pass), each product <= 0.875 and the sum range-reduced
 // every 4 digits (<= 4), differences <= 6.5, P^-1 products <= 3, plus c0 < 1: all below 8 q = 2^53.
-template <bool SEEDED>
 __global__ __launch_bounds__(64) void k_ks_finish8(RotArgs ra, const uint64_t *__restrict__ cw, uint32_t nd,
                                                    uint32_t ext,
                                                    uint32_t L, uint32_t key_rows, const ModQ *__restrict__ mods,
@@ -537,7 +645,7 @@ __global__ __launch_bounds__(64) void k_ks_finish8(RotArgs ra, const uint64_t *_
     for (int e = 0; e < kE8; e++) {
         const uint32_t pos = h * 256 + nttc::u8<0>(t, e);
         const uint32_t sc = auto_index(pos, g, log_n);
-        KeyRow<SEEDED> kr(ra, r, key_rows, log_n, i, pos, qi);
+        KeyRow<false> kr(ra, r, key_rows, log_n, i, pos, qi);
         double u0 = 0.0, u1 = 0.0;
         for (uint32_t j = 0; j < nd; j++) {
             const double d = nttc::Ar<true>::from_u64(digits[(((size_t)j * ext + i) << log_n) + sc]);
@@ -552,6 +660,65 @@ __global__ __launch_bounds__(64) void k_ks_finish8(RotArgs ra, const uint64_t *_
         const double r1 = ar.mul(u1 - v[1][e], pi);
         nttc::st_stream(out + ((size_t)i << log_n) + pos, ar.to_canon(r0));
         nttc::st_stream(out + (((size_t)L + i) << log_n) + pos, ar.to_canon(r1));
+    }
+}
+
+// k_ks_finish8 for seed-expanded keys: the inner products (with their Philox blocks) first, every position's
+// loads issued before the transforms, and c0's gathers at the start.  (With stored keys the same order, 160 VGPRs
+// and 3 waves per SIMD, measured 5% slower than k_ks_finish8's one position at a time after the transforms, 88
+// VGPRs and 5 waves: that kernel streams ~5 TB/s of keys, converted rows and outputs.)
+template <int ND>
+__global__ __launch_bounds__(64) void k_ks_finish8_seeded(RotArgs ra, const uint64_t *__restrict__ cw, uint32_t nd,
+                                                          uint32_t ext, uint32_t L, uint32_t key_rows,
+                                                          const ModQ *__restrict__ mods,
+                                                          const double *__restrict__ twf,
+                                                          const ulonglong2 *__restrict__ pinv, uint32_t log_n,
+                                                          uint32_t blocks_per_limb)
+{
+    using nttc::kE8;
+    __shared__ double tws[2][257];
+    __shared__ double tr[2][nttc::kTr8];
+    const uint32_t per_rot = L * blocks_per_limb;
+    const uint32_t r = blockIdx.x / per_rot, rem = blockIdx.x % per_rot;
+    const uint32_t i = rem / blocks_per_limb, blk = rem % blocks_per_limb;
+    const nttc::Ar<true> ar(mods[i]);
+    const uint32_t sub = threadIdx.x >> 5, t = threadIdx.x & 31;
+    const uint32_t h = blk * 2 + sub;
+    nttc::stage_twiddles8(tws[sub], twf + ((size_t)i << log_n), (1u << (log_n - 8)) + h, t, 32);
+    const uint32_t g = ra.g[r];
+    const uint64_t *c0 = ra.c0[r] + ((size_t)i << log_n);
+    uint32_t pos[kE8], sc[kE8];
+    uint64_t c0v[kE8];
+#pragma unroll
+    for (int e = 0; e < kE8; e++) {
+        pos[e] = h * 256 + nttc::u8<0>(t, e);
+        sc[e] = auto_index(pos[e], g, log_n);
+        c0v[e] = c0[sc[e]];
+    }
+    double u0[kE8], u1[kE8];
+    key_ip8<true, ND>(ra, r, nd, ext, i, i, key_rows, log_n, mods[i].q, ar, pos, sc, u0, u1);
+    __syncthreads();
+    const size_t row = ((size_t)i << log_n) + (size_t)h * 256;
+    double v[2][kE8];
+#pragma unroll
+    for (int k = 0; k < 2; k++) {
+        const uint64_t *src = cw + (((size_t)r * 2 + k) * L << log_n) + row;
+        double x[kE8];
+#pragma unroll
+        for (int e = 0; e < kE8; e++) x[e] = nttc::Ar<true>::from_raw(nttc::ld_stream(src + nttc::u8<0>(t, e)));
+        nttc::fwd8_256<nttc::kRowMask8>(x, tws[sub], tr[sub], t, ar);
+        nttc::b_to_a8(x, tr[sub], t);
+#pragma unroll
+        for (int e = 0; e < kE8; e++) v[k][e] = x[e];
+    }
+    uint64_t *out = ra.out[r];
+    const double pi = (double)pinv[i].x;
+#pragma unroll
+    for (int e = 0; e < kE8; e++) {
+        const double r0 = ar.mul(u0[e] - v[0][e], pi) + nttc::Ar<true>::from_u64(c0v[e]);
+        const double r1 = ar.mul(u1[e] - v[1][e], pi);
+        nttc::st_stream(out + ((size_t)i << log_n) + pos[e], ar.to_canon(r0));
+        nttc::st_stream(out + (((size_t)L + i) << log_n) + pos[e], ar.to_canon(r1));
     }
 }
 
@@ -702,6 +869,19 @@ size_t ks_scratch_words(const ckks_ctx *ctx, uint32_t level, uint32_t batch, uin
     return ((size_t)n_ct * (nd * ext + ctx->alpha) + (size_t)batch * (2 * ext + 2 * (level + 1))) << ctx->log_n;
 }
 
+// The fused kernels take the digit count as a template argument for 1..4 digits (dnum up to 4 at any level,
+// and the low levels of larger dnum), fully unrolled; more digits take the run-time loop.
+#define CK_ND_DISPATCH(nd, LAUNCH, SD)                                                                             \
+    do {                                                                                                           \
+        switch (nd) {                                                                                              \
+        case 1: LAUNCH(SD, 1); break;                                                                              \
+        case 2: LAUNCH(SD, 2); break;                                                                              \
+        case 3: LAUNCH(SD, 3); break;                                                                              \
+        case 4: LAUNCH(SD, 4); break;                                                                              \
+        default: LAUNCH(SD, 0); break;                                                                             \
+        }                                                                                                          \
+    } while (0)
+
 ckks_status ks_rotate_batch(ckks_ctx *ctx, uint32_t level, uint32_t count, const uint64_t *const *c0s,
                             const uint64_t *const *digs, const uint32_t *g, const uint64_t *const *keys,
                             uint64_t *const *outs, uint64_t *work, const uint64_t *seeds)
@@ -739,12 +919,14 @@ ckks_status ks_rotate_batch(ckks_ctx *ctx, uint32_t level, uint32_t count, const
             const double res = (double)count * 2 * K * N;
             prof_begin(ctx, K_KEYIP, 8.0 * res * (nd + 1.0) + 8.0 * (double)nd * K * N,
                        res * (nd * 10.0 + 4 * kOpsButterflyF64 + 8.0));
+#define CK_IPI(SD, ND)                                                                                             \
+    hipLaunchKernelGGL((k_key_ip_intt8<SD, ND>), dim3(count * K * bpl), dim3(64), 0, ctx->stream, ra, up, nd, ext, L, \
+                       K, ctx->n_q, kp, ctx->d_mod, ctx->d_itwf, ctx->log_n, bpl)
             if (seeded)
-                hipLaunchKernelGGL(k_key_ip_intt8<true>, dim3(count * K * bpl), dim3(64), 0, ctx->stream, ra, up, nd,
-                                   ext, L, K, ctx->n_q, kp, ctx->d_mod, ctx->d_itwf, ctx->log_n, bpl);
+                CK_ND_DISPATCH(nd, CK_IPI, true);
             else
-                hipLaunchKernelGGL(k_key_ip_intt8<false>, dim3(count * K * bpl), dim3(64), 0, ctx->stream, ra, up, nd,
-                                   ext, L, K, ctx->n_q, kp, ctx->d_mod, ctx->d_itwf, ctx->log_n, bpl);
+                CK_ND_DISPATCH(nd, CK_IPI, false);
+#undef CK_IPI
             prof_end(ctx, K_KEYIP);
             HIP_TRY(hipGetLastError());
             CK_TRY(launch_ntt_inv_second_pass(ctx, up, 2 * count, K, limb_range(ctx->n_q, K)));
@@ -775,12 +957,15 @@ ckks_status ks_rotate_batch(ckks_ctx *ctx, uint32_t level, uint32_t count, const
         const double res = (double)count * L * N;
         prof_begin(ctx, K_MODDOWN, 8.0 * res * (2.0 + 2.0 * nd + 2.0),
                    res * (2 * (4 * kOpsButterflyF64 + 4 * (kOpsButterflyF64 - 3)) / 2 + nd * 2 * 10.0 + 40.0));
+#define CK_FIN(SD, ND)                                                                                             \
+    hipLaunchKernelGGL((k_ks_finish8_seeded<ND>), dim3(count * L * bpl), dim3(64), 0, ctx->stream, ra, cw, nd, ext, \
+                       L, kp, ctx->d_mod, ctx->d_twf, ctx->d_pinv, ctx->log_n, bpl)
         if (seeded)
-            hipLaunchKernelGGL(k_ks_finish8<true>, dim3(count * L * bpl), dim3(64), 0, ctx->stream, ra, cw, nd, ext,
-                               L, kp, ctx->d_mod, ctx->d_twf, ctx->d_pinv, ctx->log_n, bpl);
+            CK_ND_DISPATCH(nd, CK_FIN, true);
         else
-            hipLaunchKernelGGL(k_ks_finish8<false>, dim3(count * L * bpl), dim3(64), 0, ctx->stream, ra, cw, nd, ext,
-                               L, kp, ctx->d_mod, ctx->d_twf, ctx->d_pinv, ctx->log_n, bpl);
+            hipLaunchKernelGGL(k_ks_finish8, dim3(count * L * bpl), dim3(64), 0, ctx->stream, ra, cw, nd, ext, L, kp,
+                               ctx->d_mod, ctx->d_twf, ctx->d_pinv, ctx->log_n, bpl);
+#undef CK_FIN
         prof_end(ctx, K_MODDOWN);
         HIP_TRY(hipGetLastError());
         return CKKS_OK;
@@ -835,8 +1020,11 @@ ckks_status ks_ip_accumulate(ckks_ctx *ctx, uint32_t level, uint32_t count, cons
     // digits and keys of every rotation, c0, the accumulators read (when accumulating) and written
     prof_begin(ctx, K_KEYIP, 8.0 * ctx->n * ext * (count * (3.0 * nd) + (double)L / ext * count +
                                                    outs * 2.0 * (accumulate ? 2 : 1)));
-    hipLaunchKernelGGL(k_key_ip_acc, grid, block, 0, ctx->stream, ra, nd, ext, level, ctx->n_q, ctx->n_primes(),
-                       ctx->d_pmodq, ctx->d_mod, ctx->log_n, (int)sum_all, (int)accumulate);
+#define CK_ACC(SD, ND)                                                                                             \
+    hipLaunchKernelGGL(k_key_ip_acc<ND>, grid, block, 0, ctx->stream, ra, nd, ext, level, ctx->n_q,                  \
+                       ctx->n_primes(), ctx->d_pmodq, ctx->d_mod, ctx->log_n, (int)sum_all, (int)accumulate)
+    CK_ND_DISPATCH(nd, CK_ACC, 0);
+#undef CK_ACC
     prof_end(ctx, K_KEYIP);
     HIP_TRY(hipGetLastError());
     return CKKS_OK;
