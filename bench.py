@@ -792,6 +792,14 @@ def main():
     from workloads import PROJECTION as cfg
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
+    if args.calib_copy_mib and args.only not in (None, "tile"):
+        # one plain copy of known size, for scaling the counter passes of these workloads
+        from paper_2609_12378_amd import Context
+        src = torch.ones(args.calib_copy_mib << 17, dtype=torch.uint64, device="cuda")
+        dst = torch.empty_like(src)
+        Context(12, 2, 1, 1).calib_copy(dst, src)
+        torch.cuda.synchronize()
+        del src, dst
     if args.only == "keyswitch":
         print(json.dumps(bench_keyswitch(torch, np, args.steps, args.warmup)), flush=True)
         return

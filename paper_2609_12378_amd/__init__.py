@@ -578,8 +578,10 @@ class Context:
             i += 1
 
     def calib_copy(self, dst: torch.Tensor, src: torch.Tensor):
-        _check(self.lib.ckks_calib_copy(self.h, _ptr(dst), _ptr(src), src.numel() * src.element_size()),
-               "ckks_calib_copy")
+        ps = _arg(src, "calib_copy src", torch.uint64)
+        pd = _arg(dst, "calib_copy dst", torch.uint64, numel=src.numel())
+        _check(self.lib.ckks_calib_copy(self.h, pd, ps, src.numel() * 8), "ckks_calib_copy")
 
     def calib_modmul(self, out: torch.Tensor, iters: int, mode: int):
-        _check(self.lib.ckks_calib_modmul(self.h, _ptr(out), out.numel(), iters, mode), "ckks_calib_modmul")
+        po = _arg(out, "calib_modmul out", torch.uint64)
+        _check(self.lib.ckks_calib_modmul(self.h, po, out.numel(), iters, mode), "ckks_calib_modmul")

@@ -142,5 +142,15 @@ def test_stage_inputs_checked(ctx):
         ctx.ntt(torch.zeros((2, 16), dtype=torch.int64))
 
 
+def test_probe_buffers_checked(ctx):
+    src = torch.zeros(64, dtype=torch.uint64)
+    with pytest.raises(CkksError, match="calib_copy dst: 32 elements, expected 64"):
+        ctx.calib_copy(torch.zeros(32, dtype=torch.uint64), src)
+    with pytest.raises(CkksError, match="calib_copy src: dtype"):
+        ctx.calib_copy(torch.zeros(64, dtype=torch.uint64), torch.zeros(64, dtype=torch.int64))
+    with pytest.raises(CkksError, match="calib_modmul out: dtype"):
+        ctx.calib_modmul(torch.zeros(64, dtype=torch.float64), 4, 1)
+
+
 def test_every_library_call_is_declared():
     assert "ckks_rotate" in pkg.EXPORTED and "ckks_linear_project" in pkg.EXPORTED
