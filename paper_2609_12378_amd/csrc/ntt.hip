@@ -26,10 +26,12 @@
 //  * fp64 (q < 2^50): residues held as exact integer-valued doubles in (-2q, 2q).
 //    a*w = h + l exactly (h = fl(a w), l = fma(a, w, -h)); c = rint(h / q) is
 //    within 1.5 of a w / q, so r = fma(-c, q, h) + l = a w - c q is exact and
-//    |r| < 2q; a range reduction x - q rint(x / q) keeps every stage input below
-//    2q.  About 11 full-rate fp64 instructions per butterfly.  Exactness: with
-//    |a| < 4q < 2^52 and w < q < 2^50, |a w| < 2^102 so |l| <= 2^49, and
-//    |h - c q| <= 2q + 2^49 < 2^52: every intermediate is an integer below 2^53.
+//    |r| < 2q; a range reduction x - q rint(x / q) keeps the stage inputs small.
+//    About 11 full-rate fp64 instructions per butterfly, 8 where a forward stage
+//    skips the reduction of X (fwd_col_mask, fwd_row_mask: values stay below 5q).
+//    Exactness: with |a| < 8q < 2^53 and w < q < 2^50, |a w| < 2^103 so
+//    |l| <= 2^50, and |h - c q| is a few q: every intermediate is an integer
+//    below 2^53.  The inverse's last stage carries N^-1 (Ar<true>::gs_scaled).
 // Between the two passes the row holds lazy values (integer) or raw double
 // bits (fp64); the last pass writes canonical residues in [0, q).
 #include <type_traits>
@@ -51,6 +53,23 @@ __device__ __forceinline__ size_t row_of_block(uint32_t blk_row, uint32_t limbs,
     const uint32_t b = blk_row / limbs, limb = blk_row % limbs;
     *prime_slot = limb;
     return (size_t)b * bstride + limb;
+}
+
+// fp64 forward stages that skip the range reduction of X (bit s of the mask clear: stage s lazy).  In units of
+// q a reducing stage maps a bound b on its values to 1 + 0.375 b and a lazy one to 1.375 b + 0.5 (Ar<true>).
+// Column pass (canonical input, b = 1): every value below 3.7 q, output below 1.9 q (below 2 q for every LOGS,
+// which the fused key-switching kernels that take a first pass's rows also assume); row pass after it (input
+// below 2 q): values below 5 q before the canonical output; a single-pass transform (canonical input): below
+// 4.8 q.  All stay below 8 q < 2^53, where the fp64 products are exact.  Half the stages or more are lazy at
+// N = 2^16, 3 instructions saved per lazy butterfly.
+constexpr unsigned fwd_col_mask(int logs)
+{
+    return logs <= 4 ? 0x0cu : logs == 5 ? 0x1cu : logs == 6 ? 0x34u : logs == 7 ? 0x74u : 0xd4u;
+}
+constexpr unsigned fwd_row_mask(int logs, bool first)
+{
+    return first ? (logs <= 5 ? 0x08u : logs <= 7 ? 0x28u : 0xa8u)
+                 : (logs <= 4 ? 0x04u : logs <= 6 ? 0x14u : 0x54u);
 }
 
 // Sub-transforms per block of the column pass (16 columns of 256 points) and of the row pass (8 rows of 256).
@@ -92,10 +111,11 @@ __global__ __launch_bounds__(256) void ntt_col(uint64_t *data, LimbMap map, uint
     if (!INV) {
 #pragma unroll
         for (int k = 0; k < kE; k++) x[k] = ar.from_u64(ld_stream(base + (size_t)(r + TS * k) * n2 + col));
-        fwd_top<F>(x, tw, 1, ar);
+        constexpr unsigned kMask = fwd_col_mask(LOGS);
+        fwd_top<F, kMask>(x, tw, 1, ar);
         if (LOGS > 4) {
             transpose<LOGS, true>(x, lds, col, r);
-            fwd_low<LOGS, F>(x, tw, 1, r, ar);
+            fwd_low<LOGS, F, kMask>(x, tw, 1, r, ar);
         }
 #pragma unroll
         for (int k = 0; k < kE; k++) st_stream(base + (size_t)(LOGS > 4 ? 16 * r + k : k) * n2 + col, ar.to_raw(x[k]));
@@ -106,9 +126,14 @@ __global__ __launch_bounds__(256) void ntt_col(uint64_t *data, LimbMap map, uint
             inv_low<LOGS, F>(x, tw, 1, r, ar);
             transpose<LOGS, false>(x, lds, col, r);
         }
-        inv_top<F>(x, tw, 1, ar);
+        // fp64: N^-1 folded into the last stage
+        inv_top<F, true>(x, tw, 1, ar);
 #pragma unroll
-        for (int k = 0; k < kE; k++) st_stream(base + (size_t)(r + TS * k) * n2 + col, ar.to_canon(ar.scale_n(x[k])));
+        for (int k = 0; k < kE; k++) {
+            E v = x[k];
+            if constexpr (!F) v = ar.scale_n(v);
+            st_stream(base + (size_t)(r + TS * k) * n2 + col, ar.to_canon(v));
+        }
     }
 }
 
@@ -289,10 +314,11 @@ __global__ __launch_bounds__(LOGN ? 128 : 256) void ntt_row(uint64_t *data, Limb
         x[k] = FIRST ? ar.from_u64(raw) : ar.from_raw(raw);
     }
     if (!INV) {
-        fwd_top<F>(x, tw, B, ar);
+        constexpr unsigned kMask = fwd_row_mask(LOGS, FIRST);
+        fwd_top<F, kMask>(x, tw, B, ar);
         if (LOGS > 4) {
             transpose<LOGS, true>(x, lds, sub, r);
-            fwd_low<LOGS, F>(x, tw, B, r, ar);
+            fwd_low<LOGS, F, kMask>(x, tw, B, r, ar);
             transpose<LOGS, false>(x, lds, sub, r);
         }
     } else {
@@ -301,8 +327,9 @@ __global__ __launch_bounds__(LOGN ? 128 : 256) void ntt_row(uint64_t *data, Limb
             inv_low<LOGS, F>(x, tw, B, r, ar);
             transpose<LOGS, false>(x, lds, sub, r);
         }
-        inv_top<F>(x, tw, B, ar);
-        if (LAST) {
+        // the last pass of an fp64 inverse folds N^-1 into its last stage
+        inv_top<F, LAST>(x, tw, B, ar);
+        if constexpr (LAST && !F) {
 #pragma unroll
             for (int k = 0; k < kE; k++) x[k] = ar.scale_n(x[k]);
         }

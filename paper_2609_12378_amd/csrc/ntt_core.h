@@ -64,9 +64,10 @@ struct Ar<true> {
     double q, qinv, ninv;
     __device__ explicit Ar(const ModQ &m) : q(m.qd), qinv(m.qinvd), ninv(m.ninvd) {}
     __device__ Ar() : q(0.0), qinv(0.0), ninv(0.0) {}
+    // v < 2^52 (every residue): 2^52 + v has the bits of 2^52 with v in its mantissa
     __device__ static E from_u64(uint64_t v)
     {
-        return (double)(uint32_t)(v >> 32) * 4294967296.0 + (double)(uint32_t)v;
+        return __longlong_as_double((long long)(v | 0x4330000000000000ull)) - 4503599627370496.0;
     }
     __device__ static E from_raw(uint64_t v) { return __longlong_as_double((long long)v); }
     __device__ static uint64_t to_raw(E x) { return (uint64_t)__double_as_longlong(x); }
@@ -86,9 +87,8 @@ struct Ar<true> {
         double t = fma(-floor(x * qinv), q, x);
         t = t < 0.0 ? t + q : t;
         t = t >= q ? t - q : t;
-        const double hi = floor(t * (1.0 / 4294967296.0));
-        const double lo = fma(-hi, 4294967296.0, t);
-        return ((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo;
+        // the integer t in [0, q) is the mantissa of 2^52 + t (exact below 2^52)
+        return (uint64_t)__double_as_longlong(t + 4503599627370496.0) & 0x000FFFFFFFFFFFFFull;
     }
     // exact for any int64: |v| <= 2^52 converts exactly; larger values are reduced as integers first
     __device__ E from_i64(int64_t v, const ModQ &m) const
@@ -122,10 +122,39 @@ struct Ar<true> {
         Y = mul(v, w);
     }
     __device__ E scale_n(E x) const { return mul(x, ninv); }
+    // w * N^-1 mod q in [0, q), for the last inverse stage with the scaling folded in (w canonical)
+    __device__ double scaled_twiddle(double w) const
+    {
+        double t = mul(w, ninv);
+        t = t < 0.0 ? t + q : t;
+        return t >= q ? t - q : t;
+    }
+    // the last Gentleman-Sande stage times N^-1: X' = (X + Y) N^-1, Y' = (X - Y) w N^-1 with wn = w N^-1 mod q
+    __device__ void gs_scaled(E &X, E &Y, W wn) const
+    {
+        const double u = X + Y, v = X - Y;
+        X = mul(u, ninv);
+        Y = mul(v, wn);
+    }
 };
 
+// One forward butterfly of stage s: with fp64 arithmetic a stage whose bit in RMASK is clear skips the range
+// reduction of X (ct_lazy); the integer arithmetic keeps its own lazy range [0, 4q) and ignores the mask.
+template <bool F, unsigned RMASK>
+__device__ __forceinline__ void ct_stage(const Ar<F> &ar, int s, typename Ar<F>::E &X, typename Ar<F>::E &Y,
+                                         typename Ar<F>::W w)
+{
+    if constexpr (F) {
+        if ((RMASK >> s) & 1u)
+            ar.ct(X, Y, w);
+        else
+            ar.ct_lazy(X, Y, w);
+    } else {
+        ar.ct(X, Y, w);
+    }
+}
 // Forward, top 4 stages of a sub-transform: x[k] is point u = r + TS*k.
-template <bool F>
+template <bool F, unsigned RMASK = 0xFFFFu>
 __device__ __forceinline__ void fwd_top(typename Ar<F>::E (&x)[kE], const typename Ar<F>::W *tw, uint32_t B,
                                         const Ar<F> &ar)
 {
@@ -136,12 +165,12 @@ __device__ __forceinline__ void fwd_top(typename Ar<F>::E (&x)[kE], const typena
         for (int g = 0; g < mp; g++) {
             const typename Ar<F>::W w = tw[B * mp + g];
 #pragma unroll
-            for (int j = 0; j < tk; j++) ar.ct(x[g * 2 * tk + j], x[g * 2 * tk + j + tk], w);
+            for (int j = 0; j < tk; j++) ct_stage<F, RMASK>(ar, lm, x[g * 2 * tk + j], x[g * 2 * tk + j + tk], w);
         }
     }
 }
 // Forward, remaining LOGS-4 stages: x[k] is point u = 16 r + k.
-template <int LOGS, bool F>
+template <int LOGS, bool F, unsigned RMASK = 0xFFFFu>
 __device__ __forceinline__ void fwd_low(typename Ar<F>::E (&x)[kE], const typename Ar<F>::W *tw, uint32_t B,
                                         uint32_t r, const Ar<F> &ar)
 {
@@ -152,7 +181,8 @@ __device__ __forceinline__ void fwd_low(typename Ar<F>::E (&x)[kE], const typena
         for (int g = 0; g < gpt; g++) {
             const typename Ar<F>::W w = tw[B * mp + r * gpt + g];
 #pragma unroll
-            for (int j = 0; j < t; j++) ar.ct(x[g * 2 * t + j], x[g * 2 * t + j + t], w);
+            for (int j = 0; j < t; j++)
+                ct_stage<F, RMASK>(ar, 4 + l, x[g * 2 * t + j], x[g * 2 * t + j + t], w);
         }
     }
 }
@@ -171,7 +201,8 @@ __device__ __forceinline__ void inv_low(typename Ar<F>::E (&x)[kE], const typena
         }
     }
 }
-template <bool F>
+// SCALED (fp64 only): the last stage also multiplies by N^-1 (gs_scaled), so the caller skips scale_n.
+template <bool F, bool SCALED = false>
 __device__ __forceinline__ void inv_top(typename Ar<F>::E (&x)[kE], const typename Ar<F>::W *tw, uint32_t B,
                                         const Ar<F> &ar)
 {
@@ -181,6 +212,14 @@ __device__ __forceinline__ void inv_top(typename Ar<F>::E (&x)[kE], const typena
 #pragma unroll
         for (int g = 0; g < mp; g++) {
             const typename Ar<F>::W w = tw[B * mp + g];
+            if constexpr (F && SCALED) {
+                if (lm == 0) {
+                    const double wn = ar.scaled_twiddle(w);
+#pragma unroll
+                    for (int j = 0; j < tk; j++) ar.gs_scaled(x[g * 2 * tk + j], x[g * 2 * tk + j + tk], wn);
+                    continue;
+                }
+            }
 #pragma unroll
             for (int j = 0; j < tk; j++) ar.gs(x[g * 2 * tk + j], x[g * 2 * tk + j + tk], w);
         }
