@@ -62,15 +62,12 @@ __device__ __forceinline__ size_t row_of_block(uint32_t blk_row, uint32_t limbs,
 // below 2 q): values below 5 q before the canonical output; a single-pass transform (canonical input): below
 // 4.8 q.  All stay below 8 q < 2^53, where the fp64 products are exact.  Half the stages or more are lazy at
 // N = 2^16, 3 instructions saved per lazy butterfly.
-constexpr unsigned fwd_col_mask(int logs)
-{
-    return logs <= 4 ? 0x0cu : logs == 5 ? 0x1cu : logs == 6 ? 0x34u : logs == 7 ? 0x74u : 0xd4u;
-}
-constexpr unsigned fwd_row_mask(int logs, bool first)
-{
-    return first ? (logs <= 5 ? 0x08u : logs <= 7 ? 0x28u : 0xa8u)
-                 : (logs <= 4 ? 0x04u : logs <= 6 ? 0x14u : 0x54u);
-}
+// Indexed by log2 of the sub-transform size (4..8; smaller sizes do not occur).
+constexpr unsigned kFwdColMask[9] = {0xff, 0xff, 0xff, 0xff, 0x0c, 0x1c, 0x34, 0x74, 0xd4};
+constexpr unsigned kFwdRowMask[9] = {0xff, 0xff, 0xff, 0xff, 0x04, 0x14, 0x14, 0x54, 0x54};
+constexpr unsigned kFwdSingleMask[9] = {0xff, 0xff, 0xff, 0xff, 0x08, 0x08, 0x28, 0x28, 0xa8};
+constexpr unsigned fwd_col_mask(int logs) { return kFwdColMask[logs]; }
+constexpr unsigned fwd_row_mask(int logs, bool first) { return first ? kFwdSingleMask[logs] : kFwdRowMask[logs]; }
 
 // Sub-transforms per block of the column pass (16 columns of 256 points) and of the row pass (8 rows of 256).
 constexpr uint32_t col_subs(int logs, int log_n)
