@@ -1,0 +1,95 @@
+"""GPU parity of key switching with more digits than the benchmark's dnum = 3, at N = 2^16 with 50-bit primes, where
+the fused key-switching kernels run.  Their inner products take the digit count as a compile-time argument for 1..4
+digits and as a run-time loop beyond, so both forms are compared with the oracle bit for bit:
+
+* 13 + 4 limbs, dnum 4 (alpha 4): 4 digits at level 12 (the compile-time form), 2 at level 5;
+* 13 + 2 limbs, dnum 7 (alpha 2): 7 digits at level 12 (the run-time loop), 5 at level 9;
+
+each for hoisted rotations with stored keys and with seed-expanded keys, and for a 256 x 512 projection slice with
+the lazy ModDown (whose accumulating inner product sums the giant-step rotations) at level 12.
+"""
+import dataclasses
+
+import numpy as np
+import pytest
+
+from gpu_common import require_gpu, say, to_dev, to_host
+from oracle import Ckks
+from workloads import PROJECTION, gaussian_error, rng, ternary_secret, uniform_residues, uniform_slots
+
+pytestmark = pytest.mark.gpu
+
+# (name, n_q, n_p, dnum, levels to rotate at)
+CASES = [("dnum4", 13, 4, 4, (12, 5)), ("dnum7", 13, 2, 7, (12, 9))]
+
+
+def eq(dev, host, what):
+    got = to_host(dev)
+    assert got.shape == host.shape, (what, got.shape, host.shape)
+    bad = np.argwhere(got != host)
+    assert bad.size == 0, "%s: first mismatches at %s" % (what, bad[:5].tolist())
+
+
+def context(n_q, n_p, dnum):
+    from paper_2609_12378_amd import Context
+    ctx = Context(16, n_q, n_p, dnum, q_bits=50)
+    return ctx, Ckks(16, ctx.q, ctx.p, dnum)
+
+
+def n_digits(level, n_q, dnum):
+    alpha = -(-n_q // dnum)
+    return -(-(level + 1) // alpha)
+
+
+@pytest.mark.parametrize("seeded", [False, True], ids=["stored", "seeded"])
+@pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
+def test_rotate_hoisted_many_digits(case, seeded):
+    require_gpu()
+    name, n_q, n_p, dnum, levels = case
+    ctx, ck = context(n_q, n_p, dnum)
+    n = ctx.n
+    tag = 90 + CASES.index(case) * 10 + int(seeded)
+    s = ternary_secret(rng(3, 3, extra=tag), n)
+    s_dev = to_dev(s)
+    steps = [1, -6, 32]
+    for level in levels:
+        say("rotate hoisted", name, "seeded" if seeded else "stored", "level", level, "digits",
+            n_digits(level, n_q, dnum))
+        limbs = level + 1
+        re = uniform_slots(rng(3, 1, extra=tag * 10 + level), n // 2)
+        g = rng(3, 4, extra=tag * 10 + level)
+        a, e = uniform_residues(g, ctx.q[:limbs], n), gaussian_error(g, n)
+        cto = ck.encrypt(s, ck.encode(re, None, 2.0 ** 40, limbs), a, e)
+        ctg = ctx.encrypt(s_dev, ctx.encode(to_dev(re), None, 2.0 ** 40, limbs), to_dev(a), to_dev(e))
+        keys_o, keys_g, seeds = [], [], []
+        for i, st in enumerate(steps):
+            gk = rng(3, 5, extra=tag * 100 + level * 10 + i)
+            gel = ck.galois_elt(st)
+            ke = gaussian_error(gk, (dnum, n))
+            if seeded:
+                seed = [tag * 1000 + i, level]
+                keys_g.append(ctx.keygen_galois_seeded(s_dev, gel, seed, to_dev(ke)))
+                keys_o.append(ck.seeded_key(ck.keygen_galois_seeded(s, gel, seed, ke), seed))
+                seeds.append(seed)
+            else:
+                ka = uniform_residues(gk, ctx.primes, n, lead=(dnum,))
+                keys_g.append(ctx.keygen_galois(s_dev, gel, to_dev(ka), to_dev(ke)))
+                keys_o.append(ck.keygen_galois(s, gel, ka, ke))
+        outs = (ctx.rotate_hoisted_seeded(ctg, steps, keys_g, seeds) if seeded
+                else ctx.rotate_hoisted(ctg, steps, keys_g))
+        want = ck.rotate_hoisted(cto, steps, keys_o)
+        for st, og, w in zip(steps, outs, want):
+            eq(og.data, w, "%s level %d rotation %d" % (name, level, st))
+        dre, _ = ctx.decode(ctx.decrypt(s_dev, outs[-1]))
+        assert np.max(np.abs(to_host(dre) - np.roll(re, -steps[-1]))) < 2.0 ** -18
+
+
+@pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
+def test_projection_lazy_moddown_many_digits(case):
+    from test_gpu_project import run_case
+    name, n_q, n_p, dnum, _ = case
+    cfg = dataclasses.replace(PROJECTION, name="projection_" + name, n_q=n_q, n_p=n_p, dnum=dnum)
+    say("lazy projection slice", name, "digits", n_digits(cfg.level, n_q, dnum))
+    err = run_case(cfg, 256, 512, [1], lazy=True)
+    say("lazy slice", name, "max error vs X@W", err)
+    assert err <= 2.0 ** -18
