@@ -14,7 +14,9 @@ within the stated bound:
   vector-ALU multiply-accumulate, one block meeting many runs);
 * the projection parameters at full degree (N = 2^16, 24 + 8 limbs, level 12, 128
   tokens x 256 features, n1 = 32: 31 + 32 baby and 7 giant rotations) on a
-  256 x 512 slice (runs of 128 values: the matrix-core multiply-accumulate).
+  256 x 512 slice (runs of 128 values: the matrix-core multiply-accumulate);
+* the token-major benchmark call itself (4096 x 14336, n1 = 32, lazy ModDown): outputs 0,
+  27 and 55 against the oracle's stored digests.
 """
 import dataclasses
 
@@ -195,3 +197,52 @@ def test_toy_tm_projection_lowest_level():
     err = run_case(cfg, TOY.feats, TOY.feats, 8, [0])
     say("toy tm level-1 max error vs X@W", err)
     assert err <= 2.0 ** -10
+
+
+def test_tm_projection_benchmark_shape_bit_exact():
+    """The token-major benchmark call (n1 = 32): 4096 x 14336 weights, 16 input ciphertexts at level 12 with slot
+    t * 256 + f, the lazy ModDown and the default sub-batching, with the benchmark's seeded inputs.  Output
+    ciphertexts 0, 27 and 55 are compared in full against the oracle's, stored as SHA-256 digests (with 32
+    residues per row) by tests/golden/make_projection_golden.py --layout tm; their decrypted slots must also
+    agree with X @ W within 2^-20."""
+    require_gpu()
+    import hashlib
+    import json
+    import os
+    from paper_2609_12378_amd import Context
+    from workloads import projection_inputs
+    golden_path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden",
+                               "projection_tm_4096x14336_outputs.json")
+    with open(golden_path) as f:
+        golden = json.load(f)
+    cfg = PROJECTION
+    ctx = Context(cfg.log_n, cfg.n_q, cfg.n_p, cfg.dnum, q_bits=cfg.q_bits)
+    ctx.set_lazy_moddown(True)
+    n, T, D, n1, level = ctx.n, cfg.tokens, cfg.feats, cfg.n1, cfg.level
+    inp = projection_inputs(cfg, ctx.q, ctx.primes, layout="tm")
+    s_dev = to_dev(inp.s)
+    delta = float(2 ** cfg.scale_log2)
+    cts = []
+    for i, (a, e) in enumerate(inp.enc):
+        pt = ctx.encode(to_dev(tm_pack(inp.X, T, D, i)), None, delta, level + 1)
+        cts.append(ctx.encrypt(s_dev, pt, to_dev(a), to_dev(e)))
+    keys = {st: ctx.keygen_galois(s_dev, ctx.galois_elt(st), to_dev(a), to_dev(e)) for st, (a, e) in inp.keys.items()}
+    say("token-major benchmark-shape projection: keys ready", len(keys))
+    outs = ctx.linear_project(cts, to_dev(inp.W), T, n1, keys, layout="tm")
+    assert len(outs) == cfg.d_out // D
+    pos = golden["positions"]
+    for j in (0, 27, 55):
+        rec = golden["outputs"][str(j)]
+        assert outs[j].scale == delta and outs[j].n_limbs == level
+        got = to_host(outs[j].data)
+        assert list(got.shape) == rec["shape"]
+        samples = np.array([got[c, r, pos] for c in range(2) for r in range(level)], dtype=np.uint64)
+        bad = np.argwhere(samples != np.array(rec["samples"], dtype=np.uint64))
+        assert bad.size == 0, "output %d: sampled residues differ at (row, sample) %s" % (j, bad[:5].tolist())
+        digest = hashlib.sha256(np.ascontiguousarray(got, dtype="<u8").tobytes()).hexdigest()
+        assert digest == rec["sha256"], "output %d: full ciphertext differs from the oracle's" % j
+        re, _ = ctx.decode(ctx.decrypt(s_dev, outs[j]))
+        want = tm_pack(inp.X @ inp.W[:, j * D:(j + 1) * D], T, D, 0)
+        err = float(np.max(np.abs(to_host(re) - want)))
+        say("output", j, "bit-exact against the oracle; max error vs X@W", err)
+        assert err <= 2.0 ** -20
