@@ -29,6 +29,7 @@ if ROOT not in sys.path:
 METRIC = "rotations/s at N=2^16 (keyswitch) and s per 4096x14336 ct-pt projection"
 # sums of rotations (giant steps, the attention outer sum) with one ModDown per output (--lazy-moddown)
 LAZY = {"on": False}
+PROJ_BATCH = {"pairs": 0}   # --proj-batch: pairs per multiply-accumulate launch (0: library default)
 
 
 def make_context(cfg, n_p=None, dnum=None):
@@ -36,6 +37,8 @@ def make_context(cfg, n_p=None, dnum=None):
     ctx = Context(cfg.log_n, cfg.n_q, cfg.n_p if n_p is None else n_p, cfg.dnum if dnum is None else dnum,
                   q_bits=cfg.q_bits)
     ctx.set_lazy_moddown(LAZY["on"])
+    if PROJ_BATCH["pairs"]:
+        ctx.set_proj_batch(PROJ_BATCH["pairs"])
     return ctx
 HBM_PEAK_GBS = 8000.0
 # 256 CUs x 64 lanes x 2.4 GHz of VALU issue (fp64 FMA and 32-bit integer ops are full rate)
@@ -779,10 +782,14 @@ def main():
     ap.add_argument("--lazy-moddown", type=int, default=1, choices=[0, 1],
                     help="1 (default): sums of rotations with one ModDown per output (the library's lazy mode); "
                          "0: one ModDown per rotation")
+    ap.add_argument("--proj-batch", type=int, default=0,
+                    help="at most this many (input, baby step) pairs per multiply-accumulate launch of a projection "
+                         "(0: the library's default, 128); for schedule experiments")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also run one plain device copy of this many MiB (for hardware-counter calibration)")
     args = ap.parse_args()
     LAZY["on"] = bool(args.lazy_moddown)
+    PROJ_BATCH["pairs"] = args.proj_batch
     if args.gpus != 1:
         print("bench.py runs on one GPU: the library drives a single GPU (--gpus %d requested)"
               % args.gpus, file=sys.stderr)
