@@ -725,25 +725,40 @@ def cpu_model():
 
 
 def cpu_oracle_secondary(np):
-    """The oracle's rates on the NTT and key-switching workloads, from small samples (threads as for the
-    projection baseline): one 2^16-point negacyclic NTT row, and a one- and a two-rotation hoisted call at the
-    key-switching parameters (their difference is one rotation's inner product and ModDown, the rest the shared
-    ModUp), extrapolated to 64 x 36 rows and to 32 hoisted rotations."""
+    """The oracle on the NTT and key-switching workloads in full, with its OpenMP threads (rows of the transform
+    in parallel; the key switch's limb loops): the 64 x 36 x 2^16 forward and inverse transforms (round trip
+    checked), and the 32 hoisted rotations of the key-switching batch; plus the NTT's single-threaded rate from
+    one row."""
     from oracle import Ckks, gen_primes
+    from oracle.ckks import lib as oracle_lib
     from workloads import KEYSWITCH as kcfg, NTT_BENCH as ncfg, gaussian_error, rng, ternary_secret, \
         uniform_residues, uniform_slots
     out = {}
-    pr = gen_primes(ncfg.q_bits, 2 * ncfg.n, 1)
+    threads = oracle_lib().or_threads()
+    pr = gen_primes(ncfg.q_bits, 2 * ncfg.n, ncfg.n_q)
     ck = Ckks(ncfg.log_n, pr)
-    a = uniform_residues(rng(ncfg.index, 1), pr, ck.n)
+    a = uniform_residues(rng(ncfg.index, 1), pr, ck.n, lead=(ncfg.batch,))
+    idx = list(range(ncfg.n_q)) * ncfg.batch
     t0 = time.time()
-    reps = 0
-    while time.time() - t0 < 2.0 or reps < 2:
-        ck.ntt(a, [0])
-        reps += 1
-    t_row = (time.time() - t0) / reps
-    out["ntt"] = {"s_per_direction": t_row * ncfg.batch * ncfg.n_q, "row_s": t_row,
-                  "sample": "%d forward NTT rows of 2^16 residues, scaled by 64 x 36 rows" % reps}
+    fa = ck.ntt(a, idx)
+    t_fwd = time.time() - t0
+    t0 = time.time()
+    back = ck.intt(fa, idx)
+    t_inv = time.time() - t0
+    assert np.array_equal(back, a), "oracle NTT round trip failed"
+    del fa, back
+    oracle_lib().or_set_threads(1)
+    try:
+        t0 = time.time()
+        ck.ntt(a[0, :1], [0])
+        t_row1 = time.time() - t0
+    finally:
+        oracle_lib().or_set_threads(threads)
+    out["ntt"] = {"s_per_direction": t_fwd, "inv_s": t_inv, "threads": threads,
+                  "single_thread_s_per_direction": t_row1 * ncfg.batch * ncfg.n_q,
+                  "sample": "the full 64 x 36 x 2^16 forward and inverse (round trip checked), %d threads; single "
+                            "thread: one row (%.3f s) scaled by 64 x 36" % (threads, t_row1)}
+    del a
     pr = gen_primes(kcfg.q_bits, 2 * kcfg.n, kcfg.n_q + kcfg.n_p)
     ck = Ckks(kcfg.log_n, pr[:kcfg.n_q], pr[kcfg.n_q:], kcfg.dnum)
     n, L = ck.n, kcfg.level + 1
@@ -752,19 +767,14 @@ def cpu_oracle_secondary(np):
     ct = ck.encrypt(s, ck.encode(uniform_slots(rng(kcfg.index, 1), n // 2), None, 2.0 ** 40, L),
                     uniform_residues(ge, ck.q[:L], n), gaussian_error(ge, n))
     gk = rng(kcfg.index, 5)
+    steps = list(range(1, kcfg.batch + 1))
     keys = [ck.keygen_galois(s, ck.galois_elt(r), uniform_residues(gk, ck.primes, n, lead=(kcfg.dnum,)),
-                             gaussian_error(gk, (kcfg.dnum, n))) for r in (1, 2)]
+                             gaussian_error(gk, (kcfg.dnum, n))) for r in steps]
     t0 = time.time()
-    ck.rotate_hoisted(ct, [1], keys[:1])
-    t1 = time.time() - t0
-    t0 = time.time()
-    ck.rotate_hoisted(ct, [1, 2], keys)
-    t2 = time.time() - t0
-    per_rot = max(t2 - t1, 1e-9)
-    batch = max(t1 - per_rot, 0.0) + kcfg.batch * per_rot
-    out["keyswitch"] = {"rotations_per_s": kcfg.batch / batch, "s_per_batch": batch,
-                        "sample": "hoisted calls of 1 and 2 rotations at level 23 (%.2f s, %.2f s), scaled to 32"
-                                  % (t1, t2)}
+    ck.rotate_hoisted(ct, steps, keys)
+    batch = time.time() - t0
+    out["keyswitch"] = {"rotations_per_s": kcfg.batch / batch, "s_per_batch": batch, "threads": threads,
+                        "sample": "the full batch: 32 hoisted rotations by 1..32 at level 23, %d threads" % threads}
     return out
 
 
