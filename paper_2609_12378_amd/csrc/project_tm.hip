@@ -271,21 +271,43 @@ __global__ __launch_bounds__(kThreads) void k_xdigits(const uint64_t *__restrict
     const uint32_t cb = rest % cblocks, l = rest / cblocks;
     const size_t n = (size_t)1 << log_n, ctw = 2 * (size_t)L * n;
     const uint32_t c0 = cb * 64, k0 = kb * 64;
-    for (uint32_t e = threadIdx.x; e < 64 * 64; e += kThreads) {
-        const uint32_t kk = e / 64, cc = e % 64, kappa = k0 + kk, c = c0 + cc;
-        uint64_t v = 0;
-        if (kappa < kt) {
-            const uint32_t poly = c >> log_n, pos = c & ((1u << log_n) - 1);
-            v = x2[(size_t)kappa * ctw + ((size_t)poly * L + l) * n + pos];
-        }
-        tile[kk][cc] = v;
+    // all 16 loads of a thread issued before any is stored (one memory wait per thread, not sixteen)
+    const uint32_t cc_r = threadIdx.x % 64, c = c0 + cc_r;
+    const uint32_t poly = c >> log_n, pos = c & ((1u << log_n) - 1);
+    const uint64_t *src = x2 + ((size_t)poly * L + l) * n + pos;
+    uint64_t vals[64 * 64 / kThreads];
+#pragma unroll
+    for (int i = 0; i < 64 * 64 / kThreads; i++) {
+        const uint32_t kappa = k0 + threadIdx.x / 64 + (kThreads / 64) * i;
+        vals[i] = kappa < kt ? src[(size_t)kappa * ctw] : 0;
     }
+#pragma unroll
+    for (int i = 0; i < 64 * 64 / kThreads; i++) tile[threadIdx.x / 64 + (kThreads / 64) * i][cc_r] = vals[i];
     __syncthreads();
+    // each thread writes 16 consecutive kappa of one column: one 16-byte store per digit plane (kt_pad, k0 and the
+    // 16-kappa offset are multiples of 16, and Xd is 16-byte aligned)
     const size_t plane = (size_t)L * cols * kt_pad;
-    for (uint32_t e = threadIdx.x; e < 64 * 64; e += kThreads) {
-        const uint32_t cc = e / 64, kk = e % 64;
-        digits7(tile[kk][cc], Xd + ((size_t)l * cols + c0 + cc) * kt_pad + k0 + kk, plane);
+    static_assert(kThreads == 256, "64 columns x 4 groups of 16 kappa");
+    const uint32_t cc = threadIdx.x >> 2, kq = (threadIdx.x & 3u) << 4;
+    uint32_t w[kDig][4] = {};
+#pragma unroll
+    for (int i = 0; i < 16; i++) {
+        uint64_t v = tile[kq + i][cc];
+#pragma unroll
+        for (int a = 0; a < kDig; a++) {
+            int t = (int)(v & 255u);
+            v >>= 8;
+            if (t >= 128) {
+                t -= 256;
+                v += 1;
+            }
+            w[a][i >> 2] |= (uint32_t)(uint8_t)t << (8 * (i & 3));
+        }
     }
+    int8_t *dst = Xd + ((size_t)l * cols + c0 + cc) * kt_pad + k0 + kq;
+#pragma unroll
+    for (int a = 0; a < kDig; a++)
+        *(uint4 *)(dst + (size_t)a * plane) = make_uint4(w[a][0], w[a][1], w[a][2], w[a][3]);
 }
 
 // Block (limb l, run x, polynomial, part): NW waves, wave w holds 16 positions of the run (x T + 16 (part NW + w)
