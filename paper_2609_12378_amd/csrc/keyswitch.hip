@@ -104,14 +104,16 @@ __global__ __launch_bounds__(kThreads) void k_conv(const uint64_t *in, uint32_t 
 // products y_i * [Qhat_i]_t (each below 0.875 t in magnitude, since |y_i| < s_i/2 < t) with a range reduction
 // every four terms (sums stay below 4 t < 2^53) and writes the canonical residue: the same integers as k_conv.
 // C coefficients per thread (kThreads apart, so every load and store stays coalesced): the per-target constants
-// come from LDS once for all C, and the C product chains are independent.  EXACT: ns == NS_MAX, so the source
-// loop has no guards and all source loads issue before the first is used.
+// come from LDS once for all C, and the C product chains are independent.  All source loads issue before the
+// first is used (EXACT: ns == NS_MAX, no guards in the source loop).  blockIdx.z splits the target limbs into
+// groups of t_per when a few polynomials alone would leave most SIMDs idle.
 template <int NS_MAX, int C, bool EXACT = false>
 __global__ __launch_bounds__(kThreads) void k_conv_f64(const uint64_t *in, uint32_t in_stride, uint64_t *out,
                                                         uint32_t out_stride, uint32_t split, uint32_t skip,
                                                         ConvArgs a, const double *__restrict__ qhat_inv,
                                                         const double *__restrict__ qhat_mod,
-                                                        const ModQ *__restrict__ mods, uint32_t log_n)
+                                                        const ModQ *__restrict__ mods, uint32_t log_n,
+                                                        uint32_t t_per)
 {
     __shared__ double s_mod[NS_MAX * kMaxPrimes];
     __shared__ double2 s_tq[kMaxPrimes];
@@ -124,15 +126,19 @@ __global__ __launch_bounds__(kThreads) void k_conv_f64(const uint64_t *in, uint3
     const uint32_t poly = blockIdx.y;
     if (col >= n) return;  // n is a multiple of kThreads * C
     const uint64_t *src = in + ((size_t)poly * in_stride << log_n) + col;
+    // every source load issued before any is used: with fewer than NS_MAX sources the extra loads repeat the last
+    // source row (no branch, so the loads stay together) and are ignored
     double y[C][NS_MAX];
-    if (EXACT) {
-        uint64_t raw[C][NS_MAX];
+    uint64_t raw[C][NS_MAX];
 #pragma unroll
-        for (int i = 0; i < NS_MAX; i++)
+    for (int i = 0; i < NS_MAX; i++) {
+        const int ii = EXACT ? i : min(i, ns - 1);
 #pragma unroll
-            for (int c = 0; c < C; c++) raw[c][i] = src[((size_t)i << log_n) + c * kThreads];
+        for (int c = 0; c < C; c++) raw[c][i] = src[((size_t)ii << log_n) + c * kThreads];
+    }
 #pragma unroll
-        for (int i = 0; i < NS_MAX; i++) {
+    for (int i = 0; i < NS_MAX; i++) {
+        if (EXACT || i < ns) {
             const nttc::Ar<true> ar(mods[a.src[i]]);
             const double h = 0.5 * ar.q;
 #pragma unroll
@@ -142,21 +148,11 @@ __global__ __launch_bounds__(kThreads) void k_conv_f64(const uint64_t *in, uint3
             }
         }
     }
-#pragma unroll
-    for (int i = 0; i < NS_MAX; i++) {
-        if (!EXACT && i < ns) {
-            const nttc::Ar<true> ar(mods[a.src[i]]);
-            const double h = 0.5 * ar.q;
-#pragma unroll
-            for (int c = 0; c < C; c++) {
-                const double v = ar.mul(nttc::Ar<true>::from_u64(src[((size_t)i << log_n) + c * kThreads]),
-                                        qhat_inv[i]);
-                y[c][i] = v > h ? v - ar.q : (v < -h ? v + ar.q : v);
-            }
-        }
-    }
     uint64_t *dst = out + ((size_t)poly * out_stride << log_n) + col;
-    for (int t = 0; t < nt; t++) {
+    // blockIdx.z: this block's group of t_per target limbs (several groups when one polynomial alone would leave
+    // the chip mostly idle; each group recomputes the ns centred digits)
+    const int t0 = (int)(blockIdx.z * t_per), t1 = min(nt, t0 + (int)t_per);
+    for (int t = t0; t < t1; t++) {
         nttc::Ar<true> ar;
         ar.q = s_tq[t].x;
         ar.qinv = s_tq[t].y;
@@ -751,22 +747,36 @@ ckks_status launch_conv(ckks_ctx *ctx, const ConvDev *cd, const uint64_t *in, ui
     for (int i = 0; i < cd->ns; i++) a.src[i] = cd->src[i];
     for (int t = 0; t < cd->nt; t++) a.dst[t] = cd->dst[t];
     const dim3 grid((ctx->n + kThreads - 1) / kThreads, polys), block(kThreads);
-    // fp64 kernels: two coefficients per thread where the ring has at least 512 of them
-    const bool two = ctx->n % (2 * kThreads) == 0;
-    const dim3 grid2(two ? (uint32_t)(ctx->n / (2 * kThreads)) : grid.x, polys);
+    // fp64 kernels: two coefficients per thread where the ring has at least 512 of them and that still leaves
+    // 4096 waves (4 per SIMD); with fewer polynomials one coefficient per thread, and the target limbs split over
+    // blockIdx.z until the grid has that many waves
+    const size_t waves1 = (size_t)((ctx->n + 63) / 64) * polys;
+    const bool two = ctx->n % (2 * kThreads) == 0 && waves1 / 2 >= 4096;
+    uint32_t groups = 1;
+    const uint32_t ntg = a.nt > 0 ? (uint32_t)a.nt : 1u;
+    if (!two && waves1 < 4096) groups = (uint32_t)std::min<size_t>(ntg, (4096 + waves1 - 1) / waves1);
+    const uint32_t t_per = (ntg + groups - 1) / groups;
+    groups = (ntg + t_per - 1) / t_per;
+    const dim3 grid1(grid.x, polys, groups);
+    const dim3 grid2(two ? (uint32_t)(ctx->n / (2 * kThreads)) : grid.x, polys, two ? 1 : groups);
     prof_begin(ctx, K_CONV, 8.0 * polys * (a.ns + a.nt) * ctx->n);
 #define CK_CONVF(NSM)                                                                                              \
     do {                                                                                                           \
         if (two && a.ns == NSM)                                                                                    \
             hipLaunchKernelGGL((k_conv_f64<NSM, 2, true>), grid2, block, 0, ctx->stream, in, in_stride, out,        \
                                out_stride, split, skip, a, cd->d_qhat_inv_f, cd->d_qhat_mod_f, ctx->d_mod,          \
-                               ctx->log_n);                                                                        \
+                               ctx->log_n, (uint32_t)a.nt);                                                        \
+        else if (a.ns == NSM)                                                                                      \
+            hipLaunchKernelGGL((k_conv_f64<NSM, 1, true>), grid1, block, 0, ctx->stream, in, in_stride, out,        \
+                               out_stride, split, skip, a, cd->d_qhat_inv_f, cd->d_qhat_mod_f, ctx->d_mod,          \
+                               ctx->log_n, t_per);                                                                 \
         else if (two)                                                                                              \
             hipLaunchKernelGGL((k_conv_f64<NSM, 2>), grid2, block, 0, ctx->stream, in, in_stride, out, out_stride,  \
-                               split, skip, a, cd->d_qhat_inv_f, cd->d_qhat_mod_f, ctx->d_mod, ctx->log_n);        \
+                               split, skip, a, cd->d_qhat_inv_f, cd->d_qhat_mod_f, ctx->d_mod, ctx->log_n,         \
+                               (uint32_t)a.nt);                                                                    \
         else                                                                                                       \
-            hipLaunchKernelGGL((k_conv_f64<NSM, 1>), grid, block, 0, ctx->stream, in, in_stride, out, out_stride,   \
-                               split, skip, a, cd->d_qhat_inv_f, cd->d_qhat_mod_f, ctx->d_mod, ctx->log_n);        \
+            hipLaunchKernelGGL((k_conv_f64<NSM, 1>), grid1, block, 0, ctx->stream, in, in_stride, out, out_stride,  \
+                               split, skip, a, cd->d_qhat_inv_f, cd->d_qhat_mod_f, ctx->d_mod, ctx->log_n, t_per); \
     } while (0)
     if (cd->f64 && !ctx->int_only && a.ns <= 16) {
         if (a.ns <= 8)
