@@ -102,7 +102,8 @@ __global__ __launch_bounds__(kThreads) void k_conv(const uint64_t *in, uint32_t 
 // The same conversion in fp64 (every prime below 2^50): y_i = x_i * qhat_inv_i mod s_i (|mul| < 0.875 s_i for
 // canonical operands) is moved into (-s_i/2, s_i/2] by one add or subtract of s_i, then each target sums the
 // products y_i * [Qhat_i]_t (each below 0.875 t in magnitude, since |y_i| < s_i/2 < t) with a range reduction
-// every four terms (sums stay below 4 t < 2^53) and writes the canonical residue: the same integers as k_conv.
+// after every eight terms that more follow (sums stay below 7.5 t < 2^53) and writes the canonical residue: the
+// same integers as k_conv.
 // C coefficients per thread (kThreads apart, so every load and store stays coalesced): the per-target constants
 // come from LDS once for all C, and the C product chains are independent.  All source loads issue before the
 // first is used (EXACT: ns == NS_MAX, no guards in the source loop).  blockIdx.z splits the target limbs into
@@ -166,7 +167,7 @@ __global__ __launch_bounds__(kThreads) void k_conv_f64(const uint64_t *in, uint3
 #pragma unroll
                 for (int c = 0; c < C; c++) {
                     acc[c] += ar.mul(y[c][i], w);
-                    if ((i & 3) == 3) acc[c] = ar.red(acc[c]);
+                    if ((i & 7) == 7 && i + 1 < ns) acc[c] = ar.red(acc[c]);
                 }
             }
         }
@@ -249,7 +250,7 @@ __global__ __launch_bounds__(512) void k_conv_col8(const uint64_t *__restrict__ 
             for (int i = 0; i < 8; i++) {
                 if (EXACT || i < ns) {
                     acc += ar.mul(y[k][i], s_mod[i * nt + tt]);
-                    if ((i & 3) == 3) acc = ar.red(acc);
+                    if ((i & 7) == 7 && i + 1 < ns) acc = ar.red(acc);
                 }
             }
             x[k] = ar.red(acc);
