@@ -4,9 +4,11 @@ digits and as a run-time loop beyond, so both forms are compared with the oracle
 
 * 13 + 4 limbs, dnum 4 (alpha 4): 4 digits at level 12 (the compile-time form), 2 at level 5;
 * 13 + 2 limbs, dnum 7 (alpha 2): 7 digits at level 12 (the run-time loop), 5 at level 9;
+* 16 + 8 limbs, dnum 2 (alpha 8): one digit at levels 7 and 2 (the single-digit form);
 
 each for hoisted rotations with stored keys and with seed-expanded keys, and for a 256 x 512 projection slice with
-the lazy ModDown (whose accumulating inner product sums the giant-step rotations) at level 12.
+the lazy ModDown (whose accumulating inner product sums the giant-step rotations) at level 12 (level 7 for the
+single digit).
 """
 import dataclasses
 
@@ -20,7 +22,7 @@ from workloads import PROJECTION, gaussian_error, rng, ternary_secret, uniform_r
 pytestmark = pytest.mark.gpu
 
 # (name, n_q, n_p, dnum, levels to rotate at)
-CASES = [("dnum4", 13, 4, 4, (12, 5)), ("dnum7", 13, 2, 7, (12, 9))]
+CASES = [("dnum4", 13, 4, 4, (12, 5)), ("dnum7", 13, 2, 7, (12, 9)), ("one_digit", 16, 8, 2, (7, 2))]
 
 
 def eq(dev, host, what):
@@ -87,8 +89,9 @@ def test_rotate_hoisted_many_digits(case, seeded):
 @pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
 def test_projection_lazy_moddown_many_digits(case):
     from test_gpu_project import run_case
-    name, n_q, n_p, dnum, _ = case
-    cfg = dataclasses.replace(PROJECTION, name="projection_" + name, n_q=n_q, n_p=n_p, dnum=dnum)
+    name, n_q, n_p, dnum, levels = case
+    level = max(levels) if name == "one_digit" else PROJECTION.level
+    cfg = dataclasses.replace(PROJECTION, name="projection_" + name, n_q=n_q, n_p=n_p, dnum=dnum, level=level)
     say("lazy projection slice", name, "digits", n_digits(cfg.level, n_q, dnum))
     err = run_case(cfg, 256, 512, [1], lazy=True)
     say("lazy slice", name, "max error vs X@W", err)
