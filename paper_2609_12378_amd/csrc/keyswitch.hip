@@ -600,8 +600,8 @@ __global__ __launch_bounds__(64) void k_key_ip_intt8(RotArgs ra, uint64_t *up, u
 // of the key inner product u_k = sum_j sigma_{g_r}(d_j)[i] * key_r[j][k][i] in registers, and writes
 //   out_r[k][i] = (u_k - NTT(cw[r][k][i])) * P^-1 (+ sigma_{g_r}(c0)[i] for k = 0),
 // so neither the q-limb rows of u nor the transformed conversion ever go to HBM.  Magnitudes (units of q):
-// transform outputs <= 2.5 (row pass after a reducing first pass), each product <= 0.875 and the sum range-reduced
-// every 4 digits (<= 4), differences <= 6.5, P^-1 products <= 3, plus c0 < 1: all below 8 q = 2^53.
+// column-pass outputs <= 4.3 (from inputs reduced to q/2), transform outputs <= 2.6, each product <= 0.875 and the
+// sum range-reduced every 4 digits (<= 4), differences <= 6.6, P^-1 products <= 3, plus c0 < 1: all below 8 q = 2^53.
 __global__ __launch_bounds__(64) void k_ks_finish8(RotArgs ra, const uint64_t *__restrict__ cw, uint32_t nd,
                                                    uint32_t ext,
                                                    uint32_t L, uint32_t key_rows, const ModQ *__restrict__ mods,

@@ -280,11 +280,12 @@ size_t lds_bytes(uint32_t subs)
 // size, carries a relative error of 2^-52, and |l| <= ulp(h)/2); red(x) returns
 // <= 0.5 + 2^-52 |x|.  So a reducing stage maps a bound b on its inputs to
 // 1 + 0.375 b and a lazy one to 1.375 b + 0.5.  The projection uses RMASK =
-// 0x50 for the column pass (inputs reduced, <= 0.5; largest value 4.3, output
-// <= 4.3) and 0xAA for the row pass (inputs <= 4.3; largest 3.9, output <= 2.6),
+// 0x50 for the column pass (inputs reduced, <= 0.5; largest value 5.3, output
+// <= 4.3) and 0xAA for the row pass (inputs <= 4.3; largest 6.4, output <= 2.6),
 // then accumulates products of the outputs (each <= 1.5) four at a time onto a
 // reduced sum: every value stays below 6.4 q < 2^53, so all arithmetic is exact
-// integer arithmetic on doubles.
+// integer arithmetic on doubles.  No pair of masks with fewer reducing stages
+// in total keeps these bounds below 7.9 q.
 constexpr int kE8 = 8;
 constexpr uint32_t kTr8 = 287;
 constexpr unsigned kColMask8 = 0x50, kRowMask8 = 0xAA;

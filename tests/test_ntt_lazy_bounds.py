@@ -51,3 +51,46 @@ def test_masks_are_lazy_somewhere():
 def test_a_wrong_mask_is_caught():
     # every stage lazy in a 256-point column pass overflows the exact range
     assert run(1.0, 0x00, 8)[1] > 8
+
+
+CORE = os.path.join(os.path.dirname(__file__), "..", "paper_2609_12378_amd", "csrc", "ntt_core.h")
+
+
+def masks8():
+    """kColMask8 and kRowMask8 of csrc/ntt_core.h: the 8-residue passes of the projection and key switching."""
+    m = re.search(r"constexpr unsigned kColMask8 = (0x[0-9a-fA-F]+), kRowMask8 = (0x[0-9a-fA-F]+);",
+                  open(CORE).read())
+    return int(m.group(1), 16), int(m.group(2), 16)
+
+
+def test_eight_residue_masks_and_their_consumers():
+    """Column pass from inputs reduced to q/2, then the row pass; the consumers of the row pass's outputs: the
+    multiply-accumulate (four products onto a reduced sum) and the fused ModDown (digit products reduced every
+    four terms, minus the transformed conversion, times P^-1)."""
+    col, row = masks8()
+    out_c, peak_c = run(0.5, col, 8)
+    out_r, peak_r = run(out_c, row, 8)
+    assert peak_c < 8 and peak_r < 8, (peak_c, peak_r)
+    prod = 0.5 + 0.375 * out_r
+    assert 0.5 + 4 * prod < 8                        # k_row_mac8's sums
+    diff = 0.5 + 4 * 0.875 + out_r                   # k_ks_finish8: u - v
+    assert diff < 8 and 0.5 + 0.375 * diff + 1 < 8    # (u - v) P^-1 + c0
+    # the bounds the kernels' comments state
+    assert out_c < 4.3 and peak_c < 5.3 and out_r < 2.6 and peak_r < 6.4 and 0.5 + 4 * prod < 6.4
+
+
+def test_eight_residue_masks_are_minimal():
+    """No pair of masks with fewer reducing stages in total keeps the same bounds below 7.9 q (the best such pair
+    leaves the multiply-accumulate's sums within 0.5% of the exact range)."""
+    col, row = masks8()
+    used = bin(col).count("1") + bin(row).count("1")
+    for c in range(256):
+        oc, pc = run(0.5, c, 8)
+        if pc >= 7.9:
+            continue
+        for r in range(256):
+            if bin(c).count("1") + bin(r).count("1") >= used:
+                continue
+            orr, pr = run(oc, r, 8)
+            ok = pr < 7.9 and 0.5 + 4 * (0.5 + 0.375 * orr) < 7.9 and 4.0 + orr < 7.9
+            assert not ok, (hex(c), hex(r))
