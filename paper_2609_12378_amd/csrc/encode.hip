@@ -223,7 +223,8 @@ __global__ __launch_bounds__(512) void ntt_col8_from_fft(const double2 *__restri
                                                          uint32_t limbs, const ModQ *__restrict__ mods,
                                                          const double *__restrict__ twf,
                                                          const double2 *__restrict__ fw,
-                                                         const double2 *__restrict__ twist, double cs)
+                                                         const double2 *__restrict__ twist, double cs,
+                                                         int64_t small)
 {
     using nttc::kE8;
     constexpr uint32_t log_n = 16, M = 1u << 15, MT_PITCH = 17;
@@ -289,20 +290,27 @@ __global__ __launch_bounds__(512) void ntt_col8_from_fft(const double2 *__restri
     const uint32_t col = tid & 15u, t = tid >> 4;
     const size_t coff = c0 + col;
     double vd[kE8];
-    bool big = false;
+    bool big = false, wide = false;
 #pragma unroll
     for (int k = 0; k < kE8; k++) {
         const int64_t v = mt[nttc::u8<0>(t, k) * MT_PITCH + col];
         big |= v > (1ll << 52) || v < -(1ll << 52);
+        wide |= v > small || v < -small;
         vd[k] = (double)v;
     }
+    // every coefficient of the wave below every limb's q/2 (weights at the usual scales): its range reduction is
+    // the identity, so the wave skips it for all limbs
+    const bool reduce = __any(wide);
     for (uint32_t l = 0; l < limbs; l++) {
         const ModQ md = mods[l];
         const nttc::Ar<true> ar(md);
         double wnext = 0.0;
         if (l + 1 < limbs && tid < 255) wnext = twf[((size_t)(l + 1) << log_n) + tid + 1];
         double x[kE8];
-        if (!big) {
+        if (!reduce) {
+#pragma unroll
+            for (int k = 0; k < kE8; k++) x[k] = vd[k];
+        } else if (!big) {
 #pragma unroll
             for (int k = 0; k < kE8; k++) x[k] = ar.red(vd[k]);
         } else {
@@ -522,7 +530,7 @@ ckks_status enc_ntt_first_pass(ckks_ctx *ctx, const SlotSource &src, uint32_t ba
     prof_begin(ctx, K_NTT_FWD_COL, batch * 8.0 * ctx->n * (1 + limbs),
                res * ((2 * kOpsButterflyF64 + 6 * (kOpsButterflyF64 - 3)) / 2 + 3.0));
     hipLaunchKernelGGL(ntt_col8_from_fft, dim3(batch * 16), dim3(512), 0, ctx->stream, work, out, limbs, ctx->d_mod,
-                       ctx->d_twf, ctx->d_fft_w, ctx->d_fft_twist, c);
+                       ctx->d_twf, ctx->d_fft_w, ctx->d_fft_twist, c, identity_reduction_bound(ctx, limbs));
     prof_end(ctx, K_NTT_FWD_COL);
     HIP_TRY(hipGetLastError());
     return CKKS_OK;

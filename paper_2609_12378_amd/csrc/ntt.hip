@@ -207,7 +207,7 @@ __global__ __launch_bounds__(256) void ntt_col_from_i64(const int64_t *__restric
 // table while limb l is transformed.
 __global__ __launch_bounds__(512) void ntt_col8_from_i64(const int64_t *__restrict__ m, uint64_t *out,
                                                          uint32_t limbs, const ModQ *mods, const double *twf,
-                                                         uint32_t log_n, uint32_t blocks_per_row)
+                                                         uint32_t log_n, uint32_t blocks_per_row, int64_t small)
 {
     using nttc::kE8;
     __shared__ double tws[2][256];
@@ -221,12 +221,15 @@ __global__ __launch_bounds__(512) void ntt_col8_from_i64(const int64_t *__restri
 #pragma unroll
     for (int k = 0; k < kE8; k++) v[k] = src[(size_t)nttc::u8<0>(t, k) * n2];
     double vd[kE8];
-    bool big = false;
+    bool big = false, wide = false;
 #pragma unroll
     for (int k = 0; k < kE8; k++) {
         big |= v[k] > (1ll << 52) || v[k] < -(1ll << 52);
+        wide |= v[k] > small || v[k] < -small;
         vd[k] = (double)v[k];
     }
+    // coefficients below every limb's q/2 throughout the wave: the range reduction is the identity, skipped
+    const bool reduce = __any(wide);
     if (threadIdx.x < 255) tws[0][threadIdx.x + 1] = twf[threadIdx.x + 1];
     __syncthreads();
     for (uint32_t l = 0; l < limbs; l++) {
@@ -237,7 +240,10 @@ __global__ __launch_bounds__(512) void ntt_col8_from_i64(const int64_t *__restri
         double wnext = 0.0;
         if (l + 1 < limbs && threadIdx.x < 255) wnext = twf[((size_t)(l + 1) << log_n) + threadIdx.x + 1];
         double x[kE8];
-        if (!big) {
+        if (!reduce) {
+#pragma unroll
+            for (int k = 0; k < kE8; k++) x[k] = vd[k];
+        } else if (!big) {
 #pragma unroll
             for (int k = 0; k < kE8; k++) x[k] = ar.red(vd[k]);
         } else {
@@ -553,6 +559,15 @@ ckks_status launch_ntt_inv_second_pass(ckks_ctx *ctx, uint64_t *data, uint32_t b
 
 bool ntt_uses_f64(const ckks_ctx *ctx, uint32_t limbs) { return use_f64(ctx, limb_range(0, limbs)); }
 
+// The largest s such that the fp64 range reduction x - q rint(x / q) returns x itself for every |x| <= s and every
+// prime q_0 .. q_{limbs-1}: |x| <= q/2 - 1.5 keeps |x / q| below 1/2 (with the rounding of 1/q), so rint gives 0.
+int64_t identity_reduction_bound(const ckks_ctx *ctx, uint32_t limbs)
+{
+    uint64_t qmin = ~0ull;
+    for (uint32_t l = 0; l < limbs; l++) qmin = ctx->primes[l] < qmin ? ctx->primes[l] : qmin;
+    return limbs ? (int64_t)((qmin - 3) / 2) : 0;
+}
+
 // First (column) pass only of the forward NTT of m[batch][N] into out[batch][limbs][N]; the rows are left in the
 // inter-pass form of the arithmetic ntt_uses_f64 selects.  Needs a two-pass size (s1 > 0).
 ckks_status launch_ntt_col_i64(ckks_ctx *ctx, const int64_t *m, uint64_t *out, uint32_t batch, uint32_t limbs)
@@ -572,7 +587,7 @@ ckks_status launch_ntt_col_i64(ckks_ctx *ctx, const int64_t *m, uint64_t *out, u
     if (f && s1 == 8) {
         const uint32_t bpr = (ctx->n >> 8) / 16;
         hipLaunchKernelGGL(ntt_col8_from_i64, dim3(batch * bpr), dim3(512), 0, ctx->stream, m, out, limbs,
-                           ctx->d_mod, ctx->d_twf, ctx->log_n, bpr);
+                           ctx->d_mod, ctx->d_twf, ctx->log_n, bpr, identity_reduction_bound(ctx, limbs));
         e = hipGetLastError();
     } else {
         e = f ? dispatch_col_i64<true>(s1, ctx, m, out, batch, limbs)

@@ -90,6 +90,8 @@ ckks_status enc_coeffs(ckks_ctx *ctx, const SlotSource &src, uint32_t batch, dou
 // FFT pass A into work, then pass B, twist, rounding and the column transforms of every limb in one kernel;
 // out: [batch][limbs][N] in the inter-pass form of launch_ntt_col_i64
 bool enc_fused_ok(const ckks_ctx *ctx, uint32_t limbs);
+// bound below which the fp64 range reduction modulo every prime q_0 .. q_{limbs-1} is the identity
+int64_t identity_reduction_bound(const ckks_ctx *ctx, uint32_t limbs);
 ckks_status enc_ntt_first_pass(ckks_ctx *ctx, const SlotSource &src, uint32_t batch, double scale, double2 *work,
                                uint32_t limbs, uint64_t *out);
 // out[x] = (slot index held at FFT position x) / tokens, x < N/2
