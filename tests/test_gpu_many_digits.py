@@ -5,6 +5,8 @@ digits and as a run-time loop beyond, so both forms are compared with the oracle
 * 13 + 4 limbs, dnum 4 (alpha 4): 4 digits at level 12 (the compile-time form), 2 at level 5;
 * 13 + 2 limbs, dnum 7 (alpha 2): 7 digits at level 12 (the run-time loop), 5 at level 9;
 * 16 + 8 limbs, dnum 2 (alpha 8): one digit at levels 7 and 2 (the single-digit form);
+* 56 + 8 limbs, dnum 7 (alpha 8): the largest context the library accepts (64 primes), 7 digits over 64 extended
+  rows at the top level 55 and 3 digits at level 20 (rotations only);
 
 each for hoisted rotations with stored keys and with seed-expanded keys, and for a 256 x 512 projection slice with
 the lazy ModDown (whose accumulating inner product sums the giant-step rotations) at level 12 (level 7 for the
@@ -22,7 +24,8 @@ from workloads import PROJECTION, gaussian_error, rng, ternary_secret, uniform_r
 pytestmark = pytest.mark.gpu
 
 # (name, n_q, n_p, dnum, levels to rotate at)
-CASES = [("dnum4", 13, 4, 4, (12, 5)), ("dnum7", 13, 2, 7, (12, 9)), ("one_digit", 16, 8, 2, (7, 2))]
+CASES = [("dnum4", 13, 4, 4, (12, 5)), ("dnum7", 13, 2, 7, (12, 9)), ("one_digit", 16, 8, 2, (7, 2)),
+         ("max_primes", 56, 8, 7, (55, 20))]
 
 
 def eq(dev, host, what):
@@ -86,7 +89,7 @@ def test_rotate_hoisted_many_digits(case, seeded):
         assert np.max(np.abs(to_host(dre) - np.roll(re, -steps[-1]))) < 2.0 ** -18
 
 
-@pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
+@pytest.mark.parametrize("case", CASES[:3], ids=[c[0] for c in CASES[:3]])
 def test_projection_lazy_moddown_many_digits(case):
     from test_gpu_project import run_case
     name, n_q, n_p, dnum, levels = case
