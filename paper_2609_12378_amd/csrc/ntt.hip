@@ -284,7 +284,10 @@ __global__ __launch_bounds__(512) void ntt_col8_from_i64(const int64_t *__restri
 // Row pass over N2 = 2^LOGS contiguous points of row h, twiddle base N1 + h.
 // FIRST: input is canonical residues; LAST: write canonical residues (and, for
 // the inverse, multiply by N^-1).
-template <int LOGS, bool INV, bool FIRST, bool LAST, bool F, int LOGN = 0>
+// SHARE (N = 2^16 only): the block's 8 sub-transforms are the same row h of 8 consecutive batch entries of one
+// limb, so they use the same twiddles (one table row read per block instead of eight); blocks run (batch octet,
+// limb, h) in memory order.
+template <int LOGS, bool INV, bool FIRST, bool LAST, bool F, int LOGN = 0, bool SHARE = false>
 __global__ __launch_bounds__(LOGN ? 128 : 256) void ntt_row(uint64_t *data, LimbMap map, uint32_t bstride,
                                                              const ModQ *mods, const void *tw_all,
                                                              uint32_t log_n_arg, uint32_t rows_arg, uint32_t bpp_arg)
@@ -300,14 +303,23 @@ __global__ __launch_bounds__(LOGN ? 128 : 256) void ntt_row(uint64_t *data, Limb
     extern __shared__ uint64_t lds_raw[];
     E *lds = LOGN ? lds_static : (E *)lds_raw;
     uint32_t slot;
-    const size_t poly = row_of_block(blockIdx.x / blocks_per_poly, map.n, bstride, &slot);
-    const uint32_t blk = blockIdx.x % blocks_per_poly;
+    size_t poly;
+    uint32_t h;
+    const uint32_t n1 = 1u << (log_n - LOGS);
+    const uint32_t sub = threadIdx.x / TS, r = threadIdx.x % TS;
+    if constexpr (SHARE) {
+        static_assert(!SHARE || (LOGN == 16 && LOGS == 8), "shared-twiddle rows: N = 2^16 only");
+        h = blockIdx.x % n1;
+        const uint32_t rest = blockIdx.x / n1;
+        slot = rest % map.n;
+        poly = (size_t)(8 * (rest / map.n) + sub) * bstride + slot;
+    } else {
+        poly = row_of_block(blockIdx.x / blocks_per_poly, map.n, bstride, &slot);
+        h = (blockIdx.x % blocks_per_poly) * rows_per_block + sub;
+    }
     const uint32_t prime = map.prime[slot];
     const Ar<F> ar(mods[prime]);
     const typename Ar<F>::W *tw = twp<F>(tw_all, prime, log_n);
-    const uint32_t n1 = 1u << (log_n - LOGS);
-    const uint32_t sub = threadIdx.x / TS, r = threadIdx.x % TS;
-    const uint32_t h = blk * rows_per_block + sub;
     uint64_t *base = data + (poly << log_n) + (size_t)h * S;
     const uint32_t B = n1 + h;
     E x[kE];
@@ -381,6 +393,14 @@ hipError_t launch_row(ckks_ctx *ctx, uint64_t *data, uint32_t batch, uint32_t bs
     const uint32_t bpp = n1 / rows;
     const dim3 grid(batch * map.n * bpp), block(rows * TS);
     const void *tw = INV ? inv_table<F>(ctx) : fwd_table<F>(ctx);
+    if constexpr (LOGS == 8) {
+        // batches of whole octets: each block's 8 rows share their twiddles
+        if (ctx->log_n == 16 && batch % 8 == 0) {
+            hipLaunchKernelGGL((ntt_row<LOGS, INV, FIRST, LAST, F, 16, true>), grid, block, 0, ctx->stream, data, map,
+                               bstride, ctx->d_mod, tw, ctx->log_n, rows, bpp);
+            return hipGetLastError();
+        }
+    }
     if (LOGS == 8 && ctx->log_n == 16)
         hipLaunchKernelGGL((ntt_row<LOGS, INV, FIRST, LAST, F, 16>), grid, block, 0, ctx->stream, data, map, bstride,
                            ctx->d_mod, tw, ctx->log_n, rows, bpp);
