@@ -44,10 +44,13 @@ struct ConvArgs {
 // in: [polys][ns][N] (stride in_stride rows between polys), coefficient form;
 // out row for target ti: out + (poly*out_stride + (ti < split ? ti : ti + skip)) * N.
 // A digit y_i > q_i/2 stands for y_i - q_i, so the centred sum is the sum of the
-// canonical digits plus neg * [-Q_I]_t, neg the number of such digits.  The
-// Shoup constants and the target moduli are staged in LDS once per block, so the
-// per-target loop reads them at LDS latency instead of waiting on scalar memory
-// loads.
+// canonical digits plus neg * [-Q_I]_t, neg the number of such digits.  Each
+// target's sum is accumulated exactly in 128 bits (products below 2^124; eight of
+// them and a residue below 2^128) and reduced once per eight sources, which costs
+// fewer 32-bit multiplies than a Shoup product and a conditional subtraction per
+// term.  The constants and the target moduli are staged in LDS once per block, so
+// the per-target loop reads them at LDS latency instead of waiting on scalar
+// memory loads.
 template <int NS_MAX>
 __global__ __launch_bounds__(kThreads) void k_conv(const uint64_t *in, uint32_t in_stride, uint64_t *out,
                                                     uint32_t out_stride, uint32_t split, uint32_t skip, ConvArgs a,
@@ -56,14 +59,14 @@ __global__ __launch_bounds__(kThreads) void k_conv(const uint64_t *in, uint32_t 
                                                     const ulonglong2 *__restrict__ neg_q,
                                                     const ModQ *__restrict__ mods, uint32_t log_n)
 {
-    __shared__ ulonglong2 s_mod[NS_MAX * kMaxPrimes];
-    __shared__ ulonglong2 s_neg[kMaxPrimes];
-    __shared__ uint64_t s_tq[kMaxPrimes];
+    __shared__ uint64_t s_mod[NS_MAX * kMaxPrimes];
+    __shared__ uint64_t s_neg[kMaxPrimes];
+    __shared__ ModQ s_tm[kMaxPrimes];
     const int ns = a.ns, nt = a.nt;
-    for (int k = threadIdx.x; k < ns * nt; k += kThreads) s_mod[k] = qhat_mod[k];
+    for (int k = threadIdx.x; k < ns * nt; k += kThreads) s_mod[k] = qhat_mod[k].x;
     for (int k = threadIdx.x; k < nt; k += kThreads) {
-        s_tq[k] = mods[a.dst[k]].q;
-        s_neg[k] = neg_q[k];
+        s_tm[k] = mods[a.dst[k]];
+        s_neg[k] = neg_q[k].x;
     }
     __syncthreads();
     const uint32_t n = 1u << log_n;
@@ -84,18 +87,18 @@ __global__ __launch_bounds__(kThreads) void k_conv(const uint64_t *in, uint32_t 
     }
     uint64_t *dst = out + ((size_t)poly * out_stride << log_n) + col;
     for (int t = 0; t < nt; t++) {
-        const uint64_t qt = s_tq[t], two = 2 * qt;
-        const ulonglong2 wn = s_neg[t];
-        uint64_t acc = shoup_lazy(neg, wn.x, wn.y, qt);
+        const ModQ mt = s_tm[t];
+        acc128 acc{0, 0};
+        mac(acc, neg, s_neg[t]);
 #pragma unroll
         for (int i = 0; i < NS_MAX; i++) {
             if (i < ns) {
-                const ulonglong2 w = s_mod[i * nt + t];
-                acc = csub(acc + shoup_lazy(y[i], w.x, w.y, qt), two);
+                mac(acc, y[i], s_mod[i * nt + t]);
+                if ((i & 7) == 7 && i + 1 < ns) acc = acc128{reduce128(acc, mt), 0};
             }
         }
         const uint32_t row = t < (int)split ? t : t + skip;
-        dst[(size_t)row << log_n] = csub(acc, qt);
+        dst[(size_t)row << log_n] = reduce128(acc, mt);
     }
 }
 
@@ -423,8 +426,10 @@ __device__ __forceinline__ void key_ip8(const RotArgs &ra, uint32_t r, uint32_t 
 }
 
 // u[r][k][row - row0][n] = sum_j d_j[row][sigma_{g_r}(n)] * key_r[j][k][krow][n] for rows row0 .. row0 + rows - 1
-// of Q_level u P (u holds `rows` rows per polynomial)
-template <bool SEEDED>
+// of Q_level u P (u holds `rows` rows per polynomial).  ND > 0 (stored keys): the digit count at compile time, and
+// every digit's gather and key words are loaded before the first product (3 ND loads in flight per thread instead
+// of 3); the products are summed in the same order either way.
+template <bool SEEDED, int ND = 0>
 __global__ __launch_bounds__(kThreads) void k_key_ip_batch(RotArgs ra, uint64_t *u, uint32_t nd, uint32_t ext,
                                                             uint32_t level,
                                                             uint32_t n_q, uint32_t key_rows, uint32_t row0,
@@ -441,14 +446,56 @@ __global__ __launch_bounds__(kThreads) void k_key_ip_batch(RotArgs ra, uint64_t 
     KeyRow<SEEDED> kr(ra, r, key_rows, log_n, prime, col, m.q);
     const uint64_t *digits = ra.dig[r];
     acc128 a0{0, 0}, a1{0, 0};
-    for (uint32_t j = 0; j < nd; j++) {
-        const uint64_t d = digits[(((size_t)j * ext + row) << log_n) + sc];
-        mac(a0, d, kr.b(j));
-        mac(a1, d, kr.a(j));
+    if constexpr (ND > 0 && !SEEDED) {
+        uint64_t dv[ND], bv[ND], av[ND];
+#pragma unroll
+        for (int j = 0; j < ND; j++) {
+            dv[j] = digits[(((size_t)j * ext + row) << log_n) + sc];
+            bv[j] = kr.b(j);
+            av[j] = kr.a(j);
+        }
+#pragma unroll
+        for (int j = 0; j < ND; j++) {
+            mac(a0, dv[j], bv[j]);
+            mac(a1, dv[j], av[j]);
+        }
+    } else {
+        for (uint32_t j = 0; j < nd; j++) {
+            const uint64_t d = digits[(((size_t)j * ext + row) << log_n) + sc];
+            mac(a0, d, kr.b(j));
+            mac(a1, d, kr.a(j));
+        }
     }
     uint64_t *ur = u + (((size_t)r * 2 * rows + (row - row0)) << log_n) + col;
     ur[0] = reduce128(a0, m);
     ur[(size_t)rows << log_n] = reduce128(a1, m);
+}
+
+// k_key_ip_batch with stored keys: the digit count as a template argument for 1..6 digits, the loop beyond
+template <int ND>
+void launch_key_ip_batch_nd(dim3 grid, dim3 block, hipStream_t st, const RotArgs &ra, uint64_t *u, uint32_t nd,
+                            uint32_t ext, uint32_t level, uint32_t n_q, uint32_t key_rows, uint32_t row0,
+                            uint32_t rows, const ModQ *mods, uint32_t log_n)
+{
+    hipLaunchKernelGGL((k_key_ip_batch<false, ND>), grid, block, 0, st, ra, u, nd, ext, level, n_q, key_rows, row0,
+                       rows, mods, log_n);
+}
+
+void launch_key_ip_batch_stored(dim3 grid, dim3 block, hipStream_t st, const RotArgs &ra, uint64_t *u, uint32_t nd,
+                                uint32_t ext, uint32_t level, uint32_t n_q, uint32_t key_rows, uint32_t row0,
+                                uint32_t rows, const ModQ *mods, uint32_t log_n)
+{
+#define CK_IPB(K) launch_key_ip_batch_nd<K>(grid, block, st, ra, u, nd, ext, level, n_q, key_rows, row0, rows, mods, log_n)
+    switch (nd) {
+    case 1: CK_IPB(1); break;
+    case 2: CK_IPB(2); break;
+    case 3: CK_IPB(3); break;
+    case 4: CK_IPB(4); break;
+    case 5: CK_IPB(5); break;
+    case 6: CK_IPB(6); break;
+    default: CK_IPB(0); break;
+    }
+#undef CK_IPB
 }
 
 // Lazy ModDown: the key inner products of several rotations summed over Q_level u P before one division by P.
@@ -948,8 +995,8 @@ ckks_status ks_rotate_batch(ckks_ctx *ctx, uint32_t level, uint32_t count, const
                 hipLaunchKernelGGL(k_key_ip_batch<true>, grid, block, 0, ctx->stream, ra, up, nd, ext, level,
                                    ctx->n_q, kp, L, K, ctx->d_mod, ctx->log_n);
             else
-                hipLaunchKernelGGL(k_key_ip_batch<false>, grid, block, 0, ctx->stream, ra, up, nd, ext, level,
-                                   ctx->n_q, kp, L, K, ctx->d_mod, ctx->log_n);
+                launch_key_ip_batch_stored(grid, block, ctx->stream, ra, up, nd, ext, level, ctx->n_q, kp, L, K,
+                                           ctx->d_mod, ctx->log_n);
             prof_end(ctx, K_KEYIP);
             HIP_TRY(hipGetLastError());
             CK_TRY(launch_ntt_strided(ctx, up, 2 * count, K, limb_range(ctx->n_q, K), true));
@@ -990,8 +1037,8 @@ ckks_status ks_rotate_batch(ckks_ctx *ctx, uint32_t level, uint32_t count, const
             hipLaunchKernelGGL(k_key_ip_batch<true>, grid, block, 0, ctx->stream, ra, u, nd, ext, level, ctx->n_q,
                                kp, 0u, ext, ctx->d_mod, ctx->log_n);
         else
-            hipLaunchKernelGGL(k_key_ip_batch<false>, grid, block, 0, ctx->stream, ra, u, nd, ext, level, ctx->n_q,
-                               kp, 0u, ext, ctx->d_mod, ctx->log_n);
+            launch_key_ip_batch_stored(grid, block, ctx->stream, ra, u, nd, ext, level, ctx->n_q, kp, 0u, ext,
+                                       ctx->d_mod, ctx->log_n);
         prof_end(ctx, K_KEYIP);
         HIP_TRY(hipGetLastError());
     }
