@@ -84,7 +84,10 @@ typedef struct {
  * finds psi_k (x^((q-1)/2N) for the smallest x >= 2 with psi^N = -1), and
  * uploads twiddle, Shoup-companion, FFT and basis-conversion tables (the
  * latter for ModUp and ModDown at every level).
- * hip_stream: the hipStream_t all calls are enqueued on (NULL = default). */
+ * hip_stream: the hipStream_t all calls are enqueued on (NULL = default).
+ * CKKS_EUNSUPPORTED also when dnum + 1 products of residues below the largest
+ * prime exceed an exact 128-bit sum (the integer key inner products): with
+ * 62-bit primes dnum is at most 15, below 2^60 at most 255. */
 ckks_status ckks_ctx_create(const ckks_params *params, void *hip_stream, ckks_ctx **out);
 void ckks_ctx_destroy(ckks_ctx *ctx);
 ckks_status ckks_ctx_set_stream(ckks_ctx *ctx, void *hip_stream);

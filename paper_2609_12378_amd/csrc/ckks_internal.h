@@ -86,6 +86,7 @@ struct ckks_ctx {
     bool int_only = false;               // force the integer Shoup butterflies
     uint32_t proj_max_pairs = 0;         // projection sub-batch limit (0 = by the staging budget)
     bool lazy_moddown = false;           // sums of rotations with one ModDown per output
+    uint32_t sum128_terms = 0;           // products of two residues an exact 128-bit sum holds (with a residue)
     double2 *d_fft_w = nullptr;          // [N/4]  omega^-e, omega = exp(2 pi i/(N/2))
     double2 *d_fft_wc = nullptr;         // [2048] stage-by-stage copy for 2048-point blocks (N >= 2^12)
     double2 *d_fft_twist = nullptr;      // [N/2]  zeta^-k, zeta = exp(i pi / N)

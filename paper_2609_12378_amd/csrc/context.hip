@@ -434,6 +434,20 @@ ckks_status ckks_ctx_create(const ckks_params *p, void *stream, ckks_ctx **out)
         hipError_t e = hipGetDevice(&c->device);
         if (e != hipSuccess) st = set_error(CKKS_EHIP, "hipGetDevice: %s", hipGetErrorString(e));
     }
+    if (st == CKKS_OK) {
+        // the integer kernels sum products of two residues exactly in 128 bits: at most sum128_terms of them
+        // (each below (q - 1)^2) together with one residue below q, for the largest prime q of the context
+        uint64_t qmax = 0;
+        for (uint64_t q : c->primes) qmax = q > qmax ? q : qmax;
+        const unsigned __int128 sq = (unsigned __int128)(qmax - 1) * (qmax - 1);
+        const unsigned __int128 room = ~(unsigned __int128)0 - qmax;
+        const unsigned __int128 t = sq ? room / sq : (unsigned __int128)1 << 30;
+        c->sum128_terms = t > ((unsigned __int128)1 << 30) ? 1u << 30 : (uint32_t)t;
+        // a key inner product sums dnum products (one more for the c0 term of a lazy sum)
+        if (c->dnum + 1 > c->sum128_terms)
+            st = set_error(CKKS_EUNSUPPORTED, "dnum %u: %u products of residues below 2^%d exceed an exact 128-bit sum",
+                           c->dnum, c->dnum + 1, 64 - __builtin_clzll(qmax));
+    }
     if (st == CKKS_OK) st = build_tables(c);
     if (st == CKKS_OK) st = build_all_conv(c);
     if (st == CKKS_OK) noalloc_setup(c->device);

@@ -17,6 +17,8 @@
 // ns + ns*nt + nt Shoup multiplications per coefficient.  The inner dimension
 // (ns <= 8 at the benchmark parameters) is far too small and too wide-integer
 // for the matrix cores, so it runs on the vector ALUs.
+#include <algorithm>
+
 #include "ckks_internal.h"
 #include "ntt_core.h"
 #include "ops.h"
@@ -1064,6 +1066,17 @@ ckks_status ks_ip_accumulate(ckks_ctx *ctx, uint32_t level, uint32_t count, cons
 {
     CK_REQUIRE(count >= 1 && count <= (uint32_t)kRotBatch, CKKS_EINVAL, "rotation batch of %u", count);
     const uint32_t L = level + 1, ext = L + ctx->n_p, nd = n_digits(ctx, level);
+    // one accumulator summing every rotation takes count (nd + 1) products in its exact 128-bit sum: with large
+    // primes, fewer rotations per launch, the later launches adding to the reduced sum
+    const uint32_t per = std::max(1u, ctx->sum128_terms / (nd + 1));
+    if (sum_all && count > per) {
+        for (uint32_t r0 = 0; r0 < count; r0 += per) {
+            const uint32_t cnt = std::min(per, count - r0);
+            CK_TRY(ks_ip_accumulate(ctx, level, cnt, c0s + r0, digs + r0, g + r0, keys + r0, accs, true,
+                                    accumulate || r0 > 0));
+        }
+        return CKKS_OK;
+    }
     RotArgs ra{};
     ra.count = count;
     for (uint32_t r = 0; r < count; r++) {

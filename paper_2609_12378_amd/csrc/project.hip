@@ -366,6 +366,8 @@ ProjScratch proj_scratch(const ckks_ctx *ctx, uint32_t L, uint32_t D, uint32_t d
     const size_t budget = size_t(24) << 30;
     uint32_t Pmax = std::min<uint32_t>(maxpairs, std::max<uint32_t>(1, (uint32_t)(budget / ((size_t)kJt * L * N * 8))));
     if (ctx->proj_max_pairs) Pmax = std::min(Pmax, ctx->proj_max_pairs);
+    // k_mac sums one product per pair in each exact 128-bit accumulator
+    if (kJt == kJ) Pmax = std::min(Pmax, ctx->sum128_terms);
     ps.Pb = Pmax;
     ps.xrot_w = (size_t)n_in * n1 * ctw;
     ps.acc_w = ps.tot_w = ps.rot_w = (size_t)kJt * ctw;

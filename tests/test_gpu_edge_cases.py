@@ -6,6 +6,8 @@
 * Empty calls: an NTT of zero polynomials and a hoisted rotation of zero steps do nothing and succeed.
 * An all-zero slot vector encodes to the zero plaintext; a zero weight matrix projects an encryption to a
   ciphertext that decrypts to zero within the noise.
+* A context whose integer key inner products would overflow their exact 128-bit sums (62-bit primes, dnum 16) is
+  refused at creation.
 """
 import dataclasses
 
@@ -109,3 +111,13 @@ def test_zero_slots_encode_to_zero():
     pt = ctx.encode(to_dev(z), None, 2.0 ** 30, TOY.n_q)
     assert not np.any(to_host(pt.data))
     assert np.array_equal(to_host(pt.data)[0], ck.encode(z, None, 2.0 ** 30, TOY.n_q))
+
+
+def test_digit_count_beyond_exact_sums_rejected():
+    """With 62-bit primes an exact 128-bit sum holds 16 products of residues; a context whose key inner products
+    would sum more (dnum + 1 > 16) is refused at creation, and one within the bound is accepted."""
+    require_gpu()
+    from paper_2609_12378_amd import CkksError, Context
+    with pytest.raises(CkksError, match="dnum"):
+        Context(12, 32, 2, 16, q_bits=62)
+    Context(12, 30, 2, 15, q_bits=62)

@@ -4,7 +4,8 @@
   diagonal method with 127 hoisted rotations): every output ciphertext bit for bit,
   and decrypted within 2^-12 of X @ W;
 * toy ring with the integer transform arithmetic (the unfused path: separate row
-  pass and multiply-accumulate kernels);
+  pass and multiply-accumulate kernels), and with 62-bit primes (pairs per launch capped
+  so that the exact 128-bit sums cannot overflow);
 * toy ring with a baby-step/giant-step split (n1 = 16, n2 = 8), two input and 31
   output ciphertexts (a full tile of 28 output blocks and a ragged one of 3) and at
   most seven (input, baby step) pairs per launch, so partial sums are carried across
@@ -119,6 +120,16 @@ def test_toy_projection_bit_exact():
 def test_toy_projection_integer_arithmetic():
     err = run_case(TOY, TOY.d_in, TOY.d_out, [0], arith=1)
     say("toy (integer transforms) max error vs X@W", err)
+    assert err <= 2.0 ** -12
+
+
+def test_toy_projection_62_bit_primes():
+    """62-bit primes, the largest the integer path accepts: 128 (input, baby step) pairs summed in one exact
+    128-bit accumulator would overflow it (each product is near 2^124), so the library caps the pairs per
+    multiply-accumulate launch at what the sum holds (16 here) and carries the reduced sums across launches."""
+    cfg = dataclasses.replace(TOY, name="toy_62bit", q_bits=62)
+    err = run_case(cfg, TOY.d_in, TOY.d_out, [0])
+    say("toy (62-bit primes) max error vs X@W", err)
     assert err <= 2.0 ** -12
 
 
