@@ -9,7 +9,7 @@
 // Schedule on the GPU:
 //  1. hoisted baby-step rotations: one ModUp per input ciphertext, n1 - 1
 //     key switches each, into xrot[i][b] (b = 0 is a copy of x_i);
-//  2. for a tile of J output blocks (28 on the fp64 path, 14 on the integer one) and one giant step g, the weight
+//  2. for a tile of J output blocks (28 on the fp64 path, 4 on the integer one) and one giant step g, the weight
 //     plaintexts of a sub-batch of (i, b) pairs are encoded on the fly from W
 //     (slot generation fused into the fp64 FFT -> round -> NTT column pass with
 //     the RNS reduction fused in) and consumed by k_row_mac, which finishes
@@ -78,9 +78,11 @@ __global__ __launch_bounds__(kThreads) void k_mac(uint64_t *acc, const uint64_t 
     }
 }
 
-// output blocks per tile: the blocks of one tile share each xrot read; 14 (a divisor of the 56 outputs of the
-// 4096 x 14336 projection) fills the last wave of the multiply-accumulate launches best among the divisors tried
-constexpr uint32_t kJ = 14;   // output blocks per tile on the integer path (k_mac keeps them in registers)
+// output blocks per tile: the blocks of one tile share each xrot read.  On the integer path k_mac keeps a tile's
+// 128-bit accumulators in registers: 4 blocks (60 VGPRs, 8 waves per SIMD) read each xrot residue three and a half
+// times as often as 14 (140 VGPRs, 3 waves) but hide the plaintext loads better: 0.65 -> 0.43 s of
+// multiply-accumulate per 4096 x 14336 projection at the paper's moduli (7 blocks: 0.47 s)
+constexpr uint32_t kJ = 4;    // output blocks per tile on the integer path (k_mac keeps them in registers)
 constexpr uint32_t kJF = 28;  // on the fused fp64 path (one block per output: the tile only sets xrot reuse)
 
 // Row pass of the forward NTT fused with the multiply-accumulate (fp64
