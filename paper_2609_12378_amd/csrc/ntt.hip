@@ -140,10 +140,13 @@ __global__ __launch_bounds__(256) void ntt_col(uint64_t *data, LimbMap map, uint
 // out[b][l].  The RNS reduction of an encoded plaintext is thereby fused into
 // the first NTT pass: the residues of all limbs never go through HBM before the
 // transform.
+// Integer arithmetic: below every limb's prime in magnitude (weights at the usual scales), a wave's coefficients
+// are their own residues (or q plus them), so the general reduction is skipped; `small` is the smallest q - 1.
 template <int LOGS, bool F>
 __global__ __launch_bounds__(256) void ntt_col_from_i64(const int64_t *__restrict__ m, uint64_t *out, uint32_t limbs,
                                                         const ModQ *mods, const void *tw_all, uint32_t log_n,
-                                                        uint32_t cols_per_block, uint32_t blocks_per_row)
+                                                        uint32_t cols_per_block, uint32_t blocks_per_row,
+                                                        int64_t small)
 {
     using E = typename Ar<F>::E;
     constexpr uint32_t TS = (1u << LOGS) / 16;
@@ -168,6 +171,12 @@ __global__ __launch_bounds__(256) void ntt_col_from_i64(const int64_t *__restric
             vd[k] = (double)v[k];
         }
     }
+    bool wide = false;
+    if constexpr (!F) {
+#pragma unroll
+        for (int k = 0; k < kE; k++) wide |= v[k] > small || v[k] < -small;
+    }
+    const bool reduce = __any(wide);
     for (uint32_t l = 0; l < limbs; l++) {
         const ModQ md = mods[l];
         const Ar<F> ar(md);
@@ -184,6 +193,9 @@ __global__ __launch_bounds__(256) void ntt_col_from_i64(const int64_t *__restric
 #pragma unroll
                 for (int k = 0; k < kE; k++) x[k] = ar.from_i64(sg[(size_t)(r + TS * k) * n2], md);
             }
+        } else if (!reduce) {
+#pragma unroll
+            for (int k = 0; k < kE; k++) x[k] = v[k] < 0 ? (uint64_t)v[k] + md.q : (uint64_t)v[k];
         } else {
 #pragma unroll
             for (int k = 0; k < kE; k++) x[k] = ar.from_i64(v[k], md);
@@ -419,8 +431,10 @@ hipError_t launch_col_i64(ckks_ctx *ctx, const int64_t *m, uint64_t *out, uint32
     if (cols > n2) cols = n2;
     const uint32_t bpr = n2 / cols;
     const dim3 grid(batch * bpr), block(cols * TS);
+    uint64_t qmin = ~0ull;
+    for (uint32_t l = 0; l < limbs; l++) qmin = ctx->primes[l] < qmin ? ctx->primes[l] : qmin;
     hipLaunchKernelGGL((ntt_col_from_i64<LOGS, F>), grid, block, lds_bytes<LOGS>(cols), ctx->stream, m, out, limbs,
-                       ctx->d_mod, fwd_table<F>(ctx), ctx->log_n, cols, bpr);
+                       ctx->d_mod, fwd_table<F>(ctx), ctx->log_n, cols, bpr, (int64_t)(qmin - 1));
     return hipGetLastError();
 }
 
