@@ -16,7 +16,8 @@
   limbs of 50-bit primes, dnum 3, level 12, 128 tokens x 256 features, n1 = 32,
   n2 = 8 so 31 baby and 7 giant rotations) on a 256 x 512 slice of the weights
   (one input ciphertext, two output ciphertexts), bit for bit, and decrypted
-  within 2^-18 of X @ W.
+  within 2^-18 of X @ W; the same with the integer arithmetic forced (its
+  separate row pass and 128-bit multiply-accumulate).
 
 * the down-projection parameters (n1 = 8, n2 = 32: 7 baby and 31 giant rotations) on a
   512 x 256 slice (two input ciphertexts, one output), bit for bit;
@@ -164,6 +165,15 @@ def test_projection_parameters_full_degree_slice():
     say("slice max error vs X@W", err)
     # fresh noise ~2^-29, one hoisted rotation ~2^-20.5 at most over 32768 slots, 38 rotated terms summed and
     # one rescale: the oracle measures 2^-22.4 on this slice, the bound leaves a factor of 2^4
+    assert err <= 2.0 ** -18
+
+
+def test_projection_parameters_full_degree_slice_integer_arithmetic():
+    """The same slice with the integer transform arithmetic forced (50-bit primes through the Shoup butterflies,
+    the separate row pass and the 128-bit multiply-accumulate at N = 2^16)."""
+    say("full-degree slice, integer arithmetic")
+    err = run_case(PROJECTION, 256, 512, [0, 1], arith=1)
+    say("slice (integer) max error vs X@W", err)
     assert err <= 2.0 ** -18
 
 
