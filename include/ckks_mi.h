@@ -175,7 +175,10 @@ ckks_status ckks_intt(ckks_ctx *ctx, uint64_t *dev, uint32_t batch, uint32_t lim
  * limbs, NTT domain).  The integer coefficients are
  *   m_i = round(scale * (2/N) * Re sum_j z_j zeta^(-i 5^j)), zeta = e^(i pi/N),
  * rounding half away from zero, evaluated in fp64 by the radix-2 FFT whose
- * operation order the library fixes (canonical embedding of CKKS). */
+ * operation order the library fixes (canonical embedding of CKKS).  Every
+ * |m_i| must stay below 2^63, which scale * (2/N) * sum_j |z_j| < 2^63
+ * guarantees; beyond that the coefficients are unspecified (no error is
+ * reported: the slots are not read on the host). */
 ckks_status ckks_encode(ckks_ctx *ctx, const double *dev_re, const double *dev_im, double scale,
                         uint32_t n_limbs, ckks_buf *pt_out);
 /* Decode pt (n_polys = 1) at pt->scale into N/2 slots written to the device
@@ -292,7 +295,10 @@ ckks_status ckks_automorph(ckks_ctx *ctx, const uint64_t *dev_in, uint32_t rows,
  *   out_j = Rescale( sum_{g<n2} Rot_{T n1 g}( sum_{i,b<n1} pt_{j,i,g,b} * Rot_{T b}(x_i) ) )
  * where pt_{j,i,g,b} encodes at scale q_level the slot vector
  *   p[f*T + t] = D_{n1 g + b}(A_{j,i})[(f - n1 g) mod D],  n2 = ceil(D/n1).
- * Weight plaintexts are encoded on the fly from W.  Keys: key_steps[r] ->
+ * Weight plaintexts are encoded on the fly from W (as ckks_encode: their
+ * coefficients must stay below 2^63, which q_level * max|W| < 2^63 guarantees
+ * since each diagonal holds D distinct weights repeated over T tokens and
+ * (2/N) * (N/2) = 1; beyond that they are unspecified).  Keys: key_steps[r] ->
  * dev_keys[r]; steps T*b (0 < b < n1) and T*n1*g (0 < g < n2) must be present.
  * in: d_in/D ciphertexts, all with the same n_limbs = level + 1 >= 2 and the
  * same scale; out: d_out/D ciphertexts with n_limbs = level (the rescale
