@@ -154,6 +154,8 @@ static ckks_status build_tables(ckks_ctx *c)
         m.one_s = (uint64_t)(((u128)1 << 64) / q);
         m.ninv = hm::inv(n % q, q);
         m.ninvs = hm::shoup(m.ninv, q);
+        m.iw1n = hm::mul(ipw[hm::brev(1, (int)c->log_n)], m.ninv, q);
+        m.iw1ns = hm::shoup(m.iw1n, q);
         m.qd = (double)q;
         m.qinvd = 1.0 / (double)q;
         m.ninvd = (double)m.ninv;

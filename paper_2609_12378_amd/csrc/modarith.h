@@ -21,6 +21,7 @@ struct ModQ {
     uint64_t r64, r64s;   // 2^64 mod q and its Shoup companion
     uint64_t one_s;       // floor(2^64 / q): the Shoup companion of 1
     uint64_t ninv, ninvs; // N^-1 mod q and its Shoup companion
+    uint64_t iw1n, iw1ns; // psi^-brev(1) N^-1 mod q (the inverse transform's last twiddle, N^-1 folded in), Shoup
     double qd, qinvd;     // q and fl(1/q) for the fp64 arithmetic (q < 2^50)
     double ninvd;         // N^-1 mod q as a double
 };

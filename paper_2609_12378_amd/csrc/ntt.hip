@@ -123,14 +123,10 @@ __global__ __launch_bounds__(256) void ntt_col(uint64_t *data, LimbMap map, uint
             inv_low<LOGS, F>(x, tw, 1, r, ar);
             transpose<LOGS, false>(x, lds, col, r);
         }
-        // fp64: N^-1 folded into the last stage
+        // N^-1 folded into the last stage
         inv_top<F, true>(x, tw, 1, ar);
 #pragma unroll
-        for (int k = 0; k < kE; k++) {
-            E v = x[k];
-            if constexpr (!F) v = ar.scale_n(v);
-            st_stream(base + (size_t)(r + TS * k) * n2 + col, ar.to_canon(v));
-        }
+        for (int k = 0; k < kE; k++) st_stream(base + (size_t)(r + TS * k) * n2 + col, ar.to_canon(x[k]));
     }
 }
 
@@ -354,12 +350,8 @@ __global__ __launch_bounds__(LOGN ? 128 : 256) void ntt_row(uint64_t *data, Limb
             inv_low<LOGS, F>(x, tw, B, r, ar);
             transpose<LOGS, false>(x, lds, sub, r);
         }
-        // the last pass of an fp64 inverse folds N^-1 into its last stage
+        // the last pass of an inverse folds N^-1 into its last stage (B = 1 there: a single-pass transform)
         inv_top<F, LAST>(x, tw, B, ar);
-        if constexpr (LAST && !F) {
-#pragma unroll
-            for (int k = 0; k < kE; k++) x[k] = ar.scale_n(x[k]);
-        }
     }
 #pragma unroll
     for (int k = 0; k < kE; k++) st_stream(base + r + TS * k, LAST ? ar.to_canon(x[k]) : ar.to_raw(x[k]));

@@ -26,8 +26,11 @@ template <>
 struct Ar<false> {
     using E = uint64_t;
     using W = ulonglong2;
-    uint64_t q, twoq, ninv, ninvs;
-    __device__ explicit Ar(const ModQ &m) : q(m.q), twoq(m.twoq), ninv(m.ninv), ninvs(m.ninvs) {}
+    uint64_t q, twoq, ninv, ninvs, iw1n, iw1ns;
+    __device__ explicit Ar(const ModQ &m)
+        : q(m.q), twoq(m.twoq), ninv(m.ninv), ninvs(m.ninvs), iw1n(m.iw1n), iw1ns(m.iw1ns)
+    {
+    }
     __device__ E from_u64(uint64_t v) const { return v; }
     __device__ E from_raw(uint64_t v) const { return v; }
     __device__ uint64_t to_raw(E x) const { return x; }
@@ -55,6 +58,14 @@ struct Ar<false> {
         Y = shoup_lazy(x + twoq - y, w.x, w.y, q);
     }
     __device__ E scale_n(E x) const { return shoup(x, ninv, ninvs, q); }
+    // the last Gentleman-Sande stage of an inverse transform (its twiddle is psi^-brev(1)) times N^-1, canonical:
+    // X' = (X + Y) N^-1, Y' = (X - Y) psi^-brev(1) N^-1, from X, Y in [0, 2q)
+    __device__ void gs_scaled(E &X, E &Y) const
+    {
+        const uint64_t x = X, y = Y;
+        X = shoup(x + y, ninv, ninvs, q);
+        Y = shoup(x + twoq - y, iw1n, iw1ns, q);
+    }
 };
 
 template <>
@@ -201,7 +212,8 @@ __device__ __forceinline__ void inv_low(typename Ar<F>::E (&x)[kE], const typena
         }
     }
 }
-// SCALED (fp64 only): the last stage also multiplies by N^-1 (gs_scaled), so the caller skips scale_n.
+// SCALED: the last stage also multiplies by N^-1 (gs_scaled), so the caller skips scale_n.  Only the last pass
+// of an inverse transform passes SCALED, where B = 1 (its last stage's twiddle is psi^-brev(1)).
 template <bool F, bool SCALED = false>
 __device__ __forceinline__ void inv_top(typename Ar<F>::E (&x)[kE], const typename Ar<F>::W *tw, uint32_t B,
                                         const Ar<F> &ar)
@@ -217,6 +229,13 @@ __device__ __forceinline__ void inv_top(typename Ar<F>::E (&x)[kE], const typena
                     const double wn = ar.scaled_twiddle(w);
 #pragma unroll
                     for (int j = 0; j < tk; j++) ar.gs_scaled(x[g * 2 * tk + j], x[g * 2 * tk + j + tk], wn);
+                    continue;
+                }
+            }
+            if constexpr (!F && SCALED) {
+                if (lm == 0) {
+#pragma unroll
+                    for (int j = 0; j < tk; j++) ar.gs_scaled(x[g * 2 * tk + j], x[g * 2 * tk + j + tk]);
                     continue;
                 }
             }
