@@ -565,10 +565,7 @@ extern "C" ckks_status ckks_attention_scores(ckks_ctx *ctx, const ckks_buf *q, u
         CK_TRY(rotate_core(ctx, q[c].data, level, qsteps.data(), qkeys.data(), T - 1, outs.data(), work));
         // 2. products, relinearised in one batch (key switching with sigma = identity and the relinearisation
         //    key: (d0 + u0, u1), then d1 added)
-        for (uint32_t d = 0; d < T; d++) {
-            uint64_t *dd = Dt + (size_t)d * 3 * L * N;
-            CK_TRY(launch_tensor(ctx, dd, dd + L * N, dd + 2 * L * N, A + (size_t)d * ctw, B + (size_t)d * ctw, L));
-        }
+        CK_TRY(launch_tensor_batch(ctx, Dt, Dt + L * N, Dt + 2 * L * N, 3 * L * N, A, ctw, B, ctw, T, L));
         {
             const uint32_t ext = L + ctx->n_p, nd = n_digits(ctx, level);
             const size_t dig_ct = (size_t)nd * ext * N;
@@ -589,9 +586,8 @@ extern "C" ckks_status ckks_attention_scores(ckks_ctx *ctx, const ckks_buf *q, u
                 CK_TRY(ks_rotate_batch(ctx, level, cnt, c0s.data() + r0, digs.data() + r0, g.data() + r0,
                                        rk.data() + r0, po.data() + r0, rw));
             }
-            for (uint32_t d = 0; d < T; d++)
-                CK_TRY(launch_binary(ctx, po[d] + (size_t)L * N, po[d] + (size_t)L * N, c0s[d] + (size_t)L * N, L,
-                                     limb_range(0, L), EW_ADD));
+            CK_TRY(launch_binary_batch(ctx, Pr + (size_t)L * N, ctw, Pr + (size_t)L * N, ctw, Dt + (size_t)L * N,
+                                       3 * (size_t)L * N, T, L, limb_range(0, L), EW_ADD));
         }
         // 3. U_k = sum_delta M_{(delta + k) mod hd} P_delta = z[-k mod hd] for every k, then each rotated by k
         //    (in chunks) and summed

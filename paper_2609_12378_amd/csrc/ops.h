@@ -12,6 +12,13 @@ ckks_status launch_mul_plain(ckks_ctx *ctx, uint64_t *out, const uint64_t *ct, c
                              uint32_t limbs);
 ckks_status launch_tensor(ckks_ctx *ctx, uint64_t *d0, uint64_t *d1, uint64_t *d2, const uint64_t *a,
                           const uint64_t *b, uint32_t limbs);
+// `count` independent entries in one launch (at most 65535), each pointer advanced by its own stride in words
+ckks_status launch_binary_batch(ckks_ctx *ctx, uint64_t *out, size_t out_stride, const uint64_t *a,
+                                size_t a_stride, const uint64_t *b, size_t b_stride, uint32_t count, uint32_t rows,
+                                const LimbMap &map, int op);
+ckks_status launch_tensor_batch(ckks_ctx *ctx, uint64_t *d0, uint64_t *d1, uint64_t *d2, size_t d_stride,
+                                const uint64_t *a, size_t a_stride, const uint64_t *b, size_t b_stride,
+                                uint32_t count, uint32_t limbs);
 ckks_status launch_expand_i8(ckks_ctx *ctx, uint64_t *out, const int8_t *v, const LimbMap &map);
 ckks_status launch_expand_i32(ckks_ctx *ctx, uint64_t *out, const int32_t *v, const LimbMap &map);
 ckks_status launch_encrypt(ckks_ctx *ctx, uint64_t *c0, uint64_t *c1, const uint64_t *a, const uint64_t *s,

@@ -23,13 +23,17 @@ __device__ __forceinline__ bool flat(uint32_t log_n, size_t total, size_t &i, ui
 
 inline dim3 grid_for(size_t total) { return dim3((unsigned)((total + kThreads - 1) / kThreads)); }
 
+// blockIdx.y selects the batch entry: out, a and b advance by their own strides (in words)
 __global__ __launch_bounds__(kThreads) void k_binary(uint64_t *out, const uint64_t *a, const uint64_t *b,
                                                       size_t total, uint32_t log_n, LimbMap map, const ModQ *mods,
-                                                      int op)
+                                                      int op, size_t out_stride, size_t a_stride, size_t b_stride)
 {
     size_t i;
     uint32_t row, col;
     if (!flat(log_n, total, i, row, col)) return;
+    out += blockIdx.y * out_stride;
+    a += blockIdx.y * a_stride;
+    b += blockIdx.y * b_stride;
     const ModQ m = mods[map.prime[row % map.n]];
     const uint64_t x = a[i], y = b[i];
     uint64_t r;
@@ -51,14 +55,21 @@ __global__ __launch_bounds__(kThreads) void k_mul_plain(uint64_t *out, const uin
     out[i] = mulmod(ct[i], pt[((size_t)l << log_n) + col], mods[l]);
 }
 
-// d0 = a0 b0, d1 = a0 b1 + a1 b0, d2 = a1 b1 over `limbs` q-limbs
+// d0 = a0 b0, d1 = a0 b1 + a1 b0, d2 = a1 b1 over `limbs` q-limbs; blockIdx.y selects the batch entry (d0, d1
+// and d2 advance by d_stride words, a by a_stride, b by b_stride)
 __global__ __launch_bounds__(kThreads) void k_tensor(uint64_t *d0, uint64_t *d1, uint64_t *d2, const uint64_t *a,
                                                       const uint64_t *b, size_t total, uint32_t log_n,
-                                                      const ModQ *mods)
+                                                      const ModQ *mods, size_t d_stride, size_t a_stride,
+                                                      size_t b_stride)
 {
     size_t i;
     uint32_t row, col;
     if (!flat(log_n, total, i, row, col)) return;
+    d0 += blockIdx.y * d_stride;
+    d1 += blockIdx.y * d_stride;
+    d2 += blockIdx.y * d_stride;
+    a += blockIdx.y * a_stride;
+    b += blockIdx.y * b_stride;
     const ModQ m = mods[row];
     const uint64_t a0 = a[i], a1 = a[i + total], b0 = b[i], b1 = b[i + total];
     d0[i] = mulmod(a0, b0, m);
@@ -191,11 +202,21 @@ __global__ __launch_bounds__(kThreads) void k_copy_rows(uint64_t *dst_a, size_t 
 ckks_status launch_binary(ckks_ctx *ctx, uint64_t *out, const uint64_t *a, const uint64_t *b, uint32_t rows,
                           const LimbMap &map, int op)
 {
+    return launch_binary_batch(ctx, out, 0, a, 0, b, 0, 1, rows, map, op);
+}
+
+ckks_status launch_binary_batch(ckks_ctx *ctx, uint64_t *out, size_t out_stride, const uint64_t *a,
+                                size_t a_stride, const uint64_t *b, size_t b_stride, uint32_t count, uint32_t rows,
+                                const LimbMap &map, int op)
+{
     const size_t total = (size_t)rows << ctx->log_n;
-    if (!total) return CKKS_OK;
-    prof_begin(ctx, K_ELEM, 24.0 * total);
-    hipLaunchKernelGGL(k_binary, grid_for(total), dim3(kThreads), 0, ctx->stream, out, a, b, total, ctx->log_n, map,
-                       ctx->d_mod, op);
+    if (!total || !count) return CKKS_OK;
+    CK_REQUIRE(count <= 65535u, CKKS_EINVAL, "element-wise batch of %u entries exceeds 65535", count);
+    prof_begin(ctx, K_ELEM, 24.0 * total * count);
+    dim3 grid = grid_for(total);
+    grid.y = count;
+    hipLaunchKernelGGL(k_binary, grid, dim3(kThreads), 0, ctx->stream, out, a, b, total, ctx->log_n, map,
+                       ctx->d_mod, op, out_stride, a_stride, b_stride);
     prof_end(ctx, K_ELEM);
     HIP_TRY(hipGetLastError());
     return CKKS_OK;
@@ -215,9 +236,20 @@ ckks_status launch_mul_plain(ckks_ctx *ctx, uint64_t *out, const uint64_t *ct, c
 ckks_status launch_tensor(ckks_ctx *ctx, uint64_t *d0, uint64_t *d1, uint64_t *d2, const uint64_t *a,
                           const uint64_t *b, uint32_t limbs)
 {
+    return launch_tensor_batch(ctx, d0, d1, d2, 0, a, 0, b, 0, 1, limbs);
+}
+
+ckks_status launch_tensor_batch(ckks_ctx *ctx, uint64_t *d0, uint64_t *d1, uint64_t *d2, size_t d_stride,
+                                const uint64_t *a, size_t a_stride, const uint64_t *b, size_t b_stride,
+                                uint32_t count, uint32_t limbs)
+{
     const size_t total = (size_t)limbs << ctx->log_n;
-    hipLaunchKernelGGL(k_tensor, grid_for(total), dim3(kThreads), 0, ctx->stream, d0, d1, d2, a, b, total,
-                       ctx->log_n, ctx->d_mod);
+    if (!total || !count) return CKKS_OK;
+    CK_REQUIRE(count <= 65535u, CKKS_EINVAL, "tensor-product batch of %u entries exceeds 65535", count);
+    dim3 grid = grid_for(total);
+    grid.y = count;
+    hipLaunchKernelGGL(k_tensor, grid, dim3(kThreads), 0, ctx->stream, d0, d1, d2, a, b, total, ctx->log_n,
+                       ctx->d_mod, d_stride, a_stride, b_stride);
     HIP_TRY(hipGetLastError());
     return CKKS_OK;
 }
