@@ -230,7 +230,8 @@ __global__ __launch_bounds__(kThreads) void k_sum_cts(uint64_t *out, const uint6
 }
 
 // d ([3][L][N]) = sum_{r < count} E_r x C_r: d0 += e0 c0, d1 += e0 c1 + e1 c0, d2 += e1 c1, the sums held in 128
-// bits and reduced once (count <= 2^16 keeps them below 2^128).  E_r at E + r * 2 L N ([2][L][N]); C_r at
+// bits and reduced once: the attention calls take primes below 2^50 only, so each product is below 2^100 and
+// count <= 2^16 (2^17 products in d1) keeps every sum below 2^117.  E_r at E + r * 2 L N ([2][L][N]); C_r at
 // C + r * 2 Lc N ([2][Lc][N], Lc >= L, its first L limbs used).
 __global__ __launch_bounds__(kThreads) void k_tensor_acc(uint64_t *d, const uint64_t *__restrict__ E,
                                                          const uint64_t *__restrict__ C, uint32_t count, uint32_t L,
@@ -344,6 +345,8 @@ ckks_status launch_tensor_acc(ckks_ctx *ctx, uint64_t *d, const uint64_t *E, con
                               uint32_t L, uint32_t Lc)
 {
     const size_t total = (size_t)L * ctx->n;
+    CK_REQUIRE(count <= 65536u && ntt_uses_f64(ctx, L), CKKS_EUNSUPPORTED,
+               "attention: %u products summed exactly need at most 2^16 terms and primes below 2^50", count);
     prof_begin(ctx, K_ELEM, 8.0 * total * (4.0 * count + 3.0));
     hipLaunchKernelGGL(k_tensor_acc, grid_of(total), dim3(kThreads), 0, ctx->stream, d, E, C, count, L, Lc,
                        ctx->log_n, ctx->d_mod);
