@@ -930,7 +930,7 @@ def main():
         "higher_is_better": False,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "u64",
+        "dtype": "f64",
         "data": "synthetic",
         "config": {"workload": "Llama-3-8B-shaped ct-pt projection 4096x14336, N=2^16, level 12 (13 limbs), "
                                "24+8 x 50-bit primes, dnum 3, 128 tokens x 256 features, BSGS n1=32 n2=8",
