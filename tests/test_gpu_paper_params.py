@@ -8,6 +8,8 @@ the oracle:
   compared, and a single rotation at level 12 (three digits, the last partial);
 * the projection's parameters on a 256 x 512 slice of the weights at level 12 (31 baby, 7 giant rotations;
   weight plaintexts at scale q_12 of 59 bits), with the lazy ModDown, decrypted within 2^-18 of X @ W.
+* mul_relin of two level-12 ciphertexts at scale 2^50 and the rescale after it, decrypted within 2^-20 of the
+  slot-wise product.
 """
 import numpy as np
 import pytest
@@ -125,3 +127,36 @@ def test_projection_slice_paper_params(env):
         err = float(np.max(np.abs(to_host(re) - fm_pack(Y, T, D, j))))
         say("output", j, "decrypted error", err)
         assert err <= 2.0 ** -18
+
+
+def test_mul_relin_rescale_paper_params(env):
+    """Mult + relinearisation and the rescale that follows it at level 12 of the paper's chain (two digits, the
+    second partial): the 128-bit tensor products, the relinearisation's integer key switch and the integer rescale,
+    bit for bit, and the decrypted result close to the slot-wise product."""
+    cfg, ctx, ck = env
+    n, limbs = ctx.n, 13
+    say("paper parameters: mul_relin and rescale at level 12")
+    s = ternary_secret(rng(cfg.index, 3, extra=63), n)
+    cts_o, cts_g, zs = [], [], []
+    for k in range(2):
+        z = uniform_slots(rng(cfg.index, 1, extra=64 + k), n // 2)
+        g = rng(cfg.index, 4, extra=64 + k)
+        a, e = uniform_residues(g, ctx.q[:limbs], n), gaussian_error(g, n)
+        cts_o.append(ck.encrypt(s, ck.encode(z, None, 2.0 ** 50, limbs), a, e))
+        cts_g.append(ctx.encrypt(to_dev(s), ctx.encode(to_dev(z), None, 2.0 ** 50, limbs), to_dev(a), to_dev(e)))
+        zs.append(z)
+    gk = rng(cfg.index, 5, extra=63)
+    ka, ke = uniform_residues(gk, ctx.primes, n, lead=(cfg.dnum,)), gaussian_error(gk, (cfg.dnum, n))
+    rlk_o = ck.keygen_relin(s, ka, ke)
+    rlk_g = ctx.keygen_relin(to_dev(s), to_dev(ka), to_dev(ke))
+    eq(rlk_g, rlk_o, "relinearisation key")
+    prod_g = ctx.mul_relin(cts_g[0], cts_g[1], rlk_g)
+    prod_o = ck.mul_relin(cts_o[0], cts_o[1], rlk_o)
+    eq(prod_g.data, prod_o, "mul_relin")
+    res_g = ctx.rescale(prod_g)
+    eq(res_g.data, ck.rescale(prod_o), "rescale")
+    assert abs(res_g.scale / (2.0 ** 100 / float(ctx.q[limbs - 1])) - 1.0) < 1e-15
+    re, _ = ctx.decode(ctx.decrypt(to_dev(s), res_g))
+    err = float(np.max(np.abs(to_host(re) - zs[0] * zs[1])))
+    say("decrypted error", err)
+    assert err < 2.0 ** -20
