@@ -211,8 +211,9 @@ ckks_status rescale_many(ckks_ctx *ctx, const uint64_t *c, uint32_t count, uint3
     // the top limb of every polynomial, then the same steps as one rescale over all of them
     CK_TRY(launch_copy_rows(ctx, top, N, nullptr, 0, c + (size_t)l * N, (size_t)(l + 1) * N, N, polys));
     CK_TRY(launch_ntt(ctx, top, polys, limb_range(l, 1), true));
-    CK_TRY(launch_rescale_spread(ctx, r, top, polys, l));
-    CK_TRY(launch_ntt(ctx, r, polys * l, limb_range(0, l), false));
+    // the centred top coefficients reduced modulo q_0..q_(l-1) inside the forward transform's first pass
+    CK_TRY(launch_rescale_centre(ctx, top, polys, l));
+    CK_TRY(launch_ntt_from_i64(ctx, (const int64_t *)top, r, polys, l));
     return launch_rescale_finish(ctx, out, c, r, polys, l);
 }
 
@@ -225,8 +226,8 @@ ckks_status rescale_core(ckks_ctx *ctx, const uint64_t *c, uint32_t l, uint64_t 
         HIP_TRY(hipMemcpyAsync(top + k * N, c + ((size_t)k * (l + 1) + l) * N, N * 8, hipMemcpyDeviceToDevice,
                                ctx->stream));
     CK_TRY(launch_ntt(ctx, top, 2, limb_range(l, 1), true));
-    CK_TRY(launch_rescale_spread(ctx, r, top, 2, l));
-    CK_TRY(launch_ntt(ctx, r, 2 * l, limb_range(0, l), false));
+    CK_TRY(launch_rescale_centre(ctx, top, 2, l));
+    CK_TRY(launch_ntt_from_i64(ctx, (const int64_t *)top, r, 2, l));
     return launch_rescale_finish(ctx, out, c, r, 2, l);
 }
 

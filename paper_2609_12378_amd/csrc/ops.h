@@ -31,7 +31,8 @@ ckks_status launch_keygen_digit(ckks_ctx *ctx, uint64_t *b_out, uint64_t *a_out,
 // allows them); count <= 65535
 ckks_status launch_copy_rows(ckks_ctx *ctx, uint64_t *dst_a, size_t a_stride, uint64_t *dst_b, size_t b_stride,
                              const uint64_t *src, size_t src_stride, size_t words, uint32_t count);
-ckks_status launch_rescale_spread(ckks_ctx *ctx, uint64_t *out, const uint64_t *top, uint32_t polys, uint32_t l);
+// top ([polys][N], canonical mod q_l) to centred int64 in place
+ckks_status launch_rescale_centre(ckks_ctx *ctx, uint64_t *top, uint32_t polys, uint32_t l);
 ckks_status launch_rescale_finish(ckks_ctx *ctx, uint64_t *out, const uint64_t *c, const uint64_t *r,
                                   uint32_t polys, uint32_t l);
 

@@ -146,23 +146,15 @@ __global__ __launch_bounds__(kThreads) void k_keygen(uint64_t *b_out, uint64_t *
     if (a_out) a_out[i] = a[i];
 }
 
-// Rescale, step 1: top-limb coefficients t (mod q_l) -> centred -> residues mod q_i, i < l.
-// top: [polys][N] coefficients; out: [polys][l][N]
-__global__ __launch_bounds__(kThreads) void k_rescale_spread(uint64_t *out, const uint64_t *top, size_t total,
-                                                              uint32_t log_n, uint32_t l, const ModQ *mods)
+// Rescale, step 1: top-limb coefficients t (mod q_l), canonical, to their centred values as int64 in place
+// (t > q_l / 2 -> t - q_l); the signed-input forward transform then reduces them modulo every q_i, i < l, in its
+// first pass, so the residue rows of the top limb are never written out before their transform.
+__global__ __launch_bounds__(kThreads) void k_rescale_centre(uint64_t *top, size_t total, uint64_t ql)
 {
-    size_t i;
-    uint32_t row, col;
-    if (!flat(log_n, total, i, row, col)) return;
-    const uint32_t poly = row / l, li = row % l;
-    const uint64_t ql = mods[l].q;
-    const ModQ mi = mods[li];
-    const uint64_t t = top[((size_t)poly << log_n) + col];
-    const bool neg = t > (ql >> 1);
-    const uint64_t mag = neg ? ql - t : t;  // |centred value| < q_l / 2
-    uint64_t r = csub(mag - mulhi64(mag, mi.one_s) * mi.q, mi.q);
-    if (neg && r) r = mi.q - r;
-    out[i] = r;
+    const size_t i = (size_t)blockIdx.x * kThreads + threadIdx.x;
+    if (i >= total) return;
+    const uint64_t t = top[i];
+    top[i] = t > (ql >> 1) ? t - ql : t;  // two's complement of the negative centred value
 }
 
 // Rescale, step 2: out_i = (c_i - r_i) * q_l^-1 mod q_i; c: [polys][l+1][N], r/out: [polys][l][N]
@@ -302,11 +294,11 @@ ckks_status launch_keygen_digit(ckks_ctx *ctx, uint64_t *b_out, uint64_t *a_out,
     return CKKS_OK;
 }
 
-ckks_status launch_rescale_spread(ckks_ctx *ctx, uint64_t *out, const uint64_t *top, uint32_t polys, uint32_t l)
+ckks_status launch_rescale_centre(ckks_ctx *ctx, uint64_t *top, uint32_t polys, uint32_t l)
 {
-    const size_t total = ((size_t)polys * l) << ctx->log_n;
-    hipLaunchKernelGGL(k_rescale_spread, grid_for(total), dim3(kThreads), 0, ctx->stream, out, top, total,
-                       ctx->log_n, l, ctx->d_mod);
+    const size_t total = (size_t)polys << ctx->log_n;
+    hipLaunchKernelGGL(k_rescale_centre, grid_for(total), dim3(kThreads), 0, ctx->stream, top, total,
+                       ctx->primes[l]);
     HIP_TRY(hipGetLastError());
     return CKKS_OK;
 }
